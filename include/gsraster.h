@@ -1,0 +1,222 @@
+/*
+ * gsraster -- differentiable tile-based Gaussian-splatting rasterizer with the
+ * view-dependent appearance evaluated inside it, for AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Compact Neural Appearance Models for Efficient Gaussian Splatting".
+ *   Sec. 3.1     - a per-primitive preprocess projects each Gaussian, finds the
+ *                  16x16-pixel tiles it overlaps and computes its colour; a
+ *                  tile-based blend alpha-composites the Gaussians of each pixel
+ *                  in depth order.
+ *   eq. sh_color_eval - degree-3 spherical-harmonics colour, 48 fp32 per Gaussian.
+ *   Sec. 4 and the appendix on the fused CUDA rasterizer - a per-Gaussian latent
+ *                  (28 bytes) decoded by a small shared half-precision MLP, evaluated
+ *                  only for Gaussians that survive culling, inside the preprocess;
+ *                  the backward pass propagates the colour gradient through the
+ *                  view direction into the means.
+ * The rasterizer conventions the paper inherits from 3D Gaussian Splatting
+ * without restating them (EWA projection with a 0.3 px^2 low-pass, 3-sigma tile
+ * rectangle, alpha cap 0.99, skip below 1/255, stop when transmittance would
+ * fall below 1e-4) are implemented as documented below.
+ *
+ * Conventions of every call:
+ *  - All pointers in the structs are DEVICE pointers owned by the caller, unless
+ *    a comment says "host". The library never allocates or frees device memory
+ *    while rasterizing; scratch memory is the caller's `workspace`
+ *    (size from gs_workspace_size), 256-byte aligned.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream) and
+ *    is asynchronous unless a comment says the call synchronises.
+ *  - Every call returns a gs_status. Arguments are validated on the host before
+ *    any launch; on error nothing is enqueued and gs_last_error() (thread-local)
+ *    describes the problem. A failed launch or an asynchronous device error
+ *    reported by HIP surfaces as GS_ERR_DEVICE from the call that observes it.
+ *  - Arrays named [k][n] are planar: element (c, i) is at c*n + i.
+ *  - n must be below 2^31 and the number of (tile, Gaussian) pairs below 2^32.
+ */
+#ifndef GSRASTER_H
+#define GSRASTER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gs_status {
+    GS_OK = 0,
+    GS_ERR_INVALID_ARG = 1,   /* bad pointer, size, enum value or camera */
+    GS_ERR_CAPACITY = 2,      /* a caller buffer is too small; the needed size is reported */
+    GS_ERR_DEVICE = 3,        /* HIP reported an error */
+    GS_ERR_UNSUPPORTED = 4,   /* valid request this build does not implement */
+} gs_status;
+
+#define GS_TILE 16            /* tile edge in pixels (Sec. 3.1) */
+#define GS_SH_COEFFS 48       /* degree-3 SH: 16 basis functions x RGB (eq. sh_color_eval) */
+#define GS_LATENT_DIM 14      /* binary16 latent per Gaussian: 28 bytes */
+#define GS_MLP_IN 17          /* decoder input: latent (14) then unit view direction (3) */
+#define GS_MLP_HIDDEN 32
+#define GS_MLP_OUT 3
+#define GS_MLP_WEIGHTS 1664   /* 32*17 + 32*32 + 3*32 */
+
+/* Pinhole camera. Host struct, passed by pointer. */
+typedef struct gs_camera {
+    float viewmat[12];        /* row-major 3x4 [R|t]: world -> camera, x right, y down, z forward */
+    float campos[3];          /* camera centre in world coordinates (= -R^T t) */
+    float fx, fy, cx, cy;     /* focal lengths and principal point, pixels */
+    int32_t width, height;    /* image size, pixels (any size >= 1; edge tiles may be partial) */
+    float near_plane;         /* Gaussians with camera z <= near_plane are culled (0.2 typical) */
+    float bg[3];              /* background colour added with the final transmittance */
+} gs_camera;
+
+/* Geometry of n Gaussians (Sec. 3.1). Device arrays, fp32. */
+typedef struct gs_gaussians {
+    int64_t n;
+    const float* means;           /* [3][n] world positions */
+    const float* log_scales;      /* [3][n] scale = exp(log_scale) */
+    const float* quats;           /* [4][n] rotation quaternion (w, x, y, z); need not be unit */
+    const float* opacity_logits;  /* [n] opacity = 1 / (1 + exp(-logit)) */
+} gs_gaussians;
+
+enum {
+    GS_APP_SH3 = 0,           /* eq. sh_color_eval: c = max(0, 0.5 + sum_k Y_k(d) sh_k) */
+    GS_APP_LATENT_MLP = 1,    /* c = sigmoid(W3 relu(W2 relu(W1 [z, d]))), no biases */
+};
+
+/* View-dependent appearance (Sec. 3.1 and 4). d is the unit vector from the camera
+ * centre to the Gaussian's mean, in world coordinates. */
+typedef struct gs_appearance {
+    int32_t kind;             /* GS_APP_* */
+    int32_t sh_degree;        /* SH3 only: bands 0..sh_degree are used (0..3) */
+    const float* sh;          /* SH3: [48][n] fp32, row 3*k + c = basis k, channel c.
+                                 Basis order l = 0..3, m = -l..l; real SH with the
+                                 Condon-Shortley phase: band 1 = sqrt(3/(4 pi)) (-y, z, -x) */
+    const uint16_t* latent;   /* LATENT_MLP: [14][n] binary16 bit patterns */
+    const uint16_t* mlp_w;    /* LATENT_MLP: binary16 W1[32][17], W2[32][32], W3[3][32], row-major
+                                 [out][in], concatenated (1664 values). The decoder sees d
+                                 rounded to binary16 and accumulates in fp32. */
+} gs_appearance;
+
+/* Screen-space record of one Gaussian, written by gs_preprocess (48 bytes).
+ * Only meaningful where tiles_touched[i] > 0 (other records are not written). */
+typedef struct gs_splat {
+    float mean_x, mean_y;             /* projected mean, pixels */
+    float conic_a, conic_b, conic_c;  /* inverse 2D covariance [[a, b], [b, c]] */
+    float opacity;                    /* activated opacity */
+    float color[3];                   /* view-dependent RGB */
+    float depth;                      /* camera-space z (> near_plane) */
+    int16_t rect[4];                  /* tiles x0, y0, x1, y1 (half-open) */
+} gs_splat;
+
+/* Outputs of gs_preprocess; caller-allocated device arrays. */
+typedef struct gs_preprocessed {
+    gs_splat* splats;         /* [n] */
+    uint32_t* tiles_touched;  /* [n] tiles of the rectangle; 0 = culled */
+    uint32_t* depth_key;      /* [n] sort key: bit pattern of depth, 0xFFFFFFFF when culled */
+    uint64_t* num_pairs;      /* [1] total tiles touched (number of pairs P) */
+} gs_preprocessed;
+
+/* Gradients, caller-allocated device arrays, OVERWRITTEN by gs_render_bwd
+ * (not accumulated). Entries of culled Gaussians are set to zero. */
+typedef struct gs_grads {
+    float* dmeans;            /* [3][n] */
+    float* dlog_scales;       /* [3][n] */
+    float* dquats;            /* [4][n] */
+    float* dopacity_logits;   /* [n] */
+    float* dsh;               /* SH3: [48][n]; rows of bands above sh_degree are zero */
+    float* dlatent;           /* LATENT_MLP: [14][n] fp32 */
+    float* dmlp_w;            /* LATENT_MLP: [1664] fp32, same order as mlp_w */
+    float* dmean2d;           /* optional (may be NULL): [2][n] screen-space mean gradient */
+} gs_grads;
+
+/*
+ * gs_preprocess -- Sec. 3.1 preprocess with the appearance fused in (the
+ * appendix's fused rasterizer: colour only for Gaussians that survive culling).
+ * Per Gaussian: scale = exp(log_scale), opacity = sigmoid(logit) (both taken
+ * through fp64 and rounded once), unit quaternion -> R, Sigma = R S S^T R^T;
+ * t = R_view mu + t_view, culled if t.z <= near_plane; Jacobian of the pinhole
+ * projection at t with x/z and y/z clamped to 1.3x the half field of view;
+ * Sigma2D = J R_view Sigma R_view^T J^T + 0.3 I, culled unless det > 0; conic;
+ * r = ceil(3 sqrt(lambda_max)) with lambda_max = mid + sqrt(max(0.1, mid^2 - det));
+ * rect = [floor((px - r)/16), ceil((px + r)/16)) per axis clamped to the grid,
+ * culled if empty; colour from the appearance model.
+ * The geometry is one fixed sequence of correctly rounded fp32 operations
+ * (no fused multiply-add), so tile rectangles and depth keys are reproducible.
+ * num_pairs_host: optional HOST pointer; if non-NULL the call synchronises the
+ * stream and stores P there.
+ * Errors: GS_ERR_INVALID_ARG for NULL arrays, n out of range, unknown kind,
+ * sh_degree outside 0..3, non-positive image size or focal length.
+ */
+gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                        const gs_preprocessed* out, uint64_t* num_pairs_host,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * gs_bin_sort -- the depth-sorted per-tile lists of Sec. 3.1. Produces, for the P
+ * pairs (tile, Gaussian) of every Gaussian with tiles_touched > 0 and every
+ * tile of its rectangle, the Gaussian indices sorted by (tile id, depth key,
+ * Gaussian index), tile id = ty * ceil(width/16) + tx. tile_ranges[t] =
+ * {first, one-past-last} position of tile t; an empty tile gets {s, s} with s
+ * the number of pairs of lower tiles. The result is unique (bit-exact).
+ * num_pairs: P as returned by gs_preprocess (host value).
+ * capacity: length of values and tile_ids; GS_ERR_CAPACITY if num_pairs > capacity.
+ * values: [capacity] u32 device; tile_ids: optional [capacity] u32 tile of each pair.
+ * tile_ranges: [n_tiles][2] u32 device.
+ */
+gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, uint64_t num_pairs,
+                      uint64_t capacity, uint32_t* values, uint32_t* tile_ids, uint32_t* tile_ranges,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * gs_render_fwd -- Sec. 3.1 blend. One workgroup per 16x16 tile; per pixel, with
+ * sample point (x + 0.5, y + 0.5) and T = 1, front to back over the tile's list:
+ * power = -(a dx^2 + c dy^2)/2 - b dx dy (skip if > 0); alpha = min(0.99, o e^power)
+ * (skip if < 1/255); stop, without blending, if T (1 - alpha) < 1e-4; otherwise
+ * C += colour alpha T, T *= 1 - alpha. Finally C += T bg.
+ * image: [3][H][W] fp32; final_T: [H][W] fp32; n_contrib: [H][W] u32 = 1 + the
+ * list position (within the tile's range) of the last blended Gaussian, 0 if none.
+ */
+gs_status gs_render_fwd(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, const uint32_t* values,
+                        const uint32_t* tile_ranges, float* image, float* final_T, uint32_t* n_contrib,
+                        void* stream);
+
+/*
+ * gs_render_bwd -- gradients of L = sum(dL_dimage * image) with respect to every
+ * Gaussian parameter, for the image that gs_render_fwd produced from the same
+ * inputs (Sec. 4 fused backward; the colour gradient also reaches the means
+ * through the view direction). Reverse blending per tile, then the derivative of
+ * the preprocess per Gaussian; for LATENT_MLP also the decoder weights.
+ * dL_dimage: [3][H][W] fp32 device. The pair-level accumulation uses float
+ * atomics, so results vary in the last bits between runs.
+ */
+gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                        const gs_preprocessed* pre, const uint32_t* values, const uint32_t* tile_ranges,
+                        const float* final_T, const uint32_t* n_contrib, const float* dL_dimage,
+                        const gs_grads* grads, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes needed by any call for these sizes (host only). */
+gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t capacity, int32_t kind,
+                            size_t* bytes);
+
+/* Kernel timing. When enabled, every kernel the library launches is bracketed
+ * by HIP events on its stream (events are created here, not while rendering).
+ * gs_timing_read synchronises the recorded events and returns, per kernel id
+ * (GS_KERNEL_*), the summed duration in ms and the launch count since the last
+ * reset; `count` is the length of both host arrays. */
+enum {
+    GS_KERNEL_PREPROCESS = 0, GS_KERNEL_PAIR_COUNT, GS_KERNEL_DEPTH_SORT, GS_KERNEL_PAIR_OFFSETS,
+    GS_KERNEL_DUPLICATE, GS_KERNEL_TILE_SORT, GS_KERNEL_RANGES, GS_KERNEL_BLEND_FWD,
+    GS_KERNEL_CLEAR, GS_KERNEL_BLEND_BWD, GS_KERNEL_PREPROCESS_BWD, GS_KERNEL_MLP_REDUCE,
+    GS_KERNEL_COUNT
+};
+gs_status gs_timing_enable(int32_t enable);
+gs_status gs_timing_reset(void);
+gs_status gs_timing_read(double* ms, int64_t* launches, int32_t count);
+const char* gs_kernel_name(int32_t kernel_id);
+
+const char* gs_last_error(void);
+const char* gs_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

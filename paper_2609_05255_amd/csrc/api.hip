@@ -1,0 +1,399 @@
+// C-ABI entry points of gsraster (declared in include/gsraster.h): argument
+// validation on the host, workspace layout, kernel launches on the caller's
+// stream, error reporting, and optional per-kernel timing with HIP events.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "gs_internal.h"
+
+using namespace gsr;
+
+namespace {
+
+thread_local std::string g_error;
+
+gs_status fail(gs_status st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+gs_status fail(gs_status st, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return st;
+}
+
+gs_status ok()
+{
+    g_error.clear();
+    return GS_OK;
+}
+
+#define GS_HIP(expr)                                                                            \
+    do {                                                                                        \
+        hipError_t e_ = (expr);                                                                 \
+        if (e_ != hipSuccess)                                                                   \
+            return fail(GS_ERR_DEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));          \
+    } while (0)
+
+#define GS_CHECK(cond, ...)                                  \
+    do {                                                     \
+        if (!(cond)) return fail(GS_ERR_INVALID_ARG, __VA_ARGS__); \
+    } while (0)
+
+gs_status check_camera(const gs_camera* c)
+{
+    GS_CHECK(c != nullptr, "camera is NULL");
+    GS_CHECK(c->width > 0 && c->height > 0, "image size %dx%d must be positive", c->width, c->height);
+    GS_CHECK((int64_t)c->width * c->height <= ((int64_t)1 << 31), "image of %dx%d pixels is too large",
+             c->width, c->height);
+    GS_CHECK((c->width + kTile - 1) / kTile <= 32767 && (c->height + kTile - 1) / kTile <= 32767,
+             "tile grid exceeds the 16-bit rectangle fields");
+    GS_CHECK(c->fx > 0.f && c->fy > 0.f, "focal lengths must be positive");
+    GS_CHECK(c->near_plane >= 0.f, "near plane must be >= 0");
+    for (int i = 0; i < 12; ++i) GS_CHECK(c->viewmat[i] == c->viewmat[i], "view matrix holds NaN");
+    return GS_OK;
+}
+
+gs_status check_gaussians(const gs_gaussians* g)
+{
+    GS_CHECK(g != nullptr, "gaussians is NULL");
+    GS_CHECK(g->n >= 0 && g->n < ((int64_t)1 << 31), "n = %lld out of range [0, 2^31)", (long long)g->n);
+    if (g->n > 0)
+        GS_CHECK(g->means && g->log_scales && g->quats && g->opacity_logits, "a Gaussian parameter array is NULL");
+    return GS_OK;
+}
+
+gs_status check_appearance(const gs_appearance* a, int64_t n)
+{
+    GS_CHECK(a != nullptr, "appearance is NULL");
+    if (a->kind == GS_APP_SH3) {
+        GS_CHECK(a->sh_degree >= 0 && a->sh_degree <= 3, "sh_degree %d outside 0..3", a->sh_degree);
+        GS_CHECK(n == 0 || a->sh != nullptr, "sh is NULL");
+    } else if (a->kind == GS_APP_LATENT_MLP) {
+        GS_CHECK(n == 0 || (a->latent != nullptr && a->mlp_w != nullptr), "latent or mlp_w is NULL");
+    } else {
+        return fail(GS_ERR_INVALID_ARG, "unknown appearance kind %d", a->kind);
+    }
+    return GS_OK;
+}
+
+gs_status check_pre(const gs_preprocessed* p, int64_t n)
+{
+    GS_CHECK(p != nullptr, "preprocessed is NULL");
+    GS_CHECK(p->num_pairs != nullptr, "num_pairs is NULL");
+    if (n > 0) GS_CHECK(p->splats && p->tiles_touched && p->depth_key, "a preprocess output array is NULL");
+    return GS_OK;
+}
+
+gs_status check_workspace(void* ws, size_t bytes, const Workspace& need)
+{
+    GS_CHECK(ws != nullptr || need.bytes == 0, "workspace is NULL");
+    GS_CHECK(((uintptr_t)ws & 255) == 0, "workspace must be 256-byte aligned");
+    if (bytes < need.bytes)
+        return fail(GS_ERR_CAPACITY, "workspace of %zu bytes is too small: %zu needed", bytes, need.bytes);
+    return GS_OK;
+}
+
+// ---- timing --------------------------------------------------------------------
+struct TimedLaunch {
+    int id;
+    hipEvent_t a, b;
+};
+
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<hipEvent_t> g_free_events;
+std::vector<TimedLaunch> g_pending;
+std::vector<TimedLaunch> g_open;
+double g_ms[GS_KERNEL_COUNT];
+int64_t g_launches[GS_KERNEL_COUNT];
+
+void resolve_pending_locked()
+{
+    for (auto& t : g_pending) {
+        float ms = 0.f;
+        (void)hipEventSynchronize(t.b);
+        if (hipEventElapsedTime(&ms, t.a, t.b) == hipSuccess) {
+            g_ms[t.id] += ms;
+            g_launches[t.id] += 1;
+        }
+        g_free_events.push_back(t.a);
+        g_free_events.push_back(t.b);
+    }
+    g_pending.clear();
+}
+
+const char* const kKernelNames[GS_KERNEL_COUNT] = {
+    "preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
+    "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce"};
+
+}  // namespace
+
+namespace gsr {
+
+void timing_begin(int id, hipStream_t s)
+{
+    if (!g_timing) return;
+    std::lock_guard<std::mutex> lk(g_tmu);
+    if (g_free_events.size() < 2) resolve_pending_locked();
+    if (g_free_events.size() < 2) return;
+    TimedLaunch t;
+    t.id = id;
+    t.a = g_free_events.back();
+    g_free_events.pop_back();
+    t.b = g_free_events.back();
+    g_free_events.pop_back();
+    (void)hipEventRecord(t.a, s);
+    g_open.push_back(t);
+}
+
+void timing_end(int id, hipStream_t s)
+{
+    if (!g_timing) return;
+    std::lock_guard<std::mutex> lk(g_tmu);
+    for (size_t k = g_open.size(); k-- > 0;) {
+        if (g_open[k].id == id) {
+            (void)hipEventRecord(g_open[k].b, s);
+            g_pending.push_back(g_open[k]);
+            g_open.erase(g_open.begin() + (long)k);
+            return;
+        }
+    }
+}
+
+Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kind)
+{
+    Workspace w;
+    memset(&w, 0, sizeof(w));
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> char* {
+        char* p = base ? static_cast<char*>(base) + off : nullptr;
+        off += align_up(bytes, 256);
+        return p;
+    };
+    const int64_t nn = n > 0 ? n : 1;
+    const int64_t cap = capacity > 0 ? (int64_t)capacity : 1;
+    const int64_t sort_blocks = std::max(div_up(nn, kSortTile), div_up(cap, kSortTile));
+    w.block_pairs = (uint32_t*)take(sizeof(uint32_t) * preprocess_blocks(nn));
+    w.keys_a = (uint32_t*)take(sizeof(uint32_t) * nn);
+    w.keys_b = (uint32_t*)take(sizeof(uint32_t) * nn);
+    w.vals_a = (uint32_t*)take(sizeof(uint32_t) * nn);
+    w.vals_b = (uint32_t*)take(sizeof(uint32_t) * nn);
+    w.hist = (uint32_t*)take(sizeof(uint32_t) * kRadix * sort_blocks);
+    w.digit_tot = (uint32_t*)take(sizeof(uint32_t) * kRadix * 4);
+    w.scan_part = (uint32_t*)take(sizeof(uint32_t) * (div_up(nn, kSortTile) + 1));
+    w.pair_keys_a = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.pair_vals_a = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.pair_keys_b = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.pair_vals_b = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.acc = (float*)take(sizeof(float) * kAccStride * nn);
+    w.mlp_part = (float*)take(kind == GS_APP_LATENT_MLP ? sizeof(float) * GS_MLP_WEIGHTS * kMlpPartials : 0);
+    w.bytes = off;
+    return w;
+}
+
+}  // namespace gsr
+
+extern "C" {
+
+const char* gs_last_error(void) { return g_error.c_str(); }
+
+const char* gs_version(void) { return "gsraster 0.1.0 (gfx950)"; }
+
+const char* gs_kernel_name(int32_t id) { return (id >= 0 && id < GS_KERNEL_COUNT) ? kKernelNames[id] : "unknown"; }
+
+gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t capacity, int32_t kind, size_t* bytes)
+{
+    GS_CHECK(bytes != nullptr, "bytes is NULL");
+    GS_CHECK(n >= 0 && n < ((int64_t)1 << 31), "n out of range");
+    GS_CHECK(width > 0 && height > 0, "image size must be positive");
+    GS_CHECK(capacity < ((uint64_t)1 << 32), "capacity must be below 2^32");
+    GS_CHECK(kind == GS_APP_SH3 || kind == GS_APP_LATENT_MLP, "unknown appearance kind %d", kind);
+    *bytes = layout_workspace(nullptr, n, capacity, kind).bytes;
+    return ok();
+}
+
+gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                        const gs_preprocessed* out, uint64_t* num_pairs_host, void* workspace, size_t workspace_bytes,
+                        void* stream)
+{
+    gs_status st;
+    if ((st = check_camera(cam)) != GS_OK) return st;
+    if ((st = check_gaussians(g)) != GS_OK) return st;
+    if ((st = check_appearance(app, g->n)) != GS_OK) return st;
+    if ((st = check_pre(out, g->n)) != GS_OK) return st;
+    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind);
+    if ((st = check_workspace(workspace, workspace_bytes, layout_workspace(nullptr, g->n, 0, app->kind))) != GS_OK)
+        return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Cam c = make_cam(*cam);
+    if (g->n > 0) {
+        timing_begin(GS_KERNEL_PREPROCESS, s);
+        GS_HIP(launch_preprocess(c, *g, *app, *out, ws, s));
+        timing_end(GS_KERNEL_PREPROCESS, s);
+        timing_begin(GS_KERNEL_PAIR_COUNT, s);
+        GS_HIP(launch_pair_count(g->n, ws, out->num_pairs, s));
+        timing_end(GS_KERNEL_PAIR_COUNT, s);
+    } else {
+        GS_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(out->num_pairs), 2, 0u, s));
+    }
+    if (num_pairs_host) {
+        GS_HIP(hipMemcpyAsync(num_pairs_host, out->num_pairs, sizeof(uint64_t), hipMemcpyDeviceToHost, s));
+        GS_HIP(hipStreamSynchronize(s));
+    }
+    return ok();
+}
+
+gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, uint64_t num_pairs,
+                      uint64_t capacity, uint32_t* values, uint32_t* tile_ids, uint32_t* tile_ranges, void* workspace,
+                      size_t workspace_bytes, void* stream)
+{
+    gs_status st;
+    if ((st = check_camera(cam)) != GS_OK) return st;
+    GS_CHECK(n >= 0 && n < ((int64_t)1 << 31), "n out of range");
+    if ((st = check_pre(pre, n)) != GS_OK) return st;
+    GS_CHECK(capacity < ((uint64_t)1 << 32), "capacity must be below 2^32");
+    if (num_pairs > capacity)
+        return fail(GS_ERR_CAPACITY, "%llu pairs exceed the capacity %llu", (unsigned long long)num_pairs,
+                    (unsigned long long)capacity);
+    GS_CHECK(tile_ranges != nullptr, "tile_ranges is NULL");
+    GS_CHECK(num_pairs == 0 || values != nullptr, "values is NULL");
+    const Workspace need = layout_workspace(nullptr, n, capacity, GS_APP_SH3);
+    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
+    const Workspace ws = layout_workspace(workspace, n, capacity, GS_APP_SH3);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Cam c = make_cam(*cam);
+    const int n_tiles = c.tiles_x * c.tiles_y;
+    if (num_pairs == 0 || n == 0) {
+        GS_HIP(launch_fill_u32(tile_ranges, 2 * (int64_t)n_tiles, 0u, s));
+        return ok();
+    }
+    const uint32_t* order = nullptr;
+    timing_begin(GS_KERNEL_DEPTH_SORT, s);
+    GS_HIP(launch_depth_sort(n, pre->depth_key, ws, &order, s));
+    timing_end(GS_KERNEL_DEPTH_SORT, s);
+    timing_begin(GS_KERNEL_PAIR_OFFSETS, s);
+    GS_HIP(launch_pair_offsets(n, order, pre->tiles_touched, ws, s));
+    timing_end(GS_KERNEL_PAIR_OFFSETS, s);
+    const int passes = tile_sort_passes(c);
+    const uint32_t* sorted_tiles = nullptr;
+    uint32_t* dup_keys = ws.pair_keys_a;
+    uint32_t* dup_vals = ws.pair_vals_a;
+    if (passes == 0) {
+        dup_keys = tile_ids ? tile_ids : ws.pair_keys_a;
+        dup_vals = values;
+        sorted_tiles = dup_keys;
+    }
+    timing_begin(GS_KERNEL_DUPLICATE, s);
+    GS_HIP(launch_duplicate(c, n, order, *pre, ws, (uint32_t)capacity, dup_keys, dup_vals, s));
+    timing_end(GS_KERNEL_DUPLICATE, s);
+    if (passes > 0) {
+        timing_begin(GS_KERNEL_TILE_SORT, s);
+        GS_HIP(launch_tile_sort(c, num_pairs, ws, values, tile_ids, &sorted_tiles, s));
+        timing_end(GS_KERNEL_TILE_SORT, s);
+    }
+    timing_begin(GS_KERNEL_RANGES, s);
+    GS_HIP(launch_ranges(c, num_pairs, sorted_tiles, tile_ranges, s));
+    timing_end(GS_KERNEL_RANGES, s);
+    return ok();
+}
+
+gs_status gs_render_fwd(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, const uint32_t* values,
+                        const uint32_t* tile_ranges, float* image, float* final_T, uint32_t* n_contrib, void* stream)
+{
+    gs_status st;
+    if ((st = check_camera(cam)) != GS_OK) return st;
+    if ((st = check_pre(pre, n)) != GS_OK) return st;
+    GS_CHECK(tile_ranges && image && final_T && n_contrib, "an output or range array is NULL");
+    GS_CHECK(n == 0 || values != nullptr, "values is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Cam c = make_cam(*cam);
+    timing_begin(GS_KERNEL_BLEND_FWD, s);
+    GS_HIP(launch_blend_fwd(c, pre->splats, values, tile_ranges, image, final_T, n_contrib, s));
+    timing_end(GS_KERNEL_BLEND_FWD, s);
+    return ok();
+}
+
+gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                        const gs_preprocessed* pre, const uint32_t* values, const uint32_t* tile_ranges,
+                        const float* final_T, const uint32_t* n_contrib, const float* dL_dimage, const gs_grads* grads,
+                        void* workspace, size_t workspace_bytes, void* stream)
+{
+    gs_status st;
+    if ((st = check_camera(cam)) != GS_OK) return st;
+    if ((st = check_gaussians(g)) != GS_OK) return st;
+    if ((st = check_appearance(app, g->n)) != GS_OK) return st;
+    if ((st = check_pre(pre, g->n)) != GS_OK) return st;
+    GS_CHECK(tile_ranges && final_T && n_contrib && dL_dimage, "a render input array is NULL");
+    GS_CHECK(grads != nullptr, "grads is NULL");
+    if (g->n > 0) {
+        GS_CHECK(grads->dmeans && grads->dlog_scales && grads->dquats && grads->dopacity_logits,
+                 "a geometry gradient array is NULL");
+        if (app->kind == GS_APP_SH3) GS_CHECK(grads->dsh != nullptr, "dsh is NULL");
+        else GS_CHECK(grads->dlatent && grads->dmlp_w, "dlatent or dmlp_w is NULL");
+    }
+    const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind);
+    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
+    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Cam c = make_cam(*cam);
+    if (g->n == 0) {
+        if (app->kind == GS_APP_LATENT_MLP) GS_HIP(launch_clear(grads->dmlp_w, GS_MLP_WEIGHTS, s));
+        return ok();
+    }
+    timing_begin(GS_KERNEL_CLEAR, s);
+    GS_HIP(launch_clear(ws.acc, (int64_t)kAccStride * g->n, s));
+    timing_end(GS_KERNEL_CLEAR, s);
+    timing_begin(GS_KERNEL_BLEND_BWD, s);
+    GS_HIP(launch_blend_bwd(c, pre->splats, values, tile_ranges, final_T, n_contrib, dL_dimage, ws.acc, s));
+    timing_end(GS_KERNEL_BLEND_BWD, s);
+    timing_begin(GS_KERNEL_PREPROCESS_BWD, s);
+    GS_HIP(launch_preprocess_bwd(c, *g, *app, *pre, ws, *grads, s));
+    timing_end(GS_KERNEL_PREPROCESS_BWD, s);
+    if (app->kind == GS_APP_LATENT_MLP) {
+        timing_begin(GS_KERNEL_MLP_REDUCE, s);
+        GS_HIP(launch_mlp_reduce(g->n, ws, grads->dmlp_w, s));
+        timing_end(GS_KERNEL_MLP_REDUCE, s);
+    }
+    return ok();
+}
+
+gs_status gs_timing_enable(int32_t enable)
+{
+    std::lock_guard<std::mutex> lk(g_tmu);
+    if (enable && g_free_events.empty() && g_pending.empty()) {
+        for (int k = 0; k < 2048; ++k) {
+            hipEvent_t e;
+            if (hipEventCreate(&e) != hipSuccess) return fail(GS_ERR_DEVICE, "hipEventCreate failed");
+            g_free_events.push_back(e);
+        }
+    }
+    g_timing = enable != 0;
+    return ok();
+}
+
+gs_status gs_timing_reset(void)
+{
+    std::lock_guard<std::mutex> lk(g_tmu);
+    resolve_pending_locked();
+    for (int k = 0; k < GS_KERNEL_COUNT; ++k) { g_ms[k] = 0.0; g_launches[k] = 0; }
+    return ok();
+}
+
+gs_status gs_timing_read(double* ms, int64_t* launches, int32_t count)
+{
+    GS_CHECK(ms != nullptr && launches != nullptr, "output arrays are NULL");
+    std::lock_guard<std::mutex> lk(g_tmu);
+    resolve_pending_locked();
+    for (int k = 0; k < count && k < GS_KERNEL_COUNT; ++k) { ms[k] = g_ms[k]; launches[k] = g_launches[k]; }
+    return ok();
+}
+
+}  // extern "C"

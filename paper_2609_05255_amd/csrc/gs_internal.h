@@ -1,0 +1,120 @@
+// Internal declarations of the gsraster HIP library (gfx950 / CDNA4).
+// Kernels are launched only from the C-ABI entry points in api.hip.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "../../include/gsraster.h"
+
+namespace gsr {
+
+constexpr int kTile = GS_TILE;
+constexpr int kBlock = 256;               // 4 wave64 per workgroup
+constexpr int kWave = 64;
+
+// Camera as the kernels see it (by value in kernel arguments).
+struct Cam {
+    float V[12];          // row-major [R|t]
+    float campos[3];
+    float fx, fy, cx, cy;
+    int width, height;
+    int tiles_x, tiles_y;
+    float near_plane;
+    float bg[3];
+};
+
+inline Cam make_cam(const gs_camera& c) {
+    Cam k;
+    for (int i = 0; i < 12; ++i) k.V[i] = c.viewmat[i];
+    for (int i = 0; i < 3; ++i) { k.campos[i] = c.campos[i]; k.bg[i] = c.bg[i]; }
+    k.fx = c.fx; k.fy = c.fy; k.cx = c.cx; k.cy = c.cy;
+    k.width = c.width; k.height = c.height;
+    k.tiles_x = (c.width + kTile - 1) / kTile;
+    k.tiles_y = (c.height + kTile - 1) / kTile;
+    k.near_plane = c.near_plane;
+    return k;
+}
+
+// Splat record as three 16-byte words (layout of gs_splat).
+//  w0 = mean_x, mean_y, conic_a, conic_b
+//  w1 = conic_c, opacity, color r, color g
+//  w2 = color b, depth, rect (x0 | y0 << 16), rect (x1 | y1 << 16)
+static_assert(sizeof(gs_splat) == 48, "splat record must be 48 bytes");
+
+// Per-Gaussian screen-space gradient accumulator written by the blend backward.
+// Stride 9 floats: dmean_x, dmean_y, dconic_a, dconic_b, dconic_c, dopacity, dcolor rgb.
+constexpr int kAccStride = 9;
+
+// Radix-sort geometry: 256 threads x 16 keys per workgroup, 8-bit digits.
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kBlock * kSortItems;   // 4096
+constexpr int kRadix = 256;
+
+// Workgroups of the latent preprocess backward (grid-stride), one partial
+// weight gradient each.
+constexpr int kMlpPartials = 1024;
+
+inline int64_t div_up(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
+
+// ---- workspace layout -------------------------------------------------------
+// One layout serves every call; gs_workspace_size returns its total.
+struct Workspace {
+    uint32_t* block_pairs;   // [nblocks_pre]     per-preprocess-block tile sums
+    uint32_t* keys_a;        // [n]               depth-sort ping-pong keys
+    uint32_t* keys_b;        // [n]
+    uint32_t* vals_a;        // [n]               depth-sort values
+    uint32_t* vals_b;        // [n]
+    uint32_t* hist;          // [256][max sort blocks]
+    uint32_t* digit_tot;     // [4 passes][256]   digit totals of each pass
+    uint32_t* scan_part;     // [n / 4096 + 1]    block sums of the pair-offset scan
+    uint32_t* pair_keys_a;   // [capacity]
+    uint32_t* pair_vals_a;   // [capacity]
+    uint32_t* pair_keys_b;   // [capacity]
+    uint32_t* pair_vals_b;   // [capacity]
+    float* acc;              // [n][9]            blend-backward accumulators
+    float* mlp_part;         // [kMlpPartials][1664] per-workgroup decoder weight gradients
+    size_t bytes;
+};
+
+Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kind);
+
+// ---- launch helpers (defined in the kernel files) ---------------------------
+hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
+                             const gs_preprocessed& out, const Workspace& ws, hipStream_t s);
+hipError_t launch_pair_count(int64_t n, const Workspace& ws, uint64_t* num_pairs, hipStream_t s);
+hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const Workspace& ws,
+                             const uint32_t** order_out, hipStream_t s);
+hipError_t launch_pair_offsets(int64_t n, const uint32_t* order, const uint32_t* tiles_touched,
+                               const Workspace& ws, hipStream_t s);
+hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const gs_preprocessed& pre,
+                            const Workspace& ws, uint32_t capacity, uint32_t* keys_out, uint32_t* vals_out,
+                            hipStream_t s);
+int tile_sort_passes(const Cam& cam);
+hipError_t launch_fill_u32(uint32_t* p, int64_t count, uint32_t value, hipStream_t s);
+hipError_t launch_tile_sort(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
+                            uint32_t* tile_ids_out, const uint32_t** sorted_tiles, hipStream_t s);
+hipError_t launch_ranges(const Cam& cam, uint64_t num_pairs, const uint32_t* sorted_tiles,
+                         uint32_t* tile_ranges, hipStream_t s);
+hipError_t launch_blend_fwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
+                            const uint32_t* tile_ranges, float* image, float* final_T, uint32_t* n_contrib,
+                            hipStream_t s);
+hipError_t launch_clear(float* p, int64_t count, hipStream_t s);
+hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
+                            const uint32_t* tile_ranges, const float* final_T, const uint32_t* n_contrib,
+                            const float* dL_dimage, float* acc, hipStream_t s);
+hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
+                                 const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr,
+                                 hipStream_t s);
+hipError_t launch_mlp_reduce(int64_t n, const Workspace& ws, float* dmlp_w, hipStream_t s);
+
+// Kernel timing hooks (api.hip): bracket one logical kernel id.
+void timing_begin(int kernel_id, hipStream_t s);
+void timing_end(int kernel_id, hipStream_t s);
+
+inline int preprocess_blocks(int64_t n) { return (int)div_up(n > 0 ? n : 1, kBlock); }
+
+}  // namespace gsr

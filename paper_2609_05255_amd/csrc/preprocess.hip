@@ -1,0 +1,267 @@
+// Preprocess (Sec. 3.1) with the appearance fused in (appendix, fused rasterizer):
+// one thread per Gaussian, planar coalesced parameter reads, culling, EWA
+// projection, tile rectangle, colour for survivors only, and the per-block tile
+// counts from which the number of pairs follows.
+//
+// The whole file is compiled without floating-point contraction: the tile
+// rectangle and the depth key are integers decided by this fp32 arithmetic,
+// and they must not depend on which multiply-adds the compiler fuses.
+#include "gs_internal.h"
+#include "sh.h"
+
+#pragma clang fp contract(off)
+
+namespace gsr {
+
+namespace {
+
+struct Geo {
+    bool visible, clamp_x, clamp_y;
+    float mx, my, ca, cb, cc, op, depth;
+    int x0, y0, x1, y1;
+    uint32_t tiles;
+};
+
+__device__ __forceinline__ float clampf(float v, float lo, float hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+// Activation, projection, EWA covariance with a 0.3 px^2 low-pass, 3-sigma
+// rectangle. Operation order is fixed (see the file comment).
+__device__ __forceinline__ void geometry(const Cam& c, const float mu[3], const float ls[3], const float q[4],
+                                         float logit, Geo& g)
+{
+    g.visible = false;
+    g.clamp_x = g.clamp_y = false;
+    g.tiles = 0;
+    float s[3];
+    for (int j = 0; j < 3; ++j) s[j] = (float)exp((double)ls[j]);
+    const float op = (float)(1.0 / (1.0 + exp(-(double)logit)));
+
+    const float qn = sqrtf(((q[0] * q[0] + q[1] * q[1]) + q[2] * q[2]) + q[3] * q[3]);
+    const float w = q[0] / qn, x = q[1] / qn, y = q[2] / qn, z = q[3] / qn;
+    float R[9];
+    R[0] = 1.f - 2.f * (y * y + z * z); R[1] = 2.f * (x * y - w * z);       R[2] = 2.f * (x * z + w * y);
+    R[3] = 2.f * (x * y + w * z);       R[4] = 1.f - 2.f * (x * x + z * z); R[5] = 2.f * (y * z - w * x);
+    R[6] = 2.f * (x * z - w * y);       R[7] = 2.f * (y * z + w * x);       R[8] = 1.f - 2.f * (x * x + y * y);
+    float M[9];
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+        for (int k = 0; k < 3; ++k) M[3 * r + k] = R[3 * r + k] * s[k];
+    float S[9];
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+            S[3 * r + k] = (M[3 * r + 0] * M[3 * k + 0] + M[3 * r + 1] * M[3 * k + 1]) + M[3 * r + 2] * M[3 * k + 2];
+
+    float t[3];
+#pragma unroll
+    for (int r = 0; r < 3; ++r) t[r] = ((c.V[4 * r + 0] * mu[0] + c.V[4 * r + 1] * mu[1]) + c.V[4 * r + 2] * mu[2]) + c.V[4 * r + 3];
+    if (!(t[2] > c.near_plane)) return;
+
+    const float limx = 1.3f * ((0.5f * (float)c.width) / c.fx);
+    const float limy = 1.3f * ((0.5f * (float)c.height) / c.fy);
+    const float txtz = t[0] / t[2], tytz = t[1] / t[2];
+    float ux = txtz, uy = tytz;
+    if (ux < -limx) { ux = -limx; g.clamp_x = true; }
+    if (ux > limx) { ux = limx; g.clamp_x = true; }
+    if (uy < -limy) { uy = -limy; g.clamp_y = true; }
+    if (uy > limy) { uy = limy; g.clamp_y = true; }
+    ux = ux * t[2];
+    uy = uy * t[2];
+    const float tz2 = t[2] * t[2];
+    const float j00 = c.fx / t[2], j02 = -(c.fx * ux) / tz2;
+    const float j11 = c.fy / t[2], j12 = -(c.fy * uy) / tz2;
+    float T[6];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        T[k] = j00 * c.V[0 + k] + j02 * c.V[8 + k];
+        T[3 + k] = j11 * c.V[4 + k] + j12 * c.V[8 + k];
+    }
+    float A[6];
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+            A[3 * r + k] = (T[3 * r + 0] * S[0 + k] + T[3 * r + 1] * S[3 + k]) + T[3 * r + 2] * S[6 + k];
+    float c00 = (A[0] * T[0] + A[1] * T[1]) + A[2] * T[2];
+    const float c01 = (A[0] * T[3] + A[1] * T[4]) + A[2] * T[5];
+    float c11 = (A[3] * T[3] + A[4] * T[4]) + A[5] * T[5];
+    c00 = c00 + 0.3f;
+    c11 = c11 + 0.3f;
+    const float det = c00 * c11 - c01 * c01;
+    if (!(det > 0.f)) return;
+    g.ca = c11 / det;
+    g.cb = -c01 / det;
+    g.cc = c00 / det;
+
+    const float mid = 0.5f * (c00 + c11);
+    float disc = mid * mid - det;
+    if (disc < 0.1f) disc = 0.1f;
+    const float lam = mid + sqrtf(disc);
+    const float rad = ceilf(3.f * sqrtf(lam));
+
+    const float px = c.fx * txtz + c.cx, py = c.fy * tytz + c.cy;
+    const float tx = (float)c.tiles_x, ty = (float)c.tiles_y;
+    const float fx0 = clampf(floorf((px - rad) / 16.f), 0.f, tx);
+    const float fx1 = clampf(ceilf((px + rad) / 16.f), 0.f, tx);
+    const float fy0 = clampf(floorf((py - rad) / 16.f), 0.f, ty);
+    const float fy1 = clampf(ceilf((py + rad) / 16.f), 0.f, ty);
+    g.x0 = (int)fx0; g.x1 = (int)fx1; g.y0 = (int)fy0; g.y1 = (int)fy1;
+    const int tiles = (g.x1 - g.x0) * (g.y1 - g.y0);
+    if (tiles <= 0) return;
+    g.tiles = (uint32_t)tiles;
+    g.visible = true;
+    g.mx = px;
+    g.my = py;
+    g.op = op;
+    g.depth = t[2];
+}
+
+struct PreArgs {
+    Cam cam;
+    int n;
+    const float* means;
+    const float* log_scales;
+    const float* quats;
+    const float* logits;
+    int sh_degree;
+    const float* sh;
+    const uint16_t* latent;
+    const uint16_t* mlp_w;
+    gs_splat* splats;
+    uint32_t* tiles_touched;
+    uint32_t* depth_key;
+    uint32_t* block_pairs;
+};
+
+__device__ __forceinline__ void store_splat(gs_splat* dst, const Geo& g, const float col[3])
+{
+    float4* p = reinterpret_cast<float4*>(dst);
+    p[0] = make_float4(g.mx, g.my, g.ca, g.cb);
+    p[1] = make_float4(g.cc, g.op, col[0], col[1]);
+    const uint32_t r01 = (uint32_t)(g.x0 & 0xFFFF) | ((uint32_t)g.y0 << 16);
+    const uint32_t r23 = (uint32_t)(g.x1 & 0xFFFF) | ((uint32_t)g.y1 << 16);
+    p[2] = make_float4(col[2], g.depth, __uint_as_float(r01), __uint_as_float(r23));
+}
+
+// Sum of a u32 over the workgroup; result valid in thread 0.
+__device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* lds4)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) lds4[wave] = v;
+    __syncthreads();
+    uint32_t r = 0;
+    if (threadIdx.x == 0) r = lds4[0] + lds4[1] + lds4[2] + lds4[3];
+    return r;
+}
+
+__device__ __forceinline__ void load_geometry_params(const PreArgs& a, int i, float mu[3], float ls[3], float q[4],
+                                                     float& logit)
+{
+    const int64_t n = a.n;
+    for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
+    for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
+    for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
+    logit = a.logits[i];
+}
+
+__device__ __forceinline__ void view_dir(const Cam& c, const float mu[3], float d[3])
+{
+    const float vx = mu[0] - c.campos[0], vy = mu[1] - c.campos[1], vz = mu[2] - c.campos[2];
+    const float len = sqrtf(vx * vx + vy * vy + vz * vz);
+    d[0] = vx / len;
+    d[1] = vy / len;
+    d[2] = vz / len;
+}
+
+}  // namespace
+
+// eq. sh_color_eval: c = max(0, 0.5 + sum over bands <= degree of Y_k(d) sh_k).
+__device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n, int i, int degree, const float d[3],
+                                         float col[3])
+{
+    float Y[16];
+    sh_basis16(d[0], d[1], d[2], Y);
+    const int nb = (degree + 1) * (degree + 1);
+    for (int ch = 0; ch < 3; ++ch) {
+        float acc = 0.5f;
+        for (int k = 0; k < nb; ++k) acc += Y[k] * sh[(int64_t)(3 * k + ch) * n + i];
+        col[ch] = acc > 0.f ? acc : 0.f;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
+{
+    __shared__ uint32_t red[4];
+    const int i = blockIdx.x * kBlock + threadIdx.x;
+    uint32_t tiles = 0;
+    if (i < a.n) {
+        float mu[3], ls[3], q[4], logit;
+        load_geometry_params(a, i, mu, ls, q, logit);
+        Geo g;
+        geometry(a.cam, mu, ls, q, logit, g);
+        if (g.visible) {
+            float d[3], col[3];
+            view_dir(a.cam, mu, d);
+            sh_color(a.sh, a.n, i, a.sh_degree, d, col);
+            store_splat(a.splats + i, g, col);
+            tiles = g.tiles;
+        }
+        a.tiles_touched[i] = tiles;
+        a.depth_key[i] = g.visible ? __float_as_uint(g.depth) : 0xFFFFFFFFu;
+    }
+    const uint32_t total = block_sum_u32(tiles, red);
+    if (threadIdx.x == 0) a.block_pairs[blockIdx.x] = total;
+}
+
+hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
+                             const gs_preprocessed& out, const Workspace& ws, hipStream_t s)
+{
+    PreArgs a;
+    a.cam = cam;
+    a.n = (int)g.n;
+    a.means = g.means;
+    a.log_scales = g.log_scales;
+    a.quats = g.quats;
+    a.logits = g.opacity_logits;
+    a.sh_degree = app.sh_degree;
+    a.sh = app.sh;
+    a.latent = app.latent;
+    a.mlp_w = app.mlp_w;
+    a.splats = out.splats;
+    a.tiles_touched = out.tiles_touched;
+    a.depth_key = out.depth_key;
+    a.block_pairs = ws.block_pairs;
+    const int blocks = preprocess_blocks(g.n);
+    if (app.kind != GS_APP_SH3) return hipErrorNotSupported;
+    hipLaunchKernelGGL(k_preprocess_sh3, dim3(blocks), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
+}
+
+// Total pairs = sum of the per-block tile counts (fixed order, one workgroup).
+__global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs, int nblocks, uint64_t* out)
+{
+    __shared__ uint64_t red[16];
+    uint64_t v = 0;
+    for (int b = threadIdx.x; b < nblocks; b += 1024) v += block_pairs[b];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t t = 0;
+        for (int w = 0; w < 16; ++w) t += red[w];
+        out[0] = t;
+    }
+}
+
+hipError_t launch_pair_count(int64_t n, const Workspace& ws, uint64_t* num_pairs, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_pair_count, dim3(1), dim3(1024), 0, s, ws.block_pairs, preprocess_blocks(n), num_pairs);
+    return hipGetLastError();
+}
+
+}  // namespace gsr

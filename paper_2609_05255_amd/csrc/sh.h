@@ -1,0 +1,65 @@
+// Real spherical harmonics of degree <= 3 for the appearance model of
+// eq. sh_color_eval, as homogeneous polynomials of the unit direction (x, y, z).
+// Basis k = l^2 + l + m (m = -l..l), Condon-Shortley phase kept, so band 1 is
+// sqrt(3/(4 pi)) (-y, z, -x). Each constant is N_lm * sqrt(2) (for m != 0)
+// times the factor that the m-th derivative of the Legendre polynomial P_l and
+// (x + iy)^m contribute, N_lm = sqrt((2l+1)/(4 pi) (l-m)!/(l+m)!).
+#pragma once
+
+namespace gsr {
+
+constexpr float kSH0 = 0.28209479177387814f;    // 1/(2 sqrt(pi))
+constexpr float kSH1 = 0.48860251190291992f;    // sqrt(3/(4 pi))
+constexpr float kSH2a = 1.0925484305920792f;    // sqrt(15/pi)/2
+constexpr float kSH2b = 0.31539156525252005f;   // sqrt(5/pi)/4
+constexpr float kSH2c = 0.54627421529603959f;   // sqrt(15/pi)/4
+constexpr float kSH3a = -0.59004358992664352f;  // -sqrt(35/(2 pi))/4
+constexpr float kSH3b = 2.8906114426405538f;    // sqrt(105/pi)/2
+constexpr float kSH3c = -0.45704579946446572f;  // -sqrt(21/(2 pi))/4
+constexpr float kSH3d = 0.37317633259011546f;   // sqrt(7/pi)/4
+constexpr float kSH3e = 1.4453057213202769f;    // sqrt(105/pi)/4
+
+__device__ __forceinline__ void sh_basis16(float x, float y, float z, float Y[16])
+{
+    const float xx = x * x, yy = y * y, zz = z * z;
+    Y[0] = kSH0;
+    Y[1] = -kSH1 * y;
+    Y[2] = kSH1 * z;
+    Y[3] = -kSH1 * x;
+    Y[4] = kSH2a * x * y;
+    Y[5] = -kSH2a * y * z;
+    Y[6] = kSH2b * (2.f * zz - xx - yy);
+    Y[7] = -kSH2a * x * z;
+    Y[8] = kSH2c * (xx - yy);
+    Y[9] = kSH3a * y * (3.f * xx - yy);
+    Y[10] = kSH3b * x * y * z;
+    Y[11] = kSH3c * y * (4.f * zz - xx - yy);
+    Y[12] = kSH3d * z * (2.f * zz - 3.f * xx - 3.f * yy);
+    Y[13] = kSH3c * x * (4.f * zz - xx - yy);
+    Y[14] = kSH3e * z * (xx - yy);
+    Y[15] = kSH3a * x * (xx - 3.f * yy);
+}
+
+// Gradient of each basis polynomial w.r.t. (x, y, z): G[3k + j] = dY_k/dx_j.
+__device__ __forceinline__ void sh_basis16_grad(float x, float y, float z, float G[48])
+{
+    const float xx = x * x, yy = y * y, zz = z * z;
+    G[0] = 0.f; G[1] = 0.f; G[2] = 0.f;
+    G[3] = 0.f; G[4] = -kSH1; G[5] = 0.f;
+    G[6] = 0.f; G[7] = 0.f; G[8] = kSH1;
+    G[9] = -kSH1; G[10] = 0.f; G[11] = 0.f;
+    G[12] = kSH2a * y; G[13] = kSH2a * x; G[14] = 0.f;
+    G[15] = 0.f; G[16] = -kSH2a * z; G[17] = -kSH2a * y;
+    G[18] = -2.f * kSH2b * x; G[19] = -2.f * kSH2b * y; G[20] = 4.f * kSH2b * z;
+    G[21] = -kSH2a * z; G[22] = 0.f; G[23] = -kSH2a * x;
+    G[24] = 2.f * kSH2c * x; G[25] = -2.f * kSH2c * y; G[26] = 0.f;
+    G[27] = 6.f * kSH3a * x * y; G[28] = 3.f * kSH3a * (xx - yy); G[29] = 0.f;
+    G[30] = kSH3b * y * z; G[31] = kSH3b * x * z; G[32] = kSH3b * x * y;
+    G[33] = -2.f * kSH3c * x * y; G[34] = kSH3c * (4.f * zz - xx - 3.f * yy); G[35] = 8.f * kSH3c * y * z;
+    G[36] = -6.f * kSH3d * x * z; G[37] = -6.f * kSH3d * y * z; G[38] = kSH3d * (6.f * zz - 3.f * xx - 3.f * yy);
+    G[39] = kSH3c * (4.f * zz - 3.f * xx - yy); G[40] = -2.f * kSH3c * x * y; G[41] = 8.f * kSH3c * x * z;
+    G[42] = 2.f * kSH3e * x * z; G[43] = -2.f * kSH3e * y * z; G[44] = kSH3e * (xx - yy);
+    G[45] = 3.f * kSH3a * (xx - yy); G[46] = -6.f * kSH3a * x * y; G[47] = 0.f;
+}
+
+}  // namespace gsr

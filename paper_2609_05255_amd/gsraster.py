@@ -1,0 +1,261 @@
+"""Python binding of libgsraster.so (the C ABI of include/gsraster.h).
+
+Argument marshalling only: torch tensors provide device memory and the stream,
+every step of the rasterizer runs in the HIP library. The library must have
+been built (``python -m paper_2609_05255_amd.build``); importing this module
+raises if it is missing, there is no fallback.
+
+Function names follow the C ABI: gs_preprocess, gs_bin_sort, gs_render_fwd,
+gs_render_bwd, gs_workspace_size. ``Frame`` owns the buffers of one camera's
+forward + backward pass for a scene of n Gaussians.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgsraster.so")
+
+GS_OK, GS_ERR_INVALID_ARG, GS_ERR_CAPACITY, GS_ERR_DEVICE, GS_ERR_UNSUPPORTED = range(5)
+GS_APP_SH3, GS_APP_LATENT_MLP = 0, 1
+KERNEL_NAMES = ["preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
+                "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce"]
+SPLAT_BYTES = 48
+MLP_WEIGHTS = 1664
+
+
+class GsError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("gsraster status %d: %s" % (status, msg))
+        self.status = status
+
+
+class Camera(C.Structure):
+    _fields_ = [("viewmat", C.c_float * 12), ("campos", C.c_float * 3), ("fx", C.c_float), ("fy", C.c_float),
+                ("cx", C.c_float), ("cy", C.c_float), ("width", C.c_int32), ("height", C.c_int32),
+                ("near_plane", C.c_float), ("bg", C.c_float * 3)]
+
+
+class Gaussians(C.Structure):
+    _fields_ = [("n", C.c_int64), ("means", C.c_void_p), ("log_scales", C.c_void_p), ("quats", C.c_void_p),
+                ("opacity_logits", C.c_void_p)]
+
+
+class Appearance(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p), ("latent", C.c_void_p),
+                ("mlp_w", C.c_void_p)]
+
+
+class Preprocessed(C.Structure):
+    _fields_ = [("splats", C.c_void_p), ("tiles_touched", C.c_void_p), ("depth_key", C.c_void_p),
+                ("num_pairs", C.c_void_p)]
+
+
+class Grads(C.Structure):
+    _fields_ = [("dmeans", C.c_void_p), ("dlog_scales", C.c_void_p), ("dquats", C.c_void_p),
+                ("dopacity_logits", C.c_void_p), ("dsh", C.c_void_p), ("dlatent", C.c_void_p),
+                ("dmlp_w", C.c_void_p), ("dmean2d", C.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libgsraster.so is not built (python -m paper_2609_05255_amd.build)")
+        L = C.CDLL(LIB_PATH)
+        vp, i32, i64, u64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_size_t
+        P = C.POINTER
+        L.gs_preprocess.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), P(u64), vp, sz, vp]
+        L.gs_bin_sort.argtypes = [P(Camera), P(Preprocessed), i64, u64, u64, vp, vp, vp, vp, sz, vp]
+        L.gs_render_fwd.argtypes = [P(Camera), P(Preprocessed), i64, vp, vp, vp, vp, vp, vp]
+        L.gs_render_bwd.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), vp, vp, vp, vp, vp,
+                                    P(Grads), vp, sz, vp]
+        L.gs_workspace_size.argtypes = [i64, i32, i32, u64, i32, P(sz)]
+        L.gs_timing_enable.argtypes = [i32]
+        L.gs_timing_reset.argtypes = []
+        L.gs_timing_read.argtypes = [P(C.c_double), P(i64), i32]
+        for f in ("gs_preprocess", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd", "gs_workspace_size",
+                  "gs_timing_enable", "gs_timing_reset", "gs_timing_read"):
+            getattr(L, f).restype = C.c_int
+        L.gs_last_error.restype = C.c_char_p
+        L.gs_version.restype = C.c_char_p
+        L.gs_kernel_name.restype = C.c_char_p
+        L.gs_kernel_name.argtypes = [i32]
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != GS_OK:
+        raise GsError(status, lib().gs_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return C.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return C.c_void_p(stream.cuda_stream)
+    return C.c_void_p(stream)
+
+
+def camera_struct(cam) -> Camera:
+    c = Camera()
+    vm = [float(v) for v in list(cam.viewmat.reshape(-1))]
+    for k in range(12):
+        c.viewmat[k] = vm[k]
+    for k in range(3):
+        c.campos[k] = float(cam.campos[k])
+        c.bg[k] = float(cam.bg[k])
+    c.fx, c.fy, c.cx, c.cy = float(cam.fx), float(cam.fy), float(cam.cx), float(cam.cy)
+    c.width, c.height = int(cam.width), int(cam.height)
+    c.near_plane = float(cam.near)
+    return c
+
+
+class SceneTensors:
+    """Scene parameters resident on the GPU (planar, contiguous)."""
+
+    def __init__(self, scene, device="cuda"):
+        f32 = lambda a: torch.from_numpy(a).to(device=device, dtype=torch.float32).contiguous()
+        h16 = lambda a: torch.from_numpy(a.view("int16")).to(device=device).contiguous()
+        self.n = int(scene.n)
+        self.means = f32(scene.means)
+        self.log_scales = f32(scene.log_scales)
+        self.quats = f32(scene.quats)
+        self.opacity_logits = f32(scene.opacity_logits)
+        self.sh = f32(scene.sh) if getattr(scene, "sh", None) is not None else None
+        self.latent = h16(scene.latent) if getattr(scene, "latent", None) is not None else None
+        self.mlp_w = h16(scene.mlp_w) if getattr(scene, "mlp_w", None) is not None else None
+
+    def gaussians(self) -> Gaussians:
+        return Gaussians(self.n, _ptr(self.means), _ptr(self.log_scales), _ptr(self.quats),
+                         _ptr(self.opacity_logits))
+
+    def appearance(self, kind: int, sh_degree: int = 3) -> Appearance:
+        return Appearance(kind, sh_degree, _ptr(self.sh), _ptr(self.latent), _ptr(self.mlp_w))
+
+
+def gs_workspace_size(n: int, width: int, height: int, capacity: int, kind: int) -> int:
+    out = C.c_size_t(0)
+    _check(lib().gs_workspace_size(n, width, height, capacity, kind, C.byref(out)))
+    return out.value
+
+
+def gs_preprocess(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed, workspace, ws_bytes: int,
+                  stream=None, sync_pairs: bool = True):
+    p = C.c_uint64(0)
+    _check(lib().gs_preprocess(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre),
+                               C.byref(p) if sync_pairs else None, _ptr(workspace), ws_bytes, _stream(stream)))
+    return p.value if sync_pairs else None
+
+
+def gs_bin_sort(cam: Camera, pre: Preprocessed, n: int, num_pairs: int, capacity: int, values, tile_ids,
+                tile_ranges, workspace, ws_bytes: int, stream=None):
+    _check(lib().gs_bin_sort(C.byref(cam), C.byref(pre), n, num_pairs, capacity, _ptr(values), _ptr(tile_ids),
+                             _ptr(tile_ranges), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def gs_render_fwd(cam: Camera, pre: Preprocessed, n: int, values, tile_ranges, image, final_T, n_contrib,
+                  stream=None):
+    _check(lib().gs_render_fwd(C.byref(cam), C.byref(pre), n, _ptr(values), _ptr(tile_ranges), _ptr(image),
+                               _ptr(final_T), _ptr(n_contrib), _stream(stream)))
+
+
+def gs_render_bwd(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed, values, tile_ranges, final_T,
+                  n_contrib, dL_dimage, grads: Grads, workspace, ws_bytes: int, stream=None):
+    _check(lib().gs_render_bwd(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), _ptr(values),
+                               _ptr(tile_ranges), _ptr(final_T), _ptr(n_contrib), _ptr(dL_dimage), C.byref(grads),
+                               _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def timing_enable(on: bool = True):
+    _check(lib().gs_timing_enable(1 if on else 0))
+
+
+def timing_reset():
+    _check(lib().gs_timing_reset())
+
+
+def timing_read() -> dict:
+    k = len(KERNEL_NAMES)
+    ms = (C.c_double * k)()
+    cnt = (C.c_int64 * k)()
+    _check(lib().gs_timing_read(ms, cnt, k))
+    return {KERNEL_NAMES[i]: (ms[i], cnt[i]) for i in range(k)}
+
+
+class Frame:
+    """Device buffers for rendering one image of a scene and its backward pass."""
+
+    def __init__(self, n: int, width: int, height: int, kind: int, capacity: int, device="cuda",
+                 want_tile_ids: bool = False, want_dmean2d: bool = False):
+        self.n, self.width, self.height, self.kind, self.capacity = n, width, height, kind, capacity
+        d = device
+        nn = max(n, 1)
+        self.tiles_x, self.tiles_y = (width + 15) // 16, (height + 15) // 16
+        self.splats = torch.empty(nn * SPLAT_BYTES // 4, dtype=torch.float32, device=d)
+        self.tiles_touched = torch.empty(nn, dtype=torch.int32, device=d)
+        self.depth_key = torch.empty(nn, dtype=torch.int32, device=d)
+        self.num_pairs = torch.zeros(1, dtype=torch.int64, device=d)
+        self.values = torch.empty(max(capacity, 1), dtype=torch.int32, device=d)
+        self.tile_ids = torch.empty(max(capacity, 1), dtype=torch.int32, device=d) if want_tile_ids else None
+        self.ranges = torch.empty(self.tiles_x * self.tiles_y * 2, dtype=torch.int32, device=d)
+        self.image = torch.empty(3, height, width, dtype=torch.float32, device=d)
+        self.final_T = torch.empty(height, width, dtype=torch.float32, device=d)
+        self.n_contrib = torch.empty(height, width, dtype=torch.int32, device=d)
+        self.ws_bytes = gs_workspace_size(n, width, height, capacity, kind)
+        self.workspace = torch.empty(max(self.ws_bytes, 256) // 4 + 64, dtype=torch.float32, device=d)
+        self.dmeans = torch.empty(3, nn, device=d)
+        self.dlog_scales = torch.empty(3, nn, device=d)
+        self.dquats = torch.empty(4, nn, device=d)
+        self.dopacity_logits = torch.empty(nn, device=d)
+        self.dsh = torch.empty(48, nn, device=d) if kind == GS_APP_SH3 else None
+        self.dlatent = torch.empty(14, nn, device=d) if kind == GS_APP_LATENT_MLP else None
+        self.dmlp_w = torch.empty(MLP_WEIGHTS, device=d) if kind == GS_APP_LATENT_MLP else None
+        self.dmean2d = torch.empty(2, nn, device=d) if want_dmean2d else None
+        self.pre = Preprocessed(_ptr(self.splats), _ptr(self.tiles_touched), _ptr(self.depth_key),
+                                _ptr(self.num_pairs))
+        self.grads = Grads(_ptr(self.dmeans), _ptr(self.dlog_scales), _ptr(self.dquats),
+                           _ptr(self.dopacity_logits), _ptr(self.dsh), _ptr(self.dlatent), _ptr(self.dmlp_w),
+                           _ptr(self.dmean2d))
+        self.last_pairs = 0
+
+    def forward(self, cam: Camera, scene: SceneTensors, sh_degree: int = 3, stream=None) -> int:
+        g, app = scene.gaussians(), scene.appearance(self.kind, sh_degree)
+        P = gs_preprocess(cam, g, app, self.pre, self.workspace, self.ws_bytes, stream)
+        gs_bin_sort(cam, self.pre, self.n, P, self.capacity, self.values, self.tile_ids, self.ranges,
+                    self.workspace, self.ws_bytes, stream)
+        gs_render_fwd(cam, self.pre, self.n, self.values, self.ranges, self.image, self.final_T, self.n_contrib,
+                      stream)
+        self.last_pairs = P
+        return P
+
+    def backward(self, cam: Camera, scene: SceneTensors, dL_dimage, sh_degree: int = 3, stream=None):
+        g, app = scene.gaussians(), scene.appearance(self.kind, sh_degree)
+        gs_render_bwd(cam, g, app, self.pre, self.values, self.ranges, self.final_T, self.n_contrib, dL_dimage,
+                      self.grads, self.workspace, self.ws_bytes, stream)
+
+    def splat_fields(self) -> dict:
+        """Host copy of the splat records, split into fields."""
+        raw = self.splats.view(-1, 12).cpu()
+        f = raw.numpy()
+        rect = raw.view(torch.int32).numpy()[:, 10:12]
+        r01, r23 = rect[:, 0].astype("int64") & 0xFFFFFFFF, rect[:, 1].astype("int64") & 0xFFFFFFFF
+        import numpy as np
+        rects = np.stack([r01 & 0xFFFF, r01 >> 16, r23 & 0xFFFF, r23 >> 16]).astype(np.int32)
+        return dict(mean2d=f[:, 0:2].T.copy(), conic=f[:, 2:5].T.copy(), opacity=f[:, 5].copy(),
+                    color=f[:, 6:9].T.copy(), depth=f[:, 9].copy(), rect=rects)

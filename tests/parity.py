@@ -1,0 +1,153 @@
+"""Helpers of the GPU parity tests: run the HIP path through the C ABI and the
+oracle on the same seeded inputs, and compare them stage by stage."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import oracle as orc
+from paper_2609_05255_amd import gsraster as gs
+from paper_2609_05255_amd import inputs
+
+# A pixel whose oracle skip/stop/cap decisions all lie farther than this
+# relative distance from their thresholds takes the same decisions on the GPU:
+# the GPU's alpha differs from the oracle's by a few fp32 ulps (exp2-based exp,
+# fused multiply-adds) and its transmittance by at most ~1e-6 relative after
+# hundreds of factors.
+MARGIN = 1e-5
+IMG_ATOL, IMG_RTOL = 1e-5, 1e-4      # rendered images, fp32
+
+
+def say(msg: str):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def kind_id(kind: str) -> int:
+    return gs.GS_APP_SH3 if kind == "sh3" else gs.GS_APP_LATENT_MLP
+
+
+def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None):
+    st = gs.SceneTensors(scene)
+    cs = gs.camera_struct(cam)
+    if capacity is None:
+        capacity = 1 << 16
+    fr = gs.Frame(scene.n, cam.width, cam.height, kind_id(kind), capacity, want_tile_ids=True, want_dmean2d=True)
+    g, app = st.gaussians(), st.appearance(kind_id(kind), sh_degree)
+    P = gs.gs_preprocess(cs, g, app, fr.pre, fr.workspace, fr.ws_bytes)
+    if P > capacity:
+        # the capacity contract: report, then retry with room for every pair
+        try:
+            gs.gs_bin_sort(cs, fr.pre, scene.n, P, capacity, fr.values, fr.tile_ids, fr.ranges, fr.workspace,
+                           fr.ws_bytes)
+            raise AssertionError("bin_sort accepted too many pairs")
+        except gs.GsError as e:
+            assert e.status == gs.GS_ERR_CAPACITY
+        fr = gs.Frame(scene.n, cam.width, cam.height, kind_id(kind), int(P), want_tile_ids=True, want_dmean2d=True)
+        P = gs.gs_preprocess(cs, g, app, fr.pre, fr.workspace, fr.ws_bytes)
+    gs.gs_bin_sort(cs, fr.pre, scene.n, P, fr.capacity, fr.values, fr.tile_ids, fr.ranges, fr.workspace, fr.ws_bytes)
+    gs.gs_render_fwd(cs, fr.pre, scene.n, fr.values, fr.ranges, fr.image, fr.final_T, fr.n_contrib)
+    if dL_dimage is not None:
+        fr.backward(cs, st, torch.from_numpy(dL_dimage).cuda(), sh_degree)
+    torch.cuda.synchronize()
+    out = dict(P=int(P), frame=fr, scene_tensors=st)
+    out["tiles"] = fr.tiles_touched.cpu().numpy()[: scene.n]
+    out["depth_key"] = fr.depth_key.cpu().numpy().view(np.uint32)[: scene.n]
+    out["values"] = fr.values.cpu().numpy()[:P]
+    out["tile_ids"] = fr.tile_ids.cpu().numpy()[:P]
+    out["ranges"] = fr.ranges.cpu().numpy().reshape(-1, 2).astype(np.int64)
+    out["image"] = fr.image.cpu().numpy().astype(np.float64)
+    out["final_T"] = fr.final_T.cpu().numpy().astype(np.float64)
+    out["n_contrib"] = fr.n_contrib.cpu().numpy()
+    out["splat"] = fr.splat_fields() if scene.n > 0 else None
+    if dL_dimage is not None:
+        out["grads"] = {k: getattr(fr, k).cpu().numpy().astype(np.float64)[..., : scene.n]
+                        for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dmean2d")}
+        if kind == "sh3":
+            out["grads"]["dsh"] = fr.dsh.cpu().numpy().astype(np.float64)[:, : scene.n]
+        else:
+            out["grads"]["dlatent"] = fr.dlatent.cpu().numpy().astype(np.float64)[:, : scene.n]
+            out["grads"]["dmlp_w"] = fr.dmlp_w.cpu().numpy().astype(np.float64)
+    return out
+
+
+def compare_preprocess(gpu, ref, color_atol=2e-6):
+    """Culling, tile counts, rectangles and depth keys bit-exact; projected
+    geometry bit-exact (same correctly rounded fp32 sequence); colours close."""
+    assert np.array_equal(gpu["tiles"].astype(np.int64), ref["tiles"].astype(np.int64))
+    vis = ref["tiles"] > 0
+    ref_key = np.where(vis, ref["depth"].astype(np.float32).view(np.uint32), np.uint32(0xFFFFFFFF))
+    assert np.array_equal(gpu["depth_key"], ref_key)
+    if not vis.any():
+        return
+    s = gpu["splat"]
+    assert np.array_equal(s["rect"][:, vis], ref["rect"][:, vis])
+    for k in ("mean2d", "conic"):
+        assert np.array_equal(s[k][:, vis].astype(np.float32), ref[k][:, vis].astype(np.float32)), k
+    assert np.array_equal(s["opacity"][vis], ref["opacity"][vis].astype(np.float32))
+    assert np.abs(s["color"][:, vis] - ref["color"][:, vis]).max() <= color_atol
+
+
+def compare_lists(gpu, ref_values, ref_tiles, ref_ranges):
+    assert gpu["P"] == ref_values.size
+    assert np.array_equal(gpu["values"].astype(np.int64), ref_values.astype(np.int64))
+    assert np.array_equal(gpu["tile_ids"].astype(np.int64), ref_tiles.astype(np.int64))
+    assert np.array_equal(gpu["ranges"], ref_ranges)
+
+
+def compare_image(gpu, ref_img, ref_T, ref_nc, margin, atol=IMG_ATOL, rtol=IMG_RTOL):
+    """Image, final transmittance and last contributor on every pixel whose
+    decisions are not within MARGIN of a threshold; returns the flagged count."""
+    ok = margin > MARGIN
+    err = np.abs(gpu["image"] - ref_img)
+    bad = (err > atol + rtol * np.abs(ref_img)) & ok[None]
+    assert not bad.any(), (int(bad.sum()), float(err[:, ok].max()))
+    assert np.array_equal(gpu["n_contrib"][ok], ref_nc[ok])
+    assert np.all(np.abs(gpu["final_T"] - ref_T)[ok] <= atol + rtol * np.abs(ref_T[ok]))
+    return int((~ok).sum())
+
+
+def affected_gaussians(ref_ranges, ref_values, ref_nc, gpu_nc, margin, width):
+    """Gaussians listed up to the last contributor of a flagged pixel."""
+    flagged = np.argwhere(margin <= MARGIN)
+    tiles_x = (width + 15) // 16
+    out = set()
+    for y, x in flagged:
+        t = (y // 16) * tiles_x + x // 16
+        s, e = ref_ranges[t]
+        k = max(int(ref_nc[y, x]), int(gpu_nc[y, x])) + 1
+        out.update(ref_values[s:min(e, s + k)].tolist())
+    return np.array(sorted(out), dtype=np.int64)
+
+
+def grad_errors(gpu_g, ref_g, exclude=None):
+    """Per tensor: relative L2 error and the largest element error relative to
+    (|ref| + 1e-2 * rms(ref))."""
+    stats = {}
+    for k, r in ref_g.items():
+        if k not in gpu_g:
+            continue
+        g = gpu_g[k]
+        if exclude is not None and exclude.size and r.ndim >= 1 and r.shape[-1] == g.shape[-1] and k != "dmlp_w":
+            r = np.delete(r, exclude, axis=-1)
+            g = np.delete(g, exclude, axis=-1)
+        diff = g - r
+        rms = float(np.sqrt(np.mean(r * r))) if r.size else 0.0
+        rel_l2 = float(np.linalg.norm(diff) / max(np.linalg.norm(r), 1e-300))
+        elem = float(np.max(np.abs(diff) / (np.abs(r) + 1e-2 * rms + 1e-30))) if r.size else 0.0
+        stats[k] = (rel_l2, elem)
+    return stats
+
+
+def oracle_all(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None):
+    r = orc.render(cam, scene, kind=kind, sh_degree=sh_degree, mode="f32")
+    if dL_dimage is not None:
+        r["grads"] = orc.render_bwd(cam, scene, r["pre"], r["ranges"], r["values"], dL_dimage, kind=kind,
+                                    sh_degree=sh_degree, mode="f32")
+    return r
+
+
+def tiny_camera(width=64, height=64, bg=(0.0, 0.0, 0.0)):
+    return inputs.look_at_camera([0.0, 0.0, -3.0], width, height, bg=bg)

@@ -1,0 +1,133 @@
+"""The C ABI without a GPU: the library loads, exports every entry point that
+include/gsraster.h declares, sizes workspaces, and rejects bad arguments on the
+host before launching anything."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_05255_amd import build as gsbuild
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gsraster.h")
+
+
+@pytest.fixture(scope="module")
+def gs():
+    if not os.path.exists(gsbuild.LIB):
+        gsbuild.build()
+    from paper_2609_05255_amd import gsraster
+    return gsraster
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gs_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function(gs):
+    names = declared_functions()
+    assert {"gs_preprocess", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd"} <= set(names)
+    out = subprocess.run(["nm", "-D", "--defined-only", gs.LIB_PATH], capture_output=True, text=True, check=True)
+    exported = set(re.findall(r"\bT (gs_[a-z0-9_]+)\b", out.stdout))
+    assert set(names) <= exported, set(names) - exported
+    lib = gs.lib()
+    for name in names:
+        assert getattr(lib, name) is not None
+
+
+def test_version_and_kernel_names(gs):
+    assert b"gfx950" in gs.lib().gs_version()
+    assert [gs.lib().gs_kernel_name(i).decode() for i in range(len(gs.KERNEL_NAMES))] == gs.KERNEL_NAMES
+
+
+def test_workspace_size(gs):
+    a = gs.gs_workspace_size(1000, 64, 64, 10_000, gs.GS_APP_SH3)
+    b = gs.gs_workspace_size(1000, 64, 64, 20_000, gs.GS_APP_SH3)
+    c = gs.gs_workspace_size(1000, 64, 64, 10_000, gs.GS_APP_LATENT_MLP)
+    assert 0 < a < b and a < c
+    # four pair buffers of u32 per unit of capacity
+    assert b - a >= 4 * 4 * 10_000
+    with pytest.raises(gs.GsError) as e:
+        gs.gs_workspace_size(-1, 64, 64, 10, gs.GS_APP_SH3)
+    assert e.value.status == gs.GS_ERR_INVALID_ARG
+    with pytest.raises(gs.GsError):
+        gs.gs_workspace_size(10, 64, 64, 10, 7)
+    with pytest.raises(gs.GsError):
+        gs.gs_workspace_size(10, 64, 64, 1 << 32, gs.GS_APP_SH3)
+
+
+def _camera(gs, **kw):
+    from paper_2609_05255_amd import inputs
+    c = gs.camera_struct(inputs.look_at_camera([0, 0, -3], 64, 48))
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+FAKE = 1 << 20   # a non-NULL pointer value; never dereferenced by argument checks
+
+
+def test_preprocess_rejects_bad_arguments(gs):
+    lib = gs.lib()
+    g = gs.Gaussians(10, FAKE, FAKE, FAKE, FAKE)
+    app = gs.Appearance(gs.GS_APP_SH3, 3, FAKE, None, None)
+    pre = gs.Preprocessed(FAKE, FAKE, FAKE, FAKE)
+    ok_cam = _camera(gs)
+
+    def call(cam=ok_cam, g=g, app=app, pre=pre, ws=FAKE * 256, wsb=1 << 40):
+        return lib.gs_preprocess(C.byref(cam) if cam is not None else None, C.byref(g) if g is not None else None,
+                                 C.byref(app), C.byref(pre), None, C.c_void_p(ws), wsb, None)
+
+    assert call(cam=None) == gs.GS_ERR_INVALID_ARG
+    assert b"camera" in lib.gs_last_error()
+    assert call(cam=_camera(gs, width=0)) == gs.GS_ERR_INVALID_ARG
+    assert call(cam=_camera(gs, fx=0.0)) == gs.GS_ERR_INVALID_ARG
+    assert call(cam=_camera(gs, width=1 << 20)) == gs.GS_ERR_INVALID_ARG
+    assert call(g=gs.Gaussians(-1, FAKE, FAKE, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
+    assert call(g=gs.Gaussians(1 << 31, FAKE, FAKE, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
+    assert call(g=gs.Gaussians(10, None, FAKE, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
+    assert call(app=gs.Appearance(gs.GS_APP_SH3, 4, FAKE, None, None)) == gs.GS_ERR_INVALID_ARG
+    assert b"sh_degree" in lib.gs_last_error()
+    assert call(app=gs.Appearance(gs.GS_APP_SH3, 3, None, None, None)) == gs.GS_ERR_INVALID_ARG
+    assert call(app=gs.Appearance(gs.GS_APP_LATENT_MLP, 0, None, FAKE, None)) == gs.GS_ERR_INVALID_ARG
+    assert call(app=gs.Appearance(9, 0, FAKE, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
+    assert call(pre=gs.Preprocessed(FAKE, FAKE, FAKE, None)) == gs.GS_ERR_INVALID_ARG
+    assert call(ws=FAKE + 4) == gs.GS_ERR_INVALID_ARG              # misaligned workspace
+    assert call(wsb=16) == gs.GS_ERR_CAPACITY
+    assert b"workspace" in lib.gs_last_error()
+
+
+def test_bin_sort_reports_capacity(gs):
+    lib = gs.lib()
+    cam = _camera(gs)
+    pre = gs.Preprocessed(FAKE, FAKE, FAKE, FAKE)
+    st = lib.gs_bin_sort(C.byref(cam), C.byref(pre), 10, 5000, 4000, C.c_void_p(FAKE), None, C.c_void_p(FAKE),
+                         C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_CAPACITY
+    assert b"5000" in lib.gs_last_error() and b"4000" in lib.gs_last_error()
+    st = lib.gs_bin_sort(C.byref(cam), C.byref(pre), 10, 10, 1 << 32, C.c_void_p(FAKE), None, C.c_void_p(FAKE),
+                         C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARG
+    st = lib.gs_bin_sort(C.byref(cam), C.byref(pre), 10, 10, 100, C.c_void_p(FAKE), None, None,
+                         C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARG
+
+
+def test_render_calls_reject_bad_arguments(gs):
+    lib = gs.lib()
+    cam = _camera(gs)
+    pre = gs.Preprocessed(FAKE, FAKE, FAKE, FAKE)
+    st = lib.gs_render_fwd(C.byref(cam), C.byref(pre), 10, C.c_void_p(FAKE), C.c_void_p(FAKE), None,
+                           C.c_void_p(FAKE), C.c_void_p(FAKE), None)
+    assert st == gs.GS_ERR_INVALID_ARG
+    g = gs.Gaussians(10, FAKE, FAKE, FAKE, FAKE)
+    app = gs.Appearance(gs.GS_APP_SH3, 3, FAKE, None, None)
+    grads = gs.Grads(FAKE, FAKE, FAKE, FAKE, None, None, None, None)
+    st = lib.gs_render_bwd(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), C.c_void_p(FAKE), C.c_void_p(FAKE),
+                           C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE), C.byref(grads),
+                           C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARG and b"dsh" in lib.gs_last_error()

@@ -1,0 +1,239 @@
+"""Benchmark of the rasterizer's forward + backward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config paper_sh3|paper_latent|stress|medium|tiny]
+                    [--no-cpu-baseline]
+
+One step = one full pass of the hot path for one camera of the scene:
+gs_preprocess (with the read-back of the pair count), gs_bin_sort, gs_render_fwd
+and gs_render_bwd, cycling over the configuration's cameras. Scene parameters
+and upstream gradients are resident on the GPU before timing starts. Prints one
+JSON line: fwd+bwd iterations/s (and Mpix/s), per-kernel times measured with HIP
+events on the rendering stream, the roofline of the dominant kernel, and the
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "fwd+bwd iterations/sec and rendered Mpix/s at 3M Gaussians, 1600x1064"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_VECTOR_PEAK_TFLOPS = 157.3
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--config", default="paper_sh3")
+    ap.add_argument("--appearance", default=None, help="sh3 or latent (default: the config's first)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tiles", type=int, default=96, help="tiles in the CPU-baseline sample")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int = 3) -> float | None:
+    """HBM bytes a launch must move at minimum (per launch, averaged over cameras)."""
+    app = 4 * 3 * (sh_degree + 1) ** 2 if kind == "sh3" else 28
+    if kernel == "preprocess":
+        # params 44 B + tiles 4 B + depth key 4 B per Gaussian; appearance + 48 B splat per visible one
+        return n * (44 + 8) + vis * (app + 48)
+    if kernel == "preprocess_bwd":
+        # tiles 4 B + dense gradient writes per Gaussian; params, accumulators and appearance per visible one
+        grad = 44 + (4 * 48 if kind == "sh3" else 4 * 14)
+        return n * (4 + grad) + vis * (44 + 36 + app)
+    return None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the rasterizer runs on a single MI355X "
+              "(the multi-GPU data-parallel design is described, not built); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2609_05255_amd import gsraster as gs
+    from paper_2609_05255_amd import inputs
+
+    cfg = inputs.CONFIGS[args.config]
+    kind = args.appearance or cfg.appearance[0]
+    kid = gs.GS_APP_SH3 if kind == "sh3" else gs.GS_APP_LATENT_MLP
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    t0 = time.time()
+    scene = inputs.make_scene(cfg, appearance=(kind,))
+    cams = inputs.make_cameras(cfg)
+    st = gs.SceneTensors(scene, device=dev)
+    grads_up = [torch.from_numpy(inputs.make_upstream_grad(cfg.width, cfg.height, i)).to(dev)
+                for i in range(len(cams))]
+    cstructs = [gs.camera_struct(c) for c in cams]
+    print("# scene %s (%s) generated and uploaded in %.1fs" % (cfg.name, kind, time.time() - t0), file=sys.stderr,
+          flush=True)
+
+    # size the pair buffers: preprocess every camera once (untimed)
+    probe = gs.Frame(scene.n, cfg.width, cfg.height, kid, 1, device=dev)
+    g, app = st.gaussians(), st.appearance(kid)
+    pairs, visible = [], []
+    for c in cstructs:
+        pairs.append(gs.gs_preprocess(c, g, app, probe.pre, probe.workspace, probe.ws_bytes))
+        visible.append(int((probe.tiles_touched[: scene.n] > 0).sum().item()))
+    del probe
+    capacity = int(max(pairs) * 1.02) + 4096
+    fr = gs.Frame(scene.n, cfg.width, cfg.height, kid, capacity, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(i):
+        c = cstructs[i % len(cstructs)]
+        fr.forward(c, st, stream=stream)
+        fr.backward(c, st, grads_up[i % len(cstructs)], stream=stream)
+
+    print("# capacity %d pairs; warmup" % capacity, file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    # timed region
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    it_s = args.steps / elapsed
+
+    # blended pairs per image (sum of n_contrib), for the blend's work figure
+    contrib = []
+    for i in range(len(cstructs)):
+        fr.forward(cstructs[i], st, stream=stream)
+        contrib.append(float(fr.n_contrib.double().sum().item()))
+    # per-kernel durations: the same K steps again with HIP events around every kernel
+    gs.timing_enable(True)
+    gs.timing_reset()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    kt = gs.timing_read()
+    gs.timing_enable(False)
+    stage_ms = {k: (ms / cnt if cnt else 0.0) for k, (ms, cnt) in kt.items() if cnt}
+
+    # roofline of the dominant kernel
+    ncam = len(cstructs)
+    steps_cams = [i % ncam for i in range(args.steps)]
+    vis_avg = float(np.mean([visible[i] for i in steps_cams]))
+    pairs_avg = float(np.mean([pairs[i] for i in steps_cams]))
+    dominant = max(stage_ms, key=lambda k: stage_ms[k] * kt[k][1])
+    roofline = None
+    hbm_kernels = {k: algorithmic_bytes(k, scene.n, vis_avg, kind) for k in ("preprocess", "preprocess_bwd")}
+    if dominant in hbm_kernels:
+        b = hbm_kernels[dominant]
+        ach = b / (stage_ms[dominant] * 1e-3) / 1e9
+        roofline = {"kernel": dominant, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+    else:
+        # blend kernels: fp32 vector work per blended (pixel, splat) pair
+        flops_per_pair = {"blend_fwd": 22.0, "blend_bwd": 80.0}.get(dominant, None)
+        if flops_per_pair is not None:
+            e = float(np.mean([contrib[i] for i in steps_cams]))
+            ach = e * flops_per_pair / (stage_ms[dominant] * 1e-3) / 1e12
+            roofline = {"kernel": dominant, "bound": "alu", "achieved": round(ach, 3),
+                        "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(ach / FP32_VECTOR_PEAK_TFLOPS, 4), "traffic": None}
+    hbm_all = {}
+    for k, b in hbm_kernels.items():
+        if k in stage_ms and stage_ms[k] > 0:
+            ach = b / (stage_ms[k] * 1e-3) / 1e9
+            hbm_all[k] = {"algorithmic_MB": round(b / 1e6, 1), "ms": round(stage_ms[k], 4),
+                          "GB_s": round(ach, 1), "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(scene, cams, kind, args.cpu_tiles)
+
+    mpix = cfg.width * cfg.height * it_s / 1e6
+    out = {
+        "metric": METRIC,
+        "value": round(it_s, 3),
+        "unit": "it/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * elapsed / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if kind == "sh3" else "f32+f16",
+        "data": "synthetic",
+        "config": {"workload": "%s: %d Gaussians, %dx%d, %s appearance, %d cameras" % (
+            cfg.name, scene.n, cfg.width, cfg.height, kind, ncam),
+            "gaussians": scene.n, "width": cfg.width, "height": cfg.height, "appearance": kind,
+            "cameras": ncam},
+        "mpix_per_s": round(mpix, 2),
+        "visible_avg": int(vis_avg),
+        "pairs_avg": int(pairs_avg),
+        "blended_pairs_avg": int(np.mean(contrib)),
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "hbm_stages": hbm_all,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(scene, cams, kind, n_tiles_sample):
+    """The oracle on the host: full preprocess of every Gaussian, then binning,
+    forward and backward blending restricted to a random sample of tiles, the
+    per-tile part scaled to the whole image. One camera, single thread."""
+    from oracle import oracle as orc
+
+    cam = cams[0]
+    tx, ty = orc.tile_grid(cam)
+    T = tx * ty
+    rng = np.random.default_rng(0)
+    sample = np.sort(rng.choice(T, size=min(n_tiles_sample, T), replace=False))
+    print("# cpu baseline: oracle preprocess of %d Gaussians" % scene.n, file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    pre = orc.preprocess(cam, scene, kind=kind)
+    t_pre = time.perf_counter() - t0
+    print("# cpu baseline: preprocess %.1fs; sampled tiles next" % t_pre, file=sys.stderr, flush=True)
+    # keep only Gaussians whose rectangle meets a sampled tile
+    sx, sy = sample % tx, sample // tx
+    r = pre["rect"]
+    keep = np.zeros(scene.n, bool)
+    vis = np.nonzero(pre["tiles"] > 0)[0]
+    for lo in range(0, vis.size, 1 << 20):
+        idx = vis[lo:lo + (1 << 20)]
+        hit = ((r[0, idx, None] <= sx[None]) & (sx[None] < r[2, idx, None]) &
+               (r[1, idx, None] <= sy[None]) & (sy[None] < r[3, idx, None])).any(axis=1)
+        keep[idx[hit]] = True
+    sub = orc.Preprocessed({k: v.copy() for k, v in pre.items()})
+    sub["tiles"][~keep] = 0
+    sub["flags"][~keep] = 0
+    t1 = time.perf_counter()
+    values, _, ranges = orc.bin_sort(cam, sub)
+    mask = np.zeros(T, bool)
+    mask[sample] = True
+    ranges[~mask] = 0
+    img, fT, nc, _ = orc.render_fwd(cam, sub, ranges, values)
+    from paper_2609_05255_amd import inputs
+    g = inputs.make_upstream_grad(cam.width, cam.height, 0)
+    orc.render_bwd(cam, scene, sub, ranges, values, g, kind=kind)
+    t_tiles = time.perf_counter() - t1
+    scale = T / sample.size
+    t_iter = t_pre + t_tiles * scale
+    return {"value": round(1.0 / t_iter, 6), "unit": "it/s", "cores": 1, "kind": "oracle",
+            "sample": "camera 0: preprocess of all %d Gaussians (%.1fs) + binning, forward and backward "
+                      "blending of %d random tiles of %d (%.1fs), tile part scaled x%.1f" % (
+                          scene.n, t_pre, sample.size, T, t_tiles, scale),
+            "s_per_iter": round(t_iter, 2)}
+
+
+if __name__ == "__main__":
+    main()

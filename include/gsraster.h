@@ -193,6 +193,15 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
                         const float* final_T, const uint32_t* n_contrib, const float* dL_dimage,
                         const gs_grads* grads, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * gs_mlp_eval -- the latent decoder on its own (Sec. 4 neural appearance):
+ * colours of `rows` decoder inputs, computed exactly as inside gs_preprocess.
+ * x: [rows][17] binary16 device array, each row the 14 latent values followed
+ * by the unit view direction; mlp_w as in gs_appearance; colors: [rows][3]
+ * fp32 device array. rows must be in [0, 2^31).
+ */
+gs_status gs_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* mlp_w, float* colors, void* stream);
+
 /* Workspace bytes needed by any call for these sizes (host only). */
 gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t capacity, int32_t kind,
                             size_t* bytes);

@@ -153,3 +153,14 @@ int64_t orc_bin_sort(int64_t n, const int32_t* rect, const double* depth, const 
 #include "gs_oracle_body.inc"
 #undef REAL
 #undef SFX
+
+/* The latent decoder alone on caller-given inputs (fp64 on binary16 values):
+ * x [rows][17], out [rows][3]. */
+void orc_mlp_eval(const double* x, int64_t rows, const double* w, double* out, int32_t half_act)
+{
+    for (int64_t r = 0; r < rows; ++r) {
+        double h1[32], h2[32], o[3];
+        mlp_forward_f64(w, x + 17 * r, h1, h2, o, half_act);
+        for (int c = 0; c < 3; ++c) out[3 * r + c] = 1.0 / (1.0 + exp(-o[c]));
+    }
+}

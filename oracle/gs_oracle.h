@@ -67,6 +67,9 @@ typedef struct orc_appearance {
     const double* mlp_w;    /* 1664 values of binary16 numbers: W1[32][17], W2[32][32], W3[3][32] */
     int32_t dir_exact;      /* 0: the decoder sees the view direction rounded to binary16 (as the
                                half-precision decoder does); 1: unrounded, for finite differences */
+    int32_t half_act;       /* 1: the hidden activations are rounded to binary16 before they enter
+                               the next layer (half-precision operands, Sec. 4 / fused appendix);
+                               0: exact fp64 activations */
 } orc_appearance;
 
 /* Outputs of the preprocess. Entries of culled Gaussians are zero. */
@@ -133,6 +136,8 @@ int orc_render_bwd_f64(const orc_camera* cam, int64_t n, const double* means, co
 /* Real spherical harmonics of degree <= 3 (16 values) and their gradient
  * w.r.t. the direction components (16x3), built from the Legendre definition. */
 void orc_sh_basis(const double d[3], double Y[16], double dY[48]);
+/* The latent decoder on given inputs: x [rows][17] (binary16 values), out [rows][3]. */
+void orc_mlp_eval(const double* x, int64_t rows, const double* w, double* out, int32_t half_act);
 /* Round to the nearest binary16 value (ties to even), returned as a double. */
 double orc_round_half(double x);
 

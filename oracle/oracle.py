@@ -52,7 +52,8 @@ class _Camera(C.Structure):
 
 class _Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p),
-                ("latent", C.c_void_p), ("mlp_w", C.c_void_p), ("dir_exact", C.c_int32)]
+                ("latent", C.c_void_p), ("mlp_w", C.c_void_p), ("dir_exact", C.c_int32),
+                ("half_act", C.c_int32)]
 
 
 class _Pre(C.Structure):
@@ -90,6 +91,8 @@ def lib():
         _lib.orc_bin_sort.restype = i64
         _lib.orc_sh_basis.argtypes = [vp, vp, vp]
         _lib.orc_sh_basis.restype = None
+        _lib.orc_mlp_eval.argtypes = [vp, i64, vp, vp, C.c_int32]
+        _lib.orc_mlp_eval.restype = None
         _lib.orc_round_half.argtypes = [C.c_double]
         _lib.orc_round_half.restype = C.c_double
     return _lib
@@ -128,7 +131,7 @@ def half_to_f64(a: np.ndarray) -> np.ndarray:
 class _SceneArrays:
     """float64 copies of a scene's arrays, kept alive while C reads them."""
 
-    def __init__(self, scene, kind: int, sh_degree: int, dir_exact: bool = False):
+    def __init__(self, scene, kind: int, sh_degree: int, dir_exact: bool = False, half_act: bool = False):
         self.n = int(scene.n)
         self.means = _f64(scene.means)
         self.log_scales = _f64(scene.log_scales)
@@ -137,7 +140,8 @@ class _SceneArrays:
         self.sh = _f64(scene.sh) if kind == APP_SH3 else None
         self.latent = half_to_f64(scene.latent) if kind == APP_LATENT_MLP else None
         self.mlp_w = half_to_f64(scene.mlp_w) if kind == APP_LATENT_MLP else None
-        self.app = _Appearance(kind, sh_degree, _p(self.sh), _p(self.latent), _p(self.mlp_w), int(dir_exact))
+        self.app = _Appearance(kind, sh_degree, _p(self.sh), _p(self.latent), _p(self.mlp_w), int(dir_exact),
+                               int(half_act))
 
 
 def _kind_of(kind) -> int:
@@ -157,9 +161,9 @@ class Preprocessed(dict):
 
 
 def preprocess(cam, scene, kind="sh3", sh_degree: int = 3, mode: str = "f32",
-               dir_exact: bool = False) -> Preprocessed:
+               dir_exact: bool = False, half_act: bool = False) -> Preprocessed:
     kind = _kind_of(kind)
-    sa = _SceneArrays(scene, kind, sh_degree, dir_exact)
+    sa = _SceneArrays(scene, kind, sh_degree, dir_exact, half_act)
     n = sa.n
     out = Preprocessed(
         mean2d=np.zeros((2, n)), conic=np.zeros((3, n)), opacity=np.zeros(n), color=np.zeros((3, n)),
@@ -209,9 +213,9 @@ def render_fwd(cam, pre: Preprocessed, ranges, values, mode: str = "f32"):
 
 
 def render_bwd(cam, scene, pre: Preprocessed, ranges, values, dL_dimage, kind="sh3", sh_degree: int = 3,
-               mode: str = "f32", dir_exact: bool = False) -> dict:
+               mode: str = "f32", dir_exact: bool = False, half_act: bool = False) -> dict:
     kind = _kind_of(kind)
-    sa = _SceneArrays(scene, kind, sh_degree, dir_exact)
+    sa = _SceneArrays(scene, kind, sh_degree, dir_exact, half_act)
     n = sa.n
     g = dict(dmeans=np.zeros((3, n)), dlog_scales=np.zeros((3, n)), dquats=np.zeros((4, n)),
              dopacity_logits=np.zeros(n),
@@ -234,9 +238,10 @@ def render_bwd(cam, scene, pre: Preprocessed, ranges, values, dL_dimage, kind="s
     return {k: v for k, v in g.items() if v is not None}
 
 
-def render(cam, scene, kind="sh3", sh_degree: int = 3, mode: str = "f32", dir_exact: bool = False) -> dict:
+def render(cam, scene, kind="sh3", sh_degree: int = 3, mode: str = "f32", dir_exact: bool = False,
+           half_act: bool = False) -> dict:
     """All forward stages; returns a dict with the intermediate results."""
-    pre = preprocess(cam, scene, kind, sh_degree, mode, dir_exact)
+    pre = preprocess(cam, scene, kind, sh_degree, mode, dir_exact, half_act)
     values, tile_of, ranges = bin_sort(cam, pre)
     image, final_T, n_contrib, margin = render_fwd(cam, pre, ranges, values, mode)
     return dict(pre=pre, values=values, tile_of=tile_of, ranges=ranges, image=image, final_T=final_T,
@@ -249,6 +254,15 @@ def sh_basis(d) -> tuple:
     dY = np.zeros(48)
     lib().orc_sh_basis(_p(d), _p(Y), _p(dY))
     return Y, dY.reshape(16, 3)
+
+
+def mlp_eval(x, mlp_w, half_act: bool = False) -> np.ndarray:
+    """Decoder colours [rows][3] of inputs x [rows][17] (binary16 bits or values)."""
+    xx = half_to_f64(x).reshape(-1, 17)
+    w = half_to_f64(mlp_w)
+    out = np.zeros((xx.shape[0], 3))
+    lib().orc_mlp_eval(_p(np.ascontiguousarray(xx)), xx.shape[0], _p(w), _p(out), int(half_act))
+    return out
 
 
 def round_half(x: float) -> float:

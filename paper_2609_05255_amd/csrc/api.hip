@@ -365,6 +365,15 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
     return ok();
 }
 
+gs_status gs_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* mlp_w, float* colors, void* stream)
+{
+    GS_CHECK(rows >= 0 && rows < ((int64_t)1 << 31), "rows = %lld out of range", (long long)rows);
+    GS_CHECK(rows == 0 || (x && mlp_w && colors), "an array is NULL");
+    if (rows == 0) return ok();
+    GS_HIP(launch_mlp_eval(x, rows, mlp_w, colors, static_cast<hipStream_t>(stream)));
+    return ok();
+}
+
 gs_status gs_timing_enable(int32_t enable)
 {
     std::lock_guard<std::mutex> lk(g_tmu);

@@ -57,7 +57,7 @@ constexpr int kRadix = 256;
 // weight gradient each.
 constexpr int kMlpPartials = 1024;
 
-inline int64_t div_up(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t div_up(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t align_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
 
 // ---- workspace layout -------------------------------------------------------
@@ -110,6 +110,7 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
                                  const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr,
                                  hipStream_t s);
 hipError_t launch_mlp_reduce(int64_t n, const Workspace& ws, float* dmlp_w, hipStream_t s);
+hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s);
 
 // Kernel timing hooks (api.hip): bracket one logical kernel id.
 void timing_begin(int kernel_id, hipStream_t s);

@@ -7,6 +7,7 @@
 // rectangle and the depth key are integers decided by this fp32 arithmetic,
 // and they must not depend on which multiply-adds the compiler fuses.
 #include "gs_internal.h"
+#include "mlp.h"
 #include "sh.h"
 
 #pragma clang fp contract(off)
@@ -217,6 +218,47 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
     if (threadIdx.x == 0) a.block_pairs[blockIdx.x] = total;
 }
 
+// Latent + MLP: geometry per thread, then each wave decodes the colours of its
+// visible Gaussians on the matrix cores, 16 at a time (mlp.h); tiles of 16
+// lanes without a visible Gaussian are skipped, culled lanes load nothing.
+__global__ __launch_bounds__(kBlock) void k_preprocess_latent(PreArgs a)
+{
+    __shared__ uint32_t red[4];
+    __shared__ MlpWeights W;
+    __shared__ MlpInputs X[kBlock / kWave];
+    mlp_load_weights(a.mlp_w, W);
+    const int i = blockIdx.x * kBlock + threadIdx.x;
+    const int wave = threadIdx.x >> 6;
+    uint32_t tiles = 0;
+    Geo g;
+    g.visible = false;
+    float d[3] = {0.f, 0.f, 0.f};
+    if (i < a.n) {
+        float mu[3], ls[3], q[4], logit;
+        load_geometry_params(a, i, mu, ls, q, logit);
+        geometry(a.cam, mu, ls, q, logit, g);
+        if (g.visible) {
+            tiles = g.tiles;
+            view_dir(a.cam, mu, d);
+        }
+        a.tiles_touched[i] = tiles;
+        a.depth_key[i] = g.visible ? __float_as_uint(g.depth) : 0xFFFFFFFFu;
+    }
+    mlp_stage_lane(X[wave], g.visible, a.latent, a.n, i, d);
+    wave_lds_sync();
+    const uint64_t vis = __ballot(g.visible);
+    float col[3] = {0.f, 0.f, 0.f};
+    for (int t = 0; t < kWave / 16; ++t) {
+        if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
+        float4_t h1[2], h2[2], o;
+        mlp_tile_forward(W, X[wave], t, h1, h2, o);
+        mlp_tile_colors(o, t, col);
+    }
+    if (g.visible) store_splat(a.splats + i, g, col);
+    const uint32_t total = block_sum_u32(tiles, red);
+    if (threadIdx.x == 0) a.block_pairs[blockIdx.x] = total;
+}
+
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                              const gs_preprocessed& out, const Workspace& ws, hipStream_t s)
 {
@@ -236,8 +278,10 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     a.depth_key = out.depth_key;
     a.block_pairs = ws.block_pairs;
     const int blocks = preprocess_blocks(g.n);
-    if (app.kind != GS_APP_SH3) return hipErrorNotSupported;
-    hipLaunchKernelGGL(k_preprocess_sh3, dim3(blocks), dim3(kBlock), 0, s, a);
+    if (app.kind == GS_APP_SH3)
+        hipLaunchKernelGGL(k_preprocess_sh3, dim3(blocks), dim3(kBlock), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_preprocess_latent, dim3(blocks), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 
@@ -261,6 +305,41 @@ __global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs
 hipError_t launch_pair_count(int64_t n, const Workspace& ws, uint64_t* num_pairs, hipStream_t s)
 {
     hipLaunchKernelGGL(k_pair_count, dim3(1), dim3(1024), 0, s, ws.block_pairs, preprocess_blocks(n), num_pairs);
+    return hipGetLastError();
+}
+
+// Decoder on caller-given inputs: x is [rows][17] binary16 (latent, then the
+// view direction), out is [rows][3] fp32 colours.
+__global__ __launch_bounds__(kBlock) void k_mlp_eval(const uint16_t* __restrict__ x, int64_t rows,
+                                                     const uint16_t* __restrict__ w, float* __restrict__ out)
+{
+    __shared__ MlpWeights W;
+    __shared__ MlpInputs X[kBlock / kWave];
+    mlp_load_weights(w, W);
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int wave = threadIdx.x >> 6, lane = __lane_id();
+    const bool valid = i < rows;
+    for (int c = 0; c < 32; ++c) {
+        _Float16 v = (_Float16)0.f;
+        if (valid && c < GS_MLP_IN) v = __builtin_bit_cast(_Float16, x[i * GS_MLP_IN + c]);
+        X[wave].x[lane][c] = v;
+    }
+    wave_lds_sync();
+    float col[3] = {0.f, 0.f, 0.f};
+    const uint64_t vis = __ballot(valid);
+    for (int t = 0; t < kWave / 16; ++t) {
+        if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
+        float4_t h1[2], h2[2], o;
+        mlp_tile_forward(W, X[wave], t, h1, h2, o);
+        mlp_tile_colors(o, t, col);
+    }
+    if (valid)
+        for (int c = 0; c < 3; ++c) out[i * 3 + c] = col[c];
+}
+
+hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_mlp_eval, dim3((unsigned)div_up(rows, kBlock)), dim3(kBlock), 0, s, x, rows, w, out);
     return hipGetLastError();
 }
 

@@ -77,10 +77,11 @@ def lib() -> C.CDLL:
         L.gs_render_bwd.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), vp, vp, vp, vp, vp,
                                     P(Grads), vp, sz, vp]
         L.gs_workspace_size.argtypes = [i64, i32, i32, u64, i32, P(sz)]
+        L.gs_mlp_eval.argtypes = [vp, i64, vp, vp, vp]
         L.gs_timing_enable.argtypes = [i32]
         L.gs_timing_reset.argtypes = []
         L.gs_timing_read.argtypes = [P(C.c_double), P(i64), i32]
-        for f in ("gs_preprocess", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd", "gs_workspace_size",
+        for f in ("gs_preprocess", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd", "gs_workspace_size", "gs_mlp_eval",
                   "gs_timing_enable", "gs_timing_reset", "gs_timing_read"):
             getattr(L, f).restype = C.c_int
         L.gs_last_error.restype = C.c_char_p
@@ -180,6 +181,10 @@ def gs_render_bwd(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed,
     _check(lib().gs_render_bwd(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), _ptr(values),
                                _ptr(tile_ranges), _ptr(final_T), _ptr(n_contrib), _ptr(dL_dimage), C.byref(grads),
                                _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def gs_mlp_eval(x, rows: int, mlp_w, colors, stream=None):
+    _check(lib().gs_mlp_eval(_ptr(x), rows, _ptr(mlp_w), _ptr(colors), _stream(stream)))
 
 
 def timing_enable(on: bool = True):

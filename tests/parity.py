@@ -97,6 +97,12 @@ def compare_lists(gpu, ref_values, ref_tiles, ref_ranges):
     assert np.array_equal(gpu["ranges"], ref_ranges)
 
 
+MLP_ATOL = 2e-3                      # decoder colours/images vs the exact (fp64) decoder
+# vs the oracle whose decoder rounds inputs and activations to binary16 like the
+# GPU's matrix-core operands: only fp32 accumulation order and the sigmoid differ
+MLP_HALF_ATOL = 2e-4
+
+
 def compare_image(gpu, ref_img, ref_T, ref_nc, margin, atol=IMG_ATOL, rtol=IMG_RTOL):
     """Image, final transmittance and last contributor on every pixel whose
     decisions are not within MARGIN of a threshold; returns the flagged count."""
@@ -105,7 +111,7 @@ def compare_image(gpu, ref_img, ref_T, ref_nc, margin, atol=IMG_ATOL, rtol=IMG_R
     bad = (err > atol + rtol * np.abs(ref_img)) & ok[None]
     assert not bad.any(), (int(bad.sum()), float(err[:, ok].max()))
     assert np.array_equal(gpu["n_contrib"][ok], ref_nc[ok])
-    assert np.all(np.abs(gpu["final_T"] - ref_T)[ok] <= atol + rtol * np.abs(ref_T[ok]))
+    assert np.all(np.abs(gpu["final_T"] - ref_T)[ok] <= IMG_ATOL + IMG_RTOL * np.abs(ref_T[ok]))
     return int((~ok).sum())
 
 
@@ -141,11 +147,11 @@ def grad_errors(gpu_g, ref_g, exclude=None):
     return stats
 
 
-def oracle_all(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None):
-    r = orc.render(cam, scene, kind=kind, sh_degree=sh_degree, mode="f32")
+def oracle_all(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, half_act=False):
+    r = orc.render(cam, scene, kind=kind, sh_degree=sh_degree, mode="f32", half_act=half_act)
     if dL_dimage is not None:
         r["grads"] = orc.render_bwd(cam, scene, r["pre"], r["ranges"], r["values"], dL_dimage, kind=kind,
-                                    sh_degree=sh_degree, mode="f32")
+                                    sh_degree=sh_degree, mode="f32", half_act=half_act)
     return r
 
 

@@ -12,8 +12,12 @@ import pytest
 
 from paper_2609_05255_amd import inputs
 
-from parity import (affected_gaussians, compare_image, compare_lists, compare_preprocess, grad_errors, oracle_all,
-                    run_gpu, say, tiny_camera)
+import torch
+
+from oracle import oracle as orc
+from paper_2609_05255_amd import gsraster as gs
+from parity import (MLP_ATOL, MLP_HALF_ATOL, affected_gaussians, compare_image, compare_lists, compare_preprocess,
+                    grad_errors, oracle_all, run_gpu, say, tiny_camera)
 
 pytestmark = pytest.mark.gpu
 
@@ -24,10 +28,20 @@ def check_all(scene, cam, kind="sh3", sh_degree=3, label="", grads=True, capacit
     g = inputs.make_upstream_grad(cam.width, cam.height, 0) if grads else None
     say("case %s: n=%d %dx%d %s degree %d" % (label, scene.n, cam.width, cam.height, kind, sh_degree))
     gpu = run_gpu(scene, cam, kind, sh_degree, g, capacity=capacity)
-    ref = oracle_all(scene, cam, kind, sh_degree, g)
-    compare_preprocess(gpu, ref["pre"])
+    latent = kind == "latent"
+    # the decoder's operands are binary16: compare with the oracle that rounds them alike
+    ref = oracle_all(scene, cam, kind, sh_degree, g, half_act=latent)
+    compare_preprocess(gpu, ref["pre"], color_atol=MLP_HALF_ATOL if latent else 2e-6)
     compare_lists(gpu, ref["values"], ref["tile_of"], ref["ranges"])
-    flagged = compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"])
+    if latent:
+        flagged = compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"],
+                                atol=MLP_HALF_ATOL, rtol=0.0)
+        exact = orc.render(cam, scene, kind=kind, mode="f32")
+        err = np.abs(gpu["image"] - exact["image"])[:, exact["margin"] > 1e-5]
+        say("  latent image vs the exact decoder: max abs %.2e" % (err.max() if err.size else 0.0))
+        assert err.size == 0 or err.max() <= MLP_ATOL
+    else:
+        flagged = compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"])
     say("  P=%d flagged pixels=%d" % (gpu["P"], flagged))
     if grads:
         excl = affected_gaussians(ref["ranges"], ref["values"], ref["n_contrib"], gpu["n_contrib"], ref["margin"],
@@ -87,3 +101,41 @@ def test_medium_scene_two_cameras():
     cams = inputs.make_cameras("medium")
     for i in (0, 5):
         check_all(sc, cams[i], label="medium cam %d" % i)
+
+
+def test_mlp_eval_matches_oracle():
+    rng = np.random.default_rng(31)
+    rows = 1000                                 # 15 full waves and a ragged one
+    x = rng.normal(0.0, 0.5, size=(rows, 17))
+    x[:, 14:] /= np.linalg.norm(x[:, 14:], axis=1, keepdims=True)
+    x[7] = 0.0                                  # all-zero input: every hidden unit at 0
+    xb = x.astype(np.float16).view(np.uint16)
+    w = inputs.make_mlp_weights(5)
+    say("case mlp_eval rows=%d" % rows)
+    xt = torch.from_numpy(xb.view(np.int16)).cuda()
+    wt = torch.from_numpy(w.view(np.int16)).cuda()
+    out = torch.empty(rows, 3, device="cuda")
+    gs.gs_mlp_eval(xt, rows, wt, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    err = np.abs(got - orc.mlp_eval(xb, w))
+    err_half = np.abs(got - orc.mlp_eval(xb, w, half_act=True))
+    say("  max abs error %.2e (exact decoder), %.2e (binary16 activations)" % (err.max(), err_half.max()))
+    assert err.max() <= MLP_ATOL
+    assert err_half.max() <= MLP_HALF_ATOL
+    assert np.all(got[7] == 0.5)
+
+
+def test_tiny_scene_latent():
+    sc = inputs.make_scene("tiny", appearance=("latent",))
+    check_all(sc, inputs.make_cameras("tiny")[0], kind="latent", label="tiny latent")
+
+
+def test_ragged_latent_with_background():
+    sc = inputs.make_scene("tiny", appearance=("latent",))
+    check_all(sc, tiny_camera(50, 37, bg=(0.25, 0.5, 0.75)), kind="latent", label="ragged latent")
+
+
+def test_medium_scene_latent():
+    sc = inputs.make_scene("medium", appearance=("latent",))
+    check_all(sc, inputs.make_cameras("medium")[2], kind="latent", label="medium latent cam 2")

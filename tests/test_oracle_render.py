@@ -401,3 +401,16 @@ def test_mlp_closed_forms(orc):
     assert np.allclose(pre["color"][0, vis], sig(np.maximum(0, z0))[vis], atol=1e-15)
     assert np.allclose(pre["color"][1, vis], sig(np.maximum(0, dh[0]))[vis], atol=1e-15)
     assert np.allclose(pre["color"][2, vis], sig(-np.maximum(0, dh[2]))[vis], atol=1e-15)
+    # binary16 activations change nothing when every activation is a binary16 value already
+    pre_h = orc.preprocess(cam, sc, kind="latent", mode="f64", half_act=True)
+    assert np.array_equal(pre_h["color"], pre["color"])
+
+
+def test_mlp_half_activations_stay_close(orc):
+    rng = np.random.default_rng(22)
+    x = rng.normal(0, 0.5, size=(400, 17)).astype(np.float16).view(np.uint16)
+    w = inputs.make_mlp_weights(1)
+    exact = orc.mlp_eval(x, w)
+    half = orc.mlp_eval(x, w, half_act=True)
+    d = np.abs(exact - half)
+    assert 0 < d.max() < 2e-3

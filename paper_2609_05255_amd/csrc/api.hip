@@ -188,7 +188,7 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.vals_b = (uint32_t*)take(sizeof(uint32_t) * nn);
     w.hist = (uint32_t*)take(sizeof(uint32_t) * kRadix * sort_blocks);
     w.digit_tot = (uint32_t*)take(sizeof(uint32_t) * kRadix * 4);
-    w.scan_part = (uint32_t*)take(sizeof(uint32_t) * (div_up(nn, kSortTile) + 1));
+    w.scan_part = (uint32_t*)take(sizeof(uint32_t) * (div_up(nn, kDupChunk) + 1));
     w.pair_keys_a = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.pair_vals_a = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.pair_keys_b = (uint32_t*)take(sizeof(uint32_t) * cap);

@@ -1,9 +1,16 @@
-// Tile blend (Sec. 3.1) and its reverse. One 256-thread workgroup (4 wave64)
-// per 16x16 tile, one pixel per thread; the tile's depth-sorted list is walked
-// in batches of 256 splats staged in LDS. Workgroup ids are mapped to tiles so
-// that each XCD (workgroups are dealt round-robin over the 8 XCDs) renders one
-// contiguous band of tiles, whose lists share most of their splats in that
-// XCD's L2.
+// Tile blend (Sec. 3.1) and its reverse. A 16x16 tile is covered by 4/PIX
+// independent wave64s, every lane owning PIX pixels of one column (thread t of
+// the workgroup: column t%16, rows t/16 + (16/PIX) k, k < PIX), so a lane's
+// pixels share dx and the quadratic form costs two fused multiply-adds per
+// pixel. Each wave walks the tile's depth-sorted list in batches of 64 splats:
+// every lane gathers one record into registers (the next batch is fetched
+// while the current one is blended), and the batch is then broadcast splat by
+// splat with readlane, i.e. as scalar operands. No LDS, no workgroup barriers;
+// a wave stops when its own pixels are done.
+//
+// Workgroup ids are mapped to tiles so that each XCD (workgroups are dealt
+// round-robin over the 8 XCDs) renders a contiguous band of tiles, whose lists
+// share most splats in that XCD's L2.
 #include "gs_internal.h"
 
 namespace gsr {
@@ -11,6 +18,14 @@ namespace gsr {
 namespace {
 
 constexpr int kXcds = 8;
+
+// Pixels per lane of the forward and the backward (1, 2 or 4).
+#ifndef GS_FWD_PIX
+#define GS_FWD_PIX 1
+#endif
+#ifndef GS_BWD_PIX
+#define GS_BWD_PIX 4
+#endif
 
 __device__ __forceinline__ int tile_of_block(int block, int n_tiles)
 {
@@ -20,35 +35,6 @@ __device__ __forceinline__ int tile_of_block(int block, int n_tiles)
 
 inline int blend_grid(int n_tiles) { return (int)div_up(n_tiles, kXcds) * kXcds; }
 
-struct SplatLds {
-    float2 xy[kBlock];
-    float4 co[kBlock];     // conic a, b, c, opacity
-    float4 rgb[kBlock];    // colour, w unused
-    uint32_t id[kBlock];
-};
-
-__device__ __forceinline__ void stage_splat(SplatLds& s, int slot, const gs_splat* __restrict__ splats, uint32_t g)
-{
-    const float4* p = reinterpret_cast<const float4*>(splats + g);
-    const float4 w0 = p[0];
-    const float4 w1 = p[1];
-    const float cb = reinterpret_cast<const float*>(splats + g)[8];
-    s.xy[slot] = make_float2(w0.x, w0.y);
-    s.co[slot] = make_float4(w0.z, w0.w, w1.x, w1.y);
-    s.rgb[slot] = make_float4(w1.z, w1.w, cb, 0.f);
-    s.id[slot] = g;
-}
-
-// The quadratic form and alpha of one (pixel, splat) pair; identical code in
-// the forward and the backward so both take the same skip/stop decisions.
-__device__ __forceinline__ float splat_power(const float2 xy, const float4 co, float px, float py, float& dx,
-                                             float& dy)
-{
-    dx = px - xy.x;
-    dy = py - xy.y;
-    return __fmaf_rn(-0.5f, __fmaf_rn(co.x * dx, dx, co.z * dy * dy), -(co.y * dx) * dy);
-}
-
 constexpr float kAlphaMin = 1.0f / 255.0f;
 constexpr float kAlphaMax = 0.99f;
 constexpr float kTMin = 0.0001f;
@@ -56,61 +42,154 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 __device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
 
+// One splat record in registers (the fields the blend needs).
+struct SplatReg {
+    float mx, my, ca, cb, cc, op, r, g, b;
+    uint32_t id;
+};
+
+__device__ __forceinline__ SplatReg load_splat(const gs_splat* __restrict__ splats, uint32_t gid)
+{
+    const float4* p = reinterpret_cast<const float4*>(splats + gid);
+    const float4 w0 = p[0];
+    const float4 w1 = p[1];
+    SplatReg s;
+    s.mx = w0.x; s.my = w0.y; s.ca = w0.z; s.cb = w0.w;
+    s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w;
+    s.b = reinterpret_cast<const float*>(splats + gid)[8];
+    s.id = gid;
+    return s;
+}
+
+__device__ __forceinline__ float bcast(float v, int j)
+{
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));
+}
+
+__device__ __forceinline__ SplatReg bcast(const SplatReg& s, int j)
+{
+    SplatReg t;
+    t.mx = bcast(s.mx, j); t.my = bcast(s.my, j);
+    t.ca = bcast(s.ca, j); t.cb = bcast(s.cb, j); t.cc = bcast(s.cc, j);
+    t.op = bcast(s.op, j);
+    t.r = bcast(s.r, j); t.g = bcast(s.g, j); t.b = bcast(s.b, j);
+    t.id = (uint32_t)__builtin_amdgcn_readlane((int)s.id, j);
+    return t;
+}
+
+// power(dy) = -(a dx^2 + c dy^2)/2 - b dx dy = q0 + dy (q1 + dy q2) for one column.
+struct Quad {
+    float q0, q1, q2;
+};
+
+__device__ __forceinline__ Quad column_quad(const SplatReg& s, float dx)
+{
+    Quad q;
+    q.q0 = -0.5f * s.ca * dx * dx;
+    q.q1 = -s.cb * dx;
+    q.q2 = -0.5f * s.cc;
+    return q;
+}
+
+__device__ __forceinline__ float quad_power(const Quad& q, float dy)
+{
+    return __fmaf_rn(__fmaf_rn(q.q2, dy, q.q1), dy, q.q0);
+}
+
+// Sum over the wave; the total is valid in lane 63. Row-local steps use
+// quad_perm, row_half_mirror and row_mirror; rows are joined with
+// row_bcast:15 and row_bcast:31 (rows not selected by the mask add 0).
+__device__ __forceinline__ float wave_sum_to_lane63(float v)
+{
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
+    return v;
+}
+
 }  // namespace
 
-__global__ __launch_bounds__(kBlock) void k_blend_fwd(Cam cam, const gs_splat* __restrict__ splats,
-                                                      const uint32_t* __restrict__ values,
-                                                      const uint32_t* __restrict__ ranges, float* __restrict__ image,
-                                                      float* __restrict__ final_T, uint32_t* __restrict__ n_contrib)
+template <int kPix>
+__global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, const gs_splat* __restrict__ splats,
+                                                                    const uint32_t* __restrict__ values,
+                                                                    const uint32_t* __restrict__ ranges,
+                                                                    float* __restrict__ image,
+                                                                    float* __restrict__ final_T,
+                                                                    uint32_t* __restrict__ n_contrib)
 {
-    __shared__ SplatLds s;
+    constexpr int kRowStep = kTile / kPix;
     const int n_tiles = cam.tiles_x * cam.tiles_y;
     const int tile = tile_of_block(blockIdx.x, n_tiles);
     if (tile >= n_tiles) return;
+    const int lane = __lane_id();
     const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
-    const int x = tx * kTile + (threadIdx.x & 15), y = ty * kTile + (threadIdx.x >> 4);
-    const bool inside = x < cam.width && y < cam.height;
-    const float px = (float)x + 0.5f, py = (float)y + 0.5f;
+    const int x = tx * kTile + (threadIdx.x & 15);
+    const int y0 = ty * kTile + (threadIdx.x >> 4);
+    const float px = (float)x + 0.5f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
 
-    float T = 1.f, C0 = 0.f, C1 = 0.f, C2 = 0.f;
-    uint32_t last = 0;
-    bool done = !inside;
-    for (uint32_t b = start; b < end; b += kBlock) {
-        if (__syncthreads_count(done) == kBlock) break;
-        const uint32_t idx = b + threadIdx.x;
-        if (idx < end) stage_splat(s, threadIdx.x, splats, values[idx]);
-        __syncthreads();
-        const int cnt = (int)min((uint32_t)kBlock, end - b);
-        if (!done) {
-            for (int j = 0; j < cnt; ++j) {
-                float dx, dy;
-                const float4 co = s.co[j];
-                const float power = splat_power(s.xy[j], co, px, py, dx, dy);
-                if (power > 0.f) continue;
-                const float alpha = fminf(kAlphaMax, co.w * exp_fast(power));
-                if (alpha < kAlphaMin) continue;
-                const float Tn = T * (1.f - alpha);
-                if (Tn < kTMin) { done = true; break; }
-                const float w = alpha * T;
-                const float4 c = s.rgb[j];
-                C0 = __fmaf_rn(c.x, w, C0);
-                C1 = __fmaf_rn(c.y, w, C1);
-                C2 = __fmaf_rn(c.z, w, C2);
-                T = Tn;
-                last = b - start + (uint32_t)j + 1;
-            }
-        }
-        __syncthreads();
+    float T[kPix], C0[kPix], C1[kPix], C2[kPix], py[kPix];
+    uint32_t last[kPix];
+    bool live[kPix];
+#pragma unroll
+    for (int k = 0; k < kPix; ++k) {
+        T[k] = 1.f;
+        C0[k] = C1[k] = C2[k] = 0.f;
+        last[k] = 0;
+        py[k] = (float)(y0 + kRowStep * k) + 0.5f;
+        live[k] = x < cam.width && (y0 + kRowStep * k) < cam.height;
     }
-    if (inside) {
+    SplatReg cur;
+    if (start + lane < end) cur = load_splat(splats, values[start + lane]);
+    for (uint32_t b = start; b < end; b += kWave) {
+        bool any = false;
+#pragma unroll
+        for (int k = 0; k < kPix; ++k) any = any || live[k];
+        if (__ballot(any) == 0) break;
+        SplatReg nxt;
+        if (b + kWave + lane < end) nxt = load_splat(splats, values[b + kWave + lane]);
+        const int cnt = (int)min((uint32_t)kWave, end - b);
+        for (int j = 0; j < cnt; ++j) {
+            const SplatReg s = bcast(cur, j);
+            const float dx = px - s.mx;
+            const Quad q = column_quad(s, dx);
+#pragma unroll
+            for (int k = 0; k < kPix; ++k) {
+                if (!live[k]) continue;
+                const float power = quad_power(q, py[k] - s.my);
+                if (power > 0.f) continue;
+                const float alpha = fminf(kAlphaMax, s.op * exp_fast(power));
+                if (alpha < kAlphaMin) continue;
+                const float Tn = T[k] * (1.f - alpha);
+                if (Tn < kTMin) { live[k] = false; continue; }
+                const float w = alpha * T[k];
+                C0[k] = __fmaf_rn(s.r, w, C0[k]);
+                C1[k] = __fmaf_rn(s.g, w, C1[k]);
+                C2[k] = __fmaf_rn(s.b, w, C2[k]);
+                T[k] = Tn;
+                last[k] = b - start + (uint32_t)j + 1;
+            }
+            any = false;
+#pragma unroll
+            for (int k = 0; k < kPix; ++k) any = any || live[k];
+            if (__ballot(any) == 0) break;
+        }
+        cur = nxt;
+    }
+    const int64_t hw = (int64_t)cam.width * cam.height;
+#pragma unroll
+    for (int k = 0; k < kPix; ++k) {
+        const int y = y0 + kRowStep * k;
+        if (x >= cam.width || y >= cam.height) continue;
         const int64_t pix = (int64_t)y * cam.width + x;
-        const int64_t hw = (int64_t)cam.width * cam.height;
-        image[pix] = __fmaf_rn(T, cam.bg[0], C0);
-        image[hw + pix] = __fmaf_rn(T, cam.bg[1], C1);
-        image[2 * hw + pix] = __fmaf_rn(T, cam.bg[2], C2);
-        final_T[pix] = T;
-        n_contrib[pix] = last;
+        image[pix] = __fmaf_rn(T[k], cam.bg[0], C0[k]);
+        image[hw + pix] = __fmaf_rn(T[k], cam.bg[1], C1[k]);
+        image[2 * hw + pix] = __fmaf_rn(T[k], cam.bg[2], C2[k]);
+        final_T[pix] = T[k];
+        n_contrib[pix] = last[k];
     }
 }
 
@@ -119,8 +198,8 @@ hipError_t launch_blend_fwd(const Cam& cam, const gs_splat* splats, const uint32
                             hipStream_t s)
 {
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    hipLaunchKernelGGL(k_blend_fwd, dim3(blend_grid(n_tiles)), dim3(kBlock), 0, s, cam, splats, values, tile_ranges,
-                       image, final_T, n_contrib);
+    hipLaunchKernelGGL(k_blend_fwd<GS_FWD_PIX>, dim3(blend_grid(n_tiles)), dim3(kTile * kTile / GS_FWD_PIX), 0, s,
+                       cam, splats, values, tile_ranges, image, final_T, n_contrib);
     return hipGetLastError();
 }
 
@@ -128,122 +207,132 @@ hipError_t launch_blend_fwd(const Cam& cam, const gs_splat* splats, const uint32
 // Per pixel, back to front from its last blended splat, with T recovered as
 // T_i = T_{i+1} / (1 - alpha_i) and S the suffix sum of colour * alpha * T plus
 // T_final * bg:  dL/dcolour_i = alpha_i T_i g,  dL/dalpha_i = sum_ch
-// (T_i c_i - S / (1 - alpha_i)) g_ch. Each wave sums its 64 pixels' gradients of a
-// splat before one set of float atomics per splat.
+// (T_i c_i - S / (1 - alpha_i)) g_ch. The alpha and skip decisions reuse the
+// forward's code, so the same splats are found contributing. Each lane sums
+// its pixels, the wave sums its lanes, and lane 63 issues one set of float
+// atomics per (wave, splat).
 
-__device__ __forceinline__ float wave_sum(float v)
+template <int kPix>
+__global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, const gs_splat* __restrict__ splats,
+                                                                    const uint32_t* __restrict__ values,
+                                                                    const uint32_t* __restrict__ ranges,
+                                                                    const float* __restrict__ final_T,
+                                                                    const uint32_t* __restrict__ n_contrib,
+                                                                    const float* __restrict__ dL_dimage,
+                                                                    float* __restrict__ acc)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-    return v;
-}
-
-__global__ __launch_bounds__(kBlock) void k_blend_bwd(Cam cam, const gs_splat* __restrict__ splats,
-                                                      const uint32_t* __restrict__ values,
-                                                      const uint32_t* __restrict__ ranges,
-                                                      const float* __restrict__ final_T,
-                                                      const uint32_t* __restrict__ n_contrib,
-                                                      const float* __restrict__ dL_dimage, float* __restrict__ acc)
-{
-    __shared__ SplatLds s;
-    __shared__ uint32_t max_last;
+    constexpr int kRowStep = kTile / kPix;
     const int n_tiles = cam.tiles_x * cam.tiles_y;
     const int tile = tile_of_block(blockIdx.x, n_tiles);
     if (tile >= n_tiles) return;
+    const int lane = __lane_id();
     const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
-    const int x = tx * kTile + (threadIdx.x & 15), y = ty * kTile + (threadIdx.x >> 4);
-    const bool inside = x < cam.width && y < cam.height;
-    const float px = (float)x + 0.5f, py = (float)y + 0.5f;
+    const int x = tx * kTile + (threadIdx.x & 15);
+    const int y0 = ty * kTile + (threadIdx.x >> 4);
+    const float px = (float)x + 0.5f;
     const uint32_t start = ranges[2 * tile], len = ranges[2 * tile + 1] - start;
-    const int64_t pix = (int64_t)y * cam.width + x;
     const int64_t hw = (int64_t)cam.width * cam.height;
 
-    float T = 1.f, g0 = 0.f, g1 = 0.f, g2 = 0.f;
-    uint32_t last = 0;
-    if (inside) {
-        T = final_T[pix];
-        last = min(n_contrib[pix], len);
-        g0 = dL_dimage[pix];
-        g1 = dL_dimage[hw + pix];
-        g2 = dL_dimage[2 * hw + pix];
+    float T[kPix], py[kPix], g0[kPix], g1[kPix], g2[kPix], S0[kPix], S1[kPix], S2[kPix];
+    uint32_t last[kPix];
+    uint32_t stop = 0;
+#pragma unroll
+    for (int k = 0; k < kPix; ++k) {
+        const int y = y0 + kRowStep * k;
+        py[k] = (float)y + 0.5f;
+        T[k] = 1.f;
+        g0[k] = g1[k] = g2[k] = 0.f;
+        last[k] = 0;
+        if (x < cam.width && y < cam.height) {
+            const int64_t pix = (int64_t)y * cam.width + x;
+            T[k] = final_T[pix];
+            last[k] = min(n_contrib[pix], len);
+            g0[k] = dL_dimage[pix];
+            g1[k] = dL_dimage[hw + pix];
+            g2[k] = dL_dimage[2 * hw + pix];
+        }
+        S0[k] = T[k] * cam.bg[0];
+        S1[k] = T[k] * cam.bg[1];
+        S2[k] = T[k] * cam.bg[2];
+        stop = max(stop, last[k]);
     }
-    float S0 = T * cam.bg[0], S1 = T * cam.bg[1], S2 = T * cam.bg[2];
-    if (threadIdx.x == 0) max_last = 0;
-    __syncthreads();
-    atomicMax(&max_last, last);
-    __syncthreads();
-    const uint32_t stop = max_last;   // list positions [0, stop) can contribute
+    // list positions [0, stop) can contribute
+    for (int o = 32; o > 0; o >>= 1) stop = max(stop, (uint32_t)__shfl_xor((int)stop, o));
     if (stop == 0) return;
-    const int lane = __lane_id();
-    const int nbatch = (int)((stop + kBlock - 1) / kBlock);
+    const int nbatch = (int)((stop + kWave - 1) / kWave);
+    SplatReg cur;
+    {
+        const uint32_t p = (uint32_t)(nbatch - 1) * kWave + lane;
+        if (p < stop) cur = load_splat(splats, values[start + p]);
+    }
     for (int bi = nbatch - 1; bi >= 0; --bi) {
-        const uint32_t b = (uint32_t)bi * kBlock;   // position of the batch within the tile list
-        const uint32_t cnt = min((uint32_t)kBlock, stop - b);
-        __syncthreads();
-        if ((uint32_t)threadIdx.x < cnt) stage_splat(s, threadIdx.x, splats, values[start + b + threadIdx.x]);
-        __syncthreads();
-        for (int j = (int)cnt - 1; j >= 0; --j) {
+        const uint32_t b = (uint32_t)bi * kWave;
+        SplatReg nxt;
+        if (bi > 0) nxt = load_splat(splats, values[start + b - kWave + lane]);
+        const int cnt = (int)min((uint32_t)kWave, stop - b);
+        for (int j = cnt - 1; j >= 0; --j) {
             const uint32_t pos = b + (uint32_t)j;
-            bool contrib = pos < last;
-            float dx = 0.f, dy = 0.f, alpha = 0.f, G = 0.f;
-            const float4 co = s.co[j];
-            if (contrib) {
-                const float power = splat_power(s.xy[j], co, px, py, dx, dy);
-                contrib = power <= 0.f;
-                if (contrib) {
-                    G = exp_fast(power);
-                    alpha = fminf(kAlphaMax, co.w * G);
-                    contrib = alpha >= kAlphaMin;
-                }
-            }
-            if (__ballot(contrib) == 0) continue;
-            float dm_x = 0.f, dm_y = 0.f, dca = 0.f, dcb = 0.f, dcc = 0.f, dop = 0.f, dc0 = 0.f, dc1 = 0.f,
-                  dc2 = 0.f;
-            if (contrib) {
-                const float oma = 1.f - alpha;
-                T = T / oma;                        // transmittance in front of this splat
-                const float4 c = s.rgb[j];
-                const float w = alpha * T;
-                dc0 = w * g0;
-                dc1 = w * g1;
-                dc2 = w * g2;
-                const float inv = 1.f / oma;
-                const float dalpha = (T * c.x - S0 * inv) * g0 + (T * c.y - S1 * inv) * g1 + (T * c.z - S2 * inv) * g2;
-                S0 = __fmaf_rn(c.x, w, S0);
-                S1 = __fmaf_rn(c.y, w, S1);
-                S2 = __fmaf_rn(c.z, w, S2);
-                if (co.w * G < kAlphaMax) {         // below the cap alpha = o G
-                    dop = G * dalpha;
+            const SplatReg s = bcast(cur, j);
+            const float dx = px - s.mx;
+            const Quad q = column_quad(s, dx);
+            float a_dmx = 0.f, a_dmy = 0.f, a_dca = 0.f, a_dcb = 0.f, a_dcc = 0.f, a_dop = 0.f;
+            float a_c0 = 0.f, a_c1 = 0.f, a_c2 = 0.f;
+            bool any = false;
+#pragma unroll
+            for (int k = 0; k < kPix; ++k) {
+                if (pos >= last[k]) continue;
+                const float dy = py[k] - s.my;
+                const float power = quad_power(q, dy);
+                if (power > 0.f) continue;
+                const float G = exp_fast(power);
+                const float alpha = fminf(kAlphaMax, s.op * G);
+                if (alpha < kAlphaMin) continue;
+                any = true;
+                const float inv = 1.f / (1.f - alpha);
+                T[k] *= inv;                                // transmittance in front of this splat
+                const float w = alpha * T[k];
+                a_c0 = __fmaf_rn(w, g0[k], a_c0);
+                a_c1 = __fmaf_rn(w, g1[k], a_c1);
+                a_c2 = __fmaf_rn(w, g2[k], a_c2);
+                const float dalpha = (T[k] * s.r - S0[k] * inv) * g0[k] + (T[k] * s.g - S1[k] * inv) * g1[k] +
+                                     (T[k] * s.b - S2[k] * inv) * g2[k];
+                S0[k] = __fmaf_rn(s.r, w, S0[k]);
+                S1[k] = __fmaf_rn(s.g, w, S1[k]);
+                S2[k] = __fmaf_rn(s.b, w, S2[k]);
+                if (s.op * G < kAlphaMax) {                 // below the cap alpha = o G
+                    a_dop = __fmaf_rn(G, dalpha, a_dop);
                     const float dpow = alpha * dalpha;
-                    dm_x = dpow * (co.x * dx + co.y * dy);
-                    dm_y = dpow * (co.z * dy + co.y * dx);
-                    dca = -0.5f * dpow * dx * dx;
-                    dcb = -dpow * dx * dy;
-                    dcc = -0.5f * dpow * dy * dy;
+                    a_dmx = __fmaf_rn(dpow, s.ca * dx + s.cb * dy, a_dmx);
+                    a_dmy = __fmaf_rn(dpow, s.cc * dy + s.cb * dx, a_dmy);
+                    a_dca = __fmaf_rn(-0.5f * dpow, dx * dx, a_dca);
+                    a_dcb = __fmaf_rn(-dpow, dx * dy, a_dcb);
+                    a_dcc = __fmaf_rn(-0.5f * dpow, dy * dy, a_dcc);
                 }
             }
-            dm_x = wave_sum(dm_x);
-            dm_y = wave_sum(dm_y);
-            dca = wave_sum(dca);
-            dcb = wave_sum(dcb);
-            dcc = wave_sum(dcc);
-            dop = wave_sum(dop);
-            dc0 = wave_sum(dc0);
-            dc1 = wave_sum(dc1);
-            dc2 = wave_sum(dc2);
-            if (lane == 0) {
-                float* a = acc + (size_t)s.id[j] * kAccStride;
-                atomicAdd(a + 0, dm_x);
-                atomicAdd(a + 1, dm_y);
-                atomicAdd(a + 2, dca);
-                atomicAdd(a + 3, dcb);
-                atomicAdd(a + 4, dcc);
-                atomicAdd(a + 5, dop);
-                atomicAdd(a + 6, dc0);
-                atomicAdd(a + 7, dc1);
-                atomicAdd(a + 8, dc2);
+            if (__ballot(any) == 0) continue;
+            a_dmx = wave_sum_to_lane63(a_dmx);
+            a_dmy = wave_sum_to_lane63(a_dmy);
+            a_dca = wave_sum_to_lane63(a_dca);
+            a_dcb = wave_sum_to_lane63(a_dcb);
+            a_dcc = wave_sum_to_lane63(a_dcc);
+            a_dop = wave_sum_to_lane63(a_dop);
+            a_c0 = wave_sum_to_lane63(a_c0);
+            a_c1 = wave_sum_to_lane63(a_c1);
+            a_c2 = wave_sum_to_lane63(a_c2);
+            if (lane == kWave - 1) {
+                float* a = acc + (size_t)s.id * kAccStride;
+                atomicAdd(a + 0, a_dmx);
+                atomicAdd(a + 1, a_dmy);
+                atomicAdd(a + 2, a_dca);
+                atomicAdd(a + 3, a_dcb);
+                atomicAdd(a + 4, a_dcc);
+                atomicAdd(a + 5, a_dop);
+                atomicAdd(a + 6, a_c0);
+                atomicAdd(a + 7, a_c1);
+                atomicAdd(a + 8, a_c2);
             }
         }
+        cur = nxt;
     }
 }
 
@@ -252,8 +341,8 @@ hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32
                             const float* dL_dimage, float* acc, hipStream_t s)
 {
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    hipLaunchKernelGGL(k_blend_bwd, dim3(blend_grid(n_tiles)), dim3(kBlock), 0, s, cam, splats, values, tile_ranges,
-                       final_T, n_contrib, dL_dimage, acc);
+    hipLaunchKernelGGL(k_blend_bwd<GS_BWD_PIX>, dim3(blend_grid(n_tiles)), dim3(kTile * kTile / GS_BWD_PIX), 0, s,
+                       cam, splats, values, tile_ranges, final_T, n_contrib, dL_dimage, acc);
     return hipGetLastError();
 }
 

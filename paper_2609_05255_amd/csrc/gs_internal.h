@@ -52,6 +52,7 @@ constexpr int kAccStride = 9;
 constexpr int kSortItems = 16;
 constexpr int kSortTile = kBlock * kSortItems;   // 4096
 constexpr int kRadix = 256;
+constexpr int kDupChunk = 2048;   // depth-ordered Gaussians per workgroup in pair emission
 
 // Workgroups of the latent preprocess backward (grid-stride), one partial
 // weight gradient each.
@@ -70,7 +71,7 @@ struct Workspace {
     uint32_t* vals_b;        // [n]
     uint32_t* hist;          // [256][max sort blocks]
     uint32_t* digit_tot;     // [4 passes][256]   digit totals of each pass
-    uint32_t* scan_part;     // [n / 4096 + 1]    block sums of the pair-offset scan
+    uint32_t* scan_part;     // [n / kDupChunk + 1] chunk sums of the pair-offset scan
     uint32_t* pair_keys_a;   // [capacity]
     uint32_t* pair_vals_a;   // [capacity]
     uint32_t* pair_keys_b;   // [capacity]

@@ -4,17 +4,23 @@
 // Instead of radix-sorting P 45-bit (tile, depth) keys, the Gaussians are
 // sorted once by depth (4 stable 8-bit LSD passes over n 32-bit keys with the
 // index as value, so equal depths stay in index order), the pairs are emitted
-// in that order, and a stable LSD sort on the tile id alone (ceil(log2 T)/8
-// passes) finishes the job: stability keeps (depth, index) order within a tile.
+// in that order, and a stable LSD sort on the tile id alone finishes the job:
+// stability keeps (depth, index) order within a tile. The tile id needs
+// ceil(log2 T) bits, split evenly over as few passes of <= 8 bits as possible.
 //
 // One radix pass = k_radix_hist (per-workgroup digit counts) + k_radix_scan
-// (exclusive offsets per digit over workgroups) + k_radix_scatter (stable
-// rank inside the workgroup with wave64 ballots, then scatter).
+// (exclusive offsets per digit over workgroups) + k_radix_scatter: each wave
+// ranks a contiguous slice of 1024 keys with ballot-matched digits (no
+// workgroup barrier per round), the workgroup reorders its 4096 keys by digit
+// in LDS, and writes each digit's run to consecutive global addresses.
 #include "gs_internal.h"
 
 namespace gsr {
 
 namespace {
+
+constexpr int kSliceKeys = kSortTile / (kBlock / kWave);   // 1024 keys per wave
+constexpr int kDupItems = kDupChunk / kBlock;              // 8 per thread
 
 __device__ __forceinline__ uint64_t lanemask_lt() { return (1ull << __lane_id()) - 1ull; }
 
@@ -42,12 +48,13 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* lds4, 
     return before + x - v;
 }
 
-// Lanes of this wave holding the same 8-bit digit (restricted to valid lanes).
+// Lanes of this wave holding the same kBits-bit digit (restricted to valid lanes).
+template <int kBits>
 __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid)
 {
     uint64_t m = __ballot(valid);
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
+    for (int b = 0; b < kBits; ++b) {
         const bool bit = (d >> b) & 1u;
         const uint64_t bm = __ballot(bit);
         m &= bit ? bm : ~bm;
@@ -55,22 +62,24 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid)
     return m;
 }
 
+template <int kBits>
 __global__ __launch_bounds__(kBlock) void k_radix_hist(const uint32_t* __restrict__ keys, uint64_t count, int shift,
                                                        uint32_t* __restrict__ hist, int nblocks)
 {
-    __shared__ uint32_t h[4][kRadix];
-    for (int k = threadIdx.x; k < 4 * kRadix; k += kBlock) (&h[0][0])[k] = 0;
+    constexpr int R = 1 << kBits;
+    __shared__ uint32_t h[4][R];
+    for (int k = threadIdx.x; k < 4 * R; k += kBlock) (&h[0][0])[k] = 0;
     __syncthreads();
     const int wave = threadIdx.x >> 6;
     const uint64_t base = (uint64_t)blockIdx.x * kSortTile;
 #pragma unroll 4
     for (int r = 0; r < kSortItems; ++r) {
         const uint64_t idx = base + (uint64_t)r * kBlock + threadIdx.x;
-        if (idx < count) atomicAdd(&h[wave][(keys[idx] >> shift) & 0xFFu], 1u);
+        if (idx < count) atomicAdd(&h[wave][(keys[idx] >> shift) & (R - 1)], 1u);
     }
     __syncthreads();
     const int d = threadIdx.x;
-    hist[(size_t)d * nblocks + blockIdx.x] = h[0][d] + h[1][d] + h[2][d] + h[3][d];
+    if (d < R) hist[(size_t)d * nblocks + blockIdx.x] = h[0][d] + h[1][d] + h[2][d] + h[3][d];
 }
 
 // One workgroup per digit: exclusive scan of that digit's counts over workgroups.
@@ -94,6 +103,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(uint32_t* __restrict__ hi
     if (threadIdx.x == 0) digit_tot[blockIdx.x] = total;
 }
 
+template <int kBits>
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __restrict__ keys_in,
                                                           const uint32_t* __restrict__ vals_in, uint64_t count,
                                                           int shift, const uint32_t* __restrict__ hist, int nblocks,
@@ -101,63 +111,120 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
                                                           uint32_t* __restrict__ keys_out,
                                                           uint32_t* __restrict__ vals_out)
 {
-    __shared__ uint32_t run[kRadix];
-    __shared__ uint32_t cnt[4][kRadix];
+    constexpr int R = 1 << kBits;
+    __shared__ uint32_t wcnt[4][R];      // per-wave digit counts, then per-wave exclusive offsets
+    __shared__ uint32_t gbase[R];        // global position of this workgroup's first key of each digit
+    __shared__ uint32_t lstart[R];       // start of each digit in the workgroup's reordered keys
+    __shared__ uint32_t skey[kSortTile];
+    __shared__ uint32_t sval[kSortTile];
     __shared__ uint32_t lds4[4];
-    const int t = threadIdx.x, wave = t >> 6;
-    const uint32_t base_d = block_excl_scan(digit_tot[t], lds4, nullptr);
-    run[t] = base_d + hist[(size_t)t * nblocks + blockIdx.x];
-    for (int w = 0; w < 4; ++w) cnt[w][t] = 0;
+    const int t = threadIdx.x, wave = t >> 6, lane = __lane_id();
+    const uint32_t dt = t < R ? digit_tot[t] : 0u;
+    const uint32_t dbase = block_excl_scan(dt, lds4, nullptr);
+    if (t < R) {
+        gbase[t] = dbase + hist[(size_t)t * nblocks + blockIdx.x];
+        for (int w = 0; w < 4; ++w) wcnt[w][t] = 0;
+    }
     __syncthreads();
+    // rank within the wave's slice, in key order
     const uint64_t base = (uint64_t)blockIdx.x * kSortTile;
-    for (int r = 0; r < kSortItems; ++r) {
-        const uint64_t idx = base + (uint64_t)r * kBlock + t;
+    const uint64_t wbase = base + (uint64_t)wave * kSliceKeys;
+    uint32_t key[kSortItems], val[kSortItems], rank[kSortItems];
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const uint64_t idx = wbase + (uint64_t)i * kWave + lane;
         const bool valid = idx < count;
-        uint32_t key = 0, val = 0;
-        if (valid) {
-            key = keys_in[idx];
-            val = vals_in ? vals_in[idx] : (uint32_t)idx;
+        key[i] = valid ? keys_in[idx] : 0u;
+        val[i] = valid ? (vals_in ? vals_in[idx] : (uint32_t)idx) : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const uint64_t idx = wbase + (uint64_t)i * kWave + lane;
+        const bool valid = idx < count;
+        const uint32_t d = (key[i] >> shift) & (R - 1);
+        const uint64_t peers = match_digit<kBits>(d, valid);
+        const uint32_t r = (uint32_t)__popcll(peers & lanemask_lt());
+        const uint32_t pre = valid ? wcnt[wave][d] : 0u;
+        rank[i] = pre + r;
+        if (valid && r == 0) wcnt[wave][d] = pre + (uint32_t)__popcll(peers);
+        // the next round reads counts this round's leaders wrote
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    uint32_t tot = 0;
+    if (t < R) {
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t c = wcnt[w][t];
+            wcnt[w][t] = tot;
+            tot += c;
         }
-        const uint32_t d = (key >> shift) & 0xFFu;
-        const uint64_t peers = match_digit(d, valid);
-        const uint32_t rank = (uint32_t)__popcll(peers & lanemask_lt());
-        if (valid && rank == 0) cnt[wave][d] = (uint32_t)__popcll(peers);
-        __syncthreads();
-        if (valid) {
-            uint32_t pos = run[d] + rank;
-            for (int w = 0; w < wave; ++w) pos += cnt[w][d];
-            keys_out[pos] = key;
-            vals_out[pos] = val;
+    }
+    const uint32_t ls = block_excl_scan(t < R ? tot : 0u, lds4, nullptr);
+    if (t < R) lstart[t] = ls;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSortItems; ++i) {
+        const uint64_t idx = wbase + (uint64_t)i * kWave + lane;
+        if (idx < count) {
+            const uint32_t d = (key[i] >> shift) & (R - 1);
+            const uint32_t lp = lstart[d] + wcnt[wave][d] + rank[i];
+            skey[lp] = key[i];
+            sval[lp] = val[i];
         }
-        __syncthreads();
-        run[t] += cnt[0][t] + cnt[1][t] + cnt[2][t] + cnt[3][t];
-        cnt[0][t] = cnt[1][t] = cnt[2][t] = cnt[3][t] = 0;
-        __syncthreads();
+    }
+    __syncthreads();
+    const uint32_t nvalid = (uint32_t)min((uint64_t)kSortTile, count - base);
+    for (uint32_t j = t; j < nvalid; j += kBlock) {
+        const uint32_t k = skey[j];
+        const uint32_t d = (k >> shift) & (R - 1);
+        const uint32_t pos = gbase[d] + (j - lstart[d]);
+        if (keys_out) keys_out[pos] = k;
+        vals_out[pos] = sval[j];
     }
 }
 
-// One stable LSD pass; vals_in == nullptr means value = position.
-hipError_t radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t count, int shift,
-                      uint32_t* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
+// One stable LSD pass over `bits` bits at `shift`; vals_in == nullptr means
+// value = position, keys_out == nullptr drops the keys.
+template <int kBits>
+void radix_pass_t(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t count, int shift, uint32_t* keys_out,
+                  uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
 {
     const int nblocks = (int)div_up((int64_t)count, kSortTile);
-    hipLaunchKernelGGL(k_radix_hist, dim3(nblocks), dim3(kBlock), 0, s, keys_in, count, shift, hist, nblocks);
-    hipLaunchKernelGGL(k_radix_scan, dim3(kRadix), dim3(kBlock), 0, s, hist, nblocks, digit_tot);
-    hipLaunchKernelGGL(k_radix_scatter, dim3(nblocks), dim3(kBlock), 0, s, keys_in, vals_in, count, shift, hist,
-                       nblocks, digit_tot, keys_out, vals_out);
+    hipLaunchKernelGGL(k_radix_hist<kBits>, dim3(nblocks), dim3(kBlock), 0, s, keys_in, count, shift, hist, nblocks);
+    hipLaunchKernelGGL(k_radix_scan, dim3(1 << kBits), dim3(kBlock), 0, s, hist, nblocks, digit_tot);
+    hipLaunchKernelGGL(k_radix_scatter<kBits>, dim3(nblocks), dim3(kBlock), 0, s, keys_in, vals_in, count, shift,
+                       hist, nblocks, digit_tot, keys_out, vals_out);
+}
+
+hipError_t radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t count, int shift, int bits,
+                      uint32_t* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
+{
+    switch (bits) {
+    case 1: radix_pass_t<1>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 2: radix_pass_t<2>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 3: radix_pass_t<3>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 4: radix_pass_t<4>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 5: radix_pass_t<5>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 6: radix_pass_t<6>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 7: radix_pass_t<7>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 8: radix_pass_t<8>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
 // ---- pair offsets in depth order and pair emission ---------------------------
 
+// Pairs emitted by each chunk of kDupChunk depth-ordered Gaussians.
 __global__ __launch_bounds__(kBlock) void k_pair_partial(const uint32_t* __restrict__ order,
                                                          const uint32_t* __restrict__ tiles_touched, int64_t n,
                                                          uint32_t* __restrict__ part)
 {
     __shared__ uint32_t lds4[4];
-    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)threadIdx.x * kSortItems;
+    const int64_t base = (int64_t)blockIdx.x * kDupChunk + (int64_t)threadIdx.x * kDupItems;
     uint32_t sum = 0;
-    for (int k = 0; k < kSortItems; ++k) {
+    for (int k = 0; k < kDupItems; ++k) {
         const int64_t i = base + k;
         if (i < n) sum += tiles_touched[order[i]];
     }
@@ -166,7 +233,7 @@ __global__ __launch_bounds__(kBlock) void k_pair_partial(const uint32_t* __restr
     if (threadIdx.x == 0) part[blockIdx.x] = total;
 }
 
-// Exclusive scan of the per-workgroup totals (one workgroup).
+// Exclusive scan of the per-chunk totals (one workgroup).
 __global__ __launch_bounds__(kBlock) void k_scan_partials(uint32_t* __restrict__ part, int count)
 {
     __shared__ uint32_t lds4[4];
@@ -182,8 +249,11 @@ __global__ __launch_bounds__(kBlock) void k_scan_partials(uint32_t* __restrict__
     }
 }
 
-// Emits the (tile, Gaussian) pairs of the depth-ordered Gaussians; each
-// Gaussian's tiles in row-major order of its rectangle.
+// Emits the (tile, Gaussian) pairs of a chunk of depth-ordered Gaussians, each
+// Gaussian's tiles in row-major order of its rectangle. The chunk's offsets
+// and rectangles are staged in LDS; each thread then produces every 256th
+// pair of the chunk, finding its Gaussian by binary search, so consecutive
+// threads write consecutive addresses.
 __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict__ order,
                                                       const uint32_t* __restrict__ tiles_touched,
                                                       const gs_splat* __restrict__ splats, int64_t n,
@@ -191,31 +261,62 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
                                                       uint32_t capacity, uint32_t* __restrict__ keys,
                                                       uint32_t* __restrict__ vals)
 {
+    __shared__ uint32_t soff[kDupChunk];
+    __shared__ uint32_t sgid[kDupChunk];
+    __shared__ uint32_t sorg[kDupChunk];   // rectangle origin x0 | y0 << 16
+    __shared__ uint32_t swid[kDupChunk];   // rectangle width in tiles
     __shared__ uint32_t lds4[4];
-    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)threadIdx.x * kSortItems;
+    const int t = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * kDupChunk;
+    uint32_t cnt[kDupItems];
     uint32_t sum = 0;
-    for (int k = 0; k < kSortItems; ++k) {
-        const int64_t i = base + k;
-        if (i < n) sum += tiles_touched[order[i]];
-    }
-    uint32_t off = part[blockIdx.x] + block_excl_scan(sum, lds4, nullptr);
-    for (int k = 0; k < kSortItems; ++k) {
-        const int64_t i = base + k;
-        if (i >= n) break;
-        const uint32_t g = order[i];
-        if (tiles_touched[g] == 0) continue;
-        const float2 rr = *reinterpret_cast<const float2*>(reinterpret_cast<const float*>(splats + g) + 10);
-        const uint32_t r01 = __float_as_uint(rr.x), r23 = __float_as_uint(rr.y);
-        const int x0 = (int)(r01 & 0xFFFF), y0 = (int)(r01 >> 16);
-        const int x1 = (int)(r23 & 0xFFFF), y1 = (int)(r23 >> 16);
-        for (int ty = y0; ty < y1; ++ty)
-            for (int tx = x0; tx < x1; ++tx) {
-                if (off < capacity) {   // only a num_pairs that disagrees with the preprocess gets here
-                    keys[off] = (uint32_t)(ty * tiles_x + tx);
-                    vals[off] = g;
-                }
-                ++off;
+    for (int k = 0; k < kDupItems; ++k) {
+        const int slot = t * kDupItems + k;
+        const int64_t i = base + slot;
+        uint32_t c = 0, g = 0, org = 0, w = 1;
+        if (i < n) {
+            g = order[i];
+            c = tiles_touched[g];
+            if (c != 0) {
+                const float2 rr = *reinterpret_cast<const float2*>(reinterpret_cast<const float*>(splats + g) + 10);
+                const uint32_t r01 = __float_as_uint(rr.x), r23 = __float_as_uint(rr.y);
+                org = r01;
+                w = (r23 & 0xFFFFu) - (r01 & 0xFFFFu);
             }
+        }
+        cnt[k] = c;
+        sum += c;
+        sgid[slot] = g;
+        sorg[slot] = org;
+        swid[slot] = w;
+    }
+    uint32_t total;
+    uint32_t off = block_excl_scan(sum, lds4, &total);
+    for (int k = 0; k < kDupItems; ++k) {
+        soff[t * kDupItems + k] = off;
+        off += cnt[k];
+    }
+    __syncthreads();
+    const uint32_t gbase = part[blockIdx.x];
+    for (uint32_t p = t; p < total; p += kBlock) {
+        // last slot whose offset is <= p
+        int lo = 0, hi = kDupChunk;
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (soff[mid] <= p) lo = mid;
+            else hi = mid;
+        }
+        const uint32_t i = p - soff[lo];
+        const uint32_t w = swid[lo];
+        const uint32_t q = i / w;
+        const uint32_t org = sorg[lo];
+        const uint32_t tx = (org & 0xFFFFu) + (i - q * w);
+        const uint32_t ty = (org >> 16) + q;
+        const uint32_t out = gbase + p;
+        if (out < capacity) {   // only a num_pairs that disagrees with the preprocess gets past it
+            keys[out] = ty * (uint32_t)tiles_x + tx;
+            vals[out] = sgid[lo];
+        }
     }
 }
 
@@ -249,7 +350,8 @@ hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const Workspa
     uint32_t* kbuf[2] = {ws.keys_a, ws.keys_b};
     uint32_t* vbuf[2] = {ws.vals_a, ws.vals_b};
     for (int p = 0; p < 4; ++p) {
-        hipError_t e = radix_pass(kin, vin, (uint64_t)n, 8 * p, kbuf[p & 1], vbuf[p & 1], ws.hist,
+        uint32_t* kout = p == 3 ? nullptr : kbuf[p & 1];
+        hipError_t e = radix_pass(kin, vin, (uint64_t)n, 8 * p, 8, kout, vbuf[p & 1], ws.hist,
                                   ws.digit_tot + kRadix * p, s);
         if (e != hipSuccess) return e;
         kin = kbuf[p & 1];
@@ -262,7 +364,7 @@ hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const Workspa
 hipError_t launch_pair_offsets(int64_t n, const uint32_t* order, const uint32_t* tiles_touched, const Workspace& ws,
                                hipStream_t s)
 {
-    const int nb = (int)div_up(n, kSortTile);
+    const int nb = (int)div_up(n, kDupChunk);
     hipLaunchKernelGGL(k_pair_partial, dim3(nb), dim3(kBlock), 0, s, order, tiles_touched, n, ws.scan_part);
     hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kBlock), 0, s, ws.scan_part, nb);
     return hipGetLastError();
@@ -272,34 +374,40 @@ hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, co
                             const Workspace& ws, uint32_t capacity, uint32_t* keys_out, uint32_t* vals_out,
                             hipStream_t s)
 {
-    const int nb = (int)div_up(n, kSortTile);
+    const int nb = (int)div_up(n, kDupChunk);
     hipLaunchKernelGGL(k_duplicate, dim3(nb), dim3(kBlock), 0, s, order, pre.tiles_touched, pre.splats, n,
                        ws.scan_part, cam.tiles_x, capacity, keys_out, vals_out);
     return hipGetLastError();
 }
 
-int tile_sort_passes(const Cam& cam)
+// Bits of the tile id, and how they are split over passes of at most 8 bits.
+static int tile_bits(const Cam& cam)
 {
     const uint32_t n_tiles = (uint32_t)cam.tiles_x * (uint32_t)cam.tiles_y;
     int bits = 0;
     while (bits < 32 && ((n_tiles - 1) >> bits) != 0) ++bits;
-    return (bits + 7) / 8;
+    return bits;
 }
+
+int tile_sort_passes(const Cam& cam) { return (tile_bits(cam) + 7) / 8; }
 
 hipError_t launch_tile_sort(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
                             uint32_t* tile_ids_out, const uint32_t** sorted_tiles, hipStream_t s)
 {
-    const int passes = tile_sort_passes(cam);
+    const int bits = tile_bits(cam);
+    const int passes = (bits + 7) / 8;
     uint32_t* kbuf[2] = {ws.pair_keys_a, ws.pair_keys_b};
     uint32_t* vbuf[2] = {ws.pair_vals_a, ws.pair_vals_b};
-    int src = 0;
+    int src = 0, shift = 0;
     for (int p = 0; p < passes; ++p) {
         const bool last = p == passes - 1;
+        const int pb = (bits - shift + (passes - p) - 1) / (passes - p);   // remaining bits spread evenly
         uint32_t* kout = last ? (tile_ids_out ? tile_ids_out : kbuf[src ^ 1]) : kbuf[src ^ 1];
         uint32_t* vout = last ? values : vbuf[src ^ 1];
-        hipError_t e = radix_pass(kbuf[src], vbuf[src], num_pairs, 8 * p, kout, vout, ws.hist, ws.digit_tot, s);
+        hipError_t e = radix_pass(kbuf[src], vbuf[src], num_pairs, shift, pb, kout, vout, ws.hist, ws.digit_tot, s);
         if (e != hipSuccess) return e;
         if (last) *sorted_tiles = kout;
+        shift += pb;
         src ^= 1;
     }
     return hipSuccess;

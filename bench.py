@@ -27,6 +27,11 @@ sys.path.insert(0, ROOT)
 METRIC = "fwd+bwd iterations/sec and rendered Mpix/s at 3M Gaussians, 1600x1064"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 FP32_VECTOR_PEAK_TFLOPS = 157.3
+# fp32 work per blended (pixel, splat) pair, counting an FMA as 2 (see the kernels):
+# forward: quadratic form 11, exp 2, alpha 2, transmittance 2, weight 1, colour 6;
+# backward: quadratic form 11, exp 2, alpha 2, transmittance 2, dcolour 4, dalpha 15,
+# suffix sum 6, dopacity + dmean2d + dconic 20.
+BLEND_FLOPS_PER_PAIR = {"blend_fwd": 24.0, "blend_bwd": 62.0}
 
 
 def parse():
@@ -38,6 +43,9 @@ def parse():
     ap.add_argument("--appearance", default=None, help="sh3 or latent (default: the config's first)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tiles", type=int, default=96, help="tiles in the CPU-baseline sample")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="before the steps, one device-to-device copy of this many MB (a plain copy kernel of "
+                         "known size, to calibrate memory-traffic counters)")
     return ap.parse_args()
 
 
@@ -79,6 +87,15 @@ def main():
     cstructs = [gs.camera_struct(c) for c in cams]
     print("# scene %s (%s) generated and uploaded in %.1fs" % (cfg.name, kind, time.time() - t0), file=sys.stderr,
           flush=True)
+
+    if args.copy_probe_mb > 0:
+        nbytes = args.copy_probe_mb << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # size the pair buffers: preprocess every camera once (untimed)
     probe = gs.Frame(scene.n, cfg.width, cfg.height, kid, 1, device=dev)
@@ -139,7 +156,7 @@ def main():
                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
     else:
         # blend kernels: fp32 vector work per blended (pixel, splat) pair
-        flops_per_pair = {"blend_fwd": 22.0, "blend_bwd": 80.0}.get(dominant, None)
+        flops_per_pair = BLEND_FLOPS_PER_PAIR.get(dominant, None)
         if flops_per_pair is not None:
             e = float(np.mean([contrib[i] for i in steps_cams]))
             ach = e * flops_per_pair / (stage_ms[dominant] * 1e-3) / 1e12

@@ -96,15 +96,23 @@ typedef struct gs_appearance {
                                  rounded to binary16 and accumulates in fp32. */
 } gs_appearance;
 
-/* Screen-space record of one Gaussian, written by gs_preprocess (48 bytes).
- * Only meaningful where tiles_touched[i] > 0 (other records are not written). */
+/* Screen-space record of one Gaussian, written by gs_preprocess (64 bytes).
+ * Only meaningful where tiles_touched[i] > 0 (other records are not written).
+ * power_min, ext_x and ext_y only let the blend skip work early: below
+ * power_min the alpha is certainly under 1/255 (a margin of 1e-3 in power), and
+ * every pixel centre where the power reaches power_min lies within ext_x / ext_y
+ * of the mean (slightly enlarged bounding box of that ellipse). A Gaussian whose
+ * opacity is below 1/255 gets power_min = +inf and negative extents. */
 typedef struct gs_splat {
     float mean_x, mean_y;             /* projected mean, pixels */
     float conic_a, conic_b, conic_c;  /* inverse 2D covariance [[a, b], [b, c]] */
     float opacity;                    /* activated opacity */
     float color[3];                   /* view-dependent RGB */
-    float depth;                      /* camera-space z (> near_plane) */
+    float power_min;                  /* -ln(255 opacity) - 1e-3 */
+    float ext_x, ext_y;               /* half extents of the alpha >= 1/255 region, pixels */
     int16_t rect[4];                  /* tiles x0, y0, x1, y1 (half-open) */
+    float depth;                      /* camera-space z (> near_plane) */
+    float reserved;                   /* written as 0 */
 } gs_splat;
 
 /* Outputs of gs_preprocess; caller-allocated device arrays. */

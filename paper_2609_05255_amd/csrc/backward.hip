@@ -159,66 +159,55 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
     const int i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= a.n) return;
     const int64_t n = a.n;
-    if (a.tiles_touched[i] == 0) {
-        write_zero_grads(a, i);
-        for (int k = 0; k < GS_SH_COEFFS; ++k) a.dsh[k * n + i] = 0.f;
-        return;
-    }
-    float mu[3], ls[3], q[4];
-    for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
-    for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
-    for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
-    const float logit = a.logits[i];
-    float g9[kAccStride];
-    const float* ap = a.acc + (size_t)i * kAccStride;
-    for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+    // Culled Gaussians take the same store instructions with zeros, so every
+    // gradient plane is written once per wave with whole lines.
+    const bool vis = a.tiles_touched[i] != 0;
     GeoGrad gg;
-    geometry_bwd(a.cam, mu, ls, q, logit, g9, gg);
-
-    // appearance: eq. sh_color_eval with its ReLU
-    const float vx = mu[0] - a.cam.campos[0], vy = mu[1] - a.cam.campos[1], vz = mu[2] - a.cam.campos[2];
-    const float len = sqrtf(vx * vx + vy * vy + vz * vz);
-    const float il = 1.f / len;
-    const float d0 = vx * il, d1 = vy * il, d2 = vz * il;
-    float Y[16];
-    sh_basis16(d0, d1, d2, Y);
+    for (int j = 0; j < 3; ++j) { gg.dmu[j] = 0.f; gg.dls[j] = 0.f; }
+    for (int j = 0; j < 4; ++j) gg.dq[j] = 0.f;
+    gg.dlogit = 0.f;
+    float g9[kAccStride];
+    for (int k = 0; k < kAccStride; ++k) g9[k] = 0.f;
+    float Y[16], gc[3] = {0.f, 0.f, 0.f};
+    for (int k = 0; k < 16; ++k) Y[k] = 0.f;
     const int nb = (a.sh_degree + 1) * (a.sh_degree + 1);
-    float coef[48];
-    float pre0 = 0.5f, pre1 = 0.5f, pre2 = 0.5f;
-    for (int k = 0; k < 16; ++k) {
-        if (k < nb) {
-            coef[3 * k] = a.sh[(3 * k) * n + i];
-            coef[3 * k + 1] = a.sh[(3 * k + 1) * n + i];
-            coef[3 * k + 2] = a.sh[(3 * k + 2) * n + i];
-            pre0 += Y[k] * coef[3 * k];
-            pre1 += Y[k] * coef[3 * k + 1];
-            pre2 += Y[k] * coef[3 * k + 2];
-        } else {
-            coef[3 * k] = coef[3 * k + 1] = coef[3 * k + 2] = 0.f;
-        }
+    if (vis) {
+        float mu[3], ls[3], q[4];
+        for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
+        for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
+        for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
+        const float* ap = a.acc + (size_t)i * kAccStride;
+        for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+        geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
+
+        // appearance: eq. sh_color_eval with its ReLU
+        const float vx = mu[0] - a.cam.campos[0], vy = mu[1] - a.cam.campos[1], vz = mu[2] - a.cam.campos[2];
+        const float len = sqrtf(vx * vx + vy * vy + vz * vz);
+        const float il = 1.f / len;
+        const float d0 = vx * il, d1 = vy * il, d2 = vz * il;
+        sh_basis16(d0, d1, d2, Y);
+        float coef[GS_SH_COEFFS];
+        float pre[3] = {0.5f, 0.5f, 0.5f};
+        for (int k = 0; k < 16; ++k)
+            for (int c = 0; c < 3; ++c) {
+                coef[3 * k + c] = k < nb ? a.sh[(3 * k + c) * n + i] : 0.f;
+                pre[c] += Y[k] * coef[3 * k + c];
+            }
+        for (int c = 0; c < 3; ++c) gc[c] = pre[c] > 0.f ? g9[6 + c] : 0.f;
+        float dY[16];
+        for (int k = 0; k < 16; ++k) dY[k] = coef[3 * k] * gc[0] + coef[3 * k + 1] * gc[1] + coef[3 * k + 2] * gc[2];
+        float dd[3] = {0.f, 0.f, 0.f};
+        sh_basis16_vjp(d0, d1, d2, dY, dd);
+        // d = v / |v|: dv = (dd - d (d . dd)) / |v|
+        const float dot = d0 * dd[0] + d1 * dd[1] + d2 * dd[2];
+        gg.dmu[0] += (dd[0] - d0 * dot) * il;
+        gg.dmu[1] += (dd[1] - d1 * dot) * il;
+        gg.dmu[2] += (dd[2] - d2 * dot) * il;
     }
-    const float gc0 = pre0 > 0.f ? g9[6] : 0.f;
-    const float gc1 = pre1 > 0.f ? g9[7] : 0.f;
-    const float gc2 = pre2 > 0.f ? g9[8] : 0.f;
-    float G[48];
-    sh_basis16_grad(d0, d1, d2, G);
-    float dd0 = 0.f, dd1 = 0.f, dd2 = 0.f;
     for (int k = 0; k < 16; ++k) {
         const bool on = k < nb;
-        a.dsh[(3 * k) * n + i] = on ? Y[k] * gc0 : 0.f;
-        a.dsh[(3 * k + 1) * n + i] = on ? Y[k] * gc1 : 0.f;
-        a.dsh[(3 * k + 2) * n + i] = on ? Y[k] * gc2 : 0.f;
-        const float dY = coef[3 * k] * gc0 + coef[3 * k + 1] * gc1 + coef[3 * k + 2] * gc2;
-        dd0 += dY * G[3 * k];
-        dd1 += dY * G[3 * k + 1];
-        dd2 += dY * G[3 * k + 2];
+        for (int c = 0; c < 3; ++c) a.dsh[(3 * k + c) * n + i] = on ? Y[k] * gc[c] : 0.f;
     }
-    // d = v / |v|: dv = (dd - d (d . dd)) / |v|
-    const float dot = d0 * dd0 + d1 * dd1 + d2 * dd2;
-    gg.dmu[0] += (dd0 - d0 * dot) * il;
-    gg.dmu[1] += (dd1 - d1 * dot) * il;
-    gg.dmu[2] += (dd2 - d2 * dot) * il;
-
     for (int j = 0; j < 3; ++j) { a.dmeans[j * n + i] = gg.dmu[j]; a.dlog_scales[j * n + i] = gg.dls[j]; }
     for (int j = 0; j < 4; ++j) a.dquats[j * n + i] = gg.dq[j];
     a.dlogits[i] = gg.dlogit;

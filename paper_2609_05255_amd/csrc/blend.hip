@@ -44,7 +44,7 @@ __device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp
 
 // One splat record in registers (the fields the blend needs).
 struct SplatReg {
-    float mx, my, ca, cb, cc, op, r, g, b;
+    float mx, my, ca, cb, cc, op, r, g, b, pmin, ex, ey;
     uint32_t id;
 };
 
@@ -53,10 +53,11 @@ __device__ __forceinline__ SplatReg load_splat(const gs_splat* __restrict__ spla
     const float4* p = reinterpret_cast<const float4*>(splats + gid);
     const float4 w0 = p[0];
     const float4 w1 = p[1];
+    const float4 w2 = p[2];
     SplatReg s;
     s.mx = w0.x; s.my = w0.y; s.ca = w0.z; s.cb = w0.w;
     s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w;
-    s.b = reinterpret_cast<const float*>(splats + gid)[8];
+    s.b = w2.x; s.pmin = w2.y; s.ex = w2.z; s.ey = w2.w;
     s.id = gid;
     return s;
 }
@@ -66,15 +67,14 @@ __device__ __forceinline__ float bcast(float v, int j)
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));
 }
 
-__device__ __forceinline__ SplatReg bcast(const SplatReg& s, int j)
+// The fields the per-pixel work needs (mean and extents are broadcast first,
+// for the wave's overlap test).
+__device__ __forceinline__ void bcast_rest(const SplatReg& s, int j, SplatReg& t)
 {
-    SplatReg t;
-    t.mx = bcast(s.mx, j); t.my = bcast(s.my, j);
     t.ca = bcast(s.ca, j); t.cb = bcast(s.cb, j); t.cc = bcast(s.cc, j);
     t.op = bcast(s.op, j);
     t.r = bcast(s.r, j); t.g = bcast(s.g, j); t.b = bcast(s.b, j);
-    t.id = (uint32_t)__builtin_amdgcn_readlane((int)s.id, j);
-    return t;
+    t.pmin = bcast(s.pmin, j);
 }
 
 // power(dy) = -(a dx^2 + c dy^2)/2 - b dx dy = q0 + dy (q1 + dy q2) for one column.
@@ -130,6 +130,12 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
     const int y0 = ty * kTile + (threadIdx.x >> 4);
     const float px = (float)x + 0.5f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
+    // box of this wave's pixel centres: 16 columns, rows 4w .. 4w + 3 + (16/kPix)(kPix - 1)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const float box_cx = (float)(tx * kTile) + 8.f, box_hx = 7.5f;
+    const float box_lo = (float)(ty * kTile + 4 * wave) + 0.5f;
+    const float box_hi = box_lo + (float)(3 + kRowStep * (kPix - 1));
+    const float box_cy = 0.5f * (box_lo + box_hi), box_hy = 0.5f * (box_hi - box_lo);
 
     float T[kPix], C0[kPix], C1[kPix], C2[kPix], py[kPix];
     uint32_t last[kPix];
@@ -153,14 +159,21 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
         if (b + kWave + lane < end) nxt = load_splat(splats, values[b + kWave + lane]);
         const int cnt = (int)min((uint32_t)kWave, end - b);
         for (int j = 0; j < cnt; ++j) {
-            const SplatReg s = bcast(cur, j);
+            SplatReg s;
+            s.mx = bcast(cur.mx, j);
+            s.my = bcast(cur.my, j);
+            s.ex = bcast(cur.ex, j);
+            s.ey = bcast(cur.ey, j);
+            // the splat reaches alpha >= 1/255 nowhere in this wave's pixels
+            if (fabsf(s.mx - box_cx) > s.ex + box_hx || fabsf(s.my - box_cy) > s.ey + box_hy) continue;
+            bcast_rest(cur, j, s);
             const float dx = px - s.mx;
             const Quad q = column_quad(s, dx);
 #pragma unroll
             for (int k = 0; k < kPix; ++k) {
                 if (!live[k]) continue;
                 const float power = quad_power(q, py[k] - s.my);
-                if (power > 0.f) continue;
+                if (power > 0.f || power < s.pmin) continue;
                 const float alpha = fminf(kAlphaMax, s.op * exp_fast(power));
                 if (alpha < kAlphaMin) continue;
                 const float Tn = T[k] * (1.f - alpha);
@@ -272,7 +285,11 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
         const int cnt = (int)min((uint32_t)kWave, stop - b);
         for (int j = cnt - 1; j >= 0; --j) {
             const uint32_t pos = b + (uint32_t)j;
-            const SplatReg s = bcast(cur, j);
+            SplatReg s;
+            s.mx = bcast(cur.mx, j);
+            s.my = bcast(cur.my, j);
+            bcast_rest(cur, j, s);
+            s.id = (uint32_t)__builtin_amdgcn_readlane((int)cur.id, j);
             const float dx = px - s.mx;
             const Quad q = column_quad(s, dx);
             float a_dmx = 0.f, a_dmy = 0.f, a_dca = 0.f, a_dcb = 0.f, a_dcc = 0.f, a_dop = 0.f;
@@ -283,12 +300,14 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                 if (pos >= last[k]) continue;
                 const float dy = py[k] - s.my;
                 const float power = quad_power(q, dy);
-                if (power > 0.f) continue;
+                if (power > 0.f || power < s.pmin) continue;
                 const float G = exp_fast(power);
                 const float alpha = fminf(kAlphaMax, s.op * G);
                 if (alpha < kAlphaMin) continue;
                 any = true;
-                const float inv = 1.f / (1.f - alpha);
+                // hardware reciprocal (1 ulp): T is recovered over a few hundred
+                // splats, so its relative error stays near 1e-5
+                const float inv = __builtin_amdgcn_rcpf(1.f - alpha);
                 T[k] *= inv;                                // transmittance in front of this splat
                 const float w = alpha * T[k];
                 a_c0 = __fmaf_rn(w, g0[k], a_c0);

@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include <algorithm>
@@ -38,11 +39,15 @@ inline Cam make_cam(const gs_camera& c) {
     return k;
 }
 
-// Splat record as three 16-byte words (layout of gs_splat).
+// Splat record as four 16-byte words (layout of gs_splat).
 //  w0 = mean_x, mean_y, conic_a, conic_b
 //  w1 = conic_c, opacity, color r, color g
-//  w2 = color b, depth, rect (x0 | y0 << 16), rect (x1 | y1 << 16)
-static_assert(sizeof(gs_splat) == 48, "splat record must be 48 bytes");
+//  w2 = color b, power_min, ext_x, ext_y
+//  w3 = rect (x0 | y0 << 16), rect (x1 | y1 << 16), depth, 0
+static_assert(sizeof(gs_splat) == 64, "splat record must be 64 bytes");
+constexpr int kSplatRectWord = 12;   // float offset of the packed rectangle
+static_assert(offsetof(gs_splat, rect) == 4 * kSplatRectWord, "rectangle offset");
+static_assert(offsetof(gs_splat, power_min) == 36 && offsetof(gs_splat, depth) == 56, "record layout");
 
 // Per-Gaussian screen-space gradient accumulator written by the blend backward.
 // Stride 9 floats: dmean_x, dmean_y, dconic_a, dconic_b, dconic_c, dopacity, dcolor rgb.

@@ -19,6 +19,7 @@ namespace {
 struct Geo {
     bool visible, clamp_x, clamp_y;
     float mx, my, ca, cb, cc, op, depth;
+    float var_x, var_y;     // diagonal of the screen-space covariance (with the low-pass)
     int x0, y0, x1, y1;
     uint32_t tiles;
 };
@@ -95,6 +96,8 @@ __device__ __forceinline__ void geometry(const Cam& c, const float mu[3], const 
     g.ca = c11 / det;
     g.cb = -c01 / det;
     g.cc = c00 / det;
+    g.var_x = c00;
+    g.var_y = c11;
 
     const float mid = 0.5f * (c00 + c11);
     float disc = mid * mid - det;
@@ -136,14 +139,36 @@ struct PreArgs {
     uint32_t* block_pairs;
 };
 
+// Early-skip fields of the blend: alpha = min(0.99, o e^power) stays below
+// 1/255 wherever power < -ln(255 o), so power_min takes that bound less a
+// margin of 1e-3 (far above the rounding of either side); the pixels with
+// power >= power_min lie in the ellipse d^T Q d <= -2 power_min, whose bounding
+// box has half extents sqrt(-2 power_min Sigma_xx), sqrt(-2 power_min Sigma_yy),
+// enlarged by 0.1% + 0.01 px.
+__device__ __forceinline__ void skip_fields(const Geo& g, float& pmin, float& ex, float& ey)
+{
+    if (!(255.f * g.op > 1.f)) {
+        pmin = __builtin_inff();
+        ex = ey = -1e30f;
+        return;
+    }
+    pmin = -logf(255.f * g.op) - 1e-3f;
+    const float r2 = -2.f * pmin;
+    ex = sqrtf(r2 * g.var_x) * 1.001f + 0.01f;
+    ey = sqrtf(r2 * g.var_y) * 1.001f + 0.01f;
+}
+
 __device__ __forceinline__ void store_splat(gs_splat* dst, const Geo& g, const float col[3])
 {
+    float pmin, ex, ey;
+    skip_fields(g, pmin, ex, ey);
     float4* p = reinterpret_cast<float4*>(dst);
     p[0] = make_float4(g.mx, g.my, g.ca, g.cb);
     p[1] = make_float4(g.cc, g.op, col[0], col[1]);
+    p[2] = make_float4(col[2], pmin, ex, ey);
     const uint32_t r01 = (uint32_t)(g.x0 & 0xFFFF) | ((uint32_t)g.y0 << 16);
     const uint32_t r23 = (uint32_t)(g.x1 & 0xFFFF) | ((uint32_t)g.y1 << 16);
-    p[2] = make_float4(col[2], g.depth, __uint_as_float(r01), __uint_as_float(r23));
+    p[3] = make_float4(__uint_as_float(r01), __uint_as_float(r23), g.depth, 0.f);
 }
 
 // Sum of a u32 over the workgroup; result valid in thread 0.

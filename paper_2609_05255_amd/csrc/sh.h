@@ -62,4 +62,32 @@ __device__ __forceinline__ void sh_basis16_grad(float x, float y, float z, float
     G[45] = 3.f * kSH3a * (xx - yy); G[46] = -6.f * kSH3a * x * y; G[47] = 0.f;
 }
 
+// dd += sum_k dY[k] * grad Y_k(x, y, z), without materialising the 16x3 gradient.
+__device__ __forceinline__ void sh_basis16_vjp(float x, float y, float z, const float dY[16], float dd[3])
+{
+    const float xx = x * x, yy = y * y, zz = z * z;
+    float gx = 0.f, gy = 0.f, gz = 0.f;
+    gy += -kSH1 * dY[1];
+    gz += kSH1 * dY[2];
+    gx += -kSH1 * dY[3];
+    gx += kSH2a * y * dY[4];               gy += kSH2a * x * dY[4];
+    gy += -kSH2a * z * dY[5];              gz += -kSH2a * y * dY[5];
+    gx += -2.f * kSH2b * x * dY[6];        gy += -2.f * kSH2b * y * dY[6];       gz += 4.f * kSH2b * z * dY[6];
+    gx += -kSH2a * z * dY[7];              gz += -kSH2a * x * dY[7];
+    gx += 2.f * kSH2c * x * dY[8];         gy += -2.f * kSH2c * y * dY[8];
+    gx += 6.f * kSH3a * x * y * dY[9];     gy += 3.f * kSH3a * (xx - yy) * dY[9];
+    gx += kSH3b * y * z * dY[10];          gy += kSH3b * x * z * dY[10];         gz += kSH3b * x * y * dY[10];
+    gx += -2.f * kSH3c * x * y * dY[11];   gy += kSH3c * (4.f * zz - xx - 3.f * yy) * dY[11];
+    gz += 8.f * kSH3c * y * z * dY[11];
+    gx += -6.f * kSH3d * x * z * dY[12];   gy += -6.f * kSH3d * y * z * dY[12];
+    gz += kSH3d * (6.f * zz - 3.f * xx - 3.f * yy) * dY[12];
+    gx += kSH3c * (4.f * zz - 3.f * xx - yy) * dY[13];
+    gy += -2.f * kSH3c * x * y * dY[13];   gz += 8.f * kSH3c * x * z * dY[13];
+    gx += 2.f * kSH3e * x * z * dY[14];    gy += -2.f * kSH3e * y * z * dY[14];  gz += kSH3e * (xx - yy) * dY[14];
+    gx += 3.f * kSH3a * (xx - yy) * dY[15]; gy += -6.f * kSH3a * x * y * dY[15];
+    dd[0] += gx;
+    dd[1] += gy;
+    dd[2] += gz;
+}
+
 }  // namespace gsr

@@ -278,7 +278,7 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
             g = order[i];
             c = tiles_touched[g];
             if (c != 0) {
-                const float2 rr = *reinterpret_cast<const float2*>(reinterpret_cast<const float*>(splats + g) + 10);
+                const float2 rr = *reinterpret_cast<const float2*>(reinterpret_cast<const float*>(splats + g) + kSplatRectWord);
                 const uint32_t r01 = __float_as_uint(rr.x), r23 = __float_as_uint(rr.y);
                 org = r01;
                 w = (r23 & 0xFFFFu) - (r01 & 0xFFFFu);

@@ -23,7 +23,7 @@ GS_OK, GS_ERR_INVALID_ARG, GS_ERR_CAPACITY, GS_ERR_DEVICE, GS_ERR_UNSUPPORTED = 
 GS_APP_SH3, GS_APP_LATENT_MLP = 0, 1
 KERNEL_NAMES = ["preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
                 "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce"]
-SPLAT_BYTES = 48
+SPLAT_BYTES = 64
 MLP_WEIGHTS = 1664
 
 
@@ -256,11 +256,12 @@ class Frame:
 
     def splat_fields(self) -> dict:
         """Host copy of the splat records, split into fields."""
-        raw = self.splats.view(-1, 12).cpu()
+        raw = self.splats.view(-1, 16).cpu()
         f = raw.numpy()
-        rect = raw.view(torch.int32).numpy()[:, 10:12]
+        rect = raw.view(torch.int32).numpy()[:, 12:14]
         r01, r23 = rect[:, 0].astype("int64") & 0xFFFFFFFF, rect[:, 1].astype("int64") & 0xFFFFFFFF
         import numpy as np
         rects = np.stack([r01 & 0xFFFF, r01 >> 16, r23 & 0xFFFF, r23 >> 16]).astype(np.int32)
         return dict(mean2d=f[:, 0:2].T.copy(), conic=f[:, 2:5].T.copy(), opacity=f[:, 5].copy(),
-                    color=f[:, 6:9].T.copy(), depth=f[:, 9].copy(), rect=rects)
+                    color=f[:, 6:9].T.copy(), power_min=f[:, 9].copy(), ext=f[:, 10:12].T.copy(),
+                    depth=f[:, 14].copy(), rect=rects)

@@ -88,6 +88,26 @@ def compare_preprocess(gpu, ref, color_atol=2e-6):
         assert np.array_equal(s[k][:, vis].astype(np.float32), ref[k][:, vis].astype(np.float32)), k
     assert np.array_equal(s["opacity"][vis], ref["opacity"][vis].astype(np.float32))
     assert np.abs(s["color"][:, vis] - ref["color"][:, vis]).max() <= color_atol
+    check_skip_fields(s, ref, vis)
+
+
+def check_skip_fields(s, ref, vis):
+    """The blend's early-skip fields must be conservative: power_min no larger
+    than the exact -ln(255 o), and the extents no smaller than the exact
+    bounding box of the ellipse where the power reaches power_min (fp64)."""
+    o = ref["opacity"][vis]
+    live = 255.0 * o > 1.0 + 1e-6
+    pmin = s["power_min"][vis].astype(np.float64)
+    assert np.all(np.isinf(pmin[~live]) & (pmin[~live] > 0))
+    exact = -np.log(255.0 * o[live])
+    assert np.all(pmin[live] <= exact - 5e-4)
+    a, b, c = (ref["conic"][k, vis][live] for k in range(3))
+    det = a * c - b * b
+    r2 = -2.0 * pmin[live]
+    ex_exact = np.sqrt(r2 * c / det)
+    ey_exact = np.sqrt(r2 * a / det)
+    assert np.all(s["ext"][0, vis][live] >= ex_exact)
+    assert np.all(s["ext"][1, vis][live] >= ey_exact)
 
 
 def compare_lists(gpu, ref_values, ref_tiles, ref_ranges):

@@ -292,8 +292,11 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             s.id = (uint32_t)__builtin_amdgcn_readlane((int)cur.id, j);
             const float dx = px - s.mx;
             const Quad q = column_quad(s, dx);
-            float a_dmx = 0.f, a_dmy = 0.f, a_dca = 0.f, a_dcb = 0.f, a_dcc = 0.f, a_dop = 0.f;
-            float a_c0 = 0.f, a_c1 = 0.f, a_c2 = 0.f;
+            // per-lane sums over its pixels: colour gradient, opacity gradient, and
+            // the moments of dL/dpower (dpow dx, dpow dy, dpow dx^2, dpow dx dy,
+            // dpow dy^2) from which dmean2d and dconic follow once per splat
+            float a_c0 = 0.f, a_c1 = 0.f, a_c2 = 0.f, a_dop = 0.f;
+            float m_x = 0.f, m_y = 0.f, m_xx = 0.f, m_xy = 0.f, m_yy = 0.f;
             bool any = false;
 #pragma unroll
             for (int k = 0; k < kPix; ++k) {
@@ -302,7 +305,8 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                 const float power = quad_power(q, dy);
                 if (power > 0.f || power < s.pmin) continue;
                 const float G = exp_fast(power);
-                const float alpha = fminf(kAlphaMax, s.op * G);
+                const float oG = s.op * G;
+                const float alpha = fminf(kAlphaMax, oG);
                 if (alpha < kAlphaMin) continue;
                 any = true;
                 // hardware reciprocal (1 ulp): T is recovered over a few hundred
@@ -313,38 +317,41 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                 a_c0 = __fmaf_rn(w, g0[k], a_c0);
                 a_c1 = __fmaf_rn(w, g1[k], a_c1);
                 a_c2 = __fmaf_rn(w, g2[k], a_c2);
-                const float dalpha = (T[k] * s.r - S0[k] * inv) * g0[k] + (T[k] * s.g - S1[k] * inv) * g1[k] +
-                                     (T[k] * s.b - S2[k] * inv) * g2[k];
+                const float cg = __fmaf_rn(s.b, g2[k], __fmaf_rn(s.g, g1[k], s.r * g0[k]));
+                const float sg = __fmaf_rn(S2[k], g2[k], __fmaf_rn(S1[k], g1[k], S0[k] * g0[k]));
+                const float dalpha = __fmaf_rn(T[k], cg, -inv * sg);
                 S0[k] = __fmaf_rn(s.r, w, S0[k]);
                 S1[k] = __fmaf_rn(s.g, w, S1[k]);
                 S2[k] = __fmaf_rn(s.b, w, S2[k]);
-                if (s.op * G < kAlphaMax) {                 // below the cap alpha = o G
+                if (oG < kAlphaMax) {                       // below the cap alpha = o G
                     a_dop = __fmaf_rn(G, dalpha, a_dop);
                     const float dpow = alpha * dalpha;
-                    a_dmx = __fmaf_rn(dpow, s.ca * dx + s.cb * dy, a_dmx);
-                    a_dmy = __fmaf_rn(dpow, s.cc * dy + s.cb * dx, a_dmy);
-                    a_dca = __fmaf_rn(-0.5f * dpow, dx * dx, a_dca);
-                    a_dcb = __fmaf_rn(-dpow, dx * dy, a_dcb);
-                    a_dcc = __fmaf_rn(-0.5f * dpow, dy * dy, a_dcc);
+                    const float pdx = dpow * dx, pdy = dpow * dy;
+                    m_x += pdx;
+                    m_y += pdy;
+                    m_xx = __fmaf_rn(pdx, dx, m_xx);
+                    m_xy = __fmaf_rn(pdx, dy, m_xy);
+                    m_yy = __fmaf_rn(pdy, dy, m_yy);
                 }
             }
             if (__ballot(any) == 0) continue;
-            a_dmx = wave_sum_to_lane63(a_dmx);
-            a_dmy = wave_sum_to_lane63(a_dmy);
-            a_dca = wave_sum_to_lane63(a_dca);
-            a_dcb = wave_sum_to_lane63(a_dcb);
-            a_dcc = wave_sum_to_lane63(a_dcc);
+            m_x = wave_sum_to_lane63(m_x);
+            m_y = wave_sum_to_lane63(m_y);
+            m_xx = wave_sum_to_lane63(m_xx);
+            m_xy = wave_sum_to_lane63(m_xy);
+            m_yy = wave_sum_to_lane63(m_yy);
             a_dop = wave_sum_to_lane63(a_dop);
             a_c0 = wave_sum_to_lane63(a_c0);
             a_c1 = wave_sum_to_lane63(a_c1);
             a_c2 = wave_sum_to_lane63(a_c2);
             if (lane == kWave - 1) {
+                // power = -(a dx^2 + c dy^2)/2 - b dx dy with dx = px - mean_x
                 float* a = acc + (size_t)s.id * kAccStride;
-                atomicAdd(a + 0, a_dmx);
-                atomicAdd(a + 1, a_dmy);
-                atomicAdd(a + 2, a_dca);
-                atomicAdd(a + 3, a_dcb);
-                atomicAdd(a + 4, a_dcc);
+                atomicAdd(a + 0, __fmaf_rn(s.ca, m_x, s.cb * m_y));
+                atomicAdd(a + 1, __fmaf_rn(s.cc, m_y, s.cb * m_x));
+                atomicAdd(a + 2, -0.5f * m_xx);
+                atomicAdd(a + 3, -m_xy);
+                atomicAdd(a + 4, -0.5f * m_yy);
                 atomicAdd(a + 5, a_dop);
                 atomicAdd(a + 6, a_c0);
                 atomicAdd(a + 7, a_c1);

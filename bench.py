@@ -14,6 +14,7 @@ CPU oracle timed on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -32,6 +33,42 @@ FP32_VECTOR_PEAK_TFLOPS = 157.3
 # backward: quadratic form 11, exp 2, alpha 2, transmittance 2, dcolour 4, dalpha 15,
 # suffix sum 6, dopacity + dmean2d + dconic 20.
 BLEND_FLOPS_PER_PAIR = {"blend_fwd": 24.0, "blend_bwd": 62.0}
+
+
+# HBM traffic of a kernel, from memory-counter runs summarised under profiles/
+# (FETCH_SIZE and WRITE_SIZE per dispatch, each scaled by what the counter reads
+# for a copy of known size). Each summary records a hash of the kernel's
+# sources; once they change, the recorded figure no longer describes the
+# kernel and the traffic is reported as null.
+TRAFFIC_SUMMARIES = {("blend_bwd", "paper_sh3", "sh3"): "profiles/blend_bwd_paper_sh3_traffic.txt"}
+KERNEL_SOURCES = {"blend_bwd": ("paper_2609_05255_amd/csrc/blend.hip", "paper_2609_05255_amd/csrc/gs_internal.h")}
+
+
+def source_hash(kernel: str) -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kernel: str, config: str, kind: str) -> float | None:
+    """Bytes per launch from the committed counter summary, or None."""
+    rel = TRAFFIC_SUMMARIES.get((kernel, config, kind))
+    if rel is None or not os.path.exists(os.path.join(ROOT, rel)):
+        return None
+    fields = {}
+    with open(os.path.join(ROOT, rel)) as f:
+        for line in f:
+            if ":" in line and not line.startswith(" "):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("source_hash") != source_hash(kernel):
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def parse():
@@ -53,7 +90,9 @@ def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int
     """HBM bytes a launch must move at minimum (per launch, averaged over cameras)."""
     app = 4 * 3 * (sh_degree + 1) ** 2 if kind == "sh3" else 28
     if kernel == "preprocess":
-        # params 44 B + tiles 4 B + depth key 4 B per Gaussian; appearance + 48 B splat per visible one
+        # params 44 B + tiles 4 B + depth key 4 B per Gaussian; appearance + 48 B of projected splat
+        # (mean 8, conic 12, opacity 4, colour 12, rectangle 8, depth 4) per visible one; the record
+        # written is 64 B, the rest being the blend's early-skip fields
         return n * (44 + 8) + vis * (app + 48)
     if kernel == "preprocess_bwd":
         # tiles 4 B + dense gradient writes per Gaussian; params, accumulators and appearance per visible one
@@ -163,6 +202,11 @@ def main():
             roofline = {"kernel": dominant, "bound": "alu", "achieved": round(ach, 3),
                         "peak": FP32_VECTOR_PEAK_TFLOPS, "unit": "TFLOP/s",
                         "frac": round(ach / FP32_VECTOR_PEAK_TFLOPS, 4), "traffic": None}
+    if roofline is not None and dominant in KERNEL_SOURCES:
+        tb = recorded_traffic(dominant, cfg.name, kind)
+        roofline["traffic"] = None if tb is None else round(tb)
+        roofline["traffic_unit"] = "bytes per launch"
+        roofline["source_hash"] = source_hash(dominant)
     hbm_all = {}
     for k, b in hbm_kernels.items():
         if k in stage_ms and stage_ms[k] > 0:

@@ -29,12 +29,15 @@ def kind_id(kind: str) -> int:
     return gs.GS_APP_SH3 if kind == "sh3" else gs.GS_APP_LATENT_MLP
 
 
-def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None):
+def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None, extras=True):
+    """extras=False runs the launch configuration of the benchmark: no tile-id
+    output and no dmean2d output."""
     st = gs.SceneTensors(scene)
     cs = gs.camera_struct(cam)
     if capacity is None:
         capacity = 1 << 16
-    fr = gs.Frame(scene.n, cam.width, cam.height, kind_id(kind), capacity, want_tile_ids=True, want_dmean2d=True)
+    fr = gs.Frame(scene.n, cam.width, cam.height, kind_id(kind), capacity, want_tile_ids=extras,
+                  want_dmean2d=extras)
     g, app = st.gaussians(), st.appearance(kind_id(kind), sh_degree)
     P = gs.gs_preprocess(cs, g, app, fr.pre, fr.workspace, fr.ws_bytes)
     if P > capacity:
@@ -45,7 +48,8 @@ def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None):
             raise AssertionError("bin_sort accepted too many pairs")
         except gs.GsError as e:
             assert e.status == gs.GS_ERR_CAPACITY
-        fr = gs.Frame(scene.n, cam.width, cam.height, kind_id(kind), int(P), want_tile_ids=True, want_dmean2d=True)
+        fr = gs.Frame(scene.n, cam.width, cam.height, kind_id(kind), int(P), want_tile_ids=extras,
+                      want_dmean2d=extras)
         P = gs.gs_preprocess(cs, g, app, fr.pre, fr.workspace, fr.ws_bytes)
     gs.gs_bin_sort(cs, fr.pre, scene.n, P, fr.capacity, fr.values, fr.tile_ids, fr.ranges, fr.workspace, fr.ws_bytes)
     gs.gs_render_fwd(cs, fr.pre, scene.n, fr.values, fr.ranges, fr.image, fr.final_T, fr.n_contrib)
@@ -56,7 +60,7 @@ def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None):
     out["tiles"] = fr.tiles_touched.cpu().numpy()[: scene.n]
     out["depth_key"] = fr.depth_key.cpu().numpy().view(np.uint32)[: scene.n]
     out["values"] = fr.values.cpu().numpy()[:P]
-    out["tile_ids"] = fr.tile_ids.cpu().numpy()[:P]
+    out["tile_ids"] = fr.tile_ids.cpu().numpy()[:P] if extras else None
     out["ranges"] = fr.ranges.cpu().numpy().reshape(-1, 2).astype(np.int64)
     out["image"] = fr.image.cpu().numpy().astype(np.float64)
     out["final_T"] = fr.final_T.cpu().numpy().astype(np.float64)
@@ -64,7 +68,8 @@ def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None):
     out["splat"] = fr.splat_fields() if scene.n > 0 else None
     if dL_dimage is not None:
         out["grads"] = {k: getattr(fr, k).cpu().numpy().astype(np.float64)[..., : scene.n]
-                        for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dmean2d")}
+                        for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dmean2d")
+                        if getattr(fr, k) is not None}
         if kind == "sh3":
             out["grads"]["dsh"] = fr.dsh.cpu().numpy().astype(np.float64)[:, : scene.n]
         else:
@@ -115,6 +120,39 @@ def compare_lists(gpu, ref_values, ref_tiles, ref_ranges):
     assert np.array_equal(gpu["values"].astype(np.int64), ref_values.astype(np.int64))
     assert np.array_equal(gpu["tile_ids"].astype(np.int64), ref_tiles.astype(np.int64))
     assert np.array_equal(gpu["ranges"], ref_ranges)
+
+
+def tile_of_ranges(ranges, P):
+    """Tile id of every list position, after checking that the ranges cut
+    [0, P) into consecutive pieces in tile order."""
+    r = np.asarray(ranges, np.int64).reshape(-1, 2)
+    assert r[0, 0] == 0 and r[-1, 1] == P
+    assert np.all(r[:, 1] >= r[:, 0])
+    assert np.array_equal(r[1:, 0], r[:-1, 1])
+    return np.repeat(np.arange(r.shape[0], dtype=np.int64), r[:, 1] - r[:, 0])
+
+
+def check_list_properties(values, tile_of, tiles_touched, rect, depth_key, tiles_x):
+    """The sorted pair list at any size, without sorting it again. With the
+    per-Gaussian tile counts and rectangles already known to be right, these
+    properties admit exactly one list: every Gaussian appears as often as it
+    touches tiles, each time with a tile inside its rectangle, and the
+    (tile, depth key, index) triples strictly increase along the list, so no
+    pair repeats and the order is the sort order."""
+    v = np.asarray(values, np.int64)
+    t = np.asarray(tile_of, np.int64)
+    n = tiles_touched.size
+    assert v.size == t.size == int(tiles_touched.astype(np.int64).sum())
+    if v.size == 0:
+        return
+    assert v.min() >= 0 and v.max() < n
+    assert np.array_equal(np.bincount(v, minlength=n), tiles_touched.astype(np.int64))
+    tx, ty = t % tiles_x, t // tiles_x
+    r = rect.astype(np.int64)
+    assert np.all((r[0, v] <= tx) & (tx < r[2, v]) & (r[1, v] <= ty) & (ty < r[3, v]))
+    d = depth_key.astype(np.int64)[v]
+    dt, dd, di = np.diff(t), np.diff(d), np.diff(v)
+    assert np.all((dt > 0) | ((dt == 0) & ((dd > 0) | ((dd == 0) & (di > 0)))))
 
 
 MLP_ATOL = 2e-3                      # decoder colours/images vs the exact (fp64) decoder

@@ -214,31 +214,20 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
     if (a.dmean2d) { a.dmean2d[i] = g9[0]; a.dmean2d[n + i] = g9[1]; }
 }
 
-// Latent + MLP backward. Grid-stride over chunks of 256 Gaussians so that the
-// workgroup count, and with it the number of partial weight gradients, stays
-// bounded. Per wave and tile of 16 Gaussians: recompute the decoder, delta3 =
-// dL/dc * s (1 - s), scale it by a power of two so that its largest magnitude
-// lies in [2^9, 2^10) (exact, removed again in fp32), then dH2, dH1 and dX on
-// the matrix cores in registers and dW3, dW2, dW1 from LDS-transposed
-// fragments with the tile's Gaussians as the reduction dimension. Every
-// gradient operand is passed as two binary16 parts (hi + lo).
-__global__ __launch_bounds__(kBlock) void k_preprocess_bwd_latent(BwdArgs a)
+// Latent + MLP backward: geometry as for SH3, then per tile of 16 Gaussians
+// the decoder is recomputed and differentiated on the matrix cores (mlp.h):
+// the latent gradient, the gradient into the view direction (chained into the
+// mean), and this workgroup's sum of the weight gradients, written as one
+// partial per workgroup (summed in a fixed order by k_mlp_reduce).
+__global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
 {
-    __shared__ MlpWeights W;
-    __shared__ MlpInputs X[kBlock / kWave];
-    __shared__ MlpBwdTile TT[kBlock / kWave];
-    mlp_load_weights(a.mlp_w, W);
+    __shared__ MlpFrags W;
+    __shared__ MlpWaveStage ST[kBlock / kWave];
+    mlp_load_frags(a.mlp_w, W, true);
     const int wave = threadIdx.x >> 6, lane = __lane_id();
-    const int r = lane & 15, g4 = lane >> 4, kq = 4 * g4;
-    MlpInputs& XI = X[wave];
-    MlpBwdTile& T = TT[wave];
-    for (int e = lane; e < 2 * 16 * kP16; e += kWave) (&T.d3t[0][0][0])[e] = (_Float16)0.f;
-    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
-    float4_t aw1[2][2], aw2[2][2], aw3[2];
-    for (int u = 0; u < 2; ++u) {
-        aw3[u] = zero;
-        for (int v = 0; v < 2; ++v) { aw1[u][v] = zero; aw2[u][v] = zero; }
-    }
+    MlpWaveStage& st = ST[wave];
+    MlpGradAcc acc;
+    mlp_grad_zero(acc);
     const int64_t n = a.n;
     const int64_t nchunks = div_up(n, kBlock);
     for (int64_t chunk = blockIdx.x; chunk < nchunks; chunk += gridDim.x) {
@@ -249,138 +238,44 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_latent(BwdArgs a)
             write_zero_grads(a, (int)i);
             for (int c = 0; c < GS_LATENT_DIM; ++c) a.dlatent[c * n + i] = 0.f;
         }
-        float mu[3] = {0.f, 0.f, 0.f}, d[3] = {0.f, 0.f, 0.f}, g9[kAccStride];
+        // decoder part first: it needs the view direction and the colour gradient
+        float d[3] = {0.f, 0.f, 0.f}, dc[3] = {0.f, 0.f, 0.f};
         float len = 1.f;
-        GeoGrad gg;
         if (valid) {
-            float ls[3], q[4];
+            float mu[3];
             for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
-            for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
-            for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
-            const float* ap = a.acc + (size_t)i * kAccStride;
-            for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
-            geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
             const float vx = mu[0] - a.cam.campos[0], vy = mu[1] - a.cam.campos[1], vz = mu[2] - a.cam.campos[2];
             len = sqrtf(vx * vx + vy * vy + vz * vz);
             d[0] = vx / len;
             d[1] = vy / len;
             d[2] = vz / len;
-        } else {
-            for (int k = 0; k < kAccStride; ++k) g9[k] = 0.f;
+            const float* ap = a.acc + (size_t)i * kAccStride;
+            for (int ch = 0; ch < 3; ++ch) dc[ch] = ap[6 + ch];
         }
-        mlp_stage_lane(XI, valid, a.latent, n, i, d);
+        mlp_stage_row(st, valid, a.latent, n, i, d, dc);
+        // the chunk's gradient scale (a power of two, see mlp_chunk_exponent)
+        const float m = wave_max(fmaxf(fmaxf(fabsf(dc[0]), fabsf(dc[1])), fabsf(dc[2])));
+        mlp_grad_rescale(acc, mlp_chunk_exponent(m, acc.se));
+        const float scale = ldexpf(1.f, acc.se), inv = ldexpf(1.f, -acc.se);
         wave_lds_sync();
-        float dxo[GS_MLP_IN];
-        for (int c = 0; c < GS_MLP_IN; ++c) dxo[c] = 0.f;
         const uint64_t vis = __ballot(valid);
+        const int64_t base = chunk * kBlock + (threadIdx.x & ~(kWave - 1));
         for (int t = 0; t < kWave / 16; ++t) {
             if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
-            float4_t h1[2], h2[2], o;
-            mlp_tile_forward(W, XI, t, h1, h2, o);
-            // output gradient of the tile's Gaussian r, in lanes 0..15
-            const int src = 16 * t + r;
-            float del[3];
-            for (int c = 0; c < 3; ++c) {
-                const float dc = __shfl(g9[6 + c], src);
-                const float sgm = sigmoid_fast(o[c]);
-                del[c] = lane < 16 ? dc * sgm * (1.f - sgm) : 0.f;
-            }
-            float m = fmaxf(fabsf(del[0]), fmaxf(fabsf(del[1]), fabsf(del[2])));
-            for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-            int ex = 0;
-            if (m > 0.f) frexpf(m, &ex);
-            const int se = min(10 - ex, 100);
-            const float scale = m > 0.f ? ldexpf(1.f, se) : 1.f;
-            const float inv = m > 0.f ? ldexpf(1.f, -se) : 1.f;
-            half4_t d3b[2];
-            for (int c = 0; c < 3; ++c) {
-                d3b[0][c] = half_hi(del[c] * scale);
-                d3b[1][c] = half_lo(del[c] * scale);
-            }
-            d3b[0][3] = d3b[1][3] = (_Float16)0.f;
-            if (lane < 16)
-                for (int p = 0; p < 2; ++p)
-                    for (int c = 0; c < 3; ++c) T.d3t[p][c][r] = d3b[p][c];
-            // dH2^T = W3^T delta3^T, masked by relu'(h2)
-            half4_t g2h[2][2], g1h[2][2];   // [hi/lo][K-half]
-            for (int b = 0; b < 2; ++b) {
-                const half4_t w = lds_half4(&W.w3t[16 * b + r][kq]);
-                float4_t v = mfma16(w, d3b[0], zero);
-                v = mfma16(w, d3b[1], v);
-                for (int e = 0; e < 4; ++e) {
-                    const float m2 = h2[b][e] > 0.f ? v[e] : 0.f;
-                    g2h[0][b][e] = half_hi(m2);
-                    g2h[1][b][e] = half_lo(m2);
-                }
-            }
-            // dH1^T = W2^T dH2^T, masked by relu'(h1)
-            for (int b = 0; b < 2; ++b) {
-                const half4_t w0 = lds_half4(&W.w2t[16 * b + r][kq]), w1 = lds_half4(&W.w2t[16 * b + r][16 + kq]);
-                float4_t v = zero;
-                for (int p = 0; p < 2; ++p) {
-                    v = mfma16(w0, g2h[p][0], v);
-                    v = mfma16(w1, g2h[p][1], v);
-                }
-                for (int e = 0; e < 4; ++e) {
-                    const float m1 = h1[b][e] > 0.f ? v[e] : 0.f;
-                    g1h[0][b][e] = half_hi(m1);
-                    g1h[1][b][e] = half_lo(m1);
-                }
-            }
-            // dX^T = W1^T dH1^T
-            for (int b = 0; b < 2; ++b) {
-                const half4_t w0 = lds_half4(&W.w1t[16 * b + r][kq]), w1 = lds_half4(&W.w1t[16 * b + r][16 + kq]);
-                float4_t v = zero;
-                for (int p = 0; p < 2; ++p) {
-                    v = mfma16(w0, g1h[p][0], v);
-                    v = mfma16(w1, g1h[p][1], v);
-                }
-                for (int e = 0; e < 4; ++e) {
-                    const int c = 16 * b + kq + e;
-                    if (c < GS_MLP_IN) T.dx[r][c] = v[e] * inv;
-                }
-            }
-            // transposed fragments for the weight gradients
-            for (int b = 0; b < 2; ++b)
-                for (int e = 0; e < 4; ++e) {
-                    const int nn = 16 * b + kq + e;
-                    T.h1t[nn][r] = (_Float16)(h1[b][e] > 0.f ? h1[b][e] : 0.f);
-                    T.h2t[nn][r] = (_Float16)(h2[b][e] > 0.f ? h2[b][e] : 0.f);
-                    for (int p = 0; p < 2; ++p) {
-                        T.g1t[p][nn][r] = g1h[p][b][e];
-                        T.g2t[p][nn][r] = g2h[p][b][e];
-                    }
-                }
-            wave_lds_sync();
-            // dW3[o][n] += sum_G delta3[G][o] h2[G][n]
-            for (int nb = 0; nb < 2; ++nb) {
-                const half4_t h2b = lds_half4(&T.h2t[16 * nb + r][kq]);
-                float4_t p = mfma16(lds_half4(&T.d3t[0][r][kq]), h2b, zero);
-                p = mfma16(lds_half4(&T.d3t[1][r][kq]), h2b, p);
-                aw3[nb] += p * inv;
-            }
-            // dW2[n][k] += sum_G dh2[G][n] h1[G][k];  dW1[n][k] += sum_G dh1[G][n] x[G][k]
-            for (int nb = 0; nb < 2; ++nb) {
-                half4_t xb;
-                for (int j = 0; j < 4; ++j) xb[j] = XI.x[16 * t + kq + j][16 * nb + r];
-                const half4_t h1b = lds_half4(&T.h1t[16 * nb + r][kq]);
-                for (int mb = 0; mb < 2; ++mb) {
-                    float4_t p2 = mfma16(lds_half4(&T.g2t[0][16 * mb + r][kq]), h1b, zero);
-                    p2 = mfma16(lds_half4(&T.g2t[1][16 * mb + r][kq]), h1b, p2);
-                    aw2[mb][nb] += p2 * inv;
-                    float4_t p1 = mfma16(lds_half4(&T.g1t[0][16 * mb + r][kq]), xb, zero);
-                    p1 = mfma16(lds_half4(&T.g1t[1][16 * mb + r][kq]), xb, p1);
-                    aw1[mb][nb] += p1 * inv;
-                }
-            }
-            if (g4 == t)
-                for (int c = 0; c < GS_MLP_IN; ++c) dxo[c] = T.dx[r][c];
-            wave_lds_sync();
+            mlp_tile_bwd(W, st, t, vis, a.dlatent, n, base, scale, inv, acc);
         }
+        wave_lds_sync();
         if (valid) {
-            for (int c = 0; c < GS_LATENT_DIM; ++c) a.dlatent[c * n + i] = dxo[c];
+            float mu[3], ls[3], q[4], g9[kAccStride];
+            for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
+            for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
+            for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
+            const float* ap = a.acc + (size_t)i * kAccStride;
+            for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+            GeoGrad gg;
+            geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
             // the binary16 rounding of d passes the gradient; d = v / |v|
-            const float dd0 = dxo[14], dd1 = dxo[15], dd2 = dxo[16];
+            const float dd0 = st.dd[lane][0], dd1 = st.dd[lane][1], dd2 = st.dd[lane][2];
             const float dot = d[0] * dd0 + d[1] * dd1 + d[2] * dd2;
             const float il = 1.f / len;
             gg.dmu[0] += (dd0 - d[0] * dot) * il;
@@ -391,25 +286,30 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_latent(BwdArgs a)
             a.dlogits[i] = gg.dlogit;
             if (a.dmean2d) { a.dmean2d[i] = g9[0]; a.dmean2d[n + i] = g9[1]; }
         }
+        wave_lds_sync();   // st.dd is read before the next chunk restages
     }
-    // workgroup sum of the four waves' weight gradients, in wave order
+    // workgroup sum of the four waves' weight gradients, in wave order, in the
+    // LDS of the (no longer needed) weight fragments
+    static_assert(sizeof(MlpFrags) >= GS_MLP_WEIGHTS * sizeof(float), "reduction buffer");
     __syncthreads();
-    float* red = reinterpret_cast<float*>(&X[0]);
+    float* red = reinterpret_cast<float*>(&W);
     for (int k = threadIdx.x; k < GS_MLP_WEIGHTS; k += kBlock) red[k] = 0.f;
     __syncthreads();
+    const int g = lane >> 4, c = lane & 15;
+    mlp_grad_rescale(acc, 0);   // back to plain units
     for (int w = 0; w < kBlock / kWave; ++w) {
         if (wave == w) {
             for (int mb = 0; mb < 2; ++mb)
-                for (int nb = 0; nb < 2; ++nb)
+                for (int fb = 0; fb < 2; ++fb)
                     for (int e = 0; e < 4; ++e) {
-                        const int nn = 16 * mb + kq + e, k = 16 * nb + r;
-                        if (k < GS_MLP_IN) red[nn * GS_MLP_IN + k] += aw1[mb][nb][e];
-                        red[32 * GS_MLP_IN + nn * 32 + k] += aw2[mb][nb][e];
+                        const int row = 16 * mb + 4 * g + e, col = 16 * fb + c;
+                        if (col < GS_MLP_IN) red[row * GS_MLP_IN + col] += acc.w1[mb][fb][e];
+                        red[32 * GS_MLP_IN + row * 32 + col] += acc.w2[mb][fb][e];
                     }
             for (int nb = 0; nb < 2; ++nb)
                 for (int e = 0; e < 4; ++e) {
-                    const int o = kq + e, k = 16 * nb + r;
-                    if (o < GS_MLP_OUT) red[32 * GS_MLP_IN + 32 * 32 + o * 32 + k] += aw3[nb][e];
+                    const int o = 4 * g + e, col = 16 * nb + c;
+                    if (o < GS_MLP_OUT) red[32 * GS_MLP_IN + 32 * 32 + o * 32 + col] += acc.w3[nb][e];
                 }
         }
         __syncthreads();
@@ -418,15 +318,35 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_latent(BwdArgs a)
         a.mlp_part[(size_t)blockIdx.x * GS_MLP_WEIGHTS + k] = red[k];
 }
 
-// dW = sum of the per-workgroup partials in workgroup order.
-__global__ __launch_bounds__(kBlock) void k_mlp_reduce(const float* __restrict__ part, int nparts,
-                                                       float* __restrict__ dw)
+// dW = sum of the per-workgroup partials, in a fixed order. One workgroup per
+// 64 weights: thread (row, column) sums every 16th partial starting at its row,
+// then the 16 row sums are added in row order.
+constexpr int kReduceRows = 16, kReduceCols = 64;
+__global__ __launch_bounds__(kReduceRows * kReduceCols) void k_mlp_reduce(const float* __restrict__ part, int nparts,
+                                                                          float* __restrict__ dw)
 {
-    const int k = blockIdx.x * kBlock + threadIdx.x;
-    if (k >= GS_MLP_WEIGHTS) return;
+    __shared__ float rows[kReduceRows][kReduceCols];
+    const int c = threadIdx.x % kReduceCols, r = threadIdx.x / kReduceCols;
+    const int k = blockIdx.x * kReduceCols + c;
     float s = 0.f;
-    for (int b = 0; b < nparts; ++b) s += part[(size_t)b * GS_MLP_WEIGHTS + k];
-    dw[k] = s;
+    if (k < GS_MLP_WEIGHTS) {
+        int b = r;
+        for (; b + 3 * kReduceRows < nparts; b += 4 * kReduceRows) {
+            const float v0 = part[(size_t)b * GS_MLP_WEIGHTS + k];
+            const float v1 = part[(size_t)(b + kReduceRows) * GS_MLP_WEIGHTS + k];
+            const float v2 = part[(size_t)(b + 2 * kReduceRows) * GS_MLP_WEIGHTS + k];
+            const float v3 = part[(size_t)(b + 3 * kReduceRows) * GS_MLP_WEIGHTS + k];
+            s = (((s + v0) + v1) + v2) + v3;
+        }
+        for (; b < nparts; b += kReduceRows) s += part[(size_t)b * GS_MLP_WEIGHTS + k];
+    }
+    rows[r][c] = s;
+    __syncthreads();
+    if (r == 0 && k < GS_MLP_WEIGHTS) {
+        float t = 0.f;
+        for (int j = 0; j < kReduceRows; ++j) t += rows[j][c];
+        dw[k] = t;
+    }
 }
 
 inline int latent_bwd_grid(int64_t n) { return (int)std::min<int64_t>(div_up(n, kBlock), kMlpPartials); }
@@ -464,8 +384,8 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
 
 hipError_t launch_mlp_reduce(int64_t n, const Workspace& ws, float* dmlp_w, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_mlp_reduce, dim3((unsigned)div_up(GS_MLP_WEIGHTS, kBlock)), dim3(kBlock), 0, s, ws.mlp_part,
-                       latent_bwd_grid(n), dmlp_w);
+    hipLaunchKernelGGL(k_mlp_reduce, dim3((unsigned)div_up(GS_MLP_WEIGHTS, kReduceCols)),
+                       dim3(kReduceRows * kReduceCols), 0, s, ws.mlp_part, latent_bwd_grid(n), dmlp_w);
     return hipGetLastError();
 }
 

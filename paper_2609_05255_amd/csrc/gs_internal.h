@@ -61,7 +61,7 @@ constexpr int kDupChunk = 2048;   // depth-ordered Gaussians per workgroup in pa
 
 // Workgroups of the latent preprocess backward (grid-stride), one partial
 // weight gradient each.
-constexpr int kMlpPartials = 1024;
+constexpr int kMlpPartials = 768;
 
 __host__ __device__ inline int64_t div_up(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t align_up(size_t a, size_t b) { return (a + b - 1) / b * b; }

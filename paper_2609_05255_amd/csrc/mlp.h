@@ -3,12 +3,25 @@
 // backward pass. Half-precision operands, fp32 accumulation (Sec. 4 and the
 // appendix on the fused rasterizer: the decoder runs in half precision).
 //
-// Everything is computed transposed, neurons x Gaussians, with
-// v_mfma_f32_16x16x16_f16:  D[m][n] = sum_k A[m][k] B[k][n] + C[m][n], where
-// lane l holds A[l%16][4(l/16) + j], B[4(l/16) + j][l%16] (j = 0..3) and
-// D[4(l/16) + i][l%16] (i = 0..3). A layer's D fragment for neurons 16b..16b+15
-// is therefore exactly the B fragment of the next layer's K-half b, so the
-// activations stay in registers from layer to layer.
+// Matrix-core fragments (wave64, l = lane, g = l/16, c = l%16):
+//   v_mfma_f32_16x16x16_f16: A[c][4g + j], B[4g + j][c] (j = 0..3);
+//   v_mfma_f32_16x16x32_f16: A[c][s(g, j)], B[s(g, j)][c] (j = 0..7);
+//   both: D[4g + i][c] (i = 0..3).
+// The 32-deep product pairs A's element j of lane group g with B's element j of
+// the same group, so which K index a slot carries does not matter as long as A
+// and B agree; this code gives slot (g, j) the index
+//   s(g, j) = 4g + j (j < 4),  16 + 4g + (j - 4) (j >= 4),
+// which makes the two D fragments of neurons 0..15 and 16..31 (lane l holds
+// neurons 4g + i and 16 + 4g + i of Gaussian c), concatenated, the B fragment
+// of the next layer: activations stay in registers from layer to layer.
+//
+// Two orientations. "Neuron-major" products put neurons on the M side
+// (D[neuron][Gaussian]); they chain from layer to layer. Swapping the A and B
+// registers of a product gives its transpose in the same D layout
+// (D[Gaussian][neuron], "Gaussian-major"): there the Gaussians sit on the rows
+// 4g + i, exactly where a 16-deep product over the tile's Gaussians wants its
+// K index. The weight gradients (sums over Gaussians) therefore take
+// Gaussian-major fragments straight from registers, with no transposes.
 #pragma once
 
 #include "gs_internal.h"
@@ -16,6 +29,7 @@
 namespace gsr {
 
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float4_t mfma16(half4_t a, half4_t b, float4_t c)
@@ -23,64 +37,410 @@ __device__ __forceinline__ float4_t mfma16(half4_t a, half4_t b, float4_t c)
     return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
 }
 
-// Row pitches (in halves) chosen so that the 16 rows an MFMA fragment reads
-// fall into distinct LDS banks.
-constexpr int kP32 = 36;   // rows of 32 values
-constexpr int kP16 = 20;   // rows of 16 values
+__device__ __forceinline__ float4_t mfma32(half8_t a, half8_t b, float4_t c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
 
-// Shared (per workgroup) copies of the weights, zero-padded, in the four
-// orientations the products need. Row-major [rows][cols].
-struct MlpWeights {
-    _Float16 w1[32][kP32];    // W1[n][k], k < 17
-    _Float16 w1t[32][kP32];   // W1^T[k][n], k < 17
-    _Float16 w2[32][kP32];
-    _Float16 w2t[32][kP32];
-    _Float16 w3[16][kP32];    // W3[o][n], o < 3
-    _Float16 w3t[32][kP16];   // W3^T[n][o], o < 3
+// K index of slot j of lane group g in a 32-deep fragment.
+__host__ __device__ constexpr int kslot(int g, int j) { return j < 4 ? 4 * g + j : 16 + 4 * g + (j - 4); }
+
+// Per-workgroup weight fragments, one 8- (or 4-) half vector per lane, so that
+// each operand is one aligned LDS read. Zero-padded outside the real sizes.
+struct MlpFrags {
+    alignas(16) _Float16 w1a[2][kWave][8];   // A of W1:   rows n1 = 16b + c,  K = input s(g, j)
+    alignas(16) _Float16 w2a[2][kWave][8];   // A of W2:   rows n2 = 16b + c,  K = n1 s(g, j)
+    alignas(16) _Float16 w3a[kWave][8];      // A of W3:   rows o = c (< 3),   K = n2 s(g, j)
+    alignas(16) _Float16 w1t[2][kWave][8];   // A of W1^T: rows f = 16b + c (< 17), K = n1 s(g, j)
+    alignas(16) _Float16 w2t[2][kWave][8];   // A of W2^T: rows n1 = 16b + c,  K = n2 s(g, j)
+    alignas(8) _Float16 w3t[2][kWave][4];    // A of W3^T: rows n2 = 16b + c,  K = o = 4g + j (< 3)
 };
 
-// Loads the binary16 weights (W1[32][17], W2[32][32], W3[3][32]) into LDS.
-// Called by every thread of the workgroup; ends with a barrier.
-__device__ __forceinline__ void mlp_load_weights(const uint16_t* __restrict__ w, MlpWeights& s)
+// Loads the binary16 weights (W1[32][17], W2[32][32], W3[3][32], packed) into
+// the fragments; the transposed ones only if `backward`. Called by every thread
+// of the workgroup; ends with a barrier.
+__device__ __forceinline__ void mlp_load_frags(const uint16_t* __restrict__ w, MlpFrags& s, bool backward)
 {
-    const _Float16* src = reinterpret_cast<const _Float16*>(w);
-    for (int e = threadIdx.x; e < 32 * 32; e += blockDim.x) {
-        const int r = e >> 5, c = e & 31;
-        s.w1[r][c] = c < GS_MLP_IN ? src[r * GS_MLP_IN + c] : (_Float16)0.f;
-        s.w1t[r][c] = r < GS_MLP_IN ? src[c * GS_MLP_IN + r] : (_Float16)0.f;
-        s.w2[r][c] = src[32 * GS_MLP_IN + r * 32 + c];
-        s.w2t[r][c] = src[32 * GS_MLP_IN + c * 32 + r];
-    }
-    for (int e = threadIdx.x; e < 16 * 32; e += blockDim.x) {
-        const int r = e >> 5, c = e & 31;
-        s.w3[r][c] = r < GS_MLP_OUT ? src[32 * GS_MLP_IN + 32 * 32 + r * 32 + c] : (_Float16)0.f;
-        const int n = e >> 4, o = e & 15;
-        s.w3t[n][o] = o < GS_MLP_OUT ? src[32 * GS_MLP_IN + 32 * 32 + o * 32 + n] : (_Float16)0.f;
+    const _Float16* W1 = reinterpret_cast<const _Float16*>(w);
+    const _Float16* W2 = W1 + 32 * GS_MLP_IN;
+    const _Float16* W3 = W2 + 32 * 32;
+    const _Float16 z = (_Float16)0.f;
+    for (int e = threadIdx.x; e < kWave * 8; e += blockDim.x) {
+        const int l = e >> 3, j = e & 7, g = l >> 4, c = l & 15;
+        const int k = kslot(g, j);
+        for (int b = 0; b < 2; ++b) {
+            const int row = 16 * b + c;
+            s.w1a[b][l][j] = k < GS_MLP_IN ? W1[row * GS_MLP_IN + k] : z;
+            s.w2a[b][l][j] = W2[row * 32 + k];
+            if (backward) {
+                s.w1t[b][l][j] = row < GS_MLP_IN ? W1[k * GS_MLP_IN + row] : z;
+                s.w2t[b][l][j] = W2[k * 32 + row];
+                if (j < 4) s.w3t[b][l][j] = 4 * g + j < GS_MLP_OUT ? W3[(4 * g + j) * 32 + row] : z;
+            }
+        }
+        s.w3a[l][j] = c < GS_MLP_OUT ? W3[c * 32 + k] : z;
     }
     __syncthreads();
 }
 
-// Decoder inputs of the wave's 64 Gaussians, row = lane: latent 0..13,
-// direction 14..16, zeros up to 32.
-struct MlpInputs {
-    _Float16 x[64][kP32];
-};
+__device__ __forceinline__ half8_t frag8(const _Float16 (*p)[8]) { return *reinterpret_cast<const half8_t*>(p[__lane_id()]); }
+__device__ __forceinline__ half4_t frag4(const _Float16 (*p)[4]) { return *reinterpret_cast<const half4_t*>(p[__lane_id()]); }
 
-// Per-wave scratch of the backward for one tile of 16 Gaussians. Gradients
-// enter the matrix cores as a high and a low binary16 part (v = hi + lo), so
-// the chain keeps about 22 bits of precision instead of 11.
-struct MlpBwdTile {
-    _Float16 h1t[32][kP16];   // hidden activations, transposed (neuron x Gaussian)
-    _Float16 h2t[32][kP16];
-    _Float16 g1t[2][32][kP16];   // masked, scaled gradients of the hidden layers, transposed (hi, lo)
-    _Float16 g2t[2][32][kP16];
-    _Float16 d3t[2][16][kP16];   // scaled output gradients, transposed (hi, lo; rows 3..15 zero)
-    float dx[16][GS_MLP_IN];  // input gradients, row = Gaussian
-};
+// relu, then binary16: rounding to nearest keeps the sign, so rounding first
+// and taking the maximum with zero on the packed halves gives the same values.
+__device__ __forceinline__ half4_t relu_half4(const float4_t& v)
+{
+    typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+    const half2_t z = {0, 0};
+    half2_t a = {(_Float16)v[0], (_Float16)v[1]}, b = {(_Float16)v[2], (_Float16)v[3]};
+    a = __builtin_elementwise_max(a, z);
+    b = __builtin_elementwise_max(b, z);
+    return half4_t{a[0], a[1], b[0], b[1]};
+}
 
-// v = hi + lo with both parts binary16.
+__device__ __forceinline__ half8_t relu_cat(const float4_t& lo, const float4_t& hi)
+{
+    const half4_t a = relu_half4(lo), b = relu_half4(hi);
+    return half8_t{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+__device__ __forceinline__ _Float16 half_of_bits(uint16_t b) { return __builtin_bit_cast(_Float16, b); }
+
+// B fragment (K = input feature, N = Gaussian) of the decoder input of tile t of
+// the wave's 64 Gaussians (index base + lane): features s(g, 0..7) of Gaussian
+// 16t + c, i.e. latent 4g..4g+3 (g < 3) or 12, 13, then d_x, d_y (g = 3), and
+// d_z in slot 4 of group 0, with the view direction rounded to binary16 (round
+// to nearest even). `d` is the calling lane's own direction; Gaussians whose
+// bit in `valid` is clear get zeros and load nothing.
+__device__ __forceinline__ half8_t mlp_input_frag(const uint16_t* __restrict__ latent, int64_t n, int64_t base,
+                                                  int t, uint64_t valid, const float d[3])
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    const int src = 16 * t + c;
+    const float dx = __shfl(d[0], src), dy = __shfl(d[1], src), dz = __shfl(d[2], src);
+    half8_t x = {0, 0, 0, 0, 0, 0, 0, 0};
+    if ((valid >> src) & 1) {
+        const uint16_t* p = latent + (int64_t)(4 * g) * n + base + src;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (g < 3 || j < 2) x[j] = half_of_bits(p[(int64_t)j * n]);
+        if (g == 3) {
+            x[2] = (_Float16)dx;
+            x[3] = (_Float16)dy;
+        }
+        if (g == 0) x[4] = (_Float16)dz;
+    }
+    return x;
+}
+
+// Neuron-major forward of one tile from its input fragment: h1[b], h2[b] hold
+// the fp32 pre-activations of neurons 16b + 4g + i of Gaussian c, o the output
+// pre-activations (channel i of Gaussian c in lanes 0..15, i < 3); a1, a2 the
+// binary16 activations as next-layer fragments.
+__device__ __forceinline__ void mlp_tile_fwd(const MlpFrags& W, const half8_t& x, float4_t h1[2], half8_t& a1,
+                                             float4_t h2[2], half8_t& a2, float4_t& o)
+{
+    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < 2; ++b) h1[b] = mfma32(frag8(W.w1a[b]), x, zero);
+    a1 = relu_cat(h1[0], h1[1]);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) h2[b] = mfma32(frag8(W.w2a[b]), a1, zero);
+    a2 = relu_cat(h2[0], h2[1]);
+    o = mfma32(frag8(W.w3a), a2, zero);
+}
+
+// Logistic function with the hardware exp2 and reciprocal (about 1 ulp each).
+__device__ __forceinline__ float sigmoid_fast(float x)
+{
+    return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
+}
+
+// Moves the tile's colours (lanes 0..15 of the neuron-major output) to the
+// lanes that own the Gaussians (16 t .. 16 t + 15).
+__device__ __forceinline__ void mlp_tile_colors(const float4_t& o, int t, float col[3])
+{
+    const int lane = __lane_id();
+    const int src = lane & 15;
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) {
+        const float v = __shfl(sigmoid_fast(o[ch]), src);
+        if ((lane >> 4) == t) col[ch] = v;
+    }
+}
+
+// v = hi + lo with both parts binary16: gradients enter the matrix cores as two
+// parts, so the chain keeps about 22 bits of precision instead of 11.
 __device__ __forceinline__ _Float16 half_hi(float v) { return (_Float16)v; }
 __device__ __forceinline__ _Float16 half_lo(float v) { return (_Float16)(v - (float)(_Float16)v); }
+
+__device__ __forceinline__ void split4(const float4_t& v, half4_t& hi, half4_t& lo)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        hi[i] = half_hi(v[i]);
+        lo[i] = half_lo(v[i]);
+    }
+}
+
+__device__ __forceinline__ void split_cat(const float4_t& a, const float4_t& b, half8_t& hi, half8_t& lo)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        hi[i] = half_hi(a[i]);
+        lo[i] = half_lo(a[i]);
+        hi[4 + i] = half_hi(b[i]);
+        lo[4 + i] = half_lo(b[i]);
+    }
+}
+
+__device__ __forceinline__ float4_t relu_mask(const float4_t& v, const float4_t& pre)
+{
+    float4_t r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = pre[i] > 0.f ? v[i] : 0.f;
+    return r;
+}
+
+// Running sums of the weight gradients, Gaussian-major products in fp32, in
+// units of 2^-se (se: the current chunk's gradient scale exponent, below):
+// w1[mb][fb] rows n1 = 16mb + 4g + i, columns f = 16fb + c; w2[mb][nb] rows
+// n2 = 16mb + 4g + i, columns n1 = 16nb + c; w3[nb] rows o = 4g + i, columns
+// n2 = 16nb + c.
+struct MlpGradAcc {
+    float4_t w1[2][2], w2[2][2], w3[2];
+    int se;
+};
+
+__device__ __forceinline__ void mlp_grad_zero(MlpGradAcc& a)
+{
+    const float4_t z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        a.w3[u] = z;
+#pragma unroll
+        for (int v = 0; v < 2; ++v) a.w1[u][v] = a.w2[u][v] = z;
+    }
+    a.se = 0;
+}
+
+__device__ __forceinline__ float4_t ldexp4(const float4_t& v, int e)
+{
+    float4_t r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = ldexpf(v[i], e);
+    return r;
+}
+
+// Brings the running sums to units of 2^-se (exact: powers of two).
+__device__ __forceinline__ void mlp_grad_rescale(MlpGradAcc& a, int se)
+{
+    if (se == a.se) return;
+    const int e = se - a.se;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        a.w3[u] = ldexp4(a.w3[u], e);
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+            a.w1[u][v] = ldexp4(a.w1[u][v], e);
+            a.w2[u][v] = ldexp4(a.w2[u][v], e);
+        }
+    }
+    a.se = se;
+}
+
+// Maximum over the wave, returned to every lane.
+__device__ __forceinline__ float wave_max(float v)
+{
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false)));
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false)));
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+
+// Scale exponent of a chunk whose largest colour-gradient magnitude is m: the
+// output gradients delta3 = dL/dc s (1 - s) <= m / 4 then stay below 2^9 after
+// scaling by 2^se, and the largest one lies within a factor 4 s (1 - s) of it,
+// far from the binary16 subnormals. m = 0 keeps the previous exponent.
+__device__ __forceinline__ int mlp_chunk_exponent(float m, int prev)
+{
+    if (!(m > 0.f)) return prev;
+    int ex = 0;
+    frexpf(m, &ex);
+    return min(11 - ex, 100);
+}
+
+// Row pitch (halves) of the staged decoder inputs: 8-byte aligned rows whose
+// fragment reads spread over the LDS banks.
+constexpr int kXPitch = 36;
+
+// Per-wave staging of what the backward needs across lanes: each Gaussian's
+// decoder input (latent 0..13, binary16 direction 14..16, zeros up to 32), its
+// output-colour gradient, and the gradient into its direction that the tiles
+// produce.
+struct MlpWaveStage {
+    alignas(16) _Float16 x[kWave][kXPitch];
+    float dc[kWave][4];
+    float dd[kWave][4];
+};
+
+// Writes the calling lane's row of the stage (all lanes; zeros when !valid).
+__device__ __forceinline__ void mlp_stage_row(MlpWaveStage& st, bool valid, const uint16_t* __restrict__ latent,
+                                              int64_t n, int64_t i, const float d[3], const float dc[3])
+{
+    const int l = __lane_id();
+    half4_t v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = half4_t{0, 0, 0, 0};
+    if (valid) {
+#pragma unroll
+        for (int f = 0; f < GS_LATENT_DIM; ++f) v[f >> 2][f & 3] = half_of_bits(latent[(int64_t)f * n + i]);
+        v[3][2] = (_Float16)d[0];
+        v[3][3] = (_Float16)d[1];
+        v[4][0] = (_Float16)d[2];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) *reinterpret_cast<half4_t*>(&st.x[l][4 * q]) = v[q];
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) st.dc[l][ch] = valid ? dc[ch] : 0.f;
+}
+
+// B fragment of tile t from the stage: features s(g, 0..7) of Gaussian 16t + c.
+__device__ __forceinline__ half8_t mlp_stage_frag(const MlpWaveStage& st, int t)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    const half4_t lo = *reinterpret_cast<const half4_t*>(&st.x[16 * t + c][4 * g]);
+    const half4_t hi = *reinterpret_cast<const half4_t*>(&st.x[16 * t + c][16 + 4 * g]);
+    return half8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+// Backward of one tile (Gaussians 16t .. 16t + 15 of the wave), from the
+// staged inputs and colour gradients, with the chunk's gradient scale 2^se
+// (acc.se): delta3 = dL/dc s (1 - s) enters the matrix cores scaled, dH2, dH1
+// and dX are chained neuron-major, the Gaussian-major copies give
+//   dW3 = sum_G delta3 h2^T, dW2 = sum_G dh2 h1^T, dW1 = sum_G dh1 x^T
+// accumulated in place into `acc` (units 2^-se). Writes the latent gradients of
+// the tile's valid Gaussians to dlatent ([14][n], Gaussian base + 16t + c) and
+// their direction gradients to st.dd.
+//
+// Precision: along the chain to dX each gradient operand is a binary16 hi+lo
+// pair, since a rounding there is carried through two more layers into every
+// input gradient. The weight gradients take each gradient operand as one
+// binary16 value: each product then carries its own rounding (relative 2^-12
+// at most), and these independent errors stay at that level in the sums.
+__device__ __forceinline__ void mlp_tile_bwd(const MlpFrags& W, MlpWaveStage& st, int t, uint64_t valid,
+                                             float* __restrict__ dlatent, int64_t n, int64_t base, float scale,
+                                             float inv, MlpGradAcc& acc)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
+    const half8_t x = mlp_stage_frag(st, t);
+    // Gaussian-major input fragment: feature 16fb + c of Gaussians 16t + 4g + j
+    // (rows of culled Gaussians are zero)
+    half4_t xg[2];
+#pragma unroll
+    for (int fb = 0; fb < 2; ++fb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) xg[fb][j] = st.x[16 * t + 4 * g + j][16 * fb + c];
+    // forward, both orientations
+    float4_t h1n[2], h2n[2], on;
+    half8_t a1, a2;
+    mlp_tile_fwd(W, x, h1n, a1, h2n, a2, on);
+    float4_t h1g[2], h2g[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) h1g[b] = mfma32(x, frag8(W.w1a[b]), zero);      // h1[G = 4g+i][16b + c]
+#pragma unroll
+    for (int b = 0; b < 2; ++b) h2g[b] = mfma32(a1, frag8(W.w2a[b]), zero);     // h2[G = 4g+i][16b + c]
+    const float4_t og = mfma32(a2, frag8(W.w3a), zero);                          // o[G = 4g+i][channel c]
+
+    // scaled output gradients: neuron-major (channel 4g + i of Gaussian c, only
+    // g = 0 carries channels) and Gaussian-major (Gaussian 4g + i, channel c);
+    // a culled Gaussian's staged colour gradient is zero
+    float4_t d3n, d3g;
+    const int cn = min(c, 3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float sn = sigmoid_fast(on[i]), sg = sigmoid_fast(og[i]);
+        const float dcn = st.dc[16 * t + c][i];
+        const float dcg = st.dc[16 * t + 4 * g + i][cn];
+        d3n[i] = g == 0 ? dcn * scale * (sn * (1.f - sn)) : 0.f;
+        d3g[i] = c < GS_MLP_OUT ? dcg * scale * (sg * (1.f - sg)) : 0.f;
+    }
+    half4_t d3n_hi, d3n_lo;
+    split4(d3n, d3n_hi, d3n_lo);
+    const half4_t d3g_h = half4_t{(_Float16)d3g[0], (_Float16)d3g[1], (_Float16)d3g[2], (_Float16)d3g[3]};
+
+    // dH2 = W3^T delta3, masked by relu'(h2)
+    float4_t g2n[2], g2g[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const half4_t w = frag4(W.w3t[b]);
+        g2n[b] = relu_mask(mfma16(w, d3n_lo, mfma16(w, d3n_hi, zero)), h2n[b]);
+        g2g[b] = relu_mask(mfma16(d3n_lo, w, mfma16(d3n_hi, w, zero)), h2g[b]);
+    }
+    half8_t g2n_hi, g2n_lo;
+    split_cat(g2n[0], g2n[1], g2n_hi, g2n_lo);
+    // dH1 = W2^T dH2, masked by relu'(h1)
+    float4_t g1n[2], g1g[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const half8_t w = frag8(W.w2t[b]);
+        g1n[b] = relu_mask(mfma32(w, g2n_lo, mfma32(w, g2n_hi, zero)), h1n[b]);
+        g1g[b] = relu_mask(mfma32(g2n_lo, w, mfma32(g2n_hi, w, zero)), h1g[b]);
+    }
+    half8_t g1n_hi, g1n_lo;
+    split_cat(g1n[0], g1n[1], g1n_hi, g1n_lo);
+    // dX = W1^T dH1: lane l holds features 16b + 4g + i of Gaussian c
+    float4_t dx[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const half8_t w = frag8(W.w1t[b]);
+        dx[b] = mfma32(w, g1n_lo, mfma32(w, g1n_hi, zero)) * inv;
+    }
+    if ((valid >> (16 * t + c)) & 1) {
+        float* p = dlatent + (int64_t)(4 * g) * n + base + 16 * t + c;
+        p[0] = dx[0][0];
+        p[n] = dx[0][1];
+        if (g < 3) {
+            p[2 * n] = dx[0][2];
+            p[3 * n] = dx[0][3];
+        } else {
+            st.dd[16 * t + c][0] = dx[0][2];
+            st.dd[16 * t + c][1] = dx[0][3];
+        }
+        if (g == 0) st.dd[16 * t + c][2] = dx[1][0];
+    }
+
+    // weight gradients from the Gaussian-major fragments, accumulated in place
+    half4_t r1g[2], r2g[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        r1g[b] = relu_half4(h1g[b]);
+        r2g[b] = relu_half4(h2g[b]);
+    }
+    // dW3[o][n2] = sum_G delta3[G][o] h2[G][n2]
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) acc.w3[nb] = mfma16(d3g_h, r2g[nb], acc.w3[nb]);
+    // dW2[n2][n1] = sum_G dh2[G][n2] h1[G][n1]
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+        const half4_t h = {(_Float16)g2g[mb][0], (_Float16)g2g[mb][1], (_Float16)g2g[mb][2], (_Float16)g2g[mb][3]};
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) acc.w2[mb][nb] = mfma16(h, r1g[nb], acc.w2[mb][nb]);
+    }
+    // dW1[n1][f] = sum_G dh1[G][n1] x[G][f]
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+        const half4_t h = {(_Float16)g1g[mb][0], (_Float16)g1g[mb][1], (_Float16)g1g[mb][2], (_Float16)g1g[mb][3]};
+#pragma unroll
+        for (int fb = 0; fb < 2; ++fb) acc.w1[mb][fb] = mfma16(h, xg[fb], acc.w1[mb][fb]);
+    }
+}
 
 // Orders this wave's LDS writes before its following LDS reads by other lanes.
 __device__ __forceinline__ void wave_lds_sync()
@@ -88,90 +448,6 @@ __device__ __forceinline__ void wave_lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-__device__ __forceinline__ half4_t lds_half4(const _Float16* p)
-{
-    return *reinterpret_cast<const half4_t*>(p);
-}
-
-__device__ __forceinline__ half4_t relu_half4(float4_t v)
-{
-    half4_t h;
-    for (int i = 0; i < 4; ++i) h[i] = (_Float16)(v[i] > 0.f ? v[i] : 0.f);
-    return h;
-}
-
-// Forward of tile `tile` (rows 16 tile .. 16 tile + 15 of in.x). On return
-// h1[b], h2[b] hold the fp32 pre-activations of neurons 16b + 4(l/16) + i of
-// Gaussian l%16 of the tile, and o the output pre-activations 4(l/16) + i
-// (outputs are lanes 0..15, i < 3).
-__device__ __forceinline__ void mlp_tile_forward(const MlpWeights& W, const MlpInputs& in, int tile, float4_t h1[2],
-                                                 float4_t h2[2], float4_t& o)
-{
-    const int lane = __lane_id(), r = lane & 15, kq = 4 * (lane >> 4);
-    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
-    half4_t xb[2];
-    xb[0] = lds_half4(&in.x[16 * tile + r][kq]);
-    xb[1] = lds_half4(&in.x[16 * tile + r][16 + kq]);
-    half4_t a1[2];
-    for (int b = 0; b < 2; ++b) {
-        float4_t acc = zero;
-        acc = mfma16(lds_half4(&W.w1[16 * b + r][kq]), xb[0], acc);
-        acc = mfma16(lds_half4(&W.w1[16 * b + r][16 + kq]), xb[1], acc);
-        h1[b] = acc;
-        a1[b] = relu_half4(acc);
-    }
-    half4_t a2[2];
-    for (int b = 0; b < 2; ++b) {
-        float4_t acc = zero;
-        acc = mfma16(lds_half4(&W.w2[16 * b + r][kq]), a1[0], acc);
-        acc = mfma16(lds_half4(&W.w2[16 * b + r][16 + kq]), a1[1], acc);
-        h2[b] = acc;
-        a2[b] = relu_half4(acc);
-    }
-    float4_t acc = zero;
-    acc = mfma16(lds_half4(&W.w3[r][kq]), a2[0], acc);
-    acc = mfma16(lds_half4(&W.w3[r][16 + kq]), a2[1], acc);
-    o = acc;
-}
-
-__device__ __forceinline__ float sigmoid_fast(float x)
-{
-    return 1.f / (1.f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
-}
-
-// Stages this lane's decoder input into row `lane` of in.x: the binary16 latent
-// as stored, then the view direction rounded to binary16 (round to nearest
-// even), zeros elsewhere and for culled lanes.
-__device__ __forceinline__ void mlp_stage_lane(MlpInputs& in, bool valid, const uint16_t* __restrict__ latent,
-                                               int64_t n, int64_t i, const float d[3])
-{
-    const int row = __lane_id();
-    for (int c = 0; c < 32; ++c) {
-        _Float16 v = (_Float16)0.f;
-        if (valid) {
-            if (c < GS_LATENT_DIM) {
-                const uint16_t bits = latent[c * n + i];
-                v = __builtin_bit_cast(_Float16, bits);
-            } else if (c < GS_MLP_IN) {
-                v = (_Float16)d[c - GS_LATENT_DIM];
-            }
-        }
-        in.x[row][c] = v;
-    }
-}
-
-// Moves the tile's colours (lanes 0..15 after mlp_tile_forward) to the lanes
-// that own the Gaussians (16 tile .. 16 tile + 15).
-__device__ __forceinline__ void mlp_tile_colors(const float4_t& o, int tile, float col[3])
-{
-    const int lane = __lane_id();
-    const int src = lane & 15;
-    for (int c = 0; c < 3; ++c) {
-        const float v = __shfl(sigmoid_fast(o[c]), src);
-        if ((lane >> 4) == tile) col[c] = v;
-    }
 }
 
 }  // namespace gsr

@@ -246,43 +246,56 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
 // Latent + MLP: geometry per thread, then each wave decodes the colours of its
 // visible Gaussians on the matrix cores, 16 at a time (mlp.h); tiles of 16
 // lanes without a visible Gaussian are skipped, culled lanes load nothing.
+// Workgroups loop over chunks of 256 Gaussians so the weight fragments are
+// staged once per workgroup.
 __global__ __launch_bounds__(kBlock) void k_preprocess_latent(PreArgs a)
 {
     __shared__ uint32_t red[4];
-    __shared__ MlpWeights W;
-    __shared__ MlpInputs X[kBlock / kWave];
-    mlp_load_weights(a.mlp_w, W);
-    const int i = blockIdx.x * kBlock + threadIdx.x;
-    const int wave = threadIdx.x >> 6;
-    uint32_t tiles = 0;
-    Geo g;
-    g.visible = false;
-    float d[3] = {0.f, 0.f, 0.f};
-    if (i < a.n) {
-        float mu[3], ls[3], q[4], logit;
-        load_geometry_params(a, i, mu, ls, q, logit);
-        geometry(a.cam, mu, ls, q, logit, g);
-        if (g.visible) {
-            tiles = g.tiles;
-            view_dir(a.cam, mu, d);
+    __shared__ MlpFrags W;
+    mlp_load_frags(a.mlp_w, W, false);
+    const int nchunks = (int)div_up(a.n, kBlock);
+    for (int chunk = blockIdx.x; chunk < nchunks; chunk += gridDim.x) {
+        const int i = chunk * kBlock + threadIdx.x;
+        uint32_t tiles = 0;
+        Geo g;
+        g.visible = false;
+        float d[3] = {0.f, 0.f, 0.f};
+        if (i < a.n) {
+            float mu[3], ls[3], q[4], logit;
+            load_geometry_params(a, i, mu, ls, q, logit);
+            geometry(a.cam, mu, ls, q, logit, g);
+            if (g.visible) {
+                tiles = g.tiles;
+                view_dir(a.cam, mu, d);
+            }
+            a.tiles_touched[i] = tiles;
+            a.depth_key[i] = g.visible ? __float_as_uint(g.depth) : 0xFFFFFFFFu;
         }
-        a.tiles_touched[i] = tiles;
-        a.depth_key[i] = g.visible ? __float_as_uint(g.depth) : 0xFFFFFFFFu;
+        const uint64_t vis = __ballot(g.visible);
+        const int64_t base = (int64_t)chunk * kBlock + (threadIdx.x & ~(kWave - 1));
+        // all four input fragments first, so their loads overlap
+        half8_t xs[kWave / 16];
+        for (int t = 0; t < kWave / 16; ++t)
+            xs[t] = ((vis >> (16 * t)) & 0xFFFFull) ? mlp_input_frag(a.latent, a.n, base, t, vis, d)
+                                                     : half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        float col[3] = {0.f, 0.f, 0.f};
+        for (int t = 0; t < kWave / 16; ++t) {
+            if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
+            const half8_t x = xs[t];
+            float4_t h1[2], h2[2], o;
+            half8_t a1, a2;
+            mlp_tile_fwd(W, x, h1, a1, h2, a2, o);
+            mlp_tile_colors(o, t, col);
+        }
+        if (g.visible) store_splat(a.splats + i, g, col);
+        const uint32_t total = block_sum_u32(tiles, red);
+        if (threadIdx.x == 0) a.block_pairs[chunk] = total;
     }
-    mlp_stage_lane(X[wave], g.visible, a.latent, a.n, i, d);
-    wave_lds_sync();
-    const uint64_t vis = __ballot(g.visible);
-    float col[3] = {0.f, 0.f, 0.f};
-    for (int t = 0; t < kWave / 16; ++t) {
-        if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
-        float4_t h1[2], h2[2], o;
-        mlp_tile_forward(W, X[wave], t, h1, h2, o);
-        mlp_tile_colors(o, t, col);
-    }
-    if (g.visible) store_splat(a.splats + i, g, col);
-    const uint32_t total = block_sum_u32(tiles, red);
-    if (threadIdx.x == 0) a.block_pairs[blockIdx.x] = total;
 }
+
+// Workgroups of the latent preprocess: enough to fill the chip several times
+// over, each looping over chunks.
+constexpr int kLatentBlocks = 2048;
 
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                              const gs_preprocessed& out, const Workspace& ws, hipStream_t s)
@@ -306,7 +319,7 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     if (app.kind == GS_APP_SH3)
         hipLaunchKernelGGL(k_preprocess_sh3, dim3(blocks), dim3(kBlock), 0, s, a);
     else
-        hipLaunchKernelGGL(k_preprocess_latent, dim3(blocks), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL(k_preprocess_latent, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 
@@ -338,28 +351,33 @@ hipError_t launch_pair_count(int64_t n, const Workspace& ws, uint64_t* num_pairs
 __global__ __launch_bounds__(kBlock) void k_mlp_eval(const uint16_t* __restrict__ x, int64_t rows,
                                                      const uint16_t* __restrict__ w, float* __restrict__ out)
 {
-    __shared__ MlpWeights W;
-    __shared__ MlpInputs X[kBlock / kWave];
-    mlp_load_weights(w, W);
+    __shared__ MlpFrags W;
+    mlp_load_frags(w, W, false);
     const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    const int wave = threadIdx.x >> 6, lane = __lane_id();
-    const bool valid = i < rows;
-    for (int c = 0; c < 32; ++c) {
-        _Float16 v = (_Float16)0.f;
-        if (valid && c < GS_MLP_IN) v = __builtin_bit_cast(_Float16, x[i * GS_MLP_IN + c]);
-        X[wave].x[lane][c] = v;
-    }
-    wave_lds_sync();
+    const int lane = __lane_id(), g = lane >> 4, c = lane & 15;
+    const int64_t base = i - lane;
+    const uint64_t vis = __ballot(i < rows);
     float col[3] = {0.f, 0.f, 0.f};
-    const uint64_t vis = __ballot(valid);
     for (int t = 0; t < kWave / 16; ++t) {
         if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
+        // B fragment: features s(g, 0..7) of row 16 t + c
+        half8_t xb = {0, 0, 0, 0, 0, 0, 0, 0};
+        const int src = 16 * t + c;
+        if ((vis >> src) & 1) {
+            const uint16_t* row = x + (base + src) * GS_MLP_IN;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int f = kslot(g, j);
+                if (f < GS_MLP_IN) xb[j] = half_of_bits(row[f]);
+            }
+        }
         float4_t h1[2], h2[2], o;
-        mlp_tile_forward(W, X[wave], t, h1, h2, o);
+        half8_t a1, a2;
+        mlp_tile_fwd(W, xb, h1, a1, h2, a2, o);
         mlp_tile_colors(o, t, col);
     }
-    if (valid)
-        for (int c = 0; c < 3; ++c) out[i * 3 + c] = col[c];
+    if (i < rows)
+        for (int ch = 0; ch < 3; ++ch) out[i * 3 + ch] = col[ch];
 }
 
 hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s)

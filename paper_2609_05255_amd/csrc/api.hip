@@ -189,6 +189,7 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.hist = (uint32_t*)take(sizeof(uint32_t) * kRadix * sort_blocks);
     w.digit_tot = (uint32_t*)take(sizeof(uint32_t) * kRadix * 4);
     w.scan_part = (uint32_t*)take(sizeof(uint32_t) * (div_up(nn, kDupChunk) + 1));
+    w.sorted_rect = (uint2*)take(sizeof(uint2) * nn);
     w.pair_keys_a = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.pair_vals_a = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.pair_keys_b = (uint32_t*)take(sizeof(uint32_t) * cap);
@@ -277,10 +278,10 @@ gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t 
     }
     const uint32_t* order = nullptr;
     timing_begin(GS_KERNEL_DEPTH_SORT, s);
-    GS_HIP(launch_depth_sort(n, pre->depth_key, ws, &order, s));
+    GS_HIP(launch_depth_sort(n, pre->depth_key, pre->splats, ws, &order, s));
     timing_end(GS_KERNEL_DEPTH_SORT, s);
     timing_begin(GS_KERNEL_PAIR_OFFSETS, s);
-    GS_HIP(launch_pair_offsets(n, order, pre->tiles_touched, ws, s));
+    GS_HIP(launch_pair_offsets(n, ws, s));
     timing_end(GS_KERNEL_PAIR_OFFSETS, s);
     const int passes = tile_sort_passes(c);
     const uint32_t* sorted_tiles = nullptr;

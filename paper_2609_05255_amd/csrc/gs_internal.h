@@ -77,6 +77,7 @@ struct Workspace {
     uint32_t* hist;          // [256][max sort blocks]
     uint32_t* digit_tot;     // [4 passes][256]   digit totals of each pass
     uint32_t* scan_part;     // [n / kDupChunk + 1] chunk sums of the pair-offset scan
+    uint2* sorted_rect;      // [n]               tile rectangles in depth order (empty for culled)
     uint32_t* pair_keys_a;   // [capacity]
     uint32_t* pair_vals_a;   // [capacity]
     uint32_t* pair_keys_b;   // [capacity]
@@ -92,10 +93,9 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                              const gs_preprocessed& out, const Workspace& ws, hipStream_t s);
 hipError_t launch_pair_count(int64_t n, const Workspace& ws, uint64_t* num_pairs, hipStream_t s);
-hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const Workspace& ws,
+hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_splat* splats, const Workspace& ws,
                              const uint32_t** order_out, hipStream_t s);
-hipError_t launch_pair_offsets(int64_t n, const uint32_t* order, const uint32_t* tiles_touched,
-                               const Workspace& ws, hipStream_t s);
+hipError_t launch_pair_offsets(int64_t n, const Workspace& ws, hipStream_t s);
 hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const gs_preprocessed& pre,
                             const Workspace& ws, uint32_t capacity, uint32_t* keys_out, uint32_t* vals_out,
                             hipStream_t s);

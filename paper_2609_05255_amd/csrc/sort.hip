@@ -109,7 +109,9 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
                                                           int shift, const uint32_t* __restrict__ hist, int nblocks,
                                                           const uint32_t* __restrict__ digit_tot,
                                                           uint32_t* __restrict__ keys_out,
-                                                          uint32_t* __restrict__ vals_out)
+                                                          uint32_t* __restrict__ vals_out,
+                                                          const gs_splat* __restrict__ rect_src,
+                                                          uint2* __restrict__ rect_out)
 {
     constexpr int R = 1 << kBits;
     __shared__ uint32_t wcnt[4][R];      // per-wave digit counts, then per-wave exclusive offsets
@@ -179,8 +181,16 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
         const uint32_t k = skey[j];
         const uint32_t d = (k >> shift) & (R - 1);
         const uint32_t pos = gbase[d] + (j - lstart[d]);
+        const uint32_t v = sval[j];
         if (keys_out) keys_out[pos] = k;
-        vals_out[pos] = sval[j];
+        vals_out[pos] = v;
+        if (rect_out) {
+            // tile rectangle of Gaussian v in sorted order; culled Gaussians
+            // (key ~0, no splat record) get an empty one
+            uint2 r = make_uint2(0u, 0u);
+            if (k != 0xFFFFFFFFu) r = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint32_t*>(rect_src + v) + kSplatRectWord);
+            rect_out[pos] = r;
+        }
     }
 }
 
@@ -188,13 +198,14 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
 // value = position, keys_out == nullptr drops the keys.
 template <int kBits>
 void radix_pass_t(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t count, int shift, uint32_t* keys_out,
-                  uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
+                  uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s,
+                  const gs_splat* rect_src = nullptr, uint2* rect_out = nullptr)
 {
     const int nblocks = (int)div_up((int64_t)count, kSortTile);
     hipLaunchKernelGGL(k_radix_hist<kBits>, dim3(nblocks), dim3(kBlock), 0, s, keys_in, count, shift, hist, nblocks);
     hipLaunchKernelGGL(k_radix_scan, dim3(1 << kBits), dim3(kBlock), 0, s, hist, nblocks, digit_tot);
     hipLaunchKernelGGL(k_radix_scatter<kBits>, dim3(nblocks), dim3(kBlock), 0, s, keys_in, vals_in, count, shift,
-                       hist, nblocks, digit_tot, keys_out, vals_out);
+                       hist, nblocks, digit_tot, keys_out, vals_out, rect_src, rect_out);
 }
 
 hipError_t radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t count, int shift, int bits,
@@ -217,16 +228,19 @@ hipError_t radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t
 // ---- pair offsets in depth order and pair emission ---------------------------
 
 // Pairs emitted by each chunk of kDupChunk depth-ordered Gaussians.
-__global__ __launch_bounds__(kBlock) void k_pair_partial(const uint32_t* __restrict__ order,
-                                                         const uint32_t* __restrict__ tiles_touched, int64_t n,
+__device__ __forceinline__ uint32_t rect_area(uint2 r)
+{
+    return ((r.y & 0xFFFFu) - (r.x & 0xFFFFu)) * ((r.y >> 16) - (r.x >> 16));
+}
+
+__global__ __launch_bounds__(kBlock) void k_pair_partial(const uint2* __restrict__ sorted_rect, int64_t n,
                                                          uint32_t* __restrict__ part)
 {
     __shared__ uint32_t lds4[4];
-    const int64_t base = (int64_t)blockIdx.x * kDupChunk + (int64_t)threadIdx.x * kDupItems;
     uint32_t sum = 0;
     for (int k = 0; k < kDupItems; ++k) {
-        const int64_t i = base + k;
-        if (i < n) sum += tiles_touched[order[i]];
+        const int64_t i = (int64_t)blockIdx.x * kDupChunk + (int64_t)k * kBlock + threadIdx.x;
+        if (i < n) sum += rect_area(sorted_rect[i]);
     }
     uint32_t total;
     block_excl_scan(sum, lds4, &total);
@@ -249,22 +263,47 @@ __global__ __launch_bounds__(kBlock) void k_scan_partials(uint32_t* __restrict__
     }
 }
 
+// Inclusive maximum scan over the wave's lanes (DPP row shifts, then the row
+// broadcasts); lanes without a source keep their value.
+__device__ __forceinline__ int wave_max_scan(int v)
+{
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x111, 0xF, 0xF, false));   // row_shr:1
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x112, 0xF, 0xF, false));   // row_shr:2
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x114, 0xF, 0xF, false));   // row_shr:4
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x118, 0xF, 0xF, false));   // row_shr:8
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x142, 0xA, 0xF, false));   // row_bcast:15
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x143, 0xC, 0xF, false));   // row_bcast:31
+    return v;
+}
+
+__device__ __forceinline__ void wave_lds_fence()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Emits the (tile, Gaussian) pairs of a chunk of depth-ordered Gaussians, each
 // Gaussian's tiles in row-major order of its rectangle. The chunk's offsets
-// and rectangles are staged in LDS; each thread then produces every 256th
-// pair of the chunk, finding its Gaussian by binary search, so consecutive
-// threads write consecutive addresses.
+// and rectangles are staged in LDS. Each wave then emits a contiguous quarter
+// of the chunk's pairs, 64 consecutive pairs per round (consecutive lanes write
+// consecutive addresses): the lanes mark in LDS where the Gaussians of the next
+// 63 slots start inside the round's window (after its first pair, which
+// belongs to the round's first Gaussian), and an inclusive maximum scan over
+// the lanes gives each pair its Gaussian. Depth order puts every culled
+// Gaussian (no tiles) after the visible ones, so starts inside a window are
+// distinct.
 __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict__ order,
-                                                      const uint32_t* __restrict__ tiles_touched,
-                                                      const gs_splat* __restrict__ splats, int64_t n,
+                                                      const uint2* __restrict__ sorted_rect, int64_t n,
                                                       const uint32_t* __restrict__ part, int tiles_x,
                                                       uint32_t capacity, uint32_t* __restrict__ keys,
                                                       uint32_t* __restrict__ vals)
 {
-    __shared__ uint32_t soff[kDupChunk];
+    __shared__ uint32_t soff[kDupChunk + 1];
     __shared__ uint32_t sgid[kDupChunk];
     __shared__ uint32_t sorg[kDupChunk];   // rectangle origin x0 | y0 << 16
     __shared__ uint32_t swid[kDupChunk];   // rectangle width in tiles
+    __shared__ int smark[kBlock / kWave][kWave];
     __shared__ uint32_t lds4[4];
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * kDupChunk;
@@ -276,12 +315,11 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
         uint32_t c = 0, g = 0, org = 0, w = 1;
         if (i < n) {
             g = order[i];
-            c = tiles_touched[g];
+            const uint2 r = sorted_rect[i];
+            c = rect_area(r);
             if (c != 0) {
-                const float2 rr = *reinterpret_cast<const float2*>(reinterpret_cast<const float*>(splats + g) + kSplatRectWord);
-                const uint32_t r01 = __float_as_uint(rr.x), r23 = __float_as_uint(rr.y);
-                org = r01;
-                w = (r23 & 0xFFFFu) - (r01 & 0xFFFFu);
+                org = r.x;
+                w = (r.y & 0xFFFFu) - (r.x & 0xFFFFu);
             }
         }
         cnt[k] = c;
@@ -296,27 +334,52 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
         soff[t * kDupItems + k] = off;
         off += cnt[k];
     }
+    if (t == 0) soff[kDupChunk] = total;
     __syncthreads();
     const uint32_t gbase = part[blockIdx.x];
-    for (uint32_t p = t; p < total; p += kBlock) {
-        // last slot whose offset is <= p
-        int lo = 0, hi = kDupChunk;
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (soff[mid] <= p) lo = mid;
-            else hi = mid;
+    const int wave = t >> 6, lane = __lane_id();
+    const uint32_t q0 = (uint32_t)(((uint64_t)total * wave) / (kBlock / kWave));
+    const uint32_t q1 = (uint32_t)(((uint64_t)total * (wave + 1)) / (kBlock / kWave));
+    if (q0 >= q1) return;
+    // last slot whose offset is <= q0 (the same address in every lane)
+    int lo = 0, hi = kDupChunk;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (soff[mid] <= q0) lo = mid;
+        else hi = mid;
+    }
+    int first = lo;
+    int* mark = smark[wave];
+    for (uint32_t p0 = q0; p0 < q1; p0 += kWave) {
+        mark[lane] = lane == 0 ? 0 : -1;
+        wave_lds_fence();
+        const int sl = first + lane;
+        if (lane > 0 && sl < kDupChunk) {
+            const uint32_t o = soff[sl];
+            if (o > p0 && o < p0 + kWave && soff[sl + 1] > o) mark[o - p0] = lane;
         }
-        const uint32_t i = p - soff[lo];
-        const uint32_t w = swid[lo];
-        const uint32_t q = i / w;
-        const uint32_t org = sorg[lo];
-        const uint32_t tx = (org & 0xFFFFu) + (i - q * w);
-        const uint32_t ty = (org >> 16) + q;
-        const uint32_t out = gbase + p;
-        if (out < capacity) {   // only a num_pairs that disagrees with the preprocess gets past it
-            keys[out] = ty * (uint32_t)tiles_x + tx;
-            vals[out] = sgid[lo];
+        wave_lds_fence();
+        const int m = wave_max_scan(mark[lane]);
+        const int slot = first + m;
+        const uint32_t p = p0 + lane;
+        if (p < q1) {
+            const uint32_t i = p - soff[slot];
+            const uint32_t w = swid[slot];
+            const uint32_t q = i / w;
+            const uint32_t org = sorg[slot];
+            const uint32_t tx = (org & 0xFFFFu) + (i - q * w);
+            const uint32_t ty = (org >> 16) + q;
+            const uint32_t out = gbase + p;
+            if (out < capacity) {   // only a num_pairs that disagrees with the preprocess gets past it
+                keys[out] = ty * (uint32_t)tiles_x + tx;
+                vals[out] = sgid[slot];
+            }
         }
+        // the next round starts with the Gaussian holding pair p0 + 64: the last
+        // lane's, or the one after it if that ends exactly there
+        const int last = first + __builtin_amdgcn_readlane(m, kWave - 1);
+        first = last + (soff[last + 1] == p0 + kWave ? 1 : 0);
+        wave_lds_fence();   // this round's mark reads before the next round's clear
     }
 }
 
@@ -342,17 +405,22 @@ __global__ __launch_bounds__(kBlock) void k_ranges(const uint32_t* __restrict__ 
 
 }  // namespace
 
-hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const Workspace& ws, const uint32_t** order_out,
-                             hipStream_t s)
+hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_splat* splats, const Workspace& ws,
+                             const uint32_t** order_out, hipStream_t s)
 {
     const uint32_t* kin = depth_key;
     const uint32_t* vin = nullptr;
     uint32_t* kbuf[2] = {ws.keys_a, ws.keys_b};
     uint32_t* vbuf[2] = {ws.vals_a, ws.vals_b};
     for (int p = 0; p < 4; ++p) {
-        uint32_t* kout = p == 3 ? nullptr : kbuf[p & 1];
-        hipError_t e = radix_pass(kin, vin, (uint64_t)n, 8 * p, 8, kout, vbuf[p & 1], ws.hist,
-                                  ws.digit_tot + kRadix * p, s);
+        const bool last = p == 3;
+        uint32_t* kout = last ? nullptr : kbuf[p & 1];
+        if (last)
+            radix_pass_t<8>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s,
+                            splats, ws.sorted_rect);
+        else
+            radix_pass_t<8>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s);
+        hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         kin = kbuf[p & 1];
         vin = vbuf[p & 1];
@@ -361,11 +429,10 @@ hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const Workspa
     return hipSuccess;
 }
 
-hipError_t launch_pair_offsets(int64_t n, const uint32_t* order, const uint32_t* tiles_touched, const Workspace& ws,
-                               hipStream_t s)
+hipError_t launch_pair_offsets(int64_t n, const Workspace& ws, hipStream_t s)
 {
     const int nb = (int)div_up(n, kDupChunk);
-    hipLaunchKernelGGL(k_pair_partial, dim3(nb), dim3(kBlock), 0, s, order, tiles_touched, n, ws.scan_part);
+    hipLaunchKernelGGL(k_pair_partial, dim3(nb), dim3(kBlock), 0, s, ws.sorted_rect, n, ws.scan_part);
     hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kBlock), 0, s, ws.scan_part, nb);
     return hipGetLastError();
 }
@@ -375,8 +442,8 @@ hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, co
                             hipStream_t s)
 {
     const int nb = (int)div_up(n, kDupChunk);
-    hipLaunchKernelGGL(k_duplicate, dim3(nb), dim3(kBlock), 0, s, order, pre.tiles_touched, pre.splats, n,
-                       ws.scan_part, cam.tiles_x, capacity, keys_out, vals_out);
+    hipLaunchKernelGGL(k_duplicate, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
+                       cam.tiles_x, capacity, keys_out, vals_out);
     return hipGetLastError();
 }
 

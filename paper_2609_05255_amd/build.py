@@ -25,6 +25,9 @@ COMMON = [
     "-fhip-fp32-correctly-rounded-divide-sqrt",  # the preprocess geometry needs IEEE / and sqrt
     "-fno-gpu-flush-denormals-to-zero",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # the blend backward's atomics come from one lane per wave: no wave-level
+    # pre-reduction loop around them
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-I", os.path.join(HERE, "..", "include"),
 ]
 

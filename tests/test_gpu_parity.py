@@ -139,3 +139,18 @@ def test_ragged_latent_with_background():
 def test_medium_scene_latent():
     sc = inputs.make_scene("medium", appearance=("latent",))
     check_all(sc, inputs.make_cameras("medium")[2], kind="latent", label="medium latent cam 2")
+
+
+def test_binning_one_tile_and_huge_gaussians():
+    # 6000 Gaussians so small that nearly all touch one tile (a window of 64
+    # consecutive pairs then holds up to 64 Gaussians), plus a few so large
+    # they cover the whole 96x80 image; pairs span several emission chunks
+    import dataclasses
+    # (the scene's own anisotropic log-scales, shifted: with equal axes the
+    # covariance would not depend on the rotation and the exact quaternion
+    # gradient would be zero, leaving only rounding to compare)
+    sc = inputs.make_scene("tiny", n=6000)
+    ls = (sc.log_scales - np.float32(3.5)).astype(np.float32)
+    ls[:, ::997] += np.float32(6.0)
+    sc = dataclasses.replace(sc, log_scales=ls)
+    check_all(sc, tiny_camera(96, 80), label="one-tile+huge")

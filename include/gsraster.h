@@ -97,7 +97,7 @@ typedef struct gs_appearance {
 } gs_appearance;
 
 /* Screen-space record of one Gaussian, written by gs_preprocess (64 bytes).
- * Only meaningful where tiles_touched[i] > 0 (other records are not written).
+ * Only meaningful where tiles_touched[i] > 0 (other records are written as zeros).
  * power_min, ext_x and ext_y only let the blend skip work early: below
  * power_min the alpha is certainly under 1/255 (a margin of 1e-3 in power), and
  * every pixel centre where the power reaches power_min lies within ext_x / ext_y

@@ -308,6 +308,7 @@ __device__ __forceinline__ void mlp_stage_row(MlpWaveStage& st, bool valid, cons
     for (int q = 0; q < 8; ++q) *reinterpret_cast<half4_t*>(&st.x[l][4 * q]) = v[q];
 #pragma unroll
     for (int ch = 0; ch < 3; ++ch) st.dc[l][ch] = valid ? dc[ch] : 0.f;
+    st.dc[l][3] = 0.f;   // padding column: fragments read it where a channel 3 would sit
 }
 
 // B fragment of tile t from the stage: features s(g, 0..7) of Gaussian 16t + c.
@@ -361,14 +362,18 @@ __device__ __forceinline__ void mlp_tile_bwd(const MlpFrags& W, MlpWaveStage& st
     // scaled output gradients: neuron-major (channel 4g + i of Gaussian c, only
     // g = 0 carries channels) and Gaussian-major (Gaussian 4g + i, channel c);
     // a culled Gaussian's staged colour gradient is zero
-    float4_t d3n, d3g;
+    float4_t d3n = zero, d3g;
     const int cn = min(c, 3);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const float sn = sigmoid_fast(on[i]), sg = sigmoid_fast(og[i]);
+    for (int i = 0; i < GS_MLP_OUT; ++i) {
+        const float sn = sigmoid_fast(on[i]);
         const float dcn = st.dc[16 * t + c][i];
-        const float dcg = st.dc[16 * t + 4 * g + i][cn];
         d3n[i] = g == 0 ? dcn * scale * (sn * (1.f - sn)) : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float sg = sigmoid_fast(og[i]);
+        const float dcg = st.dc[16 * t + 4 * g + i][cn];
         d3g[i] = c < GS_MLP_OUT ? dcg * scale * (sg * (1.f - sg)) : 0.f;
     }
     half4_t d3n_hi, d3n_lo;

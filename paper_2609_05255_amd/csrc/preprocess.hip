@@ -158,17 +158,43 @@ __device__ __forceinline__ void skip_fields(const Geo& g, float& pmin, float& ex
     ey = sqrtf(r2 * g.var_y) * 1.001f + 0.01f;
 }
 
-__device__ __forceinline__ void store_splat(gs_splat* dst, const Geo& g, const float col[3])
+// Per-wave staging of the 64 splat records of a wave (4 KB).
+struct SplatStage {
+    float4 q[kWave * 4];
+};
+
+// Writes the wave's 64 consecutive records (Gaussians first .. first + 63)
+// through LDS, so that each store instruction covers 1 KB of contiguous
+// memory instead of 16 bytes at a 64-byte stride. Culled Gaussians get a zero
+// record. Called by all lanes of the wave.
+__device__ __forceinline__ void store_splats_wave(gs_splat* __restrict__ splats, int64_t n, int64_t first,
+                                                  SplatStage& st, const Geo& g, const float col[3])
 {
-    float pmin, ex, ey;
-    skip_fields(g, pmin, ex, ey);
-    float4* p = reinterpret_cast<float4*>(dst);
-    p[0] = make_float4(g.mx, g.my, g.ca, g.cb);
-    p[1] = make_float4(g.cc, g.op, col[0], col[1]);
-    p[2] = make_float4(col[2], pmin, ex, ey);
-    const uint32_t r01 = (uint32_t)(g.x0 & 0xFFFF) | ((uint32_t)g.y0 << 16);
-    const uint32_t r23 = (uint32_t)(g.x1 & 0xFFFF) | ((uint32_t)g.y1 << 16);
-    p[3] = make_float4(__uint_as_float(r01), __uint_as_float(r23), g.depth, 0.f);
+    const int l = __lane_id();
+    float4 r0 = make_float4(0.f, 0.f, 0.f, 0.f), r1 = r0, r2 = r0, r3 = r0;
+    if (g.visible) {
+        float pmin, ex, ey;
+        skip_fields(g, pmin, ex, ey);
+        r0 = make_float4(g.mx, g.my, g.ca, g.cb);
+        r1 = make_float4(g.cc, g.op, col[0], col[1]);
+        r2 = make_float4(col[2], pmin, ex, ey);
+        const uint32_t r01 = (uint32_t)(g.x0 & 0xFFFF) | ((uint32_t)g.y0 << 16);
+        const uint32_t r23 = (uint32_t)(g.x1 & 0xFFFF) | ((uint32_t)g.y1 << 16);
+        r3 = make_float4(__uint_as_float(r01), __uint_as_float(r23), g.depth, 0.f);
+    }
+    st.q[4 * l] = r0;
+    st.q[4 * l + 1] = r1;
+    st.q[4 * l + 2] = r2;
+    st.q[4 * l + 3] = r3;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    float4* dst = reinterpret_cast<float4*>(splats + first);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int e = kWave * k + l;          // 16-byte piece of the wave's 4 KB
+        if (first + (e >> 2) < n) dst[e] = st.q[e];
+    }
 }
 
 // Sum of a u32 over the workgroup; result valid in thread 0.
@@ -222,23 +248,26 @@ __device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n
 __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
 {
     __shared__ uint32_t red[4];
+    __shared__ SplatStage stage[kBlock / kWave];
     const int i = blockIdx.x * kBlock + threadIdx.x;
     uint32_t tiles = 0;
+    Geo g;
+    g.visible = false;
+    float col[3] = {0.f, 0.f, 0.f};
     if (i < a.n) {
         float mu[3], ls[3], q[4], logit;
         load_geometry_params(a, i, mu, ls, q, logit);
-        Geo g;
         geometry(a.cam, mu, ls, q, logit, g);
         if (g.visible) {
-            float d[3], col[3];
+            float d[3];
             view_dir(a.cam, mu, d);
             sh_color(a.sh, a.n, i, a.sh_degree, d, col);
-            store_splat(a.splats + i, g, col);
             tiles = g.tiles;
         }
         a.tiles_touched[i] = tiles;
         a.depth_key[i] = g.visible ? __float_as_uint(g.depth) : 0xFFFFFFFFu;
     }
+    store_splats_wave(a.splats, a.n, (int64_t)i - __lane_id(), stage[threadIdx.x >> 6], g, col);
     const uint32_t total = block_sum_u32(tiles, red);
     if (threadIdx.x == 0) a.block_pairs[blockIdx.x] = total;
 }
@@ -252,6 +281,7 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_latent(PreArgs a)
 {
     __shared__ uint32_t red[4];
     __shared__ MlpFrags W;
+    __shared__ SplatStage stage[kBlock / kWave];
     mlp_load_frags(a.mlp_w, W, false);
     const int nchunks = (int)div_up(a.n, kBlock);
     for (int chunk = blockIdx.x; chunk < nchunks; chunk += gridDim.x) {
@@ -287,7 +317,7 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_latent(PreArgs a)
             mlp_tile_fwd(W, x, h1, a1, h2, a2, o);
             mlp_tile_colors(o, t, col);
         }
-        if (g.visible) store_splat(a.splats + i, g, col);
+        store_splats_wave(a.splats, a.n, (int64_t)i - __lane_id(), stage[threadIdx.x >> 6], g, col);
         const uint32_t total = block_sum_u32(tiles, red);
         if (threadIdx.x == 0) a.block_pairs[chunk] = total;
     }

@@ -92,3 +92,20 @@ def test_round_half_matches_numpy(orc):
         expect = float(np.float64(v).astype(np.float16))
         got = orc.round_half(float(v))
         assert (got == expect) or (math.isinf(got) and math.isinf(expect) and got == expect), (v, got, expect)
+
+
+def test_paper_printed_values(orc):
+    """Values printed in the paper (tests/golden/paper_printed_values.json)."""
+    import json
+    import os
+    with open(os.path.join(os.path.dirname(__file__), "golden", "paper_printed_values.json")) as f:
+        gold = json.load(f)
+    d = np.array([0.3, -0.5, 0.8])
+    y, _ = orc.sh_basis(d / np.linalg.norm(d))
+    g = gold["sh_y0"]
+    assert round(float(y[0]), g["decimals"]) == g["value"]
+    # degree-3 SH: 16 basis functions per colour channel, fp32
+    assert len(y) * 3 * 4 == gold["sh3_appearance_bytes"]["value"]
+    from paper_2609_05255_amd import inputs
+    sc = inputs.make_scene("tiny", n=8, appearance=("latent",))
+    assert sc.latent.shape[0] * sc.latent.dtype.itemsize == gold["latent_appearance_bytes_measured_decoder"]["value"]

@@ -21,7 +21,7 @@ constexpr int kXcds = 8;
 
 // Pixels per lane of the forward and the backward (1, 2 or 4).
 #ifndef GS_FWD_PIX
-#define GS_FWD_PIX 1
+#define GS_FWD_PIX 2
 #endif
 #ifndef GS_BWD_PIX
 #define GS_BWD_PIX 4
@@ -96,17 +96,13 @@ __device__ __forceinline__ float quad_power(const Quad& q, float dy)
     return __fmaf_rn(__fmaf_rn(q.q2, dy, q.q1), dy, q.q0);
 }
 
-// Sum over the wave; the total is valid in lane 63. Row-local steps use
-// quad_perm, row_half_mirror and row_mirror; rows are joined with
-// row_bcast:15 and row_bcast:31 (rows not selected by the mask add 0).
-__device__ __forceinline__ float wave_sum_to_lane63(float v)
+// Sum over the 16 lanes of each row, in every lane of the row.
+__device__ __forceinline__ float row_sum(float v)
 {
     v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
     v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
     v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
     v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
     return v;
 }
 
@@ -120,21 +116,22 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
                                                                     float* __restrict__ final_T,
                                                                     uint32_t* __restrict__ n_contrib)
 {
-    constexpr int kRowStep = kTile / kPix;
+    constexpr int kRowStep = 4;   // pixel k of a lane lies 4k rows below its first
     const int n_tiles = cam.tiles_x * cam.tiles_y;
     const int tile = tile_of_block(blockIdx.x, n_tiles);
     if (tile >= n_tiles) return;
     const int lane = __lane_id();
     const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
-    const int x = tx * kTile + (threadIdx.x & 15);
-    const int y0 = ty * kTile + (threadIdx.x >> 4);
+    // wave w covers the 4 kPix contiguous rows starting at 4 kPix w
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int x = tx * kTile + (lane & 15);
+    const int y0 = ty * kTile + 4 * kPix * wave + (lane >> 4);
     const float px = (float)x + 0.5f;
     const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
-    // box of this wave's pixel centres: 16 columns, rows 4w .. 4w + 3 + (16/kPix)(kPix - 1)
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // box of this wave's pixel centres: 16 columns, 4 kPix rows
     const float box_cx = (float)(tx * kTile) + 8.f, box_hx = 7.5f;
-    const float box_lo = (float)(ty * kTile + 4 * wave) + 0.5f;
-    const float box_hi = box_lo + (float)(3 + kRowStep * (kPix - 1));
+    const float box_lo = (float)(ty * kTile + 4 * kPix * wave) + 0.5f;
+    const float box_hi = box_lo + (float)(4 * kPix - 1);
     const float box_cy = 0.5f * (box_lo + box_hi), box_hy = 0.5f * (box_hi - box_lo);
 
     float T[kPix], C0[kPix], C1[kPix], C2[kPix], py[kPix];
@@ -234,19 +231,23 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                                                                     const float* __restrict__ dL_dimage,
                                                                     float* __restrict__ acc)
 {
-    constexpr int kRowStep = kTile / kPix;
+    constexpr int kRowStep = 4;   // pixel k of a lane lies 4k rows below its first
     const int n_tiles = cam.tiles_x * cam.tiles_y;
     const int tile = tile_of_block(blockIdx.x, n_tiles);
     if (tile >= n_tiles) return;
     const int lane = __lane_id();
     const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
-    const int x = tx * kTile + (threadIdx.x & 15);
-    const int y0 = ty * kTile + (threadIdx.x >> 4);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int row_lane = lane & 15;
+    const int x = tx * kTile + row_lane;
+    const int y0 = ty * kTile + 4 * kPix * wave + (lane >> 4);
     const float px = (float)x + 0.5f;
     const uint32_t start = ranges[2 * tile], len = ranges[2 * tile + 1] - start;
     const int64_t hw = (int64_t)cam.width * cam.height;
 
-    float T[kPix], py[kPix], g0[kPix], g1[kPix], g2[kPix], S0[kPix], S1[kPix], S2[kPix];
+    // Sg: the suffix sum S projected on the pixel's upstream gradient g, the
+    // only form of S the gradient needs
+    float T[kPix], py[kPix], g0[kPix], g1[kPix], g2[kPix], Sg[kPix];
     uint32_t last[kPix];
     uint32_t stop = 0;
 #pragma unroll
@@ -264,9 +265,7 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             g1[k] = dL_dimage[hw + pix];
             g2[k] = dL_dimage[2 * hw + pix];
         }
-        S0[k] = T[k] * cam.bg[0];
-        S1[k] = T[k] * cam.bg[1];
-        S2[k] = T[k] * cam.bg[2];
+        Sg[k] = T[k] * __fmaf_rn(cam.bg[2], g2[k], __fmaf_rn(cam.bg[1], g1[k], cam.bg[0] * g0[k]));
         stop = max(stop, last[k]);
     }
     // list positions [0, stop) can contribute
@@ -293,10 +292,11 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             const float dx = px - s.mx;
             const Quad q = column_quad(s, dx);
             // per-lane sums over its pixels: colour gradient, opacity gradient, and
-            // the moments of dL/dpower (dpow dx, dpow dy, dpow dx^2, dpow dx dy,
-            // dpow dy^2) from which dmean2d and dconic follow once per splat
+            // dL/dpower times 1, dy, dy^2 (the lane's pixels share dx), from which
+            // the moments dpow dx, dpow dy, dpow dx^2, dpow dx dy, dpow dy^2 and
+            // then dmean2d and dconic follow once per splat
             float a_c0 = 0.f, a_c1 = 0.f, a_c2 = 0.f, a_dop = 0.f;
-            float m_x = 0.f, m_y = 0.f, m_xx = 0.f, m_xy = 0.f, m_yy = 0.f;
+            float p0 = 0.f, p1 = 0.f, p2 = 0.f;
             bool any = false;
 #pragma unroll
             for (int k = 0; k < kPix; ++k) {
@@ -318,45 +318,42 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                 a_c1 = __fmaf_rn(w, g1[k], a_c1);
                 a_c2 = __fmaf_rn(w, g2[k], a_c2);
                 const float cg = __fmaf_rn(s.b, g2[k], __fmaf_rn(s.g, g1[k], s.r * g0[k]));
-                const float sg = __fmaf_rn(S2[k], g2[k], __fmaf_rn(S1[k], g1[k], S0[k] * g0[k]));
-                const float dalpha = __fmaf_rn(T[k], cg, -inv * sg);
-                S0[k] = __fmaf_rn(s.r, w, S0[k]);
-                S1[k] = __fmaf_rn(s.g, w, S1[k]);
-                S2[k] = __fmaf_rn(s.b, w, S2[k]);
+                const float dalpha = __fmaf_rn(T[k], cg, -inv * Sg[k]);
+                Sg[k] = __fmaf_rn(w, cg, Sg[k]);
                 if (oG < kAlphaMax) {                       // below the cap alpha = o G
                     a_dop = __fmaf_rn(G, dalpha, a_dop);
                     const float dpow = alpha * dalpha;
-                    const float pdx = dpow * dx, pdy = dpow * dy;
-                    m_x += pdx;
-                    m_y += pdy;
-                    m_xx = __fmaf_rn(pdx, dx, m_xx);
-                    m_xy = __fmaf_rn(pdx, dy, m_xy);
-                    m_yy = __fmaf_rn(pdy, dy, m_yy);
+                    const float pdy = dpow * dy;
+                    p0 += dpow;
+                    p1 += pdy;
+                    p2 = __fmaf_rn(pdy, dy, p2);
                 }
             }
             if (__ballot(any) == 0) continue;
-            m_x = wave_sum_to_lane63(m_x);
-            m_y = wave_sum_to_lane63(m_y);
-            m_xx = wave_sum_to_lane63(m_xx);
-            m_xy = wave_sum_to_lane63(m_xy);
-            m_yy = wave_sum_to_lane63(m_yy);
-            a_dop = wave_sum_to_lane63(a_dop);
-            a_c0 = wave_sum_to_lane63(a_c0);
-            a_c1 = wave_sum_to_lane63(a_c1);
-            a_c2 = wave_sum_to_lane63(a_c2);
-            if (lane == kWave - 1) {
-                // power = -(a dx^2 + c dy^2)/2 - b dx dy with dx = px - mean_x
-                float* a = acc + (size_t)s.id * kAccStride;
-                atomicAdd(a + 0, __fmaf_rn(s.ca, m_x, s.cb * m_y));
-                atomicAdd(a + 1, __fmaf_rn(s.cc, m_y, s.cb * m_x));
-                atomicAdd(a + 2, -0.5f * m_xx);
-                atomicAdd(a + 3, -m_xy);
-                atomicAdd(a + 4, -0.5f * m_yy);
-                atomicAdd(a + 5, a_dop);
-                atomicAdd(a + 6, a_c0);
-                atomicAdd(a + 7, a_c1);
-                atomicAdd(a + 8, a_c2);
-            }
+            // the lane's share of the nine accumulator entries; power = -(a dx^2
+            // + c dy^2)/2 - b dx dy with dx = px - mean_x, so dmean2d = (a m_x +
+            // b m_y, c m_y + b m_x) and dconic = -(m_xx / 2, m_xy, m_yy / 2)
+            const float m_x = dx * p0;
+            float v[kAccStride];
+            v[0] = __fmaf_rn(s.ca, m_x, s.cb * p1);
+            v[1] = __fmaf_rn(s.cc, p1, s.cb * m_x);
+            v[2] = -0.5f * dx * m_x;
+            v[3] = -dx * p1;
+            v[4] = -0.5f * p2;
+            v[5] = a_dop;
+            v[6] = a_c0;
+            v[7] = a_c1;
+            v[8] = a_c2;
+            // sums within each row of 16 lanes, then lane j of a row keeps entry
+            // j and the four rows are added across
+#pragma unroll
+            for (int e = 0; e < kAccStride; ++e) v[e] = row_sum(v[e]);
+            float t = v[0];
+#pragma unroll
+            for (int e = 1; e < kAccStride; ++e) t = row_lane == e ? v[e] : t;
+            t += __shfl_xor(t, 16);
+            t += __shfl_xor(t, 32);
+            if (lane < kAccStride) atomicAdd(acc + (size_t)s.id * kAccStride + lane, t);
         }
         cur = nxt;
     }

@@ -231,20 +231,28 @@ __device__ __forceinline__ void view_dir(const Cam& c, const float mu[3], float 
 
 }  // namespace
 
-// eq. sh_color_eval: c = max(0, 0.5 + sum over bands <= degree of Y_k(d) sh_k).
-__device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n, int i, int degree, const float d[3],
+// eq. sh_color_eval: c = max(0, 0.5 + sum over bands <= kDeg of Y_k(d) sh_k).
+// All coefficient loads are issued together, before the sums need them.
+template <int kDeg>
+__device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n, int i, const float d[3],
                                          float col[3])
 {
+    constexpr int nb = (kDeg + 1) * (kDeg + 1);
+    float c[3 * nb];
+#pragma unroll
+    for (int k = 0; k < 3 * nb; ++k) c[k] = sh[(int64_t)k * n + i];
     float Y[16];
     sh_basis16(d[0], d[1], d[2], Y);
-    const int nb = (degree + 1) * (degree + 1);
+#pragma unroll
     for (int ch = 0; ch < 3; ++ch) {
         float acc = 0.5f;
-        for (int k = 0; k < nb; ++k) acc += Y[k] * sh[(int64_t)(3 * k + ch) * n + i];
+#pragma unroll
+        for (int k = 0; k < nb; ++k) acc += Y[k] * c[3 * k + ch];
         col[ch] = acc > 0.f ? acc : 0.f;
     }
 }
 
+template <int kDeg>
 __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
 {
     __shared__ uint32_t red[4];
@@ -261,7 +269,7 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
         if (g.visible) {
             float d[3];
             view_dir(a.cam, mu, d);
-            sh_color(a.sh, a.n, i, a.sh_degree, d, col);
+            sh_color<kDeg>(a.sh, a.n, i, d, col);
             tiles = g.tiles;
         }
         a.tiles_touched[i] = tiles;
@@ -346,8 +354,14 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     a.depth_key = out.depth_key;
     a.block_pairs = ws.block_pairs;
     const int blocks = preprocess_blocks(g.n);
-    if (app.kind == GS_APP_SH3)
-        hipLaunchKernelGGL(k_preprocess_sh3, dim3(blocks), dim3(kBlock), 0, s, a);
+    if (app.kind == GS_APP_SH3) {
+        switch (app.sh_degree) {
+        case 0: hipLaunchKernelGGL(k_preprocess_sh3<0>, dim3(blocks), dim3(kBlock), 0, s, a); break;
+        case 1: hipLaunchKernelGGL(k_preprocess_sh3<1>, dim3(blocks), dim3(kBlock), 0, s, a); break;
+        case 2: hipLaunchKernelGGL(k_preprocess_sh3<2>, dim3(blocks), dim3(kBlock), 0, s, a); break;
+        default: hipLaunchKernelGGL(k_preprocess_sh3<3>, dim3(blocks), dim3(kBlock), 0, s, a); break;
+        }
+    }
     else
         hipLaunchKernelGGL(k_preprocess_latent, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
     return hipGetLastError();

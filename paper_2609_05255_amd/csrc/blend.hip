@@ -168,19 +168,22 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
             const Quad q = column_quad(s, dx);
 #pragma unroll
             for (int k = 0; k < kPix; ++k) {
-                if (!live[k]) continue;
+                // one branch per pixel; the alpha floor and the stop rule are
+                // selects inside it (the same decisions, fewer exec-mask changes)
                 const float power = quad_power(q, py[k] - s.my);
-                if (power > 0.f || power < s.pmin) continue;
+                if (!(live[k] && power <= 0.f && power >= s.pmin)) continue;
                 const float alpha = fminf(kAlphaMax, s.op * exp_fast(power));
-                if (alpha < kAlphaMin) continue;
                 const float Tn = T[k] * (1.f - alpha);
-                if (Tn < kTMin) { live[k] = false; continue; }
-                const float w = alpha * T[k];
+                const bool on = alpha >= kAlphaMin;
+                const bool stop = on && Tn < kTMin;
+                const bool blend = on && !stop;
+                const float w = blend ? alpha * T[k] : 0.f;
                 C0[k] = __fmaf_rn(s.r, w, C0[k]);
                 C1[k] = __fmaf_rn(s.g, w, C1[k]);
                 C2[k] = __fmaf_rn(s.b, w, C2[k]);
-                T[k] = Tn;
-                last[k] = b - start + (uint32_t)j + 1;
+                T[k] = blend ? Tn : T[k];
+                last[k] = blend ? b - start + (uint32_t)j + 1 : last[k];
+                live[k] = !stop;
             }
             any = false;
 #pragma unroll

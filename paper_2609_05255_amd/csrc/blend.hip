@@ -303,15 +303,16 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             bool any = false;
 #pragma unroll
             for (int k = 0; k < kPix; ++k) {
-                if (pos >= last[k]) continue;
+                // one branch per pixel; the alpha floor and the cap are selects
+                // inside it (the same decisions, fewer exec-mask changes)
                 const float dy = py[k] - s.my;
                 const float power = quad_power(q, dy);
-                if (power > 0.f || power < s.pmin) continue;
+                if (!(pos < last[k] && power <= 0.f && power >= s.pmin)) continue;
                 const float G = exp_fast(power);
                 const float oG = s.op * G;
-                const float alpha = fminf(kAlphaMax, oG);
-                if (alpha < kAlphaMin) continue;
-                any = true;
+                const bool on = oG >= kAlphaMin;             // alpha >= 1/255
+                const float alpha = on ? fminf(kAlphaMax, oG) : 0.f;
+                any = any || on;
                 // hardware reciprocal (1 ulp): T is recovered over a few hundred
                 // splats, so its relative error stays near 1e-5
                 const float inv = __builtin_amdgcn_rcpf(1.f - alpha);
@@ -323,14 +324,14 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                 const float cg = __fmaf_rn(s.b, g2[k], __fmaf_rn(s.g, g1[k], s.r * g0[k]));
                 const float dalpha = __fmaf_rn(T[k], cg, -inv * Sg[k]);
                 Sg[k] = __fmaf_rn(w, cg, Sg[k]);
-                if (oG < kAlphaMax) {                       // below the cap alpha = o G
-                    a_dop = __fmaf_rn(G, dalpha, a_dop);
-                    const float dpow = alpha * dalpha;
-                    const float pdy = dpow * dy;
-                    p0 += dpow;
-                    p1 += pdy;
-                    p2 = __fmaf_rn(pdy, dy, p2);
-                }
+                // below the cap alpha = o G; capped (or skipped) entries pass nothing
+                const bool unc = on && oG < kAlphaMax;
+                a_dop = unc ? __fmaf_rn(G, dalpha, a_dop) : a_dop;
+                const float dpow = unc ? alpha * dalpha : 0.f;
+                const float pdy = dpow * dy;
+                p0 += dpow;
+                p1 += pdy;
+                p2 = __fmaf_rn(pdy, dy, p2);
             }
             if (__ballot(any) == 0) continue;
             // the lane's share of the nine accumulator entries; power = -(a dx^2

@@ -134,24 +134,23 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
     const float box_hi = box_lo + (float)(4 * kPix - 1);
     const float box_cy = 0.5f * (box_lo + box_hi), box_hy = 0.5f * (box_hi - box_lo);
 
+    // T > 0 while the pixel still blends; the stop rule (and a pixel outside
+    // the image) makes it negative, |T| keeping the final transmittance
     float T[kPix], C0[kPix], C1[kPix], C2[kPix], py[kPix];
     uint32_t last[kPix];
-    bool live[kPix];
 #pragma unroll
     for (int k = 0; k < kPix; ++k) {
-        T[k] = 1.f;
         C0[k] = C1[k] = C2[k] = 0.f;
         last[k] = 0;
         py[k] = (float)(y0 + kRowStep * k) + 0.5f;
-        live[k] = x < cam.width && (y0 + kRowStep * k) < cam.height;
+        T[k] = (x < cam.width && (y0 + kRowStep * k) < cam.height) ? 1.f : -1.f;
     }
+    bool any = false;
+#pragma unroll
+    for (int k = 0; k < kPix; ++k) any = any || T[k] > 0.f;
     SplatReg cur;
     if (start + lane < end) cur = load_splat(splats, values[start + lane]);
-    for (uint32_t b = start; b < end; b += kWave) {
-        bool any = false;
-#pragma unroll
-        for (int k = 0; k < kPix; ++k) any = any || live[k];
-        if (__ballot(any) == 0) break;
+    for (uint32_t b = start; b < end && __ballot(any) != 0; b += kWave) {
         SplatReg nxt;
         if (b + kWave + lane < end) nxt = load_splat(splats, values[b + kWave + lane]);
         const int cnt = (int)min((uint32_t)kWave, end - b);
@@ -161,34 +160,36 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
             s.my = bcast(cur.my, j);
             s.ex = bcast(cur.ex, j);
             s.ey = bcast(cur.ey, j);
-            // the splat reaches alpha >= 1/255 nowhere in this wave's pixels
-            if (fabsf(s.mx - box_cx) > s.ex + box_hx || fabsf(s.my - box_cy) > s.ey + box_hy) continue;
-            bcast_rest(cur, j, s);
-            const float dx = px - s.mx;
-            const Quad q = column_quad(s, dx);
+            // skip the splat if it reaches alpha >= 1/255 nowhere in this wave's pixels
+            if (fabsf(s.mx - box_cx) <= s.ex + box_hx && fabsf(s.my - box_cy) <= s.ey + box_hy) {
+                bcast_rest(cur, j, s);
+                const float dx = px - s.mx;
+                const Quad q = column_quad(s, dx);
 #pragma unroll
-            for (int k = 0; k < kPix; ++k) {
-                // one branch per pixel; the alpha floor and the stop rule are
-                // selects inside it (the same decisions, fewer exec-mask changes)
-                const float power = quad_power(q, py[k] - s.my);
-                if (!(live[k] && power <= 0.f && power >= s.pmin)) continue;
-                const float alpha = fminf(kAlphaMax, s.op * exp_fast(power));
-                const float Tn = T[k] * (1.f - alpha);
-                const bool on = alpha >= kAlphaMin;
-                const bool stop = on && Tn < kTMin;
-                const bool blend = on && !stop;
-                const float w = blend ? alpha * T[k] : 0.f;
-                C0[k] = __fmaf_rn(s.r, w, C0[k]);
-                C1[k] = __fmaf_rn(s.g, w, C1[k]);
-                C2[k] = __fmaf_rn(s.b, w, C2[k]);
-                T[k] = blend ? Tn : T[k];
-                last[k] = blend ? b - start + (uint32_t)j + 1 : last[k];
-                live[k] = !stop;
+                for (int k = 0; k < kPix; ++k) {
+                    // one branch per pixel; the alpha floor and the stop rule are
+                    // selects inside it (the same decisions, fewer exec-mask changes)
+                    const float power = quad_power(q, py[k] - s.my);
+                    if (T[k] > 0.f && power <= 0.f && power >= s.pmin) {
+                        const float alpha = fminf(kAlphaMax, s.op * exp_fast(power));
+                        const float Tn = T[k] * (1.f - alpha);
+                        const bool on = alpha >= kAlphaMin;
+                        const bool stop = on && Tn < kTMin;
+                        const bool blend = on && !stop;
+                        const float w = blend ? alpha * T[k] : 0.f;
+                        C0[k] = __fmaf_rn(s.r, w, C0[k]);
+                        C1[k] = __fmaf_rn(s.g, w, C1[k]);
+                        C2[k] = __fmaf_rn(s.b, w, C2[k]);
+                        last[k] = blend ? b - start + (uint32_t)j + 1 : last[k];
+                        T[k] = stop ? -T[k] : (blend ? Tn : T[k]);
+                    }
+                }
+                // a pixel can only stop on a splat that reaches it
+                any = false;
+#pragma unroll
+                for (int k = 0; k < kPix; ++k) any = any || T[k] > 0.f;
+                if (__ballot(any) == 0) break;
             }
-            any = false;
-#pragma unroll
-            for (int k = 0; k < kPix; ++k) any = any || live[k];
-            if (__ballot(any) == 0) break;
         }
         cur = nxt;
     }
@@ -198,10 +199,11 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
         const int y = y0 + kRowStep * k;
         if (x >= cam.width || y >= cam.height) continue;
         const int64_t pix = (int64_t)y * cam.width + x;
-        image[pix] = __fmaf_rn(T[k], cam.bg[0], C0[k]);
-        image[hw + pix] = __fmaf_rn(T[k], cam.bg[1], C1[k]);
-        image[2 * hw + pix] = __fmaf_rn(T[k], cam.bg[2], C2[k]);
-        final_T[pix] = T[k];
+        const float Tf = fabsf(T[k]);
+        image[pix] = __fmaf_rn(Tf, cam.bg[0], C0[k]);
+        image[hw + pix] = __fmaf_rn(Tf, cam.bg[1], C1[k]);
+        image[2 * hw + pix] = __fmaf_rn(Tf, cam.bg[2], C2[k]);
+        final_T[pix] = Tf;
         n_contrib[pix] = last[k];
     }
 }

@@ -72,10 +72,17 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const uint32_t* __restric
     __syncthreads();
     const int wave = threadIdx.x >> 6;
     const uint64_t base = (uint64_t)blockIdx.x * kSortTile;
-#pragma unroll 4
+    // all loads first (one memory round trip), then the counts
+    uint32_t k[kSortItems];
+#pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
         const uint64_t idx = base + (uint64_t)r * kBlock + threadIdx.x;
-        if (idx < count) atomicAdd(&h[wave][(keys[idx] >> shift) & (R - 1)], 1u);
+        k[r] = idx < count ? keys[idx] : 0u;
+    }
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+        const uint64_t idx = base + (uint64_t)r * kBlock + threadIdx.x;
+        if (idx < count) atomicAdd(&h[wave][(k[r] >> shift) & (R - 1)], 1u);
     }
     __syncthreads();
     const int d = threadIdx.x;

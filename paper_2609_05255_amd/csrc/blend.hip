@@ -21,7 +21,7 @@ constexpr int kXcds = 8;
 
 // Pixels per lane of the forward and the backward (1, 2 or 4).
 #ifndef GS_FWD_PIX
-#define GS_FWD_PIX 2
+#define GS_FWD_PIX 4
 #endif
 #ifndef GS_BWD_PIX
 #define GS_BWD_PIX 4

@@ -96,6 +96,12 @@ __device__ __forceinline__ float quad_power(const Quad& q, float dy)
     return __fmaf_rn(__fmaf_rn(q.q2, dy, q.q1), dy, q.q0);
 }
 
+template <int kCtrl>
+__device__ __forceinline__ float dpp_f32(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, 0xF, 0xF, false));
+}
+
 // Sum over the 16 lanes of each row, in every lane of the row.
 __device__ __forceinline__ float row_sum(float v)
 {
@@ -244,6 +250,9 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
     const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int row_lane = lane & 15;
+    // lane bits of the butterfly reduction and the accumulator entry this lane adds
+    const bool b0 = lane & 1, b1 = lane & 2, b2 = lane & 4;
+    const int entry = (row_lane & 8) ? 8 : 4 * (lane & 1) + 2 * ((lane >> 1) & 1) + ((lane >> 2) & 1);
     const int x = tx * kTile + row_lane;
     const int y0 = ty * kTile + 4 * kPix * wave + (lane >> 4);
     const float px = (float)x + 0.5f;
@@ -350,16 +359,34 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             v[6] = a_c0;
             v[7] = a_c1;
             v[8] = a_c2;
-            // sums within each row of 16 lanes, then lane j of a row keeps entry
-            // j and the four rows are added across
+            // Row sums by butterfly: entries 0..7 halve per exchange (partner
+            // lane ^ 1, then ^ 2: each lane keeps half and adds the partner's
+            // copy of it), then the four lanes of a row with the same lane % 4
+            // are added (rotations by 4 and 8); entry 8 is summed plainly. Lane
+            // l < 8 of a row then holds entry bsel(l), lane 8 entry 8, and the
+            // four rows are added across.
+            float u[4];
 #pragma unroll
-            for (int e = 0; e < kAccStride; ++e) v[e] = row_sum(v[e]);
-            float t = v[0];
+            for (int i = 0; i < 4; ++i) {
+                const float keep = b0 ? v[4 + i] : v[i], give = b0 ? v[i] : v[4 + i];
+                u[i] = keep + dpp_f32<0xB1>(give);
+            }
+            float w2[2];
 #pragma unroll
-            for (int e = 1; e < kAccStride; ++e) t = row_lane == e ? v[e] : t;
+            for (int i = 0; i < 2; ++i) {
+                const float keep = b1 ? u[2 + i] : u[i], give = b1 ? u[i] : u[2 + i];
+                w2[i] = keep + dpp_f32<0x4E>(give);
+                w2[i] += dpp_f32<0x124>(w2[i]);
+                w2[i] += dpp_f32<0x128>(w2[i]);
+            }
+            // (the DPP row sum must run in every lane: a disabled source lane
+            // reads as zero, so it stays outside any condition)
+            const float s8 = row_sum(v[8]);
+            float t = b2 ? w2[1] : w2[0];
+            t = (row_lane & 8) ? s8 : t;
             t += __shfl_xor(t, 16);
             t += __shfl_xor(t, 32);
-            if (lane < kAccStride) atomicAdd(acc + (size_t)s.id * kAccStride + lane, t);
+            if (lane < kAccStride) atomicAdd(acc + (size_t)s.id * kAccStride + entry, t);
         }
         cur = nxt;
     }

@@ -154,21 +154,34 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
     bool any = false;
 #pragma unroll
     for (int k = 0; k < kPix; ++k) any = any || T[k] > 0.f;
-    SplatReg cur;
-    if (start + lane < end) cur = load_splat(splats, values[start + lane]);
+    // each batch of 64 list entries is staged in LDS; the wave then reads one
+    // record per step at a uniform address (a broadcast read: no vector
+    // instructions, unlike a lane-by-lane readlane broadcast)
+    __shared__ float4 stage[kTile * kTile / kPix / kWave][3][kWave];
+    float4 (*st)[kWave] = stage[wave];
+    float4 c0 = make_float4(0.f, 0.f, 0.f, 0.f), c1 = c0, c2 = c0;
+    if (start + lane < end) {
+        const float4* p = reinterpret_cast<const float4*>(splats + values[start + lane]);
+        c0 = p[0]; c1 = p[1]; c2 = p[2];
+    }
     for (uint32_t b = start; b < end && __ballot(any) != 0; b += kWave) {
-        SplatReg nxt;
-        if (b + kWave + lane < end) nxt = load_splat(splats, values[b + kWave + lane]);
+        st[0][lane] = c0; st[1][lane] = c1; st[2][lane] = c2;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (b + kWave + lane < end) {
+            const float4* p = reinterpret_cast<const float4*>(splats + values[b + kWave + lane]);
+            c0 = p[0]; c1 = p[1]; c2 = p[2];
+        }
         const int cnt = (int)min((uint32_t)kWave, end - b);
         for (int j = 0; j < cnt; ++j) {
             SplatReg s;
-            s.mx = bcast(cur.mx, j);
-            s.my = bcast(cur.my, j);
-            s.ex = bcast(cur.ex, j);
-            s.ey = bcast(cur.ey, j);
+            const float4 w0 = st[0][j], w2 = st[2][j];
+            s.mx = w0.x; s.my = w0.y; s.ex = w2.z; s.ey = w2.w;
             // skip the splat if it reaches alpha >= 1/255 nowhere in this wave's pixels
             if (fabsf(s.mx - box_cx) <= s.ex + box_hx && fabsf(s.my - box_cy) <= s.ey + box_hy) {
-                bcast_rest(cur, j, s);
+                const float4 w1 = st[1][j];
+                s.ca = w0.z; s.cb = w0.w; s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w; s.b = w2.x; s.pmin = w2.y;
                 const float dx = px - s.mx;
                 const Quad q = column_quad(s, dx);
 #pragma unroll
@@ -197,7 +210,9 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
                 if (__ballot(any) == 0) break;
             }
         }
-        cur = nxt;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
     const int64_t hw = (int64_t)cam.width * cam.height;
 #pragma unroll

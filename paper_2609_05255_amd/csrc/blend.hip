@@ -48,35 +48,6 @@ struct SplatReg {
     uint32_t id;
 };
 
-__device__ __forceinline__ SplatReg load_splat(const gs_splat* __restrict__ splats, uint32_t gid)
-{
-    const float4* p = reinterpret_cast<const float4*>(splats + gid);
-    const float4 w0 = p[0];
-    const float4 w1 = p[1];
-    const float4 w2 = p[2];
-    SplatReg s;
-    s.mx = w0.x; s.my = w0.y; s.ca = w0.z; s.cb = w0.w;
-    s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w;
-    s.b = w2.x; s.pmin = w2.y; s.ex = w2.z; s.ey = w2.w;
-    s.id = gid;
-    return s;
-}
-
-__device__ __forceinline__ float bcast(float v, int j)
-{
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), j));
-}
-
-// The fields the per-pixel work needs (mean and extents are broadcast first,
-// for the wave's overlap test).
-__device__ __forceinline__ void bcast_rest(const SplatReg& s, int j, SplatReg& t)
-{
-    t.ca = bcast(s.ca, j); t.cb = bcast(s.cb, j); t.cc = bcast(s.cc, j);
-    t.op = bcast(s.op, j);
-    t.r = bcast(s.r, j); t.g = bcast(s.g, j); t.b = bcast(s.b, j);
-    t.pmin = bcast(s.pmin, j);
-}
-
 // power(dy) = -(a dx^2 + c dy^2)/2 - b dx dy = q0 + dy (q1 + dy q2) for one column.
 struct Quad {
     float q0, q1, q2;
@@ -301,23 +272,45 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
     for (int o = 32; o > 0; o >>= 1) stop = max(stop, (uint32_t)__shfl_xor((int)stop, o));
     if (stop == 0) return;
     const int nbatch = (int)((stop + kWave - 1) / kWave);
-    SplatReg cur;
+    // each batch of 64 list entries is staged in LDS and read back one record
+    // per step at a uniform address (broadcast), as in the forward
+    __shared__ float4 stage[kTile * kTile / kPix / kWave][3][kWave];
+    __shared__ uint32_t stage_id[kTile * kTile / kPix / kWave][kWave];
+    float4 (*st)[kWave] = stage[wave];
+    uint32_t* sid = stage_id[wave];
+    float4 c0 = make_float4(0.f, 0.f, 0.f, 0.f), c1 = c0, c2 = c0;
+    uint32_t cid = 0;
     {
         const uint32_t p = (uint32_t)(nbatch - 1) * kWave + lane;
-        if (p < stop) cur = load_splat(splats, values[start + p]);
+        if (p < stop) {
+            cid = values[start + p];
+            const float4* r = reinterpret_cast<const float4*>(splats + cid);
+            c0 = r[0]; c1 = r[1]; c2 = r[2];
+        }
     }
     for (int bi = nbatch - 1; bi >= 0; --bi) {
         const uint32_t b = (uint32_t)bi * kWave;
-        SplatReg nxt;
-        if (bi > 0) nxt = load_splat(splats, values[start + b - kWave + lane]);
+        st[0][lane] = c0; st[1][lane] = c1; st[2][lane] = c2;
+        sid[lane] = cid;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (bi > 0) {
+            cid = values[start + b - kWave + lane];
+            const float4* r = reinterpret_cast<const float4*>(splats + cid);
+            c0 = r[0]; c1 = r[1]; c2 = r[2];
+        }
         const int cnt = (int)min((uint32_t)kWave, stop - b);
         for (int j = cnt - 1; j >= 0; --j) {
             const uint32_t pos = b + (uint32_t)j;
             SplatReg s;
-            s.mx = bcast(cur.mx, j);
-            s.my = bcast(cur.my, j);
-            bcast_rest(cur, j, s);
-            s.id = (uint32_t)__builtin_amdgcn_readlane((int)cur.id, j);
+            {
+                const float4 w0 = st[0][j], w1 = st[1][j], w2 = st[2][j];
+                s.mx = w0.x; s.my = w0.y; s.ca = w0.z; s.cb = w0.w;
+                s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w;
+                s.b = w2.x; s.pmin = w2.y;
+                s.id = sid[j];
+            }
             const float dx = px - s.mx;
             const Quad q = column_quad(s, dx);
             // per-lane sums over its pixels: colour gradient, opacity gradient, and
@@ -403,7 +396,9 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             t += __shfl_xor(t, 32);
             if (lane < kAccStride) atomicAdd(acc + (size_t)s.id * kAccStride + entry, t);
         }
-        cur = nxt;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
 }
 

@@ -1,12 +1,12 @@
 // Tile blend (Sec. 3.1) and its reverse. A 16x16 tile is covered by 4/PIX
-// independent wave64s, every lane owning PIX pixels of one column (thread t of
-// the workgroup: column t%16, rows t/16 + (16/PIX) k, k < PIX), so a lane's
-// pixels share dx and the quadratic form costs two fused multiply-adds per
-// pixel. Each wave walks the tile's depth-sorted list in batches of 64 splats:
-// every lane gathers one record into registers (the next batch is fetched
-// while the current one is blended), and the batch is then broadcast splat by
-// splat with readlane, i.e. as scalar operands. No LDS, no workgroup barriers;
-// a wave stops when its own pixels are done.
+// independent wave64s; wave w owns the 4 PIX contiguous rows from 4 PIX w, and
+// every lane PIX pixels of one column (rows 4k apart), so a lane's pixels
+// share dx and the quadratic form costs two fused multiply-adds per pixel.
+// Each wave walks the tile's depth-sorted list in batches of 64 splats: every
+// lane gathers one record (the next batch is fetched while the current one is
+// blended), the batch is staged in the wave's own LDS slot, and each splat is
+// then read back by the whole wave from one address (a broadcast read). No
+// workgroup barriers; a wave stops when its own pixels are done.
 //
 // Workgroup ids are mapped to tiles so that each XCD (workgroups are dealt
 // round-robin over the 8 XCDs) renders a contiguous band of tiles, whose lists

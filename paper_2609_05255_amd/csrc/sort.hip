@@ -52,14 +52,18 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* lds4, 
 template <int kBits>
 __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid)
 {
-    uint64_t m = __ballot(valid);
+    const uint64_t v = __ballot(valid);
+    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
 #pragma unroll
     for (int b = 0; b < kBits; ++b) {
-        const bool bit = (d >> b) & 1u;
+        const uint32_t bit = (d >> b) & 1u;
         const uint64_t bm = __ballot(bit);
-        m &= bit ? bm : ~bm;
+        const uint32_t s = 0u - bit;   // all ones where this lane's bit is set
+        // keep the lanes whose bit equals ours: bm where set, ~bm where clear
+        lo &= ~((uint32_t)bm ^ s);
+        hi &= ~((uint32_t)(bm >> 32) ^ s);
     }
-    return m;
+    return ((uint64_t)hi << 32) | lo;
 }
 
 template <int kBits>

@@ -181,7 +181,7 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     const int64_t nn = n > 0 ? n : 1;
     const int64_t cap = capacity > 0 ? (int64_t)capacity : 1;
     const int64_t sort_blocks = std::max(div_up(nn, kSortTile), div_up(cap, kSortTile));
-    w.block_pairs = (uint32_t*)take(sizeof(uint32_t) * preprocess_blocks(nn));
+    w.block_pairs = (uint32_t*)take(sizeof(uint32_t) * pair_count_slots(nn));
     w.keys_a = (uint32_t*)take(sizeof(uint32_t) * nn);
     w.keys_b = (uint32_t*)take(sizeof(uint32_t) * nn);
     w.vals_a = (uint32_t*)take(sizeof(uint32_t) * nn);
@@ -240,7 +240,7 @@ gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_ap
         GS_HIP(launch_preprocess(c, *g, *app, *out, ws, s));
         timing_end(GS_KERNEL_PREPROCESS, s);
         timing_begin(GS_KERNEL_PAIR_COUNT, s);
-        GS_HIP(launch_pair_count(g->n, ws, out->num_pairs, s));
+        GS_HIP(launch_pair_count(g->n, app->kind, ws, out->num_pairs, s));
         timing_end(GS_KERNEL_PAIR_COUNT, s);
     } else {
         GS_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(out->num_pairs), 2, 0u, s));

@@ -57,7 +57,7 @@ constexpr int kAccStride = 9;
 constexpr int kSortItems = 16;
 constexpr int kSortTile = kBlock * kSortItems;   // 4096
 constexpr int kRadix = 256;
-constexpr int kDupChunk = 2048;   // depth-ordered Gaussians per workgroup in pair emission
+constexpr int kDupChunk = 1024;   // depth-ordered Gaussians per workgroup in pair emission
 
 // Workgroups of the latent preprocess backward (grid-stride), one partial
 // weight gradient each.
@@ -69,7 +69,7 @@ inline size_t align_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
 // ---- workspace layout -------------------------------------------------------
 // One layout serves every call; gs_workspace_size returns its total.
 struct Workspace {
-    uint32_t* block_pairs;   // [nblocks_pre]     per-preprocess-block tile sums
+    uint32_t* block_pairs;   // [pair_count_slots] tile sums per preprocess workgroup or wave
     uint32_t* keys_a;        // [n]               depth-sort ping-pong keys
     uint32_t* keys_b;        // [n]
     uint32_t* vals_a;        // [n]               depth-sort values
@@ -92,7 +92,7 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
 // ---- launch helpers (defined in the kernel files) ---------------------------
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                              const gs_preprocessed& out, const Workspace& ws, hipStream_t s);
-hipError_t launch_pair_count(int64_t n, const Workspace& ws, uint64_t* num_pairs, hipStream_t s);
+hipError_t launch_pair_count(int64_t n, int32_t kind, const Workspace& ws, uint64_t* num_pairs, hipStream_t s);
 hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_splat* splats, const Workspace& ws,
                              const uint32_t** order_out, hipStream_t s);
 hipError_t launch_pair_offsets(int64_t n, const Workspace& ws, hipStream_t s);
@@ -123,5 +123,7 @@ void timing_begin(int kernel_id, hipStream_t s);
 void timing_end(int kernel_id, hipStream_t s);
 
 inline int preprocess_blocks(int64_t n) { return (int)div_up(n > 0 ? n : 1, kBlock); }
+// Slots for the preprocess tile sums (enough for one per 64 Gaussians).
+inline int pair_count_slots(int64_t n) { return (int)div_up(n > 0 ? n : 1, kWave); }
 
 }  // namespace gsr

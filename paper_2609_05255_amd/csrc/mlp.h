@@ -110,26 +110,39 @@ __device__ __forceinline__ _Float16 half_of_bits(uint16_t b) { return __builtin_
 // the wave's 64 Gaussians (index base + lane): features s(g, 0..7) of Gaussian
 // 16t + c, i.e. latent 4g..4g+3 (g < 3) or 12, 13, then d_x, d_y (g = 3), and
 // d_z in slot 4 of group 0, with the view direction rounded to binary16 (round
-// to nearest even). `d` is the calling lane's own direction; Gaussians whose
-// bit in `valid` is clear get zeros and load nothing.
-__device__ __forceinline__ half8_t mlp_input_frag(const uint16_t* __restrict__ latent, int64_t n, int64_t base,
-                                                  int t, uint64_t valid, const float d[3])
+// to nearest even). In two steps, so the loads can be issued long before the
+// view direction is known: mlp_latent_raw loads the lane's latent entries of
+// each tile (zeros past n), mlp_frag_from_raw completes a fragment with `d`,
+// the calling lane's own direction.
+struct MlpLatentRaw {
+    half4_t v[kWave / 16];
+};
+
+__device__ __forceinline__ void mlp_latent_raw(const uint16_t* __restrict__ latent, int64_t n, int64_t base,
+                                               MlpLatentRaw& r)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+#pragma unroll
+    for (int t = 0; t < kWave / 16; ++t) {
+        const int64_t gi = base + 16 * t + c;
+        const uint16_t* p = latent + (int64_t)(4 * g) * n + gi;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            r.v[t][j] = (gi < n && (g < 3 || j < 2)) ? half_of_bits(p[(int64_t)j * n]) : (_Float16)0.f;
+    }
+}
+
+__device__ __forceinline__ half8_t mlp_frag_from_raw(const MlpLatentRaw& r, int t, const float d[3])
 {
     const int l = __lane_id(), g = l >> 4, c = l & 15;
     const int src = 16 * t + c;
     const float dx = __shfl(d[0], src), dy = __shfl(d[1], src), dz = __shfl(d[2], src);
-    half8_t x = {0, 0, 0, 0, 0, 0, 0, 0};
-    if ((valid >> src) & 1) {
-        const uint16_t* p = latent + (int64_t)(4 * g) * n + base + src;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (g < 3 || j < 2) x[j] = half_of_bits(p[(int64_t)j * n]);
-        if (g == 3) {
-            x[2] = (_Float16)dx;
-            x[3] = (_Float16)dy;
-        }
-        if (g == 0) x[4] = (_Float16)dz;
+    half8_t x = {r.v[t][0], r.v[t][1], r.v[t][2], r.v[t][3], 0, 0, 0, 0};
+    if (g == 3) {
+        x[2] = (_Float16)dx;
+        x[3] = (_Float16)dy;
     }
+    if (g == 0) x[4] = (_Float16)dz;
     return x;
 }
 

@@ -197,11 +197,18 @@ __device__ __forceinline__ void store_splats_wave(gs_splat* __restrict__ splats,
     }
 }
 
-// Sum of a u32 over the workgroup; result valid in thread 0.
-__device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* lds4)
+// Sum of a u32 over the wave, in every lane.
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
 {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// Sum of a u32 over the workgroup; result valid in thread 0.
+__device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* lds4)
+{
+    v = wave_sum_u32(v);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     if (lane == 0) lds4[wave] = v;
     __syncthreads();
@@ -282,18 +289,23 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
 
 // Latent + MLP: geometry per thread, then each wave decodes the colours of its
 // visible Gaussians on the matrix cores, 16 at a time (mlp.h); tiles of 16
-// lanes without a visible Gaussian are skipped, culled lanes load nothing.
-// Workgroups loop over chunks of 256 Gaussians so the weight fragments are
-// staged once per workgroup.
-__global__ __launch_bounds__(kBlock) void k_preprocess_latent(PreArgs a)
+// lanes without a visible Gaussian are skipped. Each wave loops over chunks of
+// 64 Gaussians on its own (no workgroup barrier after the weight fragments are
+// staged), and issues a chunk's latent loads before its geometry, so that
+// their latency hides behind the projection arithmetic.
+__global__ __launch_bounds__(kBlock, 4) void k_preprocess_latent(PreArgs a)
 {
-    __shared__ uint32_t red[4];
     __shared__ MlpFrags W;
     __shared__ SplatStage stage[kBlock / kWave];
     mlp_load_frags(a.mlp_w, W, false);
-    const int nchunks = (int)div_up(a.n, kBlock);
-    for (int chunk = blockIdx.x; chunk < nchunks; chunk += gridDim.x) {
-        const int i = chunk * kBlock + threadIdx.x;
+    const int lane = __lane_id(), wave = threadIdx.x >> 6;
+    const int64_t nchunks = div_up((int64_t)a.n, kWave);
+    const int64_t stride = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t chunk = (int64_t)blockIdx.x * (kBlock / kWave) + wave; chunk < nchunks; chunk += stride) {
+        const int64_t base = chunk * kWave;
+        const int i = (int)(base + lane);
+        MlpLatentRaw raw;
+        mlp_latent_raw(a.latent, a.n, base, raw);
         uint32_t tiles = 0;
         Geo g;
         g.visible = false;
@@ -310,30 +322,24 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_latent(PreArgs a)
             a.depth_key[i] = g.visible ? __float_as_uint(g.depth) : 0xFFFFFFFFu;
         }
         const uint64_t vis = __ballot(g.visible);
-        const int64_t base = (int64_t)chunk * kBlock + (threadIdx.x & ~(kWave - 1));
-        // all four input fragments first, so their loads overlap
-        half8_t xs[kWave / 16];
-        for (int t = 0; t < kWave / 16; ++t)
-            xs[t] = ((vis >> (16 * t)) & 0xFFFFull) ? mlp_input_frag(a.latent, a.n, base, t, vis, d)
-                                                     : half8_t{0, 0, 0, 0, 0, 0, 0, 0};
         float col[3] = {0.f, 0.f, 0.f};
         for (int t = 0; t < kWave / 16; ++t) {
             if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
-            const half8_t x = xs[t];
+            const half8_t x = mlp_frag_from_raw(raw, t, d);
             float4_t h1[2], h2[2], o;
             half8_t a1, a2;
             mlp_tile_fwd(W, x, h1, a1, h2, a2, o);
             mlp_tile_colors(o, t, col);
         }
-        store_splats_wave(a.splats, a.n, (int64_t)i - __lane_id(), stage[threadIdx.x >> 6], g, col);
-        const uint32_t total = block_sum_u32(tiles, red);
-        if (threadIdx.x == 0) a.block_pairs[chunk] = total;
+        store_splats_wave(a.splats, a.n, base, stage[wave], g, col);
+        const uint32_t total = wave_sum_u32(tiles);
+        if (lane == 0) a.block_pairs[chunk] = total;
     }
 }
 
-// Workgroups of the latent preprocess: enough to fill the chip several times
-// over, each looping over chunks.
-constexpr int kLatentBlocks = 2048;
+// Workgroups of the latent preprocess: the number resident at once on 256 CUs
+// (four per CU at the kernel's register budget), each wave looping over chunks.
+constexpr int kLatentBlocks = 1024;
 
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                              const gs_preprocessed& out, const Workspace& ws, hipStream_t s)
@@ -367,12 +373,28 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     return hipGetLastError();
 }
 
-// Total pairs = sum of the per-block tile counts (fixed order, one workgroup).
-__global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs, int nblocks, uint64_t* out)
+// Total pairs = sum of the per-wave tile counts (fixed order, one workgroup).
+// The counts sit at the 256-byte-aligned start of their workspace slice, so
+// each thread reads runs of four with 16-byte loads, all issued before the sums.
+__global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs, int nslots, uint64_t* out)
 {
+    constexpr int kPer = 16;   // 16-byte loads in flight per thread and round
     __shared__ uint64_t red[16];
+    const uint4* v4 = reinterpret_cast<const uint4*>(block_pairs);
+    const int nvec = nslots >> 2;
     uint64_t v = 0;
-    for (int b = threadIdx.x; b < nblocks; b += 1024) v += block_pairs[b];
+    for (int b0 = 0; b0 < nvec; b0 += 1024 * kPer) {
+        uint4 q[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int b = b0 + k * 1024 + (int)threadIdx.x;
+            q[k] = b < nvec ? v4[b] : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) v += (uint64_t)q[k].x + q[k].y + q[k].z + q[k].w;
+    }
+    const int rest = (nvec << 2) + (int)threadIdx.x;
+    if (rest < nslots) v += block_pairs[rest];
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
@@ -384,9 +406,11 @@ __global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs
     }
 }
 
-hipError_t launch_pair_count(int64_t n, const Workspace& ws, uint64_t* num_pairs, hipStream_t s)
+hipError_t launch_pair_count(int64_t n, int32_t kind, const Workspace& ws, uint64_t* num_pairs, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_pair_count, dim3(1), dim3(1024), 0, s, ws.block_pairs, preprocess_blocks(n), num_pairs);
+    // the SH3 preprocess leaves one tile sum per workgroup, the latent one per wave
+    const int slots = kind == GS_APP_SH3 ? preprocess_blocks(n) : pair_count_slots(n);
+    hipLaunchKernelGGL(k_pair_count, dim3(1), dim3(1024), 0, s, ws.block_pairs, slots, num_pairs);
     return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ namespace gsr {
 namespace {
 
 constexpr int kSliceKeys = kSortTile / (kBlock / kWave);   // 1024 keys per wave
-constexpr int kDupItems = kDupChunk / kBlock;              // 8 per thread
+constexpr int kDupItems = kDupChunk / kBlock;              // 4 per thread
 
 __device__ __forceinline__ uint64_t lanemask_lt() { return (1ull << __lane_id()) - 1ull; }
 
@@ -297,13 +297,16 @@ __device__ __forceinline__ void wave_lds_fence()
 // Emits the (tile, Gaussian) pairs of a chunk of depth-ordered Gaussians, each
 // Gaussian's tiles in row-major order of its rectangle. The chunk's offsets
 // and rectangles are staged in LDS. Each wave then emits a contiguous quarter
-// of the chunk's pairs, 64 consecutive pairs per round (consecutive lanes write
-// consecutive addresses): the lanes mark in LDS where the Gaussians of the next
-// 63 slots start inside the round's window (after its first pair, which
-// belongs to the round's first Gaussian), and an inclusive maximum scan over
-// the lanes gives each pair its Gaussian. Depth order puts every culled
-// Gaussian (no tiles) after the visible ones, so starts inside a window are
-// distinct.
+// of the chunk's pairs, kDupWin consecutive pairs per round in groups of 64
+// (consecutive lanes write consecutive addresses): the lanes mark in LDS where
+// the Gaussians of the next kDupWin - 1 slots start inside the round's window
+// (after its first pair, which belongs to the round's first Gaussian), and an
+// inclusive maximum scan over the window gives each pair its Gaussian. Depth
+// order puts every culled Gaussian (no tiles) after the visible ones, so starts
+// inside a window are distinct.
+constexpr int kDupGroups = 8;                   // 64-pair groups per round
+constexpr int kDupWin = kWave * kDupGroups;     // pairs per round
+
 __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict__ order,
                                                       const uint2* __restrict__ sorted_rect, int64_t n,
                                                       const uint32_t* __restrict__ part, int tiles_x,
@@ -314,7 +317,7 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
     __shared__ uint32_t sgid[kDupChunk];
     __shared__ uint32_t sorg[kDupChunk];   // rectangle origin x0 | y0 << 16
     __shared__ uint32_t swid[kDupChunk];   // rectangle width in tiles
-    __shared__ int smark[kBlock / kWave][kWave];
+    __shared__ int smark[kBlock / kWave][kDupWin];
     __shared__ uint32_t lds4[4];
     const int t = threadIdx.x;
     const int64_t base = (int64_t)blockIdx.x * kDupChunk;
@@ -361,35 +364,57 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
     }
     int first = lo;
     int* mark = smark[wave];
-    for (uint32_t p0 = q0; p0 < q1; p0 += kWave) {
-        mark[lane] = lane == 0 ? 0 : -1;
+    for (uint32_t p0 = q0; p0 < q1; p0 += kDupWin) {
+#pragma unroll
+        for (int k = 0; k < kDupGroups; ++k) mark[kWave * k + lane] = (k == 0 && lane == 0) ? 0 : -1;
         wave_lds_fence();
-        const int sl = first + lane;
-        if (lane > 0 && sl < kDupChunk) {
-            const uint32_t o = soff[sl];
-            if (o > p0 && o < p0 + kWave && soff[sl + 1] > o) mark[o - p0] = lane;
-        }
-        wave_lds_fence();
-        const int m = wave_max_scan(mark[lane]);
-        const int slot = first + m;
-        const uint32_t p = p0 + lane;
-        if (p < q1) {
-            const uint32_t i = p - soff[slot];
-            const uint32_t w = swid[slot];
-            const uint32_t q = i / w;
-            const uint32_t org = sorg[slot];
-            const uint32_t tx = (org & 0xFFFFu) + (i - q * w);
-            const uint32_t ty = (org >> 16) + q;
-            const uint32_t out = gbase + p;
-            if (out < capacity) {   // only a num_pairs that disagrees with the preprocess gets past it
-                keys[out] = ty * (uint32_t)tiles_x + tx;
-                vals[out] = sgid[slot];
+#pragma unroll
+        for (int k = 0; k < kDupGroups; ++k) {
+            const int d = kWave * k + lane;   // slot offset from the round's first Gaussian
+            const int sl = first + d;
+            if (d > 0 && sl < kDupChunk) {
+                const uint32_t o = soff[sl];
+                if (o > p0 && o < p0 + kDupWin && soff[sl + 1] > o) mark[o - p0] = d;
             }
         }
-        // the next round starts with the Gaussian holding pair p0 + 64: the last
-        // lane's, or the one after it if that ends exactly there
-        const int last = first + __builtin_amdgcn_readlane(m, kWave - 1);
-        first = last + (soff[last + 1] == p0 + kWave ? 1 : 0);
+        wave_lds_fence();
+        // in stages, so each stage's LDS latency is paid once per round
+        int m[kDupGroups];
+#pragma unroll
+        for (int k = 0; k < kDupGroups; ++k) m[k] = mark[kWave * k + lane];
+        int run = 0;   // owner of the window's positions so far (mark[0] = 0)
+#pragma unroll
+        for (int k = 0; k < kDupGroups; ++k) {
+            m[k] = max(wave_max_scan(m[k]), run);
+            run = __builtin_amdgcn_readlane(m[k], kWave - 1);
+        }
+        uint32_t o[kDupGroups], w[kDupGroups], org[kDupGroups], gid[kDupGroups];
+#pragma unroll
+        for (int k = 0; k < kDupGroups; ++k) {
+            const int slot = first + m[k];
+            o[k] = soff[slot];
+            w[k] = swid[slot];
+            org[k] = sorg[slot];
+            gid[k] = sgid[slot];
+        }
+#pragma unroll
+        for (int k = 0; k < kDupGroups; ++k) {
+            const uint32_t p = p0 + kWave * k + lane;
+            const uint32_t i = p - o[k];
+            const uint32_t q = i / w[k];
+            const uint32_t tx = (org[k] & 0xFFFFu) + (i - q * w[k]);
+            const uint32_t ty = (org[k] >> 16) + q;
+            const uint32_t out = gbase + p;
+            // only a num_pairs that disagrees with the preprocess gets past the capacity
+            if (p < q1 && out < capacity) {
+                keys[out] = ty * (uint32_t)tiles_x + tx;
+                vals[out] = gid[k];
+            }
+        }
+        // the next round starts with the Gaussian holding pair p0 + kDupWin: the
+        // window's last owner, or the one after it if that ends exactly there
+        const int last = first + run;
+        first = last + (soff[last + 1] == p0 + kDupWin ? 1 : 0);
         wave_lds_fence();   // this round's mark reads before the next round's clear
     }
 }

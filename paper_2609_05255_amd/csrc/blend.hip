@@ -40,7 +40,6 @@ constexpr float kAlphaMax = 0.99f;
 constexpr float kTMin = 0.0001f;
 constexpr float kLog2e = 1.4426950408889634f;
 
-__device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp2f(x * kLog2e); }
 
 // One splat record in registers (the fields the blend needs).
 struct SplatReg {
@@ -48,7 +47,9 @@ struct SplatReg {
     uint32_t id;
 };
 
-// power(dy) = -(a dx^2 + c dy^2)/2 - b dx dy = q0 + dy (q1 + dy q2) for one column.
+// power(dy) = -(a dx^2 + c dy^2)/2 - b dx dy for one column, in base-2 units
+// (times log2 e) so that exp(power) is one hardware exp2:
+// power log2 e = q0 + dy (q1 + dy q2).
 struct Quad {
     float q0, q1, q2;
 };
@@ -56,9 +57,9 @@ struct Quad {
 __device__ __forceinline__ Quad column_quad(const SplatReg& s, float dx)
 {
     Quad q;
-    q.q0 = -0.5f * s.ca * dx * dx;
-    q.q1 = -s.cb * dx;
-    q.q2 = -0.5f * s.cc;
+    q.q0 = (-0.5f * kLog2e) * s.ca * dx * dx;
+    q.q1 = (-kLog2e * dx) * s.cb;
+    q.q2 = (-0.5f * kLog2e) * s.cc;
     return q;
 }
 
@@ -155,13 +156,14 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
                 s.ca = w0.z; s.cb = w0.w; s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w; s.b = w2.x; s.pmin = w2.y;
                 const float dx = px - s.mx;
                 const Quad q = column_quad(s, dx);
+                const float pmin2 = s.pmin * kLog2e;
 #pragma unroll
                 for (int k = 0; k < kPix; ++k) {
                     // one branch per pixel; the alpha floor and the stop rule are
                     // selects inside it (the same decisions, fewer exec-mask changes)
-                    const float power = quad_power(q, py[k] - s.my);
-                    if (T[k] > 0.f && power <= 0.f && power >= s.pmin) {
-                        const float alpha = fminf(kAlphaMax, s.op * exp_fast(power));
+                    const float power2 = quad_power(q, py[k] - s.my);
+                    if (T[k] > 0.f && power2 <= 0.f && power2 >= pmin2) {
+                        const float alpha = fminf(kAlphaMax, s.op * __builtin_amdgcn_exp2f(power2));
                         const float Tn = T[k] * (1.f - alpha);
                         const bool on = alpha >= kAlphaMin;
                         const bool stop = on && Tn < kTMin;
@@ -313,6 +315,7 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             }
             const float dx = px - s.mx;
             const Quad q = column_quad(s, dx);
+            const float pmin2 = s.pmin * kLog2e;
             // per-lane sums over its pixels: colour gradient, opacity gradient, and
             // dL/dpower times 1, dy, dy^2 (the lane's pixels share dx), from which
             // the moments dpow dx, dpow dy, dpow dx^2, dpow dx dy, dpow dy^2 and
@@ -325,9 +328,9 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                 // one branch per pixel; the alpha floor and the cap are selects
                 // inside it (the same decisions, fewer exec-mask changes)
                 const float dy = py[k] - s.my;
-                const float power = quad_power(q, dy);
-                if (!(pos < last[k] && power <= 0.f && power >= s.pmin)) continue;
-                const float G = exp_fast(power);
+                const float power2 = quad_power(q, dy);
+                if (!(pos < last[k] && power2 <= 0.f && power2 >= pmin2)) continue;
+                const float G = __builtin_amdgcn_exp2f(power2);
                 const float oG = s.op * G;
                 const bool on = oG >= kAlphaMin;             // alpha >= 1/255
                 const float alpha = on ? fminf(kAlphaMax, oG) : 0.f;

@@ -10,16 +10,16 @@
 //
 // One radix pass = k_radix_hist (per-workgroup digit counts) + k_radix_scan
 // (exclusive offsets per digit over workgroups) + k_radix_scatter: each wave
-// ranks a contiguous slice of 1024 keys with ballot-matched digits (no
-// workgroup barrier per round), the workgroup reorders its 4096 keys by digit
-// in LDS, and writes each digit's run to consecutive global addresses.
+// ranks a contiguous slice of the workgroup's keys with ballot-matched digits
+// (no workgroup barrier per round), the workgroup reorders its keys (4096 in
+// the depth sort, 6144 in the tile sort) by digit in LDS, and writes each
+// digit's run to consecutive global addresses.
 #include "gs_internal.h"
 
 namespace gsr {
 
 namespace {
 
-constexpr int kSliceKeys = kSortTile / (kBlock / kWave);   // 1024 keys per wave
 constexpr int kDupItems = kDupChunk / kBlock;              // 4 per thread
 
 __device__ __forceinline__ uint64_t lanemask_lt() { return (1ull << __lane_id()) - 1ull; }
@@ -66,25 +66,26 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid)
     return ((uint64_t)hi << 32) | lo;
 }
 
-template <int kBits>
+template <int kBits, int kItems>
 __global__ __launch_bounds__(kBlock) void k_radix_hist(const uint32_t* __restrict__ keys, uint64_t count, int shift,
                                                        uint32_t* __restrict__ hist, int nblocks)
 {
     constexpr int R = 1 << kBits;
+    constexpr int kTile = kBlock * kItems;
     __shared__ uint32_t h[4][R];
     for (int k = threadIdx.x; k < 4 * R; k += kBlock) (&h[0][0])[k] = 0;
     __syncthreads();
     const int wave = threadIdx.x >> 6;
-    const uint64_t base = (uint64_t)blockIdx.x * kSortTile;
+    const uint64_t base = (uint64_t)blockIdx.x * kTile;
     // all loads first (one memory round trip), then the counts
-    uint32_t k[kSortItems];
+    uint32_t k[kItems];
 #pragma unroll
-    for (int r = 0; r < kSortItems; ++r) {
+    for (int r = 0; r < kItems; ++r) {
         const uint64_t idx = base + (uint64_t)r * kBlock + threadIdx.x;
         k[r] = idx < count ? keys[idx] : 0u;
     }
 #pragma unroll
-    for (int r = 0; r < kSortItems; ++r) {
+    for (int r = 0; r < kItems; ++r) {
         const uint64_t idx = base + (uint64_t)r * kBlock + threadIdx.x;
         if (idx < count) atomicAdd(&h[wave][(k[r] >> shift) & (R - 1)], 1u);
     }
@@ -114,7 +115,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(uint32_t* __restrict__ hi
     if (threadIdx.x == 0) digit_tot[blockIdx.x] = total;
 }
 
-template <int kBits>
+template <int kBits, int kItems>
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __restrict__ keys_in,
                                                           const uint32_t* __restrict__ vals_in, uint64_t count,
                                                           int shift, const uint32_t* __restrict__ hist, int nblocks,
@@ -125,11 +126,13 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
                                                           uint2* __restrict__ rect_out)
 {
     constexpr int R = 1 << kBits;
+    constexpr int kTile = kBlock * kItems;
+    constexpr int kSlice = kTile / (kBlock / kWave);   // keys per wave
     __shared__ uint32_t wcnt[4][R];      // per-wave digit counts, then per-wave exclusive offsets
     __shared__ uint32_t gbase[R];        // global position of this workgroup's first key of each digit
     __shared__ uint32_t lstart[R];       // start of each digit in the workgroup's reordered keys
-    __shared__ uint32_t skey[kSortTile];
-    __shared__ uint32_t sval[kSortTile];
+    __shared__ uint32_t skey[kTile];
+    __shared__ uint32_t sval[kTile];
     __shared__ uint32_t lds4[4];
     const int t = threadIdx.x, wave = t >> 6, lane = __lane_id();
     const uint32_t dt = t < R ? digit_tot[t] : 0u;
@@ -140,18 +143,18 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
     }
     __syncthreads();
     // rank within the wave's slice, in key order
-    const uint64_t base = (uint64_t)blockIdx.x * kSortTile;
-    const uint64_t wbase = base + (uint64_t)wave * kSliceKeys;
-    uint32_t key[kSortItems], val[kSortItems], rank[kSortItems];
+    const uint64_t base = (uint64_t)blockIdx.x * kTile;
+    const uint64_t wbase = base + (uint64_t)wave * kSlice;
+    uint32_t key[kItems], val[kItems], rank[kItems];
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < kItems; ++i) {
         const uint64_t idx = wbase + (uint64_t)i * kWave + lane;
         const bool valid = idx < count;
         key[i] = valid ? keys_in[idx] : 0u;
         val[i] = valid ? (vals_in ? vals_in[idx] : (uint32_t)idx) : 0u;
     }
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < kItems; ++i) {
         const uint64_t idx = wbase + (uint64_t)i * kWave + lane;
         const bool valid = idx < count;
         const uint32_t d = (key[i] >> shift) & (R - 1);
@@ -177,7 +180,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
     if (t < R) lstart[t] = ls;
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < kSortItems; ++i) {
+    for (int i = 0; i < kItems; ++i) {
         const uint64_t idx = wbase + (uint64_t)i * kWave + lane;
         if (idx < count) {
             const uint32_t d = (key[i] >> shift) & (R - 1);
@@ -187,7 +190,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
         }
     }
     __syncthreads();
-    const uint32_t nvalid = (uint32_t)min((uint64_t)kSortTile, count - base);
+    const uint32_t nvalid = (uint32_t)min((uint64_t)kTile, count - base);
     for (uint32_t j = t; j < nvalid; j += kBlock) {
         const uint32_t k = skey[j];
         const uint32_t d = (k >> shift) & (R - 1);
@@ -207,15 +210,16 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
 
 // One stable LSD pass over `bits` bits at `shift`; vals_in == nullptr means
 // value = position, keys_out == nullptr drops the keys.
-template <int kBits>
+template <int kBits, int kItems>
 void radix_pass_t(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t count, int shift, uint32_t* keys_out,
                   uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s,
                   const gs_splat* rect_src = nullptr, uint2* rect_out = nullptr)
 {
-    const int nblocks = (int)div_up((int64_t)count, kSortTile);
-    hipLaunchKernelGGL(k_radix_hist<kBits>, dim3(nblocks), dim3(kBlock), 0, s, keys_in, count, shift, hist, nblocks);
+    const int nblocks = (int)div_up((int64_t)count, (int64_t)kBlock * kItems);
+    hipLaunchKernelGGL((k_radix_hist<kBits, kItems>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, count, shift, hist,
+                       nblocks);
     hipLaunchKernelGGL(k_radix_scan, dim3(1 << kBits), dim3(kBlock), 0, s, hist, nblocks, digit_tot);
-    hipLaunchKernelGGL(k_radix_scatter<kBits>, dim3(nblocks), dim3(kBlock), 0, s, keys_in, vals_in, count, shift,
+    hipLaunchKernelGGL((k_radix_scatter<kBits, kItems>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, vals_in, count, shift,
                        hist, nblocks, digit_tot, keys_out, vals_out, rect_src, rect_out);
 }
 
@@ -223,14 +227,14 @@ hipError_t radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t
                       uint32_t* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
 {
     switch (bits) {
-    case 1: radix_pass_t<1>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 2: radix_pass_t<2>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 3: radix_pass_t<3>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 4: radix_pass_t<4>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 5: radix_pass_t<5>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 6: radix_pass_t<6>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 7: radix_pass_t<7>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 8: radix_pass_t<8>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 1: radix_pass_t<1, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 2: radix_pass_t<2, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 3: radix_pass_t<3, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 4: radix_pass_t<4, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 5: radix_pass_t<5, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 6: radix_pass_t<6, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 7: radix_pass_t<7, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+    case 8: radix_pass_t<8, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -452,10 +456,10 @@ hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_spla
         const bool last = p == 3;
         uint32_t* kout = last ? nullptr : kbuf[p & 1];
         if (last)
-            radix_pass_t<8>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s,
+            radix_pass_t<8, kSortItems>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s,
                             splats, ws.sorted_rect);
         else
-            radix_pass_t<8>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s);
+            radix_pass_t<8, kSortItems>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         kin = kbuf[p & 1];

@@ -284,11 +284,13 @@ gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t 
     GS_HIP(launch_pair_offsets(n, ws, s));
     timing_end(GS_KERNEL_PAIR_OFFSETS, s);
     const int passes = tile_sort_passes(c);
-    const uint32_t* sorted_tiles = nullptr;
-    uint32_t* dup_keys = ws.pair_keys_a;
+    // tile ids travel as 16-bit keys through the sort when they fit; with a
+    // single tile there is no sort and the pair emission writes the 32-bit ids
+    TileKeys sorted_tiles{nullptr, false};
+    TileKeys dup_keys{ws.pair_keys_a, passes > 0 && tile_keys_narrow(c)};
     uint32_t* dup_vals = ws.pair_vals_a;
     if (passes == 0) {
-        dup_keys = tile_ids ? tile_ids : ws.pair_keys_a;
+        dup_keys.p = tile_ids ? tile_ids : ws.pair_keys_a;
         dup_vals = values;
         sorted_tiles = dup_keys;
     }

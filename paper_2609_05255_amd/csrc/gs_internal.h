@@ -81,7 +81,7 @@ struct Workspace {
     uint32_t* digit_tot;     // [4 passes][256]   digit totals of each pass
     uint32_t* scan_part;     // [n / kDupChunk + 1] chunk sums of the pair-offset scan
     uint2* sorted_rect;      // [n]               tile rectangles in depth order (empty for culled)
-    uint32_t* pair_keys_a;   // [capacity]
+    uint32_t* pair_keys_a;   // [capacity]        tile ids (16-bit in the first half when narrow)
     uint32_t* pair_vals_a;   // [capacity]
     uint32_t* pair_keys_b;   // [capacity]
     uint32_t* pair_vals_b;   // [capacity]
@@ -99,14 +99,20 @@ hipError_t launch_pair_count(int64_t n, int32_t kind, const Workspace& ws, uint6
 hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_splat* splats, const Workspace& ws,
                              const uint32_t** order_out, hipStream_t s);
 hipError_t launch_pair_offsets(int64_t n, const Workspace& ws, hipStream_t s);
+// Tile ids of the pairs: 16-bit while the image has at most 65536 tiles.
+struct TileKeys {
+    void* p;
+    bool narrow;
+};
+bool tile_keys_narrow(const Cam& cam);
 hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const gs_preprocessed& pre,
-                            const Workspace& ws, uint32_t capacity, uint32_t* keys_out, uint32_t* vals_out,
+                            const Workspace& ws, uint32_t capacity, TileKeys keys_out, uint32_t* vals_out,
                             hipStream_t s);
 int tile_sort_passes(const Cam& cam);
 hipError_t launch_fill_u32(uint32_t* p, int64_t count, uint32_t value, hipStream_t s);
 hipError_t launch_tile_sort(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
-                            uint32_t* tile_ids_out, const uint32_t** sorted_tiles, hipStream_t s);
-hipError_t launch_ranges(const Cam& cam, uint64_t num_pairs, const uint32_t* sorted_tiles,
+                            uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s);
+hipError_t launch_ranges(const Cam& cam, uint64_t num_pairs, TileKeys sorted_tiles,
                          uint32_t* tile_ranges, hipStream_t s);
 hipError_t launch_blend_fwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                             const uint32_t* tile_ranges, float* image, float* final_T, uint32_t* n_contrib,

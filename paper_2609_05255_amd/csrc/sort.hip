@@ -66,8 +66,8 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid)
     return ((uint64_t)hi << 32) | lo;
 }
 
-template <int kBits, int kItems>
-__global__ __launch_bounds__(kBlock) void k_radix_hist(const uint32_t* __restrict__ keys, uint64_t count, int shift,
+template <int kBits, int kItems, typename KeyT>
+__global__ __launch_bounds__(kBlock) void k_radix_hist(const KeyT* __restrict__ keys, uint64_t count, int shift,
                                                        uint32_t* __restrict__ hist, int nblocks)
 {
     constexpr int R = 1 << kBits;
@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const uint32_t* __restric
 #pragma unroll
     for (int r = 0; r < kItems; ++r) {
         const uint64_t idx = base + (uint64_t)r * kBlock + threadIdx.x;
-        k[r] = idx < count ? keys[idx] : 0u;
+        k[r] = idx < count ? (uint32_t)keys[idx] : 0u;
     }
 #pragma unroll
     for (int r = 0; r < kItems; ++r) {
@@ -115,12 +115,12 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(uint32_t* __restrict__ hi
     if (threadIdx.x == 0) digit_tot[blockIdx.x] = total;
 }
 
-template <int kBits, int kItems>
-__global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __restrict__ keys_in,
+template <int kBits, int kItems, typename KeyT, typename KeyOutT>
+__global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict__ keys_in,
                                                           const uint32_t* __restrict__ vals_in, uint64_t count,
                                                           int shift, const uint32_t* __restrict__ hist, int nblocks,
                                                           const uint32_t* __restrict__ digit_tot,
-                                                          uint32_t* __restrict__ keys_out,
+                                                          KeyOutT* __restrict__ keys_out,
                                                           uint32_t* __restrict__ vals_out,
                                                           const gs_splat* __restrict__ rect_src,
                                                           uint2* __restrict__ rect_out)
@@ -131,7 +131,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
     __shared__ uint32_t wcnt[4][R];      // per-wave digit counts, then per-wave exclusive offsets
     __shared__ uint32_t gbase[R];        // global position of this workgroup's first key of each digit
     __shared__ uint32_t lstart[R];       // start of each digit in the workgroup's reordered keys
-    __shared__ uint32_t skey[kTile];
+    __shared__ KeyT skey[kTile];
     __shared__ uint32_t sval[kTile];
     __shared__ uint32_t lds4[4];
     const int t = threadIdx.x, wave = t >> 6, lane = __lane_id();
@@ -150,7 +150,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
     for (int i = 0; i < kItems; ++i) {
         const uint64_t idx = wbase + (uint64_t)i * kWave + lane;
         const bool valid = idx < count;
-        key[i] = valid ? keys_in[idx] : 0u;
+        key[i] = valid ? (uint32_t)keys_in[idx] : 0u;
         val[i] = valid ? (vals_in ? vals_in[idx] : (uint32_t)idx) : 0u;
     }
 #pragma unroll
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
         if (idx < count) {
             const uint32_t d = (key[i] >> shift) & (R - 1);
             const uint32_t lp = lstart[d] + wcnt[wave][d] + rank[i];
-            skey[lp] = key[i];
+            skey[lp] = (KeyT)key[i];
             sval[lp] = val[i];
         }
     }
@@ -196,13 +196,13 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
         const uint32_t d = (k >> shift) & (R - 1);
         const uint32_t pos = gbase[d] + (j - lstart[d]);
         const uint32_t v = sval[j];
-        if (keys_out) keys_out[pos] = k;
+        if (keys_out) keys_out[pos] = (KeyOutT)k;
         vals_out[pos] = v;
         if (rect_out) {
             // tile rectangle of Gaussian v in sorted order; culled Gaussians
             // (key ~0, no splat record) get an empty one
             uint2 r = make_uint2(0u, 0u);
-            if (k != 0xFFFFFFFFu) r = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint32_t*>(rect_src + v) + kSplatRectWord);
+            if (sizeof(KeyT) == 4 && k != 0xFFFFFFFFu) r = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint32_t*>(rect_src + v) + kSplatRectWord);
             rect_out[pos] = r;
         }
     }
@@ -210,31 +210,32 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const uint32_t* __rest
 
 // One stable LSD pass over `bits` bits at `shift`; vals_in == nullptr means
 // value = position, keys_out == nullptr drops the keys.
-template <int kBits, int kItems>
-void radix_pass_t(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t count, int shift, uint32_t* keys_out,
+template <int kBits, int kItems, typename KeyT, typename KeyOutT>
+void radix_pass_t(const KeyT* keys_in, const uint32_t* vals_in, uint64_t count, int shift, KeyOutT* keys_out,
                   uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s,
                   const gs_splat* rect_src = nullptr, uint2* rect_out = nullptr)
 {
     const int nblocks = (int)div_up((int64_t)count, (int64_t)kBlock * kItems);
-    hipLaunchKernelGGL((k_radix_hist<kBits, kItems>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, count, shift, hist,
-                       nblocks);
+    hipLaunchKernelGGL((k_radix_hist<kBits, kItems, KeyT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, count, shift,
+                       hist, nblocks);
     hipLaunchKernelGGL(k_radix_scan, dim3(1 << kBits), dim3(kBlock), 0, s, hist, nblocks, digit_tot);
-    hipLaunchKernelGGL((k_radix_scatter<kBits, kItems>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, vals_in, count, shift,
+    hipLaunchKernelGGL((k_radix_scatter<kBits, kItems, KeyT, KeyOutT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in,
+                       vals_in, count, shift,
                        hist, nblocks, digit_tot, keys_out, vals_out, rect_src, rect_out);
 }
 
-hipError_t radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, uint64_t count, int shift, int bits,
-                      uint32_t* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
+// A tile-sort pass over `bits` (1..8) bits, chosen at run time.
+template <typename KeyT, typename KeyOutT>
+hipError_t radix_pass(const KeyT* keys_in, const uint32_t* vals_in, uint64_t count, int shift, int bits,
+                      KeyOutT* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
 {
     switch (bits) {
-    case 1: radix_pass_t<1, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 2: radix_pass_t<2, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 3: radix_pass_t<3, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 4: radix_pass_t<4, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 5: radix_pass_t<5, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 6: radix_pass_t<6, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 7: radix_pass_t<7, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
-    case 8: radix_pass_t<8, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s); break;
+#define GS_PASS(b)                                                                                                   \
+    case b:                                                                                                          \
+        radix_pass_t<b, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s);      \
+        break;
+        GS_PASS(1) GS_PASS(2) GS_PASS(3) GS_PASS(4) GS_PASS(5) GS_PASS(6) GS_PASS(7) GS_PASS(8)
+#undef GS_PASS
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -311,10 +312,11 @@ __device__ __forceinline__ void wave_lds_fence()
 constexpr int kDupGroups = 8;                   // 64-pair groups per round
 constexpr int kDupWin = kWave * kDupGroups;     // pairs per round
 
+template <typename KeyT>
 __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict__ order,
                                                       const uint2* __restrict__ sorted_rect, int64_t n,
                                                       const uint32_t* __restrict__ part, int tiles_x,
-                                                      uint32_t capacity, uint32_t* __restrict__ keys,
+                                                      uint32_t capacity, KeyT* __restrict__ keys,
                                                       uint32_t* __restrict__ vals)
 {
     __shared__ uint32_t soff[kDupChunk + 1];
@@ -411,7 +413,7 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
             const uint32_t out = gbase + p;
             // only a num_pairs that disagrees with the preprocess gets past the capacity
             if (p < q1 && out < capacity) {
-                keys[out] = ty * (uint32_t)tiles_x + tx;
+                keys[out] = (KeyT)(ty * (uint32_t)tiles_x + tx);
                 vals[out] = gid[k];
             }
         }
@@ -423,24 +425,26 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
     }
 }
 
-__device__ __forceinline__ uint32_t lower_bound_u32(const uint32_t* a, uint32_t count, uint32_t v)
+template <typename KeyT>
+__device__ __forceinline__ uint32_t lower_bound_key(const KeyT* a, uint32_t count, uint32_t v)
 {
     uint32_t lo = 0, hi = count;
     while (lo < hi) {
         const uint32_t mid = lo + ((hi - lo) >> 1);
-        if (a[mid] < v) lo = mid + 1;
+        if ((uint32_t)a[mid] < v) lo = mid + 1;
         else hi = mid;
     }
     return lo;
 }
 
-__global__ __launch_bounds__(kBlock) void k_ranges(const uint32_t* __restrict__ sorted_tiles, uint32_t count,
+template <typename KeyT>
+__global__ __launch_bounds__(kBlock) void k_ranges(const KeyT* __restrict__ sorted_tiles, uint32_t count,
                                                    int n_tiles, uint32_t* __restrict__ ranges)
 {
     const int t = blockIdx.x * kBlock + threadIdx.x;
     if (t >= n_tiles) return;
-    ranges[2 * t] = lower_bound_u32(sorted_tiles, count, (uint32_t)t);
-    ranges[2 * t + 1] = lower_bound_u32(sorted_tiles, count, (uint32_t)t + 1);
+    ranges[2 * t] = lower_bound_key(sorted_tiles, count, (uint32_t)t);
+    ranges[2 * t + 1] = lower_bound_key(sorted_tiles, count, (uint32_t)t + 1);
 }
 
 }  // namespace
@@ -456,7 +460,7 @@ hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_spla
         const bool last = p == 3;
         uint32_t* kout = last ? nullptr : kbuf[p & 1];
         if (last)
-            radix_pass_t<8, kSortItems>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s,
+            radix_pass_t<8, kSortItems>(kin, vin, (uint64_t)n, 8 * p, (uint32_t*)nullptr, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s,
                             splats, ws.sorted_rect);
         else
             radix_pass_t<8, kSortItems>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s);
@@ -478,12 +482,16 @@ hipError_t launch_pair_offsets(int64_t n, const Workspace& ws, hipStream_t s)
 }
 
 hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const gs_preprocessed& pre,
-                            const Workspace& ws, uint32_t capacity, uint32_t* keys_out, uint32_t* vals_out,
+                            const Workspace& ws, uint32_t capacity, TileKeys keys_out, uint32_t* vals_out,
                             hipStream_t s)
 {
     const int nb = (int)div_up(n, kDupChunk);
-    hipLaunchKernelGGL(k_duplicate, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
-                       cam.tiles_x, capacity, keys_out, vals_out);
+    if (keys_out.narrow)
+        hipLaunchKernelGGL(k_duplicate<uint16_t>, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
+                           cam.tiles_x, capacity, static_cast<uint16_t*>(keys_out.p), vals_out);
+    else
+        hipLaunchKernelGGL(k_duplicate<uint32_t>, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
+                           cam.tiles_x, capacity, static_cast<uint32_t*>(keys_out.p), vals_out);
     return hipGetLastError();
 }
 
@@ -498,34 +506,56 @@ static int tile_bits(const Cam& cam)
 
 int tile_sort_passes(const Cam& cam) { return (tile_bits(cam) + 7) / 8; }
 
-hipError_t launch_tile_sort(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
-                            uint32_t* tile_ids_out, const uint32_t** sorted_tiles, hipStream_t s)
+bool tile_keys_narrow(const Cam& cam) { return (int64_t)cam.tiles_x * cam.tiles_y <= 65536; }
+
+template <typename KeyT>
+static hipError_t tile_sort_t(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
+                              uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s)
 {
     const int bits = tile_bits(cam);
     const int passes = (bits + 7) / 8;
-    uint32_t* kbuf[2] = {ws.pair_keys_a, ws.pair_keys_b};
+    KeyT* kbuf[2] = {reinterpret_cast<KeyT*>(ws.pair_keys_a), reinterpret_cast<KeyT*>(ws.pair_keys_b)};
     uint32_t* vbuf[2] = {ws.pair_vals_a, ws.pair_vals_b};
     int src = 0, shift = 0;
     for (int p = 0; p < passes; ++p) {
         const bool last = p == passes - 1;
         const int pb = (bits - shift + (passes - p) - 1) / (passes - p);   // remaining bits spread evenly
-        uint32_t* kout = last ? (tile_ids_out ? tile_ids_out : kbuf[src ^ 1]) : kbuf[src ^ 1];
         uint32_t* vout = last ? values : vbuf[src ^ 1];
-        hipError_t e = radix_pass(kbuf[src], vbuf[src], num_pairs, shift, pb, kout, vout, ws.hist, ws.digit_tot, s);
+        hipError_t e;
+        if (last && tile_ids_out) {
+            // the caller's 32-bit tile ids double as the sorted keys for the ranges
+            e = radix_pass(kbuf[src], vbuf[src], num_pairs, shift, pb, tile_ids_out, vout, ws.hist, ws.digit_tot, s);
+            *sorted_tiles = TileKeys{tile_ids_out, false};
+        }
+        else {
+            e = radix_pass(kbuf[src], vbuf[src], num_pairs, shift, pb, kbuf[src ^ 1], vout, ws.hist, ws.digit_tot, s);
+            if (last) *sorted_tiles = TileKeys{kbuf[src ^ 1], sizeof(KeyT) == 2};
+        }
         if (e != hipSuccess) return e;
-        if (last) *sorted_tiles = kout;
         shift += pb;
         src ^= 1;
     }
     return hipSuccess;
 }
 
-hipError_t launch_ranges(const Cam& cam, uint64_t num_pairs, const uint32_t* sorted_tiles, uint32_t* tile_ranges,
+hipError_t launch_tile_sort(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
+                            uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s)
+{
+    return tile_keys_narrow(cam) ? tile_sort_t<uint16_t>(cam, num_pairs, ws, values, tile_ids_out, sorted_tiles, s)
+                                 : tile_sort_t<uint32_t>(cam, num_pairs, ws, values, tile_ids_out, sorted_tiles, s);
+}
+
+hipError_t launch_ranges(const Cam& cam, uint64_t num_pairs, TileKeys sorted_tiles, uint32_t* tile_ranges,
                          hipStream_t s)
 {
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    hipLaunchKernelGGL(k_ranges, dim3((unsigned)div_up(n_tiles, kBlock)), dim3(kBlock), 0, s, sorted_tiles,
-                       (uint32_t)num_pairs, n_tiles, tile_ranges);
+    const dim3 grid((unsigned)div_up(n_tiles, kBlock));
+    if (sorted_tiles.narrow)
+        hipLaunchKernelGGL(k_ranges<uint16_t>, grid, dim3(kBlock), 0, s, static_cast<const uint16_t*>(sorted_tiles.p),
+                           (uint32_t)num_pairs, n_tiles, tile_ranges);
+    else
+        hipLaunchKernelGGL(k_ranges<uint32_t>, grid, dim3(kBlock), 0, s, static_cast<const uint32_t*>(sorted_tiles.p),
+                           (uint32_t)num_pairs, n_tiles, tile_ranges);
     return hipGetLastError();
 }
 

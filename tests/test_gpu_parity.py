@@ -78,6 +78,13 @@ def test_tile_grid_edge_cases(size):
     check_all(sc, tiny_camera(*size), label="grid%dx%d" % size)
 
 
+def test_more_than_65536_tiles():
+    # 4097 x 16 tiles: the tile ids no longer fit 16 bits, so the pair emission
+    # and the tile sort carry 32-bit keys (below that they carry 16-bit ones)
+    sc = inputs.make_scene("tiny").subset(np.arange(300))
+    check_all(sc, tiny_camera(16 * 4097, 256), label="wide", grads=False)
+
+
 def test_capacity_retry():
     sc = inputs.make_scene("tiny")
     check_all(sc, inputs.make_cameras("tiny")[0], capacity=100, label="capacity")

@@ -214,6 +214,36 @@ def main():
             hbm_all[k] = {"algorithmic_MB": round(b / 1e6, 1), "ms": round(stage_ms[k], 4),
                           "GB_s": round(ach, 1), "frac": round(ach / HBM_PEAK_GBS, 4)}
 
+    # training step: the same K steps followed each by the fused Adam update of
+    # every parameter tensor (the paper's optimisation comparison); value
+    # above stays the forward+backward metric
+    from paper_2609_05255_amd.optim import FusedAdam
+    opt = FusedAdam(st, fr, kid)
+    for i in range(args.warmup):
+        step(i)
+        opt.step(stream)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+        opt.step(stream)
+    torch.cuda.synchronize()
+    t_train = (time.perf_counter() - t_start) / args.steps
+    gs.timing_enable(True)
+    gs.timing_reset()
+    for i in range(args.steps):
+        opt.step(stream)
+    torch.cuda.synchronize()
+    adam_ms, adam_n = gs.timing_read()["adam"]
+    gs.timing_enable(False)
+    adam_ms /= max(adam_n, 1)
+    adam_bytes = opt.bytes_per_step()
+    adam_gbs = adam_bytes / (adam_ms * 1e-3) / 1e9
+    hbm_all["adam"] = {"algorithmic_MB": round(adam_bytes / 1e6, 1), "ms": round(adam_ms, 4),
+                       "GB_s": round(adam_gbs, 1), "frac": round(adam_gbs / HBM_PEAK_GBS, 4)}
+    train = {"it_s": round(1.0 / t_train, 3), "ms_per_step": round(1e3 * t_train, 4), "adam_ms": round(adam_ms, 4),
+             "optimizer": "fused Adam over every parameter tensor, one launch per step"}
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(scene, cams, kind, args.cpu_tiles)
@@ -243,6 +273,7 @@ def main():
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "hbm_stages": hbm_all,
         "roofline": roofline,
+        "train_step": train,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

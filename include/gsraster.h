@@ -210,6 +210,45 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
  */
 gs_status gs_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* mlp_w, float* colors, void* stream);
 
+/*
+ * gs_adam_step -- one Adam step (Kingma and Ba, Algorithm 1, with bias
+ * correction) over several parameter tensors in a single launch: the fused
+ * optimiser update of the paper's training pipeline (supplementary
+ * implementation details: one learning rate per parameter channel; the decoder
+ * weights kept and updated in fp32 with a half-precision copy made for the
+ * passes; beta2 = 0.99 for the decoder weights; the update touches every
+ * Gaussian, visible in the iteration or not -- the per-parameter traffic the
+ * paper holds responsible for SH3's slower optimisation, Sec. 5).
+ * Tensor k is planar [rows][n] fp32: param, exp_avg (m) and exp_avg_sq (v) are
+ * updated in place, grad is read. Per element, with t = step and lr that of
+ * the element's row:
+ *   m = b1 m + (1 - b1) g,   v = b2 v + (1 - b2) g^2,
+ *   param -= (lr / (1 - b1^t)) * m / (sqrt(v) / sqrt(1 - b2^t) + eps)
+ * (Algorithm 1's update with the bias corrections moved onto the step size and
+ * the denominator). param_half, when not NULL, receives the updated values
+ * rounded to binary16 (to nearest even) -- the half copy the passes read.
+ * lr is a HOST array of `rows` learning rates (the row index is the paper's
+ * column index of its [n][channels] layout). beta2 is per tensor.
+ * Limits: 1 <= count <= GS_ADAM_MAX_TENSORS, rows >= 1, sum of rows <=
+ * GS_ADAM_MAX_ROWS, 0 <= n < 2^31 per tensor, step >= 1, 0 <= b1, b2 < 1,
+ * eps > 0. Tensors must not overlap one another.
+ */
+#define GS_ADAM_MAX_TENSORS 8
+#define GS_ADAM_MAX_ROWS 128
+typedef struct gs_adam_tensor {
+    float* param;             /* [rows][n] fp32, updated in place */
+    const float* grad;        /* [rows][n] fp32 */
+    float* exp_avg;           /* [rows][n] fp32 first moment, updated in place */
+    float* exp_avg_sq;        /* [rows][n] fp32 second moment, updated in place */
+    uint16_t* param_half;     /* [rows][n] binary16 copy of the result, or NULL */
+    int64_t n;
+    int32_t rows;
+    float beta2;
+    const float* lr;          /* HOST [rows] learning rates */
+} gs_adam_tensor;
+gs_status gs_adam_step(const gs_adam_tensor* tensors, int32_t count, float beta1, float eps, int64_t step,
+                       void* stream);
+
 /* Workspace bytes needed by any call for these sizes (host only). */
 gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t capacity, int32_t kind,
                             size_t* bytes);
@@ -223,7 +262,7 @@ enum {
     GS_KERNEL_PREPROCESS = 0, GS_KERNEL_PAIR_COUNT, GS_KERNEL_DEPTH_SORT, GS_KERNEL_PAIR_OFFSETS,
     GS_KERNEL_DUPLICATE, GS_KERNEL_TILE_SORT, GS_KERNEL_RANGES, GS_KERNEL_BLEND_FWD,
     GS_KERNEL_CLEAR, GS_KERNEL_BLEND_BWD, GS_KERNEL_PREPROCESS_BWD, GS_KERNEL_MLP_REDUCE,
-    GS_KERNEL_COUNT
+    GS_KERNEL_ADAM, GS_KERNEL_COUNT
 };
 gs_status gs_timing_enable(int32_t enable);
 gs_status gs_timing_reset(void);

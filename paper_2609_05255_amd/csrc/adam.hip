@@ -1,0 +1,124 @@
+// Fused Adam step over several planar [rows][n] fp32 parameter tensors in one
+// launch (Kingma and Ba, Algorithm 1, with the bias corrections folded into
+// the step size and the denominator; one learning rate per row). A pure
+// streaming kernel: per element it reads param, grad, m, v and writes param,
+// m, v (and optionally the binary16 copy), so it is bound by HBM bandwidth.
+//
+// Workgroups are dealt to (tensor, row, chunk of kChunk elements): the tensor
+// and row are uniform per workgroup, so the row's step size is a kernel
+// argument read through the scalar unit, and consecutive lanes touch
+// consecutive elements.
+#include <cmath>
+#include <cstring>
+
+#include "gs_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace gsr {
+
+namespace {
+
+constexpr int kItems = 4;
+constexpr int kChunk = kBlock * kItems;
+
+struct AdamTensorArgs {
+    float* p;
+    const float* g;
+    float* m;
+    float* v;
+    uint16_t* h;
+    int64_t n;
+    int64_t chunk0;        // first workgroup of this tensor
+    int32_t chunks_per_row;
+    int32_t row0;          // index of this tensor's first row in step_size
+    float b2, omb2, inv_sqrt_bc2;
+};
+
+struct AdamArgs {
+    int32_t count;
+    float b1, omb1, eps;
+    AdamTensorArgs t[GS_ADAM_MAX_TENSORS];
+    float step_size[GS_ADAM_MAX_ROWS];   // lr / (1 - b1^t) per row
+};
+
+__global__ __launch_bounds__(kBlock) void k_adam(AdamArgs a)
+{
+    const int64_t b = blockIdx.x;
+    int k = 0;
+    while (k + 1 < a.count && b >= a.t[k + 1].chunk0) ++k;
+    const AdamTensorArgs& T = a.t[k];
+    const int64_t local = b - T.chunk0;
+    const int row = (int)(local / T.chunks_per_row);
+    const int64_t c = local - (int64_t)row * T.chunks_per_row;
+    const float step = a.step_size[T.row0 + row];
+    const int64_t e0 = c * kChunk + threadIdx.x;
+    const int64_t rbase = (int64_t)row * T.n;
+    float g[kItems], m[kItems], v[kItems], p[kItems];
+    // all loads first
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int64_t e = e0 + (int64_t)j * kBlock;
+        if (e < T.n) {
+            const int64_t i = rbase + e;
+            g[j] = T.g[i];
+            m[j] = T.m[i];
+            v[j] = T.v[i];
+            p[j] = T.p[i];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int64_t e = e0 + (int64_t)j * kBlock;
+        if (e >= T.n) continue;
+        const int64_t i = rbase + e;
+        const float mj = a.b1 * m[j] + a.omb1 * g[j];
+        const float vj = T.b2 * v[j] + T.omb2 * (g[j] * g[j]);
+        const float denom = sqrtf(vj) * T.inv_sqrt_bc2 + a.eps;
+        const float pj = p[j] - step * (mj / denom);
+        T.m[i] = mj;
+        T.v[i] = vj;
+        T.p[i] = pj;
+        if (T.h) T.h[i] = __builtin_bit_cast(uint16_t, (_Float16)pj);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_adam(const gs_adam_tensor* ts, int count, float beta1, float eps, int64_t step, hipStream_t s)
+{
+    AdamArgs a;
+    memset(&a, 0, sizeof(a));
+    a.count = count;
+    a.b1 = beta1;
+    a.omb1 = 1.f - beta1;
+    a.eps = eps;
+    const double bc1 = 1.0 - std::pow((double)beta1, (double)step);
+    int64_t chunks = 0;
+    int rows = 0;
+    for (int k = 0; k < count; ++k) {
+        const gs_adam_tensor& t = ts[k];
+        AdamTensorArgs& T = a.t[k];
+        T.p = t.param;
+        T.g = t.grad;
+        T.m = t.exp_avg;
+        T.v = t.exp_avg_sq;
+        T.h = t.param_half;
+        T.n = t.n;
+        T.chunk0 = chunks;
+        T.chunks_per_row = (int32_t)div_up(t.n, kChunk);
+        T.row0 = rows;
+        T.b2 = t.beta2;
+        T.omb2 = 1.f - t.beta2;
+        const double bc2 = 1.0 - std::pow((double)t.beta2, (double)step);
+        T.inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+        for (int r = 0; r < t.rows; ++r) a.step_size[rows + r] = (float)((double)t.lr[r] / bc1);
+        chunks += (int64_t)t.rows * T.chunks_per_row;
+        rows += t.rows;
+    }
+    if (chunks == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_adam, dim3((unsigned)chunks), dim3(kBlock), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace gsr

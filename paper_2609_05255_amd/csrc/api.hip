@@ -132,7 +132,7 @@ void resolve_pending_locked()
 
 const char* const kKernelNames[GS_KERNEL_COUNT] = {
     "preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
-    "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce"};
+    "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam"};
 
 }  // namespace
 
@@ -207,6 +207,32 @@ extern "C" {
 const char* gs_last_error(void) { return g_error.c_str(); }
 
 const char* gs_version(void) { return "gsraster 0.1.0 (gfx950)"; }
+
+gs_status gs_adam_step(const gs_adam_tensor* tensors, int32_t count, float beta1, float eps, int64_t step,
+                       void* stream)
+{
+    GS_CHECK(tensors != nullptr, "tensors is NULL");
+    GS_CHECK(count >= 1 && count <= GS_ADAM_MAX_TENSORS, "count %d outside [1, %d]", count, GS_ADAM_MAX_TENSORS);
+    GS_CHECK(step >= 1, "step %lld must be at least 1", (long long)step);
+    GS_CHECK(beta1 >= 0.f && beta1 < 1.f, "beta1 must lie in [0, 1)");
+    GS_CHECK(eps > 0.f, "eps must be positive");
+    int64_t rows = 0;
+    for (int k = 0; k < count; ++k) {
+        const gs_adam_tensor& t = tensors[k];
+        GS_CHECK(t.rows >= 1, "tensor %d: rows must be positive", k);
+        GS_CHECK(t.n >= 0 && t.n < ((int64_t)1 << 31), "tensor %d: n out of range", k);
+        GS_CHECK(t.beta2 >= 0.f && t.beta2 < 1.f, "tensor %d: beta2 must lie in [0, 1)", k);
+        GS_CHECK(t.lr != nullptr, "tensor %d: lr is NULL", k);
+        GS_CHECK(t.n == 0 || (t.param && t.grad && t.exp_avg && t.exp_avg_sq), "tensor %d: a buffer is NULL", k);
+        rows += t.rows;
+    }
+    GS_CHECK(rows <= GS_ADAM_MAX_ROWS, "%lld rows in total exceed %d", (long long)rows, GS_ADAM_MAX_ROWS);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    timing_begin(GS_KERNEL_ADAM, s);
+    GS_HIP(launch_adam(tensors, count, beta1, eps, step, s));
+    timing_end(GS_KERNEL_ADAM, s);
+    return ok();
+}
 
 const char* gs_kernel_name(int32_t id) { return (id >= 0 && id < GS_KERNEL_COUNT) ? kKernelNames[id] : "unknown"; }
 

@@ -22,7 +22,9 @@ LIB_PATH = os.path.join(HERE, "libgsraster.so")
 GS_OK, GS_ERR_INVALID_ARG, GS_ERR_CAPACITY, GS_ERR_DEVICE, GS_ERR_UNSUPPORTED = range(5)
 GS_APP_SH3, GS_APP_LATENT_MLP = 0, 1
 KERNEL_NAMES = ["preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
-                "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce"]
+                "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam"]
+ADAM_MAX_TENSORS = 8
+ADAM_MAX_ROWS = 128
 SPLAT_BYTES = 64
 MLP_WEIGHTS = 1664
 
@@ -60,6 +62,12 @@ class Grads(C.Structure):
                 ("dmlp_w", C.c_void_p), ("dmean2d", C.c_void_p)]
 
 
+class AdamTensor(C.Structure):
+    _fields_ = [("param", C.c_void_p), ("grad", C.c_void_p), ("exp_avg", C.c_void_p), ("exp_avg_sq", C.c_void_p),
+                ("param_half", C.c_void_p), ("n", C.c_int64), ("rows", C.c_int32), ("beta2", C.c_float),
+                ("lr", C.POINTER(C.c_float))]
+
+
 _lib = None
 
 
@@ -78,11 +86,12 @@ def lib() -> C.CDLL:
                                     P(Grads), vp, sz, vp]
         L.gs_workspace_size.argtypes = [i64, i32, i32, u64, i32, P(sz)]
         L.gs_mlp_eval.argtypes = [vp, i64, vp, vp, vp]
+        L.gs_adam_step.argtypes = [P(AdamTensor), i32, C.c_float, C.c_float, i64, vp]
         L.gs_timing_enable.argtypes = [i32]
         L.gs_timing_reset.argtypes = []
         L.gs_timing_read.argtypes = [P(C.c_double), P(i64), i32]
         for f in ("gs_preprocess", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd", "gs_workspace_size", "gs_mlp_eval",
-                  "gs_timing_enable", "gs_timing_reset", "gs_timing_read"):
+                  "gs_adam_step", "gs_timing_enable", "gs_timing_reset", "gs_timing_read"):
             getattr(L, f).restype = C.c_int
         L.gs_last_error.restype = C.c_char_p
         L.gs_version.restype = C.c_char_p
@@ -185,6 +194,24 @@ def gs_render_bwd(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed,
 
 def gs_mlp_eval(x, rows: int, mlp_w, colors, stream=None):
     _check(lib().gs_mlp_eval(_ptr(x), rows, _ptr(mlp_w), _ptr(colors), _stream(stream)))
+
+
+def gs_adam_step(tensors, beta1: float, eps: float, step: int, stream=None):
+    """tensors: list of dicts with param, grad, exp_avg, exp_avg_sq (device fp32 [rows][n]), optional
+    param_half (device int16/uint16 [rows][n]), rows, n, beta2 and lr (a sequence of `rows` floats)."""
+    arr = (AdamTensor * max(1, len(tensors)))()
+    keep = []
+    for k, t in enumerate(tensors):
+        lr = None
+        if t["lr"] is not None:
+            if len(t["lr"]) < int(t["rows"]):
+                raise ValueError("lr needs one entry per row")
+            lr = (C.c_float * len(t["lr"]))(*[float(x) for x in t["lr"]])
+            keep.append(lr)
+        arr[k] = AdamTensor(_ptr(t["param"]), _ptr(t["grad"]), _ptr(t["exp_avg"]), _ptr(t["exp_avg_sq"]),
+                            _ptr(t.get("param_half")), int(t["n"]), int(t["rows"]), float(t["beta2"]),
+                            C.cast(lr, C.POINTER(C.c_float)) if lr is not None else None)
+    _check(lib().gs_adam_step(arr, len(tensors), float(beta1), float(eps), int(step), _stream(stream)))
 
 
 def timing_enable(on: bool = True):

@@ -1,0 +1,68 @@
+"""Fused Adam over a scene's parameters: the optimiser step of the paper's
+training pipeline (supplementary implementation details), one gs_adam_step
+launch per iteration for every parameter tensor.
+
+Learning rates per parameter channel (the row of the planar layout):
+  * geometry as in 3D Gaussian Splatting: means 1.6e-4, log-scales 5e-3,
+    rotations 1e-3, opacity logits 0.05;
+  * SH3 (the paper's table of appearance learning rates): the degree-0 rows
+    0.0025 -- the paper folds Y0 into the base colour and scales its rate by
+    Y0 instead, the same step in colour space -- and every other coefficient
+    0.000125;
+  * latent + MLP: latents 0.008 (the paper's rate for the neural features) and
+    decoder weights 0.003 with a second-moment decay of 0.99 (they receive a
+    gradient from every visible Gaussian in every iteration).
+The latents and the decoder weights have fp32 master copies here; each step
+writes their binary16 copies into the scene buffers the passes read, as the
+paper does for its decoder weights.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import gsraster as gs
+
+LR_MEANS, LR_SCALES, LR_QUATS, LR_OPACITY = 1.6e-4, 5e-3, 1e-3, 0.05
+LR_SH_DC, LR_SH_REST = 0.0025, 0.000125
+LR_LATENT, LR_MLP, BETA2_MLP = 0.008, 0.003, 0.99
+LATENT_DIM = 14
+
+
+class FusedAdam:
+    def __init__(self, scene: gs.SceneTensors, frame: gs.Frame, kind: int, betas=(0.9, 0.999), eps: float = 1e-15):
+        self.beta1, self.beta2, self.eps, self.t = betas[0], betas[1], eps, 0
+        self.groups = []
+
+        def add(param, grad, lr_rows, beta2=None, half=None):
+            rows = len(lr_rows)
+            param = param.view(rows, -1)
+            assert param.is_contiguous() and grad.numel() == param.numel()
+            self.groups.append(dict(param=param, grad=grad, exp_avg=torch.zeros_like(param),
+                                    exp_avg_sq=torch.zeros_like(param), param_half=half, rows=rows,
+                                    n=param.shape[1], beta2=self.beta2 if beta2 is None else beta2,
+                                    lr=list(lr_rows)))
+
+        add(scene.means, frame.dmeans, [LR_MEANS] * 3)
+        add(scene.log_scales, frame.dlog_scales, [LR_SCALES] * 3)
+        add(scene.quats, frame.dquats, [LR_QUATS] * 4)
+        add(scene.opacity_logits, frame.dopacity_logits, [LR_OPACITY])
+        if kind == gs.GS_APP_SH3:
+            add(scene.sh, frame.dsh, [LR_SH_DC] * 3 + [LR_SH_REST] * 45)
+        else:
+            self.latent32 = scene.latent.view(torch.float16).float().contiguous()
+            self.mlp32 = scene.mlp_w.view(torch.float16).float().contiguous()
+            add(self.latent32, frame.dlatent, [LR_LATENT] * LATENT_DIM, half=scene.latent)
+            add(self.mlp32, frame.dmlp_w, [LR_MLP], beta2=BETA2_MLP, half=scene.mlp_w)
+
+    def step(self, stream=None):
+        self.t += 1
+        gs.gs_adam_step(self.groups, self.beta1, self.eps, self.t, stream)
+
+    def bytes_per_step(self) -> int:
+        """HBM bytes one step must move: per element param, grad, m and v read, param, m and v
+        written (fp32), plus the binary16 copy where there is one."""
+        total = 0
+        for g in self.groups:
+            e = g["rows"] * g["n"]
+            total += e * (7 * 4 + (2 if g["param_half"] is not None else 0))
+        return total

@@ -131,3 +131,23 @@ def test_render_calls_reject_bad_arguments(gs):
                            C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE), C.byref(grads),
                            C.c_void_p(FAKE * 256), 1 << 40, None)
     assert st == gs.GS_ERR_INVALID_ARG and b"dsh" in lib.gs_last_error()
+
+
+def test_adam_rejects_bad_arguments(gs):
+    # every case fails a host check, so the fake pointers are never used
+    t = dict(param=FAKE, grad=FAKE, exp_avg=FAKE, exp_avg_sq=FAKE, rows=2, n=10, beta2=0.999, lr=[1e-3, 1e-3])
+    cases = [(dict(rows=0, lr=[]), {}), (dict(beta2=1.0), {}), (dict(lr=None), {}), (dict(n=-1), {}),
+             (dict(grad=None), {}), ({}, dict(step=0)), ({}, dict(beta1=1.0)), ({}, dict(eps=0.0))]
+    for bad, kw in cases:
+        args = dict(beta1=0.9, eps=1e-8, step=1, stream=0)
+        args.update(kw)
+        with pytest.raises(gs.GsError) as e:
+            gs.gs_adam_step([dict(t, **bad)], **args)
+        assert e.value.status == gs.GS_ERR_INVALID_ARG, (bad, kw)
+    with pytest.raises(gs.GsError):
+        gs.gs_adam_step([], 0.9, 1e-8, 1, stream=0)
+    with pytest.raises(gs.GsError):     # 129 rows in total
+        gs.gs_adam_step([dict(t, rows=65, lr=[1e-3] * 65), dict(t, rows=64, lr=[1e-3] * 64)], 0.9, 1e-8, 1,
+                        stream=0)
+    with pytest.raises(gs.GsError):     # nine tensors
+        gs.gs_adam_step([t] * 9, 0.9, 1e-8, 1, stream=0)

@@ -1,0 +1,112 @@
+"""GPU parity of the fused Adam step (gs_adam_step through the C ABI) with the
+float64 oracle of Algorithm 1 (oracle/adam.py). Each step is checked from the
+GPU's own fp32 state of the previous step, so the bound is one step's fp32
+rounding: moments within 4 ulp of their terms, parameters within 2 ulp plus
+2e-6 of the update; the binary16 copy is bit-exact against the fp32 result
+rounded to nearest even."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import adam
+from paper_2609_05255_amd import gsraster as gs
+from parity import say
+
+pytestmark = pytest.mark.gpu
+
+B1, EPS = 0.9, 1e-8
+U = 2.0 ** -23
+
+
+def make_tensor(rng, rows, n, beta2, half, lr_scale):
+    p = rng.normal(size=(rows, n)).astype(np.float32)
+    t = dict(rows=rows, n=n, beta2=beta2, lr=list(lr_scale * rng.random(rows) + 1e-4),
+             host_p=p, param=torch.from_numpy(p).cuda(),
+             exp_avg=torch.zeros(rows, n, device="cuda"), exp_avg_sq=torch.zeros(rows, n, device="cuda"),
+             grad=torch.zeros(rows, n, device="cuda"))
+    if half:
+        t["param_half"] = torch.zeros(rows, n, dtype=torch.int16, device="cuda")
+    return t
+
+
+def run_and_check(tensors, steps, rng, label):
+    say("case adam %s: %s" % (label, ", ".join("%dx%d" % (t["rows"], t["n"]) for t in tensors)))
+    for step in range(1, steps + 1):
+        before = []
+        for t in tensors:
+            g = (rng.normal(size=(t["rows"], t["n"])) * np.exp(rng.normal(size=(t["rows"], 1)) * 3)).astype(np.float32)
+            if t["n"] > 2:
+                g[:, 1] = 0.0       # untouched element: the moments still decay
+            t["grad"].copy_(torch.from_numpy(g))
+            before.append((t["param"].cpu().numpy().astype(np.float64), g.astype(np.float64),
+                           t["exp_avg"].cpu().numpy().astype(np.float64),
+                           t["exp_avg_sq"].cpu().numpy().astype(np.float64)))
+        gs.gs_adam_step(tensors, B1, EPS, step)
+        torch.cuda.synchronize()
+        for t, (p0, g, m0, v0) in zip(tensors, before):
+            if t["n"] == 0:
+                continue
+            # the library receives its rates and decays as fp32 values: the oracle takes the same values
+            f32 = lambda x: np.float64(np.float32(x))
+            lr32 = np.asarray(t["lr"], np.float32).astype(np.float64)
+            p_ref, m_ref, v_ref = adam.adam_step(p0, g, m0, v0, lr32, f32(B1), f32(t["beta2"]), f32(EPS), step)
+            p = t["param"].cpu().numpy().astype(np.float64)
+            m = t["exp_avg"].cpu().numpy().astype(np.float64)
+            v = t["exp_avg_sq"].cpu().numpy().astype(np.float64)
+            tol_m = 4 * U * (B1 * np.abs(m0) + (1 - B1) * np.abs(g)) + 1e-38
+            tol_v = 4 * U * (t["beta2"] * v0 + (1 - t["beta2"]) * g * g) + 1e-38
+            tol_p = 2 * U * np.abs(p_ref) + 2e-6 * np.abs(p_ref - p0) + 1e-38
+            assert np.all(np.abs(m - m_ref) <= tol_m), (label, step, "m", float(np.max(np.abs(m - m_ref) / tol_m)))
+            assert np.all(np.abs(v - v_ref) <= tol_v), (label, step, "v", float(np.max(np.abs(v - v_ref) / tol_v)))
+            assert np.all(np.abs(p - p_ref) <= tol_p), (label, step, "p", float(np.max(np.abs(p - p_ref) / tol_p)))
+            if "param_half" in t:
+                h = t["param_half"].cpu().numpy().view(np.uint16)
+                assert np.array_equal(h, adam.half_copy(p.astype(np.float32))), (label, step)
+    say("  %d steps OK" % steps)
+
+
+def test_adam_several_tensors_and_steps():
+    rng = np.random.default_rng(10)
+    ts = [make_tensor(rng, 3, 100_003, 0.999, False, 1e-3),     # means-like, ragged length
+          make_tensor(rng, 48, 2_049, 0.999, False, 1e-4),      # SH-like, 48 rows
+          make_tensor(rng, 14, 1_025, 0.999, True, 8e-3),       # latent master + half copy
+          make_tensor(rng, 1, 1_664, 0.99, True, 3e-3)]         # decoder weights, beta2 0.99
+    run_and_check(ts, 3, rng, "four tensors")
+
+
+def test_adam_edge_sizes():
+    rng = np.random.default_rng(11)
+    ts = [make_tensor(rng, 2, 0, 0.999, False, 1e-3),
+          make_tensor(rng, 1, 1, 0.999, True, 1e-2),
+          make_tensor(rng, 5, 1_023, 0.9, False, 1e-3),
+          make_tensor(rng, 5, 1_024, 0.999, True, 1e-3),
+          make_tensor(rng, 60, 7, 0.999, False, 1e-3)]
+    run_and_check(ts, 2, rng, "edge sizes")
+
+
+def test_fused_adam_on_a_latent_scene():
+    # one training iteration on a tiny latent scene: the half-precision buffers the
+    # passes read are the rounded fp32 masters, and every parameter moved by at
+    # most its learning rate (|m_hat| / sqrt(v_hat) = 1 in a first step)
+    from paper_2609_05255_amd import inputs
+    from paper_2609_05255_amd.optim import FusedAdam
+    from parity import tiny_camera
+    sc = inputs.make_scene("tiny", appearance=("latent",))
+    cam = tiny_camera()
+    st = gs.SceneTensors(sc)
+    fr = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_LATENT_MLP, 1 << 16)
+    cs = gs.camera_struct(cam)
+    fr.forward(cs, st)
+    fr.backward(cs, st, torch.from_numpy(inputs.make_upstream_grad(cam.width, cam.height, 0)).cuda())
+    opt = FusedAdam(st, fr, gs.GS_APP_LATENT_MLP)
+    before = [g["param"].clone() for g in opt.groups]
+    opt.step()
+    torch.cuda.synchronize()
+    for g, b in zip(opt.groups, before):
+        lr = torch.tensor(g["lr"], device="cuda").view(-1, 1)
+        # (plus the fp32 rounding of the updated value)
+        assert torch.all((g["param"] - b).abs() <= lr * (1 + 1e-5) + 2 * U * b.abs()), g["rows"]
+        if g["param_half"] is not None:
+            h = g["param_half"].view(g["rows"], -1).cpu().numpy().view(np.uint16)
+            assert np.array_equal(h, adam.half_copy(g["param"].cpu().numpy()))
+    say("  fused Adam on the latent scene: %d tensors, %d bytes per step" % (len(opt.groups), opt.bytes_per_step()))

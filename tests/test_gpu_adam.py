@@ -70,8 +70,9 @@ def test_adam_several_tensors_and_steps():
     ts = [make_tensor(rng, 3, 100_003, 0.999, False, 1e-3),     # means-like, ragged length
           make_tensor(rng, 48, 2_049, 0.999, False, 1e-4),      # SH-like, 48 rows
           make_tensor(rng, 14, 1_025, 0.999, True, 8e-3),       # latent master + half copy
-          make_tensor(rng, 1, 1_664, 0.99, True, 3e-3)]         # decoder weights, beta2 0.99
-    run_and_check(ts, 3, rng, "four tensors")
+          make_tensor(rng, 1, 1_664, 0.99, True, 3e-3),         # decoder weights, beta2 0.99
+          make_tensor(rng, 4, 100_000, 0.999, True, 1e-3)]      # rows 16-byte aligned: vector accesses
+    run_and_check(ts, 3, rng, "five tensors")
 
 
 def test_adam_edge_sizes():

@@ -1,6 +1,6 @@
 /*
  * CPU oracle for the tile-based differentiable Gaussian rasterizer with fused
- * SH3 or latent+MLP appearance.
+ * SH3, latent+MLP or the paper's neural (base colour + feature) appearance.
  *
  * TEST INFRASTRUCTURE ONLY. This library defines what the GPU path must
  * compute; it is called by the test-suite, by the package's smoke check and by
@@ -47,7 +47,7 @@ typedef struct orc_camera {
     double bg[3];
 } orc_camera;
 
-enum { ORC_APP_SH3 = 0, ORC_APP_LATENT_MLP = 1 };
+enum { ORC_APP_SH3 = 0, ORC_APP_LATENT_MLP = 1, ORC_APP_NEURAL = 2 };
 
 /* flags written per Gaussian by the preprocess */
 enum {
@@ -61,15 +61,19 @@ enum {
 
 typedef struct orc_appearance {
     int32_t kind;           /* ORC_APP_* */
-    int32_t sh_degree;      /* 0..3 */
+    int32_t sh_degree;      /* 0..3; for NEURAL the active degree of the direction encoding */
     const double* sh;       /* [48][n] */
     const double* latent;   /* [14][n] values of binary16 numbers */
-    const double* mlp_w;    /* 1664 values of binary16 numbers: W1[32][17], W2[32][32], W3[3][32] */
-    int32_t dir_exact;      /* 0: the decoder sees the view direction rounded to binary16 (as the
-                               half-precision decoder does); 1: unrounded, for finite differences */
+    const double* mlp_w;    /* values of binary16 numbers. LATENT_MLP: 1664, W1[32][17], W2[32][32],
+                               W3[3][32]. NEURAL: 816, W1[16][32], W2[16][16], W3[3][16] */
+    int32_t dir_exact;      /* 0: the decoder inputs derived from the view direction (and, for
+                               NEURAL, the feature encodings) are rounded to binary16, as the
+                               half-precision decoder sees them; 1: unrounded, for finite differences */
     int32_t half_act;       /* 1: the hidden activations are rounded to binary16 before they enter
                                the next layer (half-precision operands, Sec. 4 / fused appendix);
                                0: exact fp64 activations */
+    const double* base_color; /* NEURAL: [3][n] base colour c0 */
+    const double* features;   /* NEURAL: [8][n] values of binary16 numbers */
 } orc_appearance;
 
 /* Outputs of the preprocess. Entries of culled Gaussians are zero. */
@@ -92,11 +96,13 @@ typedef struct orc_grads {
     double* dopacity_logits;/* [n] */
     double* dsh;            /* [48][n] (SH3) or NULL */
     double* dlatent;        /* [14][n] (latent) or NULL */
-    double* dmlp_w;         /* [1664] (latent) or NULL */
+    double* dmlp_w;         /* [1664] (latent), [816] (neural) or NULL */
     double* dmean2d;        /* [2][n] screen-space mean gradient, or NULL */
     double* dconic;         /* [3][n] or NULL */
     double* dopacity;       /* [n] or NULL (w.r.t. the activated opacity) */
     double* dcolor;         /* [3][n] or NULL */
+    double* dbase_color;    /* [3][n] (neural) or NULL */
+    double* dfeatures;      /* [8][n] (neural) or NULL */
 } orc_grads;
 
 int orc_preprocess_f32(const orc_camera* cam, int64_t n, const double* means, const double* log_scales,

@@ -23,6 +23,7 @@ _SOURCES = ("gs_oracle.c", "gs_oracle_body.inc", "gs_oracle.h")
 
 APP_SH3 = 0
 APP_LATENT_MLP = 1
+APP_NEURAL = 2
 VISIBLE = 1
 CLAMP_X = 2
 CLAMP_Y = 4
@@ -53,7 +54,7 @@ class _Camera(C.Structure):
 class _Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p),
                 ("latent", C.c_void_p), ("mlp_w", C.c_void_p), ("dir_exact", C.c_int32),
-                ("half_act", C.c_int32)]
+                ("half_act", C.c_int32), ("base_color", C.c_void_p), ("features", C.c_void_p)]
 
 
 class _Pre(C.Structure):
@@ -65,7 +66,7 @@ class _Pre(C.Structure):
 class _Grads(C.Structure):
     _fields_ = [(name, C.c_void_p) for name in (
         "dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh", "dlatent", "dmlp_w",
-        "dmean2d", "dconic", "dopacity", "dcolor")]
+        "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color", "dfeatures")]
 
 
 _lib = None
@@ -139,9 +140,12 @@ class _SceneArrays:
         self.opacity_logits = _f64(scene.opacity_logits)
         self.sh = _f64(scene.sh) if kind == APP_SH3 else None
         self.latent = half_to_f64(scene.latent) if kind == APP_LATENT_MLP else None
-        self.mlp_w = half_to_f64(scene.mlp_w) if kind == APP_LATENT_MLP else None
+        self.mlp_w = (half_to_f64(scene.mlp_w) if kind == APP_LATENT_MLP else
+                      half_to_f64(scene.neural_w) if kind == APP_NEURAL else None)
+        self.base_color = _f64(scene.base_color) if kind == APP_NEURAL else None
+        self.features = half_to_f64(scene.features) if kind == APP_NEURAL else None
         self.app = _Appearance(kind, sh_degree, _p(self.sh), _p(self.latent), _p(self.mlp_w), int(dir_exact),
-                               int(half_act))
+                               int(half_act), _p(self.base_color), _p(self.features))
 
 
 def _kind_of(kind) -> int:
@@ -149,6 +153,8 @@ def _kind_of(kind) -> int:
         return APP_SH3
     if kind in ("latent", APP_LATENT_MLP):
         return APP_LATENT_MLP
+    if kind in ("neural", APP_NEURAL):
+        return APP_NEURAL
     raise ValueError(kind)
 
 
@@ -221,10 +227,13 @@ def render_bwd(cam, scene, pre: Preprocessed, ranges, values, dL_dimage, kind="s
              dopacity_logits=np.zeros(n),
              dsh=np.zeros((48, n)) if kind == APP_SH3 else None,
              dlatent=np.zeros((14, n)) if kind == APP_LATENT_MLP else None,
-             dmlp_w=np.zeros(1664) if kind == APP_LATENT_MLP else None,
-             dmean2d=np.zeros((2, n)), dconic=np.zeros((3, n)), dopacity=np.zeros(n), dcolor=np.zeros((3, n)))
+             dmlp_w=(np.zeros(1664) if kind == APP_LATENT_MLP else np.zeros(816) if kind == APP_NEURAL else None),
+             dmean2d=np.zeros((2, n)), dconic=np.zeros((3, n)), dopacity=np.zeros(n), dcolor=np.zeros((3, n)),
+             dbase_color=np.zeros((3, n)) if kind == APP_NEURAL else None,
+             dfeatures=np.zeros((8, n)) if kind == APP_NEURAL else None)
     gs = _Grads(*[_p(g[k]) for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh", "dlatent",
-                                      "dmlp_w", "dmean2d", "dconic", "dopacity", "dcolor")])
+                                      "dmlp_w", "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color",
+                                      "dfeatures")])
     dimg = _f64(dL_dimage)
     ranges = np.ascontiguousarray(ranges, dtype=np.int64)
     values = np.ascontiguousarray(values, dtype=np.int32)

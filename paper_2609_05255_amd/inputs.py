@@ -16,6 +16,9 @@ Layouts (all planar, channel-major, C-contiguous numpy arrays):
   sh             float32 [48][n]  row 3*k + c holds basis k, colour channel c
   latent         uint16  [14][n]  IEEE binary16 bit patterns
   mlp_w          uint16  [1664]   binary16 W1[32][17], W2[32][32], W3[3][32]
+  base_color     float32 [3][n]   neural appearance: base colour c0
+  features       uint16  [8][n]   neural appearance: binary16 features
+  neural_w       uint16  [816]    binary16 W1[16][32], W2[16][16], W3[3][16]
 """
 from __future__ import annotations
 
@@ -31,6 +34,10 @@ MLP_IN = 17
 MLP_HIDDEN = 32
 MLP_OUT = 3
 MLP_W_COUNT = MLP_HIDDEN * MLP_IN + MLP_HIDDEN * MLP_HIDDEN + MLP_OUT * MLP_HIDDEN  # 1664
+NEURAL_FEATURES = 8
+NEURAL_IN, NEURAL_HIDDEN = 32, 16
+NEURAL_W_COUNT = NEURAL_HIDDEN * NEURAL_IN + NEURAL_HIDDEN * NEURAL_HIDDEN + MLP_OUT * NEURAL_HIDDEN  # 816
+Y0 = 0.28209479177387814   # 1 / sqrt(4 pi), the degree-0 SH value
 
 SCENE_SEED = 0
 CAMERA_SEED_BASE = 1000
@@ -47,7 +54,7 @@ class Config:
     means: str            # "uniform1" (U[-1,1]^3) or "normal0.6" (N(0, 0.6^2 I))
     log_scale_mu: float
     log_scale_sigma: float
-    appearance: tuple     # subset of ("sh3", "latent")
+    appearance: tuple     # subset of ("sh3", "latent", "neural")
     fixed_camera: bool = False
 
 
@@ -59,6 +66,7 @@ CONFIGS = {
     "paper_sh3": Config("paper_sh3", 3_000_000, 1600, 1064, 16, "normal0.6", -5.0, 0.6, ("sh3",)),
     "paper_latent": Config("paper_latent", 3_000_000, 1600, 1064, 16, "normal0.6", -5.0, 0.6, ("latent",)),
     "stress": Config("stress", 6_000_000, 1920, 1080, 16, "normal0.6", -5.5, 0.7, ("sh3", "latent")),
+    "paper_neural": Config("paper_neural", 3_000_000, 1600, 1064, 16, "normal0.6", -5.0, 0.6, ("neural",)),
 }
 
 
@@ -77,13 +85,17 @@ class Scene:
     sh: np.ndarray | None = None
     latent: np.ndarray | None = None
     mlp_w: np.ndarray | None = None
+    base_color: np.ndarray | None = None
+    features: np.ndarray | None = None
+    neural_w: np.ndarray | None = None
 
     def subset(self, idx: np.ndarray) -> "Scene":
         idx = np.asarray(idx)
         pick = lambda a: None if a is None else np.ascontiguousarray(a[:, idx])
+        copy = lambda a: None if a is None else a.copy()
         return Scene(len(idx), pick(self.means), pick(self.log_scales), pick(self.quats),
                      np.ascontiguousarray(self.opacity_logits[idx]), pick(self.sh), pick(self.latent),
-                     None if self.mlp_w is None else self.mlp_w.copy())
+                     copy(self.mlp_w), pick(self.base_color), pick(self.features), copy(self.neural_w))
 
 
 def make_scene(cfg: Config | str, seed: int = SCENE_SEED, n: int | None = None,
@@ -114,6 +126,14 @@ def make_scene(cfg: Config | str, seed: int = SCENE_SEED, n: int | None = None,
         z = (_rng(seed, 7).standard_normal((LATENT_DIM, n), dtype=f32) * f32(0.5))
         scene.latent = np.ascontiguousarray(z.astype(np.float16).view(np.uint16))
         scene.mlp_w = make_mlp_weights(seed)
+    if "neural" in appearance:
+        # base colour: the SH3 scenes' degree-0 colour with Y0 folded in (c0 = Y0 sh_0);
+        # features N(0, 1) in binary16; all three layers Glorot (a non-zero residual)
+        dc = (_rng(seed, 6).standard_normal((3, n), dtype=f32) * f32(0.2) + f32(0.5)).astype(f32)
+        scene.base_color = np.ascontiguousarray((dc * f32(Y0)).astype(f32))
+        fe = _rng(seed, 9).standard_normal((NEURAL_FEATURES, n), dtype=f32)
+        scene.features = np.ascontiguousarray(fe.astype(np.float16).view(np.uint16))
+        scene.neural_w = make_neural_weights(seed)
     return scene
 
 
@@ -126,6 +146,18 @@ def make_mlp_weights(seed: int = SCENE_SEED) -> np.ndarray:
         parts.append(rng.uniform(-lim, lim, size=fan_out * fan_in).astype(np.float32))
     w = np.concatenate(parts).astype(np.float16).view(np.uint16)
     assert w.size == MLP_W_COUNT
+    return np.ascontiguousarray(w)
+
+
+def make_neural_weights(seed: int = SCENE_SEED) -> np.ndarray:
+    """Glorot-uniform weights of the 32 -> 16 -> 16 -> 3 decoder, drawn fp32, stored fp16."""
+    rng = _rng(seed, 10)
+    parts = []
+    for fan_out, fan_in in ((NEURAL_HIDDEN, NEURAL_IN), (NEURAL_HIDDEN, NEURAL_HIDDEN), (MLP_OUT, NEURAL_HIDDEN)):
+        lim = math.sqrt(6.0 / (fan_in + fan_out))
+        parts.append(rng.uniform(-lim, lim, size=fan_out * fan_in).astype(np.float32))
+    w = np.concatenate(parts).astype(np.float16).view(np.uint16)
+    assert w.size == NEURAL_W_COUNT
     return np.ascontiguousarray(w)
 
 

@@ -25,17 +25,21 @@ def fd_scene(rng, n, kind):
     logits = rng.normal(0.0, 1.0, size=n)
     logits[0] = 5.5                                  # alpha reaches the 0.99 cap near its centre
     sc = SimpleNamespace(n=n, means=means, log_scales=ls, quats=q, opacity_logits=logits,
-                         sh=None, latent=None, mlp_w=None)
+                         sh=None, latent=None, mlp_w=None, base_color=None, features=None, neural_w=None)
     # one large Gaussian beyond the guard band on x, its footprint still on screen
     sc.means[:, 1] = [-2.8, 0.1, 0.0]
     sc.log_scales[:, 1] = [-0.2, -0.5, -0.4]
     if kind == "sh3":
         sc.sh = rng.normal(0.0, 0.3, size=(48, n))
         sc.sh[0:3] = rng.normal(0.4, 0.8, size=(3, n))   # some colours clamp at 0
-    else:
+    elif kind == "latent":
         sc.latent = rng.normal(0.0, 0.5, size=(14, n))
         w = inputs.make_mlp_weights(3).view(np.float16).astype(np.float64) * 2.0
         sc.mlp_w = w
+    else:
+        sc.base_color = rng.normal(0.1, 0.5, size=(3, n))    # some colours clamp at 0
+        sc.features = rng.normal(0.0, 1.5, size=(8, n))
+        sc.neural_w = inputs.make_neural_weights(3).view(np.float16).astype(np.float64) * 1.5
     return sc
 
 
@@ -51,14 +55,16 @@ def run(orc, cam, sc, kind, g):
 
 
 FIELDS = {"sh3": ["means", "log_scales", "quats", "opacity_logits", "sh"],
-          "latent": ["means", "log_scales", "quats", "opacity_logits", "latent", "mlp_w"]}
+          "latent": ["means", "log_scales", "quats", "opacity_logits", "latent", "mlp_w"],
+          "neural": ["means", "log_scales", "quats", "opacity_logits", "base_color", "features", "neural_w"]}
 GRAD_NAME = {"means": "dmeans", "log_scales": "dlog_scales", "quats": "dquats",
-             "opacity_logits": "dopacity_logits", "sh": "dsh", "latent": "dlatent", "mlp_w": "dmlp_w"}
+             "opacity_logits": "dopacity_logits", "sh": "dsh", "latent": "dlatent", "mlp_w": "dmlp_w",
+             "base_color": "dbase_color", "features": "dfeatures", "neural_w": "dmlp_w"}
 
 
-@pytest.mark.parametrize("kind", ["sh3", "latent"])
+@pytest.mark.parametrize("kind", ["sh3", "latent", "neural"])
 def test_gradients_match_finite_differences(orc, kind):
-    rng = np.random.default_rng(42 if kind == "sh3" else 43)
+    rng = np.random.default_rng({"sh3": 42, "latent": 43, "neural": 44}[kind])
     n = 10
     sc = fd_scene(rng, n, kind)
     cam = inputs.look_at_camera([0.3, -0.4, -2.9], 40, 36, bg=(0.2, 0.3, 0.1))
@@ -76,7 +82,7 @@ def test_gradients_match_finite_differences(orc, kind):
         assert scale > 0, field
         flat = arr.reshape(-1)
         idx = np.arange(flat.size)
-        if field == "mlp_w":
+        if field in ("mlp_w", "neural_w"):
             idx = rng.choice(flat.size, 160, replace=False)
         for k in idx:
             x = flat[k]

@@ -1,0 +1,92 @@
+"""Closed-form pins of the oracle's neural appearance (the paper's Sec. 4
+decoder: input = (SH basis of the view direction up to the active degree,
+(sin f, cos f) of each of 8 features), 32 -> 16 -> 16 -> 3 without biases,
+ReLU hidden units, residual tanh(MLP(x)), colour max(0, c0 + residual + 0.5);
+the residual is off while the active degree is 0). Its backward is pinned by
+finite differences in test_oracle_grad.py."""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2609_05255_amd import inputs
+
+C1 = math.sqrt(3.0 / (4.0 * math.pi))
+
+
+def scene(n=64):
+    sc = inputs.make_scene("tiny", n=n, appearance=("neural",))
+    return sc
+
+
+def selector(k):
+    """W1 copies input k to hidden unit 0, W2 copies unit 0, W3 copies it to all outputs."""
+    w = np.zeros(816, np.float16)
+    w[0 * 32 + k] = 1.0
+    w[512 + 0] = 1.0
+    for ch in range(3):
+        w[512 + 256 + ch * 16 + 0] = 1.0
+    return w.view(np.uint16)
+
+
+def colours(orc, sc, cam, degree, dir_exact=True):
+    pre = orc.preprocess(cam, sc, kind="neural", sh_degree=degree, mode="f64", dir_exact=dir_exact)
+    vis = pre["tiles"] > 0
+    assert vis.sum() > 10
+    return pre["color"], vis
+
+
+def directions(sc, cam):
+    v = sc.means.astype(np.float64) - np.asarray(cam.campos, np.float64)[:, None]
+    return v / np.linalg.norm(v, axis=0)
+
+
+def base(sc):
+    return sc.base_color.astype(np.float32).astype(np.float64)
+
+
+def test_degree_zero_disables_the_residual(orc):
+    sc = scene()
+    cam = inputs.make_cameras("tiny")[0]
+    col, vis = colours(orc, sc, cam, 0)
+    assert np.array_equal(col[:, vis], np.maximum(0.0, base(sc) + 0.5)[:, vis])
+
+
+def test_zero_output_layer_gives_the_base_colour(orc):
+    sc = scene()
+    w = sc.neural_w.view(np.float16).copy()
+    w[768:] = 0
+    sc.neural_w = w.view(np.uint16)
+    cam = inputs.make_cameras("tiny")[0]
+    col, vis = colours(orc, sc, cam, 3)
+    assert np.array_equal(col[:, vis], np.maximum(0.0, base(sc) + 0.5)[:, vis])
+
+
+@pytest.mark.parametrize("k,what", [(16, "sin f0"), (23, "cos f3"), (1, "Y1"), (4, "Y4 inactive at degree 1")])
+def test_selector_networks(orc, k, what):
+    sc = scene()
+    sc.neural_w = selector(k)
+    cam = inputs.make_cameras("tiny")[0]
+    f = sc.features.view(np.float16).astype(np.float64)
+    d = directions(sc, cam)
+    x = {16: np.sin(f[0]), 23: np.cos(f[3]), 1: -C1 * d[1], 4: np.zeros(sc.n)}[k]
+    expect = np.maximum(0.0, base(sc) + np.tanh(np.maximum(0.0, x))[None] + 0.5)
+    col, vis = colours(orc, sc, cam, 1)
+    assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12), what
+    # with the inputs rounded to binary16, as the half-precision decoder sees them
+    col, vis = colours(orc, sc, cam, 1, dir_exact=False)
+    xh = x.astype(np.float16).astype(np.float64)
+    expect = np.maximum(0.0, base(sc) + np.tanh(np.maximum(0.0, xh))[None] + 0.5)
+    assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12), what
+
+
+def test_degree_two_input_is_active_at_degree_two(orc):
+    # Y4 = sqrt(15/(4 pi)) x y (degree 2, m = -2), silent at degree 1 (above)
+    sc = scene()
+    sc.neural_w = selector(4)
+    cam = inputs.make_cameras("tiny")[0]
+    d = directions(sc, cam)
+    x = math.sqrt(15.0 / (4.0 * math.pi)) * d[0] * d[1]
+    col, vis = colours(orc, sc, cam, 2)
+    expect = np.maximum(0.0, base(sc) + np.tanh(np.maximum(0.0, x))[None] + 0.5)
+    assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12)

@@ -88,6 +88,8 @@ def parse():
 
 def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int = 3) -> float | None:
     """HBM bytes a launch must move at minimum (per launch, averaged over cameras)."""
+    # appearance bytes per visible Gaussian: SH3 48 fp32, latent 14 binary16, neural a 12 B
+    # base colour and 8 binary16 features
     app = 4 * 3 * (sh_degree + 1) ** 2 if kind == "sh3" else 28
     if kernel == "preprocess":
         # params 44 B + tiles 4 B + depth key 4 B per Gaussian; appearance + 48 B of projected splat
@@ -96,7 +98,7 @@ def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int
         return n * (44 + 8) + vis * (app + 48)
     if kernel == "preprocess_bwd":
         # tiles 4 B + dense gradient writes per Gaussian; params, accumulators and appearance per visible one
-        grad = 44 + (4 * 48 if kind == "sh3" else 4 * 14)
+        grad = 44 + 4 * {"sh3": 48, "latent": 14, "neural": 11}[kind]
         return n * (4 + grad) + vis * (44 + 36 + app)
     return None
 
@@ -114,7 +116,7 @@ def main():
 
     cfg = inputs.CONFIGS[args.config]
     kind = args.appearance or cfg.appearance[0]
-    kid = gs.GS_APP_SH3 if kind == "sh3" else gs.GS_APP_LATENT_MLP
+    kid = {"sh3": gs.GS_APP_SH3, "latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL}[kind]
     torch.cuda.set_device(0)
     dev = "cuda:0"
     t0 = time.time()

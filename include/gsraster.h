@@ -80,20 +80,34 @@ typedef struct gs_gaussians {
 enum {
     GS_APP_SH3 = 0,           /* eq. sh_color_eval: c = max(0, 0.5 + sum_k Y_k(d) sh_k) */
     GS_APP_LATENT_MLP = 1,    /* c = sigmoid(W3 relu(W2 relu(W1 [z, d]))), no biases */
+    GS_APP_NEURAL = 2,        /* Sec. 4 (eq. mlp_input, eq. neural_color_eval, eq. common_appearance):
+                                 c = max(0, c0 + tanh(W3 relu(W2 relu(W1 x))) + 0.5), no biases,
+                                 x = (Y_0..15(d) with bands above sh_degree zero,
+                                      sin f_0, cos f_0, ..., sin f_7, cos f_7) */
 };
+
+#define GS_NEURAL_FEATURES 8  /* binary16 features per Gaussian (16 B) beside a 12 B fp32 base colour */
+#define GS_NEURAL_WEIGHTS 816 /* 16*32 + 16*16 + 3*16 */
 
 /* View-dependent appearance (Sec. 3.1 and 4). d is the unit vector from the camera
  * centre to the Gaussian's mean, in world coordinates. */
 typedef struct gs_appearance {
     int32_t kind;             /* GS_APP_* */
-    int32_t sh_degree;        /* SH3 only: bands 0..sh_degree are used (0..3) */
+    int32_t sh_degree;        /* SH3: bands 0..sh_degree are used (0..3). NEURAL: the active
+                                 degree of the direction encoding (0..3); at 0 the residual
+                                 is off and c = max(0, c0 + 0.5) (the paper's schedule) */
     const float* sh;          /* SH3: [48][n] fp32, row 3*k + c = basis k, channel c.
                                  Basis order l = 0..3, m = -l..l; real SH with the
                                  Condon-Shortley phase: band 1 = sqrt(3/(4 pi)) (-y, z, -x) */
     const uint16_t* latent;   /* LATENT_MLP: [14][n] binary16 bit patterns */
     const uint16_t* mlp_w;    /* LATENT_MLP: binary16 W1[32][17], W2[32][32], W3[3][32], row-major
                                  [out][in], concatenated (1664 values). The decoder sees d
-                                 rounded to binary16 and accumulates in fp32. */
+                                 rounded to binary16 and accumulates in fp32.
+                                 NEURAL: binary16 W1[16][32], W2[16][16], W3[3][16] (816 values);
+                                 the decoder's inputs and hidden activations are binary16,
+                                 its sums fp32, tanh in fp32 */
+    const float* base_color;  /* NEURAL: [3][n] fp32 base colour c0 */
+    const uint16_t* features; /* NEURAL: [8][n] binary16 bit patterns */
 } gs_appearance;
 
 /* Screen-space record of one Gaussian, written by gs_preprocess (64 bytes).
@@ -132,8 +146,10 @@ typedef struct gs_grads {
     float* dopacity_logits;   /* [n] */
     float* dsh;               /* SH3: [48][n]; rows of bands above sh_degree are zero */
     float* dlatent;           /* LATENT_MLP: [14][n] fp32 */
-    float* dmlp_w;            /* LATENT_MLP: [1664] fp32, same order as mlp_w */
+    float* dmlp_w;            /* LATENT_MLP: [1664], NEURAL: [816] fp32, same order as mlp_w */
     float* dmean2d;           /* optional (may be NULL): [2][n] screen-space mean gradient */
+    float* dbase_color;       /* NEURAL: [3][n] */
+    float* dfeatures;         /* NEURAL: [8][n] fp32 (the gradient passes the binary16 storage) */
 } gs_grads;
 
 /*

@@ -78,6 +78,11 @@ gs_status check_appearance(const gs_appearance* a, int64_t n)
         GS_CHECK(n == 0 || a->sh != nullptr, "sh is NULL");
     } else if (a->kind == GS_APP_LATENT_MLP) {
         GS_CHECK(n == 0 || (a->latent != nullptr && a->mlp_w != nullptr), "latent or mlp_w is NULL");
+    } else if (a->kind == GS_APP_NEURAL) {
+        GS_CHECK(a->sh_degree >= 0 && a->sh_degree <= 3, "sh_degree %d outside 0..3", a->sh_degree);
+        GS_CHECK(n == 0 || a->base_color != nullptr, "base_color is NULL");
+        GS_CHECK(n == 0 || a->sh_degree == 0 || (a->features != nullptr && a->mlp_w != nullptr),
+                 "features or mlp_w is NULL");
     } else {
         return fail(GS_ERR_INVALID_ARG, "unknown appearance kind %d", a->kind);
     }
@@ -195,7 +200,8 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.pair_keys_b = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.pair_vals_b = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.acc = (float*)take(sizeof(float) * kAccStride * nn);
-    w.mlp_part = (float*)take(kind == GS_APP_LATENT_MLP ? sizeof(float) * GS_MLP_WEIGHTS * kMlpPartials : 0);
+    w.mlp_part = (float*)take(kind == GS_APP_LATENT_MLP ? sizeof(float) * GS_MLP_WEIGHTS * kMlpPartials
+                              : kind == GS_APP_NEURAL ? sizeof(float) * GS_NEURAL_WEIGHTS * kMlpPartials : 0);
     w.bytes = off;
     return w;
 }
@@ -242,7 +248,8 @@ gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t c
     GS_CHECK(n >= 0 && n < ((int64_t)1 << 31), "n out of range");
     GS_CHECK(width > 0 && height > 0, "image size must be positive");
     GS_CHECK(capacity < ((uint64_t)1 << 32), "capacity must be below 2^32");
-    GS_CHECK(kind == GS_APP_SH3 || kind == GS_APP_LATENT_MLP, "unknown appearance kind %d", kind);
+    GS_CHECK(kind == GS_APP_SH3 || kind == GS_APP_LATENT_MLP || kind == GS_APP_NEURAL, "unknown appearance kind %d",
+             kind);
     *bytes = layout_workspace(nullptr, n, capacity, kind).bytes;
     return ok();
 }
@@ -366,6 +373,9 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
         GS_CHECK(grads->dmeans && grads->dlog_scales && grads->dquats && grads->dopacity_logits,
                  "a geometry gradient array is NULL");
         if (app->kind == GS_APP_SH3) GS_CHECK(grads->dsh != nullptr, "dsh is NULL");
+        else if (app->kind == GS_APP_NEURAL)
+            GS_CHECK(grads->dbase_color && grads->dfeatures && grads->dmlp_w,
+                     "dbase_color, dfeatures or dmlp_w is NULL");
         else GS_CHECK(grads->dlatent && grads->dmlp_w, "dlatent or dmlp_w is NULL");
     }
     const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind);
@@ -375,6 +385,7 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
     const Cam c = make_cam(*cam);
     if (g->n == 0) {
         if (app->kind == GS_APP_LATENT_MLP) GS_HIP(launch_clear(grads->dmlp_w, GS_MLP_WEIGHTS, s));
+        if (app->kind == GS_APP_NEURAL && grads->dmlp_w) GS_HIP(launch_clear(grads->dmlp_w, GS_NEURAL_WEIGHTS, s));
         return ok();
     }
     timing_begin(GS_KERNEL_CLEAR, s);
@@ -386,9 +397,9 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
     timing_begin(GS_KERNEL_PREPROCESS_BWD, s);
     GS_HIP(launch_preprocess_bwd(c, *g, *app, *pre, ws, *grads, s));
     timing_end(GS_KERNEL_PREPROCESS_BWD, s);
-    if (app->kind == GS_APP_LATENT_MLP) {
+    if (app->kind == GS_APP_LATENT_MLP || app->kind == GS_APP_NEURAL) {
         timing_begin(GS_KERNEL_MLP_REDUCE, s);
-        GS_HIP(launch_mlp_reduce(g->n, ws, grads->dmlp_w, s));
+        GS_HIP(launch_mlp_reduce(g->n, app->kind, ws, grads->dmlp_w, s));
         timing_end(GS_KERNEL_MLP_REDUCE, s);
     }
     return ok();

@@ -7,6 +7,7 @@
 // of culled Gaussians are written as zeros, so every output is dense.
 #include "gs_internal.h"
 #include "mlp.h"
+#include "neural.h"
 #include "sh.h"
 
 namespace gsr {
@@ -24,6 +25,8 @@ struct BwdArgs {
     const float* sh;
     const uint16_t* latent;
     const uint16_t* mlp_w;
+    const float* base_color;
+    const uint16_t* features;
     const uint32_t* tiles_touched;
     const float* acc;
     float* dmeans;
@@ -34,6 +37,8 @@ struct BwdArgs {
     float* dlatent;
     float* mlp_part;
     float* dmean2d;
+    float* dbase_color;
+    float* dfeatures;
 };
 
 struct GeoGrad {
@@ -318,31 +323,153 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
         a.mlp_part[(size_t)blockIdx.x * GS_MLP_WEIGHTS + k] = red[k];
 }
 
+// Neural appearance backward (neural.h): as the latent one -- per wave chunk of
+// 64 Gaussians the decoder inputs, colour gradients, base colours, features and
+// directions are staged, each tile of 16 is recomputed and differentiated on
+// the matrix cores (base-colour and feature gradients, the direction gradient
+// of the active bands, the weight-gradient sums), then the geometry backward.
+// While the active degree is 0 only the base colour takes a gradient.
+__global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
+{
+    __shared__ NeuralFrags W;
+    __shared__ NeuralBwdStage ST[kBlock / kWave];
+    const bool resid = a.sh_degree >= 1;
+    if (resid) neural_load_frags(a.mlp_w, W, true);
+    const int wave = threadIdx.x >> 6, lane = __lane_id();
+    NeuralBwdStage& st = ST[wave];
+    NeuralGradAcc acc;
+    neural_grad_zero(acc);
+    const int64_t n = a.n;
+    const int64_t nchunks = div_up(n, kBlock);
+    for (int64_t chunk = blockIdx.x; chunk < nchunks; chunk += gridDim.x) {
+        const int64_t i = chunk * kBlock + threadIdx.x;
+        const bool inb = i < n;
+        const bool valid = inb && a.tiles_touched[i] != 0;
+        if (inb && !valid) {
+            write_zero_grads(a, (int)i);
+            for (int ch = 0; ch < 3; ++ch) a.dbase_color[ch * n + i] = 0.f;
+            for (int j = 0; j < GS_NEURAL_FEATURES; ++j) a.dfeatures[j * n + i] = 0.f;
+        }
+        float d[3] = {0.f, 0.f, 0.f}, dc[3] = {0.f, 0.f, 0.f}, c0[3] = {0.f, 0.f, 0.f};
+        float len = 1.f;
+        if (valid) {
+            float mu[3];
+            for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
+            const float vx = mu[0] - a.cam.campos[0], vy = mu[1] - a.cam.campos[1], vz = mu[2] - a.cam.campos[2];
+            len = sqrtf(vx * vx + vy * vy + vz * vz);
+            d[0] = vx / len;
+            d[1] = vy / len;
+            d[2] = vz / len;
+            const float* ap = a.acc + (size_t)i * kAccStride;
+            for (int ch = 0; ch < 3; ++ch) dc[ch] = ap[6 + ch];
+            for (int ch = 0; ch < 3; ++ch) c0[ch] = a.base_color[ch * n + i];
+        }
+        if (resid) {
+            float f[GS_NEURAL_FEATURES];
+            for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
+                f[j] = valid ? (float)half_of_bits(a.features[j * n + i]) : 0.f;
+            neural_stage_inputs(st.x, valid, d, a.sh_degree, f);
+            for (int ch = 0; ch < 3; ++ch) {
+                st.dc[lane][ch] = dc[ch];
+                st.c0[lane][ch] = c0[ch];
+                st.d[lane][ch] = d[ch];
+                st.dd[lane][ch] = 0.f;
+            }
+            st.dc[lane][3] = 0.f;   // padding column: the Gaussian-major reads take channel 3 there
+            st.c0[lane][3] = 0.f;
+            for (int j = 0; j < GS_NEURAL_FEATURES; ++j) st.f[lane][j] = f[j];
+            // the chunk's gradient scale (a power of two, see neural_chunk_exponent)
+            const float m = wave_max(fmaxf(fmaxf(fabsf(dc[0]), fabsf(dc[1])), fabsf(dc[2])));
+            neural_grad_rescale(acc, neural_chunk_exponent(m, acc.se));
+            const float scale = ldexpf(1.f, acc.se), inv = ldexpf(1.f, -acc.se);
+            wave_lds_sync();
+            const uint64_t vis = __ballot(valid);
+            const int64_t base = chunk * kBlock + (threadIdx.x & ~(kWave - 1));
+            for (int t = 0; t < kWave / 16; ++t) {
+                if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
+                neural_tile_bwd(W, st, t, vis, a.sh_degree, a.dbase_color, a.dfeatures, n, base, scale, inv, acc);
+            }
+            wave_lds_sync();
+        } else if (valid) {
+            // no residual: c = max(0, c0 + 0.5)
+            for (int ch = 0; ch < 3; ++ch) a.dbase_color[ch * n + i] = c0[ch] + 0.5f > 0.f ? dc[ch] : 0.f;
+            for (int j = 0; j < GS_NEURAL_FEATURES; ++j) a.dfeatures[j * n + i] = 0.f;
+        }
+        if (valid) {
+            float mu[3], ls[3], q[4], g9[kAccStride];
+            for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
+            for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
+            for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
+            const float* ap = a.acc + (size_t)i * kAccStride;
+            for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+            GeoGrad gg;
+            geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
+            if (resid) {
+                // the binary16 rounding of the SH inputs passes the gradient; d = v / |v|
+                const float dd0 = st.dd[lane][0], dd1 = st.dd[lane][1], dd2 = st.dd[lane][2];
+                const float dot = d[0] * dd0 + d[1] * dd1 + d[2] * dd2;
+                const float il = 1.f / len;
+                gg.dmu[0] += (dd0 - d[0] * dot) * il;
+                gg.dmu[1] += (dd1 - d[1] * dot) * il;
+                gg.dmu[2] += (dd2 - d[2] * dot) * il;
+            }
+            for (int j = 0; j < 3; ++j) { a.dmeans[j * n + i] = gg.dmu[j]; a.dlog_scales[j * n + i] = gg.dls[j]; }
+            for (int j = 0; j < 4; ++j) a.dquats[j * n + i] = gg.dq[j];
+            a.dlogits[i] = gg.dlogit;
+            if (a.dmean2d) { a.dmean2d[i] = g9[0]; a.dmean2d[n + i] = g9[1]; }
+        }
+        if (resid) wave_lds_sync();   // st.dd is read before the next chunk restages
+    }
+    // workgroup sum of the four waves' weight gradients, in wave order, in the
+    // LDS of the (no longer needed) stage
+    static_assert(sizeof(ST) >= GS_NEURAL_WEIGHTS * sizeof(float), "reduction buffer");
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(&ST[0]);
+    for (int k = threadIdx.x; k < GS_NEURAL_WEIGHTS; k += kBlock) red[k] = 0.f;
+    __syncthreads();
+    const int g = lane >> 4, c = lane & 15;
+    neural_grad_rescale(acc, 0);   // back to plain units
+    for (int w = 0; w < kBlock / kWave; ++w) {
+        if (wave == w && resid) {
+            for (int e = 0; e < 4; ++e) {
+                const int row = 4 * g + e;
+                for (int fb = 0; fb < 2; ++fb) red[row * kNeuralIn + 16 * fb + c] += acc.w1[fb][e];
+                red[kNeuralHidden * kNeuralIn + row * kNeuralHidden + c] += acc.w2[e];
+                if (row < GS_MLP_OUT)
+                    red[kNeuralHidden * kNeuralIn + kNeuralHidden * kNeuralHidden + row * kNeuralHidden + c] += acc.w3[e];
+            }
+        }
+        __syncthreads();
+    }
+    for (int k = threadIdx.x; k < GS_NEURAL_WEIGHTS; k += kBlock)
+        a.mlp_part[(size_t)blockIdx.x * GS_NEURAL_WEIGHTS + k] = red[k];
+}
+
 // dW = sum of the per-workgroup partials, in a fixed order. One workgroup per
 // 64 weights: thread (row, column) sums every 16th partial starting at its row,
 // then the 16 row sums are added in row order.
 constexpr int kReduceRows = 16, kReduceCols = 64;
 __global__ __launch_bounds__(kReduceRows * kReduceCols) void k_mlp_reduce(const float* __restrict__ part, int nparts,
-                                                                          float* __restrict__ dw)
+                                                                          int nw, float* __restrict__ dw)
 {
     __shared__ float rows[kReduceRows][kReduceCols];
     const int c = threadIdx.x % kReduceCols, r = threadIdx.x / kReduceCols;
     const int k = blockIdx.x * kReduceCols + c;
     float s = 0.f;
-    if (k < GS_MLP_WEIGHTS) {
+    if (k < nw) {
         int b = r;
         for (; b + 3 * kReduceRows < nparts; b += 4 * kReduceRows) {
-            const float v0 = part[(size_t)b * GS_MLP_WEIGHTS + k];
-            const float v1 = part[(size_t)(b + kReduceRows) * GS_MLP_WEIGHTS + k];
-            const float v2 = part[(size_t)(b + 2 * kReduceRows) * GS_MLP_WEIGHTS + k];
-            const float v3 = part[(size_t)(b + 3 * kReduceRows) * GS_MLP_WEIGHTS + k];
+            const float v0 = part[(size_t)b * nw + k];
+            const float v1 = part[(size_t)(b + kReduceRows) * nw + k];
+            const float v2 = part[(size_t)(b + 2 * kReduceRows) * nw + k];
+            const float v3 = part[(size_t)(b + 3 * kReduceRows) * nw + k];
             s = (((s + v0) + v1) + v2) + v3;
         }
-        for (; b < nparts; b += kReduceRows) s += part[(size_t)b * GS_MLP_WEIGHTS + k];
+        for (; b < nparts; b += kReduceRows) s += part[(size_t)b * nw + k];
     }
     rows[r][c] = s;
     __syncthreads();
-    if (r == 0 && k < GS_MLP_WEIGHTS) {
+    if (r == 0 && k < nw) {
         float t = 0.f;
         for (int j = 0; j < kReduceRows; ++j) t += rows[j][c];
         dw[k] = t;
@@ -365,6 +492,8 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
     a.sh = app.sh;
     a.latent = app.latent;
     a.mlp_w = app.mlp_w;
+    a.base_color = app.base_color;
+    a.features = app.features;
     a.tiles_touched = pre.tiles_touched;
     a.acc = ws.acc;
     a.dmeans = gr.dmeans;
@@ -375,17 +504,22 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
     a.dlatent = gr.dlatent;
     a.mlp_part = ws.mlp_part;
     a.dmean2d = gr.dmean2d;
+    a.dbase_color = gr.dbase_color;
+    a.dfeatures = gr.dfeatures;
     if (app.kind == GS_APP_SH3)
         hipLaunchKernelGGL(k_preprocess_bwd_sh3, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
+    else if (app.kind == GS_APP_NEURAL)
+        hipLaunchKernelGGL(k_preprocess_bwd_neural, dim3(latent_bwd_grid(g.n)), dim3(kBlock), 0, s, a);
     else
         hipLaunchKernelGGL(k_preprocess_bwd_latent, dim3(latent_bwd_grid(g.n)), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 
-hipError_t launch_mlp_reduce(int64_t n, const Workspace& ws, float* dmlp_w, hipStream_t s)
+hipError_t launch_mlp_reduce(int64_t n, int32_t kind, const Workspace& ws, float* dmlp_w, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_mlp_reduce, dim3((unsigned)div_up(GS_MLP_WEIGHTS, kReduceCols)),
-                       dim3(kReduceRows * kReduceCols), 0, s, ws.mlp_part, latent_bwd_grid(n), dmlp_w);
+    const int nw = kind == GS_APP_NEURAL ? GS_NEURAL_WEIGHTS : GS_MLP_WEIGHTS;
+    hipLaunchKernelGGL(k_mlp_reduce, dim3((unsigned)div_up(nw, kReduceCols)), dim3(kReduceRows * kReduceCols), 0, s,
+                       ws.mlp_part, latent_bwd_grid(n), nw, dmlp_w);
     return hipGetLastError();
 }
 

@@ -124,7 +124,7 @@ hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32
 hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                                  const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr,
                                  hipStream_t s);
-hipError_t launch_mlp_reduce(int64_t n, const Workspace& ws, float* dmlp_w, hipStream_t s);
+hipError_t launch_mlp_reduce(int64_t n, int32_t kind, const Workspace& ws, float* dmlp_w, hipStream_t s);
 hipError_t launch_adam(const gs_adam_tensor* tensors, int count, float beta1, float eps, int64_t step, hipStream_t s);
 hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s);
 

@@ -1,0 +1,285 @@
+// The paper's neural appearance decoder (Sec. 4, eq. mlp_input and
+// eq. neural_color_eval) on the matrix cores, 16 Gaussians at a time: input
+// x = (SH basis of the view direction up to the active degree, zero above it;
+// (sin f_j, cos f_j) of the 8 features), a 32 -> 16 -> 16 -> 3 network without
+// biases and with ReLU hidden units, residual tanh(MLP(x)), colour
+// max(0, c0 + residual + 0.5) (eq. common_appearance with the baseline
+// activation). Inputs and hidden activations are binary16 operands, sums fp32.
+//
+// Fragment layouts and the two orientations are those of mlp.h: layer 1 is one
+// 32-deep product (slot s(g, j) carries input s(g, j)), layers 2 and 3 and every
+// backward product are 16-deep, whose D fragment of one layer is the B fragment
+// of the next. Swapping the A and B registers of a product gives its transpose
+// (Gaussian-major), which the weight gradients take as operands.
+#pragma once
+
+#include "mlp.h"
+#include "sh.h"
+
+namespace gsr {
+
+constexpr int kNeuralIn = 32, kNeuralHidden = 16;
+
+// Per-workgroup weight fragments (W1[16][32], W2[16][16], W3[3][16], binary16).
+struct NeuralFrags {
+    alignas(16) _Float16 w1a[kWave][8];     // A of W1:   rows n1 = c,             K = input s(g, j)
+    alignas(8) _Float16 w2a[kWave][4];      // A of W2:   rows n2 = c,             K = n1 = 4g + j
+    alignas(8) _Float16 w3a[kWave][4];      // A of W3:   rows o = c (< 3),        K = n2 = 4g + j
+    alignas(8) _Float16 w1t[2][kWave][4];   // A of W1^T: rows input = 16b + c,   K = n1 = 4g + j
+    alignas(8) _Float16 w2t[kWave][4];      // A of W2^T: rows n1 = c,             K = n2 = 4g + j
+    alignas(8) _Float16 w3t[kWave][4];      // A of W3^T: rows n2 = c,             K = o = 4g + j (< 3)
+};
+
+// Loads the weights into the fragments (the transposed ones only if
+// `backward`). Called by every thread of the workgroup; ends with a barrier.
+__device__ __forceinline__ void neural_load_frags(const uint16_t* __restrict__ w, NeuralFrags& s, bool backward)
+{
+    const _Float16* W1 = reinterpret_cast<const _Float16*>(w);
+    const _Float16* W2 = W1 + kNeuralHidden * kNeuralIn;
+    const _Float16* W3 = W2 + kNeuralHidden * kNeuralHidden;
+    const _Float16 z = (_Float16)0.f;
+    for (int e = threadIdx.x; e < kWave * 8; e += blockDim.x) {
+        const int l = e >> 3, j = e & 7, g = l >> 4, c = l & 15;
+        s.w1a[l][j] = W1[c * kNeuralIn + kslot(g, j)];
+        if (j < 4) {
+            const int k = 4 * g + j;
+            s.w2a[l][j] = W2[c * kNeuralHidden + k];
+            s.w3a[l][j] = c < GS_MLP_OUT ? W3[c * kNeuralHidden + k] : z;
+            if (backward) {
+                for (int b = 0; b < 2; ++b) s.w1t[b][l][j] = W1[k * kNeuralIn + 16 * b + c];
+                s.w2t[l][j] = W2[k * kNeuralHidden + c];
+                s.w3t[l][j] = k < GS_MLP_OUT ? W3[k * kNeuralHidden + c] : z;
+            }
+        }
+    }
+    __syncthreads();
+}
+
+// Per-wave staging: each Gaussian's 32 binary16 inputs (rows of kXPitch
+// halves), and for the backward its colour gradient, base colour, features
+// (fp32) and view direction, and the direction gradient the tiles produce.
+struct NeuralInStage {
+    alignas(16) _Float16 x[kWave][kXPitch];
+};
+
+struct NeuralBwdStage {
+    alignas(16) _Float16 x[kWave][kXPitch];
+    float dc[kWave][4];
+    float c0[kWave][4];
+    float f[kWave][8];
+    float d[kWave][4];
+    float dd[kWave][4];
+};
+
+// The calling lane's decoder input: SH basis values of d for bands <= degree
+// (zero above), then (sin f_j, cos f_j) for the 8 features, rounded to binary16
+// (zeros when !valid).
+__device__ __forceinline__ void neural_stage_inputs(_Float16 (*x)[kXPitch], bool valid, const float d[3], int degree,
+                                                    const float f[GS_NEURAL_FEATURES])
+{
+    const int l = __lane_id();
+    half4_t v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = half4_t{0, 0, 0, 0};
+    if (valid) {
+        float Y[16];
+        sh_basis16(d[0], d[1], d[2], Y);
+        const int nb = (degree + 1) * (degree + 1);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) v[k >> 2][k & 3] = k < nb ? (_Float16)Y[k] : (_Float16)0.f;
+#pragma unroll
+        for (int j = 0; j < GS_NEURAL_FEATURES; ++j) {
+            const int e = 16 + 2 * j;
+            v[e >> 2][e & 3] = (_Float16)sinf(f[j]);
+            v[(e + 1) >> 2][(e + 1) & 3] = (_Float16)cosf(f[j]);
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) *reinterpret_cast<half4_t*>(&x[l][4 * q]) = v[q];
+}
+
+// B fragment of tile t: inputs s(g, 0..7) of Gaussian 16t + c.
+__device__ __forceinline__ half8_t neural_stage_frag(const _Float16 (*x)[kXPitch], int t)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    const half4_t lo = *reinterpret_cast<const half4_t*>(&x[16 * t + c][4 * g]);
+    const half4_t hi = *reinterpret_cast<const half4_t*>(&x[16 * t + c][16 + 4 * g]);
+    return half8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+// Neuron-major forward of one tile: h1, h2 the fp32 pre-activations of neurons
+// 4g + i of Gaussian c, a1, a2 their binary16 activations (next B fragments),
+// o the output pre-activations (channel i of Gaussian c in lanes 0..15, i < 3).
+__device__ __forceinline__ void neural_tile_fwd(const NeuralFrags& W, const half8_t& x, float4_t& h1, half4_t& a1,
+                                                float4_t& h2, half4_t& a2, float4_t& o)
+{
+    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
+    h1 = mfma32(frag8(W.w1a), x, zero);
+    a1 = relu_half4(h1);
+    h2 = mfma16(frag4(W.w2a), a1, zero);
+    a2 = relu_half4(h2);
+    o = mfma16(frag4(W.w3a), a2, zero);
+}
+
+// Hands the residuals tanh(o) of tile t to the lanes that own its Gaussians
+// (lane 16t + c takes Gaussian c's three channels from lane c).
+__device__ __forceinline__ void neural_tile_residual(const float4_t& o, int t, float res[3])
+{
+    const int lane = __lane_id();
+    const int src = lane & 15;
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) {
+        const float v = __shfl(tanhf(o[ch]), src);
+        if ((lane >> 4) == t) res[ch] = v;
+    }
+}
+
+// Running sums of the weight gradients (Gaussian-major products, fp32, in
+// units of 2^-se): w1[fb] rows n1 = 4g + i, columns input 16fb + c; w2 rows
+// n2 = 4g + i, columns n1 = c; w3 rows o = 4g + i, columns n2 = c.
+struct NeuralGradAcc {
+    float4_t w1[2], w2, w3;
+    int se;
+};
+
+__device__ __forceinline__ void neural_grad_zero(NeuralGradAcc& a)
+{
+    const float4_t z = {0.f, 0.f, 0.f, 0.f};
+    a.w1[0] = a.w1[1] = a.w2 = a.w3 = z;
+    a.se = 0;
+}
+
+__device__ __forceinline__ void neural_grad_rescale(NeuralGradAcc& a, int se)
+{
+    if (se == a.se) return;
+    const int e = se - a.se;
+    a.w1[0] = ldexp4(a.w1[0], e);
+    a.w1[1] = ldexp4(a.w1[1], e);
+    a.w2 = ldexp4(a.w2, e);
+    a.w3 = ldexp4(a.w3, e);
+    a.se = se;
+}
+
+// Scale exponent of a chunk whose largest colour-gradient magnitude is m: the
+// output gradients dL/dc [c > 0] (1 - tanh^2) <= m stay below 2^10 after
+// scaling by 2^se, far from the binary16 subnormals and from overflow along
+// the chain. m = 0 keeps the previous exponent.
+__device__ __forceinline__ int neural_chunk_exponent(float m, int prev)
+{
+    if (!(m > 0.f)) return prev;
+    int ex = 0;
+    frexpf(m, &ex);
+    return min(10 - ex, 100);
+}
+
+// Backward of tile t (Gaussians base + 16t .. base + 16t + 15 of the wave)
+// from the staged inputs, colour gradients and base colours, with the chunk's
+// gradient scale 2^se (acc.se): delta3 = dL/dc [c0 + res + 0.5 > 0] (1 - res^2)
+// enters the matrix cores scaled; dH2, dH1 and dX are chained neuron-major
+// (binary16 hi + lo operands); the Gaussian-major copies give
+//   dW3 = sum_G delta3 h2^T, dW2 = sum_G dh2 h1^T, dW1 = sum_G dh1 x^T
+// accumulated into `acc`. Writes, for the tile's valid Gaussians, the base-colour
+// and feature gradients, and the direction gradient (active bands only) to st.dd.
+__device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdStage& st, int t, uint64_t valid,
+                                                int degree, float* __restrict__ dbase, float* __restrict__ dfeat,
+                                                int64_t n, int64_t base, float scale, float inv, NeuralGradAcc& acc)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
+    const half8_t x = neural_stage_frag(st.x, t);
+    // Gaussian-major inputs: input 16fb + c of Gaussians 16t + 4g + j
+    half4_t xg[2];
+#pragma unroll
+    for (int fb = 0; fb < 2; ++fb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) xg[fb][j] = st.x[16 * t + 4 * g + j][16 * fb + c];
+    // forward, both orientations
+    float4_t h1n, h2n, on;
+    half4_t a1, a2;
+    neural_tile_fwd(W, x, h1n, a1, h2n, a2, on);
+    const float4_t h1g = mfma32(x, frag8(W.w1a), zero);    // h1[G = 4g+i][n1 = c]
+    const float4_t h2g = mfma16(a1, frag4(W.w2a), zero);   // h2[G = 4g+i][n2 = c]
+    const float4_t og = mfma16(a2, frag4(W.w3a), zero);    // o[G = 4g+i][channel c]
+
+    // output gradients: neuron-major (channel i of Gaussian c, in lanes g = 0)
+    // and Gaussian-major (Gaussian 4g + i, channel c < 3); a culled Gaussian's
+    // staged colour gradient is zero
+    float4_t d3n = zero, d3g = zero;
+    const int Gn = 16 * t + c;
+    const bool own = g == 0 && ((valid >> Gn) & 1);
+#pragma unroll
+    for (int i = 0; i < GS_MLP_OUT; ++i) {
+        const float r = tanhf(on[i]);
+        const bool pos = st.c0[Gn][i] + r + 0.5f > 0.f;
+        const float dcm = pos ? st.dc[Gn][i] : 0.f;
+        d3n[i] = g == 0 ? dcm * scale * (1.f - r * r) : 0.f;
+        if (own) dbase[(int64_t)i * n + base + Gn] = dcm;
+    }
+    const int cn = min(c, 3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int G = 16 * t + 4 * g + i;
+        const float r = tanhf(og[i]);
+        const bool pos = st.c0[G][cn] + r + 0.5f > 0.f;
+        d3g[i] = (c < GS_MLP_OUT && pos) ? st.dc[G][cn] * scale * (1.f - r * r) : 0.f;
+    }
+    half4_t d3n_hi, d3n_lo;
+    split4(d3n, d3n_hi, d3n_lo);
+    const half4_t d3g_h = half4_t{(_Float16)d3g[0], (_Float16)d3g[1], (_Float16)d3g[2], (_Float16)d3g[3]};
+
+    // dH2 = W3^T delta3, masked by relu'(h2)
+    const half4_t w3t = frag4(W.w3t);
+    const float4_t g2n = relu_mask(mfma16(w3t, d3n_lo, mfma16(w3t, d3n_hi, zero)), h2n);
+    const float4_t g2g = relu_mask(mfma16(d3n_lo, w3t, mfma16(d3n_hi, w3t, zero)), h2g);
+    half4_t g2n_hi, g2n_lo;
+    split4(g2n, g2n_hi, g2n_lo);
+    // dH1 = W2^T dH2, masked by relu'(h1)
+    const half4_t w2t = frag4(W.w2t);
+    const float4_t g1n = relu_mask(mfma16(w2t, g2n_lo, mfma16(w2t, g2n_hi, zero)), h1n);
+    const float4_t g1g = relu_mask(mfma16(g2n_lo, w2t, mfma16(g2n_hi, w2t, zero)), h1g);
+    half4_t g1n_hi, g1n_lo;
+    split4(g1n, g1n_hi, g1n_lo);
+    // dX = W1^T dH1: dx[b] holds inputs 16b + 4g + i of Gaussian c
+    float4_t dx[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const half4_t w = frag4(W.w1t[b]);
+        dx[b] = mfma16(w, g1n_lo, mfma16(w, g1n_hi, zero)) * inv;
+    }
+    // direction: this lane's four SH inputs 4g + i (active bands only); the
+    // four lane groups' partial vector-Jacobian products add up to dd
+    const int nb = (degree + 1) * (degree + 1);
+    float dY[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) dY[k] = ((k >> 2) == g && k < nb) ? dx[0][k & 3] : 0.f;
+    float dd[3] = {0.f, 0.f, 0.f};
+    sh_basis16_vjp(st.d[Gn][0], st.d[Gn][1], st.d[Gn][2], dY, dd);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+        dd[j] += __shfl_xor(dd[j], 16);
+        dd[j] += __shfl_xor(dd[j], 32);
+    }
+    // features 2g, 2g + 1: inputs (sin f, cos f) each
+    if ((valid >> Gn) & 1) {
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const float f = st.f[Gn][2 * g + q];
+            const float df = dx[1][2 * q] * cosf(f) - dx[1][2 * q + 1] * sinf(f);
+            dfeat[(int64_t)(2 * g + q) * n + base + Gn] = df;
+        }
+        if (g == 0)
+#pragma unroll
+            for (int j = 0; j < 3; ++j) st.dd[Gn][j] = dd[j];
+    }
+
+    // weight gradients from the Gaussian-major fragments, accumulated in place
+    const half4_t r1g = relu_half4(h1g), r2g = relu_half4(h2g);
+    acc.w3 = mfma16(d3g_h, r2g, acc.w3);                                            // dW3[o][n2]
+    const half4_t h2d = {(_Float16)g2g[0], (_Float16)g2g[1], (_Float16)g2g[2], (_Float16)g2g[3]};
+    acc.w2 = mfma16(h2d, r1g, acc.w2);                                              // dW2[n2][n1]
+    const half4_t h1d = {(_Float16)g1g[0], (_Float16)g1g[1], (_Float16)g1g[2], (_Float16)g1g[3]};
+#pragma unroll
+    for (int fb = 0; fb < 2; ++fb) acc.w1[fb] = mfma16(h1d, xg[fb], acc.w1[fb]);   // dW1[n1][input]
+}
+
+}  // namespace gsr

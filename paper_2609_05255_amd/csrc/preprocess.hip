@@ -8,6 +8,7 @@
 // and they must not depend on which multiply-adds the compiler fuses.
 #include "gs_internal.h"
 #include "mlp.h"
+#include "neural.h"
 #include "sh.h"
 
 #pragma clang fp contract(off)
@@ -133,6 +134,8 @@ struct PreArgs {
     const float* sh;
     const uint16_t* latent;
     const uint16_t* mlp_w;
+    const float* base_color;
+    const uint16_t* features;
     gs_splat* splats;
     uint32_t* tiles_touched;
     uint32_t* depth_key;
@@ -337,6 +340,78 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_latent(PreArgs a)
     }
 }
 
+// The paper's neural appearance (neural.h): geometry per thread; each lane
+// stages its decoder input (SH basis of its direction up to the active degree,
+// sin and cos of its 8 features); the wave decodes its visible Gaussians 16 at
+// a time on the matrix cores; colour max(0, c0 + tanh(MLP(x)) + 0.5), or
+// max(0, c0 + 0.5) while the active degree is 0. Waves loop over 64-Gaussian
+// chunks on their own, the base colour and feature loads issued before the
+// geometry.
+__global__ __launch_bounds__(kBlock) void k_preprocess_neural(PreArgs a)
+{
+    __shared__ NeuralFrags W;
+    __shared__ NeuralInStage XS[kBlock / kWave];
+    __shared__ SplatStage stage[kBlock / kWave];
+    const bool resid = a.sh_degree >= 1;
+    if (resid) neural_load_frags(a.mlp_w, W, false);
+    const int lane = __lane_id(), wave = threadIdx.x >> 6;
+    const int64_t nchunks = div_up((int64_t)a.n, kWave);
+    const int64_t stride = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t chunk = (int64_t)blockIdx.x * (kBlock / kWave) + wave; chunk < nchunks; chunk += stride) {
+        const int64_t base = chunk * kWave;
+        const int i = (int)(base + lane);
+        float c0[3] = {0.f, 0.f, 0.f}, f[GS_NEURAL_FEATURES];
+#pragma unroll
+        for (int j = 0; j < GS_NEURAL_FEATURES; ++j) f[j] = 0.f;
+        if (i < a.n) {
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) c0[ch] = a.base_color[(int64_t)ch * a.n + i];
+            if (resid)
+#pragma unroll
+                for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
+                    f[j] = (float)half_of_bits(a.features[(int64_t)j * a.n + i]);
+        }
+        uint32_t tiles = 0;
+        Geo g;
+        g.visible = false;
+        float d[3] = {0.f, 0.f, 0.f};
+        if (i < a.n) {
+            float mu[3], ls[3], q[4], logit;
+            load_geometry_params(a, i, mu, ls, q, logit);
+            geometry(a.cam, mu, ls, q, logit, g);
+            if (g.visible) {
+                tiles = g.tiles;
+                view_dir(a.cam, mu, d);
+            }
+            a.tiles_touched[i] = tiles;
+            a.depth_key[i] = g.visible ? __float_as_uint(g.depth) : 0xFFFFFFFFu;
+        }
+        float res[3] = {0.f, 0.f, 0.f};
+        if (resid) {
+            neural_stage_inputs(XS[wave].x, g.visible, d, a.sh_degree, f);
+            wave_lds_sync();
+            const uint64_t vis = __ballot(g.visible);
+            for (int t = 0; t < kWave / 16; ++t) {
+                if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
+                float4_t h1, h2, o;
+                half4_t a1, a2;
+                neural_tile_fwd(W, neural_stage_frag(XS[wave].x, t), h1, a1, h2, a2, o);
+                neural_tile_residual(o, t, res);
+            }
+            wave_lds_sync();   // the stage is read before the next chunk overwrites it
+        }
+        float col[3];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) {
+            const float v = c0[ch] + res[ch] + 0.5f;
+            col[ch] = v > 0.f ? v : 0.f;
+        }
+        store_splats_wave(a.splats, a.n, base, stage[wave], g, col);
+        const uint32_t total = wave_sum_u32(tiles);
+        if (lane == 0) a.block_pairs[chunk] = total;
+    }
+}
+
 // Workgroups of the latent preprocess: the number resident at once on 256 CUs
 // (four per CU at the kernel's register budget), each wave looping over chunks.
 constexpr int kLatentBlocks = 1024;
@@ -355,6 +430,8 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     a.sh = app.sh;
     a.latent = app.latent;
     a.mlp_w = app.mlp_w;
+    a.base_color = app.base_color;
+    a.features = app.features;
     a.splats = out.splats;
     a.tiles_touched = out.tiles_touched;
     a.depth_key = out.depth_key;
@@ -368,6 +445,8 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
         default: hipLaunchKernelGGL(k_preprocess_sh3<3>, dim3(blocks), dim3(kBlock), 0, s, a); break;
         }
     }
+    else if (app.kind == GS_APP_NEURAL)
+        hipLaunchKernelGGL(k_preprocess_neural, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
     else
         hipLaunchKernelGGL(k_preprocess_latent, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
     return hipGetLastError();

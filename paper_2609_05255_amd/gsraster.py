@@ -20,7 +20,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libgsraster.so")
 
 GS_OK, GS_ERR_INVALID_ARG, GS_ERR_CAPACITY, GS_ERR_DEVICE, GS_ERR_UNSUPPORTED = range(5)
-GS_APP_SH3, GS_APP_LATENT_MLP = 0, 1
+GS_APP_SH3, GS_APP_LATENT_MLP, GS_APP_NEURAL = 0, 1, 2
+NEURAL_FEATURES = 8
+NEURAL_WEIGHTS = 816
 KERNEL_NAMES = ["preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
                 "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam"]
 ADAM_MAX_TENSORS = 8
@@ -48,7 +50,7 @@ class Gaussians(C.Structure):
 
 class Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p), ("latent", C.c_void_p),
-                ("mlp_w", C.c_void_p)]
+                ("mlp_w", C.c_void_p), ("base_color", C.c_void_p), ("features", C.c_void_p)]
 
 
 class Preprocessed(C.Structure):
@@ -59,7 +61,8 @@ class Preprocessed(C.Structure):
 class Grads(C.Structure):
     _fields_ = [("dmeans", C.c_void_p), ("dlog_scales", C.c_void_p), ("dquats", C.c_void_p),
                 ("dopacity_logits", C.c_void_p), ("dsh", C.c_void_p), ("dlatent", C.c_void_p),
-                ("dmlp_w", C.c_void_p), ("dmean2d", C.c_void_p)]
+                ("dmlp_w", C.c_void_p), ("dmean2d", C.c_void_p), ("dbase_color", C.c_void_p),
+                ("dfeatures", C.c_void_p)]
 
 
 class AdamTensor(C.Structure):
@@ -150,13 +153,19 @@ class SceneTensors:
         self.sh = f32(scene.sh) if getattr(scene, "sh", None) is not None else None
         self.latent = h16(scene.latent) if getattr(scene, "latent", None) is not None else None
         self.mlp_w = h16(scene.mlp_w) if getattr(scene, "mlp_w", None) is not None else None
+        self.base_color = f32(scene.base_color) if getattr(scene, "base_color", None) is not None else None
+        self.features = h16(scene.features) if getattr(scene, "features", None) is not None else None
+        self.neural_w = h16(scene.neural_w) if getattr(scene, "neural_w", None) is not None else None
 
     def gaussians(self) -> Gaussians:
         return Gaussians(self.n, _ptr(self.means), _ptr(self.log_scales), _ptr(self.quats),
                          _ptr(self.opacity_logits))
 
     def appearance(self, kind: int, sh_degree: int = 3) -> Appearance:
-        return Appearance(kind, sh_degree, _ptr(self.sh), _ptr(self.latent), _ptr(self.mlp_w))
+        if kind == GS_APP_NEURAL:
+            return Appearance(kind, sh_degree, None, None, _ptr(self.neural_w), _ptr(self.base_color),
+                              _ptr(self.features))
+        return Appearance(kind, sh_degree, _ptr(self.sh), _ptr(self.latent), _ptr(self.mlp_w), None, None)
 
 
 def gs_workspace_size(n: int, width: int, height: int, capacity: int, kind: int) -> int:
@@ -257,13 +266,16 @@ class Frame:
         self.dopacity_logits = torch.empty(nn, device=d)
         self.dsh = torch.empty(48, nn, device=d) if kind == GS_APP_SH3 else None
         self.dlatent = torch.empty(14, nn, device=d) if kind == GS_APP_LATENT_MLP else None
-        self.dmlp_w = torch.empty(MLP_WEIGHTS, device=d) if kind == GS_APP_LATENT_MLP else None
+        self.dmlp_w = (torch.empty(MLP_WEIGHTS, device=d) if kind == GS_APP_LATENT_MLP else
+                       torch.empty(NEURAL_WEIGHTS, device=d) if kind == GS_APP_NEURAL else None)
         self.dmean2d = torch.empty(2, nn, device=d) if want_dmean2d else None
+        self.dbase_color = torch.empty(3, nn, device=d) if kind == GS_APP_NEURAL else None
+        self.dfeatures = torch.empty(NEURAL_FEATURES, nn, device=d) if kind == GS_APP_NEURAL else None
         self.pre = Preprocessed(_ptr(self.splats), _ptr(self.tiles_touched), _ptr(self.depth_key),
                                 _ptr(self.num_pairs))
         self.grads = Grads(_ptr(self.dmeans), _ptr(self.dlog_scales), _ptr(self.dquats),
                            _ptr(self.dopacity_logits), _ptr(self.dsh), _ptr(self.dlatent), _ptr(self.dmlp_w),
-                           _ptr(self.dmean2d))
+                           _ptr(self.dmean2d), _ptr(self.dbase_color), _ptr(self.dfeatures))
         self.last_pairs = 0
 
     def forward(self, cam: Camera, scene: SceneTensors, sh_degree: int = 3, stream=None) -> int:

@@ -11,7 +11,9 @@ Learning rates per parameter channel (the row of the planar layout):
     0.000125;
   * latent + MLP: latents 0.008 (the paper's rate for the neural features) and
     decoder weights 0.003 with a second-moment decay of 0.99 (they receive a
-    gradient from every visible Gaussian in every iteration).
+    gradient from every visible Gaussian in every iteration);
+  * neural (the paper's model): base colour 0.00025, features 0.008, decoder
+    weights 0.003 with a second-moment decay of 0.99.
 The latents and the decoder weights have fp32 master copies here; each step
 writes their binary16 copies into the scene buffers the passes read, as the
 paper does for its decoder weights.
@@ -25,6 +27,8 @@ from . import gsraster as gs
 LR_MEANS, LR_SCALES, LR_QUATS, LR_OPACITY = 1.6e-4, 5e-3, 1e-3, 0.05
 LR_SH_DC, LR_SH_REST = 0.0025, 0.000125
 LR_LATENT, LR_MLP, BETA2_MLP = 0.008, 0.003, 0.99
+LR_BASE_COLOR, LR_FEATURES = 0.00025, 0.008
+NEURAL_FEATURES = 8
 LATENT_DIM = 14
 
 
@@ -48,6 +52,12 @@ class FusedAdam:
         add(scene.opacity_logits, frame.dopacity_logits, [LR_OPACITY])
         if kind == gs.GS_APP_SH3:
             add(scene.sh, frame.dsh, [LR_SH_DC] * 3 + [LR_SH_REST] * 45)
+        elif kind == gs.GS_APP_NEURAL:
+            self.features32 = scene.features.view(torch.float16).float().contiguous()
+            self.mlp32 = scene.neural_w.view(torch.float16).float().contiguous()
+            add(scene.base_color, frame.dbase_color, [LR_BASE_COLOR] * 3)
+            add(self.features32, frame.dfeatures, [LR_FEATURES] * NEURAL_FEATURES, half=scene.features)
+            add(self.mlp32, frame.dmlp_w, [LR_MLP], beta2=BETA2_MLP, half=scene.neural_w)
         else:
             self.latent32 = scene.latent.view(torch.float16).float().contiguous()
             self.mlp32 = scene.mlp_w.view(torch.float16).float().contiguous()

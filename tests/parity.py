@@ -26,7 +26,7 @@ def say(msg: str):
 
 
 def kind_id(kind: str) -> int:
-    return gs.GS_APP_SH3 if kind == "sh3" else gs.GS_APP_LATENT_MLP
+    return {"sh3": gs.GS_APP_SH3, "latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL}[kind]
 
 
 def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None, extras=True):
@@ -72,15 +72,22 @@ def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None, 
                         if getattr(fr, k) is not None}
         if kind == "sh3":
             out["grads"]["dsh"] = fr.dsh.cpu().numpy().astype(np.float64)[:, : scene.n]
+        elif kind == "neural":
+            out["grads"]["dbase_color"] = fr.dbase_color.cpu().numpy().astype(np.float64)[:, : scene.n]
+            out["grads"]["dfeatures"] = fr.dfeatures.cpu().numpy().astype(np.float64)[:, : scene.n]
+            out["grads"]["dmlp_w"] = fr.dmlp_w.cpu().numpy().astype(np.float64)
         else:
             out["grads"]["dlatent"] = fr.dlatent.cpu().numpy().astype(np.float64)[:, : scene.n]
             out["grads"]["dmlp_w"] = fr.dmlp_w.cpu().numpy().astype(np.float64)
     return out
 
 
-def compare_preprocess(gpu, ref, color_atol=2e-6):
+def compare_preprocess(gpu, ref, color_atol=2e-6, flip=None):
     """Culling, tile counts, rectangles and depth keys bit-exact; projected
-    geometry bit-exact (same correctly rounded fp32 sequence); colours close."""
+    geometry bit-exact (same correctly rounded fp32 sequence); colours close.
+    With ``flip = (loose, frac)`` a colour may miss ``color_atol`` by a binary16
+    rounding flip: all within ``loose``, at most ``frac`` of them beyond
+    ``color_atol``."""
     assert np.array_equal(gpu["tiles"].astype(np.int64), ref["tiles"].astype(np.int64))
     vis = ref["tiles"] > 0
     ref_key = np.where(vis, ref["depth"].astype(np.float32).view(np.uint32), np.uint32(0xFFFFFFFF))
@@ -92,7 +99,13 @@ def compare_preprocess(gpu, ref, color_atol=2e-6):
     for k in ("mean2d", "conic"):
         assert np.array_equal(s[k][:, vis].astype(np.float32), ref[k][:, vis].astype(np.float32)), k
     assert np.array_equal(s["opacity"][vis], ref["opacity"][vis].astype(np.float32))
-    assert np.abs(s["color"][:, vis] - ref["color"][:, vis]).max() <= color_atol
+    err = np.abs(s["color"][:, vis] - ref["color"][:, vis]).max(axis=0)
+    if flip is None:
+        assert err.max() <= color_atol, err.max()
+    else:
+        beyond = float((err > color_atol).mean())
+        say("  colours: max abs %.2e, %.3f%% beyond %.0e" % (err.max(), 100 * beyond, color_atol))
+        assert err.max() <= flip[0] and beyond <= flip[1], (err.max(), beyond)
     check_skip_fields(s, ref, vis)
 
 
@@ -159,6 +172,18 @@ MLP_ATOL = 2e-3                      # decoder colours/images vs the exact (fp64
 # vs the oracle whose decoder rounds inputs and activations to binary16 like the
 # GPU's matrix-core operands: only fp32 accumulation order and the sigmoid differ
 MLP_HALF_ATOL = 2e-4
+# The neural decoder's encodings (SH basis, sin, cos) and hidden sums are fp32
+# on the GPU and fp64 in the oracle before both round to binary16, so about one
+# value in 2^11 rounds to the neighbouring binary16 number on one side only.
+# A flipped hidden unit (|h| < 4, spacing <= 2^-9) moves an output o by up to
+# max|W3| 2^-9 = 0.56 * 2^-9 ~ 1.1e-3 (Glorot bound sqrt(6/19)), and the colour
+# c0 + tanh(o) + 0.5 by as much (tanh' <= 1; the latent's sigmoid' <= 1/4 keeps
+# its flips under MLP_HALF_ATOL). So every neural colour and pixel is within
+# NEURAL_FLIP_ATOL and at most NEURAL_FLIP_FRAC of the Gaussians miss
+# MLP_HALF_ATOL.
+NEURAL_FLIP_ATOL = 2e-3
+NEURAL_FLIP_FRAC = 0.01
+NEURAL_FLIP = (NEURAL_FLIP_ATOL, NEURAL_FLIP_FRAC)
 
 
 def compare_image(gpu, ref_img, ref_T, ref_nc, margin, atol=IMG_ATOL, rtol=IMG_RTOL):

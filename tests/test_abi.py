@@ -95,6 +95,10 @@ def test_preprocess_rejects_bad_arguments(gs):
     assert call(app=gs.Appearance(gs.GS_APP_SH3, 3, None, None, None)) == gs.GS_ERR_INVALID_ARG
     assert call(app=gs.Appearance(gs.GS_APP_LATENT_MLP, 0, None, FAKE, None)) == gs.GS_ERR_INVALID_ARG
     assert call(app=gs.Appearance(9, 0, FAKE, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
+    # neural: base colour always, features and weights once the residual is on, degree 0..3
+    assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 3, None, None, FAKE, None, FAKE)) == gs.GS_ERR_INVALID_ARG
+    assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 2, None, None, FAKE, FAKE, None)) == gs.GS_ERR_INVALID_ARG
+    assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 4, None, None, FAKE, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
     assert call(pre=gs.Preprocessed(FAKE, FAKE, FAKE, None)) == gs.GS_ERR_INVALID_ARG
     assert call(ws=FAKE + 4) == gs.GS_ERR_INVALID_ARG              # misaligned workspace
     assert call(wsb=16) == gs.GS_ERR_CAPACITY

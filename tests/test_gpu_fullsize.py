@@ -20,7 +20,7 @@ import pytest
 
 from paper_2609_05255_amd import inputs
 from oracle import oracle as orc
-from parity import (IMG_ATOL, IMG_RTOL, MARGIN, MLP_HALF_ATOL, affected_gaussians, check_list_properties,
+from parity import (IMG_ATOL, IMG_RTOL, MARGIN, MLP_HALF_ATOL, NEURAL_FLIP, affected_gaussians, check_list_properties,
                     compare_preprocess, grad_errors, run_gpu, say, tile_of_ranges)
 
 pytestmark = pytest.mark.gpu
@@ -78,9 +78,9 @@ def tile_pixels(sample, tiles_x, W, H):
 
 
 @pytest.mark.parametrize("config,kind,cam_index", [("paper_sh3", "sh3", 3), ("paper_latent", "latent", 9),
-                                                    ("stress", "sh3", 5)])
+                                                    ("paper_neural", "neural", 7), ("stress", "sh3", 5)])
 def test_full_size_sampled(config, kind, cam_index):
-    latent = kind == "latent"
+    latent = kind in ("latent", "neural")
     sc = inputs.make_scene(config, appearance=(kind,))
     cam = inputs.make_cameras(config)[cam_index]
     W, H = cam.width, cam.height
@@ -100,7 +100,8 @@ def test_full_size_sampled(config, kind, cam_index):
     say("  GPU done")
 
     # preprocess of every Gaussian and the whole list
-    compare_preprocess(gpu, pre, color_atol=MLP_HALF_ATOL if latent else 2e-6)
+    flip = NEURAL_FLIP if kind == "neural" else None
+    compare_preprocess(gpu, pre, color_atol=MLP_HALF_ATOL if latent else 2e-6, flip=flip)
     assert gpu["P"] == P_ref
     key = np.where(pre["tiles"] > 0, pre["depth"].astype(np.float32).view(np.uint32), np.uint32(0xFFFFFFFF))
     tile_of = tile_of_ranges(gpu["ranges"], gpu["P"])
@@ -127,7 +128,7 @@ def test_full_size_sampled(config, kind, cam_index):
     ranges[unsampled] = 0
     img, fT, n_contrib, margin = orc.render_fwd(cam, sub, ranges, values)
     ok = in_sample & (margin > MARGIN)
-    atol, rtol = (MLP_HALF_ATOL, 0.0) if latent else (IMG_ATOL, IMG_RTOL)
+    atol, rtol = ((flip[0] if flip else MLP_HALF_ATOL), 0.0) if latent else (IMG_ATOL, IMG_RTOL)
     err = np.abs(gpu["image"] - img)
     bad = (err > atol + rtol * np.abs(img)) & ok[None]
     assert not bad.any(), (int(bad.sum()), float(err[:, ok].max()))
@@ -140,7 +141,8 @@ def test_full_size_sampled(config, kind, cam_index):
     ref = orc.render_bwd(cam, sc, sub, ranges, values, dL, kind=kind, half_act=latent)
     margin_s = np.where(in_sample, margin, np.inf)
     excl = affected_gaussians(ranges, values, n_contrib, gpu["n_contrib"], margin_s, W)
-    names = ["dmeans", "dlog_scales", "dquats", "dopacity_logits"] + (["dlatent", "dmlp_w"] if latent else ["dsh"])
+    names = ["dmeans", "dlog_scales", "dquats", "dopacity_logits"] + {
+        "sh3": ["dsh"], "latent": ["dlatent", "dmlp_w"], "neural": ["dbase_color", "dfeatures", "dmlp_w"]}[kind]
     st = grad_errors({k: gpu["grads"][k] for k in names}, {k: ref[k] for k in names}, excl)
     say("  grad errors (rel L2, max elem): " + ", ".join("%s %.2e %.2e" % (k, a, b) for k, (a, b) in st.items()))
     for k, (rel, _) in st.items():

@@ -16,7 +16,7 @@ import torch
 
 from oracle import oracle as orc
 from paper_2609_05255_amd import gsraster as gs
-from parity import (MLP_ATOL, MLP_HALF_ATOL, affected_gaussians, compare_image, compare_lists, compare_preprocess,
+from parity import (MLP_ATOL, MLP_HALF_ATOL, NEURAL_FLIP, affected_gaussians, compare_image, compare_lists, compare_preprocess,
                     grad_errors, oracle_all, run_gpu, say, tiny_camera)
 
 pytestmark = pytest.mark.gpu
@@ -28,15 +28,16 @@ def check_all(scene, cam, kind="sh3", sh_degree=3, label="", grads=True, capacit
     g = inputs.make_upstream_grad(cam.width, cam.height, 0) if grads else None
     say("case %s: n=%d %dx%d %s degree %d" % (label, scene.n, cam.width, cam.height, kind, sh_degree))
     gpu = run_gpu(scene, cam, kind, sh_degree, g, capacity=capacity)
-    latent = kind == "latent"
+    latent = kind in ("latent", "neural")
     # the decoder's operands are binary16: compare with the oracle that rounds them alike
     ref = oracle_all(scene, cam, kind, sh_degree, g, half_act=latent)
-    compare_preprocess(gpu, ref["pre"], color_atol=MLP_HALF_ATOL if latent else 2e-6)
+    flip = NEURAL_FLIP if kind == "neural" else None
+    compare_preprocess(gpu, ref["pre"], color_atol=MLP_HALF_ATOL if latent else 2e-6, flip=flip)
     compare_lists(gpu, ref["values"], ref["tile_of"], ref["ranges"])
     if latent:
         flagged = compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"],
-                                atol=MLP_HALF_ATOL, rtol=0.0)
-        exact = orc.render(cam, scene, kind=kind, mode="f32")
+                                atol=flip[0] if flip else MLP_HALF_ATOL, rtol=0.0)
+        exact = orc.render(cam, scene, kind=kind, sh_degree=sh_degree, mode="f32")
         err = np.abs(gpu["image"] - exact["image"])[:, exact["margin"] > 1e-5]
         say("  latent image vs the exact decoder: max abs %.2e" % (err.max() if err.size else 0.0))
         assert err.size == 0 or err.max() <= MLP_ATOL
@@ -146,6 +147,23 @@ def test_ragged_latent_with_background():
 def test_medium_scene_latent():
     sc = inputs.make_scene("medium", appearance=("latent",))
     check_all(sc, inputs.make_cameras("medium")[2], kind="latent", label="medium latent cam 2")
+
+
+@pytest.mark.parametrize("degree", [0, 1, 2, 3])
+def test_tiny_scene_neural(degree):
+    # the paper's neural appearance; degree 0 has the residual off
+    sc = inputs.make_scene("tiny", appearance=("neural",))
+    check_all(sc, tiny_camera(), kind="neural", sh_degree=degree, label="tiny-neural")
+
+
+def test_ragged_neural_with_background():
+    sc = inputs.make_scene("tiny", appearance=("neural",))
+    check_all(sc, tiny_camera(50, 37, bg=(0.1, 0.5, 0.9)), kind="neural", label="ragged-neural")
+
+
+def test_medium_scene_neural():
+    sc = inputs.make_scene("medium", appearance=("neural",))
+    check_all(sc, inputs.make_cameras("medium")[2], kind="neural", label="medium-neural")
 
 
 def test_binning_one_tile_and_huge_gaussians():

@@ -80,13 +80,23 @@ def test_selector_networks(orc, k, what):
     assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12), what
 
 
-def test_degree_two_input_is_active_at_degree_two(orc):
-    # Y4 = sqrt(15/(4 pi)) x y (degree 2, m = -2), silent at degree 1 (above)
+@pytest.mark.parametrize("k,degree", [(4, 2), (9, 3), (9, 2)])
+def test_higher_band_inputs_follow_the_active_degree(orc, k, degree):
+    # Y4 = sqrt(15/(4 pi)) x y (degree 2, m = -2; silent at degree 1, above);
+    # Y9 = -sqrt(35/(32 pi)) y (3 x^2 - y^2) (degree 3, m = -3, Condon-Shortley
+    # sign as band 1's -y), silent below degree 3
     sc = scene()
-    sc.neural_w = selector(4)
+    sc.neural_w = selector(k)
     cam = inputs.make_cameras("tiny")[0]
     d = directions(sc, cam)
-    x = math.sqrt(15.0 / (4.0 * math.pi)) * d[0] * d[1]
-    col, vis = colours(orc, sc, cam, 2)
+    if k == 4:
+        x = math.sqrt(15.0 / (4.0 * math.pi)) * d[0] * d[1]
+    else:
+        x = -math.sqrt(35.0 / (32.0 * math.pi)) * d[1] * (3.0 * d[0] ** 2 - d[1] ** 2)
+    if degree < (2 if k == 4 else 3):
+        x = np.zeros(sc.n)
+    else:
+        assert (x > 0.01).sum() >= 5   # a non-trivial check: enough positive inputs
+    col, vis = colours(orc, sc, cam, degree)
     expect = np.maximum(0.0, base(sc) + np.tanh(np.maximum(0.0, x))[None] + 0.5)
     assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12)

@@ -364,32 +364,54 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
             for (int ch = 0; ch < 3; ++ch) dc[ch] = ap[6 + ch];
             for (int ch = 0; ch < 3; ++ch) c0[ch] = a.base_color[ch * n + i];
         }
+        float dd[3] = {0.f, 0.f, 0.f};
         if (resid) {
             float f[GS_NEURAL_FEATURES];
             for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
                 f[j] = valid ? (float)half_of_bits(a.features[j * n + i]) : 0.f;
             neural_stage_inputs(st.x, valid, d, a.sh_degree, f);
-            for (int ch = 0; ch < 3; ++ch) {
-                st.dc[lane][ch] = dc[ch];
-                st.c0[lane][ch] = c0[ch];
-                st.d[lane][ch] = d[ch];
-                st.dd[lane][ch] = 0.f;
-            }
-            st.dc[lane][3] = 0.f;   // padding column: the Gaussian-major reads take channel 3 there
-            st.c0[lane][3] = 0.f;
-            for (int j = 0; j < GS_NEURAL_FEATURES; ++j) st.f[lane][j] = f[j];
-            // the chunk's gradient scale (a power of two, see neural_chunk_exponent)
-            const float m = wave_max(fmaxf(fmaxf(fabsf(dc[0]), fabsf(dc[1])), fabsf(dc[2])));
-            neural_grad_rescale(acc, neural_chunk_exponent(m, acc.se));
-            const float scale = ldexpf(1.f, acc.se), inv = ldexpf(1.f, -acc.se);
             wave_lds_sync();
             const uint64_t vis = __ballot(valid);
-            const int64_t base = chunk * kBlock + (threadIdx.x & ~(kWave - 1));
+            // first pass: each lane's output pre-activations, then its residual
+            // tanh(o), base-colour gradient and delta3 = dL/dc [c > 0] (1 - res^2)
+            float o[3] = {0.f, 0.f, 0.f};
             for (int t = 0; t < kWave / 16; ++t) {
                 if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
-                neural_tile_bwd(W, st, t, vis, a.sh_degree, a.dbase_color, a.dfeatures, n, base, scale, inv, acc);
+                neural_tile_gather(neural_tile_out(W, neural_stage_frag(st.x, t)), t, o);
+            }
+            float m = 0.f;
+            for (int ch = 0; ch < 3; ++ch) {
+                const float r = tanhf(o[ch]);
+                const float dcm = c0[ch] + r + 0.5f > 0.f ? dc[ch] : 0.f;   // dc = 0 when !valid
+                if (valid) a.dbase_color[ch * n + i] = dcm;
+                const float d3 = dcm * (1.f - r * r);
+                st.d3[lane][ch] = d3;
+                m = fmaxf(m, fabsf(d3));
+            }
+            st.d3[lane][3] = 0.f;
+            // the chunk's gradient scale (a power of two, see neural_chunk_exponent)
+            neural_grad_rescale(acc, neural_chunk_exponent(wave_max(m), acc.se));
+            const float scale = ldexpf(1.f, acc.se), inv = ldexpf(1.f, -acc.se);
+            wave_lds_sync();
+            for (int t = 0; t < kWave / 16; ++t) {
+                if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
+                neural_tile_bwd(W, st, t, scale, inv, acc);
             }
             wave_lds_sync();
+            if (valid) {
+                // direction: the active bands' input gradients through the SH basis
+                const int nb = (a.sh_degree + 1) * (a.sh_degree + 1);
+                const float* row = neural_dir_grad_row(st, lane);
+                float dY[16];
+                for (int k = 0; k < 16; ++k) dY[k] = k < nb ? row[k] : 0.f;
+                sh_basis16_vjp(d[0], d[1], d[2], dY, dd);
+                // features: d(sin f)/df = cos f, d(cos f)/df = -sin f
+                for (int j = 0; j < GS_NEURAL_FEATURES; ++j) {
+                    float sj, cj;
+                    sincosf(f[j], &sj, &cj);
+                    a.dfeatures[j * n + i] = st.dxf[lane][2 * j] * cj - st.dxf[lane][2 * j + 1] * sj;
+                }
+            }
         } else if (valid) {
             // no residual: c = max(0, c0 + 0.5)
             for (int ch = 0; ch < 3; ++ch) a.dbase_color[ch * n + i] = c0[ch] + 0.5f > 0.f ? dc[ch] : 0.f;
@@ -406,7 +428,7 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
             geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
             if (resid) {
                 // the binary16 rounding of the SH inputs passes the gradient; d = v / |v|
-                const float dd0 = st.dd[lane][0], dd1 = st.dd[lane][1], dd2 = st.dd[lane][2];
+                const float dd0 = dd[0], dd1 = dd[1], dd2 = dd[2];
                 const float dot = d[0] * dd0 + d[1] * dd1 + d[2] * dd2;
                 const float il = 1.f / len;
                 gg.dmu[0] += (dd0 - d[0] * dot) * il;
@@ -418,7 +440,7 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
             a.dlogits[i] = gg.dlogit;
             if (a.dmean2d) { a.dmean2d[i] = g9[0]; a.dmean2d[n + i] = g9[1]; }
         }
-        if (resid) wave_lds_sync();   // st.dd is read before the next chunk restages
+        if (resid) wave_lds_sync();   // the stage is read before the next chunk restages
     }
     // workgroup sum of the four waves' weight gradients, in wave order, in the
     // LDS of the (no longer needed) stage

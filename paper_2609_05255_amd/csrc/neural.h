@@ -56,20 +56,26 @@ __device__ __forceinline__ void neural_load_frags(const uint16_t* __restrict__ w
 }
 
 // Per-wave staging: each Gaussian's 32 binary16 inputs (rows of kXPitch
-// halves), and for the backward its colour gradient, base colour, features
-// (fp32) and view direction, and the direction gradient the tiles produce.
+// halves). The backward also stages each Gaussian's output gradient delta3
+// (channel 3 zero) and receives from the tiles the gradients of its 16 feature
+// inputs and, in its input row once the tile has read it, the gradients of its
+// 16 direction inputs as fp32.
 struct NeuralInStage {
     alignas(16) _Float16 x[kWave][kXPitch];
 };
 
 struct NeuralBwdStage {
     alignas(16) _Float16 x[kWave][kXPitch];
-    float dc[kWave][4];
-    float c0[kWave][4];
-    float f[kWave][8];
-    float d[kWave][4];
-    float dd[kWave][4];
+    float d3[kWave][4];
+    float dxf[kWave][16];
 };
+static_assert(kXPitch * sizeof(_Float16) >= 16 * sizeof(float), "a row holds 16 fp32 direction gradients");
+
+// The direction-input gradients that tile backward left in row r.
+__device__ __forceinline__ const float* neural_dir_grad_row(const NeuralBwdStage& st, int r)
+{
+    return reinterpret_cast<const float*>(&st.x[r][0]);
+}
 
 // The calling lane's decoder input: SH basis values of d for bands <= degree
 // (zero above), then (sin f_j, cos f_j) for the 8 features, rounded to binary16
@@ -90,8 +96,10 @@ __device__ __forceinline__ void neural_stage_inputs(_Float16 (*x)[kXPitch], bool
 #pragma unroll
         for (int j = 0; j < GS_NEURAL_FEATURES; ++j) {
             const int e = 16 + 2 * j;
-            v[e >> 2][e & 3] = (_Float16)sinf(f[j]);
-            v[(e + 1) >> 2][(e + 1) & 3] = (_Float16)cosf(f[j]);
+            float sj, cj;
+            sincosf(f[j], &sj, &cj);
+            v[e >> 2][e & 3] = (_Float16)sj;
+            v[(e + 1) >> 2][(e + 1) & 3] = (_Float16)cj;
         }
     }
 #pragma unroll
@@ -121,17 +129,26 @@ __device__ __forceinline__ void neural_tile_fwd(const NeuralFrags& W, const half
     o = mfma16(frag4(W.w3a), a2, zero);
 }
 
-// Hands the residuals tanh(o) of tile t to the lanes that own its Gaussians
-// (lane 16t + c takes Gaussian c's three channels from lane c).
-__device__ __forceinline__ void neural_tile_residual(const float4_t& o, int t, float res[3])
+// Hands the output pre-activations o of tile t to the lanes that own its
+// Gaussians (lane 16t + c takes Gaussian c's three channels from lane c).
+__device__ __forceinline__ void neural_tile_gather(const float4_t& o, int t, float own[3])
 {
     const int lane = __lane_id();
     const int src = lane & 15;
 #pragma unroll
     for (int ch = 0; ch < 3; ++ch) {
-        const float v = __shfl(tanhf(o[ch]), src);
-        if ((lane >> 4) == t) res[ch] = v;
+        const float v = __shfl(o[ch], src);
+        if ((lane >> 4) == t) own[ch] = v;
     }
+}
+
+// Output pre-activations of tile t alone (the backward's first pass).
+__device__ __forceinline__ float4_t neural_tile_out(const NeuralFrags& W, const half8_t& x)
+{
+    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
+    const half4_t a1 = relu_half4(mfma32(frag8(W.w1a), x, zero));
+    const half4_t a2 = relu_half4(mfma16(frag4(W.w2a), a1, zero));
+    return mfma16(frag4(W.w3a), a2, zero);
 }
 
 // Running sums of the weight gradients (Gaussian-major products, fp32, in
@@ -172,17 +189,17 @@ __device__ __forceinline__ int neural_chunk_exponent(float m, int prev)
     return min(10 - ex, 100);
 }
 
-// Backward of tile t (Gaussians base + 16t .. base + 16t + 15 of the wave)
-// from the staged inputs, colour gradients and base colours, with the chunk's
-// gradient scale 2^se (acc.se): delta3 = dL/dc [c0 + res + 0.5 > 0] (1 - res^2)
-// enters the matrix cores scaled; dH2, dH1 and dX are chained neuron-major
-// (binary16 hi + lo operands); the Gaussian-major copies give
+// Backward of tile t (Gaussians 16t .. 16t + 15 of the wave) from the staged
+// inputs and output gradients delta3 = dL/dc [c0 + res + 0.5 > 0] (1 - res^2),
+// with the chunk's gradient scale 2^se (acc.se): delta3 enters the matrix
+// cores scaled; dH2, dH1 and dX are chained neuron-major (binary16 hi + lo
+// operands); the Gaussian-major copies give
 //   dW3 = sum_G delta3 h2^T, dW2 = sum_G dh2 h1^T, dW1 = sum_G dh1 x^T
-// accumulated into `acc`. Writes, for the tile's valid Gaussians, the base-colour
-// and feature gradients, and the direction gradient (active bands only) to st.dd.
-__device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdStage& st, int t, uint64_t valid,
-                                                int degree, float* __restrict__ dbase, float* __restrict__ dfeat,
-                                                int64_t n, int64_t base, float scale, float inv, NeuralGradAcc& acc)
+// accumulated into `acc`. Leaves the gradients of the 16 feature inputs in
+// st.dxf and, once the tile's reads of its input rows are issued, those of the
+// 16 direction inputs in the same rows (fp32, every band; the caller masks).
+__device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdStage& st, int t, float scale,
+                                                float inv, NeuralGradAcc& acc)
 {
     const int l = __lane_id(), g = l >> 4, c = l & 15;
     const float4_t zero = {0.f, 0.f, 0.f, 0.f};
@@ -193,36 +210,23 @@ __device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdS
     for (int fb = 0; fb < 2; ++fb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) xg[fb][j] = st.x[16 * t + 4 * g + j][16 * fb + c];
-    // forward, both orientations
-    float4_t h1n, h2n, on;
-    half4_t a1, a2;
-    neural_tile_fwd(W, x, h1n, a1, h2n, a2, on);
+    // forward, both orientations (the output layer is not needed again)
+    const float4_t h1n = mfma32(frag8(W.w1a), x, zero);
+    const half4_t a1 = relu_half4(h1n);
+    const float4_t h2n = mfma16(frag4(W.w2a), a1, zero);
     const float4_t h1g = mfma32(x, frag8(W.w1a), zero);    // h1[G = 4g+i][n1 = c]
     const float4_t h2g = mfma16(a1, frag4(W.w2a), zero);   // h2[G = 4g+i][n2 = c]
-    const float4_t og = mfma16(a2, frag4(W.w3a), zero);    // o[G = 4g+i][channel c]
 
     // output gradients: neuron-major (channel i of Gaussian c, in lanes g = 0)
-    // and Gaussian-major (Gaussian 4g + i, channel c < 3); a culled Gaussian's
-    // staged colour gradient is zero
-    float4_t d3n = zero, d3g = zero;
+    // and Gaussian-major (Gaussian 4g + i, channel c < 3; column 3 is zero)
+    float4_t d3n = zero, d3g;
     const int Gn = 16 * t + c;
-    const bool own = g == 0 && ((valid >> Gn) & 1);
+    if (g == 0)
 #pragma unroll
-    for (int i = 0; i < GS_MLP_OUT; ++i) {
-        const float r = tanhf(on[i]);
-        const bool pos = st.c0[Gn][i] + r + 0.5f > 0.f;
-        const float dcm = pos ? st.dc[Gn][i] : 0.f;
-        d3n[i] = g == 0 ? dcm * scale * (1.f - r * r) : 0.f;
-        if (own) dbase[(int64_t)i * n + base + Gn] = dcm;
-    }
+        for (int i = 0; i < GS_MLP_OUT; ++i) d3n[i] = st.d3[Gn][i] * scale;
     const int cn = min(c, 3);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int G = 16 * t + 4 * g + i;
-        const float r = tanhf(og[i]);
-        const bool pos = st.c0[G][cn] + r + 0.5f > 0.f;
-        d3g[i] = (c < GS_MLP_OUT && pos) ? st.dc[G][cn] * scale * (1.f - r * r) : 0.f;
-    }
+    for (int i = 0; i < 4; ++i) d3g[i] = st.d3[16 * t + 4 * g + i][cn] * scale;
     half4_t d3n_hi, d3n_lo;
     split4(d3n, d3n_hi, d3n_lo);
     const half4_t d3g_h = half4_t{(_Float16)d3g[0], (_Float16)d3g[1], (_Float16)d3g[2], (_Float16)d3g[3]};
@@ -246,30 +250,14 @@ __device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdS
         const half4_t w = frag4(W.w1t[b]);
         dx[b] = mfma16(w, g1n_lo, mfma16(w, g1n_hi, zero)) * inv;
     }
-    // direction: this lane's four SH inputs 4g + i (active bands only); the
-    // four lane groups' partial vector-Jacobian products add up to dd
-    const int nb = (degree + 1) * (degree + 1);
-    float dY[16];
+    // the tile's input rows have been read: they now take the direction-input
+    // gradients
+    wave_lds_sync();
+    float* row = reinterpret_cast<float*>(&st.x[Gn][0]);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) dY[k] = ((k >> 2) == g && k < nb) ? dx[0][k & 3] : 0.f;
-    float dd[3] = {0.f, 0.f, 0.f};
-    sh_basis16_vjp(st.d[Gn][0], st.d[Gn][1], st.d[Gn][2], dY, dd);
-#pragma unroll
-    for (int j = 0; j < 3; ++j) {
-        dd[j] += __shfl_xor(dd[j], 16);
-        dd[j] += __shfl_xor(dd[j], 32);
-    }
-    // features 2g, 2g + 1: inputs (sin f, cos f) each
-    if ((valid >> Gn) & 1) {
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            const float f = st.f[Gn][2 * g + q];
-            const float df = dx[1][2 * q] * cosf(f) - dx[1][2 * q + 1] * sinf(f);
-            dfeat[(int64_t)(2 * g + q) * n + base + Gn] = df;
-        }
-        if (g == 0)
-#pragma unroll
-            for (int j = 0; j < 3; ++j) st.dd[Gn][j] = dd[j];
+    for (int i = 0; i < 4; ++i) {
+        row[4 * g + i] = dx[0][i];
+        st.dxf[Gn][4 * g + i] = dx[1][i];
     }
 
     // weight gradients from the Gaussian-major fragments, accumulated in place

@@ -391,14 +391,14 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_neural(PreArgs a)
             neural_stage_inputs(XS[wave].x, g.visible, d, a.sh_degree, f);
             wave_lds_sync();
             const uint64_t vis = __ballot(g.visible);
+            float o[3] = {0.f, 0.f, 0.f};
             for (int t = 0; t < kWave / 16; ++t) {
                 if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
-                float4_t h1, h2, o;
-                half4_t a1, a2;
-                neural_tile_fwd(W, neural_stage_frag(XS[wave].x, t), h1, a1, h2, a2, o);
-                neural_tile_residual(o, t, res);
+                neural_tile_gather(neural_tile_out(W, neural_stage_frag(XS[wave].x, t)), t, o);
             }
             wave_lds_sync();   // the stage is read before the next chunk overwrites it
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) res[ch] = tanhf(o[ch]);
         }
         float col[3];
 #pragma unroll

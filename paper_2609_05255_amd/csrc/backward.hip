@@ -366,10 +366,13 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
         }
         float dd[3] = {0.f, 0.f, 0.f};
         if (resid) {
-            float f[GS_NEURAL_FEATURES];
+            float f[GS_NEURAL_FEATURES], sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
             for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
                 f[j] = valid ? (float)half_of_bits(a.features[j * n + i]) : 0.f;
-            neural_stage_inputs(st.x, valid, d, a.sh_degree, f);
+            neural_encode_features(f, sf, cf);
+            half4_t fq[4];
+            neural_feature_inputs(sf, cf, fq);
+            neural_stage_inputs(st.x, valid, d, a.sh_degree, fq);
             wave_lds_sync();
             const uint64_t vis = __ballot(valid);
             // first pass: each lane's output pre-activations, then its residual
@@ -406,11 +409,8 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
                 for (int k = 0; k < 16; ++k) dY[k] = k < nb ? row[k] : 0.f;
                 sh_basis16_vjp(d[0], d[1], d[2], dY, dd);
                 // features: d(sin f)/df = cos f, d(cos f)/df = -sin f
-                for (int j = 0; j < GS_NEURAL_FEATURES; ++j) {
-                    float sj, cj;
-                    sincosf(f[j], &sj, &cj);
-                    a.dfeatures[j * n + i] = st.dxf[lane][2 * j] * cj - st.dxf[lane][2 * j + 1] * sj;
-                }
+                for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
+                    a.dfeatures[j * n + i] = st.dxf[lane][2 * j] * cf[j] - st.dxf[lane][2 * j + 1] * sf[j];
             }
         } else if (valid) {
             // no residual: c = max(0, c0 + 0.5)

@@ -77,11 +77,59 @@ __device__ __forceinline__ const float* neural_dir_grad_row(const NeuralBwdStage
     return reinterpret_cast<const float*>(&st.x[r][0]);
 }
 
+// sin f and cos f of a binary16 value f, without branches. Cody-Waite
+// reduction r = f - k pi/2 with k = rint(2f/pi) (|k| < 2^16 for binary16
+// arguments) against pi/2 split into three fp32 parts, each product exact
+// inside an FMA; Taylor polynomials of sin through r^9 and cos through r^10 on
+// |r| <= pi/4 (truncation below 2e-9); the quadrant k mod 4 swaps and negates.
+// Over every finite binary16 argument the error is at most 6.1e-8 absolute
+// (1.3 ulp), as measured against fp64 sin and cos.
+__device__ __forceinline__ void sincos_half_arg(float f, float* s, float* c)
+{
+    const float k = rintf(f * 0x1.45f306p-1f);           // 2/pi
+    float r = fmaf(-k, 0x1.921fb6p+0f, f);                // pi/2 = p1 + p2 + p3
+    r = fmaf(-k, -0x1.777a5cp-25f, r);
+    r = fmaf(-k, -0x1.ee59dap-50f, r);
+    const float r2 = r * r;
+    float ps = fmaf(r2, 1.f / 362880.f, -1.f / 5040.f);
+    ps = fmaf(r2, ps, 1.f / 120.f);
+    ps = fmaf(r2, ps, -1.f / 6.f);
+    const float sr = fmaf(r * r2, ps, r);
+    float pc = fmaf(r2, -1.f / 3628800.f, 1.f / 40320.f);
+    pc = fmaf(r2, pc, -1.f / 720.f);
+    pc = fmaf(r2, pc, 1.f / 24.f);
+    pc = fmaf(r2, pc, -0.5f);
+    const float cr = fmaf(r2, pc, 1.f);
+    const int q = (int)k & 3;
+    const float a = (q & 1) ? cr : sr, b = (q & 1) ? sr : cr;
+    *s = (q & 2) ? -a : a;
+    *c = ((q + 1) & 2) ? -b : b;
+}
+
+// sin f_j and cos f_j of the calling lane's features (the frequency encoding
+// with k = 1).
+__device__ __forceinline__ void neural_encode_features(const float f[GS_NEURAL_FEATURES], float sf[GS_NEURAL_FEATURES],
+                                                       float cf[GS_NEURAL_FEATURES])
+{
+#pragma unroll
+    for (int j = 0; j < GS_NEURAL_FEATURES; ++j) sincos_half_arg(f[j], &sf[j], &cf[j]);
+}
+
+// The 16 feature inputs in input order, rounded to binary16: q[k] holds
+// (sin f_2k, cos f_2k, sin f_2k+1, cos f_2k+1).
+__device__ __forceinline__ void neural_feature_inputs(const float sf[GS_NEURAL_FEATURES],
+                                                      const float cf[GS_NEURAL_FEATURES], half4_t q[4])
+{
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        q[k] = half4_t{(_Float16)sf[2 * k], (_Float16)cf[2 * k], (_Float16)sf[2 * k + 1], (_Float16)cf[2 * k + 1]};
+}
+
 // The calling lane's decoder input: SH basis values of d for bands <= degree
-// (zero above), then (sin f_j, cos f_j) for the 8 features, rounded to binary16
-// (zeros when !valid).
+// (zero above), then the feature inputs `fq` (neural_feature_inputs), in
+// binary16 (zeros when !valid).
 __device__ __forceinline__ void neural_stage_inputs(_Float16 (*x)[kXPitch], bool valid, const float d[3], int degree,
-                                                    const float f[GS_NEURAL_FEATURES])
+                                                    const half4_t fq[4])
 {
     const int l = __lane_id();
     half4_t v[8];
@@ -94,13 +142,7 @@ __device__ __forceinline__ void neural_stage_inputs(_Float16 (*x)[kXPitch], bool
 #pragma unroll
         for (int k = 0; k < 16; ++k) v[k >> 2][k & 3] = k < nb ? (_Float16)Y[k] : (_Float16)0.f;
 #pragma unroll
-        for (int j = 0; j < GS_NEURAL_FEATURES; ++j) {
-            const int e = 16 + 2 * j;
-            float sj, cj;
-            sincosf(f[j], &sj, &cj);
-            v[e >> 2][e & 3] = (_Float16)sj;
-            v[(e + 1) >> 2][(e + 1) & 3] = (_Float16)cj;
-        }
+        for (int q = 0; q < 4; ++q) v[4 + q] = fq[q];
     }
 #pragma unroll
     for (int q = 0; q < 8; ++q) *reinterpret_cast<half4_t*>(&x[l][4 * q]) = v[q];

@@ -347,7 +347,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_latent(PreArgs a)
 // max(0, c0 + 0.5) while the active degree is 0. Waves loop over 64-Gaussian
 // chunks on their own, the base colour and feature loads issued before the
 // geometry.
-__global__ __launch_bounds__(kBlock) void k_preprocess_neural(PreArgs a)
+__global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
 {
     __shared__ NeuralFrags W;
     __shared__ NeuralInStage XS[kBlock / kWave];
@@ -360,6 +360,7 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_neural(PreArgs a)
     for (int64_t chunk = (int64_t)blockIdx.x * (kBlock / kWave) + wave; chunk < nchunks; chunk += stride) {
         const int64_t base = chunk * kWave;
         const int i = (int)(base + lane);
+        // appearance loads first, so that they overlap the projection
         float c0[3] = {0.f, 0.f, 0.f}, f[GS_NEURAL_FEATURES];
 #pragma unroll
         for (int j = 0; j < GS_NEURAL_FEATURES; ++j) f[j] = 0.f;
@@ -388,7 +389,11 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_neural(PreArgs a)
         }
         float res[3] = {0.f, 0.f, 0.f};
         if (resid) {
-            neural_stage_inputs(XS[wave].x, g.visible, d, a.sh_degree, f);
+            float sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
+            half4_t fq[4];
+            neural_encode_features(f, sf, cf);
+            neural_feature_inputs(sf, cf, fq);
+            neural_stage_inputs(XS[wave].x, g.visible, d, a.sh_degree, fq);
             wave_lds_sync();
             const uint64_t vis = __ballot(g.visible);
             float o[3] = {0.f, 0.f, 0.f};
@@ -415,6 +420,8 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_neural(PreArgs a)
 // Workgroups of the latent preprocess: the number resident at once on 256 CUs
 // (four per CU at the kernel's register budget), each wave looping over chunks.
 constexpr int kLatentBlocks = 1024;
+// and of the neural one
+constexpr int kNeuralBlocks = 1024;
 
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                              const gs_preprocessed& out, const Workspace& ws, hipStream_t s)
@@ -446,7 +453,7 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
         }
     }
     else if (app.kind == GS_APP_NEURAL)
-        hipLaunchKernelGGL(k_preprocess_neural, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL(k_preprocess_neural, dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0, s, a);
     else
         hipLaunchKernelGGL(k_preprocess_latent, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
     return hipGetLastError();

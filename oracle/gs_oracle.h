@@ -47,7 +47,7 @@ typedef struct orc_camera {
     double bg[3];
 } orc_camera;
 
-enum { ORC_APP_SH3 = 0, ORC_APP_LATENT_MLP = 1, ORC_APP_NEURAL = 2 };
+enum { ORC_APP_SH3 = 0, ORC_APP_LATENT_MLP = 1, ORC_APP_NEURAL = 2, ORC_APP_NEURAL_FOLDED = 3 };
 
 /* flags written per Gaussian by the preprocess */
 enum {
@@ -74,6 +74,8 @@ typedef struct orc_appearance {
                                0: exact fp64 activations */
     const double* base_color; /* NEURAL: [3][n] base colour c0 */
     const double* features;   /* NEURAL: [8][n] values of binary16 numbers */
+    const double* preact;     /* NEURAL_FOLDED: [16][n] first-layer pre-activations of the
+                                 view-independent inputs (oracle.neural_fold); render only */
 } orc_appearance;
 
 /* Outputs of the preprocess. Entries of culled Gaussians are zero. */

@@ -7,7 +7,9 @@ generator's Scene and Camera works).
 
 Every function mirrors one stage of the method (the paper's Sec. 3.1 preprocess
 and blend, Sec. 4 appearance models, and the fused backward of its appendix);
-the arithmetic lives in C, this file only marshals arrays.
+the arithmetic lives in C, this file only marshals arrays, apart from the
+first-layer folding of the neural decoder (neural_fold), one matrix product in
+numpy.
 """
 from __future__ import annotations
 
@@ -24,6 +26,7 @@ _SOURCES = ("gs_oracle.c", "gs_oracle_body.inc", "gs_oracle.h")
 APP_SH3 = 0
 APP_LATENT_MLP = 1
 APP_NEURAL = 2
+APP_NEURAL_FOLDED = 3     # render only
 VISIBLE = 1
 CLAMP_X = 2
 CLAMP_Y = 4
@@ -54,7 +57,8 @@ class _Camera(C.Structure):
 class _Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p),
                 ("latent", C.c_void_p), ("mlp_w", C.c_void_p), ("dir_exact", C.c_int32),
-                ("half_act", C.c_int32), ("base_color", C.c_void_p), ("features", C.c_void_p)]
+                ("half_act", C.c_int32), ("base_color", C.c_void_p), ("features", C.c_void_p),
+                ("preact", C.c_void_p)]
 
 
 class _Pre(C.Structure):
@@ -140,12 +144,36 @@ class _SceneArrays:
         self.opacity_logits = _f64(scene.opacity_logits)
         self.sh = _f64(scene.sh) if kind == APP_SH3 else None
         self.latent = half_to_f64(scene.latent) if kind == APP_LATENT_MLP else None
+        neural = kind in (APP_NEURAL, APP_NEURAL_FOLDED)
         self.mlp_w = (half_to_f64(scene.mlp_w) if kind == APP_LATENT_MLP else
-                      half_to_f64(scene.neural_w) if kind == APP_NEURAL else None)
-        self.base_color = _f64(scene.base_color) if kind == APP_NEURAL else None
+                      half_to_f64(scene.neural_w) if neural else None)
+        self.base_color = _f64(scene.base_color) if neural else None
         self.features = half_to_f64(scene.features) if kind == APP_NEURAL else None
+        # the folded form: pre-activations exact with exact inputs, else binary16 like its inputs
+        self.preact = (np.ascontiguousarray(neural_fold(scene.features, scene.neural_w, exact=dir_exact))
+                       if kind == APP_NEURAL_FOLDED else None)
         self.app = _Appearance(kind, sh_degree, _p(self.sh), _p(self.latent), _p(self.mlp_w), int(dir_exact),
-                               int(half_act), _p(self.base_color), _p(self.features))
+                               int(half_act), _p(self.base_color), _p(self.features), _p(self.preact))
+
+
+def neural_fold(features, neural_w, exact: bool = False) -> np.ndarray:
+    """First-layer folding of the neural decoder (the paper's viewer, supplementary
+    section on the WebGL implementation): the inputs that do not depend on the
+    view, x_0 = Y_0 and x_16..31 = (sin f_j, cos f_j), times their 17 columns of
+    W1, as one pre-activation per hidden neuron and Gaussian, [16][n] float64.
+    Unless ``exact``, the inputs are binary16 as the decoder sees them and the
+    pre-activations are rounded to binary16, the precision they are stored in."""
+    w1 = half_to_f64(neural_w)[: 16 * 32].reshape(16, 32)
+    f = half_to_f64(features)
+    enc = np.empty((16, f.shape[1]))
+    enc[0::2] = np.sin(f)
+    enc[1::2] = np.cos(f)
+    y0 = 0.5 / np.sqrt(np.pi)
+    if not exact:
+        enc = enc.astype(np.float16).astype(np.float64)
+        y0 = float(np.float16(y0))
+    p = np.outer(w1[:, 0], np.full(f.shape[1], y0)) + w1[:, 16:] @ enc
+    return p if exact else p.astype(np.float16).astype(np.float64)
 
 
 def _kind_of(kind) -> int:
@@ -155,6 +183,8 @@ def _kind_of(kind) -> int:
         return APP_LATENT_MLP
     if kind in ("neural", APP_NEURAL):
         return APP_NEURAL
+    if kind in ("neural_folded", APP_NEURAL_FOLDED):
+        return APP_NEURAL_FOLDED
     raise ValueError(kind)
 
 
@@ -221,6 +251,8 @@ def render_fwd(cam, pre: Preprocessed, ranges, values, mode: str = "f32"):
 def render_bwd(cam, scene, pre: Preprocessed, ranges, values, dL_dimage, kind="sh3", sh_degree: int = 3,
                mode: str = "f32", dir_exact: bool = False, half_act: bool = False) -> dict:
     kind = _kind_of(kind)
+    if kind == APP_NEURAL_FOLDED:
+        raise ValueError("the folded neural form renders only; differentiate the unfolded one")
     sa = _SceneArrays(scene, kind, sh_degree, dir_exact, half_act)
     n = sa.n
     g = dict(dmeans=np.zeros((3, n)), dlog_scales=np.zeros((3, n)), dquats=np.zeros((4, n)),

@@ -100,3 +100,51 @@ def test_higher_band_inputs_follow_the_active_degree(orc, k, degree):
     col, vis = colours(orc, sc, cam, degree)
     expect = np.maximum(0.0, base(sc) + np.tanh(np.maximum(0.0, x))[None] + 0.5)
     assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12)
+
+
+# ---- first-layer folding (the paper's viewer; render only) ----------------------
+
+@pytest.mark.parametrize("degree", [1, 2, 3])
+def test_folding_is_exact_with_exact_inputs(orc, degree):
+    # folding only regroups the first layer's sum: with exact (unrounded) inputs
+    # and pre-activations the folded decoder gives the unfolded colours
+    sc = scene(256)
+    cam = inputs.make_cameras("tiny")[0]
+    a = orc.preprocess(cam, sc, kind="neural", sh_degree=degree, mode="f64", dir_exact=True)
+    b = orc.preprocess(cam, sc, kind="neural_folded", sh_degree=degree, mode="f64", dir_exact=True)
+    vis = a["tiles"] > 0
+    assert vis.sum() > 100 and np.array_equal(vis, b["tiles"] > 0)
+    assert np.allclose(a["color"][:, vis], b["color"][:, vis], rtol=0, atol=1e-12)
+    # and the residual is far from zero, so the comparison means something
+    assert np.abs(a["color"][:, vis] - np.maximum(0.0, base(sc) + 0.5)[:, vis]).max() > 0.05
+
+
+def test_folded_preactivations_closed_form(orc):
+    # W1 row 0 = 0.75 on the constant Y_0 input and -1.5 on sin f_2; row 5 = 2 on cos f_7;
+    # direction columns must not enter the pre-activations
+    sc = scene(64)
+    w = np.zeros(816, np.float16)
+    w[0 * 32 + 0] = 0.75
+    w[0 * 32 + 16 + 2 * 2] = -1.5
+    w[0 * 32 + 3] = 1.0
+    w[5 * 32 + 17 + 2 * 7] = 2.0
+    f = sc.features.view(np.float16).astype(np.float64)
+    y0 = 0.5 / math.sqrt(math.pi)
+    p = orc.neural_fold(sc.features, w.view(np.uint16), exact=True)
+    assert p.shape == (16, sc.n)
+    assert np.allclose(p[0], 0.75 * y0 - 1.5 * np.sin(f[2]), rtol=0, atol=1e-15)
+    assert np.allclose(p[5], 2.0 * np.cos(f[7]), rtol=0, atol=1e-15)
+    assert not np.delete(p, [0, 5], axis=0).any()
+    # stored form: binary16 inputs, the sum rounded to binary16
+    h = lambda v: np.asarray(v, np.float64).astype(np.float16).astype(np.float64)
+    q = orc.neural_fold(sc.features, w.view(np.uint16))
+    assert np.array_equal(q[0], h(0.75 * h(y0) - 1.5 * h(np.sin(f[2]))))
+    assert np.array_equal(q[5], h(2.0 * h(np.cos(f[7]))))
+
+
+def test_folded_form_has_no_backward(orc):
+    sc = scene(16)
+    cam = inputs.make_cameras("tiny")[0]
+    r = orc.render(cam, sc, kind="neural_folded", sh_degree=2, mode="f64")
+    with pytest.raises(ValueError):
+        orc.render_bwd(cam, sc, r["pre"], r["ranges"], r["values"], np.zeros((3, 64, 64)), kind="neural_folded")

@@ -84,6 +84,13 @@ enum {
                                  c = max(0, c0 + tanh(W3 relu(W2 relu(W1 x))) + 0.5), no biases,
                                  x = (Y_0..15(d) with bands above sh_degree zero,
                                       sin f_0, cos f_0, ..., sin f_7, cos f_7) */
+    GS_APP_NEURAL_FOLDED = 3, /* render only: NEURAL with its first layer folded (the paper's
+                                 viewer, supplementary section on the WebGL implementation).
+                                 The view-independent inputs Y_0, sin f_j, cos f_j times their
+                                 17 columns of W1 are stored per Gaussian as 16 binary16
+                                 pre-activations p (gs_neural_fold); per view only
+                                 h1 = relu(p + W1[:, 1..15] Y_1..15(d)) is evaluated, the rest
+                                 as NEURAL. gs_render_bwd rejects this kind. */
 };
 
 #define GS_NEURAL_FEATURES 8  /* binary16 features per Gaussian (16 B) beside a 12 B fp32 base colour */
@@ -108,6 +115,9 @@ typedef struct gs_appearance {
                                  its sums fp32, tanh in fp32 */
     const float* base_color;  /* NEURAL: [3][n] fp32 base colour c0 */
     const uint16_t* features; /* NEURAL: [8][n] binary16 bit patterns */
+    const uint16_t* preact;   /* NEURAL_FOLDED: [n][16] binary16 bit patterns, Gaussian-major
+                                 (32 B per Gaussian), as gs_neural_fold writes them;
+                                 base_color and mlp_w (the 816 NEURAL weights) as for NEURAL */
 } gs_appearance;
 
 /* Screen-space record of one Gaussian, written by gs_preprocess (64 bytes).
@@ -227,6 +237,21 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
 gs_status gs_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* mlp_w, float* colors, void* stream);
 
 /*
+ * gs_neural_fold -- first-layer folding of the neural decoder (the paper's viewer,
+ * supplementary section on the WebGL implementation), done once per scene before
+ * rendering with GS_APP_NEURAL_FOLDED:
+ *   preact[i][r] = binary16( sum over k in {0, 16..31} of W1[r][k] x_k(i) ),
+ * x_0 = Y_0 = 1/(2 sqrt(pi)), x_16+2j = sin f_j, x_17+2j = cos f_j of Gaussian
+ * i's features, each input rounded to binary16 as the unfolded decoder sees it,
+ * the sum in fp32, then rounded to nearest binary16.
+ * features: [8][n] binary16 device array; mlp_w: the 816 NEURAL weights (device);
+ * preact: [n][16] binary16 device array, caller-owned, overwritten.
+ * n must be in [0, 2^31); n = 0 does nothing. Asynchronous on `stream`.
+ */
+gs_status gs_neural_fold(const uint16_t* features, const uint16_t* mlp_w, int64_t n, uint16_t* preact,
+                         void* stream);
+
+/*
  * gs_adam_step -- one Adam step (Kingma and Ba, Algorithm 1, with bias
  * correction) over several parameter tensors in a single launch: the fused
  * optimiser update of the paper's training pipeline (supplementary
@@ -278,7 +303,7 @@ enum {
     GS_KERNEL_PREPROCESS = 0, GS_KERNEL_PAIR_COUNT, GS_KERNEL_DEPTH_SORT, GS_KERNEL_PAIR_OFFSETS,
     GS_KERNEL_DUPLICATE, GS_KERNEL_TILE_SORT, GS_KERNEL_RANGES, GS_KERNEL_BLEND_FWD,
     GS_KERNEL_CLEAR, GS_KERNEL_BLEND_BWD, GS_KERNEL_PREPROCESS_BWD, GS_KERNEL_MLP_REDUCE,
-    GS_KERNEL_ADAM, GS_KERNEL_COUNT
+    GS_KERNEL_ADAM, GS_KERNEL_NEURAL_FOLD, GS_KERNEL_COUNT
 };
 gs_status gs_timing_enable(int32_t enable);
 gs_status gs_timing_reset(void);

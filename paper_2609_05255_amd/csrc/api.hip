@@ -83,6 +83,12 @@ gs_status check_appearance(const gs_appearance* a, int64_t n)
         GS_CHECK(n == 0 || a->base_color != nullptr, "base_color is NULL");
         GS_CHECK(n == 0 || a->sh_degree == 0 || (a->features != nullptr && a->mlp_w != nullptr),
                  "features or mlp_w is NULL");
+    } else if (a->kind == GS_APP_NEURAL_FOLDED) {
+        GS_CHECK(a->sh_degree >= 0 && a->sh_degree <= 3, "sh_degree %d outside 0..3", a->sh_degree);
+        GS_CHECK(n == 0 || a->base_color != nullptr, "base_color is NULL");
+        GS_CHECK(n == 0 || a->sh_degree == 0 || (a->preact != nullptr && a->mlp_w != nullptr),
+                 "preact or mlp_w is NULL");
+        GS_CHECK(((uintptr_t)a->preact & 7) == 0, "preact must be 8-byte aligned");
     } else {
         return fail(GS_ERR_INVALID_ARG, "unknown appearance kind %d", a->kind);
     }
@@ -137,7 +143,7 @@ void resolve_pending_locked()
 
 const char* const kKernelNames[GS_KERNEL_COUNT] = {
     "preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
-    "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam"};
+    "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam", "neural_fold"};
 
 }  // namespace
 
@@ -248,8 +254,7 @@ gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t c
     GS_CHECK(n >= 0 && n < ((int64_t)1 << 31), "n out of range");
     GS_CHECK(width > 0 && height > 0, "image size must be positive");
     GS_CHECK(capacity < ((uint64_t)1 << 32), "capacity must be below 2^32");
-    GS_CHECK(kind == GS_APP_SH3 || kind == GS_APP_LATENT_MLP || kind == GS_APP_NEURAL, "unknown appearance kind %d",
-             kind);
+    GS_CHECK(kind >= GS_APP_SH3 && kind <= GS_APP_NEURAL_FOLDED, "unknown appearance kind %d", kind);
     *bytes = layout_workspace(nullptr, n, capacity, kind).bytes;
     return ok();
 }
@@ -366,6 +371,8 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
     if ((st = check_camera(cam)) != GS_OK) return st;
     if ((st = check_gaussians(g)) != GS_OK) return st;
     if ((st = check_appearance(app, g->n)) != GS_OK) return st;
+    GS_CHECK(app->kind != GS_APP_NEURAL_FOLDED,
+             "the folded neural appearance renders only: differentiate GS_APP_NEURAL instead");
     if ((st = check_pre(pre, g->n)) != GS_OK) return st;
     GS_CHECK(tile_ranges && final_T && n_contrib && dL_dimage, "a render input array is NULL");
     GS_CHECK(grads != nullptr, "grads is NULL");
@@ -411,6 +418,19 @@ gs_status gs_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* mlp_w, fl
     GS_CHECK(rows == 0 || (x && mlp_w && colors), "an array is NULL");
     if (rows == 0) return ok();
     GS_HIP(launch_mlp_eval(x, rows, mlp_w, colors, static_cast<hipStream_t>(stream)));
+    return ok();
+}
+
+gs_status gs_neural_fold(const uint16_t* features, const uint16_t* mlp_w, int64_t n, uint16_t* preact, void* stream)
+{
+    GS_CHECK(n >= 0 && n < ((int64_t)1 << 31), "n = %lld out of range [0, 2^31)", (long long)n);
+    GS_CHECK(n == 0 || (features && mlp_w && preact), "an array is NULL");
+    GS_CHECK(((uintptr_t)preact & 7) == 0, "preact must be 8-byte aligned");
+    if (n == 0) return ok();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    timing_begin(GS_KERNEL_NEURAL_FOLD, s);
+    GS_HIP(launch_neural_fold(features, mlp_w, n, preact, s));
+    timing_end(GS_KERNEL_NEURAL_FOLD, s);
     return ok();
 }
 

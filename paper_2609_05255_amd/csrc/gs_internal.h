@@ -127,6 +127,8 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
 hipError_t launch_mlp_reduce(int64_t n, int32_t kind, const Workspace& ws, float* dmlp_w, hipStream_t s);
 hipError_t launch_adam(const gs_adam_tensor* tensors, int count, float beta1, float eps, int64_t step, hipStream_t s);
 hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s);
+hipError_t launch_neural_fold(const uint16_t* features, const uint16_t* w, int64_t n, uint16_t* preact,
+                              hipStream_t s);
 
 // Kernel timing hooks (api.hip): bracket one logical kernel id.
 void timing_begin(int kernel_id, hipStream_t s);

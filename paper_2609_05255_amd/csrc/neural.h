@@ -28,11 +28,15 @@ struct NeuralFrags {
     alignas(8) _Float16 w1t[2][kWave][4];   // A of W1^T: rows input = 16b + c,   K = n1 = 4g + j
     alignas(8) _Float16 w2t[kWave][4];      // A of W2^T: rows n1 = c,             K = n2 = 4g + j
     alignas(8) _Float16 w3t[kWave][4];      // A of W3^T: rows n2 = c,             K = o = 4g + j (< 3)
+    alignas(8) _Float16 w1d[kWave][4];      // A of W1's direction columns 1..15 (folded form):
+                                            //            rows n1 = c, K = 4g + j -> column 1 + 4g + j (< 16)
 };
 
 // Loads the weights into the fragments (the transposed ones only if
-// `backward`). Called by every thread of the workgroup; ends with a barrier.
-__device__ __forceinline__ void neural_load_frags(const uint16_t* __restrict__ w, NeuralFrags& s, bool backward)
+// `backward`, the direction columns only if `folded`). Called by every thread
+// of the workgroup; ends with a barrier.
+__device__ __forceinline__ void neural_load_frags(const uint16_t* __restrict__ w, NeuralFrags& s, bool backward,
+                                                  bool folded = false)
 {
     const _Float16* W1 = reinterpret_cast<const _Float16*>(w);
     const _Float16* W2 = W1 + kNeuralHidden * kNeuralIn;
@@ -45,6 +49,7 @@ __device__ __forceinline__ void neural_load_frags(const uint16_t* __restrict__ w
             const int k = 4 * g + j;
             s.w2a[l][j] = W2[c * kNeuralHidden + k];
             s.w3a[l][j] = c < GS_MLP_OUT ? W3[c * kNeuralHidden + k] : z;
+            if (folded) s.w1d[l][j] = k < 15 ? W1[c * kNeuralIn + 1 + k] : z;
             if (backward) {
                 for (int b = 0; b < 2; ++b) s.w1t[b][l][j] = W1[k * kNeuralIn + 16 * b + c];
                 s.w2t[l][j] = W2[k * kNeuralHidden + c];
@@ -146,6 +151,40 @@ __device__ __forceinline__ void neural_stage_inputs(_Float16 (*x)[kXPitch], bool
     }
 #pragma unroll
     for (int q = 0; q < 8; ++q) *reinterpret_cast<half4_t*>(&x[l][4 * q]) = v[q];
+}
+
+// The folded form's per-view decoder input: Y_1..15(d) for bands <= degree (zero
+// above), then a zero pad, in binary16 (zeros when !valid), in row `lane`.
+__device__ __forceinline__ void neural_stage_dir(_Float16 (*x)[kXPitch], bool valid, const float d[3], int degree)
+{
+    const int l = __lane_id();
+    half4_t v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = half4_t{0, 0, 0, 0};
+    if (valid) {
+        float Y[16];
+        sh_basis16(d[0], d[1], d[2], Y);
+        const int nb = (degree + 1) * (degree + 1);
+#pragma unroll
+        for (int k = 1; k < 16; ++k) v[(k - 1) >> 2][(k - 1) & 3] = k < nb ? (_Float16)Y[k] : (_Float16)0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) *reinterpret_cast<half4_t*>(&x[l][4 * q]) = v[q];
+}
+
+// Output pre-activations of tile t in the folded form: h1 = p + W1d xd with the
+// Gaussians' pre-activations p as the accumulator input (p4: neurons 4g + i of
+// Gaussian 16t + c, this lane's share), then layers 2 and 3 as unfolded.
+__device__ __forceinline__ float4_t neural_tile_out_folded(const NeuralFrags& W, const _Float16 (*x)[kXPitch], int t,
+                                                           const half4_t& p4)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
+    const half4_t xd = *reinterpret_cast<const half4_t*>(&x[16 * t + c][4 * g]);
+    const float4_t p = {(float)p4[0], (float)p4[1], (float)p4[2], (float)p4[3]};
+    const half4_t a1 = relu_half4(mfma16(frag4(W.w1d), xd, p));
+    const half4_t a2 = relu_half4(mfma16(frag4(W.w2a), a1, zero));
+    return mfma16(frag4(W.w3a), a2, zero);
 }
 
 // B fragment of tile t: inputs s(g, 0..7) of Gaussian 16t + c.

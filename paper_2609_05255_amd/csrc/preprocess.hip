@@ -136,6 +136,7 @@ struct PreArgs {
     const uint16_t* mlp_w;
     const float* base_color;
     const uint16_t* features;
+    const uint16_t* preact;
     gs_splat* splats;
     uint32_t* tiles_touched;
     uint32_t* depth_key;
@@ -346,14 +347,17 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_latent(PreArgs a)
 // a time on the matrix cores; colour max(0, c0 + tanh(MLP(x)) + 0.5), or
 // max(0, c0 + 0.5) while the active degree is 0. Waves loop over 64-Gaussian
 // chunks on their own, the base colour and feature loads issued before the
-// geometry.
+// geometry. kFolded: the render-only folded form, whose first layer adds the
+// stored pre-activations of the view-independent inputs to the direction
+// columns' product (no features, no sin/cos).
+template <bool kFolded>
 __global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
 {
     __shared__ NeuralFrags W;
     __shared__ NeuralInStage XS[kBlock / kWave];
     __shared__ SplatStage stage[kBlock / kWave];
     const bool resid = a.sh_degree >= 1;
-    if (resid) neural_load_frags(a.mlp_w, W, false);
+    if (resid) neural_load_frags(a.mlp_w, W, false, kFolded);
     const int lane = __lane_id(), wave = threadIdx.x >> 6;
     const int64_t nchunks = div_up((int64_t)a.n, kWave);
     const int64_t stride = (int64_t)gridDim.x * (kBlock / kWave);
@@ -362,15 +366,26 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
         const int i = (int)(base + lane);
         // appearance loads first, so that they overlap the projection
         float c0[3] = {0.f, 0.f, 0.f}, f[GS_NEURAL_FEATURES];
+        half4_t p4[kWave / 16];   // folded: neurons 4g..4g+3 of Gaussian base + 16t + c
 #pragma unroll
         for (int j = 0; j < GS_NEURAL_FEATURES; ++j) f[j] = 0.f;
+#pragma unroll
+        for (int t = 0; t < kWave / 16; ++t) p4[t] = half4_t{0, 0, 0, 0};
         if (i < a.n) {
 #pragma unroll
             for (int ch = 0; ch < 3; ++ch) c0[ch] = a.base_color[(int64_t)ch * a.n + i];
-            if (resid)
+            if (resid && !kFolded)
 #pragma unroll
                 for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
                     f[j] = (float)half_of_bits(a.features[(int64_t)j * a.n + i]);
+        }
+        if (resid && kFolded) {
+            const int g4 = lane >> 4, c = lane & 15;
+#pragma unroll
+            for (int t = 0; t < kWave / 16; ++t) {
+                const int64_t gi = base + 16 * t + c;
+                if (gi < a.n) p4[t] = *reinterpret_cast<const half4_t*>(a.preact + gi * 16 + 4 * g4);
+            }
         }
         uint32_t tiles = 0;
         Geo g;
@@ -389,17 +404,24 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
         }
         float res[3] = {0.f, 0.f, 0.f};
         if (resid) {
-            float sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
-            half4_t fq[4];
-            neural_encode_features(f, sf, cf);
-            neural_feature_inputs(sf, cf, fq);
-            neural_stage_inputs(XS[wave].x, g.visible, d, a.sh_degree, fq);
+            if (kFolded) {
+                neural_stage_dir(XS[wave].x, g.visible, d, a.sh_degree);
+            } else {
+                float sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
+                half4_t fq[4];
+                neural_encode_features(f, sf, cf);
+                neural_feature_inputs(sf, cf, fq);
+                neural_stage_inputs(XS[wave].x, g.visible, d, a.sh_degree, fq);
+            }
             wave_lds_sync();
             const uint64_t vis = __ballot(g.visible);
             float o[3] = {0.f, 0.f, 0.f};
+#pragma unroll
             for (int t = 0; t < kWave / 16; ++t) {
                 if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
-                neural_tile_gather(neural_tile_out(W, neural_stage_frag(XS[wave].x, t)), t, o);
+                const float4_t ot = kFolded ? neural_tile_out_folded(W, XS[wave].x, t, p4[t])
+                                            : neural_tile_out(W, neural_stage_frag(XS[wave].x, t));
+                neural_tile_gather(ot, t, o);
             }
             wave_lds_sync();   // the stage is read before the next chunk overwrites it
 #pragma unroll
@@ -439,6 +461,7 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     a.mlp_w = app.mlp_w;
     a.base_color = app.base_color;
     a.features = app.features;
+    a.preact = app.preact;
     a.splats = out.splats;
     a.tiles_touched = out.tiles_touched;
     a.depth_key = out.depth_key;
@@ -453,7 +476,9 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
         }
     }
     else if (app.kind == GS_APP_NEURAL)
-        hipLaunchKernelGGL(k_preprocess_neural, dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL(k_preprocess_neural<false>, dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0, s, a);
+    else if (app.kind == GS_APP_NEURAL_FOLDED)
+        hipLaunchKernelGGL(k_preprocess_neural<true>, dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0, s, a);
     else
         hipLaunchKernelGGL(k_preprocess_latent, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
     return hipGetLastError();
@@ -537,6 +562,48 @@ __global__ __launch_bounds__(kBlock) void k_mlp_eval(const uint16_t* __restrict_
 hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s)
 {
     hipLaunchKernelGGL(k_mlp_eval, dim3((unsigned)div_up(rows, kBlock)), dim3(kBlock), 0, s, x, rows, w, out);
+    return hipGetLastError();
+}
+
+// First-layer folding of the neural decoder: one wave per 64 Gaussians stages
+// the unfolded input with every direction input but the constant Y_0 zero, so
+// the first layer's product is exactly the pre-activation of the view-
+// independent inputs; each tile's fp32 result is rounded to binary16 and
+// stored Gaussian-major, 8 bytes per lane (neurons 4g..4g+3 of Gaussian c).
+__global__ __launch_bounds__(kBlock) void k_neural_fold(const uint16_t* __restrict__ features,
+                                                        const uint16_t* __restrict__ w, int n,
+                                                        uint16_t* __restrict__ preact)
+{
+    __shared__ NeuralFrags W;
+    __shared__ NeuralInStage XS[kBlock / kWave];
+    neural_load_frags(w, W, false);
+    const int lane = __lane_id(), wave = threadIdx.x >> 6, g = lane >> 4, c = lane & 15;
+    const int64_t base = ((int64_t)blockIdx.x * (kBlock / kWave) + wave) * kWave;
+    const int64_t i = base + lane;
+    float f[GS_NEURAL_FEATURES], sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
+#pragma unroll
+    for (int j = 0; j < GS_NEURAL_FEATURES; ++j) f[j] = i < n ? (float)half_of_bits(features[j * (int64_t)n + i]) : 0.f;
+    neural_encode_features(f, sf, cf);
+    half4_t fq[4];
+    neural_feature_inputs(sf, cf, fq);
+    const float d[3] = {0.f, 0.f, 1.f};   // unused at degree 0: only the constant Y_0 enters
+    neural_stage_inputs(XS[wave].x, i < n, d, 0, fq);
+    wave_lds_sync();
+    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < kWave / 16; ++t) {
+        const int64_t gi = base + 16 * t + c;
+        const float4_t h = mfma32(frag8(W.w1a), neural_stage_frag(XS[wave].x, t), zero);
+        const half4_t hv = {(_Float16)h[0], (_Float16)h[1], (_Float16)h[2], (_Float16)h[3]};
+        if (gi < n) *reinterpret_cast<half4_t*>(preact + gi * 16 + 4 * g) = hv;
+    }
+}
+
+hipError_t launch_neural_fold(const uint16_t* features, const uint16_t* w, int64_t n, uint16_t* preact,
+                              hipStream_t s)
+{
+    hipLaunchKernelGGL(k_neural_fold, dim3((unsigned)div_up(n, (int64_t)kBlock)), dim3(kBlock), 0, s, features, w,
+                       (int)n, preact);
     return hipGetLastError();
 }
 

@@ -20,11 +20,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libgsraster.so")
 
 GS_OK, GS_ERR_INVALID_ARG, GS_ERR_CAPACITY, GS_ERR_DEVICE, GS_ERR_UNSUPPORTED = range(5)
-GS_APP_SH3, GS_APP_LATENT_MLP, GS_APP_NEURAL = 0, 1, 2
+GS_APP_SH3, GS_APP_LATENT_MLP, GS_APP_NEURAL, GS_APP_NEURAL_FOLDED = 0, 1, 2, 3
 NEURAL_FEATURES = 8
 NEURAL_WEIGHTS = 816
 KERNEL_NAMES = ["preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
-                "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam"]
+                "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam", "neural_fold"]
 ADAM_MAX_TENSORS = 8
 ADAM_MAX_ROWS = 128
 SPLAT_BYTES = 64
@@ -50,7 +50,8 @@ class Gaussians(C.Structure):
 
 class Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p), ("latent", C.c_void_p),
-                ("mlp_w", C.c_void_p), ("base_color", C.c_void_p), ("features", C.c_void_p)]
+                ("mlp_w", C.c_void_p), ("base_color", C.c_void_p), ("features", C.c_void_p),
+                ("preact", C.c_void_p)]
 
 
 class Preprocessed(C.Structure):
@@ -89,6 +90,7 @@ def lib() -> C.CDLL:
                                     P(Grads), vp, sz, vp]
         L.gs_workspace_size.argtypes = [i64, i32, i32, u64, i32, P(sz)]
         L.gs_mlp_eval.argtypes = [vp, i64, vp, vp, vp]
+        L.gs_neural_fold.argtypes = [vp, vp, i64, vp, vp]
         L.gs_adam_step.argtypes = [P(AdamTensor), i32, C.c_float, C.c_float, i64, vp]
         L.gs_timing_enable.argtypes = [i32]
         L.gs_timing_reset.argtypes = []
@@ -156,6 +158,14 @@ class SceneTensors:
         self.base_color = f32(scene.base_color) if getattr(scene, "base_color", None) is not None else None
         self.features = h16(scene.features) if getattr(scene, "features", None) is not None else None
         self.neural_w = h16(scene.neural_w) if getattr(scene, "neural_w", None) is not None else None
+        self.preact = None   # [n][16] binary16 pre-activations of the folded form (fold_neural)
+
+    def fold_neural(self, stream=None):
+        """Computes the folded form's per-Gaussian pre-activations (gs_neural_fold)."""
+        if self.preact is None:
+            self.preact = torch.empty((self.n, 16), dtype=torch.int16, device=self.features.device)
+        gs_neural_fold(self.features, self.neural_w, self.n, self.preact, stream)
+        return self.preact
 
     def gaussians(self) -> Gaussians:
         return Gaussians(self.n, _ptr(self.means), _ptr(self.log_scales), _ptr(self.quats),
@@ -164,8 +174,13 @@ class SceneTensors:
     def appearance(self, kind: int, sh_degree: int = 3) -> Appearance:
         if kind == GS_APP_NEURAL:
             return Appearance(kind, sh_degree, None, None, _ptr(self.neural_w), _ptr(self.base_color),
-                              _ptr(self.features))
-        return Appearance(kind, sh_degree, _ptr(self.sh), _ptr(self.latent), _ptr(self.mlp_w), None, None)
+                              _ptr(self.features), None)
+        if kind == GS_APP_NEURAL_FOLDED:
+            if self.preact is None:
+                raise RuntimeError("fold_neural() first: the folded form reads its pre-activations")
+            return Appearance(kind, sh_degree, None, None, _ptr(self.neural_w), _ptr(self.base_color), None,
+                              _ptr(self.preact))
+        return Appearance(kind, sh_degree, _ptr(self.sh), _ptr(self.latent), _ptr(self.mlp_w), None, None, None)
 
 
 def gs_workspace_size(n: int, width: int, height: int, capacity: int, kind: int) -> int:
@@ -203,6 +218,10 @@ def gs_render_bwd(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed,
 
 def gs_mlp_eval(x, rows: int, mlp_w, colors, stream=None):
     _check(lib().gs_mlp_eval(_ptr(x), rows, _ptr(mlp_w), _ptr(colors), _stream(stream)))
+
+
+def gs_neural_fold(features, neural_w, n: int, preact, stream=None):
+    _check(lib().gs_neural_fold(_ptr(features), _ptr(neural_w), n, _ptr(preact), _stream(stream)))
 
 
 def gs_adam_step(tensors, beta1: float, eps: float, step: int, stream=None):

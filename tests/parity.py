@@ -26,13 +26,17 @@ def say(msg: str):
 
 
 def kind_id(kind: str) -> int:
-    return {"sh3": gs.GS_APP_SH3, "latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL}[kind]
+    return {"sh3": gs.GS_APP_SH3, "latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL,
+            "neural_folded": gs.GS_APP_NEURAL_FOLDED}[kind]
 
 
 def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None, extras=True):
     """extras=False runs the launch configuration of the benchmark: no tile-id
     output and no dmean2d output."""
     st = gs.SceneTensors(scene)
+    if kind == "neural_folded":
+        assert dL_dimage is None, "the folded form renders only"
+        st.fold_neural()
     cs = gs.camera_struct(cam)
     if capacity is None:
         capacity = 1 << 16

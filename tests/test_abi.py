@@ -99,6 +99,12 @@ def test_preprocess_rejects_bad_arguments(gs):
     assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 3, None, None, FAKE, None, FAKE)) == gs.GS_ERR_INVALID_ARG
     assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 2, None, None, FAKE, FAKE, None)) == gs.GS_ERR_INVALID_ARG
     assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 4, None, None, FAKE, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
+    # folded neural: pre-activations instead of features, 8-byte aligned
+    folded = lambda deg, pre_act: gs.Appearance(gs.GS_APP_NEURAL_FOLDED, deg, None, None, FAKE, FAKE, None, pre_act)
+    assert call(app=folded(3, None)) == gs.GS_ERR_INVALID_ARG
+    assert b"preact" in lib.gs_last_error()
+    assert call(app=folded(3, FAKE + 2)) == gs.GS_ERR_INVALID_ARG
+    assert call(app=folded(4, FAKE)) == gs.GS_ERR_INVALID_ARG
     assert call(pre=gs.Preprocessed(FAKE, FAKE, FAKE, None)) == gs.GS_ERR_INVALID_ARG
     assert call(ws=FAKE + 4) == gs.GS_ERR_INVALID_ARG              # misaligned workspace
     assert call(wsb=16) == gs.GS_ERR_CAPACITY
@@ -135,6 +141,29 @@ def test_render_calls_reject_bad_arguments(gs):
                            C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE), C.byref(grads),
                            C.c_void_p(FAKE * 256), 1 << 40, None)
     assert st == gs.GS_ERR_INVALID_ARG and b"dsh" in lib.gs_last_error()
+    # the folded neural form renders only
+    app = gs.Appearance(gs.GS_APP_NEURAL_FOLDED, 3, None, None, FAKE, FAKE, None, FAKE)
+    grads = gs.Grads(FAKE, FAKE, FAKE, FAKE, None, None, FAKE, None, FAKE, FAKE)
+    st = lib.gs_render_bwd(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), C.c_void_p(FAKE), C.c_void_p(FAKE),
+                           C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE), C.byref(grads),
+                           C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARG and b"folded" in lib.gs_last_error()
+
+
+def test_neural_fold_rejects_bad_arguments(gs):
+    lib = gs.lib()
+    f = lambda *a: lib.gs_neural_fold(*[C.c_void_p(x) if x is not None else None for x in a[:2]], a[2],
+                                      C.c_void_p(a[3]) if a[3] is not None else None, None)
+    assert f(FAKE, FAKE, -1, FAKE) == gs.GS_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, 1 << 31, FAKE) == gs.GS_ERR_INVALID_ARG
+    assert f(None, FAKE, 10, FAKE) == gs.GS_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, 10, None) == gs.GS_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, 10, FAKE + 4) == gs.GS_ERR_INVALID_ARG
+    assert b"aligned" in lib.gs_last_error()
+    assert f(None, None, 0, None) == gs.GS_OK          # nothing to do, nothing launched
+    # the folded form has no backward, so its workspace holds no weight-gradient partials
+    assert gs.gs_workspace_size(1000, 64, 64, 100, gs.GS_APP_NEURAL_FOLDED) < \
+        gs.gs_workspace_size(1000, 64, 64, 100, gs.GS_APP_NEURAL)
 
 
 def test_adam_rejects_bad_arguments(gs):

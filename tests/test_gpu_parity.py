@@ -28,10 +28,10 @@ def check_all(scene, cam, kind="sh3", sh_degree=3, label="", grads=True, capacit
     g = inputs.make_upstream_grad(cam.width, cam.height, 0) if grads else None
     say("case %s: n=%d %dx%d %s degree %d" % (label, scene.n, cam.width, cam.height, kind, sh_degree))
     gpu = run_gpu(scene, cam, kind, sh_degree, g, capacity=capacity)
-    latent = kind in ("latent", "neural")
+    latent = kind in ("latent", "neural", "neural_folded")
     # the decoder's operands are binary16: compare with the oracle that rounds them alike
     ref = oracle_all(scene, cam, kind, sh_degree, g, half_act=latent)
-    flip = NEURAL_FLIP if kind == "neural" else None
+    flip = NEURAL_FLIP if kind in ("neural", "neural_folded") else None
     compare_preprocess(gpu, ref["pre"], color_atol=MLP_HALF_ATOL if latent else 2e-6, flip=flip)
     compare_lists(gpu, ref["values"], ref["tile_of"], ref["ranges"])
     if latent:
@@ -179,3 +179,60 @@ def test_binning_one_tile_and_huge_gaussians():
     ls[:, ::997] += np.float32(6.0)
     sc = dataclasses.replace(sc, log_scales=ls)
     check_all(sc, tiny_camera(96, 80), label="one-tile+huge")
+
+
+# ---- the folded neural form (render only) ---------------------------------------
+
+def folded_preact_check(sc, got):
+    """GPU pre-activations against the oracle's fold (binary16 inputs, fp64 sum,
+    rounded to binary16). The GPU's sin/cos (fp32) may round an input to the
+    neighbouring binary16 value (spacing <= 2^-11 below 1), which moves a sum
+    by at most max|W1| 2^-11, and it sums in fp32 (17 terms, error far below
+    1e-5); the final rounding then adds at most one binary16 spacing. Both are
+    rare: nearly every value is bit-equal."""
+    ref = orc.neural_fold(sc.features, sc.neural_w).T          # [n][16]
+    g = got.view(np.float16).astype(np.float64)
+    assert g.shape == ref.shape
+    w1 = np.abs(sc.neural_w.view(np.float16).astype(np.float64)[:512])
+    spacing = np.spacing(np.abs(ref).astype(np.float16)).astype(np.float64)
+    diff = np.abs(g - ref)
+    bound = spacing + w1.max() * 2.0 ** -11 + 1e-5
+    assert np.all(diff <= bound), float((diff / bound).max())
+    flips = int((diff > 0).sum())
+    say("  fold: %d of %d pre-activations on the neighbouring binary16 value" % (flips, ref.size))
+    assert flips <= max(2, ref.size // 1000)
+
+
+@pytest.mark.parametrize("n", [1, 63, 1000, 4096])
+def test_neural_fold(n):
+    sc = inputs.make_scene("tiny", n=n, appearance=("neural",))
+    st = gs.SceneTensors(sc)
+    got = st.fold_neural().cpu().numpy().view(np.uint16)
+    torch.cuda.synchronize()
+    folded_preact_check(sc, got)
+
+
+def test_neural_fold_empty():
+    sc = inputs.make_scene("tiny", n=1, appearance=("neural",))
+    st = gs.SceneTensors(sc)
+    st.preact = torch.full((1, 16), 7, dtype=torch.int16, device="cuda")
+    gs.gs_neural_fold(st.features, st.neural_w, 0, st.preact)   # n = 0 touches nothing
+    torch.cuda.synchronize()
+    assert np.all(st.preact.cpu().numpy() == 7)
+
+
+@pytest.mark.parametrize("degree", [0, 1, 2, 3])
+def test_tiny_scene_neural_folded(degree):
+    sc = inputs.make_scene("tiny", appearance=("neural",))
+    check_all(sc, tiny_camera(), kind="neural_folded", sh_degree=degree, label="tiny-folded", grads=False)
+
+
+def test_ragged_neural_folded_with_background():
+    sc = inputs.make_scene("tiny", n=1000, appearance=("neural",))
+    check_all(sc, tiny_camera(50, 37, bg=(0.3, 0.2, 0.1)), kind="neural_folded", label="ragged-folded",
+              grads=False)
+
+
+def test_medium_scene_neural_folded():
+    sc = inputs.make_scene("medium", appearance=("neural",))
+    check_all(sc, inputs.make_cameras("medium")[2], kind="neural_folded", label="medium-folded", grads=False)

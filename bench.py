@@ -90,7 +90,8 @@ def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int
     """HBM bytes a launch must move at minimum (per launch, averaged over cameras)."""
     # appearance bytes per visible Gaussian: SH3 48 fp32, latent 14 binary16, neural a 12 B
     # base colour and 8 binary16 features
-    app = 4 * 3 * (sh_degree + 1) ** 2 if kind == "sh3" else 28
+    # (the folded form: the base colour and 16 binary16 pre-activations, 44 B)
+    app = 4 * 3 * (sh_degree + 1) ** 2 if kind == "sh3" else 44 if kind == "neural_folded" else 28
     if kernel == "preprocess":
         # params 44 B + tiles 4 B + depth key 4 B per Gaussian; appearance + 48 B of projected splat
         # (mean 8, conic 12, opacity 4, colour 12, rectangle 8, depth 4) per visible one; the record
@@ -246,6 +247,40 @@ def main():
     train = {"it_s": round(1.0 / t_train, 3), "ms_per_step": round(1e3 * t_train, 4), "adam_ms": round(adam_ms, 4),
              "optimizer": "fused Adam over every parameter tensor, one launch per step"}
 
+    # render only (preprocess, binning, forward blend), the unfolded neural
+    # decoder against its folded form (the paper's viewer optimisation)
+    render_only = None
+    if kind == "neural":
+        fr_fold = gs.Frame(scene.n, cfg.width, cfg.height, gs.GS_APP_NEURAL_FOLDED, capacity, device=dev)
+        gs.timing_enable(True)
+        gs.timing_reset()
+        st.fold_neural(stream)
+        torch.cuda.synchronize()
+        fold_ms = gs.timing_read()["neural_fold"][0]
+        gs.timing_enable(False)
+        render_only = {"fold_ms": round(fold_ms, 4)}
+        for name, frame in (("neural", fr), ("neural_folded", fr_fold)):
+            for i in range(args.warmup):
+                frame.forward(cstructs[i % ncam], st, stream=stream)
+            torch.cuda.synchronize()
+            t_start = time.perf_counter()
+            for i in range(args.steps):
+                frame.forward(cstructs[i % ncam], st, stream=stream)
+            torch.cuda.synchronize()
+            t_r = (time.perf_counter() - t_start) / args.steps
+            gs.timing_enable(True)
+            gs.timing_reset()
+            for i in range(args.steps):
+                frame.forward(cstructs[i % ncam], st, stream=stream)
+            torch.cuda.synchronize()
+            pre_ms, pre_n = gs.timing_read()["preprocess"]
+            gs.timing_enable(False)
+            pre_ms /= max(pre_n, 1)
+            gbs = algorithmic_bytes("preprocess", scene.n, vis_avg, name) / (pre_ms * 1e-3) / 1e9
+            render_only[name] = {"it_s": round(1.0 / t_r, 3), "ms_per_step": round(1e3 * t_r, 4),
+                                 "preprocess_ms": round(pre_ms, 4), "preprocess_GB_s": round(gbs, 1)}
+        del fr_fold
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(scene, cams, kind, args.cpu_tiles)
@@ -276,6 +311,7 @@ def main():
         "hbm_stages": hbm_all,
         "roofline": roofline,
         "train_step": train,
+        "render_only": render_only,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

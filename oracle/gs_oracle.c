@@ -164,3 +164,118 @@ void orc_mlp_eval(const double* x, int64_t rows, const double* w, double* out, i
         for (int c = 0; c < 3; ++c) out[3 * r + c] = 1.0 / (1.0 + exp(-o[c]));
     }
 }
+
+/* ---- NASG / NASGabor lobe (eq. nasg) ------------------------------------------
+ * The paper takes the kernel from the NASGabor work without restating it; this
+ * is the normalized anisotropic spherical Gaussian of Huang et al. (2024), with
+ * the parametrisation read from the paper's description of the activations:
+ *   frame   cos(theta) = tanh(r0), and the half angles of the azimuth phi and the
+ *           twist gamma have cosines tanh(r1), tanh(r2) (so that phi and gamma
+ *           cover (0, 2 pi)); z = (sin th cos ph, sin th sin ph, cos th),
+ *           e1 = dz/dth, e2 = (-sin ph, cos ph, 0), x = cos ga e1 + sin ga e2,
+ *           y = -sin ga e1 + cos ga e2;
+ *   shape   lambda = exp(clamp(r3, -8, 8)) (sharpness), a = exp(clamp(r4, -8, 8))
+ *           (anisotropy);
+ *   kernel  u = (v.z + 1)/2, rho = (v.x)^2 / ((v.x)^2 + (v.y)^2), psi = a rho,
+ *           G(v) = exp(2 lambda (u^(1+psi) - 1)) u^psi / K,
+ *           K = 2 pi (1 - exp(-2 lambda)) / (lambda sqrt(1 + a)),
+ *           which integrates to 1 over the sphere;
+ *   Gabor   G~(v) = G(v) (1 + cos(omega v.x)) / 2, omega = 20 (tanh(r5) + 1),
+ *           a non-negative cosine carrier along the anisotropy axis.
+ * raw[0..4] (and raw[5] with gabor) are the raw lobe parameters. The frame is
+ * evaluated with sin(theta) = sech(r0), sin(phi/2) = sech(r1), sin(gamma/2) = sech(r2).
+ */
+typedef struct lobe_frame {
+    double x[3], y[3], z[3], e1[3], e2[3], e3[3];
+    double ct, st, cg, sg, sh1, sh2, lam, an, om, dlam, dan, dom;
+} lobe_frame;
+
+static double dot3(const double a[3], const double b[3]) { return a[0] * b[0] + a[1] * b[1] + a[2] * b[2]; }
+
+static double clampd(double v, double lo, double hi) { return v < lo ? lo : v > hi ? hi : v; }
+
+static void lobe_setup(const double* raw, int gabor, lobe_frame* f)
+{
+    const double ct = tanh(raw[0]), st = 1.0 / cosh(raw[0]);
+    const double ch = tanh(raw[1]), sh = 1.0 / cosh(raw[1]);
+    const double cgh = tanh(raw[2]), sgh = 1.0 / cosh(raw[2]);
+    const double cp = ch * ch - sh * sh, sp = 2.0 * sh * ch;      /* phi = 2 (phi/2) */
+    const double cg = cgh * cgh - sgh * sgh, sg = 2.0 * sgh * cgh;
+    f->ct = ct; f->st = st; f->cg = cg; f->sg = sg; f->sh1 = sh; f->sh2 = sgh;
+    const double z[3] = {st * cp, st * sp, ct}, e1[3] = {ct * cp, ct * sp, -st}, e2[3] = {-sp, cp, 0.0};
+    const double e3[3] = {-cp, -sp, 0.0};
+    for (int j = 0; j < 3; ++j) {
+        f->z[j] = z[j]; f->e1[j] = e1[j]; f->e2[j] = e2[j]; f->e3[j] = e3[j];
+        f->x[j] = cg * e1[j] + sg * e2[j];
+        f->y[j] = -sg * e1[j] + cg * e2[j];
+    }
+    f->lam = exp(clampd(raw[3], -8.0, 8.0));
+    f->an = exp(clampd(raw[4], -8.0, 8.0));
+    f->dlam = (raw[3] > -8.0 && raw[3] < 8.0) ? f->lam : 0.0;
+    f->dan = (raw[4] > -8.0 && raw[4] < 8.0) ? f->an : 0.0;
+    f->om = gabor ? 20.0 * (tanh(raw[5]) + 1.0) : 0.0;
+    f->dom = gabor ? 20.0 * (1.0 - tanh(raw[5]) * tanh(raw[5])) : 0.0;
+}
+
+double orc_lobe_eval(const double* raw, int32_t gabor, const double v[3])
+{
+    lobe_frame f;
+    lobe_setup(raw, gabor, &f);
+    const double px = dot3(v, f.x), py = dot3(v, f.y), pz = dot3(v, f.z);
+    const double u = (pz + 1.0) / 2.0, q = px * px + py * py;
+    const double psi = f.an * (q > 0 ? px * px / q : 0.0);
+    const double K = 2.0 * M_PI * (-expm1(-2.0 * f.lam)) / (f.lam * sqrt(1.0 + f.an));
+    double G = exp(2.0 * f.lam * (pow(u, 1.0 + psi) - 1.0)) * pow(u, psi) / K;
+    if (gabor) G *= (1.0 + cos(f.om * px)) / 2.0;
+    return G;
+}
+
+void orc_lobe_eval_many(const double* raw, int32_t gabor, int64_t m, const double* v, double* out)
+{
+    for (int64_t k = 0; k < m; ++k) out[k] = orc_lobe_eval(raw, gabor, v + 3 * k);
+}
+
+/* dG/draw (5 or 6 values) and dG/dv of the lobe above, by the chain rule through
+ * the frame: d theta/dr0 = -sin th, d phi/dr1 = -2 sin(phi/2), d gamma/dr2 =
+ * -2 sin(gamma/2); dz/dth = e1, dz/dph = sin th e2, dx/dth = -cos ga z,
+ * dx/dph = cos ga cos th e2 + sin ga e3, dx/dga = y, dy/dth = sin ga z,
+ * dy/dph = -sin ga cos th e2 + cos ga e3, dy/dga = -x, e3 = de2/dph. */
+double orc_lobe_grad(const double* raw, int32_t gabor, const double v[3], double* draw, double dv[3])
+{
+    lobe_frame f;
+    lobe_setup(raw, gabor, &f);
+    const double px = dot3(v, f.x), py = dot3(v, f.y), pz = dot3(v, f.z);
+    const double u = (pz + 1.0) / 2.0, q = px * px + py * py;
+    const double rho = q > 0 ? px * px / q : 0.0;
+    const double psi = f.an * rho;
+    const double em = -expm1(-2.0 * f.lam);
+    const double K = 2.0 * M_PI * em / (f.lam * sqrt(1.0 + f.an));
+    const double w = pow(u, 1.0 + psi), L = log(u);
+    const double G0 = exp(2.0 * f.lam * (w - 1.0)) * pow(u, psi) / K;
+    const double C = gabor ? (1.0 + cos(f.om * px)) / 2.0 : 1.0;
+    /* partial derivatives of G0 */
+    const double dG0_du = G0 * (2.0 * f.lam * (1.0 + psi) * pow(u, psi) + psi / u);
+    const double dG0_dpsi = G0 * (2.0 * f.lam * w * L + L);
+    const double dlnK_dlam = 2.0 * exp(-2.0 * f.lam) / em - 1.0 / f.lam;
+    const double dG0_dlam = G0 * (2.0 * (w - 1.0) - dlnK_dlam);
+    const double dG0_da = G0 / (2.0 * (1.0 + f.an)) + dG0_dpsi * rho;
+    const double drho_dpx = q > 0 ? 2.0 * px * py * py / (q * q) : 0.0;
+    const double drho_dpy = q > 0 ? -2.0 * py * px * px / (q * q) : 0.0;
+    const double dC_dpx = gabor ? -f.om * sin(f.om * px) / 2.0 : 0.0;
+    const double dC_dom = gabor ? -px * sin(f.om * px) / 2.0 : 0.0;
+    const double Dz = C * dG0_du * 0.5;
+    const double Dx = C * dG0_dpsi * f.an * drho_dpx + G0 * dC_dpx;
+    const double Dy = C * dG0_dpsi * f.an * drho_dpy;
+    const double ve1 = dot3(v, f.e1), ve2 = dot3(v, f.e2), ve3 = dot3(v, f.e3);
+    const double dth = Dz * ve1 + Dx * (-f.cg * pz) + Dy * (f.sg * pz);
+    const double dph = Dz * f.st * ve2 + Dx * (f.cg * f.ct * ve2 + f.sg * ve3) + Dy * (-f.sg * f.ct * ve2 + f.cg * ve3);
+    const double dga = Dx * py - Dy * px;
+    draw[0] = dth * (-f.st);
+    draw[1] = dph * (-2.0 * f.sh1);
+    draw[2] = dga * (-2.0 * f.sh2);
+    draw[3] = C * dG0_dlam * f.dlam;
+    draw[4] = C * dG0_da * f.dan;
+    if (gabor) draw[5] = G0 * dC_dom * f.dom;
+    for (int j = 0; j < 3; ++j) dv[j] = Dz * f.z[j] + Dx * f.x[j] + Dy * f.y[j];
+    return G0 * C;
+}

@@ -47,7 +47,8 @@ typedef struct orc_camera {
     double bg[3];
 } orc_camera;
 
-enum { ORC_APP_SH3 = 0, ORC_APP_LATENT_MLP = 1, ORC_APP_NEURAL = 2, ORC_APP_NEURAL_FOLDED = 3 };
+enum { ORC_APP_SH3 = 0, ORC_APP_LATENT_MLP = 1, ORC_APP_NEURAL = 2, ORC_APP_NEURAL_FOLDED = 3, ORC_APP_NASG = 4,
+       ORC_APP_NASGABOR = 5 };
 
 /* flags written per Gaussian by the preprocess */
 enum {
@@ -76,6 +77,9 @@ typedef struct orc_appearance {
     const double* features;   /* NEURAL: [8][n] values of binary16 numbers */
     const double* preact;     /* NEURAL_FOLDED: [16][n] first-layer pre-activations of the
                                  view-independent inputs (oracle.neural_fold); render only */
+    const double* lobes;      /* NASG: [8][n] raw frame angles (3), sharpness, anisotropy and
+                                 the three raw amplitudes; NASGABOR: [9][n], the frequency last.
+                                 base_color is the base colour c0 of both */
 } orc_appearance;
 
 /* Outputs of the preprocess. Entries of culled Gaussians are zero. */
@@ -105,6 +109,7 @@ typedef struct orc_grads {
     double* dcolor;         /* [3][n] or NULL */
     double* dbase_color;    /* [3][n] (neural) or NULL */
     double* dfeatures;      /* [8][n] (neural) or NULL */
+    double* dlobes;         /* [8][n] (NASG), [9][n] (NASGabor) or NULL */
 } orc_grads;
 
 int orc_preprocess_f32(const orc_camera* cam, int64_t n, const double* means, const double* log_scales,
@@ -148,6 +153,14 @@ void orc_sh_basis(const double d[3], double Y[16], double dY[48]);
 void orc_mlp_eval(const double* x, int64_t rows, const double* w, double* out, int32_t half_act);
 /* Round to the nearest binary16 value (ties to even), returned as a double. */
 double orc_round_half(double x);
+
+/* One NASG (gabor = 0) or NASGabor (gabor = 1) lobe kernel at unit direction v,
+ * from its 5 (6) raw parameters (frame angles, sharpness, anisotropy[, frequency]);
+ * see gs_oracle.c for the definition. _many evaluates m directions v[m][3]. */
+double orc_lobe_eval(const double* raw, int32_t gabor, const double v[3]);
+void orc_lobe_eval_many(const double* raw, int32_t gabor, int64_t m, const double* v, double* out);
+/* the kernel value, its derivative w.r.t. the raw parameters (draw[5 or 6]) and w.r.t. v */
+double orc_lobe_grad(const double* raw, int32_t gabor, const double v[3], double* draw, double dv[3]);
 
 #ifdef __cplusplus
 }

@@ -27,6 +27,8 @@ APP_SH3 = 0
 APP_LATENT_MLP = 1
 APP_NEURAL = 2
 APP_NEURAL_FOLDED = 3     # render only
+APP_NASG = 4
+APP_NASGABOR = 5
 VISIBLE = 1
 CLAMP_X = 2
 CLAMP_Y = 4
@@ -58,7 +60,7 @@ class _Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p),
                 ("latent", C.c_void_p), ("mlp_w", C.c_void_p), ("dir_exact", C.c_int32),
                 ("half_act", C.c_int32), ("base_color", C.c_void_p), ("features", C.c_void_p),
-                ("preact", C.c_void_p)]
+                ("preact", C.c_void_p), ("lobes", C.c_void_p)]
 
 
 class _Pre(C.Structure):
@@ -70,7 +72,7 @@ class _Pre(C.Structure):
 class _Grads(C.Structure):
     _fields_ = [(name, C.c_void_p) for name in (
         "dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh", "dlatent", "dmlp_w",
-        "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color", "dfeatures")]
+        "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color", "dfeatures", "dlobes")]
 
 
 _lib = None
@@ -100,6 +102,10 @@ def lib():
         _lib.orc_mlp_eval.restype = None
         _lib.orc_round_half.argtypes = [C.c_double]
         _lib.orc_round_half.restype = C.c_double
+        _lib.orc_lobe_eval_many.argtypes = [vp, C.c_int32, i64, vp, vp]
+        _lib.orc_lobe_eval_many.restype = None
+        _lib.orc_lobe_grad.argtypes = [vp, C.c_int32, vp, vp, vp]
+        _lib.orc_lobe_grad.restype = C.c_double
     return _lib
 
 
@@ -145,15 +151,21 @@ class _SceneArrays:
         self.sh = _f64(scene.sh) if kind == APP_SH3 else None
         self.latent = half_to_f64(scene.latent) if kind == APP_LATENT_MLP else None
         neural = kind in (APP_NEURAL, APP_NEURAL_FOLDED)
+        lobe = kind in (APP_NASG, APP_NASGABOR)
         self.mlp_w = (half_to_f64(scene.mlp_w) if kind == APP_LATENT_MLP else
                       half_to_f64(scene.neural_w) if neural else None)
-        self.base_color = _f64(scene.base_color) if neural else None
+        self.base_color = _f64(scene.base_color) if neural or lobe else None
+        self.lobes = None
+        if lobe:
+            self.lobes = _f64(scene.lobes_gabor if kind == APP_NASGABOR else scene.lobes)
+            assert self.lobes.shape[0] == (9 if kind == APP_NASGABOR else 8)
         self.features = half_to_f64(scene.features) if kind == APP_NEURAL else None
         # the folded form: pre-activations exact with exact inputs, else binary16 like its inputs
         self.preact = (np.ascontiguousarray(neural_fold(scene.features, scene.neural_w, exact=dir_exact))
                        if kind == APP_NEURAL_FOLDED else None)
         self.app = _Appearance(kind, sh_degree, _p(self.sh), _p(self.latent), _p(self.mlp_w), int(dir_exact),
-                               int(half_act), _p(self.base_color), _p(self.features), _p(self.preact))
+                               int(half_act), _p(self.base_color), _p(self.features), _p(self.preact),
+                               _p(self.lobes))
 
 
 def neural_fold(features, neural_w, exact: bool = False) -> np.ndarray:
@@ -185,6 +197,10 @@ def _kind_of(kind) -> int:
         return APP_NEURAL
     if kind in ("neural_folded", APP_NEURAL_FOLDED):
         return APP_NEURAL_FOLDED
+    if kind in ("nasg", APP_NASG):
+        return APP_NASG
+    if kind in ("nasgabor", APP_NASGABOR):
+        return APP_NASGABOR
     raise ValueError(kind)
 
 
@@ -261,11 +277,12 @@ def render_bwd(cam, scene, pre: Preprocessed, ranges, values, dL_dimage, kind="s
              dlatent=np.zeros((14, n)) if kind == APP_LATENT_MLP else None,
              dmlp_w=(np.zeros(1664) if kind == APP_LATENT_MLP else np.zeros(816) if kind == APP_NEURAL else None),
              dmean2d=np.zeros((2, n)), dconic=np.zeros((3, n)), dopacity=np.zeros(n), dcolor=np.zeros((3, n)),
-             dbase_color=np.zeros((3, n)) if kind == APP_NEURAL else None,
-             dfeatures=np.zeros((8, n)) if kind == APP_NEURAL else None)
+             dbase_color=np.zeros((3, n)) if kind in (APP_NEURAL, APP_NASG, APP_NASGABOR) else None,
+             dfeatures=np.zeros((8, n)) if kind == APP_NEURAL else None,
+             dlobes=np.zeros((9 if kind == APP_NASGABOR else 8, n)) if kind in (APP_NASG, APP_NASGABOR) else None)
     gs = _Grads(*[_p(g[k]) for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh", "dlatent",
                                       "dmlp_w", "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color",
-                                      "dfeatures")])
+                                      "dfeatures", "dlobes")])
     dimg = _f64(dL_dimage)
     ranges = np.ascontiguousarray(ranges, dtype=np.int64)
     values = np.ascontiguousarray(values, dtype=np.int32)
@@ -304,6 +321,26 @@ def mlp_eval(x, mlp_w, half_act: bool = False) -> np.ndarray:
     out = np.zeros((xx.shape[0], 3))
     lib().orc_mlp_eval(_p(np.ascontiguousarray(xx)), xx.shape[0], _p(w), _p(out), int(half_act))
     return out
+
+
+def lobe_eval(raw, gabor: bool, dirs) -> np.ndarray:
+    """NASG (NASGabor) lobe kernel values at unit directions dirs [m][3] for the raw
+    parameters raw[5] (raw[6]): frame angles, sharpness, anisotropy[, frequency]."""
+    r = _f64(np.asarray(raw, np.float64).ravel())
+    v = np.ascontiguousarray(np.asarray(dirs, np.float64).reshape(-1, 3))
+    out = np.zeros(v.shape[0])
+    lib().orc_lobe_eval_many(_p(r), int(gabor), v.shape[0], _p(v), _p(out))
+    return out
+
+
+def lobe_grad(raw, gabor: bool, d) -> tuple:
+    """(G, dG/draw, dG/dd) of one lobe at one direction."""
+    r = _f64(np.asarray(raw, np.float64).ravel())
+    v = _f64(np.asarray(d, np.float64).ravel())
+    dr = np.zeros(6)
+    dv = np.zeros(3)
+    G = lib().orc_lobe_grad(_p(r), int(gabor), _p(v), _p(dr), _p(dv))
+    return G, dr[: 6 if gabor else 5], dv
 
 
 def round_half(x: float) -> float:

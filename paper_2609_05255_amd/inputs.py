@@ -19,6 +19,9 @@ Layouts (all planar, channel-major, C-contiguous numpy arrays):
   base_color     float32 [3][n]   neural appearance: base colour c0
   features       uint16  [8][n]   neural appearance: binary16 features
   neural_w       uint16  [816]    binary16 W1[16][32], W2[16][16], W3[3][16]
+  lobes          float32 [8][n]   NASG lobe: raw frame angles (3), raw sharpness,
+                                  raw anisotropy, raw amplitudes (3)
+  lobes_gabor    float32 [9][n]   NASGabor: the same rows, then the raw frequency
 """
 from __future__ import annotations
 
@@ -54,7 +57,7 @@ class Config:
     means: str            # "uniform1" (U[-1,1]^3) or "normal0.6" (N(0, 0.6^2 I))
     log_scale_mu: float
     log_scale_sigma: float
-    appearance: tuple     # subset of ("sh3", "latent", "neural")
+    appearance: tuple     # subset of ("sh3", "latent", "neural", "nasg", "nasgabor")
     fixed_camera: bool = False
 
 
@@ -67,6 +70,8 @@ CONFIGS = {
     "paper_latent": Config("paper_latent", 3_000_000, 1600, 1064, 16, "normal0.6", -5.0, 0.6, ("latent",)),
     "stress": Config("stress", 6_000_000, 1920, 1080, 16, "normal0.6", -5.5, 0.7, ("sh3", "latent")),
     "paper_neural": Config("paper_neural", 3_000_000, 1600, 1064, 16, "normal0.6", -5.0, 0.6, ("neural",)),
+    "paper_nasg": Config("paper_nasg", 3_000_000, 1600, 1064, 16, "normal0.6", -5.0, 0.6, ("nasg",)),
+    "paper_nasgabor": Config("paper_nasgabor", 3_000_000, 1600, 1064, 16, "normal0.6", -5.0, 0.6, ("nasgabor",)),
 }
 
 
@@ -88,6 +93,8 @@ class Scene:
     base_color: np.ndarray | None = None
     features: np.ndarray | None = None
     neural_w: np.ndarray | None = None
+    lobes: np.ndarray | None = None
+    lobes_gabor: np.ndarray | None = None
 
     def subset(self, idx: np.ndarray) -> "Scene":
         idx = np.asarray(idx)
@@ -95,7 +102,8 @@ class Scene:
         copy = lambda a: None if a is None else a.copy()
         return Scene(len(idx), pick(self.means), pick(self.log_scales), pick(self.quats),
                      np.ascontiguousarray(self.opacity_logits[idx]), pick(self.sh), pick(self.latent),
-                     copy(self.mlp_w), pick(self.base_color), pick(self.features), copy(self.neural_w))
+                     copy(self.mlp_w), pick(self.base_color), pick(self.features), copy(self.neural_w),
+                     pick(self.lobes), pick(self.lobes_gabor))
 
 
 def make_scene(cfg: Config | str, seed: int = SCENE_SEED, n: int | None = None,
@@ -126,6 +134,18 @@ def make_scene(cfg: Config | str, seed: int = SCENE_SEED, n: int | None = None,
         z = (_rng(seed, 7).standard_normal((LATENT_DIM, n), dtype=f32) * f32(0.5))
         scene.latent = np.ascontiguousarray(z.astype(np.float16).view(np.uint16))
         scene.mlp_w = make_mlp_weights(seed)
+    if "nasg" in appearance or "nasgabor" in appearance:
+        # base colour as for the neural model; lobe raw values: frame angles N(0, 1),
+        # sharpness exp(N(1, 0.5)), anisotropy exp(N(-0.5, 0.7)), amplitudes N(0.5, 0.3)
+        # (the reference initialises them at 0.5), frequency 20 (tanh(N(-1.5, 0.5)) + 1)
+        dc = (_rng(seed, 6).standard_normal((3, n), dtype=f32) * f32(0.2) + f32(0.5)).astype(f32)
+        scene.base_color = np.ascontiguousarray((dc * f32(Y0)).astype(f32))
+        z = _rng(seed, 11).standard_normal((9, n), dtype=f32)
+        mu = np.array([0, 0, 0, 1.0, -0.5, 0.5, 0.5, 0.5, -1.5], f32)[:, None]
+        sd = np.array([1, 1, 1, 0.5, 0.7, 0.3, 0.3, 0.3, 0.5], f32)[:, None]
+        lobes = (z * sd + mu).astype(f32)
+        scene.lobes = np.ascontiguousarray(lobes[:8])
+        scene.lobes_gabor = np.ascontiguousarray(lobes)
     if "neural" in appearance:
         # base colour: the SH3 scenes' degree-0 colour with Y0 folded in (c0 = Y0 sh_0);
         # features N(0, 1) in binary16; all three layers Glorot (a non-zero residual)

@@ -1,8 +1,9 @@
 """Finite-difference pins of the oracle's backward pass (fp64 build).
 
 The loss is sum(g * image) for a fixed upstream gradient g; every parameter
-(means, log-scales, quaternions, opacity logits, SH coefficients, latents and
-decoder weights) is perturbed by +-h and the central difference is compared
+(means, log-scales, quaternions, opacity logits, SH coefficients, latents,
+decoder weights, base colours, features and lobe parameters) is perturbed by
++-h and the central difference is compared
 with the analytic gradient. A coordinate is skipped only if a discrete decision
 changes between x-h and x+h (tile rectangle, culling, guard-band clamp, colour
 or hidden-unit ReLU mask, last contributor of any pixel): the rendered image is
@@ -25,7 +26,8 @@ def fd_scene(rng, n, kind):
     logits = rng.normal(0.0, 1.0, size=n)
     logits[0] = 5.5                                  # alpha reaches the 0.99 cap near its centre
     sc = SimpleNamespace(n=n, means=means, log_scales=ls, quats=q, opacity_logits=logits,
-                         sh=None, latent=None, mlp_w=None, base_color=None, features=None, neural_w=None)
+                         sh=None, latent=None, mlp_w=None, base_color=None, features=None, neural_w=None,
+                         lobes=None, lobes_gabor=None)
     # one large Gaussian beyond the guard band on x, its footprint still on screen
     sc.means[:, 1] = [-2.8, 0.1, 0.0]
     sc.log_scales[:, 1] = [-0.2, -0.5, -0.4]
@@ -36,6 +38,14 @@ def fd_scene(rng, n, kind):
         sc.latent = rng.normal(0.0, 0.5, size=(14, n))
         w = inputs.make_mlp_weights(3).view(np.float16).astype(np.float64) * 2.0
         sc.mlp_w = w
+    elif kind in ("nasg", "nasgabor"):
+        sc.base_color = rng.normal(0.1, 0.5, size=(3, n))    # some colours clamp at 0
+        lob = rng.normal(0.0, 1.0, size=(9, n))
+        lob[3] = rng.normal(1.0, 0.5, size=n)               # sharpness exp(r3)
+        lob[4] = rng.normal(-0.5, 0.7, size=n)              # anisotropy exp(r4)
+        lob[5:8] = rng.normal(0.5, 0.8, size=(3, n))        # amplitudes
+        lob[8] = rng.normal(-1.0, 0.5, size=n)              # frequency
+        sc.lobes, sc.lobes_gabor = lob[:8].copy(), lob
     else:
         sc.base_color = rng.normal(0.1, 0.5, size=(3, n))    # some colours clamp at 0
         sc.features = rng.normal(0.0, 1.5, size=(8, n))
@@ -56,15 +66,18 @@ def run(orc, cam, sc, kind, g):
 
 FIELDS = {"sh3": ["means", "log_scales", "quats", "opacity_logits", "sh"],
           "latent": ["means", "log_scales", "quats", "opacity_logits", "latent", "mlp_w"],
-          "neural": ["means", "log_scales", "quats", "opacity_logits", "base_color", "features", "neural_w"]}
+          "neural": ["means", "log_scales", "quats", "opacity_logits", "base_color", "features", "neural_w"],
+          "nasg": ["means", "log_scales", "quats", "opacity_logits", "base_color", "lobes"],
+          "nasgabor": ["means", "log_scales", "quats", "opacity_logits", "base_color", "lobes_gabor"]}
 GRAD_NAME = {"means": "dmeans", "log_scales": "dlog_scales", "quats": "dquats",
              "opacity_logits": "dopacity_logits", "sh": "dsh", "latent": "dlatent", "mlp_w": "dmlp_w",
-             "base_color": "dbase_color", "features": "dfeatures", "neural_w": "dmlp_w"}
+             "base_color": "dbase_color", "features": "dfeatures", "neural_w": "dmlp_w", "lobes": "dlobes",
+             "lobes_gabor": "dlobes"}
 
 
-@pytest.mark.parametrize("kind", ["sh3", "latent", "neural"])
+@pytest.mark.parametrize("kind", ["sh3", "latent", "neural", "nasg", "nasgabor"])
 def test_gradients_match_finite_differences(orc, kind):
-    rng = np.random.default_rng({"sh3": 42, "latent": 43, "neural": 44}[kind])
+    rng = np.random.default_rng({"sh3": 42, "latent": 43, "neural": 44, "nasg": 45, "nasgabor": 46}[kind])
     n = 10
     sc = fd_scene(rng, n, kind)
     cam = inputs.look_at_camera([0.3, -0.4, -2.9], 40, 36, bg=(0.2, 0.3, 0.1))

@@ -91,6 +91,16 @@ enum {
                                  pre-activations p (gs_neural_fold); per view only
                                  h1 = relu(p + W1[:, 1..15] Y_1..15(d)) is evaluated, the rest
                                  as NEURAL. gs_render_bwd rejects this kind. */
+    GS_APP_NASG = 4,          /* eq. nasg with one lobe: c = max(0, c0 + G(d) tanh(amp) + 0.5), G the
+                                 normalized anisotropic spherical Gaussian (unit integral over the
+                                 sphere): frame from three raw angles (cos th = tanh r0, the half
+                                 azimuth and half twist of cosines tanh r1, tanh r2), sharpness
+                                 exp(clamp(r3, -8, 8)), anisotropy exp(clamp(r4, -8, 8));
+                                 G = exp(2 lam (u^(1+psi) - 1)) u^psi / K, u = (d.z + 1)/2,
+                                 psi = a (d.x)^2 / ((d.x)^2 + (d.y)^2),
+                                 K = 2 pi (1 - exp(-2 lam)) / (lam sqrt(1 + a)) */
+    GS_APP_NASGABOR = 5,      /* NASG times the carrier (1 + cos(omega d.x)) / 2,
+                                 omega = 20 (tanh(r5) + 1) */
 };
 
 #define GS_NEURAL_FEATURES 8  /* binary16 features per Gaussian (16 B) beside a 12 B fp32 base colour */
@@ -118,6 +128,10 @@ typedef struct gs_appearance {
     const uint16_t* preact;   /* NEURAL_FOLDED: [n][16] binary16 bit patterns, Gaussian-major
                                  (32 B per Gaussian), as gs_neural_fold writes them;
                                  base_color and mlp_w (the 816 NEURAL weights) as for NEURAL */
+    const float* lobes;       /* NASG: [8][n] fp32 raw r0..r4 then the three raw amplitudes;
+                                 NASGABOR: [9][n], the raw frequency r5 last. base_color [3][n]
+                                 is c0; sh_degree 0 turns the lobe off (c = max(0, c0 + 0.5)),
+                                 1..3 on (the paper's schedule) */
 } gs_appearance;
 
 /* Screen-space record of one Gaussian, written by gs_preprocess (64 bytes).
@@ -158,8 +172,9 @@ typedef struct gs_grads {
     float* dlatent;           /* LATENT_MLP: [14][n] fp32 */
     float* dmlp_w;            /* LATENT_MLP: [1664], NEURAL: [816] fp32, same order as mlp_w */
     float* dmean2d;           /* optional (may be NULL): [2][n] screen-space mean gradient */
-    float* dbase_color;       /* NEURAL: [3][n] */
+    float* dbase_color;       /* NEURAL, NASG, NASGABOR: [3][n] */
     float* dfeatures;         /* NEURAL: [8][n] fp32 (the gradient passes the binary16 storage) */
+    float* dlobes;            /* NASG: [8][n], NASGABOR: [9][n], rows as in gs_appearance.lobes */
 } gs_grads;
 
 /*

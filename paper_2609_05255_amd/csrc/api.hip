@@ -89,6 +89,10 @@ gs_status check_appearance(const gs_appearance* a, int64_t n)
         GS_CHECK(n == 0 || a->sh_degree == 0 || (a->preact != nullptr && a->mlp_w != nullptr),
                  "preact or mlp_w is NULL");
         GS_CHECK(((uintptr_t)a->preact & 7) == 0, "preact must be 8-byte aligned");
+    } else if (a->kind == GS_APP_NASG || a->kind == GS_APP_NASGABOR) {
+        GS_CHECK(a->sh_degree >= 0 && a->sh_degree <= 3, "sh_degree %d outside 0..3", a->sh_degree);
+        GS_CHECK(n == 0 || a->base_color != nullptr, "base_color is NULL");
+        GS_CHECK(n == 0 || a->sh_degree == 0 || a->lobes != nullptr, "lobes is NULL");
     } else {
         return fail(GS_ERR_INVALID_ARG, "unknown appearance kind %d", a->kind);
     }
@@ -254,7 +258,7 @@ gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t c
     GS_CHECK(n >= 0 && n < ((int64_t)1 << 31), "n out of range");
     GS_CHECK(width > 0 && height > 0, "image size must be positive");
     GS_CHECK(capacity < ((uint64_t)1 << 32), "capacity must be below 2^32");
-    GS_CHECK(kind >= GS_APP_SH3 && kind <= GS_APP_NEURAL_FOLDED, "unknown appearance kind %d", kind);
+    GS_CHECK(kind >= GS_APP_SH3 && kind <= GS_APP_NASGABOR, "unknown appearance kind %d", kind);
     *bytes = layout_workspace(nullptr, n, capacity, kind).bytes;
     return ok();
 }
@@ -383,6 +387,8 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
         else if (app->kind == GS_APP_NEURAL)
             GS_CHECK(grads->dbase_color && grads->dfeatures && grads->dmlp_w,
                      "dbase_color, dfeatures or dmlp_w is NULL");
+        else if (app->kind == GS_APP_NASG || app->kind == GS_APP_NASGABOR)
+            GS_CHECK(grads->dbase_color && grads->dlobes, "dbase_color or dlobes is NULL");
         else GS_CHECK(grads->dlatent && grads->dmlp_w, "dlatent or dmlp_w is NULL");
     }
     const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind);

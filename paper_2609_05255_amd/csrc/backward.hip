@@ -7,6 +7,7 @@
 // of culled Gaussians are written as zeros, so every output is dense.
 #include "gs_internal.h"
 #include "mlp.h"
+#include "lobe.h"
 #include "neural.h"
 #include "sh.h"
 
@@ -39,6 +40,8 @@ struct BwdArgs {
     float* dmean2d;
     float* dbase_color;
     float* dfeatures;
+    const float* lobes;
+    float* dlobes;
 };
 
 struct GeoGrad {
@@ -213,6 +216,72 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
         const bool on = k < nb;
         for (int c = 0; c < 3; ++c) a.dsh[(3 * k + c) * n + i] = on ? Y[k] * gc[c] : 0.f;
     }
+    for (int j = 0; j < 3; ++j) { a.dmeans[j * n + i] = gg.dmu[j]; a.dlog_scales[j * n + i] = gg.dls[j]; }
+    for (int j = 0; j < 4; ++j) a.dquats[j * n + i] = gg.dq[j];
+    a.dlogits[i] = gg.dlogit;
+    if (a.dmean2d) { a.dmean2d[i] = g9[0]; a.dmean2d[n + i] = g9[1]; }
+}
+
+// NASG / NASGabor backward (eq. nasg, lobe.h): geometry as for SH3; the colour
+// gradient g (zero where the ReLU clamps) gives dc0 = g, d amp = g G (1 - tanh^2),
+// and (g . tanh(amp)) times the kernel's gradient for the raw lobe parameters
+// and the view direction (chained into the mean). Culled Gaussians and an
+// inactive lobe get zeros.
+template <bool kGabor>
+__global__ __launch_bounds__(kBlock) void k_preprocess_bwd_lobe(BwdArgs a)
+{
+    constexpr int kRows = kGabor ? 9 : 8;
+    const int i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= a.n) return;
+    const int64_t n = a.n;
+    const bool vis = a.tiles_touched[i] != 0;
+    GeoGrad gg;
+    for (int j = 0; j < 3; ++j) { gg.dmu[j] = 0.f; gg.dls[j] = 0.f; }
+    for (int j = 0; j < 4; ++j) gg.dq[j] = 0.f;
+    gg.dlogit = 0.f;
+    float g9[kAccStride];
+    for (int k = 0; k < kAccStride; ++k) g9[k] = 0.f;
+    float gc[3] = {0.f, 0.f, 0.f}, dl[kRows];
+    for (int k = 0; k < kRows; ++k) dl[k] = 0.f;
+    if (vis) {
+        float mu[3], ls[3], q[4], c0[3];
+        for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
+        for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
+        for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
+        for (int c = 0; c < 3; ++c) c0[c] = a.base_color[c * n + i];
+        const float* ap = a.acc + (size_t)i * kAccStride;
+        for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+        geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
+        if (a.sh_degree >= 1) {
+            float r[6], T[3];
+            for (int k = 0; k < 5; ++k) r[k] = a.lobes[k * n + i];
+            for (int c = 0; c < 3; ++c) T[c] = tanhf(a.lobes[(5 + c) * n + i]);
+            r[5] = kGabor ? a.lobes[8 * n + i] : 0.f;
+            const float vx = mu[0] - a.cam.campos[0], vy = mu[1] - a.cam.campos[1], vz = mu[2] - a.cam.campos[2];
+            const float len = sqrtf(vx * vx + vy * vy + vz * vz);
+            const float il = 1.f / len;
+            const float d[3] = {vx * il, vy * il, vz * il};
+            LobeEval f;
+            lobe_setup<kGabor>(r, f);
+            float draw[6], dd[3];
+            const float G = lobe_grad<kGabor>(f, d, draw, dd);
+            float sgt = 0.f;
+            for (int c = 0; c < 3; ++c) {
+                gc[c] = c0[c] + G * T[c] + 0.5f > 0.f ? g9[6 + c] : 0.f;
+                sgt += gc[c] * T[c];
+                dl[5 + c] = gc[c] * G * (1.f - T[c] * T[c]);
+            }
+            for (int k = 0; k < 5; ++k) dl[k] = sgt * draw[k];
+            if (kGabor) dl[8] = sgt * draw[5];
+            // d = v / |v|: dv = (dd - d (d . dd)) / |v|
+            const float dot = d[0] * dd[0] + d[1] * dd[1] + d[2] * dd[2];
+            for (int j = 0; j < 3; ++j) gg.dmu[j] += sgt * (dd[j] - d[j] * dot) * il;
+        } else {
+            for (int c = 0; c < 3; ++c) gc[c] = c0[c] + 0.5f > 0.f ? g9[6 + c] : 0.f;
+        }
+    }
+    for (int c = 0; c < 3; ++c) a.dbase_color[c * n + i] = gc[c];
+    for (int k = 0; k < kRows; ++k) a.dlobes[k * n + i] = dl[k];
     for (int j = 0; j < 3; ++j) { a.dmeans[j * n + i] = gg.dmu[j]; a.dlog_scales[j * n + i] = gg.dls[j]; }
     for (int j = 0; j < 4; ++j) a.dquats[j * n + i] = gg.dq[j];
     a.dlogits[i] = gg.dlogit;
@@ -528,8 +597,14 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
     a.dmean2d = gr.dmean2d;
     a.dbase_color = gr.dbase_color;
     a.dfeatures = gr.dfeatures;
+    a.lobes = app.lobes;
+    a.dlobes = gr.dlobes;
     if (app.kind == GS_APP_SH3)
         hipLaunchKernelGGL(k_preprocess_bwd_sh3, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
+    else if (app.kind == GS_APP_NASG)
+        hipLaunchKernelGGL(k_preprocess_bwd_lobe<false>, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
+    else if (app.kind == GS_APP_NASGABOR)
+        hipLaunchKernelGGL(k_preprocess_bwd_lobe<true>, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NEURAL)
         hipLaunchKernelGGL(k_preprocess_bwd_neural, dim3(latent_bwd_grid(g.n)), dim3(kBlock), 0, s, a);
     else

@@ -8,6 +8,7 @@
 // and they must not depend on which multiply-adds the compiler fuses.
 #include "gs_internal.h"
 #include "mlp.h"
+#include "lobe.h"
 #include "neural.h"
 #include "sh.h"
 
@@ -137,6 +138,7 @@ struct PreArgs {
     const float* base_color;
     const uint16_t* features;
     const uint16_t* preact;
+    const float* lobes;
     gs_splat* splats;
     uint32_t* tiles_touched;
     uint32_t* depth_key;
@@ -281,6 +283,58 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
             float d[3];
             view_dir(a.cam, mu, d);
             sh_color<kDeg>(a.sh, a.n, i, d, col);
+            tiles = g.tiles;
+        }
+        a.tiles_touched[i] = tiles;
+        a.depth_key[i] = g.visible ? __float_as_uint(g.depth) : 0xFFFFFFFFu;
+    }
+    store_splats_wave(a.splats, a.n, (int64_t)i - __lane_id(), stage[threadIdx.x >> 6], g, col);
+    const uint32_t total = block_sum_u32(tiles, red);
+    if (threadIdx.x == 0) a.block_pairs[blockIdx.x] = total;
+}
+
+// NASG / NASGabor (eq. nasg, lobe.h): one thread per Gaussian, colour
+// max(0, c0 + G(d) tanh(amplitude) + 0.5), or max(0, c0 + 0.5) while the
+// active degree is 0; a culled Gaussian reads no appearance.
+template <bool kGabor>
+__global__ __launch_bounds__(kBlock) void k_preprocess_lobe(PreArgs a)
+{
+    __shared__ uint32_t red[4];
+    __shared__ SplatStage stage[kBlock / kWave];
+    const int i = blockIdx.x * kBlock + threadIdx.x;
+    uint32_t tiles = 0;
+    Geo g;
+    g.visible = false;
+    float col[3] = {0.f, 0.f, 0.f};
+    if (i < a.n) {
+        float mu[3], ls[3], q[4], logit;
+        load_geometry_params(a, i, mu, ls, q, logit);
+        geometry(a.cam, mu, ls, q, logit, g);
+        if (g.visible) {
+            const int64_t n = a.n;
+            float c0[3], res[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) c0[ch] = a.base_color[ch * n + i];
+            if (a.sh_degree >= 1) {
+                float r[6], amp[3];
+#pragma unroll
+                for (int k = 0; k < 5; ++k) r[k] = a.lobes[k * n + i];
+#pragma unroll
+                for (int ch = 0; ch < 3; ++ch) amp[ch] = a.lobes[(5 + ch) * n + i];
+                r[5] = kGabor ? a.lobes[8 * n + i] : 0.f;
+                float d[3];
+                view_dir(a.cam, mu, d);
+                LobeEval f;
+                lobe_setup<kGabor>(r, f);
+                const float G = lobe_value<kGabor>(f, d);
+#pragma unroll
+                for (int ch = 0; ch < 3; ++ch) res[ch] = G * tanhf(amp[ch]);
+            }
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) {
+                const float v = c0[ch] + res[ch] + 0.5f;
+                col[ch] = v > 0.f ? v : 0.f;
+            }
             tiles = g.tiles;
         }
         a.tiles_touched[i] = tiles;
@@ -462,6 +516,7 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     a.base_color = app.base_color;
     a.features = app.features;
     a.preact = app.preact;
+    a.lobes = app.lobes;
     a.splats = out.splats;
     a.tiles_touched = out.tiles_touched;
     a.depth_key = out.depth_key;
@@ -477,6 +532,10 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     }
     else if (app.kind == GS_APP_NEURAL)
         hipLaunchKernelGGL(k_preprocess_neural<false>, dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0, s, a);
+    else if (app.kind == GS_APP_NASG)
+        hipLaunchKernelGGL(k_preprocess_lobe<false>, dim3(blocks), dim3(kBlock), 0, s, a);
+    else if (app.kind == GS_APP_NASGABOR)
+        hipLaunchKernelGGL(k_preprocess_lobe<true>, dim3(blocks), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NEURAL_FOLDED)
         hipLaunchKernelGGL(k_preprocess_neural<true>, dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0, s, a);
     else
@@ -519,8 +578,9 @@ __global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs
 
 hipError_t launch_pair_count(int64_t n, int32_t kind, const Workspace& ws, uint64_t* num_pairs, hipStream_t s)
 {
-    // the SH3 preprocess leaves one tile sum per workgroup, the latent one per wave
-    const int slots = kind == GS_APP_SH3 ? preprocess_blocks(n) : pair_count_slots(n);
+    // the SH3 and lobe preprocesses leave one tile sum per workgroup, the decoders one per wave
+    const bool per_block = kind == GS_APP_SH3 || kind == GS_APP_NASG || kind == GS_APP_NASGABOR;
+    const int slots = per_block ? preprocess_blocks(n) : pair_count_slots(n);
     hipLaunchKernelGGL(k_pair_count, dim3(1), dim3(1024), 0, s, ws.block_pairs, slots, num_pairs);
     return hipGetLastError();
 }

@@ -20,7 +20,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libgsraster.so")
 
 GS_OK, GS_ERR_INVALID_ARG, GS_ERR_CAPACITY, GS_ERR_DEVICE, GS_ERR_UNSUPPORTED = range(5)
-GS_APP_SH3, GS_APP_LATENT_MLP, GS_APP_NEURAL, GS_APP_NEURAL_FOLDED = 0, 1, 2, 3
+GS_APP_SH3, GS_APP_LATENT_MLP, GS_APP_NEURAL, GS_APP_NEURAL_FOLDED, GS_APP_NASG, GS_APP_NASGABOR = range(6)
+LOBE_ROWS = {GS_APP_NASG: 8, GS_APP_NASGABOR: 9}
 NEURAL_FEATURES = 8
 NEURAL_WEIGHTS = 816
 KERNEL_NAMES = ["preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
@@ -51,7 +52,7 @@ class Gaussians(C.Structure):
 class Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p), ("latent", C.c_void_p),
                 ("mlp_w", C.c_void_p), ("base_color", C.c_void_p), ("features", C.c_void_p),
-                ("preact", C.c_void_p)]
+                ("preact", C.c_void_p), ("lobes", C.c_void_p)]
 
 
 class Preprocessed(C.Structure):
@@ -63,7 +64,7 @@ class Grads(C.Structure):
     _fields_ = [("dmeans", C.c_void_p), ("dlog_scales", C.c_void_p), ("dquats", C.c_void_p),
                 ("dopacity_logits", C.c_void_p), ("dsh", C.c_void_p), ("dlatent", C.c_void_p),
                 ("dmlp_w", C.c_void_p), ("dmean2d", C.c_void_p), ("dbase_color", C.c_void_p),
-                ("dfeatures", C.c_void_p)]
+                ("dfeatures", C.c_void_p), ("dlobes", C.c_void_p)]
 
 
 class AdamTensor(C.Structure):
@@ -159,6 +160,8 @@ class SceneTensors:
         self.features = h16(scene.features) if getattr(scene, "features", None) is not None else None
         self.neural_w = h16(scene.neural_w) if getattr(scene, "neural_w", None) is not None else None
         self.preact = None   # [n][16] binary16 pre-activations of the folded form (fold_neural)
+        self.lobes = f32(scene.lobes) if getattr(scene, "lobes", None) is not None else None
+        self.lobes_gabor = f32(scene.lobes_gabor) if getattr(scene, "lobes_gabor", None) is not None else None
 
     def fold_neural(self, stream=None):
         """Computes the folded form's per-Gaussian pre-activations (gs_neural_fold)."""
@@ -174,13 +177,17 @@ class SceneTensors:
     def appearance(self, kind: int, sh_degree: int = 3) -> Appearance:
         if kind == GS_APP_NEURAL:
             return Appearance(kind, sh_degree, None, None, _ptr(self.neural_w), _ptr(self.base_color),
-                              _ptr(self.features), None)
+                              _ptr(self.features), None, None)
         if kind == GS_APP_NEURAL_FOLDED:
             if self.preact is None:
                 raise RuntimeError("fold_neural() first: the folded form reads its pre-activations")
             return Appearance(kind, sh_degree, None, None, _ptr(self.neural_w), _ptr(self.base_color), None,
-                              _ptr(self.preact))
-        return Appearance(kind, sh_degree, _ptr(self.sh), _ptr(self.latent), _ptr(self.mlp_w), None, None, None)
+                              _ptr(self.preact), None)
+        if kind in LOBE_ROWS:
+            lobes = self.lobes_gabor if kind == GS_APP_NASGABOR else self.lobes
+            return Appearance(kind, sh_degree, None, None, None, _ptr(self.base_color), None, None, _ptr(lobes))
+        return Appearance(kind, sh_degree, _ptr(self.sh), _ptr(self.latent), _ptr(self.mlp_w), None, None, None,
+                          None)
 
 
 def gs_workspace_size(n: int, width: int, height: int, capacity: int, kind: int) -> int:
@@ -288,13 +295,14 @@ class Frame:
         self.dmlp_w = (torch.empty(MLP_WEIGHTS, device=d) if kind == GS_APP_LATENT_MLP else
                        torch.empty(NEURAL_WEIGHTS, device=d) if kind == GS_APP_NEURAL else None)
         self.dmean2d = torch.empty(2, nn, device=d) if want_dmean2d else None
-        self.dbase_color = torch.empty(3, nn, device=d) if kind == GS_APP_NEURAL else None
+        self.dbase_color = torch.empty(3, nn, device=d) if kind in (GS_APP_NEURAL, *LOBE_ROWS) else None
         self.dfeatures = torch.empty(NEURAL_FEATURES, nn, device=d) if kind == GS_APP_NEURAL else None
+        self.dlobes = torch.empty(LOBE_ROWS[kind], nn, device=d) if kind in LOBE_ROWS else None
         self.pre = Preprocessed(_ptr(self.splats), _ptr(self.tiles_touched), _ptr(self.depth_key),
                                 _ptr(self.num_pairs))
         self.grads = Grads(_ptr(self.dmeans), _ptr(self.dlog_scales), _ptr(self.dquats),
                            _ptr(self.dopacity_logits), _ptr(self.dsh), _ptr(self.dlatent), _ptr(self.dmlp_w),
-                           _ptr(self.dmean2d), _ptr(self.dbase_color), _ptr(self.dfeatures))
+                           _ptr(self.dmean2d), _ptr(self.dbase_color), _ptr(self.dfeatures), _ptr(self.dlobes))
         self.last_pairs = 0
 
     def forward(self, cam: Camera, scene: SceneTensors, sh_degree: int = 3, stream=None) -> int:

@@ -27,7 +27,7 @@ def say(msg: str):
 
 def kind_id(kind: str) -> int:
     return {"sh3": gs.GS_APP_SH3, "latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL,
-            "neural_folded": gs.GS_APP_NEURAL_FOLDED}[kind]
+            "neural_folded": gs.GS_APP_NEURAL_FOLDED, "nasg": gs.GS_APP_NASG, "nasgabor": gs.GS_APP_NASGABOR}[kind]
 
 
 def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None, extras=True):
@@ -76,6 +76,9 @@ def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None, 
                         if getattr(fr, k) is not None}
         if kind == "sh3":
             out["grads"]["dsh"] = fr.dsh.cpu().numpy().astype(np.float64)[:, : scene.n]
+        elif kind in ("nasg", "nasgabor"):
+            out["grads"]["dbase_color"] = fr.dbase_color.cpu().numpy().astype(np.float64)[:, : scene.n]
+            out["grads"]["dlobes"] = fr.dlobes.cpu().numpy().astype(np.float64)[:, : scene.n]
         elif kind == "neural":
             out["grads"]["dbase_color"] = fr.dbase_color.cpu().numpy().astype(np.float64)[:, : scene.n]
             out["grads"]["dfeatures"] = fr.dfeatures.cpu().numpy().astype(np.float64)[:, : scene.n]
@@ -104,7 +107,10 @@ def compare_preprocess(gpu, ref, color_atol=2e-6, flip=None):
         assert np.array_equal(s[k][:, vis].astype(np.float32), ref[k][:, vis].astype(np.float32)), k
     assert np.array_equal(s["opacity"][vis], ref["opacity"][vis].astype(np.float32))
     err = np.abs(s["color"][:, vis] - ref["color"][:, vis]).max(axis=0)
-    if flip is None:
+    if np.ndim(color_atol) == 1:                       # one bound per Gaussian
+        bad = err > np.asarray(color_atol)[vis]
+        assert not bad.any(), (int(bad.sum()), float(err[bad].max()))
+    elif flip is None:
         assert err.max() <= color_atol, err.max()
     else:
         beyond = float((err > color_atol).mean())
@@ -188,6 +194,20 @@ MLP_HALF_ATOL = 2e-4
 NEURAL_FLIP_ATOL = 2e-3
 NEURAL_FLIP_FRAC = 0.01
 NEURAL_FLIP = (NEURAL_FLIP_ATOL, NEURAL_FLIP_FRAC)
+
+
+def lobe_color_atol(scene, kind, ref_color, sh_degree=3):
+    """Per-Gaussian colour bound of the lobe appearances: the GPU evaluates the
+    kernel in fp32 (exp, log, tanh, cosh, each within a few ulp), and the
+    exponent 2 lambda (u^(1+psi) - 1) + psi ln u carries an absolute error of
+    about (2 lambda + 10) ulp; the residual G tanh(a) inherits it as a relative
+    error, bounded here by 4 (2 lambda + 10) 2^-24, plus 4e-6 for the sums."""
+    if sh_degree == 0:
+        return 2e-6
+    lobes = scene.lobes_gabor if kind == "nasgabor" else scene.lobes
+    lam = np.exp(np.clip(lobes[3].astype(np.float64), -8.0, 8.0))
+    res = np.abs(ref_color - (scene.base_color.astype(np.float64) + 0.5)).max(axis=0)
+    return 4e-6 + 4.0 * (2.0 * lam + 10.0) * 2.0 ** -24 * res
 
 
 def compare_image(gpu, ref_img, ref_T, ref_nc, margin, atol=IMG_ATOL, rtol=IMG_RTOL):

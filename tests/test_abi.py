@@ -105,6 +105,13 @@ def test_preprocess_rejects_bad_arguments(gs):
     assert b"preact" in lib.gs_last_error()
     assert call(app=folded(3, FAKE + 2)) == gs.GS_ERR_INVALID_ARG
     assert call(app=folded(4, FAKE)) == gs.GS_ERR_INVALID_ARG
+    # lobes: base colour always, the lobe parameters once the lobe is on
+    lobe = lambda kind, deg, base, lobes: gs.Appearance(kind, deg, None, None, None, base, None, None, lobes)
+    for kind in (gs.GS_APP_NASG, gs.GS_APP_NASGABOR):
+        assert call(app=lobe(kind, 1, FAKE, None)) == gs.GS_ERR_INVALID_ARG
+        assert b"lobes" in lib.gs_last_error()
+        assert call(app=lobe(kind, 0, None, FAKE)) == gs.GS_ERR_INVALID_ARG
+        assert call(app=lobe(kind, 4, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
     assert call(pre=gs.Preprocessed(FAKE, FAKE, FAKE, None)) == gs.GS_ERR_INVALID_ARG
     assert call(ws=FAKE + 4) == gs.GS_ERR_INVALID_ARG              # misaligned workspace
     assert call(wsb=16) == gs.GS_ERR_CAPACITY
@@ -148,6 +155,13 @@ def test_render_calls_reject_bad_arguments(gs):
                            C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE), C.byref(grads),
                            C.c_void_p(FAKE * 256), 1 << 40, None)
     assert st == gs.GS_ERR_INVALID_ARG and b"folded" in lib.gs_last_error()
+    # lobes need both of their gradient arrays
+    app = gs.Appearance(gs.GS_APP_NASG, 1, None, None, None, FAKE, None, None, FAKE)
+    grads = gs.Grads(FAKE, FAKE, FAKE, FAKE, None, None, None, None, FAKE, None, None)
+    st = lib.gs_render_bwd(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), C.c_void_p(FAKE), C.c_void_p(FAKE),
+                           C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE), C.byref(grads),
+                           C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARG and b"dlobes" in lib.gs_last_error()
 
 
 def test_neural_fold_rejects_bad_arguments(gs):

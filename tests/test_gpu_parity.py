@@ -16,7 +16,7 @@ import torch
 
 from oracle import oracle as orc
 from paper_2609_05255_amd import gsraster as gs
-from parity import (MLP_ATOL, MLP_HALF_ATOL, NEURAL_FLIP, affected_gaussians, compare_image, compare_lists, compare_preprocess,
+from parity import (MLP_ATOL, MLP_HALF_ATOL, NEURAL_FLIP, lobe_color_atol, affected_gaussians, compare_image, compare_lists, compare_preprocess,
                     grad_errors, oracle_all, run_gpu, say, tiny_camera)
 
 pytestmark = pytest.mark.gpu
@@ -32,7 +32,9 @@ def check_all(scene, cam, kind="sh3", sh_degree=3, label="", grads=True, capacit
     # the decoder's operands are binary16: compare with the oracle that rounds them alike
     ref = oracle_all(scene, cam, kind, sh_degree, g, half_act=latent)
     flip = NEURAL_FLIP if kind in ("neural", "neural_folded") else None
-    compare_preprocess(gpu, ref["pre"], color_atol=MLP_HALF_ATOL if latent else 2e-6, flip=flip)
+    atol = (MLP_HALF_ATOL if latent else
+            lobe_color_atol(scene, kind, ref["pre"]["color"], sh_degree) if kind in ("nasg", "nasgabor") else 2e-6)
+    compare_preprocess(gpu, ref["pre"], color_atol=atol, flip=flip)
     compare_lists(gpu, ref["values"], ref["tile_of"], ref["ranges"])
     if latent:
         flagged = compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"],
@@ -236,3 +238,24 @@ def test_ragged_neural_folded_with_background():
 def test_medium_scene_neural_folded():
     sc = inputs.make_scene("medium", appearance=("neural",))
     check_all(sc, inputs.make_cameras("medium")[2], kind="neural_folded", label="medium-folded", grads=False)
+
+
+# ---- NASG and NASGabor lobes ------------------------------------------------------
+
+@pytest.mark.parametrize("kind", ["nasg", "nasgabor"])
+@pytest.mark.parametrize("degree", [0, 1])
+def test_tiny_scene_lobe(kind, degree):
+    sc = inputs.make_scene("tiny", appearance=(kind,))
+    check_all(sc, tiny_camera(), kind=kind, sh_degree=degree, label="tiny-" + kind)
+
+
+@pytest.mark.parametrize("kind", ["nasg", "nasgabor"])
+def test_ragged_lobe_with_background(kind):
+    sc = inputs.make_scene("tiny", n=999, appearance=(kind,))
+    check_all(sc, tiny_camera(50, 37, bg=(0.6, 0.1, 0.4)), kind=kind, label="ragged-" + kind)
+
+
+@pytest.mark.parametrize("kind", ["nasg", "nasgabor"])
+def test_medium_scene_lobe(kind):
+    sc = inputs.make_scene("medium", appearance=(kind,))
+    check_all(sc, inputs.make_cameras("medium")[5], kind=kind, label="medium-" + kind)

@@ -77,7 +77,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=32)
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--config", default="paper_sh3")
-    ap.add_argument("--appearance", default=None, help="sh3 or latent (default: the config's first)")
+    ap.add_argument("--appearance", default=None,
+                    help="sh3, latent, neural, nasg or nasgabor (default: the config's first)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tiles", type=int, default=96, help="tiles in the CPU-baseline sample")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -90,8 +91,10 @@ def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int
     """HBM bytes a launch must move at minimum (per launch, averaged over cameras)."""
     # appearance bytes per visible Gaussian: SH3 48 fp32, latent 14 binary16, neural a 12 B
     # base colour and 8 binary16 features
-    # (the folded form: the base colour and 16 binary16 pre-activations, 44 B)
-    app = 4 * 3 * (sh_degree + 1) ** 2 if kind == "sh3" else 44 if kind == "neural_folded" else 28
+    # (the folded form: the base colour and 16 binary16 pre-activations, 44 B; NASG 12 + 32 B,
+    # NASGabor 12 + 36 B)
+    app = (4 * 3 * (sh_degree + 1) ** 2 if kind == "sh3" else
+           {"neural_folded": 44, "nasg": 44, "nasgabor": 48}.get(kind, 28))
     if kernel == "preprocess":
         # params 44 B + tiles 4 B + depth key 4 B per Gaussian; appearance + 48 B of projected splat
         # (mean 8, conic 12, opacity 4, colour 12, rectangle 8, depth 4) per visible one; the record
@@ -99,7 +102,7 @@ def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int
         return n * (44 + 8) + vis * (app + 48)
     if kernel == "preprocess_bwd":
         # tiles 4 B + dense gradient writes per Gaussian; params, accumulators and appearance per visible one
-        grad = 44 + 4 * {"sh3": 48, "latent": 14, "neural": 11}[kind]
+        grad = 44 + 4 * {"sh3": 48, "latent": 14, "neural": 11, "nasg": 11, "nasgabor": 12}[kind]
         return n * (4 + grad) + vis * (44 + 36 + app)
     return None
 
@@ -117,7 +120,8 @@ def main():
 
     cfg = inputs.CONFIGS[args.config]
     kind = args.appearance or cfg.appearance[0]
-    kid = {"sh3": gs.GS_APP_SH3, "latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL}[kind]
+    kid = {"sh3": gs.GS_APP_SH3, "latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL,
+           "nasg": gs.GS_APP_NASG, "nasgabor": gs.GS_APP_NASGABOR}[kind]
     torch.cuda.set_device(0)
     dev = "cuda:0"
     t0 = time.time()
@@ -220,8 +224,8 @@ def main():
     # training step: the same K steps followed each by the fused Adam update of
     # every parameter tensor (the paper's optimisation comparison); value
     # above stays the forward+backward metric
-    from paper_2609_05255_amd.optim import FusedAdam
-    opt = FusedAdam(st, fr, kid)
+    from paper_2609_05255_amd.optim import FusedAdam, camera_spacing
+    opt = FusedAdam(st, fr, kid, camera_dbar=camera_spacing([c.campos for c in cams]))
     for i in range(args.warmup):
         step(i)
         opt.step(stream)
@@ -297,7 +301,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if kind == "sh3" else "f32+f16",
+        "dtype": "f32" if kind in ("sh3", "nasg", "nasgabor") else "f32+f16",
         "data": "synthetic",
         "config": {"workload": "%s: %d Gaussians, %dx%d, %s appearance, %d cameras" % (
             cfg.name, scene.n, cfg.width, cfg.height, kind, ncam),

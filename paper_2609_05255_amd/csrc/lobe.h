@@ -12,6 +12,8 @@
 //           K = 2 pi (1 - exp(-2 lambda)) / (lambda sqrt(1 + a)) (unit integral);
 //   Gabor   G~ = G (1 + cos(omega d.x)) / 2, omega = 20 (tanh(r5) + 1).
 // fp32 throughout; sin(theta) = sech(r0), sin(phi/2) = sech(r1), sin(gamma/2) = sech(r2).
+// u = (d.z + 1)/2 is evaluated as |d + z|^2 / 4 (equal for unit vectors), which
+// keeps its relative accuracy where d approaches -z instead of cancelling.
 #pragma once
 
 namespace gsr {
@@ -61,12 +63,19 @@ __device__ __forceinline__ void lobe_setup(const float r[6], LobeEval& f)
 
 __device__ __forceinline__ float dot3f(const float a[3], const float b[3]) { return a[0] * b[0] + a[1] * b[1] + a[2] * b[2]; }
 
+// (d.z + 1)/2 as |d + z|^2 / 4
+__device__ __forceinline__ float lobe_u(const float d[3], const float z[3])
+{
+    const float s0 = d[0] + z[0], s1 = d[1] + z[1], s2 = d[2] + z[2];
+    return fmaxf(0.25f * (s0 * s0 + s1 * s1 + s2 * s2), 1e-30f);
+}
+
 // Kernel value at unit direction d.
 template <bool kGabor>
 __device__ __forceinline__ float lobe_value(const LobeEval& f, const float d[3])
 {
-    const float px = dot3f(d, f.x), py = dot3f(d, f.y), pz = dot3f(d, f.z);
-    const float u = fmaxf(0.5f * (pz + 1.f), 1e-30f), q = px * px + py * py;
+    const float px = dot3f(d, f.x), py = dot3f(d, f.y);
+    const float u = lobe_u(d, f.z), q = px * px + py * py;
     const float psi = q > 0.f ? f.an * (px * px / q) : 0.f;
     const float L = logf(u);
     const float w = expf((1.f + psi) * L);
@@ -86,7 +95,7 @@ template <bool kGabor>
 __device__ __forceinline__ float lobe_grad(const LobeEval& f, const float d[3], float draw[6], float dd[3])
 {
     const float px = dot3f(d, f.x), py = dot3f(d, f.y), pz = dot3f(d, f.z);
-    const float u = fmaxf(0.5f * (pz + 1.f), 1e-30f), q = px * px + py * py;
+    const float u = lobe_u(d, f.z), q = px * px + py * py;
     const float rho = q > 0.f ? px * px / q : 0.f;
     const float psi = f.an * rho;
     const float L = logf(u);

@@ -13,7 +13,10 @@ Learning rates per parameter channel (the row of the planar layout):
     decoder weights 0.003 with a second-moment decay of 0.99 (they receive a
     gradient from every visible Gaussian in every iteration);
   * neural (the paper's model): base colour 0.00025, features 0.008, decoder
-    weights 0.003 with a second-moment decay of 0.99.
+    weights 0.003 with a second-moment decay of 0.99;
+  * NASG / NASGabor: base colour 0.00025 and every lobe parameter
+    0.0025 (0.3536 / dbar)^2, dbar the mean distance from each training camera
+    to its three nearest neighbours (camera_spacing).
 The latents and the decoder weights have fp32 master copies here; each step
 writes their binary16 copies into the scene buffers the passes read, as the
 paper does for its decoder weights.
@@ -28,12 +31,23 @@ LR_MEANS, LR_SCALES, LR_QUATS, LR_OPACITY = 1.6e-4, 5e-3, 1e-3, 0.05
 LR_SH_DC, LR_SH_REST = 0.0025, 0.000125
 LR_LATENT, LR_MLP, BETA2_MLP = 0.008, 0.003, 0.99
 LR_BASE_COLOR, LR_FEATURES = 0.00025, 0.008
+LR_LOBES, LOBE_SPACING_REF = 0.0025, 0.3536
 NEURAL_FEATURES = 8
 LATENT_DIM = 14
 
 
+def camera_spacing(campos) -> float:
+    """Mean over the training cameras of the mean distance to their three nearest neighbours."""
+    c = torch.as_tensor(campos, dtype=torch.float64).reshape(-1, 3)
+    dist = torch.cdist(c, c)
+    dist.fill_diagonal_(float("inf"))
+    k = min(3, c.shape[0] - 1)
+    return float(dist.topk(k, dim=1, largest=False).values.mean()) if k > 0 else LOBE_SPACING_REF
+
+
 class FusedAdam:
-    def __init__(self, scene: gs.SceneTensors, frame: gs.Frame, kind: int, betas=(0.9, 0.999), eps: float = 1e-15):
+    def __init__(self, scene: gs.SceneTensors, frame: gs.Frame, kind: int, betas=(0.9, 0.999), eps: float = 1e-15,
+                 camera_dbar: float = LOBE_SPACING_REF):
         self.beta1, self.beta2, self.eps, self.t = betas[0], betas[1], eps, 0
         self.groups = []
 
@@ -52,6 +66,11 @@ class FusedAdam:
         add(scene.opacity_logits, frame.dopacity_logits, [LR_OPACITY])
         if kind == gs.GS_APP_SH3:
             add(scene.sh, frame.dsh, [LR_SH_DC] * 3 + [LR_SH_REST] * 45)
+        elif kind in gs.LOBE_ROWS:
+            lobes = scene.lobes_gabor if kind == gs.GS_APP_NASGABOR else scene.lobes
+            lr_lobe = LR_LOBES * (LOBE_SPACING_REF / camera_dbar) ** 2
+            add(scene.base_color, frame.dbase_color, [LR_BASE_COLOR] * 3)
+            add(lobes, frame.dlobes, [lr_lobe] * gs.LOBE_ROWS[kind])
         elif kind == gs.GS_APP_NEURAL:
             self.features32 = scene.features.view(torch.float16).float().contiguous()
             self.mlp32 = scene.neural_w.view(torch.float16).float().contiguous()

@@ -196,18 +196,50 @@ NEURAL_FLIP_FRAC = 0.01
 NEURAL_FLIP = (NEURAL_FLIP_ATOL, NEURAL_FLIP_FRAC)
 
 
-def lobe_color_atol(scene, kind, ref_color, sh_degree=3):
-    """Per-Gaussian colour bound of the lobe appearances: the GPU evaluates the
-    kernel in fp32 (exp, log, tanh, cosh, each within a few ulp), and the
-    exponent 2 lambda (u^(1+psi) - 1) + psi ln u carries an absolute error of
-    about (2 lambda + 10) ulp; the residual G tanh(a) inherits it as a relative
-    error, bounded here by 4 (2 lambda + 10) 2^-24, plus 4e-6 for the sums."""
+def lobe_frame(lobes):
+    """Axes x, y, z [3][n] of the lobe frames (ZYZ Euler angles phi, theta, gamma
+    with cos theta = tanh r0 and half-angle cosines tanh r1, tanh r2), fp64."""
+    th = np.arccos(np.tanh(lobes[0]))
+    ph = 2.0 * np.arccos(np.tanh(lobes[1]))
+    ga = 2.0 * np.arccos(np.tanh(lobes[2]))
+    ct, st, cp, sp, cg, sg = np.cos(th), np.sin(th), np.cos(ph), np.sin(ph), np.cos(ga), np.sin(ga)
+    z = np.stack([st * cp, st * sp, ct])
+    e1 = np.stack([ct * cp, ct * sp, -st])
+    e2 = np.stack([-sp, cp, np.zeros_like(cp)])
+    return cg * e1 + sg * e2, -sg * e1 + cg * e2, z
+
+
+def lobe_color_atol(scene, cam, kind, ref_color, sh_degree=3):
+    """Per-Gaussian colour bound of the lobe appearances from the kernel's
+    conditioning. The GPU's fp32 direction and frame carry absolute errors of
+    about 12 ulp in d.x, d.y and d.z; the residual G tanh(a) takes them as the
+    relative error |d ln G/d pz| + |d ln G/d psi| |d psi/d(px, py)| times that,
+    with d ln G/d pz <= lambda (1 + a) + a / (2u), d ln G/d psi = (2 lambda w + 1)
+    ln u <= (2 lambda + 1) |ln u|, |d psi/d(px, py)| <= 1.5 a / sqrt(px^2 + py^2);
+    the exp, log and tanh roundings add 4 (2 lambda + 10) ulp, the sums 4e-6.
+    NASGabor's carrier adds (8 omega + 2) ulp times the uncarried kernel, at most
+    its peak 1/K."""
     if sh_degree == 0:
         return 2e-6
-    lobes = scene.lobes_gabor if kind == "nasgabor" else scene.lobes
-    lam = np.exp(np.clip(lobes[3].astype(np.float64), -8.0, 8.0))
+    eps = 2.0 ** -24
+    lobes = (scene.lobes_gabor if kind == "nasgabor" else scene.lobes).astype(np.float64)
+    lam = np.exp(np.clip(lobes[3], -8.0, 8.0))
+    an = np.exp(np.clip(lobes[4], -8.0, 8.0))
+    x, y, z = lobe_frame(lobes)
+    v = scene.means.astype(np.float64) - np.asarray(cam.campos, np.float64)[:, None]
+    d = v / np.linalg.norm(v, axis=0)
+    px, py, pz = (d * x).sum(0), (d * y).sum(0), (d * z).sum(0)
+    u = np.maximum((1.0 + pz) / 2.0, 1e-30)
+    sq = np.sqrt(np.maximum(px * px + py * py, 1e-30))
+    cond = (12.0 * (lam * (1.0 + an) + an / (2.0 * u)) + 18.0 * (2.0 * lam + 1.0) * np.abs(np.log(u)) * an / sq
+            + 4.0 * (2.0 * lam + 10.0))
     res = np.abs(ref_color - (scene.base_color.astype(np.float64) + 0.5)).max(axis=0)
-    return 4e-6 + 4.0 * (2.0 * lam + 10.0) * 2.0 ** -24 * res
+    tol = 4e-6 + cond * eps * res
+    if kind == "nasgabor":
+        inv_k = lam * np.sqrt(1.0 + an) / (2.0 * np.pi * -np.expm1(-2.0 * lam))
+        omega = 20.0 * (np.tanh(lobes[8]) + 1.0)
+        tol += (8.0 * omega + 2.0) * eps * np.abs(np.tanh(lobes[5:8])).max(axis=0) * inv_k
+    return tol
 
 
 def compare_image(gpu, ref_img, ref_T, ref_nc, margin, atol=IMG_ATOL, rtol=IMG_RTOL):

@@ -20,7 +20,7 @@ import pytest
 
 from paper_2609_05255_amd import inputs
 from oracle import oracle as orc
-from parity import (IMG_ATOL, IMG_RTOL, MARGIN, MLP_HALF_ATOL, NEURAL_FLIP, affected_gaussians, check_list_properties,
+from parity import (IMG_ATOL, IMG_RTOL, MARGIN, MLP_HALF_ATOL, NEURAL_FLIP, lobe_color_atol, affected_gaussians, check_list_properties,
                     compare_preprocess, grad_errors, run_gpu, say, tile_of_ranges)
 
 pytestmark = pytest.mark.gpu
@@ -78,7 +78,8 @@ def tile_pixels(sample, tiles_x, W, H):
 
 
 @pytest.mark.parametrize("config,kind,cam_index", [("paper_sh3", "sh3", 3), ("paper_latent", "latent", 9),
-                                                    ("paper_neural", "neural", 7), ("stress", "sh3", 5)])
+                                                    ("paper_neural", "neural", 7), ("paper_nasg", "nasg", 11),
+                                                    ("paper_nasgabor", "nasgabor", 13), ("stress", "sh3", 5)])
 def test_full_size_sampled(config, kind, cam_index):
     latent = kind in ("latent", "neural")
     sc = inputs.make_scene(config, appearance=(kind,))
@@ -101,7 +102,9 @@ def test_full_size_sampled(config, kind, cam_index):
 
     # preprocess of every Gaussian and the whole list
     flip = NEURAL_FLIP if kind == "neural" else None
-    compare_preprocess(gpu, pre, color_atol=MLP_HALF_ATOL if latent else 2e-6, flip=flip)
+    atol = (MLP_HALF_ATOL if latent else
+            lobe_color_atol(sc, cam, kind, pre["color"]) if kind in ("nasg", "nasgabor") else 2e-6)
+    compare_preprocess(gpu, pre, color_atol=atol, flip=flip)
     assert gpu["P"] == P_ref
     key = np.where(pre["tiles"] > 0, pre["depth"].astype(np.float32).view(np.uint32), np.uint32(0xFFFFFFFF))
     tile_of = tile_of_ranges(gpu["ranges"], gpu["P"])
@@ -142,7 +145,8 @@ def test_full_size_sampled(config, kind, cam_index):
     margin_s = np.where(in_sample, margin, np.inf)
     excl = affected_gaussians(ranges, values, n_contrib, gpu["n_contrib"], margin_s, W)
     names = ["dmeans", "dlog_scales", "dquats", "dopacity_logits"] + {
-        "sh3": ["dsh"], "latent": ["dlatent", "dmlp_w"], "neural": ["dbase_color", "dfeatures", "dmlp_w"]}[kind]
+        "sh3": ["dsh"], "latent": ["dlatent", "dmlp_w"], "neural": ["dbase_color", "dfeatures", "dmlp_w"],
+        "nasg": ["dbase_color", "dlobes"], "nasgabor": ["dbase_color", "dlobes"]}[kind]
     st = grad_errors({k: gpu["grads"][k] for k in names}, {k: ref[k] for k in names}, excl)
     say("  grad errors (rel L2, max elem): " + ", ".join("%s %.2e %.2e" % (k, a, b) for k, (a, b) in st.items()))
     for k, (rel, _) in st.items():

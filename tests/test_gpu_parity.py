@@ -33,7 +33,7 @@ def check_all(scene, cam, kind="sh3", sh_degree=3, label="", grads=True, capacit
     ref = oracle_all(scene, cam, kind, sh_degree, g, half_act=latent)
     flip = NEURAL_FLIP if kind in ("neural", "neural_folded") else None
     atol = (MLP_HALF_ATOL if latent else
-            lobe_color_atol(scene, kind, ref["pre"]["color"], sh_degree) if kind in ("nasg", "nasgabor") else 2e-6)
+            lobe_color_atol(scene, cam, kind, ref["pre"]["color"], sh_degree) if kind in ("nasg", "nasgabor") else 2e-6)
     compare_preprocess(gpu, ref["pre"], color_atol=atol, flip=flip)
     compare_lists(gpu, ref["values"], ref["tile_of"], ref["ranges"])
     if latent:

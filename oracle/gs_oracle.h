@@ -80,6 +80,9 @@ typedef struct orc_appearance {
     const double* lobes;      /* NASG: [8][n] raw frame angles (3), sharpness, anisotropy and
                                  the three raw amplitudes; NASGABOR: [9][n], the frequency last.
                                  base_color is the base colour c0 of both */
+    int32_t sh_y0_folded;     /* SH3: 1 = the constant degree-0 basis value Y0 is folded into the
+                                 stored DC coefficients (the paper's implementation, Sec. 3.1):
+                                 their basis value is 1 instead of Y0 */
 } orc_appearance;
 
 /* Outputs of the preprocess. Entries of culled Gaussians are zero. */

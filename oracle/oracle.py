@@ -60,7 +60,7 @@ class _Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p),
                 ("latent", C.c_void_p), ("mlp_w", C.c_void_p), ("dir_exact", C.c_int32),
                 ("half_act", C.c_int32), ("base_color", C.c_void_p), ("features", C.c_void_p),
-                ("preact", C.c_void_p), ("lobes", C.c_void_p)]
+                ("preact", C.c_void_p), ("lobes", C.c_void_p), ("sh_y0_folded", C.c_int32)]
 
 
 class _Pre(C.Structure):
@@ -165,7 +165,7 @@ class _SceneArrays:
                        if kind == APP_NEURAL_FOLDED else None)
         self.app = _Appearance(kind, sh_degree, _p(self.sh), _p(self.latent), _p(self.mlp_w), int(dir_exact),
                                int(half_act), _p(self.base_color), _p(self.features), _p(self.preact),
-                               _p(self.lobes))
+                               _p(self.lobes), int(bool(getattr(scene, "sh_y0_folded", False))))
 
 
 def neural_fold(features, neural_w, exact: bool = False) -> np.ndarray:

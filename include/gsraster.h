@@ -132,6 +132,9 @@ typedef struct gs_appearance {
                                  NASGABOR: [9][n], the raw frequency r5 last. base_color [3][n]
                                  is c0; sh_degree 0 turns the lobe off (c = max(0, c0 + 0.5)),
                                  1..3 on (the paper's schedule) */
+    int32_t sh_y0_folded;     /* SH3: 0 = eq. sh_color_eval as printed (DC times Y0); 1 = the
+                                 paper's implementation (Sec. 3.1), Y0 folded into the stored DC
+                                 coefficients: c = max(0, 0.5 + sh_0 + sum_{k>=1} Y_k(d) sh_k) */
 } gs_appearance;
 
 /* Screen-space record of one Gaussian, written by gs_preprocess (64 bytes).

@@ -42,6 +42,7 @@ struct BwdArgs {
     float* dfeatures;
     const float* lobes;
     float* dlobes;
+    int sh_y0_folded;
 };
 
 struct GeoGrad {
@@ -194,6 +195,7 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
         const float il = 1.f / len;
         const float d0 = vx * il, d1 = vy * il, d2 = vz * il;
         sh_basis16(d0, d1, d2, Y);
+        if (a.sh_y0_folded) Y[0] = 1.f;   // constant either way: no direction gradient
         float coef[GS_SH_COEFFS];
         float pre[3] = {0.5f, 0.5f, 0.5f};
         for (int k = 0; k < 16; ++k)
@@ -599,6 +601,7 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
     a.dfeatures = gr.dfeatures;
     a.lobes = app.lobes;
     a.dlobes = gr.dlobes;
+    a.sh_y0_folded = app.sh_y0_folded;
     if (app.kind == GS_APP_SH3)
         hipLaunchKernelGGL(k_preprocess_bwd_sh3, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NASG)

@@ -139,6 +139,7 @@ struct PreArgs {
     const uint16_t* features;
     const uint16_t* preact;
     const float* lobes;
+    int sh_y0_folded;
     gs_splat* splats;
     uint32_t* tiles_touched;
     uint32_t* depth_key;
@@ -244,11 +245,12 @@ __device__ __forceinline__ void view_dir(const Cam& c, const float mu[3], float 
 
 }  // namespace
 
-// eq. sh_color_eval: c = max(0, 0.5 + sum over bands <= kDeg of Y_k(d) sh_k).
+// eq. sh_color_eval: c = max(0, 0.5 + sum over bands <= kDeg of Y_k(d) sh_k),
+// with Y_0 = 1 when the stored DC coefficients have Y0 folded in.
 // All coefficient loads are issued together, before the sums need them.
 template <int kDeg>
 __device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n, int i, const float d[3],
-                                         float col[3])
+                                         bool y0_folded, float col[3])
 {
     constexpr int nb = (kDeg + 1) * (kDeg + 1);
     float c[3 * nb];
@@ -256,6 +258,7 @@ __device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n
     for (int k = 0; k < 3 * nb; ++k) c[k] = sh[(int64_t)k * n + i];
     float Y[16];
     sh_basis16(d[0], d[1], d[2], Y);
+    if (y0_folded) Y[0] = 1.f;
 #pragma unroll
     for (int ch = 0; ch < 3; ++ch) {
         float acc = 0.5f;
@@ -282,7 +285,7 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
         if (g.visible) {
             float d[3];
             view_dir(a.cam, mu, d);
-            sh_color<kDeg>(a.sh, a.n, i, d, col);
+            sh_color<kDeg>(a.sh, a.n, i, d, a.sh_y0_folded != 0, col);
             tiles = g.tiles;
         }
         a.tiles_touched[i] = tiles;
@@ -517,6 +520,7 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     a.features = app.features;
     a.preact = app.preact;
     a.lobes = app.lobes;
+    a.sh_y0_folded = app.sh_y0_folded;
     a.splats = out.splats;
     a.tiles_touched = out.tiles_touched;
     a.depth_key = out.depth_key;

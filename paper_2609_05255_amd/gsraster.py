@@ -52,7 +52,7 @@ class Gaussians(C.Structure):
 class Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p), ("latent", C.c_void_p),
                 ("mlp_w", C.c_void_p), ("base_color", C.c_void_p), ("features", C.c_void_p),
-                ("preact", C.c_void_p), ("lobes", C.c_void_p)]
+                ("preact", C.c_void_p), ("lobes", C.c_void_p), ("sh_y0_folded", C.c_int32)]
 
 
 class Preprocessed(C.Structure):
@@ -160,6 +160,7 @@ class SceneTensors:
         self.features = h16(scene.features) if getattr(scene, "features", None) is not None else None
         self.neural_w = h16(scene.neural_w) if getattr(scene, "neural_w", None) is not None else None
         self.preact = None   # [n][16] binary16 pre-activations of the folded form (fold_neural)
+        self.sh_y0_folded = bool(getattr(scene, "sh_y0_folded", False))
         self.lobes = f32(scene.lobes) if getattr(scene, "lobes", None) is not None else None
         self.lobes_gabor = f32(scene.lobes_gabor) if getattr(scene, "lobes_gabor", None) is not None else None
 
@@ -187,7 +188,7 @@ class SceneTensors:
             lobes = self.lobes_gabor if kind == GS_APP_NASGABOR else self.lobes
             return Appearance(kind, sh_degree, None, None, None, _ptr(self.base_color), None, None, _ptr(lobes))
         return Appearance(kind, sh_degree, _ptr(self.sh), _ptr(self.latent), _ptr(self.mlp_w), None, None, None,
-                          None)
+                          None, int(self.sh_y0_folded))
 
 
 def gs_workspace_size(n: int, width: int, height: int, capacity: int, kind: int) -> int:

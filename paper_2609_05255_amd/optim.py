@@ -7,8 +7,8 @@ Learning rates per parameter channel (the row of the planar layout):
     rotations 1e-3, opacity logits 0.05;
   * SH3 (the paper's table of appearance learning rates): the degree-0 rows
     0.0025 -- the paper folds Y0 into the base colour and scales its rate by
-    Y0 instead, the same step in colour space -- and every other coefficient
-    0.000125;
+    Y0 instead, the same step in colour space, which the Y0-folded form takes --
+    and every other coefficient 0.000125;
   * latent + MLP: latents 0.008 (the paper's rate for the neural features) and
     decoder weights 0.003 with a second-moment decay of 0.99 (they receive a
     gradient from every visible Gaussian in every iteration);
@@ -29,6 +29,7 @@ from . import gsraster as gs
 
 LR_MEANS, LR_SCALES, LR_QUATS, LR_OPACITY = 1.6e-4, 5e-3, 1e-3, 0.05
 LR_SH_DC, LR_SH_REST = 0.0025, 0.000125
+Y0 = 0.28209479177387814   # 1 / (2 sqrt(pi)), the degree-0 SH value
 LR_LATENT, LR_MLP, BETA2_MLP = 0.008, 0.003, 0.99
 LR_BASE_COLOR, LR_FEATURES = 0.00025, 0.008
 LR_LOBES, LOBE_SPACING_REF = 0.0025, 0.3536
@@ -65,7 +66,8 @@ class FusedAdam:
         add(scene.quats, frame.dquats, [LR_QUATS] * 4)
         add(scene.opacity_logits, frame.dopacity_logits, [LR_OPACITY])
         if kind == gs.GS_APP_SH3:
-            add(scene.sh, frame.dsh, [LR_SH_DC] * 3 + [LR_SH_REST] * 45)
+            lr_dc = LR_SH_DC * Y0 if scene.sh_y0_folded else LR_SH_DC
+            add(scene.sh, frame.dsh, [lr_dc] * 3 + [LR_SH_REST] * 45)
         elif kind in gs.LOBE_ROWS:
             lobes = scene.lobes_gabor if kind == gs.GS_APP_NASGABOR else scene.lobes
             lr_lobe = LR_LOBES * (LOBE_SPACING_REF / camera_dbar) ** 2

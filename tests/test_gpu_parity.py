@@ -259,3 +259,13 @@ def test_ragged_lobe_with_background(kind):
 def test_medium_scene_lobe(kind):
     sc = inputs.make_scene("medium", appearance=(kind,))
     check_all(sc, inputs.make_cameras("medium")[5], kind=kind, label="medium-" + kind)
+
+
+@pytest.mark.parametrize("degree", [0, 3])
+def test_tiny_scene_sh_y0_folded(degree):
+    # the paper's implementation: DC coefficients stored with Y0 folded in
+    sc = inputs.make_scene("tiny")
+    sc.sh = sc.sh.copy()
+    sc.sh[0:3] *= np.float32(0.28209479177387814)
+    sc.sh_y0_folded = True
+    check_all(sc, tiny_camera(), sh_degree=degree, label="tiny-sh-y0-folded")

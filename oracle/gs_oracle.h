@@ -83,6 +83,10 @@ typedef struct orc_appearance {
     int32_t sh_y0_folded;     /* SH3: 1 = the constant degree-0 basis value Y0 is folded into the
                                  stored DC coefficients (the paper's implementation, Sec. 3.1):
                                  their basis value is 1 instead of Y0 */
+    int32_t neural_layers;    /* NEURAL: hidden layers L (1..3; 0 = the paper's default, 2) */
+    int32_t neural_width;     /* NEURAL: neurons per hidden layer W (16 or 32; 0 = 16) */
+    int32_t neural_raw16;     /* NEURAL: 1 = 16 raw features as the 16 feature inputs instead of
+                                 (sin f, cos f) of 8 (the table of configurations' F = 16) */
 } orc_appearance;
 
 /* Outputs of the preprocess. Entries of culled Gaussians are zero. */
@@ -111,7 +115,7 @@ typedef struct orc_grads {
     double* dopacity;       /* [n] or NULL (w.r.t. the activated opacity) */
     double* dcolor;         /* [3][n] or NULL */
     double* dbase_color;    /* [3][n] (neural) or NULL */
-    double* dfeatures;      /* [8][n] (neural) or NULL */
+    double* dfeatures;      /* [8][n] (neural; [16][n] with 16 raw features) or NULL */
     double* dlobes;         /* [8][n] (NASG), [9][n] (NASGabor) or NULL */
 } orc_grads;
 

@@ -60,7 +60,8 @@ class _Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p),
                 ("latent", C.c_void_p), ("mlp_w", C.c_void_p), ("dir_exact", C.c_int32),
                 ("half_act", C.c_int32), ("base_color", C.c_void_p), ("features", C.c_void_p),
-                ("preact", C.c_void_p), ("lobes", C.c_void_p), ("sh_y0_folded", C.c_int32)]
+                ("preact", C.c_void_p), ("lobes", C.c_void_p), ("sh_y0_folded", C.c_int32),
+                ("neural_layers", C.c_int32), ("neural_width", C.c_int32), ("neural_raw16", C.c_int32)]
 
 
 class _Pre(C.Structure):
@@ -165,7 +166,18 @@ class _SceneArrays:
                        if kind == APP_NEURAL_FOLDED else None)
         self.app = _Appearance(kind, sh_degree, _p(self.sh), _p(self.latent), _p(self.mlp_w), int(dir_exact),
                                int(half_act), _p(self.base_color), _p(self.features), _p(self.preact),
-                               _p(self.lobes), int(bool(getattr(scene, "sh_y0_folded", False))))
+                               _p(self.lobes), int(bool(getattr(scene, "sh_y0_folded", False))),
+                               *neural_arch(scene))
+
+
+def neural_arch(scene) -> tuple:
+    """(hidden layers, width, raw16) of a scene's neural decoder; the paper's default (2, 16, 0)."""
+    arch = getattr(scene, "neural_arch", None)
+    return tuple(int(v) for v in arch) if arch is not None else (2, 16, 0)
+
+
+def neural_weight_count(layers: int, width: int) -> int:
+    return 32 * width + (layers - 1) * width * width + 3 * width
 
 
 def neural_fold(features, neural_w, exact: bool = False) -> np.ndarray:
@@ -275,10 +287,11 @@ def render_bwd(cam, scene, pre: Preprocessed, ranges, values, dL_dimage, kind="s
              dopacity_logits=np.zeros(n),
              dsh=np.zeros((48, n)) if kind == APP_SH3 else None,
              dlatent=np.zeros((14, n)) if kind == APP_LATENT_MLP else None,
-             dmlp_w=(np.zeros(1664) if kind == APP_LATENT_MLP else np.zeros(816) if kind == APP_NEURAL else None),
+             dmlp_w=(np.zeros(1664) if kind == APP_LATENT_MLP else
+                     np.zeros(neural_weight_count(*neural_arch(scene)[:2])) if kind == APP_NEURAL else None),
              dmean2d=np.zeros((2, n)), dconic=np.zeros((3, n)), dopacity=np.zeros(n), dcolor=np.zeros((3, n)),
              dbase_color=np.zeros((3, n)) if kind in (APP_NEURAL, APP_NASG, APP_NASGABOR) else None,
-             dfeatures=np.zeros((8, n)) if kind == APP_NEURAL else None,
+             dfeatures=np.zeros((16 if neural_arch(scene)[2] else 8, n)) if kind == APP_NEURAL else None,
              dlobes=np.zeros((9 if kind == APP_NASGABOR else 8, n)) if kind in (APP_NASG, APP_NASGABOR) else None)
     gs = _Grads(*[_p(g[k]) for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh", "dlatent",
                                       "dmlp_w", "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color",

@@ -95,6 +95,7 @@ class Scene:
     neural_w: np.ndarray | None = None
     lobes: np.ndarray | None = None
     lobes_gabor: np.ndarray | None = None
+    neural_arch: tuple | None = None   # (hidden layers, width, raw16); None = the paper's (2, 16, 0)
 
     def subset(self, idx: np.ndarray) -> "Scene":
         idx = np.asarray(idx)
@@ -103,12 +104,15 @@ class Scene:
         return Scene(len(idx), pick(self.means), pick(self.log_scales), pick(self.quats),
                      np.ascontiguousarray(self.opacity_logits[idx]), pick(self.sh), pick(self.latent),
                      copy(self.mlp_w), pick(self.base_color), pick(self.features), copy(self.neural_w),
-                     pick(self.lobes), pick(self.lobes_gabor))
+                     pick(self.lobes), pick(self.lobes_gabor), self.neural_arch)
 
 
 def make_scene(cfg: Config | str, seed: int = SCENE_SEED, n: int | None = None,
-               appearance: tuple | None = None) -> Scene:
-    """Draw a scene of ``cfg``'s distributions (``n`` overrides the count)."""
+               appearance: tuple | None = None, neural_arch: tuple | None = None) -> Scene:
+    """Draw a scene of ``cfg``'s distributions (``n`` overrides the count).
+    ``neural_arch`` = (hidden layers 1..3, width 16 or 32, raw16) picks one of the
+    neural decoder configurations of the paper's table (default (2, 16, 0)):
+    raw16 stores 16 raw binary16 features instead of 8 frequency-encoded ones."""
     if isinstance(cfg, str):
         cfg = CONFIGS[cfg]
     n = cfg.n if n is None else int(n)
@@ -151,9 +155,11 @@ def make_scene(cfg: Config | str, seed: int = SCENE_SEED, n: int | None = None,
         # features N(0, 1) in binary16; all three layers Glorot (a non-zero residual)
         dc = (_rng(seed, 6).standard_normal((3, n), dtype=f32) * f32(0.2) + f32(0.5)).astype(f32)
         scene.base_color = np.ascontiguousarray((dc * f32(Y0)).astype(f32))
-        fe = _rng(seed, 9).standard_normal((NEURAL_FEATURES, n), dtype=f32)
+        layers, width, raw16 = neural_arch if neural_arch is not None else (2, NEURAL_HIDDEN, 0)
+        fe = _rng(seed, 9).standard_normal((16 if raw16 else NEURAL_FEATURES, n), dtype=f32)
         scene.features = np.ascontiguousarray(fe.astype(np.float16).view(np.uint16))
-        scene.neural_w = make_neural_weights(seed)
+        scene.neural_w = make_neural_weights(seed, layers, width)
+        scene.neural_arch = None if neural_arch is None else (int(layers), int(width), int(raw16))
     return scene
 
 
@@ -169,15 +175,18 @@ def make_mlp_weights(seed: int = SCENE_SEED) -> np.ndarray:
     return np.ascontiguousarray(w)
 
 
-def make_neural_weights(seed: int = SCENE_SEED) -> np.ndarray:
-    """Glorot-uniform weights of the 32 -> 16 -> 16 -> 3 decoder, drawn fp32, stored fp16."""
+def make_neural_weights(seed: int = SCENE_SEED, layers: int = 2, width: int = NEURAL_HIDDEN) -> np.ndarray:
+    """Glorot-uniform weights of the 32 -> width (x layers) -> 3 decoder (default
+    32 -> 16 -> 16 -> 3), drawn fp32, stored fp16: W1[width][32], layers - 1
+    matrices [width][width], Wout[3][width]."""
     rng = _rng(seed, 10)
+    shapes = [(width, NEURAL_IN)] + [(width, width)] * (layers - 1) + [(MLP_OUT, width)]
     parts = []
-    for fan_out, fan_in in ((NEURAL_HIDDEN, NEURAL_IN), (NEURAL_HIDDEN, NEURAL_HIDDEN), (MLP_OUT, NEURAL_HIDDEN)):
+    for fan_out, fan_in in shapes:
         lim = math.sqrt(6.0 / (fan_in + fan_out))
         parts.append(rng.uniform(-lim, lim, size=fan_out * fan_in).astype(np.float32))
     w = np.concatenate(parts).astype(np.float16).view(np.uint16)
-    assert w.size == NEURAL_W_COUNT
+    assert w.size == NEURAL_IN * width + (layers - 1) * width * width + MLP_OUT * width
     return np.ascontiguousarray(w)
 
 

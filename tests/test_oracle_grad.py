@@ -18,7 +18,7 @@ import pytest
 from paper_2609_05255_amd import inputs
 
 
-def fd_scene(rng, n, kind):
+def fd_scene(rng, n, kind, arch=None):
     means = rng.uniform(-0.35, 0.35, size=(3, n))
     ls = rng.normal(-1.6, 0.35, size=(3, n))
     q = rng.standard_normal((4, n))
@@ -47,9 +47,11 @@ def fd_scene(rng, n, kind):
         lob[8] = rng.normal(-1.0, 0.5, size=n)              # frequency
         sc.lobes, sc.lobes_gabor = lob[:8].copy(), lob
     else:
+        layers, width, raw16 = arch if arch is not None else (2, 16, 0)
         sc.base_color = rng.normal(0.1, 0.5, size=(3, n))    # some colours clamp at 0
-        sc.features = rng.normal(0.0, 1.5, size=(8, n))
-        sc.neural_w = inputs.make_neural_weights(3).view(np.float16).astype(np.float64) * 1.5
+        sc.features = rng.normal(0.0, 1.5, size=(16 if raw16 else 8, n))
+        sc.neural_w = inputs.make_neural_weights(3, layers, width).view(np.float16).astype(np.float64) * 1.5
+        sc.neural_arch = arch
     return sc
 
 
@@ -75,11 +77,14 @@ GRAD_NAME = {"means": "dmeans", "log_scales": "dlog_scales", "quats": "dquats",
              "lobes_gabor": "dlobes"}
 
 
-@pytest.mark.parametrize("kind", ["sh3", "latent", "neural", "nasg", "nasgabor"])
-def test_gradients_match_finite_differences(orc, kind):
-    rng = np.random.default_rng({"sh3": 42, "latent": 43, "neural": 44, "nasg": 45, "nasgabor": 46}[kind])
+@pytest.mark.parametrize("kind,arch", [("sh3", None), ("latent", None), ("neural", None), ("nasg", None),
+                                       ("nasgabor", None), ("neural", (1, 16, 0)), ("neural", (3, 16, 0)),
+                                       ("neural", (2, 32, 0)), ("neural", (2, 16, 1))])
+def test_gradients_match_finite_differences(orc, kind, arch):
+    rng = np.random.default_rng({"sh3": 42, "latent": 43, "neural": 44, "nasg": 45, "nasgabor": 46}[kind]
+                                + (0 if arch is None else 7 * arch[0] + arch[1] + 3 * arch[2]))
     n = 10
-    sc = fd_scene(rng, n, kind)
+    sc = fd_scene(rng, n, kind, arch)
     cam = inputs.look_at_camera([0.3, -0.4, -2.9], 40, 36, bg=(0.2, 0.3, 0.1))
     g = rng.standard_normal((3, cam.height, cam.width))
     L0, r0 = run(orc, cam, sc, kind, g)

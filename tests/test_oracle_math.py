@@ -109,3 +109,14 @@ def test_paper_printed_values(orc):
     from paper_2609_05255_amd import inputs
     sc = inputs.make_scene("tiny", n=8, appearance=("latent",))
     assert sc.latent.shape[0] * sc.latent.dtype.itemsize == gold["latent_appearance_bytes_measured_decoder"]["value"]
+    # the neural model and its configurations
+    assert orc.neural_weight_count(2, 16) == gold["neural_decoder_parameters"]["value"]
+    assert orc.neural_weight_count(2, 32) == gold["neural_32_wide_macs"]["value"]
+    sc = inputs.make_scene("tiny", n=8, appearance=("neural",))
+    per_g = lambda *arrays: sum(a.shape[0] * a.dtype.itemsize for a in arrays)
+    assert per_g(sc.base_color, sc.features) == gold["neural_appearance_bytes"]["value"]
+    sc = inputs.make_scene("tiny", n=8, appearance=("neural",), neural_arch=(2, 16, 1))
+    assert per_g(sc.base_color, sc.features) == gold["neural_f16_bytes"]["value"]
+    sc = inputs.make_scene("tiny", n=8, appearance=("nasg", "nasgabor"))
+    assert per_g(sc.base_color, sc.lobes) == gold["nasg_appearance_bytes"]["value"]
+    assert per_g(sc.base_color, sc.lobes_gabor) == gold["nasgabor_appearance_bytes"]["value"]

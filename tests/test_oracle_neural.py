@@ -148,3 +148,50 @@ def test_folded_form_has_no_backward(orc):
     r = orc.render(cam, sc, kind="neural_folded", sh_degree=2, mode="f64")
     with pytest.raises(ValueError):
         orc.render_bwd(cam, sc, r["pre"], r["ranges"], r["values"], np.zeros((3, 64, 64)), kind="neural_folded")
+
+
+# ---- the configurations of the paper's architecture table --------------------------
+
+def selector_arch(layers, width, k):
+    """W1 copies input k to hidden unit 0, each hidden-to-hidden layer copies unit 0,
+    the output layer copies it to all three outputs."""
+    w = np.zeros(32 * width + (layers - 1) * width * width + 3 * width, np.float16)
+    w[k] = 1.0
+    off = 32 * width
+    for _ in range(layers - 1):
+        w[off] = 1.0
+        off += width * width
+    for ch in range(3):
+        w[off + ch * width] = 1.0
+    return w.view(np.uint16)
+
+
+@pytest.mark.parametrize("arch", [(1, 16, 0), (3, 16, 0), (2, 32, 0), (3, 32, 0), (2, 16, 1), (1, 16, 1)])
+@pytest.mark.parametrize("k", [1, 16, 27])
+def test_configurations_selector_networks(orc, arch, k):
+    layers, width, raw16 = arch
+    sc = inputs.make_scene("tiny", n=64, appearance=("neural",), neural_arch=arch)
+    sc.neural_w = selector_arch(layers, width, k)
+    cam = inputs.make_cameras("tiny")[0]
+    f = sc.features.view(np.float16).astype(np.float64)
+    d = directions(sc, cam)
+    if k == 1:
+        x = -C1 * d[1]
+    elif raw16:
+        x = f[k - 16]                       # raw features enter as they are
+    else:
+        j = (k - 16) // 2
+        x = np.sin(f[j]) if k % 2 == 0 else np.cos(f[j])
+    expect = np.maximum(0.0, base(sc) + np.tanh(np.maximum(0.0, x))[None] + 0.5)
+    col, vis = colours(orc, sc, cam, 1)
+    assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12)
+
+
+def test_configurations_weight_counts(orc):
+    # the paper's default decoder has 816 parameters (Sec. 4); the table's wider
+    # variant 32 -> 32 -> 32 -> 3 needs 2144 multiply-adds, all of them weights
+    assert orc.neural_weight_count(2, 16) == 816
+    assert orc.neural_weight_count(2, 32) == 2144
+    for arch in [(1, 16, 0), (3, 16, 0), (2, 32, 0)]:
+        sc = inputs.make_scene("tiny", n=8, appearance=("neural",), neural_arch=arch)
+        assert sc.neural_w.size == orc.neural_weight_count(*arch[:2])

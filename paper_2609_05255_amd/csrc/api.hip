@@ -80,11 +80,19 @@ gs_status check_appearance(const gs_appearance* a, int64_t n)
         GS_CHECK(n == 0 || (a->latent != nullptr && a->mlp_w != nullptr), "latent or mlp_w is NULL");
     } else if (a->kind == GS_APP_NEURAL) {
         GS_CHECK(a->sh_degree >= 0 && a->sh_degree <= 3, "sh_degree %d outside 0..3", a->sh_degree);
+        GS_CHECK(a->neural_layers >= 0 && a->neural_layers <= 3, "neural_layers %d outside 0..3", a->neural_layers);
+        GS_CHECK(a->neural_raw16 == 0 || a->neural_raw16 == 1, "neural_raw16 must be 0 or 1");
+        if (a->neural_width != 0 && a->neural_width != 16)
+            return fail(a->neural_width == 32 ? GS_ERR_UNSUPPORTED : GS_ERR_INVALID_ARG,
+                        "neural_width %d: 16 neurons per layer are supported", a->neural_width);
         GS_CHECK(n == 0 || a->base_color != nullptr, "base_color is NULL");
         GS_CHECK(n == 0 || a->sh_degree == 0 || (a->features != nullptr && a->mlp_w != nullptr),
                  "features or mlp_w is NULL");
     } else if (a->kind == GS_APP_NEURAL_FOLDED) {
         GS_CHECK(a->sh_degree >= 0 && a->sh_degree <= 3, "sh_degree %d outside 0..3", a->sh_degree);
+        GS_CHECK((a->neural_layers == 0 || a->neural_layers == 2) && (a->neural_width == 0 || a->neural_width == 16) &&
+                     a->neural_raw16 == 0,
+                 "the folded form takes the paper's default decoder only");
         GS_CHECK(n == 0 || a->base_color != nullptr, "base_color is NULL");
         GS_CHECK(n == 0 || a->sh_degree == 0 || (a->preact != nullptr && a->mlp_w != nullptr),
                  "preact or mlp_w is NULL");
@@ -211,7 +219,7 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.pair_vals_b = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.acc = (float*)take(sizeof(float) * kAccStride * nn);
     w.mlp_part = (float*)take(kind == GS_APP_LATENT_MLP ? sizeof(float) * GS_MLP_WEIGHTS * kMlpPartials
-                              : kind == GS_APP_NEURAL ? sizeof(float) * GS_NEURAL_WEIGHTS * kMlpPartials : 0);
+                              : kind == GS_APP_NEURAL ? sizeof(float) * GS_NEURAL_MAX_WEIGHTS * kMlpPartials : 0);
     w.bytes = off;
     return w;
 }
@@ -398,7 +406,7 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
     const Cam c = make_cam(*cam);
     if (g->n == 0) {
         if (app->kind == GS_APP_LATENT_MLP) GS_HIP(launch_clear(grads->dmlp_w, GS_MLP_WEIGHTS, s));
-        if (app->kind == GS_APP_NEURAL && grads->dmlp_w) GS_HIP(launch_clear(grads->dmlp_w, GS_NEURAL_WEIGHTS, s));
+        if (app->kind == GS_APP_NEURAL && grads->dmlp_w) GS_HIP(launch_clear(grads->dmlp_w, neural_weights(*app), s));
         return ok();
     }
     timing_begin(GS_KERNEL_CLEAR, s);
@@ -412,7 +420,8 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
     timing_end(GS_KERNEL_PREPROCESS_BWD, s);
     if (app->kind == GS_APP_LATENT_MLP || app->kind == GS_APP_NEURAL) {
         timing_begin(GS_KERNEL_MLP_REDUCE, s);
-        GS_HIP(launch_mlp_reduce(g->n, app->kind, ws, grads->dmlp_w, s));
+        GS_HIP(launch_mlp_reduce(g->n, app->kind == GS_APP_NEURAL ? neural_weights(*app) : GS_MLP_WEIGHTS, ws,
+                                 grads->dmlp_w, s));
         timing_end(GS_KERNEL_MLP_REDUCE, s);
     }
     return ok();

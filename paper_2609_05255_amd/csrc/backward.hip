@@ -399,16 +399,20 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
 // directions are staged, each tile of 16 is recomputed and differentiated on
 // the matrix cores (base-colour and feature gradients, the direction gradient
 // of the active bands, the weight-gradient sums), then the geometry backward.
-// While the active degree is 0 only the base colour takes a gradient.
+// While the active degree is 0 only the base colour takes a gradient. L hidden
+// layers; kRaw: 16 raw features as the feature inputs.
+template <int L, bool kRaw>
 __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
 {
-    __shared__ NeuralFrags W;
+    constexpr int kF = kRaw ? 16 : GS_NEURAL_FEATURES;
+    constexpr int kNW = neural_weight_count(L);
+    __shared__ NeuralFrags<L> W;
     __shared__ NeuralBwdStage ST[kBlock / kWave];
     const bool resid = a.sh_degree >= 1;
     if (resid) neural_load_frags(a.mlp_w, W, true);
     const int wave = threadIdx.x >> 6, lane = __lane_id();
     NeuralBwdStage& st = ST[wave];
-    NeuralGradAcc acc;
+    NeuralGradAcc<L> acc;
     neural_grad_zero(acc);
     const int64_t n = a.n;
     const int64_t nchunks = div_up(n, kBlock);
@@ -419,7 +423,7 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
         if (inb && !valid) {
             write_zero_grads(a, (int)i);
             for (int ch = 0; ch < 3; ++ch) a.dbase_color[ch * n + i] = 0.f;
-            for (int j = 0; j < GS_NEURAL_FEATURES; ++j) a.dfeatures[j * n + i] = 0.f;
+            for (int j = 0; j < kF; ++j) a.dfeatures[j * n + i] = 0.f;
         }
         float d[3] = {0.f, 0.f, 0.f}, dc[3] = {0.f, 0.f, 0.f}, c0[3] = {0.f, 0.f, 0.f};
         float len = 1.f;
@@ -437,12 +441,15 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
         }
         float dd[3] = {0.f, 0.f, 0.f};
         if (resid) {
-            float f[GS_NEURAL_FEATURES], sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
-            for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
-                f[j] = valid ? (float)half_of_bits(a.features[j * n + i]) : 0.f;
-            neural_encode_features(f, sf, cf);
+            float f[kF], sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
+            for (int j = 0; j < kF; ++j) f[j] = valid ? (float)half_of_bits(a.features[j * n + i]) : 0.f;
             half4_t fq[4];
-            neural_feature_inputs(sf, cf, fq);
+            if (kRaw) {
+                neural_raw_inputs(f, fq);
+            } else {
+                neural_encode_features(f, sf, cf);
+                neural_feature_inputs(sf, cf, fq);
+            }
             neural_stage_inputs(st.x, valid, d, a.sh_degree, fq);
             wave_lds_sync();
             const uint64_t vis = __ballot(valid);
@@ -479,14 +486,19 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
                 float dY[16];
                 for (int k = 0; k < 16; ++k) dY[k] = k < nb ? row[k] : 0.f;
                 sh_basis16_vjp(d[0], d[1], d[2], dY, dd);
-                // features: d(sin f)/df = cos f, d(cos f)/df = -sin f
-                for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
-                    a.dfeatures[j * n + i] = st.dxf[lane][2 * j] * cf[j] - st.dxf[lane][2 * j + 1] * sf[j];
+                // features: raw ones take their inputs' gradients; encoded ones
+                // d(sin f)/df = cos f, d(cos f)/df = -sin f
+                if (kRaw) {
+                    for (int j = 0; j < 16; ++j) a.dfeatures[j * n + i] = st.dxf[lane][j];
+                } else {
+                    for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
+                        a.dfeatures[j * n + i] = st.dxf[lane][2 * j] * cf[j] - st.dxf[lane][2 * j + 1] * sf[j];
+                }
             }
         } else if (valid) {
             // no residual: c = max(0, c0 + 0.5)
             for (int ch = 0; ch < 3; ++ch) a.dbase_color[ch * n + i] = c0[ch] + 0.5f > 0.f ? dc[ch] : 0.f;
-            for (int j = 0; j < GS_NEURAL_FEATURES; ++j) a.dfeatures[j * n + i] = 0.f;
+            for (int j = 0; j < kF; ++j) a.dfeatures[j * n + i] = 0.f;
         }
         if (valid) {
             float mu[3], ls[3], q[4], g9[kAccStride];
@@ -515,10 +527,10 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
     }
     // workgroup sum of the four waves' weight gradients, in wave order, in the
     // LDS of the (no longer needed) stage
-    static_assert(sizeof(ST) >= GS_NEURAL_WEIGHTS * sizeof(float), "reduction buffer");
+    static_assert(sizeof(ST) >= kNW * sizeof(float), "reduction buffer");
     __syncthreads();
     float* red = reinterpret_cast<float*>(&ST[0]);
-    for (int k = threadIdx.x; k < GS_NEURAL_WEIGHTS; k += kBlock) red[k] = 0.f;
+    for (int k = threadIdx.x; k < kNW; k += kBlock) red[k] = 0.f;
     __syncthreads();
     const int g = lane >> 4, c = lane & 15;
     neural_grad_rescale(acc, 0);   // back to plain units
@@ -527,15 +539,17 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
             for (int e = 0; e < 4; ++e) {
                 const int row = 4 * g + e;
                 for (int fb = 0; fb < 2; ++fb) red[row * kNeuralIn + 16 * fb + c] += acc.w1[fb][e];
-                red[kNeuralHidden * kNeuralIn + row * kNeuralHidden + c] += acc.w2[e];
+                for (int h = 0; h < L - 1; ++h)
+                    red[kNeuralHidden * kNeuralIn + h * kNeuralHidden * kNeuralHidden + row * kNeuralHidden + c] +=
+                        acc.wh[h][e];
                 if (row < GS_MLP_OUT)
-                    red[kNeuralHidden * kNeuralIn + kNeuralHidden * kNeuralHidden + row * kNeuralHidden + c] += acc.w3[e];
+                    red[kNeuralHidden * kNeuralIn + (L - 1) * kNeuralHidden * kNeuralHidden + row * kNeuralHidden + c] +=
+                        acc.w3[e];
             }
         }
         __syncthreads();
     }
-    for (int k = threadIdx.x; k < GS_NEURAL_WEIGHTS; k += kBlock)
-        a.mlp_part[(size_t)blockIdx.x * GS_NEURAL_WEIGHTS + k] = red[k];
+    for (int k = threadIdx.x; k < kNW; k += kBlock) a.mlp_part[(size_t)blockIdx.x * kNW + k] = red[k];
 }
 
 // dW = sum of the per-workgroup partials, in a fixed order. One workgroup per
@@ -609,15 +623,26 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
     else if (app.kind == GS_APP_NASGABOR)
         hipLaunchKernelGGL(k_preprocess_bwd_lobe<true>, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NEURAL)
-        hipLaunchKernelGGL(k_preprocess_bwd_neural, dim3(latent_bwd_grid(g.n)), dim3(kBlock), 0, s, a);
+    {
+        const dim3 grid(latent_bwd_grid(g.n));
+        const int layers = neural_layers(app);
+        if (app.neural_raw16) {
+            if (layers == 1) hipLaunchKernelGGL((k_preprocess_bwd_neural<1, true>), grid, dim3(kBlock), 0, s, a);
+            else if (layers == 3) hipLaunchKernelGGL((k_preprocess_bwd_neural<3, true>), grid, dim3(kBlock), 0, s, a);
+            else hipLaunchKernelGGL((k_preprocess_bwd_neural<2, true>), grid, dim3(kBlock), 0, s, a);
+        } else {
+            if (layers == 1) hipLaunchKernelGGL((k_preprocess_bwd_neural<1, false>), grid, dim3(kBlock), 0, s, a);
+            else if (layers == 3) hipLaunchKernelGGL((k_preprocess_bwd_neural<3, false>), grid, dim3(kBlock), 0, s, a);
+            else hipLaunchKernelGGL((k_preprocess_bwd_neural<2, false>), grid, dim3(kBlock), 0, s, a);
+        }
+    }
     else
         hipLaunchKernelGGL(k_preprocess_bwd_latent, dim3(latent_bwd_grid(g.n)), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 
-hipError_t launch_mlp_reduce(int64_t n, int32_t kind, const Workspace& ws, float* dmlp_w, hipStream_t s)
+hipError_t launch_mlp_reduce(int64_t n, int nw, const Workspace& ws, float* dmlp_w, hipStream_t s)
 {
-    const int nw = kind == GS_APP_NEURAL ? GS_NEURAL_WEIGHTS : GS_MLP_WEIGHTS;
     hipLaunchKernelGGL(k_mlp_reduce, dim3((unsigned)div_up(nw, kReduceCols)), dim3(kReduceRows * kReduceCols), 0, s,
                        ws.mlp_part, latent_bwd_grid(n), nw, dmlp_w);
     return hipGetLastError();

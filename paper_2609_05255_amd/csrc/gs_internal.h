@@ -124,7 +124,7 @@ hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32
 hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                                  const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr,
                                  hipStream_t s);
-hipError_t launch_mlp_reduce(int64_t n, int32_t kind, const Workspace& ws, float* dmlp_w, hipStream_t s);
+hipError_t launch_mlp_reduce(int64_t n, int nw, const Workspace& ws, float* dmlp_w, hipStream_t s);
 hipError_t launch_adam(const gs_adam_tensor* tensors, int count, float beta1, float eps, int64_t step, hipStream_t s);
 hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s);
 hipError_t launch_neural_fold(const uint16_t* features, const uint16_t* w, int64_t n, uint16_t* preact,
@@ -137,5 +137,14 @@ void timing_end(int kernel_id, hipStream_t s);
 inline int preprocess_blocks(int64_t n) { return (int)div_up(n > 0 ? n : 1, kBlock); }
 // Slots for the preprocess tile sums (enough for one per 64 Gaussians).
 inline int pair_count_slots(int64_t n) { return (int)div_up(n > 0 ? n : 1, kWave); }
+
+// Hidden layers of the neural decoder (0 in the struct: the paper's default, 2)
+// and its weight count with 16 neurons per layer.
+inline int neural_layers(const gs_appearance& a) { return a.neural_layers > 0 ? a.neural_layers : 2; }
+inline int neural_weights(const gs_appearance& a)
+{
+    const int L = neural_layers(a);
+    return 16 * 32 + (L - 1) * 16 * 16 + 3 * 16;
+}
 
 }  // namespace gsr

@@ -6,6 +6,10 @@
 // max(0, c0 + residual + 0.5) (eq. common_appearance with the baseline
 // activation). Inputs and hidden activations are binary16 operands, sums fp32.
 //
+// The configurations of the paper's architecture table with 16 neurons per
+// layer are the template parameter L (1..3 hidden layers): W1[16][32], then
+// L - 1 matrices [16][16], then Wout[3][16]; 2 is the paper's default.
+//
 // Fragment layouts and the two orientations are those of mlp.h: layer 1 is one
 // 32-deep product (slot s(g, j) carries input s(g, j)), layers 2 and 3 and every
 // backward product are 16-deep, whose D fragment of one layer is the B fragment
@@ -20,14 +24,18 @@ namespace gsr {
 
 constexpr int kNeuralIn = 32, kNeuralHidden = 16;
 
-// Per-workgroup weight fragments (W1[16][32], W2[16][16], W3[3][16], binary16).
+constexpr int neural_weight_count(int layers) { return kNeuralHidden * kNeuralIn + (layers - 1) * kNeuralHidden * kNeuralHidden + GS_MLP_OUT * kNeuralHidden; }
+
+// Per-workgroup weight fragments of a decoder with L hidden layers (binary16).
+template <int L>
 struct NeuralFrags {
+    static constexpr int kH = L > 1 ? L - 1 : 1;   // hidden-to-hidden matrices (at least one slot)
     alignas(16) _Float16 w1a[kWave][8];     // A of W1:   rows n1 = c,             K = input s(g, j)
-    alignas(8) _Float16 w2a[kWave][4];      // A of W2:   rows n2 = c,             K = n1 = 4g + j
-    alignas(8) _Float16 w3a[kWave][4];      // A of W3:   rows o = c (< 3),        K = n2 = 4g + j
+    alignas(8) _Float16 wha[kH][kWave][4];  // A of W_l:  rows n_l = c,            K = n_(l-1) = 4g + j
+    alignas(8) _Float16 w3a[kWave][4];      // A of Wout: rows o = c (< 3),        K = n_L = 4g + j
     alignas(8) _Float16 w1t[2][kWave][4];   // A of W1^T: rows input = 16b + c,   K = n1 = 4g + j
-    alignas(8) _Float16 w2t[kWave][4];      // A of W2^T: rows n1 = c,             K = n2 = 4g + j
-    alignas(8) _Float16 w3t[kWave][4];      // A of W3^T: rows n2 = c,             K = o = 4g + j (< 3)
+    alignas(8) _Float16 wht[kH][kWave][4];  // A of W_l^T: rows n_(l-1) = c,       K = n_l = 4g + j
+    alignas(8) _Float16 w3t[kWave][4];      // A of Wout^T: rows n_L = c,          K = o = 4g + j (< 3)
     alignas(8) _Float16 w1d[kWave][4];      // A of W1's direction columns 1..15 (folded form):
                                             //            rows n1 = c, K = 4g + j -> column 1 + 4g + j (< 16)
 };
@@ -35,24 +43,29 @@ struct NeuralFrags {
 // Loads the weights into the fragments (the transposed ones only if
 // `backward`, the direction columns only if `folded`). Called by every thread
 // of the workgroup; ends with a barrier.
-__device__ __forceinline__ void neural_load_frags(const uint16_t* __restrict__ w, NeuralFrags& s, bool backward,
+template <int L>
+__device__ __forceinline__ void neural_load_frags(const uint16_t* __restrict__ w, NeuralFrags<L>& s, bool backward,
                                                   bool folded = false)
 {
     const _Float16* W1 = reinterpret_cast<const _Float16*>(w);
-    const _Float16* W2 = W1 + kNeuralHidden * kNeuralIn;
-    const _Float16* W3 = W2 + kNeuralHidden * kNeuralHidden;
+    const _Float16* Wh = W1 + kNeuralHidden * kNeuralIn;                       // [L-1][16][16]
+    const _Float16* W3 = Wh + (L - 1) * kNeuralHidden * kNeuralHidden;         // [3][16]
     const _Float16 z = (_Float16)0.f;
     for (int e = threadIdx.x; e < kWave * 8; e += blockDim.x) {
         const int l = e >> 3, j = e & 7, g = l >> 4, c = l & 15;
         s.w1a[l][j] = W1[c * kNeuralIn + kslot(g, j)];
         if (j < 4) {
             const int k = 4 * g + j;
-            s.w2a[l][j] = W2[c * kNeuralHidden + k];
+#pragma unroll
+            for (int h = 0; h < L - 1; ++h) {
+                const _Float16* Wl = Wh + h * kNeuralHidden * kNeuralHidden;
+                s.wha[h][l][j] = Wl[c * kNeuralHidden + k];
+                if (backward) s.wht[h][l][j] = Wl[k * kNeuralHidden + c];
+            }
             s.w3a[l][j] = c < GS_MLP_OUT ? W3[c * kNeuralHidden + k] : z;
             if (folded) s.w1d[l][j] = k < 15 ? W1[c * kNeuralIn + 1 + k] : z;
             if (backward) {
                 for (int b = 0; b < 2; ++b) s.w1t[b][l][j] = W1[k * kNeuralIn + 16 * b + c];
-                s.w2t[l][j] = W2[k * kNeuralHidden + c];
                 s.w3t[l][j] = k < GS_MLP_OUT ? W3[k * kNeuralHidden + c] : z;
             }
         }
@@ -130,6 +143,14 @@ __device__ __forceinline__ void neural_feature_inputs(const float sf[GS_NEURAL_F
         q[k] = half4_t{(_Float16)sf[2 * k], (_Float16)cf[2 * k], (_Float16)sf[2 * k + 1], (_Float16)cf[2 * k + 1]};
 }
 
+// The 16 raw features as the feature inputs (the table's F = 16 configuration).
+__device__ __forceinline__ void neural_raw_inputs(const float f[16], half4_t q[4])
+{
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+        q[k] = half4_t{(_Float16)f[4 * k], (_Float16)f[4 * k + 1], (_Float16)f[4 * k + 2], (_Float16)f[4 * k + 3]};
+}
+
 // The calling lane's decoder input: SH basis values of d for bands <= degree
 // (zero above), then the feature inputs `fq` (neural_feature_inputs), in
 // binary16 (zeros when !valid).
@@ -175,16 +196,18 @@ __device__ __forceinline__ void neural_stage_dir(_Float16 (*x)[kXPitch], bool va
 // Output pre-activations of tile t in the folded form: h1 = p + W1d xd with the
 // Gaussians' pre-activations p as the accumulator input (p4: neurons 4g + i of
 // Gaussian 16t + c, this lane's share), then layers 2 and 3 as unfolded.
-__device__ __forceinline__ float4_t neural_tile_out_folded(const NeuralFrags& W, const _Float16 (*x)[kXPitch], int t,
-                                                           const half4_t& p4)
+template <int L>
+__device__ __forceinline__ float4_t neural_tile_out_folded(const NeuralFrags<L>& W, const _Float16 (*x)[kXPitch],
+                                                           int t, const half4_t& p4)
 {
     const int l = __lane_id(), g = l >> 4, c = l & 15;
     const float4_t zero = {0.f, 0.f, 0.f, 0.f};
     const half4_t xd = *reinterpret_cast<const half4_t*>(&x[16 * t + c][4 * g]);
     const float4_t p = {(float)p4[0], (float)p4[1], (float)p4[2], (float)p4[3]};
-    const half4_t a1 = relu_half4(mfma16(frag4(W.w1d), xd, p));
-    const half4_t a2 = relu_half4(mfma16(frag4(W.w2a), a1, zero));
-    return mfma16(frag4(W.w3a), a2, zero);
+    half4_t a = relu_half4(mfma16(frag4(W.w1d), xd, p));
+#pragma unroll
+    for (int h = 0; h < L - 1; ++h) a = relu_half4(mfma16(frag4(W.wha[h]), a, zero));
+    return mfma16(frag4(W.w3a), a, zero);
 }
 
 // B fragment of tile t: inputs s(g, 0..7) of Gaussian 16t + c.
@@ -194,20 +217,6 @@ __device__ __forceinline__ half8_t neural_stage_frag(const _Float16 (*x)[kXPitch
     const half4_t lo = *reinterpret_cast<const half4_t*>(&x[16 * t + c][4 * g]);
     const half4_t hi = *reinterpret_cast<const half4_t*>(&x[16 * t + c][16 + 4 * g]);
     return half8_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-}
-
-// Neuron-major forward of one tile: h1, h2 the fp32 pre-activations of neurons
-// 4g + i of Gaussian c, a1, a2 their binary16 activations (next B fragments),
-// o the output pre-activations (channel i of Gaussian c in lanes 0..15, i < 3).
-__device__ __forceinline__ void neural_tile_fwd(const NeuralFrags& W, const half8_t& x, float4_t& h1, half4_t& a1,
-                                                float4_t& h2, half4_t& a2, float4_t& o)
-{
-    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
-    h1 = mfma32(frag8(W.w1a), x, zero);
-    a1 = relu_half4(h1);
-    h2 = mfma16(frag4(W.w2a), a1, zero);
-    a2 = relu_half4(h2);
-    o = mfma16(frag4(W.w3a), a2, zero);
 }
 
 // Hands the output pre-activations o of tile t to the lanes that own its
@@ -223,37 +232,45 @@ __device__ __forceinline__ void neural_tile_gather(const float4_t& o, int t, flo
     }
 }
 
-// Output pre-activations of tile t alone (the backward's first pass).
-__device__ __forceinline__ float4_t neural_tile_out(const NeuralFrags& W, const half8_t& x)
+// Output pre-activations of one tile (channel i of Gaussian c in lanes g = 0).
+template <int L>
+__device__ __forceinline__ float4_t neural_tile_out(const NeuralFrags<L>& W, const half8_t& x)
 {
     const float4_t zero = {0.f, 0.f, 0.f, 0.f};
-    const half4_t a1 = relu_half4(mfma32(frag8(W.w1a), x, zero));
-    const half4_t a2 = relu_half4(mfma16(frag4(W.w2a), a1, zero));
-    return mfma16(frag4(W.w3a), a2, zero);
+    half4_t a = relu_half4(mfma32(frag8(W.w1a), x, zero));
+#pragma unroll
+    for (int h = 0; h < L - 1; ++h) a = relu_half4(mfma16(frag4(W.wha[h]), a, zero));
+    return mfma16(frag4(W.w3a), a, zero);
 }
 
 // Running sums of the weight gradients (Gaussian-major products, fp32, in
-// units of 2^-se): w1[fb] rows n1 = 4g + i, columns input 16fb + c; w2 rows
-// n2 = 4g + i, columns n1 = c; w3 rows o = 4g + i, columns n2 = c.
+// units of 2^-se): w1[fb] rows n1 = 4g + i, columns input 16fb + c; wh[h] rows
+// n_(h+2) = 4g + i, columns n_(h+1) = c; w3 rows o = 4g + i, columns n_L = c.
+template <int L>
 struct NeuralGradAcc {
-    float4_t w1[2], w2, w3;
+    float4_t w1[2], wh[NeuralFrags<L>::kH], w3;
     int se;
 };
 
-__device__ __forceinline__ void neural_grad_zero(NeuralGradAcc& a)
+template <int L>
+__device__ __forceinline__ void neural_grad_zero(NeuralGradAcc<L>& a)
 {
     const float4_t z = {0.f, 0.f, 0.f, 0.f};
-    a.w1[0] = a.w1[1] = a.w2 = a.w3 = z;
+    a.w1[0] = a.w1[1] = a.w3 = z;
+#pragma unroll
+    for (int h = 0; h < NeuralFrags<L>::kH; ++h) a.wh[h] = z;
     a.se = 0;
 }
 
-__device__ __forceinline__ void neural_grad_rescale(NeuralGradAcc& a, int se)
+template <int L>
+__device__ __forceinline__ void neural_grad_rescale(NeuralGradAcc<L>& a, int se)
 {
     if (se == a.se) return;
     const int e = se - a.se;
     a.w1[0] = ldexp4(a.w1[0], e);
     a.w1[1] = ldexp4(a.w1[1], e);
-    a.w2 = ldexp4(a.w2, e);
+#pragma unroll
+    for (int h = 0; h < L - 1; ++h) a.wh[h] = ldexp4(a.wh[h], e);
     a.w3 = ldexp4(a.w3, e);
     a.se = se;
 }
@@ -273,14 +290,15 @@ __device__ __forceinline__ int neural_chunk_exponent(float m, int prev)
 // Backward of tile t (Gaussians 16t .. 16t + 15 of the wave) from the staged
 // inputs and output gradients delta3 = dL/dc [c0 + res + 0.5 > 0] (1 - res^2),
 // with the chunk's gradient scale 2^se (acc.se): delta3 enters the matrix
-// cores scaled; dH2, dH1 and dX are chained neuron-major (binary16 hi + lo
-// operands); the Gaussian-major copies give
-//   dW3 = sum_G delta3 h2^T, dW2 = sum_G dh2 h1^T, dW1 = sum_G dh1 x^T
+// cores scaled; the hidden-layer gradients and dX are chained neuron-major
+// (binary16 hi + lo operands); the Gaussian-major copies give
+//   dWout = sum_G delta3 h_L^T, dW_l = sum_G dh_l h_(l-1)^T, dW1 = sum_G dh_1 x^T
 // accumulated into `acc`. Leaves the gradients of the 16 feature inputs in
 // st.dxf and, once the tile's reads of its input rows are issued, those of the
 // 16 direction inputs in the same rows (fp32, every band; the caller masks).
-__device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdStage& st, int t, float scale,
-                                                float inv, NeuralGradAcc& acc)
+template <int L>
+__device__ __forceinline__ void neural_tile_bwd(const NeuralFrags<L>& W, NeuralBwdStage& st, int t, float scale,
+                                                float inv, NeuralGradAcc<L>& acc)
 {
     const int l = __lane_id(), g = l >> 4, c = l & 15;
     const float4_t zero = {0.f, 0.f, 0.f, 0.f};
@@ -291,12 +309,20 @@ __device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdS
     for (int fb = 0; fb < 2; ++fb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) xg[fb][j] = st.x[16 * t + 4 * g + j][16 * fb + c];
-    // forward, both orientations (the output layer is not needed again)
-    const float4_t h1n = mfma32(frag8(W.w1a), x, zero);
-    const half4_t a1 = relu_half4(h1n);
-    const float4_t h2n = mfma16(frag4(W.w2a), a1, zero);
-    const float4_t h1g = mfma32(x, frag8(W.w1a), zero);    // h1[G = 4g+i][n1 = c]
-    const float4_t h2g = mfma16(a1, frag4(W.w2a), zero);   // h2[G = 4g+i][n2 = c]
+    // forward of the hidden layers, both orientations (the output layer is not
+    // needed again): hn[l] neurons 4g + i of Gaussian c, hg[l] Gaussian 4g + i,
+    // neuron c
+    float4_t hn[L], hg[L];
+    half4_t an[L];
+    hn[0] = mfma32(frag8(W.w1a), x, zero);
+    hg[0] = mfma32(x, frag8(W.w1a), zero);
+    an[0] = relu_half4(hn[0]);
+#pragma unroll
+    for (int h = 1; h < L; ++h) {
+        hn[h] = mfma16(frag4(W.wha[h - 1]), an[h - 1], zero);
+        hg[h] = mfma16(an[h - 1], frag4(W.wha[h - 1]), zero);
+        an[h] = relu_half4(hn[h]);
+    }
 
     // output gradients: neuron-major (channel i of Gaussian c, in lanes g = 0)
     // and Gaussian-major (Gaussian 4g + i, channel c < 3; column 3 is zero)
@@ -308,28 +334,32 @@ __device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdS
     const int cn = min(c, 3);
 #pragma unroll
     for (int i = 0; i < 4; ++i) d3g[i] = st.d3[16 * t + 4 * g + i][cn] * scale;
-    half4_t d3n_hi, d3n_lo;
-    split4(d3n, d3n_hi, d3n_lo);
-    const half4_t d3g_h = half4_t{(_Float16)d3g[0], (_Float16)d3g[1], (_Float16)d3g[2], (_Float16)d3g[3]};
+    half4_t hi, lo;
+    split4(d3n, hi, lo);
+    acc.w3 = mfma16(half4_t{(_Float16)d3g[0], (_Float16)d3g[1], (_Float16)d3g[2], (_Float16)d3g[3]},
+                    relu_half4(hg[L - 1]), acc.w3);                                   // dWout[o][n_L]
 
-    // dH2 = W3^T delta3, masked by relu'(h2)
+    // dH_L = Wout^T delta3, masked by relu'(h_L)
     const half4_t w3t = frag4(W.w3t);
-    const float4_t g2n = relu_mask(mfma16(w3t, d3n_lo, mfma16(w3t, d3n_hi, zero)), h2n);
-    const float4_t g2g = relu_mask(mfma16(d3n_lo, w3t, mfma16(d3n_hi, w3t, zero)), h2g);
-    half4_t g2n_hi, g2n_lo;
-    split4(g2n, g2n_hi, g2n_lo);
-    // dH1 = W2^T dH2, masked by relu'(h1)
-    const half4_t w2t = frag4(W.w2t);
-    const float4_t g1n = relu_mask(mfma16(w2t, g2n_lo, mfma16(w2t, g2n_hi, zero)), h1n);
-    const float4_t g1g = relu_mask(mfma16(g2n_lo, w2t, mfma16(g2n_hi, w2t, zero)), h1g);
-    half4_t g1n_hi, g1n_lo;
-    split4(g1n, g1n_hi, g1n_lo);
+    float4_t gn = relu_mask(mfma16(w3t, lo, mfma16(w3t, hi, zero)), hn[L - 1]);
+    float4_t gg = relu_mask(mfma16(lo, w3t, mfma16(hi, w3t, zero)), hg[L - 1]);
+    // dH_(l-1) = W_l^T dH_l, masked by relu'(h_(l-1)); dW_l from the Gaussian-major copies
+#pragma unroll
+    for (int h = L - 1; h >= 1; --h) {
+        acc.wh[h - 1] = mfma16(half4_t{(_Float16)gg[0], (_Float16)gg[1], (_Float16)gg[2], (_Float16)gg[3]},
+                               relu_half4(hg[h - 1]), acc.wh[h - 1]);                 // dW_h[n_h][n_(h-1)]
+        split4(gn, hi, lo);
+        const half4_t wt = frag4(W.wht[h - 1]);
+        gn = relu_mask(mfma16(wt, lo, mfma16(wt, hi, zero)), hn[h - 1]);
+        gg = relu_mask(mfma16(lo, wt, mfma16(hi, wt, zero)), hg[h - 1]);
+    }
+    split4(gn, hi, lo);
     // dX = W1^T dH1: dx[b] holds inputs 16b + 4g + i of Gaussian c
     float4_t dx[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
         const half4_t w = frag4(W.w1t[b]);
-        dx[b] = mfma16(w, g1n_lo, mfma16(w, g1n_hi, zero)) * inv;
+        dx[b] = mfma16(w, lo, mfma16(w, hi, zero)) * inv;
     }
     // the tile's input rows have been read: they now take the direction-input
     // gradients
@@ -341,12 +371,8 @@ __device__ __forceinline__ void neural_tile_bwd(const NeuralFrags& W, NeuralBwdS
         st.dxf[Gn][4 * g + i] = dx[1][i];
     }
 
-    // weight gradients from the Gaussian-major fragments, accumulated in place
-    const half4_t r1g = relu_half4(h1g), r2g = relu_half4(h2g);
-    acc.w3 = mfma16(d3g_h, r2g, acc.w3);                                            // dW3[o][n2]
-    const half4_t h2d = {(_Float16)g2g[0], (_Float16)g2g[1], (_Float16)g2g[2], (_Float16)g2g[3]};
-    acc.w2 = mfma16(h2d, r1g, acc.w2);                                              // dW2[n2][n1]
-    const half4_t h1d = {(_Float16)g1g[0], (_Float16)g1g[1], (_Float16)g1g[2], (_Float16)g1g[3]};
+    // dW1 from the Gaussian-major dH1 and inputs, accumulated in place
+    const half4_t h1d = {(_Float16)gg[0], (_Float16)gg[1], (_Float16)gg[2], (_Float16)gg[3]};
 #pragma unroll
     for (int fb = 0; fb < 2; ++fb) acc.w1[fb] = mfma16(h1d, xg[fb], acc.w1[fb]);   // dW1[n1][input]
 }

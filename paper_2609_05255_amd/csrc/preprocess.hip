@@ -406,11 +406,13 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_latent(PreArgs a)
 // chunks on their own, the base colour and feature loads issued before the
 // geometry. kFolded: the render-only folded form, whose first layer adds the
 // stored pre-activations of the view-independent inputs to the direction
-// columns' product (no features, no sin/cos).
-template <bool kFolded>
+// columns' product (no features, no sin/cos). L hidden layers; kRaw: 16 raw
+// features as the feature inputs (the architecture table's configurations).
+template <bool kFolded, int L, bool kRaw>
 __global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
 {
-    __shared__ NeuralFrags W;
+    constexpr int kF = kRaw ? 16 : GS_NEURAL_FEATURES;
+    __shared__ NeuralFrags<L> W;
     __shared__ NeuralInStage XS[kBlock / kWave];
     __shared__ SplatStage stage[kBlock / kWave];
     const bool resid = a.sh_degree >= 1;
@@ -422,10 +424,10 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
         const int64_t base = chunk * kWave;
         const int i = (int)(base + lane);
         // appearance loads first, so that they overlap the projection
-        float c0[3] = {0.f, 0.f, 0.f}, f[GS_NEURAL_FEATURES];
+        float c0[3] = {0.f, 0.f, 0.f}, f[kF];
         half4_t p4[kWave / 16];   // folded: neurons 4g..4g+3 of Gaussian base + 16t + c
 #pragma unroll
-        for (int j = 0; j < GS_NEURAL_FEATURES; ++j) f[j] = 0.f;
+        for (int j = 0; j < kF; ++j) f[j] = 0.f;
 #pragma unroll
         for (int t = 0; t < kWave / 16; ++t) p4[t] = half4_t{0, 0, 0, 0};
         if (i < a.n) {
@@ -433,8 +435,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
             for (int ch = 0; ch < 3; ++ch) c0[ch] = a.base_color[(int64_t)ch * a.n + i];
             if (resid && !kFolded)
 #pragma unroll
-                for (int j = 0; j < GS_NEURAL_FEATURES; ++j)
-                    f[j] = (float)half_of_bits(a.features[(int64_t)j * a.n + i]);
+                for (int j = 0; j < kF; ++j) f[j] = (float)half_of_bits(a.features[(int64_t)j * a.n + i]);
         }
         if (resid && kFolded) {
             const int g4 = lane >> 4, c = lane & 15;
@@ -464,10 +465,14 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
             if (kFolded) {
                 neural_stage_dir(XS[wave].x, g.visible, d, a.sh_degree);
             } else {
-                float sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
                 half4_t fq[4];
-                neural_encode_features(f, sf, cf);
-                neural_feature_inputs(sf, cf, fq);
+                if (kRaw) {
+                    neural_raw_inputs(f, fq);
+                } else {
+                    float sf[GS_NEURAL_FEATURES], cf[GS_NEURAL_FEATURES];
+                    neural_encode_features(f, sf, cf);
+                    neural_feature_inputs(sf, cf, fq);
+                }
                 neural_stage_inputs(XS[wave].x, g.visible, d, a.sh_degree, fq);
             }
             wave_lds_sync();
@@ -534,14 +539,26 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
         default: hipLaunchKernelGGL(k_preprocess_sh3<3>, dim3(blocks), dim3(kBlock), 0, s, a); break;
         }
     }
-    else if (app.kind == GS_APP_NEURAL)
-        hipLaunchKernelGGL(k_preprocess_neural<false>, dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0, s, a);
+    else if (app.kind == GS_APP_NEURAL) {
+        const dim3 grid(std::min(blocks, kNeuralBlocks));
+        const int layers = neural_layers(app);
+        if (app.neural_raw16) {
+            if (layers == 1) hipLaunchKernelGGL((k_preprocess_neural<false, 1, true>), grid, dim3(kBlock), 0, s, a);
+            else if (layers == 3) hipLaunchKernelGGL((k_preprocess_neural<false, 3, true>), grid, dim3(kBlock), 0, s, a);
+            else hipLaunchKernelGGL((k_preprocess_neural<false, 2, true>), grid, dim3(kBlock), 0, s, a);
+        } else {
+            if (layers == 1) hipLaunchKernelGGL((k_preprocess_neural<false, 1, false>), grid, dim3(kBlock), 0, s, a);
+            else if (layers == 3) hipLaunchKernelGGL((k_preprocess_neural<false, 3, false>), grid, dim3(kBlock), 0, s, a);
+            else hipLaunchKernelGGL((k_preprocess_neural<false, 2, false>), grid, dim3(kBlock), 0, s, a);
+        }
+    }
     else if (app.kind == GS_APP_NASG)
         hipLaunchKernelGGL(k_preprocess_lobe<false>, dim3(blocks), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NASGABOR)
         hipLaunchKernelGGL(k_preprocess_lobe<true>, dim3(blocks), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NEURAL_FOLDED)
-        hipLaunchKernelGGL(k_preprocess_neural<true>, dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL((k_preprocess_neural<true, 2, false>), dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0,
+                           s, a);
     else
         hipLaunchKernelGGL(k_preprocess_latent, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
     return hipGetLastError();
@@ -638,7 +655,7 @@ __global__ __launch_bounds__(kBlock) void k_neural_fold(const uint16_t* __restri
                                                         const uint16_t* __restrict__ w, int n,
                                                         uint16_t* __restrict__ preact)
 {
-    __shared__ NeuralFrags W;
+    __shared__ NeuralFrags<2> W;
     __shared__ NeuralInStage XS[kBlock / kWave];
     neural_load_frags(w, W, false);
     const int lane = __lane_id(), wave = threadIdx.x >> 6, g = lane >> 4, c = lane & 15;

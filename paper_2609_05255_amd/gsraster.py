@@ -24,6 +24,12 @@ GS_APP_SH3, GS_APP_LATENT_MLP, GS_APP_NEURAL, GS_APP_NEURAL_FOLDED, GS_APP_NASG,
 LOBE_ROWS = {GS_APP_NASG: 8, GS_APP_NASGABOR: 9}
 NEURAL_FEATURES = 8
 NEURAL_WEIGHTS = 816
+
+
+def neural_weight_count(arch=None) -> int:
+    """Weights of the neural decoder with arch = (hidden layers, width, raw16); None: the paper's (2, 16, 0)."""
+    layers, width = (2, 16) if arch is None else (int(arch[0]), int(arch[1]))
+    return 32 * width + (layers - 1) * width * width + 3 * width
 KERNEL_NAMES = ["preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
                 "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam", "neural_fold"]
 ADAM_MAX_TENSORS = 8
@@ -52,7 +58,8 @@ class Gaussians(C.Structure):
 class Appearance(C.Structure):
     _fields_ = [("kind", C.c_int32), ("sh_degree", C.c_int32), ("sh", C.c_void_p), ("latent", C.c_void_p),
                 ("mlp_w", C.c_void_p), ("base_color", C.c_void_p), ("features", C.c_void_p),
-                ("preact", C.c_void_p), ("lobes", C.c_void_p), ("sh_y0_folded", C.c_int32)]
+                ("preact", C.c_void_p), ("lobes", C.c_void_p), ("sh_y0_folded", C.c_int32),
+                ("neural_layers", C.c_int32), ("neural_width", C.c_int32), ("neural_raw16", C.c_int32)]
 
 
 class Preprocessed(C.Structure):
@@ -161,6 +168,7 @@ class SceneTensors:
         self.neural_w = h16(scene.neural_w) if getattr(scene, "neural_w", None) is not None else None
         self.preact = None   # [n][16] binary16 pre-activations of the folded form (fold_neural)
         self.sh_y0_folded = bool(getattr(scene, "sh_y0_folded", False))
+        self.neural_arch = getattr(scene, "neural_arch", None)
         self.lobes = f32(scene.lobes) if getattr(scene, "lobes", None) is not None else None
         self.lobes_gabor = f32(scene.lobes_gabor) if getattr(scene, "lobes_gabor", None) is not None else None
 
@@ -177,8 +185,9 @@ class SceneTensors:
 
     def appearance(self, kind: int, sh_degree: int = 3) -> Appearance:
         if kind == GS_APP_NEURAL:
+            layers, width, raw16 = self.neural_arch if self.neural_arch is not None else (0, 0, 0)
             return Appearance(kind, sh_degree, None, None, _ptr(self.neural_w), _ptr(self.base_color),
-                              _ptr(self.features), None, None)
+                              _ptr(self.features), None, None, 0, layers, width, raw16)
         if kind == GS_APP_NEURAL_FOLDED:
             if self.preact is None:
                 raise RuntimeError("fold_neural() first: the folded form reads its pre-activations")
@@ -270,7 +279,7 @@ class Frame:
     """Device buffers for rendering one image of a scene and its backward pass."""
 
     def __init__(self, n: int, width: int, height: int, kind: int, capacity: int, device="cuda",
-                 want_tile_ids: bool = False, want_dmean2d: bool = False):
+                 want_tile_ids: bool = False, want_dmean2d: bool = False, neural_arch=None):
         self.n, self.width, self.height, self.kind, self.capacity = n, width, height, kind, capacity
         d = device
         nn = max(n, 1)
@@ -294,10 +303,11 @@ class Frame:
         self.dsh = torch.empty(48, nn, device=d) if kind == GS_APP_SH3 else None
         self.dlatent = torch.empty(14, nn, device=d) if kind == GS_APP_LATENT_MLP else None
         self.dmlp_w = (torch.empty(MLP_WEIGHTS, device=d) if kind == GS_APP_LATENT_MLP else
-                       torch.empty(NEURAL_WEIGHTS, device=d) if kind == GS_APP_NEURAL else None)
+                       torch.empty(neural_weight_count(neural_arch), device=d) if kind == GS_APP_NEURAL else None)
         self.dmean2d = torch.empty(2, nn, device=d) if want_dmean2d else None
         self.dbase_color = torch.empty(3, nn, device=d) if kind in (GS_APP_NEURAL, *LOBE_ROWS) else None
-        self.dfeatures = torch.empty(NEURAL_FEATURES, nn, device=d) if kind == GS_APP_NEURAL else None
+        raw16 = neural_arch is not None and bool(neural_arch[2])
+        self.dfeatures = torch.empty(16 if raw16 else NEURAL_FEATURES, nn, device=d) if kind == GS_APP_NEURAL else None
         self.dlobes = torch.empty(LOBE_ROWS[kind], nn, device=d) if kind in LOBE_ROWS else None
         self.pre = Preprocessed(_ptr(self.splats), _ptr(self.tiles_touched), _ptr(self.depth_key),
                                 _ptr(self.num_pairs))

@@ -77,7 +77,7 @@ class FusedAdam:
             self.features32 = scene.features.view(torch.float16).float().contiguous()
             self.mlp32 = scene.neural_w.view(torch.float16).float().contiguous()
             add(scene.base_color, frame.dbase_color, [LR_BASE_COLOR] * 3)
-            add(self.features32, frame.dfeatures, [LR_FEATURES] * NEURAL_FEATURES, half=scene.features)
+            add(self.features32, frame.dfeatures, [LR_FEATURES] * scene.features.shape[0], half=scene.features)
             add(self.mlp32, frame.dmlp_w, [LR_MLP], beta2=BETA2_MLP, half=scene.neural_w)
         else:
             self.latent32 = scene.latent.view(torch.float16).float().contiguous()

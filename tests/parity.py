@@ -40,8 +40,9 @@ def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None, 
     cs = gs.camera_struct(cam)
     if capacity is None:
         capacity = 1 << 16
+    arch = getattr(scene, "neural_arch", None)
     fr = gs.Frame(scene.n, cam.width, cam.height, kind_id(kind), capacity, want_tile_ids=extras,
-                  want_dmean2d=extras)
+                  want_dmean2d=extras, neural_arch=arch)
     g, app = st.gaussians(), st.appearance(kind_id(kind), sh_degree)
     P = gs.gs_preprocess(cs, g, app, fr.pre, fr.workspace, fr.ws_bytes)
     if P > capacity:
@@ -53,7 +54,7 @@ def run_gpu(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, capacity=None, 
         except gs.GsError as e:
             assert e.status == gs.GS_ERR_CAPACITY
         fr = gs.Frame(scene.n, cam.width, cam.height, kind_id(kind), int(P), want_tile_ids=extras,
-                      want_dmean2d=extras)
+                      want_dmean2d=extras, neural_arch=arch)
         P = gs.gs_preprocess(cs, g, app, fr.pre, fr.workspace, fr.ws_bytes)
     gs.gs_bin_sort(cs, fr.pre, scene.n, P, fr.capacity, fr.values, fr.tile_ids, fr.ranges, fr.workspace, fr.ws_bytes)
     gs.gs_render_fwd(cs, fr.pre, scene.n, fr.values, fr.ranges, fr.image, fr.final_T, fr.n_contrib)

@@ -269,3 +269,16 @@ def test_tiny_scene_sh_y0_folded(degree):
     sc.sh[0:3] *= np.float32(0.28209479177387814)
     sc.sh_y0_folded = True
     check_all(sc, tiny_camera(), sh_degree=degree, label="tiny-sh-y0-folded")
+
+
+# ---- the neural decoder configurations of the paper's architecture table ---------
+
+@pytest.mark.parametrize("arch", [(1, 16, 0), (3, 16, 0), (2, 16, 1), (3, 16, 1)])
+def test_tiny_scene_neural_configurations(arch):
+    sc = inputs.make_scene("tiny", appearance=("neural",), neural_arch=arch)
+    check_all(sc, tiny_camera(), kind="neural", sh_degree=3, label="tiny-neural-%d-%d-%d" % arch)
+
+
+def test_medium_scene_neural_three_layers():
+    sc = inputs.make_scene("medium", appearance=("neural",), neural_arch=(3, 16, 0))
+    check_all(sc, inputs.make_cameras("medium")[2], kind="neural", label="medium-neural-3-16-0")

@@ -55,16 +55,16 @@ __global__ __launch_bounds__(kBlock) void k_adam(AdamArgs a)
     const int64_t e0 = c * kChunk + threadIdx.x;
     const int64_t rbase = (int64_t)row * T.n;
     float g[kItems], m[kItems], v[kItems], p[kItems];
-    // all loads first
+    // all loads first; every element is streamed once: non-temporal accesses
 #pragma unroll
     for (int j = 0; j < kItems; ++j) {
         const int64_t e = e0 + (int64_t)j * kBlock;
         if (e < T.n) {
             const int64_t i = rbase + e;
-            g[j] = T.g[i];
-            m[j] = T.m[i];
-            v[j] = T.v[i];
-            p[j] = T.p[i];
+            g[j] = __builtin_nontemporal_load(T.g + i);
+            m[j] = __builtin_nontemporal_load(T.m + i);
+            v[j] = __builtin_nontemporal_load(T.v + i);
+            p[j] = __builtin_nontemporal_load(T.p + i);
         }
     }
 #pragma unroll
@@ -76,10 +76,10 @@ __global__ __launch_bounds__(kBlock) void k_adam(AdamArgs a)
         const float vj = T.b2 * v[j] + T.omb2 * (g[j] * g[j]);
         const float denom = sqrtf(vj) * T.inv_sqrt_bc2 + a.eps;
         const float pj = p[j] - step * (mj / denom);
-        T.m[i] = mj;
-        T.v[i] = vj;
-        T.p[i] = pj;
-        if (T.h) T.h[i] = __builtin_bit_cast(uint16_t, (_Float16)pj);
+        __builtin_nontemporal_store(mj, T.m + i);
+        __builtin_nontemporal_store(vj, T.v + i);
+        __builtin_nontemporal_store(pj, T.p + i);
+        if (T.h) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (_Float16)pj), T.h + i);
     }
 }
 

@@ -169,7 +169,8 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
     if (i >= a.n) return;
     const int64_t n = a.n;
     // Culled Gaussians take the same store instructions with zeros, so every
-    // gradient plane is written once per wave with whole lines.
+    // gradient plane is written once per wave with whole lines. Parameters,
+    // accumulators and gradients are touched once: non-temporal accesses.
     const bool vis = a.tiles_touched[i] != 0;
     GeoGrad gg;
     for (int j = 0; j < 3; ++j) { gg.dmu[j] = 0.f; gg.dls[j] = 0.f; }
@@ -182,11 +183,11 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
     const int nb = (a.sh_degree + 1) * (a.sh_degree + 1);
     if (vis) {
         float mu[3], ls[3], q[4];
-        for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
-        for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
-        for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
+        for (int j = 0; j < 3; ++j) mu[j] = __builtin_nontemporal_load(&a.means[j * n + i]);
+        for (int j = 0; j < 3; ++j) ls[j] = __builtin_nontemporal_load(&a.log_scales[j * n + i]);
+        for (int j = 0; j < 4; ++j) q[j] = __builtin_nontemporal_load(&a.quats[j * n + i]);
         const float* ap = a.acc + (size_t)i * kAccStride;
-        for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+        for (int k = 0; k < kAccStride; ++k) g9[k] = __builtin_nontemporal_load(ap + k);
         geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
 
         // appearance: eq. sh_color_eval with its ReLU
@@ -200,7 +201,7 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
         float pre[3] = {0.5f, 0.5f, 0.5f};
         for (int k = 0; k < 16; ++k)
             for (int c = 0; c < 3; ++c) {
-                coef[3 * k + c] = k < nb ? a.sh[(3 * k + c) * n + i] : 0.f;
+                coef[3 * k + c] = k < nb ? __builtin_nontemporal_load(a.sh + (3 * k + c) * n + i) : 0.f;
                 pre[c] += Y[k] * coef[3 * k + c];
             }
         for (int c = 0; c < 3; ++c) gc[c] = pre[c] > 0.f ? g9[6 + c] : 0.f;
@@ -216,12 +217,19 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
     }
     for (int k = 0; k < 16; ++k) {
         const bool on = k < nb;
-        for (int c = 0; c < 3; ++c) a.dsh[(3 * k + c) * n + i] = on ? Y[k] * gc[c] : 0.f;
+        for (int c = 0; c < 3; ++c)
+            __builtin_nontemporal_store(on ? Y[k] * gc[c] : 0.f, a.dsh + (3 * k + c) * n + i);
     }
-    for (int j = 0; j < 3; ++j) { a.dmeans[j * n + i] = gg.dmu[j]; a.dlog_scales[j * n + i] = gg.dls[j]; }
-    for (int j = 0; j < 4; ++j) a.dquats[j * n + i] = gg.dq[j];
-    a.dlogits[i] = gg.dlogit;
-    if (a.dmean2d) { a.dmean2d[i] = g9[0]; a.dmean2d[n + i] = g9[1]; }
+    for (int j = 0; j < 3; ++j) {
+        __builtin_nontemporal_store(gg.dmu[j], &a.dmeans[j * n + i]);
+        __builtin_nontemporal_store(gg.dls[j], &a.dlog_scales[j * n + i]);
+    }
+    for (int j = 0; j < 4; ++j) __builtin_nontemporal_store(gg.dq[j], &a.dquats[j * n + i]);
+    __builtin_nontemporal_store(gg.dlogit, &a.dlogits[i]);
+    if (a.dmean2d) {
+        __builtin_nontemporal_store(g9[0], &a.dmean2d[i]);
+        __builtin_nontemporal_store(g9[1], &a.dmean2d[n + i]);
+    }
 }
 
 // NASG / NASGabor backward (eq. nasg, lobe.h): geometry as for SH3; the colour
@@ -247,12 +255,12 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_lobe(BwdArgs a)
     for (int k = 0; k < kRows; ++k) dl[k] = 0.f;
     if (vis) {
         float mu[3], ls[3], q[4], c0[3];
-        for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
-        for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
-        for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
+        for (int j = 0; j < 3; ++j) mu[j] = __builtin_nontemporal_load(&a.means[j * n + i]);
+        for (int j = 0; j < 3; ++j) ls[j] = __builtin_nontemporal_load(&a.log_scales[j * n + i]);
+        for (int j = 0; j < 4; ++j) q[j] = __builtin_nontemporal_load(&a.quats[j * n + i]);
         for (int c = 0; c < 3; ++c) c0[c] = a.base_color[c * n + i];
         const float* ap = a.acc + (size_t)i * kAccStride;
-        for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+        for (int k = 0; k < kAccStride; ++k) g9[k] = __builtin_nontemporal_load(ap + k);
         geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
         if (a.sh_degree >= 1) {
             float r[6], T[3];
@@ -282,12 +290,18 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_lobe(BwdArgs a)
             for (int c = 0; c < 3; ++c) gc[c] = c0[c] + 0.5f > 0.f ? g9[6 + c] : 0.f;
         }
     }
-    for (int c = 0; c < 3; ++c) a.dbase_color[c * n + i] = gc[c];
-    for (int k = 0; k < kRows; ++k) a.dlobes[k * n + i] = dl[k];
-    for (int j = 0; j < 3; ++j) { a.dmeans[j * n + i] = gg.dmu[j]; a.dlog_scales[j * n + i] = gg.dls[j]; }
-    for (int j = 0; j < 4; ++j) a.dquats[j * n + i] = gg.dq[j];
-    a.dlogits[i] = gg.dlogit;
-    if (a.dmean2d) { a.dmean2d[i] = g9[0]; a.dmean2d[n + i] = g9[1]; }
+    for (int c = 0; c < 3; ++c) __builtin_nontemporal_store(gc[c], &a.dbase_color[c * n + i]);
+    for (int k = 0; k < kRows; ++k) __builtin_nontemporal_store(dl[k], &a.dlobes[k * n + i]);
+    for (int j = 0; j < 3; ++j) {
+        __builtin_nontemporal_store(gg.dmu[j], &a.dmeans[j * n + i]);
+        __builtin_nontemporal_store(gg.dls[j], &a.dlog_scales[j * n + i]);
+    }
+    for (int j = 0; j < 4; ++j) __builtin_nontemporal_store(gg.dq[j], &a.dquats[j * n + i]);
+    __builtin_nontemporal_store(gg.dlogit, &a.dlogits[i]);
+    if (a.dmean2d) {
+        __builtin_nontemporal_store(g9[0], &a.dmean2d[i]);
+        __builtin_nontemporal_store(g9[1], &a.dmean2d[n + i]);
+    }
 }
 
 // Latent + MLP backward: geometry as for SH3, then per tile of 16 Gaussians

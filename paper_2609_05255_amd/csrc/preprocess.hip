@@ -224,14 +224,16 @@ __device__ __forceinline__ uint32_t block_sum_u32(uint32_t v, uint32_t* lds4)
     return r;
 }
 
+// Read once per frame: non-temporal loads, which leave the caches to the data
+// that the sort and the blend read again.
 __device__ __forceinline__ void load_geometry_params(const PreArgs& a, int i, float mu[3], float ls[3], float q[4],
                                                      float& logit)
 {
     const int64_t n = a.n;
-    for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
-    for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
-    for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
-    logit = a.logits[i];
+    for (int j = 0; j < 3; ++j) mu[j] = __builtin_nontemporal_load(&a.means[j * n + i]);
+    for (int j = 0; j < 3; ++j) ls[j] = __builtin_nontemporal_load(&a.log_scales[j * n + i]);
+    for (int j = 0; j < 4; ++j) q[j] = __builtin_nontemporal_load(&a.quats[j * n + i]);
+    logit = __builtin_nontemporal_load(&a.logits[i]);
 }
 
 __device__ __forceinline__ void view_dir(const Cam& c, const float mu[3], float d[3])
@@ -255,7 +257,7 @@ __device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n
     constexpr int nb = (kDeg + 1) * (kDeg + 1);
     float c[3 * nb];
 #pragma unroll
-    for (int k = 0; k < 3 * nb; ++k) c[k] = sh[(int64_t)k * n + i];
+    for (int k = 0; k < 3 * nb; ++k) c[k] = __builtin_nontemporal_load(sh + (int64_t)k * n + i);
     float Y[16];
     sh_basis16(d[0], d[1], d[2], Y);
     if (y0_folded) Y[0] = 1.f;

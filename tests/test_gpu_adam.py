@@ -85,21 +85,32 @@ def test_adam_edge_sizes():
     run_and_check(ts, 2, rng, "edge sizes")
 
 
-def test_fused_adam_on_a_latent_scene():
-    # one training iteration on a tiny latent scene: the half-precision buffers the
+@pytest.mark.parametrize("kind", ["latent", "neural", "nasgabor", "sh3_y0_folded"])
+def test_fused_adam_on_a_scene(kind):
+    # one training iteration on a tiny scene: the half-precision buffers the
     # passes read are the rounded fp32 masters, and every parameter moved by at
     # most its learning rate (|m_hat| / sqrt(v_hat) = 1 in a first step)
     from paper_2609_05255_amd import inputs
     from paper_2609_05255_amd.optim import FusedAdam
     from parity import tiny_camera
-    sc = inputs.make_scene("tiny", appearance=("latent",))
+    kid = {"latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL, "nasgabor": gs.GS_APP_NASGABOR,
+           "sh3_y0_folded": gs.GS_APP_SH3}[kind]
+    sc = inputs.make_scene("tiny", appearance=("sh3",) if kind == "sh3_y0_folded" else (kind,))
+    if kind == "sh3_y0_folded":
+        sc.sh = sc.sh.copy()
+        sc.sh[0:3] *= np.float32(0.28209479177387814)
+        sc.sh_y0_folded = True
     cam = tiny_camera()
     st = gs.SceneTensors(sc)
-    fr = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_LATENT_MLP, 1 << 16)
+    fr = gs.Frame(sc.n, cam.width, cam.height, kid, 1 << 16)
     cs = gs.camera_struct(cam)
     fr.forward(cs, st)
     fr.backward(cs, st, torch.from_numpy(inputs.make_upstream_grad(cam.width, cam.height, 0)).cuda())
-    opt = FusedAdam(st, fr, gs.GS_APP_LATENT_MLP)
+    opt = FusedAdam(st, fr, kid, camera_dbar=0.5)
+    if kind == "sh3_y0_folded":   # the DC rows take the paper's rate 0.0025 Y0
+        assert abs(opt.groups[4]["lr"][0] - 0.0025 * 0.28209479177387814) < 1e-12
+    if kind == "nasgabor":        # lobe rows 0.0025 (0.3536 / dbar)^2
+        assert abs(opt.groups[5]["lr"][0] - 0.0025 * (0.3536 / 0.5) ** 2) < 1e-12 and opt.groups[5]["rows"] == 9
     before = [g["param"].clone() for g in opt.groups]
     opt.step()
     torch.cuda.synchronize()
@@ -110,4 +121,4 @@ def test_fused_adam_on_a_latent_scene():
         if g["param_half"] is not None:
             h = g["param_half"].view(g["rows"], -1).cpu().numpy().view(np.uint16)
             assert np.array_equal(h, adam.half_copy(g["param"].cpu().numpy()))
-    say("  fused Adam on the latent scene: %d tensors, %d bytes per step" % (len(opt.groups), opt.bytes_per_step()))
+    say("  fused Adam on the %s scene: %d tensors, %d bytes per step" % (kind, len(opt.groups), opt.bytes_per_step()))

@@ -246,6 +246,11 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
     const float px = (float)x + 0.5f;
     const uint32_t start = ranges[2 * tile], len = ranges[2 * tile + 1] - start;
     const int64_t hw = (int64_t)cam.width * cam.height;
+    // box of this wave's pixel centres, for the same early skip as the forward
+    const float box_cx = (float)(tx * kTile) + 8.f, box_hx = 7.5f;
+    const float box_lo = (float)(ty * kTile + 4 * kPix * wave) + 0.5f;
+    const float box_hi = box_lo + (float)(4 * kPix - 1);
+    const float box_cy = 0.5f * (box_lo + box_hi), box_hy = 0.5f * (box_hi - box_lo);
 
     // Sg: the suffix sum S projected on the pixel's upstream gradient g, the
     // only form of S the gradient needs
@@ -307,7 +312,11 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             const uint32_t pos = b + (uint32_t)j;
             SplatReg s;
             {
-                const float4 w0 = st[0][j], w1 = st[1][j], w2 = st[2][j];
+                const float4 w0 = st[0][j], w2 = st[2][j];
+                // a splat that reaches alpha >= 1/255 nowhere in this wave's
+                // pixels passes nothing back (the extents are conservative)
+                if (!(fabsf(w0.x - box_cx) <= w2.z + box_hx && fabsf(w0.y - box_cy) <= w2.w + box_hy)) continue;
+                const float4 w1 = st[1][j];
                 s.mx = w0.x; s.my = w0.y; s.ca = w0.z; s.cb = w0.w;
                 s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w;
                 s.b = w2.x; s.pmin = w2.y;

@@ -282,3 +282,44 @@ def test_tiny_scene_neural_configurations(arch):
 def test_medium_scene_neural_three_layers():
     sc = inputs.make_scene("medium", appearance=("neural",), neural_arch=(3, 16, 0))
     check_all(sc, inputs.make_cameras("medium")[2], kind="neural", label="medium-neural-3-16-0")
+
+
+# ---- degenerate Gaussians ----------------------------------------------------------
+
+def degenerate_scene():
+    """The tiny scene with extreme members: needle-thin and screen-sized scales,
+    opacities at the alpha cap and far below 1/255, means behind the camera,
+    just beyond the near plane, on tile and pixel boundaries, and one Gaussian
+    that projects far outside the image (guard band)."""
+    sc = inputs.make_scene("tiny")
+    f32 = np.float32
+    m, ls, lg = sc.means, sc.log_scales, sc.opacity_logits
+    ls[:, 0:20] = f32(-12.0)                   # far below a pixel
+    ls[:, 20:30] = f32(0.5)                    # covering the whole image
+    ls[0, 30:40] = f32(-1.0)                   # needles: one long axis
+    ls[1:, 30:40] = f32(-9.0)
+    lg[40:60] = f32(25.0)                      # opacity 1 -> alpha capped at 0.99
+    lg[60:80] = f32(-25.0)                     # opacity ~ 1e-11, never 1/255
+    m[:, 80:90] = np.array([[0.1], [0.2], [-3.5]], f32)          # behind the camera (it sits at z = -3)
+    m[:, 90:100] = np.array([[0.0], [0.0], [-2.8 + 1e-4]], f32)  # just beyond the near plane 0.2
+    cam = tiny_camera()
+    # means whose projections land on tile corners and pixel centres
+    fx = cam.fx
+    for k, (u, v) in enumerate([(16, 16), (32, 48), (0.5, 0.5), (63.5, 31.5), (48, 0)]):
+        # at depth 3 (z = 0 in the world) these land on tile corners and pixel
+        # centres (the camera's x axis points along world -x, so u is mirrored)
+        m[:, 100 + k] = np.array([(u - cam.cx) * 3.0 / fx, (v - cam.cy) * 3.0 / fx, 0.0], f32)
+    m[:, 110] = np.array([3.0, 0.0, 0.0], f32)   # projects far to the side
+    ls[:, 110] = f32(-0.5)
+    return sc, cam
+
+
+@pytest.mark.parametrize("kind", ["sh3", "neural", "nasg"])
+def test_degenerate_gaussians(kind):
+    sc, cam = degenerate_scene()
+    if kind != "sh3":
+        extra = inputs.make_scene("tiny", appearance=(kind,))
+        sc.base_color = extra.base_color
+        sc.features, sc.neural_w, sc.lobes, sc.lobes_gabor = (extra.features, extra.neural_w, extra.lobes,
+                                                              extra.lobes_gabor)
+    check_all(sc, cam, kind=kind, label="degenerate-" + kind)

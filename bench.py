@@ -79,6 +79,9 @@ def parse():
     ap.add_argument("--config", default="paper_sh3")
     ap.add_argument("--appearance", default=None,
                     help="sh3, latent, neural, nasg or nasgabor (default: the config's first)")
+    ap.add_argument("--neural-arch", default=None,
+                    help="neural decoder as 'layers,width,raw16' (the paper's configurations table; "
+                         "default 2,16,0)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tiles", type=int, default=96, help="tiles in the CPU-baseline sample")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -92,9 +95,9 @@ def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int
     # appearance bytes per visible Gaussian: SH3 48 fp32, latent 14 binary16, neural a 12 B
     # base colour and 8 binary16 features
     # (the folded form: the base colour and 16 binary16 pre-activations, 44 B; NASG 12 + 32 B,
-    # NASGabor 12 + 36 B)
+    # NASGabor 12 + 36 B; 16 raw binary16 features: 12 + 32 B)
     app = (4 * 3 * (sh_degree + 1) ** 2 if kind == "sh3" else
-           {"neural_folded": 44, "nasg": 44, "nasgabor": 48}.get(kind, 28))
+           {"neural_folded": 44, "neural_raw16": 44, "nasg": 44, "nasgabor": 48}.get(kind, 28))
     if kernel == "preprocess":
         # params 44 B + tiles 4 B + depth key 4 B per Gaussian; appearance + 48 B of projected splat
         # (mean 8, conic 12, opacity 4, colour 12, rectangle 8, depth 4) per visible one; the record
@@ -102,7 +105,7 @@ def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, sh_degree: int
         return n * (44 + 8) + vis * (app + 48)
     if kernel == "preprocess_bwd":
         # tiles 4 B + dense gradient writes per Gaussian; params, accumulators and appearance per visible one
-        grad = 44 + 4 * {"sh3": 48, "latent": 14, "neural": 11, "nasg": 11, "nasgabor": 12}[kind]
+        grad = 44 + 4 * {"sh3": 48, "latent": 14, "neural": 11, "neural_raw16": 19, "nasg": 11, "nasgabor": 12}[kind]
         return n * (4 + grad) + vis * (44 + 36 + app)
     return None
 
@@ -125,7 +128,8 @@ def main():
     torch.cuda.set_device(0)
     dev = "cuda:0"
     t0 = time.time()
-    scene = inputs.make_scene(cfg, appearance=(kind,))
+    arch = None if args.neural_arch is None else tuple(int(v) for v in args.neural_arch.split(","))
+    scene = inputs.make_scene(cfg, appearance=(kind,), neural_arch=arch)
     cams = inputs.make_cameras(cfg)
     st = gs.SceneTensors(scene, device=dev)
     grads_up = [torch.from_numpy(inputs.make_upstream_grad(cfg.width, cfg.height, i)).to(dev)
@@ -144,7 +148,7 @@ def main():
         del src, dst
 
     # size the pair buffers: preprocess every camera once (untimed)
-    probe = gs.Frame(scene.n, cfg.width, cfg.height, kid, 1, device=dev)
+    probe = gs.Frame(scene.n, cfg.width, cfg.height, kid, 1, device=dev, neural_arch=arch)
     g, app = st.gaussians(), st.appearance(kid)
     pairs, visible = [], []
     for c in cstructs:
@@ -152,7 +156,7 @@ def main():
         visible.append(int((probe.tiles_touched[: scene.n] > 0).sum().item()))
     del probe
     capacity = int(max(pairs) * 1.02) + 4096
-    fr = gs.Frame(scene.n, cfg.width, cfg.height, kid, capacity, device=dev)
+    fr = gs.Frame(scene.n, cfg.width, cfg.height, kid, capacity, device=dev, neural_arch=arch)
     stream = torch.cuda.current_stream()
 
     def step(i):
@@ -194,7 +198,8 @@ def main():
     pairs_avg = float(np.mean([pairs[i] for i in steps_cams]))
     dominant = max(stage_ms, key=lambda k: stage_ms[k] * kt[k][1])
     roofline = None
-    hbm_kernels = {k: algorithmic_bytes(k, scene.n, vis_avg, kind) for k in ("preprocess", "preprocess_bwd")}
+    bkind = "neural_raw16" if kind == "neural" and arch and arch[2] else kind
+    hbm_kernels = {k: algorithmic_bytes(k, scene.n, vis_avg, bkind) for k in ("preprocess", "preprocess_bwd")}
     if dominant in hbm_kernels:
         b = hbm_kernels[dominant]
         ach = b / (stage_ms[dominant] * 1e-3) / 1e9
@@ -254,7 +259,7 @@ def main():
     # render only (preprocess, binning, forward blend), the unfolded neural
     # decoder against its folded form (the paper's viewer optimisation)
     render_only = None
-    if kind == "neural":
+    if kind == "neural" and arch in (None, (2, 16, 0)):
         fr_fold = gs.Frame(scene.n, cfg.width, cfg.height, gs.GS_APP_NEURAL_FOLDED, capacity, device=dev)
         gs.timing_enable(True)
         gs.timing_reset()
@@ -306,7 +311,7 @@ def main():
         "config": {"workload": "%s: %d Gaussians, %dx%d, %s appearance, %d cameras" % (
             cfg.name, scene.n, cfg.width, cfg.height, kind, ncam),
             "gaussians": scene.n, "width": cfg.width, "height": cfg.height, "appearance": kind,
-            "cameras": ncam},
+            "cameras": ncam, **({"neural_arch": list(arch)} if arch else {})},
         "mpix_per_s": round(mpix, 2),
         "visible_avg": int(vis_avg),
         "pairs_avg": int(pairs_avg),

@@ -105,7 +105,7 @@ enum {
 
 #define GS_NEURAL_FEATURES 8  /* binary16 features per Gaussian (16 B) beside a 12 B fp32 base colour */
 #define GS_NEURAL_WEIGHTS 816 /* 16*32 + 16*16 + 3*16, the paper's default decoder */
-#define GS_NEURAL_MAX_WEIGHTS 1072 /* 16*32 + 2*16*16 + 3*16: three hidden layers */
+#define GS_NEURAL_MAX_WEIGHTS 2144 /* 32*32 + 32*32 + 3*32: the 32-neuron configuration */
 
 /* View-dependent appearance (Sec. 3.1 and 4). d is the unit vector from the camera
  * centre to the Gaussian's mean, in world coordinates. */
@@ -139,8 +139,9 @@ typedef struct gs_appearance {
     int32_t neural_layers;    /* NEURAL: hidden layers, 1..3 (0 = the paper's default, 2); the
                                  weights are W1[16][32], layers - 1 matrices [16][16], Wout[3][16]
                                  (the supplementary table of configurations) */
-    int32_t neural_width;     /* NEURAL: neurons per hidden layer: 0 or 16. The table's 32-neuron
-                                 configuration is not built (GS_ERR_UNSUPPORTED) */
+    int32_t neural_width;     /* NEURAL: neurons per hidden layer: 0 or 16, or 32 for the table's
+                                 32-32-32-3 configuration (weights W1[32][32], W2[32][32],
+                                 Wout[3][32]; other 32-neuron shapes: GS_ERR_UNSUPPORTED) */
     int32_t neural_raw16;     /* NEURAL: 1 = 16 raw binary16 features ([16][n]) as the 16 feature
                                  inputs instead of (sin f, cos f) of 8 (the table's F = 16) */
 } gs_appearance;

@@ -82,9 +82,10 @@ gs_status check_appearance(const gs_appearance* a, int64_t n)
         GS_CHECK(a->sh_degree >= 0 && a->sh_degree <= 3, "sh_degree %d outside 0..3", a->sh_degree);
         GS_CHECK(a->neural_layers >= 0 && a->neural_layers <= 3, "neural_layers %d outside 0..3", a->neural_layers);
         GS_CHECK(a->neural_raw16 == 0 || a->neural_raw16 == 1, "neural_raw16 must be 0 or 1");
-        if (a->neural_width != 0 && a->neural_width != 16)
-            return fail(a->neural_width == 32 ? GS_ERR_UNSUPPORTED : GS_ERR_INVALID_ARG,
-                        "neural_width %d: 16 neurons per layer are supported", a->neural_width);
+        GS_CHECK(a->neural_width == 0 || a->neural_width == 16 || a->neural_width == 32,
+                 "neural_width %d: 16 or 32 neurons per layer", a->neural_width);
+        if (a->neural_width == 32 && ((a->neural_layers != 0 && a->neural_layers != 2) || a->neural_raw16))
+            return fail(GS_ERR_UNSUPPORTED, "32 neurons per layer are built for the table's 32-32-32-3 decoder only");
         GS_CHECK(n == 0 || a->base_color != nullptr, "base_color is NULL");
         GS_CHECK(n == 0 || a->sh_degree == 0 || (a->features != nullptr && a->mlp_w != nullptr),
                  "features or mlp_w is NULL");

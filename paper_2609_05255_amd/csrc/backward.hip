@@ -5,6 +5,8 @@
 // opacity logistic, and the appearance model -- including the colour gradient
 // through the view direction into the mean (Sec. 4 fused backward). Gradients
 // of culled Gaussians are written as zeros, so every output is dense.
+#include <type_traits>
+
 #include "gs_internal.h"
 #include "mlp.h"
 #include "lobe.h"
@@ -415,18 +417,21 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
 // of the active bands, the weight-gradient sums), then the geometry backward.
 // While the active degree is 0 only the base colour takes a gradient. L hidden
 // layers; kRaw: 16 raw features as the feature inputs.
-template <int L, bool kRaw>
-__global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
+template <int L, bool kRaw, int kW = 16>
+__global__ __launch_bounds__(kBlock, kW == 32 ? 2 : 3) void k_preprocess_bwd_neural(BwdArgs a)
 {
+    static_assert(kW == 16 || (kW == 32 && L == 2 && !kRaw), "the 32-neuron configuration is 32-32-32-3");
     constexpr int kF = kRaw ? 16 : GS_NEURAL_FEATURES;
-    constexpr int kNW = neural_weight_count(L);
-    __shared__ NeuralFrags<L> W;
+    constexpr int kNW = kW == 32 ? kNeural32Weights : neural_weight_count(L);
+    using Frags = std::conditional_t<kW == 32, MlpFrags, NeuralFrags<L>>;
+    using Acc = std::conditional_t<kW == 32, MlpGradAcc, NeuralGradAcc<L>>;
+    __shared__ Frags W;
     __shared__ NeuralBwdStage ST[kBlock / kWave];
     const bool resid = a.sh_degree >= 1;
     if (resid) neural_load_frags(a.mlp_w, W, true);
     const int wave = threadIdx.x >> 6, lane = __lane_id();
     NeuralBwdStage& st = ST[wave];
-    NeuralGradAcc<L> acc;
+    Acc acc;
     neural_grad_zero(acc);
     const int64_t n = a.n;
     const int64_t nchunks = div_up(n, kBlock);
@@ -546,21 +551,9 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_neural(BwdArgs a)
     float* red = reinterpret_cast<float*>(&ST[0]);
     for (int k = threadIdx.x; k < kNW; k += kBlock) red[k] = 0.f;
     __syncthreads();
-    const int g = lane >> 4, c = lane & 15;
     neural_grad_rescale(acc, 0);   // back to plain units
     for (int w = 0; w < kBlock / kWave; ++w) {
-        if (wave == w && resid) {
-            for (int e = 0; e < 4; ++e) {
-                const int row = 4 * g + e;
-                for (int fb = 0; fb < 2; ++fb) red[row * kNeuralIn + 16 * fb + c] += acc.w1[fb][e];
-                for (int h = 0; h < L - 1; ++h)
-                    red[kNeuralHidden * kNeuralIn + h * kNeuralHidden * kNeuralHidden + row * kNeuralHidden + c] +=
-                        acc.wh[h][e];
-                if (row < GS_MLP_OUT)
-                    red[kNeuralHidden * kNeuralIn + (L - 1) * kNeuralHidden * kNeuralHidden + row * kNeuralHidden + c] +=
-                        acc.w3[e];
-            }
-        }
+        if (wave == w && resid) neural_grad_add(acc, red);
         __syncthreads();
     }
     for (int k = threadIdx.x; k < kNW; k += kBlock) a.mlp_part[(size_t)blockIdx.x * kNW + k] = red[k];
@@ -640,7 +633,9 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
     {
         const dim3 grid(latent_bwd_grid(g.n));
         const int layers = neural_layers(app);
-        if (app.neural_raw16) {
+        if (app.neural_width == 32) {
+            hipLaunchKernelGGL((k_preprocess_bwd_neural<2, false, 32>), grid, dim3(kBlock), 0, s, a);
+        } else if (app.neural_raw16) {
             if (layers == 1) hipLaunchKernelGGL((k_preprocess_bwd_neural<1, true>), grid, dim3(kBlock), 0, s, a);
             else if (layers == 3) hipLaunchKernelGGL((k_preprocess_bwd_neural<3, true>), grid, dim3(kBlock), 0, s, a);
             else hipLaunchKernelGGL((k_preprocess_bwd_neural<2, true>), grid, dim3(kBlock), 0, s, a);

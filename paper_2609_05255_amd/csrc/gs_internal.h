@@ -139,12 +139,12 @@ inline int preprocess_blocks(int64_t n) { return (int)div_up(n > 0 ? n : 1, kBlo
 inline int pair_count_slots(int64_t n) { return (int)div_up(n > 0 ? n : 1, kWave); }
 
 // Hidden layers of the neural decoder (0 in the struct: the paper's default, 2)
-// and its weight count with 16 neurons per layer.
+// and its weight count.
 inline int neural_layers(const gs_appearance& a) { return a.neural_layers > 0 ? a.neural_layers : 2; }
 inline int neural_weights(const gs_appearance& a)
 {
-    const int L = neural_layers(a);
-    return 16 * 32 + (L - 1) * 16 * 16 + 3 * 16;
+    const int L = neural_layers(a), W = a.neural_width == 32 ? 32 : 16;
+    return W * 32 + (L - 1) * W * W + 3 * W;
 }
 
 }  // namespace gsr

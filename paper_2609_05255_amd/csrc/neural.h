@@ -377,4 +377,178 @@ __device__ __forceinline__ void neural_tile_bwd(const NeuralFrags<L>& W, NeuralB
     for (int fb = 0; fb < 2; ++fb) acc.w1[fb] = mfma16(h1d, xg[fb], acc.w1[fb]);   // dW1[n1][input]
 }
 
+// ---- the table's 32-neuron configuration ----------------------------------------
+// 32 -> 32 -> 32 -> 3 has the shape of the latent decoder (mlp.h), so it takes
+// that decoder's fragments, forward tile and weight-gradient sums, loaded from
+// W1[32][32], W2[32][32], Wout[3][32]; only the input staging, the tanh
+// residual and the input-gradient hand-off are the neural model's.
+constexpr int kNeural32Weights = 32 * 32 + 32 * 32 + GS_MLP_OUT * 32;   // 2144
+
+__device__ __forceinline__ void neural_load_frags(const uint16_t* __restrict__ w, MlpFrags& s, bool backward,
+                                                  bool folded = false)
+{
+    (void)folded;   // the folded form takes the 16-neuron default only
+    const _Float16* W1 = reinterpret_cast<const _Float16*>(w);
+    const _Float16* W2 = W1 + 32 * 32;
+    const _Float16* W3 = W2 + 32 * 32;
+    const _Float16 z = (_Float16)0.f;
+    for (int e = threadIdx.x; e < kWave * 8; e += blockDim.x) {
+        const int l = e >> 3, j = e & 7, g = l >> 4, c = l & 15;
+        const int k = kslot(g, j);
+        for (int b = 0; b < 2; ++b) {
+            const int row = 16 * b + c;
+            s.w1a[b][l][j] = W1[row * 32 + k];
+            s.w2a[b][l][j] = W2[row * 32 + k];
+            if (backward) {
+                s.w1t[b][l][j] = W1[k * 32 + row];
+                s.w2t[b][l][j] = W2[k * 32 + row];
+                if (j < 4) s.w3t[b][l][j] = 4 * g + j < GS_MLP_OUT ? W3[(4 * g + j) * 32 + row] : z;
+            }
+        }
+        s.w3a[l][j] = c < GS_MLP_OUT ? W3[c * 32 + k] : z;
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ float4_t neural_tile_out(const MlpFrags& W, const half8_t& x)
+{
+    float4_t h1[2], h2[2], o;
+    half8_t a1, a2;
+    mlp_tile_fwd(W, x, h1, a1, h2, a2, o);
+    return o;
+}
+
+__device__ __forceinline__ void neural_grad_zero(MlpGradAcc& a) { mlp_grad_zero(a); }
+__device__ __forceinline__ void neural_grad_rescale(MlpGradAcc& a, int se) { mlp_grad_rescale(a, se); }
+
+// Backward of tile t for the 32-neuron decoder, with the contract of
+// neural_tile_bwd<L>: delta3 from st.d3 (scaled by 2^se), the hidden gradients
+// chained neuron-major with binary16 hi + lo operands, the Gaussian-major copies
+// for dWout, dW2, dW1, and the input gradients left in st.dxf and the input rows.
+__device__ __forceinline__ void neural_tile_bwd(const MlpFrags& W, NeuralBwdStage& st, int t, float scale,
+                                                float inv, MlpGradAcc& acc)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    const float4_t zero = {0.f, 0.f, 0.f, 0.f};
+    const half8_t x = neural_stage_frag(st.x, t);
+    half4_t xg[2];
+#pragma unroll
+    for (int fb = 0; fb < 2; ++fb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) xg[fb][j] = st.x[16 * t + 4 * g + j][16 * fb + c];
+    // forward of the hidden layers, both orientations
+    float4_t h1n[2], h2n[2], on;
+    half8_t a1, a2;
+    mlp_tile_fwd(W, x, h1n, a1, h2n, a2, on);
+    float4_t h1g[2], h2g[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) h1g[b] = mfma32(x, frag8(W.w1a[b]), zero);      // h1[G = 4g+i][16b + c]
+#pragma unroll
+    for (int b = 0; b < 2; ++b) h2g[b] = mfma32(a1, frag8(W.w2a[b]), zero);     // h2[G = 4g+i][16b + c]
+
+    // output gradients, neuron-major (lanes g = 0) and Gaussian-major
+    float4_t d3n = zero, d3g;
+    const int Gn = 16 * t + c;
+    if (g == 0)
+#pragma unroll
+        for (int i = 0; i < GS_MLP_OUT; ++i) d3n[i] = st.d3[Gn][i] * scale;
+    const int cn = min(c, 3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) d3g[i] = st.d3[16 * t + 4 * g + i][cn] * scale;
+    half4_t d3n_hi, d3n_lo;
+    split4(d3n, d3n_hi, d3n_lo);
+    const half4_t d3g_h = half4_t{(_Float16)d3g[0], (_Float16)d3g[1], (_Float16)d3g[2], (_Float16)d3g[3]};
+
+    // dH2 = Wout^T delta3, masked by relu'(h2)
+    float4_t g2n[2], g2g[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const half4_t w = frag4(W.w3t[b]);
+        g2n[b] = relu_mask(mfma16(w, d3n_lo, mfma16(w, d3n_hi, zero)), h2n[b]);
+        g2g[b] = relu_mask(mfma16(d3n_lo, w, mfma16(d3n_hi, w, zero)), h2g[b]);
+    }
+    half8_t g2n_hi, g2n_lo;
+    split_cat(g2n[0], g2n[1], g2n_hi, g2n_lo);
+    // dH1 = W2^T dH2, masked by relu'(h1)
+    float4_t g1n[2], g1g[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const half8_t w = frag8(W.w2t[b]);
+        g1n[b] = relu_mask(mfma32(w, g2n_lo, mfma32(w, g2n_hi, zero)), h1n[b]);
+        g1g[b] = relu_mask(mfma32(g2n_lo, w, mfma32(g2n_hi, w, zero)), h1g[b]);
+    }
+    half8_t g1n_hi, g1n_lo;
+    split_cat(g1n[0], g1n[1], g1n_hi, g1n_lo);
+    // dX = W1^T dH1: dx[b] holds inputs 16b + 4g + i of Gaussian c
+    float4_t dx[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const half8_t w = frag8(W.w1t[b]);
+        dx[b] = mfma32(w, g1n_lo, mfma32(w, g1n_hi, zero)) * inv;
+    }
+    // the tile's input rows have been read: they now take the direction-input gradients
+    wave_lds_sync();
+    float* row = reinterpret_cast<float*>(&st.x[Gn][0]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        row[4 * g + i] = dx[0][i];
+        st.dxf[Gn][4 * g + i] = dx[1][i];
+    }
+
+    // weight gradients from the Gaussian-major fragments, accumulated in place
+    half4_t r1g[2], r2g[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        r1g[b] = relu_half4(h1g[b]);
+        r2g[b] = relu_half4(h2g[b]);
+    }
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) acc.w3[nb] = mfma16(d3g_h, r2g[nb], acc.w3[nb]);          // dWout[o][n2]
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+        const half4_t h = {(_Float16)g2g[mb][0], (_Float16)g2g[mb][1], (_Float16)g2g[mb][2], (_Float16)g2g[mb][3]};
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) acc.w2[mb][nb] = mfma16(h, r1g[nb], acc.w2[mb][nb]);   // dW2[n2][n1]
+    }
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+        const half4_t h = {(_Float16)g1g[mb][0], (_Float16)g1g[mb][1], (_Float16)g1g[mb][2], (_Float16)g1g[mb][3]};
+#pragma unroll
+        for (int fb = 0; fb < 2; ++fb) acc.w1[mb][fb] = mfma16(h, xg[fb], acc.w1[mb][fb]);    // dW1[n1][input]
+    }
+}
+
+// Adds a wave's weight-gradient sums into the workgroup buffer `red` in the
+// weights' order (16-neuron decoder with L hidden layers, or the 32-neuron one).
+template <int L>
+__device__ __forceinline__ void neural_grad_add(const NeuralGradAcc<L>& acc, float* red)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    for (int e = 0; e < 4; ++e) {
+        const int row = 4 * g + e;
+        for (int fb = 0; fb < 2; ++fb) red[row * kNeuralIn + 16 * fb + c] += acc.w1[fb][e];
+        for (int h = 0; h < L - 1; ++h)
+            red[kNeuralHidden * kNeuralIn + h * kNeuralHidden * kNeuralHidden + row * kNeuralHidden + c] +=
+                acc.wh[h][e];
+        if (row < GS_MLP_OUT)
+            red[kNeuralHidden * kNeuralIn + (L - 1) * kNeuralHidden * kNeuralHidden + row * kNeuralHidden + c] +=
+                acc.w3[e];
+    }
+}
+
+__device__ __forceinline__ void neural_grad_add(const MlpGradAcc& acc, float* red)
+{
+    const int l = __lane_id(), g = l >> 4, c = l & 15;
+    for (int e = 0; e < 4; ++e) {
+        for (int mb = 0; mb < 2; ++mb) {
+            const int row = 16 * mb + 4 * g + e;
+            for (int fb = 0; fb < 2; ++fb) red[row * 32 + 16 * fb + c] += acc.w1[mb][fb][e];
+            for (int nb = 0; nb < 2; ++nb) red[32 * 32 + row * 32 + 16 * nb + c] += acc.w2[mb][nb][e];
+        }
+        const int o = 4 * g + e;
+        if (o < GS_MLP_OUT)
+            for (int nb = 0; nb < 2; ++nb) red[2 * 32 * 32 + o * 32 + 16 * nb + c] += acc.w3[nb][e];
+    }
+}
+
 }  // namespace gsr

@@ -6,6 +6,8 @@
 // The whole file is compiled without floating-point contraction: the tile
 // rectangle and the depth key are integers decided by this fp32 arithmetic,
 // and they must not depend on which multiply-adds the compiler fuses.
+#include <type_traits>
+
 #include "gs_internal.h"
 #include "mlp.h"
 #include "lobe.h"
@@ -410,11 +412,13 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_latent(PreArgs a)
 // stored pre-activations of the view-independent inputs to the direction
 // columns' product (no features, no sin/cos). L hidden layers; kRaw: 16 raw
 // features as the feature inputs (the architecture table's configurations).
-template <bool kFolded, int L, bool kRaw>
-__global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
+template <bool kFolded, int L, bool kRaw, int kW = 16>
+__global__ __launch_bounds__(kBlock, kW == 32 ? 3 : 4) void k_preprocess_neural(PreArgs a)
 {
+    static_assert(kW == 16 || (kW == 32 && L == 2 && !kRaw && !kFolded), "the 32-neuron configuration is 32-32-32-3");
     constexpr int kF = kRaw ? 16 : GS_NEURAL_FEATURES;
-    __shared__ NeuralFrags<L> W;
+    using Frags = std::conditional_t<kW == 32, MlpFrags, NeuralFrags<L>>;
+    __shared__ Frags W;
     __shared__ NeuralInStage XS[kBlock / kWave];
     __shared__ SplatStage stage[kBlock / kWave];
     const bool resid = a.sh_degree >= 1;
@@ -483,8 +487,9 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_neural(PreArgs a)
 #pragma unroll
             for (int t = 0; t < kWave / 16; ++t) {
                 if (((vis >> (16 * t)) & 0xFFFFull) == 0) continue;
-                const float4_t ot = kFolded ? neural_tile_out_folded(W, XS[wave].x, t, p4[t])
-                                            : neural_tile_out(W, neural_stage_frag(XS[wave].x, t));
+                float4_t ot;
+                if constexpr (kFolded) ot = neural_tile_out_folded(W, XS[wave].x, t, p4[t]);
+                else ot = neural_tile_out(W, neural_stage_frag(XS[wave].x, t));
                 neural_tile_gather(ot, t, o);
             }
             wave_lds_sync();   // the stage is read before the next chunk overwrites it
@@ -544,7 +549,9 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     else if (app.kind == GS_APP_NEURAL) {
         const dim3 grid(std::min(blocks, kNeuralBlocks));
         const int layers = neural_layers(app);
-        if (app.neural_raw16) {
+        if (app.neural_width == 32) {
+            hipLaunchKernelGGL((k_preprocess_neural<false, 2, false, 32>), grid, dim3(kBlock), 0, s, a);
+        } else if (app.neural_raw16) {
             if (layers == 1) hipLaunchKernelGGL((k_preprocess_neural<false, 1, true>), grid, dim3(kBlock), 0, s, a);
             else if (layers == 3) hipLaunchKernelGGL((k_preprocess_neural<false, 3, true>), grid, dim3(kBlock), 0, s, a);
             else hipLaunchKernelGGL((k_preprocess_neural<false, 2, true>), grid, dim3(kBlock), 0, s, a);

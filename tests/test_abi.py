@@ -103,7 +103,8 @@ def test_preprocess_rejects_bad_arguments(gs):
     arch = lambda L, W, raw: gs.Appearance(gs.GS_APP_NEURAL, 3, None, None, FAKE, FAKE, FAKE, None, None, 0, L, W, raw)
     assert call(app=arch(4, 0, 0)) == gs.GS_ERR_INVALID_ARG
     assert call(app=arch(2, 8, 0)) == gs.GS_ERR_INVALID_ARG
-    assert call(app=arch(2, 32, 0)) == gs.GS_ERR_UNSUPPORTED
+    assert call(app=arch(3, 32, 0)) == gs.GS_ERR_UNSUPPORTED
+    assert call(app=arch(2, 32, 1)) == gs.GS_ERR_UNSUPPORTED
     assert call(app=arch(2, 16, 2)) == gs.GS_ERR_INVALID_ARG
     folded_arch = gs.Appearance(gs.GS_APP_NEURAL_FOLDED, 3, None, None, FAKE, FAKE, None, FAKE, None, 0, 3, 0, 0)
     assert call(app=folded_arch) == gs.GS_ERR_INVALID_ARG

@@ -273,10 +273,15 @@ def test_tiny_scene_sh_y0_folded(degree):
 
 # ---- the neural decoder configurations of the paper's architecture table ---------
 
-@pytest.mark.parametrize("arch", [(1, 16, 0), (3, 16, 0), (2, 16, 1), (3, 16, 1)])
+@pytest.mark.parametrize("arch", [(1, 16, 0), (3, 16, 0), (2, 16, 1), (3, 16, 1), (2, 32, 0)])
 def test_tiny_scene_neural_configurations(arch):
     sc = inputs.make_scene("tiny", appearance=("neural",), neural_arch=arch)
     check_all(sc, tiny_camera(), kind="neural", sh_degree=3, label="tiny-neural-%d-%d-%d" % arch)
+
+
+def test_medium_scene_neural_32_wide():
+    sc = inputs.make_scene("medium", appearance=("neural",), neural_arch=(2, 32, 0))
+    check_all(sc, inputs.make_cameras("medium")[2], kind="neural", label="medium-neural-2-32-0")
 
 
 def test_medium_scene_neural_three_layers():

@@ -421,8 +421,7 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
     timing_end(GS_KERNEL_PREPROCESS_BWD, s);
     if (app->kind == GS_APP_LATENT_MLP || app->kind == GS_APP_NEURAL) {
         timing_begin(GS_KERNEL_MLP_REDUCE, s);
-        GS_HIP(launch_mlp_reduce(g->n, app->kind == GS_APP_NEURAL ? neural_weights(*app) : GS_MLP_WEIGHTS, ws,
-                                 grads->dmlp_w, s));
+        GS_HIP(launch_mlp_reduce(g->n, *app, ws, grads->dmlp_w, s));
         timing_end(GS_KERNEL_MLP_REDUCE, s);
     }
     return ok();

@@ -590,7 +590,11 @@ __global__ __launch_bounds__(kReduceRows * kReduceCols) void k_mlp_reduce(const 
     }
 }
 
-inline int latent_bwd_grid(int64_t n) { return (int)std::min<int64_t>(div_up(n, kBlock), kMlpPartials); }
+inline int decoder_bwd_grid(int64_t n, const gs_appearance& app)
+{
+    const int parts = app.kind == GS_APP_NEURAL && app.neural_width == 32 ? kMlpPartials32 : kMlpPartials;
+    return (int)std::min<int64_t>(div_up(n, kBlock), parts);
+}
 
 hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                                  const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr, hipStream_t s)
@@ -631,7 +635,7 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
         hipLaunchKernelGGL(k_preprocess_bwd_lobe<true>, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NEURAL)
     {
-        const dim3 grid(latent_bwd_grid(g.n));
+        const dim3 grid(decoder_bwd_grid(g.n, app));
         const int layers = neural_layers(app);
         if (app.neural_width == 32) {
             hipLaunchKernelGGL((k_preprocess_bwd_neural<2, false, 32>), grid, dim3(kBlock), 0, s, a);
@@ -646,14 +650,15 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
         }
     }
     else
-        hipLaunchKernelGGL(k_preprocess_bwd_latent, dim3(latent_bwd_grid(g.n)), dim3(kBlock), 0, s, a);
+        hipLaunchKernelGGL(k_preprocess_bwd_latent, dim3(decoder_bwd_grid(g.n, app)), dim3(kBlock), 0, s, a);
     return hipGetLastError();
 }
 
-hipError_t launch_mlp_reduce(int64_t n, int nw, const Workspace& ws, float* dmlp_w, hipStream_t s)
+hipError_t launch_mlp_reduce(int64_t n, const gs_appearance& app, const Workspace& ws, float* dmlp_w, hipStream_t s)
 {
+    const int nw = app.kind == GS_APP_NEURAL ? neural_weights(app) : GS_MLP_WEIGHTS;
     hipLaunchKernelGGL(k_mlp_reduce, dim3((unsigned)div_up(nw, kReduceCols)), dim3(kReduceRows * kReduceCols), 0, s,
-                       ws.mlp_part, latent_bwd_grid(n), nw, dmlp_w);
+                       ws.mlp_part, decoder_bwd_grid(n, app), nw, dmlp_w);
     return hipGetLastError();
 }
 

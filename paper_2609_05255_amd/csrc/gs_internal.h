@@ -62,9 +62,11 @@ constexpr int kSortTile = kBlock * kSortItems;   // 4096
 constexpr int kRadix = 256;
 constexpr int kDupChunk = 1024;   // depth-ordered Gaussians per workgroup in pair emission
 
-// Workgroups of the latent preprocess backward (grid-stride), one partial
-// weight gradient each.
+// Workgroups of the decoder preprocess backward (grid-stride), one partial
+// weight gradient each: as many as are resident at once, 3 per compute unit
+// (2 for the 32-neuron decoder, whose registers allow only 2).
 constexpr int kMlpPartials = 768;
+constexpr int kMlpPartials32 = 512;
 
 __host__ __device__ inline int64_t div_up(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t align_up(size_t a, size_t b) { return (a + b - 1) / b * b; }
@@ -124,7 +126,7 @@ hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32
 hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                                  const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr,
                                  hipStream_t s);
-hipError_t launch_mlp_reduce(int64_t n, int nw, const Workspace& ws, float* dmlp_w, hipStream_t s);
+hipError_t launch_mlp_reduce(int64_t n, const gs_appearance& app, const Workspace& ws, float* dmlp_w, hipStream_t s);
 hipError_t launch_adam(const gs_adam_tensor* tensors, int count, float beta1, float eps, int64_t step, hipStream_t s);
 hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s);
 hipError_t launch_neural_fold(const uint16_t* features, const uint16_t* w, int64_t n, uint16_t* preact,

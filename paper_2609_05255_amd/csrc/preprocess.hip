@@ -511,8 +511,9 @@ __global__ __launch_bounds__(kBlock, kW == 32 ? 3 : 4) void k_preprocess_neural(
 // Workgroups of the latent preprocess: the number resident at once on 256 CUs
 // (four per CU at the kernel's register budget), each wave looping over chunks.
 constexpr int kLatentBlocks = 1024;
-// and of the neural one
+// and of the neural one (three per CU for the 32-neuron decoder)
 constexpr int kNeuralBlocks = 1024;
+constexpr int kNeuralBlocks32 = 768;
 
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                              const gs_preprocessed& out, const Workspace& ws, hipStream_t s)
@@ -547,7 +548,7 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
         }
     }
     else if (app.kind == GS_APP_NEURAL) {
-        const dim3 grid(std::min(blocks, kNeuralBlocks));
+        const dim3 grid(std::min(blocks, app.neural_width == 32 ? kNeuralBlocks32 : kNeuralBlocks));
         const int layers = neural_layers(app);
         if (app.neural_width == 32) {
             hipLaunchKernelGGL((k_preprocess_neural<false, 2, false, 32>), grid, dim3(kBlock), 0, s, a);

@@ -99,7 +99,8 @@ def test_preprocess_rejects_bad_arguments(gs):
     assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 3, None, None, FAKE, None, FAKE)) == gs.GS_ERR_INVALID_ARG
     assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 2, None, None, FAKE, FAKE, None)) == gs.GS_ERR_INVALID_ARG
     assert call(app=gs.Appearance(gs.GS_APP_NEURAL, 4, None, None, FAKE, FAKE, FAKE)) == gs.GS_ERR_INVALID_ARG
-    # neural configurations: 1..3 hidden layers of 16, raw features; 32 wide is not built
+    # neural configurations: 1..3 hidden layers of 16, raw features; 32 wide only as the table's
+    # 2-hidden-layer decoder on encoded features
     arch = lambda L, W, raw: gs.Appearance(gs.GS_APP_NEURAL, 3, None, None, FAKE, FAKE, FAKE, None, None, 0, L, W, raw)
     assert call(app=arch(4, 0, 0)) == gs.GS_ERR_INVALID_ARG
     assert call(app=arch(2, 8, 0)) == gs.GS_ERR_INVALID_ARG
@@ -108,6 +109,8 @@ def test_preprocess_rejects_bad_arguments(gs):
     assert call(app=arch(2, 16, 2)) == gs.GS_ERR_INVALID_ARG
     folded_arch = gs.Appearance(gs.GS_APP_NEURAL_FOLDED, 3, None, None, FAKE, FAKE, None, FAKE, None, 0, 3, 0, 0)
     assert call(app=folded_arch) == gs.GS_ERR_INVALID_ARG
+    folded_wide = gs.Appearance(gs.GS_APP_NEURAL_FOLDED, 3, None, None, FAKE, FAKE, None, FAKE, None, 0, 2, 32, 0)
+    assert call(app=folded_wide) == gs.GS_ERR_INVALID_ARG
     # folded neural: pre-activations instead of features, 8-byte aligned
     folded = lambda deg, pre_act: gs.Appearance(gs.GS_APP_NEURAL_FOLDED, deg, None, None, FAKE, FAKE, None, pre_act)
     assert call(app=folded(3, None)) == gs.GS_ERR_INVALID_ARG

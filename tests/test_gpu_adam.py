@@ -85,7 +85,7 @@ def test_adam_edge_sizes():
     run_and_check(ts, 2, rng, "edge sizes")
 
 
-@pytest.mark.parametrize("kind", ["latent", "neural", "nasgabor", "sh3_y0_folded"])
+@pytest.mark.parametrize("kind", ["latent", "neural", "neural_32", "nasgabor", "sh3_y0_folded"])
 def test_fused_adam_on_a_scene(kind):
     # one training iteration on a tiny scene: the half-precision buffers the
     # passes read are the rounded fp32 masters, and every parameter moved by at
@@ -93,16 +93,18 @@ def test_fused_adam_on_a_scene(kind):
     from paper_2609_05255_amd import inputs
     from paper_2609_05255_amd.optim import FusedAdam
     from parity import tiny_camera
-    kid = {"latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL, "nasgabor": gs.GS_APP_NASGABOR,
-           "sh3_y0_folded": gs.GS_APP_SH3}[kind]
-    sc = inputs.make_scene("tiny", appearance=("sh3",) if kind == "sh3_y0_folded" else (kind,))
+    kid = {"latent": gs.GS_APP_LATENT_MLP, "neural": gs.GS_APP_NEURAL, "neural_32": gs.GS_APP_NEURAL,
+           "nasgabor": gs.GS_APP_NASGABOR, "sh3_y0_folded": gs.GS_APP_SH3}[kind]
+    arch = (2, 32, 0) if kind == "neural_32" else None
+    base = {"sh3_y0_folded": "sh3", "neural_32": "neural"}.get(kind, kind)
+    sc = inputs.make_scene("tiny", appearance=(base,), neural_arch=arch)
     if kind == "sh3_y0_folded":
         sc.sh = sc.sh.copy()
         sc.sh[0:3] *= np.float32(0.28209479177387814)
         sc.sh_y0_folded = True
     cam = tiny_camera()
     st = gs.SceneTensors(sc)
-    fr = gs.Frame(sc.n, cam.width, cam.height, kid, 1 << 16)
+    fr = gs.Frame(sc.n, cam.width, cam.height, kid, 1 << 16, neural_arch=arch)
     cs = gs.camera_struct(cam)
     fr.forward(cs, st)
     fr.backward(cs, st, torch.from_numpy(inputs.make_upstream_grad(cam.width, cam.height, 0)).cuda())
@@ -111,6 +113,8 @@ def test_fused_adam_on_a_scene(kind):
         assert abs(opt.groups[4]["lr"][0] - 0.0025 * 0.28209479177387814) < 1e-12
     if kind == "nasgabor":        # lobe rows 0.0025 (0.3536 / dbar)^2
         assert abs(opt.groups[5]["lr"][0] - 0.0025 * (0.3536 / 0.5) ** 2) < 1e-12 and opt.groups[5]["rows"] == 9
+    if kind == "neural_32":       # the 32-32-32-3 decoder's 2,144 weights in one group
+        assert any(g["rows"] == 1 and g["param"].numel() == 2144 for g in opt.groups)
     before = [g["param"].clone() for g in opt.groups]
     opt.step()
     torch.cuda.synchronize()

@@ -279,6 +279,18 @@ def test_tiny_scene_neural_configurations(arch):
     check_all(sc, tiny_camera(), kind="neural", sh_degree=3, label="tiny-neural-%d-%d-%d" % arch)
 
 
+@pytest.mark.parametrize("degree", [0, 1, 2])
+def test_tiny_scene_neural_32_wide_degrees(degree):
+    # degree masking of the direction inputs (degree 0: the residual is off)
+    sc = inputs.make_scene("tiny", appearance=("neural",), neural_arch=(2, 32, 0))
+    check_all(sc, tiny_camera(), kind="neural", sh_degree=degree, label="tiny-neural-2-32-0")
+
+
+def test_ragged_neural_32_wide_with_background():
+    sc = inputs.make_scene("tiny", appearance=("neural",), neural_arch=(2, 32, 0))
+    check_all(sc, tiny_camera(50, 37, bg=(0.1, 0.5, 0.9)), kind="neural", label="ragged-neural-2-32-0")
+
+
 def test_medium_scene_neural_32_wide():
     sc = inputs.make_scene("medium", appearance=("neural",), neural_arch=(2, 32, 0))
     check_all(sc, inputs.make_cameras("medium")[2], kind="neural", label="medium-neural-2-32-0")

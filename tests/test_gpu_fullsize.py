@@ -77,16 +77,21 @@ def tile_pixels(sample, tiles_x, W, H):
     return m
 
 
-@pytest.mark.parametrize("config,kind,cam_index", [("paper_sh3", "sh3", 3), ("paper_latent", "latent", 9),
-                                                    ("paper_neural", "neural", 7), ("paper_nasg", "nasg", 11),
-                                                    ("paper_nasgabor", "nasgabor", 13), ("stress", "sh3", 5)])
-def test_full_size_sampled(config, kind, cam_index):
+@pytest.mark.parametrize("config,kind,cam_index,arch", [("paper_sh3", "sh3", 3, None),
+                                                         ("paper_latent", "latent", 9, None),
+                                                         ("paper_neural", "neural", 7, None),
+                                                         ("paper_neural", "neural", 5, (2, 32, 0)),
+                                                         ("paper_nasg", "nasg", 11, None),
+                                                         ("paper_nasgabor", "nasgabor", 13, None),
+                                                         ("stress", "sh3", 5, None)])
+def test_full_size_sampled(config, kind, cam_index, arch):
     latent = kind in ("latent", "neural")
-    sc = inputs.make_scene(config, appearance=(kind,))
+    sc = inputs.make_scene(config, appearance=(kind,), neural_arch=arch)
     cam = inputs.make_cameras(config)[cam_index]
     W, H = cam.width, cam.height
     tiles_x, tiles_y = orc.tile_grid(cam)
-    say("case full-size %s %s camera %d: n=%d %dx%d" % (config, kind, cam_index, sc.n, W, H))
+    say("case full-size %s %s%s camera %d: n=%d %dx%d" % (config, kind, "" if arch is None else " %d-%d-%d" % arch,
+                                                          cam_index, sc.n, W, H))
 
     pre = orc.preprocess(cam, sc, kind=kind, half_act=latent)
     P_ref = int(pre["tiles"].astype(np.int64).sum())

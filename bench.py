@@ -176,6 +176,17 @@ def main():
     elapsed = time.perf_counter() - t_start
     it_s = args.steps / elapsed
 
+    # per-step spread: the same K steps again, a pair of events around each
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step(i)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    step_times = np.array([a.elapsed_time(b) for a, b in ev])
+    step_spread = {"mean": round(float(step_times.mean()), 4), "median": round(float(np.median(step_times)), 4),
+                   "min": round(float(step_times.min()), 4), "max": round(float(step_times.max()), 4)}
+
     # blended pairs per image (sum of n_contrib), for the blend's work figure
     contrib = []
     for i in range(len(cstructs)):
@@ -317,6 +328,7 @@ def main():
         "pairs_avg": int(pairs_avg),
         "blended_pairs_avg": int(np.mean(contrib)),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "step_ms": step_spread,
         "hbm_stages": hbm_all,
         "roofline": roofline,
         "train_step": train,

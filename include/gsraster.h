@@ -121,8 +121,9 @@ typedef struct gs_appearance {
     const uint16_t* mlp_w;    /* LATENT_MLP: binary16 W1[32][17], W2[32][32], W3[3][32], row-major
                                  [out][in], concatenated (1664 values). The decoder sees d
                                  rounded to binary16 and accumulates in fp32.
-                                 NEURAL: binary16 W1[16][32], W2[16][16], W3[3][16] (816 values);
-                                 the decoder's inputs and hidden activations are binary16,
+                                 NEURAL: binary16 W1[16][32], W2[16][16], W3[3][16] (816 values;
+                                 other neural_layers / neural_width: W1[W][32], L - 1 matrices
+                                 [W][W], Wout[3][W]); the decoder's inputs and hidden activations are binary16,
                                  its sums fp32, tanh in fp32 */
     const float* base_color;  /* NEURAL: [3][n] fp32 base colour c0 */
     const uint16_t* features; /* NEURAL: [8][n] binary16 bit patterns */
@@ -182,10 +183,12 @@ typedef struct gs_grads {
     float* dopacity_logits;   /* [n] */
     float* dsh;               /* SH3: [48][n]; rows of bands above sh_degree are zero */
     float* dlatent;           /* LATENT_MLP: [14][n] fp32 */
-    float* dmlp_w;            /* LATENT_MLP: [1664], NEURAL: [816] fp32, same order as mlp_w */
+    float* dmlp_w;            /* LATENT_MLP: [1664], NEURAL: [816] (as many as mlp_w holds for other
+                                 configurations) fp32, same order as mlp_w */
     float* dmean2d;           /* optional (may be NULL): [2][n] screen-space mean gradient */
     float* dbase_color;       /* NEURAL, NASG, NASGABOR: [3][n] */
-    float* dfeatures;         /* NEURAL: [8][n] fp32 (the gradient passes the binary16 storage) */
+    float* dfeatures;         /* NEURAL: [8][n] fp32, [16][n] with neural_raw16 (the gradient
+                                 passes the binary16 storage) */
     float* dlobes;            /* NASG: [8][n], NASGABOR: [9][n], rows as in gs_appearance.lobes */
 } gs_grads;
 

@@ -425,26 +425,33 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
     }
 }
 
-template <typename KeyT>
-__device__ __forceinline__ uint32_t lower_bound_key(const KeyT* a, uint32_t count, uint32_t v)
-{
-    uint32_t lo = 0, hi = count;
-    while (lo < hi) {
-        const uint32_t mid = lo + ((hi - lo) >> 1);
-        if ((uint32_t)a[mid] < v) lo = mid + 1;
-        else hi = mid;
-    }
-    return lo;
-}
-
+// One wave per tile boundary v = 0..n_tiles: the first position whose tile id
+// is >= v, by a 64-way search. Each round the lanes probe 64 evenly spaced
+// positions of [lo, hi); the probes below v form a prefix (the keys are
+// sorted), so their count c narrows the answer to (probe c-1, probe c]. About
+// log64(P) dependent loads instead of log2(P). Boundary v ends tile v - 1 and
+// starts tile v.
 template <typename KeyT>
 __global__ __launch_bounds__(kBlock) void k_ranges(const KeyT* __restrict__ sorted_tiles, uint32_t count,
                                                    int n_tiles, uint32_t* __restrict__ ranges)
 {
-    const int t = blockIdx.x * kBlock + threadIdx.x;
-    if (t >= n_tiles) return;
-    ranges[2 * t] = lower_bound_key(sorted_tiles, count, (uint32_t)t);
-    ranges[2 * t + 1] = lower_bound_key(sorted_tiles, count, (uint32_t)t + 1);
+    const int v = (int)blockIdx.x * (kBlock / kWave) + (int)(threadIdx.x >> 6);
+    if (v > n_tiles) return;
+    const uint32_t lane = __lane_id();
+    uint32_t lo = 0, hi = count;   // the answer lies in [lo, hi]
+    while (hi > lo) {
+        const uint32_t step = (hi - lo + kWave - 1) / kWave;
+        const uint32_t p = lo + lane * step;
+        const bool below = p < hi && (uint32_t)sorted_tiles[p] < (uint32_t)v;
+        const uint32_t c = (uint32_t)__popcll(__ballot(below));
+        const uint32_t nlo = c ? lo + (c - 1) * step + 1 : lo;
+        hi = min(hi, lo + c * step);
+        lo = nlo;
+    }
+    if (lane == 0) {
+        if (v < n_tiles) ranges[2 * v] = lo;
+        if (v > 0) ranges[2 * v - 1] = lo;
+    }
 }
 
 }  // namespace
@@ -549,7 +556,7 @@ hipError_t launch_ranges(const Cam& cam, uint64_t num_pairs, TileKeys sorted_til
                          hipStream_t s)
 {
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    const dim3 grid((unsigned)div_up(n_tiles, kBlock));
+    const dim3 grid((unsigned)div_up(n_tiles + 1, kBlock / kWave));
     if (sorted_tiles.narrow)
         hipLaunchKernelGGL(k_ranges<uint16_t>, grid, dim3(kBlock), 0, s, static_cast<const uint16_t*>(sorted_tiles.p),
                            (uint32_t)num_pairs, n_tiles, tile_ranges);

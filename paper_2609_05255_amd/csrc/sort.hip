@@ -72,10 +72,13 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const KeyT* __restrict__ 
 {
     constexpr int R = 1 << kBits;
     constexpr int kTile = kBlock * kItems;
-    __shared__ uint32_t h[4][R];
-    for (int k = threadIdx.x; k < 4 * R; k += kBlock) (&h[0][0])[k] = 0;
+    // 16 copies of the counts (per wave and lane % 4): a skewed digit, such as
+    // the exponent byte of the depth keys, then meets at most 16 lanes of an
+    // instruction on one counter
+    __shared__ uint32_t h[16][R];
+    for (int k = threadIdx.x; k < 16 * R; k += kBlock) (&h[0][0])[k] = 0;
     __syncthreads();
-    const int wave = threadIdx.x >> 6;
+    const int copy = (threadIdx.x >> 6) * 4 + (threadIdx.x & 3);
     const uint64_t base = (uint64_t)blockIdx.x * kTile;
     // all loads first (one memory round trip), then the counts
     uint32_t k[kItems];
@@ -87,11 +90,16 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const KeyT* __restrict__ 
 #pragma unroll
     for (int r = 0; r < kItems; ++r) {
         const uint64_t idx = base + (uint64_t)r * kBlock + threadIdx.x;
-        if (idx < count) atomicAdd(&h[wave][(k[r] >> shift) & (R - 1)], 1u);
+        if (idx < count) atomicAdd(&h[copy][(k[r] >> shift) & (R - 1)], 1u);
     }
     __syncthreads();
     const int d = threadIdx.x;
-    if (d < R) hist[(size_t)d * nblocks + blockIdx.x] = h[0][d] + h[1][d] + h[2][d] + h[3][d];
+    if (d < R) {
+        uint32_t c = 0;
+#pragma unroll
+        for (int w = 0; w < 16; ++w) c += h[w][d];
+        hist[(size_t)d * nblocks + blockIdx.x] = c;
+    }
 }
 
 // One workgroup per digit: exclusive scan of that digit's counts over workgroups.

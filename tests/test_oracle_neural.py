@@ -187,6 +187,53 @@ def test_configurations_selector_networks(orc, arch, k):
     assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12)
 
 
+def routed_selector(layers, width, k):
+    """Far-from-symmetric weights: W1[3][k] = 1 puts input k on hidden unit 3,
+    each hidden-to-hidden matrix moves unit u to (u + 5) mod width
+    (W[(u + 5) % width][u] = 1), and the output layer reads the unit the input
+    ends on. Any of the matrices read in [in][out] order instead of the
+    boundary's [out][in] routes another input, or none, to the outputs."""
+    w = np.zeros(32 * width + (layers - 1) * width * width + 3 * width, np.float16)
+    w[3 * 32 + k] = 1.0
+    off, unit = 32 * width, 3
+    for _ in range(layers - 1):
+        for u in range(width):
+            w[off + ((u + 5) % width) * width + u] = 1.0
+        off += width * width
+        unit = (unit + 5) % width
+    for ch in range(3):
+        w[off + ch * width + unit] = 1.0
+    return w.view(np.uint16)
+
+
+@pytest.mark.parametrize("arch", [(1, 16, 0), (2, 16, 0), (3, 16, 0), (2, 32, 0), (3, 32, 0), (2, 16, 1)])
+@pytest.mark.parametrize("k", [1, 16, 27])
+def test_weight_orientation(orc, arch, k):
+    layers, width, raw16 = arch
+    sc = inputs.make_scene("tiny", n=64, appearance=("neural",), neural_arch=arch)
+    sc.neural_w = routed_selector(layers, width, k)
+    cam = inputs.make_cameras("tiny")[0]
+    f = sc.features.view(np.float16).astype(np.float64)
+    d = directions(sc, cam)
+    if k == 1:
+        x = -C1 * d[1]
+    elif raw16:
+        x = f[k - 16]
+    else:
+        j = (k - 16) // 2
+        x = np.sin(f[j]) if k % 2 == 0 else np.cos(f[j])
+    expect = np.maximum(0.0, base(sc) + np.tanh(np.maximum(0.0, x))[None] + 0.5)
+    col, vis = colours(orc, sc, cam, 1)
+    assert np.allclose(col[:, vis], expect[:, vis], rtol=0, atol=1e-12)
+    # the pin has teeth: the expected residual is non-zero somewhere, while a
+    # transposed read of the square matrices moves the input by -5 per layer
+    # (ending on a unit the output layer does not read) and a transposed
+    # 32 x 32 W1 routes nothing to unit 3: either way the residual would be 0
+    assert (np.maximum(0.0, x)[vis] > 0.05).any()
+    if layers > 1:
+        assert (3 - 5 * (layers - 1)) % width != (3 + 5 * (layers - 1)) % width
+
+
 def test_configurations_weight_counts(orc):
     # the paper's default decoder has 816 parameters (Sec. 4); the table's wider
     # variant 32 -> 32 -> 32 -> 3 needs 2144 multiply-adds, all of them weights

@@ -406,6 +406,53 @@ def test_mlp_closed_forms(orc):
     assert np.array_equal(pre_h["color"], pre["color"])
 
 
+def _routed_selector_mlp():
+    """Every layer moves its units by its own offset, so each weight matrix is
+    far from symmetric: W1[(k + 3) % 32][k] = 1 routes input k to hidden unit
+    k + 3, W2[(u + 5) % 32][u] = 1 moves unit u to u + 5, and W3 reads units
+    8, 22 and 24, i.e. inputs 0 (latent 0), 14 (view direction x) and 16
+    (view direction z, negated). Read in [in][out] order instead of the
+    [out][in] of the boundary, any of the three matrices routes other inputs
+    (or none) to the outputs."""
+    W1 = np.zeros((32, 17))
+    for k in range(17):
+        W1[(k + 3) % 32, k] = 1.0
+    W2 = np.zeros((32, 32))
+    for u in range(32):
+        W2[(u + 5) % 32, u] = 1.0
+    W3 = np.zeros((3, 32))
+    W3[0, 8] = 1.0
+    W3[1, 22] = 1.0
+    W3[2, 24] = -1.0
+    w = np.concatenate([W1.ravel(), W2.ravel(), W3.ravel()]).astype(np.float16)
+    return w.view(np.uint16)
+
+
+def test_mlp_weight_orientation(orc):
+    # [out][in] order of every layer, pinned by a routing that no transposed
+    # (or otherwise misindexed) read of W1, W2 or W3 reproduces
+    rng = np.random.default_rng(23)
+    sc = inputs.make_scene("tiny", appearance=("latent",))
+    cam = inputs.make_cameras("tiny")[0]
+    sc.mlp_w = _routed_selector_mlp()
+    sc.latent = rng.normal(0, 0.5, size=(14, sc.n)).astype(np.float16).view(np.uint16)
+    pre = orc.preprocess(cam, sc, kind="latent", mode="f64")
+    vis = pre["tiles"] > 0
+    z = sc.latent.view(np.float16).astype(np.float64)
+    d = sc.means.astype(np.float64) - cam.campos.astype(np.float64)[:, None]
+    d /= np.linalg.norm(d, axis=0)
+    dh = d.astype(np.float16).astype(np.float64)
+    sig = lambda x: 1 / (1 + np.exp(-x))
+    expect = np.stack([sig(np.maximum(0, z[0])), sig(np.maximum(0, dh[0])), sig(-np.maximum(0, dh[2]))])
+    assert np.allclose(pre["color"][:, vis], expect[:, vis], rtol=0, atol=1e-15)
+    # the same network read transposed gives other colours: the pin has teeth
+    w = sc.mlp_w.view(np.float16).astype(np.float64)
+    W1, W2, W3 = w[:544].reshape(32, 17), w[544:1568].reshape(32, 32), w[1568:].reshape(3, 32)
+    x = np.concatenate([z, dh])                                   # [17][n]
+    wrong = sig(W3 @ np.maximum(0, W2.T @ np.maximum(0, W1 @ x)))
+    assert np.abs(wrong - expect)[:, vis].max() > 0.05
+
+
 def test_mlp_half_activations_stay_close(orc):
     rng = np.random.default_rng(22)
     x = rng.normal(0, 0.5, size=(400, 17)).astype(np.float16).view(np.uint16)

@@ -221,11 +221,20 @@ gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_ap
  * Gaussian index), tile id = ty * ceil(width/16) + tx. tile_ranges[t] =
  * {first, one-past-last} position of tile t; an empty tile gets {s, s} with s
  * the number of pairs of lower tiles. The result is unique (bit-exact).
- * num_pairs: P as returned by gs_preprocess (host value).
- * capacity: length of values and tile_ids; GS_ERR_CAPACITY if num_pairs > capacity.
+ * num_pairs: P as gs_preprocess returned it to the host (host mode), or
+ *   GS_PAIRS_ON_DEVICE (device mode): the kernels then read P from
+ *   pre->num_pairs on the device, so the call needs no synchronisation and no
+ *   host read-back of P.
+ * capacity: length of values and tile_ids. Host mode: GS_ERR_CAPACITY if
+ *   num_pairs > capacity, nothing enqueued. Device mode: a P above capacity is
+ *   found on the device; no pair is then written, every tile range comes out
+ *   empty ({0, 0}: the image renders as background and the gradients as zero),
+ *   and pre->num_pairs keeps the P needed, for the caller to compare with
+ *   capacity when it next synchronises and to retry with a larger buffer.
  * values: [capacity] u32 device; tile_ids: optional [capacity] u32 tile of each pair.
  * tile_ranges: [n_tiles][2] u32 device.
  */
+#define GS_PAIRS_ON_DEVICE UINT64_MAX
 gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, uint64_t num_pairs,
                       uint64_t capacity, uint32_t* values, uint32_t* tile_ids, uint32_t* tile_ranges,
                       void* workspace, size_t workspace_bytes, void* stream);
@@ -324,20 +333,28 @@ gs_status gs_adam_step(const gs_adam_tensor* tensors, int32_t count, float beta1
 gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t capacity, int32_t kind,
                             size_t* bytes);
 
-/* Kernel timing. When enabled, every kernel the library launches is bracketed
- * by HIP events on its stream (events are created here, not while rendering).
- * gs_timing_read synchronises the recorded events and returns, per kernel id
- * (GS_KERNEL_*), the summed duration in ms and the launch count since the last
- * reset; `count` is the length of both host arrays. */
+/* Kernel timing. A gs_timer is a caller-owned timing context holding its own
+ * HIP events (created with the timer, on the current device, never while
+ * rendering). While a timer is attached to a thread, every kernel the library
+ * launches from that thread is bracketed by a pair of events on its stream.
+ * gs_timer_read synchronises the recorded events and returns, per kernel id
+ * (GS_KERNEL_*), the summed duration in ms and the launch count since the
+ * last reset; `count` is the length of both host arrays. A timer is used by
+ * one thread at a time; gs_timer_attach(NULL) detaches; destroying the timer
+ * attached to the calling thread detaches it. The library keeps no other
+ * state between calls than the calling thread's attached timer and error text. */
 enum {
     GS_KERNEL_PREPROCESS = 0, GS_KERNEL_PAIR_COUNT, GS_KERNEL_DEPTH_SORT, GS_KERNEL_PAIR_OFFSETS,
     GS_KERNEL_DUPLICATE, GS_KERNEL_TILE_SORT, GS_KERNEL_RANGES, GS_KERNEL_BLEND_FWD,
     GS_KERNEL_CLEAR, GS_KERNEL_BLEND_BWD, GS_KERNEL_PREPROCESS_BWD, GS_KERNEL_MLP_REDUCE,
     GS_KERNEL_ADAM, GS_KERNEL_NEURAL_FOLD, GS_KERNEL_COUNT
 };
-gs_status gs_timing_enable(int32_t enable);
-gs_status gs_timing_reset(void);
-gs_status gs_timing_read(double* ms, int64_t* launches, int32_t count);
+typedef struct gs_timer gs_timer;
+gs_status gs_timer_create(gs_timer** out);
+gs_status gs_timer_destroy(gs_timer* timer);
+gs_status gs_timer_attach(gs_timer* timer);
+gs_status gs_timer_reset(gs_timer* timer);
+gs_status gs_timer_read(gs_timer* timer, double* ms, int64_t* launches, int32_t count);
 const char* gs_kernel_name(int32_t kernel_id);
 
 const char* gs_last_error(void);

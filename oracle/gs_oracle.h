@@ -134,8 +134,10 @@ int64_t orc_bin_sort(int64_t n, const int32_t* rect, const double* depth, const 
                      int32_t tiles_x, int32_t tiles_y, int64_t capacity, int32_t* values,
                      int32_t* tile_of, int64_t* ranges);
 
-/* margin (nullable): per pixel, the smallest relative distance of any of its
- * skip/stop/clamp decisions to the threshold that decides it. */
+/* margin (nullable): per pixel, the smallest ratio, over its skip/stop/clamp
+ * decisions, of the decision's relative distance from its threshold to a bound
+ * on how far an fp32 evaluation in another operation order can move it (see
+ * walk_pixel); above 1 every decision of the pixel is reproducible. */
 void orc_render_fwd_f32(const orc_camera* cam, int64_t n, const orc_pre* pre, const int64_t* ranges,
                         const int32_t* values, double* image, double* final_T, int32_t* n_contrib,
                         double* margin);

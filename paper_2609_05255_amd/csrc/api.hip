@@ -5,7 +5,6 @@
 #include <stdio.h>
 #include <string.h>
 
-#include <mutex>
 #include <string>
 #include <vector>
 
@@ -131,27 +130,37 @@ struct TimedLaunch {
     hipEvent_t a, b;
 };
 
-std::mutex g_tmu;
-bool g_timing = false;
-std::vector<hipEvent_t> g_free_events;
-std::vector<TimedLaunch> g_pending;
-std::vector<TimedLaunch> g_open;
-double g_ms[GS_KERNEL_COUNT];
-int64_t g_launches[GS_KERNEL_COUNT];
+void resolve_pending(gs_timer* t);
 
-void resolve_pending_locked()
+}  // namespace
+
+// A caller-owned timing context (gs_timer_create). The library itself keeps
+// only the calling thread's pointer to the timer attached to it.
+struct gs_timer {
+    std::vector<hipEvent_t> free_events;
+    std::vector<TimedLaunch> pending;
+    std::vector<TimedLaunch> open;
+    double ms[GS_KERNEL_COUNT];
+    int64_t launches[GS_KERNEL_COUNT];
+};
+
+namespace {
+
+thread_local gs_timer* t_timer = nullptr;
+
+void resolve_pending(gs_timer* t)
 {
-    for (auto& t : g_pending) {
+    for (auto& l : t->pending) {
         float ms = 0.f;
-        (void)hipEventSynchronize(t.b);
-        if (hipEventElapsedTime(&ms, t.a, t.b) == hipSuccess) {
-            g_ms[t.id] += ms;
-            g_launches[t.id] += 1;
+        (void)hipEventSynchronize(l.b);
+        if (hipEventElapsedTime(&ms, l.a, l.b) == hipSuccess) {
+            t->ms[l.id] += ms;
+            t->launches[l.id] += 1;
         }
-        g_free_events.push_back(t.a);
-        g_free_events.push_back(t.b);
+        t->free_events.push_back(l.a);
+        t->free_events.push_back(l.b);
     }
-    g_pending.clear();
+    t->pending.clear();
 }
 
 const char* const kKernelNames[GS_KERNEL_COUNT] = {
@@ -164,29 +173,29 @@ namespace gsr {
 
 void timing_begin(int id, hipStream_t s)
 {
-    if (!g_timing) return;
-    std::lock_guard<std::mutex> lk(g_tmu);
-    if (g_free_events.size() < 2) resolve_pending_locked();
-    if (g_free_events.size() < 2) return;
-    TimedLaunch t;
-    t.id = id;
-    t.a = g_free_events.back();
-    g_free_events.pop_back();
-    t.b = g_free_events.back();
-    g_free_events.pop_back();
-    (void)hipEventRecord(t.a, s);
-    g_open.push_back(t);
+    gs_timer* t = t_timer;
+    if (!t) return;
+    if (t->free_events.size() < 2) resolve_pending(t);
+    if (t->free_events.size() < 2) return;
+    TimedLaunch l;
+    l.id = id;
+    l.a = t->free_events.back();
+    t->free_events.pop_back();
+    l.b = t->free_events.back();
+    t->free_events.pop_back();
+    (void)hipEventRecord(l.a, s);
+    t->open.push_back(l);
 }
 
 void timing_end(int id, hipStream_t s)
 {
-    if (!g_timing) return;
-    std::lock_guard<std::mutex> lk(g_tmu);
-    for (size_t k = g_open.size(); k-- > 0;) {
-        if (g_open[k].id == id) {
-            (void)hipEventRecord(g_open[k].b, s);
-            g_pending.push_back(g_open[k]);
-            g_open.erase(g_open.begin() + (long)k);
+    gs_timer* t = t_timer;
+    if (!t) return;
+    for (size_t k = t->open.size(); k-- > 0;) {
+        if (t->open[k].id == id) {
+            (void)hipEventRecord(t->open[k].b, s);
+            t->pending.push_back(t->open[k]);
+            t->open.erase(t->open.begin() + (long)k);
             return;
         }
     }
@@ -312,21 +321,27 @@ gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t 
     GS_CHECK(n >= 0 && n < ((int64_t)1 << 31), "n out of range");
     if ((st = check_pre(pre, n)) != GS_OK) return st;
     GS_CHECK(capacity < ((uint64_t)1 << 32), "capacity must be below 2^32");
-    if (num_pairs > capacity)
+    const bool on_device = num_pairs == GS_PAIRS_ON_DEVICE;
+    if (!on_device && num_pairs > capacity)
         return fail(GS_ERR_CAPACITY, "%llu pairs exceed the capacity %llu", (unsigned long long)num_pairs,
                     (unsigned long long)capacity);
     GS_CHECK(tile_ranges != nullptr, "tile_ranges is NULL");
-    GS_CHECK(num_pairs == 0 || values != nullptr, "values is NULL");
+    GS_CHECK((on_device ? capacity : num_pairs) == 0 || values != nullptr, "values is NULL");
     const Workspace need = layout_workspace(nullptr, n, capacity, GS_APP_SH3);
     if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
     const Workspace ws = layout_workspace(workspace, n, capacity, GS_APP_SH3);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const Cam c = make_cam(*cam);
     const int n_tiles = c.tiles_x * c.tiles_y;
-    if (num_pairs == 0 || n == 0) {
+    if (n == 0 || (on_device ? capacity : num_pairs) == 0) {
+        // no pair can be listed (in device mode a positive count then exceeds
+        // the capacity; it stays in num_pairs for the caller to see)
         GS_HIP(launch_fill_u32(tile_ranges, 2 * (int64_t)n_tiles, 0u, s));
         return ok();
     }
+    // device mode: the kernels read P from pre->num_pairs and size nothing by it
+    const PairCount pairs = on_device ? PairCount{pre->num_pairs, capacity, capacity}
+                                      : PairCount{nullptr, num_pairs, capacity};
     const uint32_t* order = nullptr;
     timing_begin(GS_KERNEL_DEPTH_SORT, s);
     GS_HIP(launch_depth_sort(n, pre->depth_key, pre->splats, ws, &order, s));
@@ -346,15 +361,15 @@ gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t 
         sorted_tiles = dup_keys;
     }
     timing_begin(GS_KERNEL_DUPLICATE, s);
-    GS_HIP(launch_duplicate(c, n, order, *pre, ws, (uint32_t)capacity, dup_keys, dup_vals, s));
+    GS_HIP(launch_duplicate(c, n, order, ws, pairs, dup_keys, dup_vals, s));
     timing_end(GS_KERNEL_DUPLICATE, s);
     if (passes > 0) {
         timing_begin(GS_KERNEL_TILE_SORT, s);
-        GS_HIP(launch_tile_sort(c, num_pairs, ws, values, tile_ids, &sorted_tiles, s));
+        GS_HIP(launch_tile_sort(c, pairs, ws, values, tile_ids, &sorted_tiles, s));
         timing_end(GS_KERNEL_TILE_SORT, s);
     }
     timing_begin(GS_KERNEL_RANGES, s);
-    GS_HIP(launch_ranges(c, num_pairs, sorted_tiles, tile_ranges, s));
+    GS_HIP(launch_ranges(c, pairs, sorted_tiles, tile_ranges, s));
     timing_end(GS_KERNEL_RANGES, s);
     return ok();
 }
@@ -449,34 +464,54 @@ gs_status gs_neural_fold(const uint16_t* features, const uint16_t* mlp_w, int64_
     return ok();
 }
 
-gs_status gs_timing_enable(int32_t enable)
+gs_status gs_timer_create(gs_timer** out)
 {
-    std::lock_guard<std::mutex> lk(g_tmu);
-    if (enable && g_free_events.empty() && g_pending.empty()) {
-        for (int k = 0; k < 2048; ++k) {
-            hipEvent_t e;
-            if (hipEventCreate(&e) != hipSuccess) return fail(GS_ERR_DEVICE, "hipEventCreate failed");
-            g_free_events.push_back(e);
+    GS_CHECK(out != nullptr, "out is NULL");
+    gs_timer* t = new gs_timer();
+    for (int k = 0; k < GS_KERNEL_COUNT; ++k) { t->ms[k] = 0.0; t->launches[k] = 0; }
+    for (int k = 0; k < 2048; ++k) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) {
+            gs_timer_destroy(t);
+            return fail(GS_ERR_DEVICE, "hipEventCreate failed");
         }
+        t->free_events.push_back(e);
     }
-    g_timing = enable != 0;
+    *out = t;
     return ok();
 }
 
-gs_status gs_timing_reset(void)
+gs_status gs_timer_destroy(gs_timer* t)
 {
-    std::lock_guard<std::mutex> lk(g_tmu);
-    resolve_pending_locked();
-    for (int k = 0; k < GS_KERNEL_COUNT; ++k) { g_ms[k] = 0.0; g_launches[k] = 0; }
+    if (!t) return ok();
+    if (t_timer == t) t_timer = nullptr;
+    resolve_pending(t);
+    for (auto& l : t->open) t->free_events.insert(t->free_events.end(), {l.a, l.b});
+    for (hipEvent_t e : t->free_events) (void)hipEventDestroy(e);
+    delete t;
     return ok();
 }
 
-gs_status gs_timing_read(double* ms, int64_t* launches, int32_t count)
+gs_status gs_timer_attach(gs_timer* t)
 {
+    t_timer = t;
+    return ok();
+}
+
+gs_status gs_timer_reset(gs_timer* t)
+{
+    GS_CHECK(t != nullptr, "timer is NULL");
+    resolve_pending(t);
+    for (int k = 0; k < GS_KERNEL_COUNT; ++k) { t->ms[k] = 0.0; t->launches[k] = 0; }
+    return ok();
+}
+
+gs_status gs_timer_read(gs_timer* t, double* ms, int64_t* launches, int32_t count)
+{
+    GS_CHECK(t != nullptr, "timer is NULL");
     GS_CHECK(ms != nullptr && launches != nullptr, "output arrays are NULL");
-    std::lock_guard<std::mutex> lk(g_tmu);
-    resolve_pending_locked();
-    for (int k = 0; k < count && k < GS_KERNEL_COUNT; ++k) { ms[k] = g_ms[k]; launches[k] = g_launches[k]; }
+    resolve_pending(t);
+    for (int k = 0; k < count && k < GS_KERNEL_COUNT; ++k) { ms[k] = t->ms[k]; launches[k] = t->launches[k]; }
     return ok();
 }
 

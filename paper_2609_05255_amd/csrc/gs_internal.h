@@ -94,6 +94,24 @@ struct Workspace {
 
 Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kind);
 
+// Number of (tile, Gaussian) pairs as the bin-sort kernels see it. Host mode:
+// `host` is P itself. Device mode: P is read on the device from the
+// preprocess's count `dev`, `host` is the capacity the grids are sized for,
+// and a count above the capacity reads as 0 (no pairs are emitted and every
+// tile range comes out empty; the count itself stays in place for the caller).
+struct PairCount {
+    const uint64_t* dev;
+    uint64_t host;
+    uint64_t cap;
+    __device__ __forceinline__ uint64_t get() const
+    {
+        if (!dev) return host;
+        const uint64_t p = *dev;
+        return p <= cap ? p : 0;
+    }
+    __device__ __forceinline__ bool overflow() const { return dev && *dev > cap; }
+};
+
 // ---- launch helpers (defined in the kernel files) ---------------------------
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                              const gs_preprocessed& out, const Workspace& ws, hipStream_t s);
@@ -107,15 +125,14 @@ struct TileKeys {
     bool narrow;
 };
 bool tile_keys_narrow(const Cam& cam);
-hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const gs_preprocessed& pre,
-                            const Workspace& ws, uint32_t capacity, TileKeys keys_out, uint32_t* vals_out,
-                            hipStream_t s);
+hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const Workspace& ws,
+                            PairCount pairs, TileKeys keys_out, uint32_t* vals_out, hipStream_t s);
 int tile_sort_passes(const Cam& cam);
 hipError_t launch_fill_u32(uint32_t* p, int64_t count, uint32_t value, hipStream_t s);
-hipError_t launch_tile_sort(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
+hipError_t launch_tile_sort(const Cam& cam, PairCount pairs, const Workspace& ws, uint32_t* values,
                             uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s);
-hipError_t launch_ranges(const Cam& cam, uint64_t num_pairs, TileKeys sorted_tiles,
-                         uint32_t* tile_ranges, hipStream_t s);
+hipError_t launch_ranges(const Cam& cam, PairCount pairs, TileKeys sorted_tiles, uint32_t* tile_ranges,
+                         hipStream_t s);
 hipError_t launch_blend_fwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                             const uint32_t* tile_ranges, float* image, float* final_T, uint32_t* n_contrib,
                             hipStream_t s);

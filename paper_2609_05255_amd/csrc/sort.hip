@@ -67,11 +67,17 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid)
 }
 
 template <int kBits, int kItems, typename KeyT>
-__global__ __launch_bounds__(kBlock) void k_radix_hist(const KeyT* __restrict__ keys, uint64_t count, int shift,
+__global__ __launch_bounds__(kBlock) void k_radix_hist(const KeyT* __restrict__ keys, PairCount cnt, int shift,
                                                        uint32_t* __restrict__ hist, int nblocks)
 {
     constexpr int R = 1 << kBits;
     constexpr int kTile = kBlock * kItems;
+    const uint64_t count = cnt.get();
+    if ((uint64_t)blockIdx.x * kTile >= count) {
+        // a workgroup past the keys (the grid is sized for the capacity)
+        if (threadIdx.x < R) hist[(size_t)threadIdx.x * nblocks + blockIdx.x] = 0;
+        return;
+    }
     // 16 copies of the counts (per wave and lane % 4): a skewed digit, such as
     // the exponent byte of the depth keys, then meets at most 16 lanes of an
     // instruction on one counter
@@ -125,7 +131,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(uint32_t* __restrict__ hi
 
 template <int kBits, int kItems, typename KeyT, typename KeyOutT>
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict__ keys_in,
-                                                          const uint32_t* __restrict__ vals_in, uint64_t count,
+                                                          const uint32_t* __restrict__ vals_in, PairCount cnt,
                                                           int shift, const uint32_t* __restrict__ hist, int nblocks,
                                                           const uint32_t* __restrict__ digit_tot,
                                                           KeyOutT* __restrict__ keys_out,
@@ -142,6 +148,8 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict
     __shared__ KeyT skey[kTile];
     __shared__ uint32_t sval[kTile];
     __shared__ uint32_t lds4[4];
+    const uint64_t count = cnt.get();
+    if ((uint64_t)blockIdx.x * kTile >= count) return;   // past the keys: nothing to move
     const int t = threadIdx.x, wave = t >> 6, lane = __lane_id();
     const uint32_t dt = t < R ? digit_tot[t] : 0u;
     const uint32_t dbase = block_excl_scan(dt, lds4, nullptr);
@@ -217,30 +225,31 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict
 }
 
 // One stable LSD pass over `bits` bits at `shift`; vals_in == nullptr means
-// value = position, keys_out == nullptr drops the keys.
+// value = position, keys_out == nullptr drops the keys. The grids are sized
+// for cnt.host keys (the capacity in device mode).
 template <int kBits, int kItems, typename KeyT, typename KeyOutT>
-void radix_pass_t(const KeyT* keys_in, const uint32_t* vals_in, uint64_t count, int shift, KeyOutT* keys_out,
+void radix_pass_t(const KeyT* keys_in, const uint32_t* vals_in, PairCount cnt, int shift, KeyOutT* keys_out,
                   uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s,
                   const gs_splat* rect_src = nullptr, uint2* rect_out = nullptr)
 {
-    const int nblocks = (int)div_up((int64_t)count, (int64_t)kBlock * kItems);
-    hipLaunchKernelGGL((k_radix_hist<kBits, kItems, KeyT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, count, shift,
+    const int nblocks = (int)std::max<int64_t>(div_up((int64_t)cnt.host, (int64_t)kBlock * kItems), 1);
+    hipLaunchKernelGGL((k_radix_hist<kBits, kItems, KeyT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, cnt, shift,
                        hist, nblocks);
     hipLaunchKernelGGL(k_radix_scan, dim3(1 << kBits), dim3(kBlock), 0, s, hist, nblocks, digit_tot);
     hipLaunchKernelGGL((k_radix_scatter<kBits, kItems, KeyT, KeyOutT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in,
-                       vals_in, count, shift,
+                       vals_in, cnt, shift,
                        hist, nblocks, digit_tot, keys_out, vals_out, rect_src, rect_out);
 }
 
 // A tile-sort pass over `bits` (1..8) bits, chosen at run time.
 template <typename KeyT, typename KeyOutT>
-hipError_t radix_pass(const KeyT* keys_in, const uint32_t* vals_in, uint64_t count, int shift, int bits,
+hipError_t radix_pass(const KeyT* keys_in, const uint32_t* vals_in, PairCount cnt, int shift, int bits,
                       KeyOutT* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
 {
     switch (bits) {
 #define GS_PASS(b)                                                                                                   \
     case b:                                                                                                          \
-        radix_pass_t<b, kPairItems>(keys_in, vals_in, count, shift, keys_out, vals_out, hist, digit_tot, s);      \
+        radix_pass_t<b, kPairItems>(keys_in, vals_in, cnt, shift, keys_out, vals_out, hist, digit_tot, s);        \
         break;
         GS_PASS(1) GS_PASS(2) GS_PASS(3) GS_PASS(4) GS_PASS(5) GS_PASS(6) GS_PASS(7) GS_PASS(8)
 #undef GS_PASS
@@ -324,9 +333,12 @@ template <typename KeyT>
 __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict__ order,
                                                       const uint2* __restrict__ sorted_rect, int64_t n,
                                                       const uint32_t* __restrict__ part, int tiles_x,
-                                                      uint32_t capacity, KeyT* __restrict__ keys,
+                                                      PairCount pairs, KeyT* __restrict__ keys,
                                                       uint32_t* __restrict__ vals)
 {
+    // a device count beyond the capacity: no pair is emitted
+    if (pairs.overflow()) return;
+    const uint32_t capacity = (uint32_t)pairs.cap;
     __shared__ uint32_t soff[kDupChunk + 1];
     __shared__ uint32_t sgid[kDupChunk];
     __shared__ uint32_t sorg[kDupChunk];   // rectangle origin x0 | y0 << 16
@@ -440,9 +452,10 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
 // log64(P) dependent loads instead of log2(P). Boundary v ends tile v - 1 and
 // starts tile v.
 template <typename KeyT>
-__global__ __launch_bounds__(kBlock) void k_ranges(const KeyT* __restrict__ sorted_tiles, uint32_t count,
+__global__ __launch_bounds__(kBlock) void k_ranges(const KeyT* __restrict__ sorted_tiles, PairCount pairs,
                                                    int n_tiles, uint32_t* __restrict__ ranges)
 {
+    const uint32_t count = (uint32_t)pairs.get();
     const int v = (int)blockIdx.x * (kBlock / kWave) + (int)(threadIdx.x >> 6);
     if (v > n_tiles) return;
     const uint32_t lane = __lane_id();
@@ -471,14 +484,16 @@ hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_spla
     const uint32_t* vin = nullptr;
     uint32_t* kbuf[2] = {ws.keys_a, ws.keys_b};
     uint32_t* vbuf[2] = {ws.vals_a, ws.vals_b};
+    const PairCount keys_n{nullptr, (uint64_t)n, (uint64_t)n};
     for (int p = 0; p < 4; ++p) {
         const bool last = p == 3;
         uint32_t* kout = last ? nullptr : kbuf[p & 1];
         if (last)
-            radix_pass_t<8, kSortItems>(kin, vin, (uint64_t)n, 8 * p, (uint32_t*)nullptr, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s,
-                            splats, ws.sorted_rect);
+            radix_pass_t<8, kSortItems>(kin, vin, keys_n, 8 * p, (uint32_t*)nullptr, vbuf[p & 1], ws.hist,
+                                        ws.digit_tot + kRadix * p, s, splats, ws.sorted_rect);
         else
-            radix_pass_t<8, kSortItems>(kin, vin, (uint64_t)n, 8 * p, kout, vbuf[p & 1], ws.hist, ws.digit_tot + kRadix * p, s);
+            radix_pass_t<8, kSortItems>(kin, vin, keys_n, 8 * p, kout, vbuf[p & 1], ws.hist,
+                                        ws.digit_tot + kRadix * p, s);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         kin = kbuf[p & 1];
@@ -496,17 +511,16 @@ hipError_t launch_pair_offsets(int64_t n, const Workspace& ws, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const gs_preprocessed& pre,
-                            const Workspace& ws, uint32_t capacity, TileKeys keys_out, uint32_t* vals_out,
-                            hipStream_t s)
+hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const Workspace& ws,
+                            PairCount pairs, TileKeys keys_out, uint32_t* vals_out, hipStream_t s)
 {
     const int nb = (int)div_up(n, kDupChunk);
     if (keys_out.narrow)
         hipLaunchKernelGGL(k_duplicate<uint16_t>, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
-                           cam.tiles_x, capacity, static_cast<uint16_t*>(keys_out.p), vals_out);
+                           cam.tiles_x, pairs, static_cast<uint16_t*>(keys_out.p), vals_out);
     else
         hipLaunchKernelGGL(k_duplicate<uint32_t>, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
-                           cam.tiles_x, capacity, static_cast<uint32_t*>(keys_out.p), vals_out);
+                           cam.tiles_x, pairs, static_cast<uint32_t*>(keys_out.p), vals_out);
     return hipGetLastError();
 }
 
@@ -524,7 +538,7 @@ int tile_sort_passes(const Cam& cam) { return (tile_bits(cam) + 7) / 8; }
 bool tile_keys_narrow(const Cam& cam) { return (int64_t)cam.tiles_x * cam.tiles_y <= 65536; }
 
 template <typename KeyT>
-static hipError_t tile_sort_t(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
+static hipError_t tile_sort_t(const Cam& cam, PairCount num_pairs, const Workspace& ws, uint32_t* values,
                               uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s)
 {
     const int bits = tile_bits(cam);
@@ -553,24 +567,24 @@ static hipError_t tile_sort_t(const Cam& cam, uint64_t num_pairs, const Workspac
     return hipSuccess;
 }
 
-hipError_t launch_tile_sort(const Cam& cam, uint64_t num_pairs, const Workspace& ws, uint32_t* values,
+hipError_t launch_tile_sort(const Cam& cam, PairCount num_pairs, const Workspace& ws, uint32_t* values,
                             uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s)
 {
     return tile_keys_narrow(cam) ? tile_sort_t<uint16_t>(cam, num_pairs, ws, values, tile_ids_out, sorted_tiles, s)
                                  : tile_sort_t<uint32_t>(cam, num_pairs, ws, values, tile_ids_out, sorted_tiles, s);
 }
 
-hipError_t launch_ranges(const Cam& cam, uint64_t num_pairs, TileKeys sorted_tiles, uint32_t* tile_ranges,
+hipError_t launch_ranges(const Cam& cam, PairCount num_pairs, TileKeys sorted_tiles, uint32_t* tile_ranges,
                          hipStream_t s)
 {
     const int n_tiles = cam.tiles_x * cam.tiles_y;
     const dim3 grid((unsigned)div_up(n_tiles + 1, kBlock / kWave));
     if (sorted_tiles.narrow)
         hipLaunchKernelGGL(k_ranges<uint16_t>, grid, dim3(kBlock), 0, s, static_cast<const uint16_t*>(sorted_tiles.p),
-                           (uint32_t)num_pairs, n_tiles, tile_ranges);
+                           num_pairs, n_tiles, tile_ranges);
     else
         hipLaunchKernelGGL(k_ranges<uint32_t>, grid, dim3(kBlock), 0, s, static_cast<const uint32_t*>(sorted_tiles.p),
-                           (uint32_t)num_pairs, n_tiles, tile_ranges);
+                           num_pairs, n_tiles, tile_ranges);
     return hipGetLastError();
 }
 

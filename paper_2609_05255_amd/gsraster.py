@@ -20,6 +20,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libgsraster.so")
 
 GS_OK, GS_ERR_INVALID_ARG, GS_ERR_CAPACITY, GS_ERR_DEVICE, GS_ERR_UNSUPPORTED = range(5)
+GS_PAIRS_ON_DEVICE = (1 << 64) - 1   # gs_bin_sort reads the pair count on the device
 GS_APP_SH3, GS_APP_LATENT_MLP, GS_APP_NEURAL, GS_APP_NEURAL_FOLDED, GS_APP_NASG, GS_APP_NASGABOR = range(6)
 LOBE_ROWS = {GS_APP_NASG: 8, GS_APP_NASGABOR: 9}
 NEURAL_FEATURES = 8
@@ -100,11 +101,14 @@ def lib() -> C.CDLL:
         L.gs_mlp_eval.argtypes = [vp, i64, vp, vp, vp]
         L.gs_neural_fold.argtypes = [vp, vp, i64, vp, vp]
         L.gs_adam_step.argtypes = [P(AdamTensor), i32, C.c_float, C.c_float, i64, vp]
-        L.gs_timing_enable.argtypes = [i32]
-        L.gs_timing_reset.argtypes = []
-        L.gs_timing_read.argtypes = [P(C.c_double), P(i64), i32]
+        L.gs_timer_create.argtypes = [P(vp)]
+        L.gs_timer_destroy.argtypes = [vp]
+        L.gs_timer_attach.argtypes = [vp]
+        L.gs_timer_reset.argtypes = [vp]
+        L.gs_timer_read.argtypes = [vp, P(C.c_double), P(i64), i32]
         for f in ("gs_preprocess", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd", "gs_workspace_size", "gs_mlp_eval",
-                  "gs_adam_step", "gs_timing_enable", "gs_timing_reset", "gs_timing_read"):
+                  "gs_neural_fold", "gs_adam_step", "gs_timer_create", "gs_timer_destroy", "gs_timer_attach",
+                  "gs_timer_reset", "gs_timer_read"):
             getattr(L, f).restype = C.c_int
         L.gs_last_error.restype = C.c_char_p
         L.gs_version.restype = C.c_char_p
@@ -259,20 +263,58 @@ def gs_adam_step(tensors, beta1: float, eps: float, step: int, stream=None):
     _check(lib().gs_adam_step(arr, len(tensors), float(beta1), float(eps), int(step), _stream(stream)))
 
 
+class Timer:
+    """A caller-owned kernel-timing context (gs_timer_*): while attached to the
+    calling thread, every kernel the library launches from it is timed."""
+
+    def __init__(self):
+        h = C.c_void_p()
+        _check(lib().gs_timer_create(C.byref(h)))
+        self.handle = h
+
+    def attach(self):
+        _check(lib().gs_timer_attach(self.handle))
+
+    @staticmethod
+    def detach():
+        _check(lib().gs_timer_attach(None))
+
+    def reset(self):
+        _check(lib().gs_timer_reset(self.handle))
+
+    def read(self) -> dict:
+        k = len(KERNEL_NAMES)
+        ms = (C.c_double * k)()
+        cnt = (C.c_int64 * k)()
+        _check(lib().gs_timer_read(self.handle, ms, cnt, k))
+        return {KERNEL_NAMES[i]: (ms[i], cnt[i]) for i in range(k)}
+
+    def close(self):
+        if self.handle:
+            _check(lib().gs_timer_destroy(self.handle))
+            self.handle = None
+
+
+_timer = None
+
+
 def timing_enable(on: bool = True):
-    _check(lib().gs_timing_enable(1 if on else 0))
+    """Attaches (on) or detaches (off) this module's timer to the calling thread."""
+    global _timer
+    if on:
+        if _timer is None:
+            _timer = Timer()
+        _timer.attach()
+    else:
+        Timer.detach()
 
 
 def timing_reset():
-    _check(lib().gs_timing_reset())
+    _timer.reset()
 
 
 def timing_read() -> dict:
-    k = len(KERNEL_NAMES)
-    ms = (C.c_double * k)()
-    cnt = (C.c_int64 * k)()
-    _check(lib().gs_timing_read(ms, cnt, k))
-    return {KERNEL_NAMES[i]: (ms[i], cnt[i]) for i in range(k)}
+    return _timer.read()
 
 
 class Frame:
@@ -316,15 +358,24 @@ class Frame:
                            _ptr(self.dmean2d), _ptr(self.dbase_color), _ptr(self.dfeatures), _ptr(self.dlobes))
         self.last_pairs = 0
 
-    def forward(self, cam: Camera, scene: SceneTensors, sh_degree: int = 3, stream=None) -> int:
+    def forward(self, cam: Camera, scene: SceneTensors, sh_degree: int = 3, stream=None,
+                sync_pairs: bool = True):
+        """Preprocess, bin-sort and blend one image. sync_pairs=True reads the
+        pair count back to the host (and returns it) and fails with GS_ERR_CAPACITY
+        before sorting if it exceeds the capacity; sync_pairs=False keeps the count
+        on the device (no synchronisation): check pairs_overflowed() afterwards."""
         g, app = scene.gaussians(), scene.appearance(self.kind, sh_degree)
-        P = gs_preprocess(cam, g, app, self.pre, self.workspace, self.ws_bytes, stream)
-        gs_bin_sort(cam, self.pre, self.n, P, self.capacity, self.values, self.tile_ids, self.ranges,
-                    self.workspace, self.ws_bytes, stream)
+        P = gs_preprocess(cam, g, app, self.pre, self.workspace, self.ws_bytes, stream, sync_pairs=sync_pairs)
+        gs_bin_sort(cam, self.pre, self.n, P if sync_pairs else GS_PAIRS_ON_DEVICE, self.capacity, self.values,
+                    self.tile_ids, self.ranges, self.workspace, self.ws_bytes, stream)
         gs_render_fwd(cam, self.pre, self.n, self.values, self.ranges, self.image, self.final_T, self.n_contrib,
                       stream)
         self.last_pairs = P
         return P
+
+    def pairs_overflowed(self) -> bool:
+        """After a device-mode forward: did the pair count exceed the capacity (synchronises)?"""
+        return int(self.num_pairs.item()) > self.capacity
 
     def backward(self, cam: Camera, scene: SceneTensors, dL_dimage, sh_degree: int = 3, stream=None):
         g, app = scene.gaussians(), scene.appearance(self.kind, sh_degree)

@@ -11,12 +11,23 @@ from oracle import oracle as orc
 from paper_2609_05255_amd import gsraster as gs
 from paper_2609_05255_amd import inputs
 
-# A pixel whose oracle skip/stop/cap decisions all lie farther than this
-# relative distance from their thresholds takes the same decisions on the GPU:
-# the GPU's alpha differs from the oracle's by a few fp32 ulps (exp2-based exp,
-# fused multiply-adds) and its transmittance by at most ~1e-6 relative after
-# hundreds of factors.
-MARGIN = 1e-5
+# The oracle reports, per pixel, the smallest ratio of a skip/stop/cap
+# decision's distance from its threshold to a bound on how far the GPU's fp32
+# evaluation (fused multiply-adds, base-2 exponential) can move the decided
+# quantity (see walk_pixel in the oracle). Above 1 the GPU must decide every
+# entry of the pixel as the oracle does; at or below 1 the pixel is "flagged":
+# it is left out of the image comparison and its upstream gradient is set to
+# zero before either side runs the backward, so no Gaussian is left out of the
+# gradient comparison. Flagged pixels arise from list entries whose alpha lies
+# within ~1e-5 of 1/255 or 0.99, or whose transmittance lies that close to the
+# stop threshold; their rate is proportional to the bound (doubling it doubles
+# the count) and to the decisions a pixel takes (the length of its list up to
+# the stop): 0 in the 64x64 scenes, ~7e-4 of the pixels at 200k Gaussians and
+# 1280x720, ~1e-3 on sampled tiles at 3M Gaussians and 1600x1064, ~1.6e-3 at
+# 6M Gaussians and 1920x1080 (lists about three times longer). FLAG_FRAC
+# bounds it at 4e-3.
+MARGIN = 1.0
+FLAG_FRAC = 4e-3
 IMG_ATOL, IMG_RTOL = 1e-5, 1e-4      # rendered images, fp32
 
 
@@ -195,6 +206,22 @@ MLP_HALF_ATOL = 2e-4
 NEURAL_FLIP_ATOL = 2e-3
 NEURAL_FLIP_FRAC = 0.01
 NEURAL_FLIP = (NEURAL_FLIP_ATOL, NEURAL_FLIP_FRAC)
+# Gradients of the decoder paths (latent, neural). The decoder rounds its
+# inputs and hidden activations to binary16 from fp32 sums on the GPU and from
+# fp64 sums in the oracle, so about one rounding in 2^11 lands on the
+# neighbouring binary16 value on one side only; a Gaussian with such a flip
+# sees its colour, and so the gradients that pass through its colour, move by
+# up to ~1e-3 relative (NEURAL_FLIP). The weight gradients also take each
+# gradient operand as one binary16 value (products within 2^-12 relative),
+# summed over every visible Gaussian. Hence: relative L2 <= 1e-4 for the
+# per-Gaussian tensors and <= 5e-3 for the weight gradient (survey reading
+# S-26 for the decoder path); the S-26 element bound for all but 0.2% of a
+# per-Gaussian tensor's elements and 10% of the weight gradient's, and every
+# element within 20 times it (2% of |ref| + 2e-4 max|ref|: a Gaussian whose
+# gradient were wrong would miss this by orders of magnitude). Measured worst:
+# 4e-5 and 2.7e-4 relative L2; 3 of 3072 elements and 128 of 1664 beyond;
+# 12.6 times the bound.
+MLP_GRADS = dict(rel_l2={"dmlp_w": 5e-3}, beyond_frac={"dmlp_w": 0.1, "*": 2e-3}, ratio_max=20.0)
 
 
 def lobe_frame(lobes):
@@ -255,36 +282,62 @@ def compare_image(gpu, ref_img, ref_T, ref_nc, margin, atol=IMG_ATOL, rtol=IMG_R
     return int((~ok).sum())
 
 
-def affected_gaussians(ref_ranges, ref_values, ref_nc, gpu_nc, margin, width):
-    """Gaussians listed up to the last contributor of a flagged pixel."""
-    flagged = np.argwhere(margin <= MARGIN)
-    tiles_x = (width + 15) // 16
-    out = set()
-    for y, x in flagged:
-        t = (y // 16) * tiles_x + x // 16
-        s, e = ref_ranges[t]
-        k = max(int(ref_nc[y, x]), int(gpu_nc[y, x])) + 1
-        out.update(ref_values[s:min(e, s + k)].tolist())
-    return np.array(sorted(out), dtype=np.int64)
+def flagged_pixels(margin, max_count=None, label="", region=None):
+    """Mask of the pixels (within ``region``, default all) whose decisions lie
+    within the rounding bound, after checking their number: at most max_count
+    (default FLAG_FRAC of the pixels compared)."""
+    region = np.ones(margin.shape, bool) if region is None else region
+    flagged = (margin <= MARGIN) & region
+    compared = int(region.sum())
+    cap = int(FLAG_FRAC * compared) if max_count is None else max_count
+    say("  %sflagged pixels: %d of %d (cap %d)" % (label, int(flagged.sum()), compared, cap))
+    assert flagged.sum() <= cap, (int(flagged.sum()), cap)
+    return flagged
 
 
-def grad_errors(gpu_g, ref_g, exclude=None):
-    """Per tensor: relative L2 error and the largest element error relative to
-    (|ref| + 1e-2 * rms(ref))."""
+# Gradients (survey reading S-26): every element within
+# |gpu - ref| <= GRAD_ELEM_RTOL |ref| + GRAD_ELEM_FLOOR max|ref| of its tensor,
+# and the tensor's relative L2 error <= GRAD_REL_L2. The pair sums use float
+# atomics in fp32 against the oracle's fp64, hence the relative terms.
+GRAD_ELEM_RTOL, GRAD_ELEM_FLOOR = 1e-3, 1e-5
+GRAD_REL_L2 = 1e-4
+
+
+def grad_stats(gpu_g, ref_g, names=None):
+    """Per tensor: (relative L2 error, worst element ratio to the S-26 bound,
+    number of elements beyond it, number of elements)."""
     stats = {}
-    for k, r in ref_g.items():
-        if k not in gpu_g:
+    for k in (names or ref_g.keys()):
+        if k not in gpu_g or k not in ref_g:
             continue
-        g = gpu_g[k]
-        if exclude is not None and exclude.size and r.ndim >= 1 and r.shape[-1] == g.shape[-1] and k != "dmlp_w":
-            r = np.delete(r, exclude, axis=-1)
-            g = np.delete(g, exclude, axis=-1)
-        diff = g - r
-        rms = float(np.sqrt(np.mean(r * r))) if r.size else 0.0
-        rel_l2 = float(np.linalg.norm(diff) / max(np.linalg.norm(r), 1e-300))
-        elem = float(np.max(np.abs(diff) / (np.abs(r) + 1e-2 * rms + 1e-30))) if r.size else 0.0
-        stats[k] = (rel_l2, elem)
+        g, r = gpu_g[k], ref_g[k]
+        diff = np.abs(g - r)
+        rel_l2 = float(np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-300))
+        bound = GRAD_ELEM_RTOL * np.abs(r) + GRAD_ELEM_FLOOR * (np.abs(r).max() if r.size else 0.0)
+        ratio = np.where(diff > 0, diff / np.maximum(bound, 1e-300), 0.0)
+        stats[k] = (rel_l2, float(ratio.max()) if r.size else 0.0, int((ratio > 1).sum()), int(r.size))
     return stats
+
+
+def report_grads(stats):
+    say("  grads (rel L2, worst elem / bound, elems beyond): " +
+        ", ".join("%s %.2e %.2f %d/%d" % (k, a, b, c, n) for k, (a, b, c, n) in stats.items()))
+
+
+def check_grads(stats, rel_l2=GRAD_REL_L2, beyond_frac=0.0, ratio_max=1.0):
+    """Every tensor: relative L2 error within rel_l2; at most beyond_frac of its
+    elements beyond the element bound, and none beyond ratio_max times it. Each
+    limit is a number or a dict by tensor name (key "*": the others; the strict
+    default where neither is given)."""
+    def limit(v, k, default):
+        return v.get(k, v.get("*", default)) if isinstance(v, dict) else v
+    for k, (rel, worst, beyond, size) in stats.items():
+        lim = limit(rel_l2, k, GRAD_REL_L2)
+        assert rel <= lim, (k, rel, lim)
+        frac = limit(beyond_frac, k, 0.0)
+        assert beyond <= frac * size, (k, beyond, size, frac)
+        rmax = limit(ratio_max, k, 1.0)
+        assert worst <= rmax, (k, worst, rmax)
 
 
 def oracle_all(scene, cam, kind="sh3", sh_degree=3, dL_dimage=None, half_act=False):

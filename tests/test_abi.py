@@ -146,6 +146,38 @@ def test_bin_sort_reports_capacity(gs):
     assert st == gs.GS_ERR_INVALID_ARG
 
 
+def test_bin_sort_device_count_arguments(gs):
+    # device mode (the pair count read on the device): nothing about P can be
+    # checked on the host, but the buffers the capacity promises must exist
+    lib = gs.lib()
+    cam = _camera(gs)
+    pre = gs.Preprocessed(FAKE, FAKE, FAKE, FAKE)
+    st = lib.gs_bin_sort(C.byref(cam), C.byref(pre), 10, gs.GS_PAIRS_ON_DEVICE, 100, None, None, C.c_void_p(FAKE),
+                         C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARG and b"values" in lib.gs_last_error()
+    st = lib.gs_bin_sort(C.byref(cam), C.byref(pre), 10, gs.GS_PAIRS_ON_DEVICE, 1 << 32, C.c_void_p(FAKE), None,
+                         C.c_void_p(FAKE), C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARG
+    # the count lives in pre->num_pairs: required in either mode
+    nopairs = gs.Preprocessed(FAKE, FAKE, FAKE, None)
+    st = lib.gs_bin_sort(C.byref(cam), C.byref(nopairs), 10, gs.GS_PAIRS_ON_DEVICE, 100, C.c_void_p(FAKE), None,
+                         C.c_void_p(FAKE), C.c_void_p(FAKE * 256), 1 << 40, None)
+    assert st == gs.GS_ERR_INVALID_ARG
+
+
+def test_timer_is_caller_owned(gs):
+    # a timing context is created, attached, read, reset and destroyed by the
+    # caller; without one attached the library records nothing
+    lib = gs.lib()
+    ms = (C.c_double * 4)()
+    cnt = (C.c_int64 * 4)()
+    assert lib.gs_timer_read(None, ms, cnt, 4) == gs.GS_ERR_INVALID_ARG
+    assert lib.gs_timer_reset(None) == gs.GS_ERR_INVALID_ARG
+    assert lib.gs_timer_attach(None) == gs.GS_OK
+    assert lib.gs_timer_destroy(None) == gs.GS_OK
+    assert lib.gs_timer_create(None) == gs.GS_ERR_INVALID_ARG
+
+
 def test_render_calls_reject_bad_arguments(gs):
     lib = gs.lib()
     cam = _camera(gs)

@@ -3,9 +3,11 @@
 Bit-exact: culling, tiles touched, tile rectangles, depth keys, the projected
 means/conics/opacities (one correctly rounded fp32 operation sequence on both
 sides), the number of pairs, the sorted per-tile lists, tile ids and ranges.
-Images: abs 1e-5 + rel 1e-4 on pixels whose decisions are not within 1e-5
-(relative) of the skip/stop/cap thresholds; the rest are counted.
-Gradients: relative L2 error per tensor <= 1e-3 (pair sums use float atomics).
+Images: abs 1e-5 + rel 1e-4 on every pixel whose decisions lie outside the
+rounding bound of the oracle's margin; the others (flagged) are counted and
+bounded, and get a zero upstream gradient on both sides.
+Gradients (survey reading S-26): every element within 1e-3 |ref| + 1e-5 max|ref|
+and relative L2 <= 1e-4 per tensor; the decoder paths as stated in MLP_GRADS.
 """
 import numpy as np
 import pytest
@@ -16,56 +18,61 @@ import torch
 
 from oracle import oracle as orc
 from paper_2609_05255_amd import gsraster as gs
-from parity import (MLP_ATOL, MLP_HALF_ATOL, NEURAL_FLIP, lobe_color_atol, affected_gaussians, compare_image, compare_lists, compare_preprocess,
-                    grad_errors, oracle_all, run_gpu, say, tiny_camera)
+from parity import (MLP_ATOL, MLP_HALF_ATOL, MLP_GRADS, NEURAL_FLIP, check_grads, compare_image, compare_lists,
+                    compare_preprocess, flagged_pixels, grad_stats, lobe_color_atol, report_grads, run_gpu, say,
+                    tiny_camera)
 
 pytestmark = pytest.mark.gpu
 
-GRAD_REL_L2 = 1e-3
 
-
-def check_all(scene, cam, kind="sh3", sh_degree=3, label="", grads=True, capacity=None):
-    g = inputs.make_upstream_grad(cam.width, cam.height, 0) if grads else None
+def check_all(scene, cam, kind="sh3", sh_degree=3, label="", grads=True, capacity=None, max_flagged=None,
+              cam_seed=0):
     say("case %s: n=%d %dx%d %s degree %d" % (label, scene.n, cam.width, cam.height, kind, sh_degree))
-    gpu = run_gpu(scene, cam, kind, sh_degree, g, capacity=capacity)
     latent = kind in ("latent", "neural", "neural_folded")
     # the decoder's operands are binary16: compare with the oracle that rounds them alike
-    ref = oracle_all(scene, cam, kind, sh_degree, g, half_act=latent)
+    ref = orc.render(cam, scene, kind=kind, sh_degree=sh_degree, mode="f32", half_act=latent)
+    flagged = flagged_pixels(ref["margin"], max_flagged)
+    g = None
+    if grads:
+        g = (inputs.make_upstream_grad(cam.width, cam.height, cam_seed) * ~flagged[None]).astype(np.float32)
+        ref["grads"] = orc.render_bwd(cam, scene, ref["pre"], ref["ranges"], ref["values"], g, kind=kind,
+                                      sh_degree=sh_degree, mode="f32", half_act=latent)
+    gpu = run_gpu(scene, cam, kind, sh_degree, g, capacity=capacity)
     flip = NEURAL_FLIP if kind in ("neural", "neural_folded") else None
     atol = (MLP_HALF_ATOL if latent else
             lobe_color_atol(scene, cam, kind, ref["pre"]["color"], sh_degree) if kind in ("nasg", "nasgabor") else 2e-6)
     compare_preprocess(gpu, ref["pre"], color_atol=atol, flip=flip)
     compare_lists(gpu, ref["values"], ref["tile_of"], ref["ranges"])
     if latent:
-        flagged = compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"],
-                                atol=flip[0] if flip else MLP_HALF_ATOL, rtol=0.0)
+        compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"],
+                      atol=flip[0] if flip else MLP_HALF_ATOL, rtol=0.0)
         exact = orc.render(cam, scene, kind=kind, sh_degree=sh_degree, mode="f32")
-        err = np.abs(gpu["image"] - exact["image"])[:, exact["margin"] > 1e-5]
+        err = np.abs(gpu["image"] - exact["image"])[:, exact["margin"] > 1.0]
         say("  latent image vs the exact decoder: max abs %.2e" % (err.max() if err.size else 0.0))
         assert err.size == 0 or err.max() <= MLP_ATOL
     else:
-        flagged = compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"])
-    say("  P=%d flagged pixels=%d" % (gpu["P"], flagged))
+        compare_image(gpu, ref["image"], ref["final_T"], ref["n_contrib"], ref["margin"])
+    say("  P=%d" % gpu["P"])
     if grads:
-        excl = affected_gaussians(ref["ranges"], ref["values"], ref["n_contrib"], gpu["n_contrib"], ref["margin"],
-                                  cam.width)
-        st = grad_errors(gpu["grads"], ref["grads"], excl)
-        say("  grad errors (rel L2, max elem): " + ", ".join("%s %.2e %.2e" % (k, a, b) for k, (a, b) in st.items()))
-        for k, (rel, _) in st.items():
-            assert rel <= GRAD_REL_L2, (k, rel)
+        st = grad_stats(gpu["grads"], ref["grads"])
+        report_grads(st)
+        if kind in ("latent", "neural"):
+            check_grads(st, **MLP_GRADS)
+        else:
+            check_grads(st)
     return gpu, ref
 
 
 def test_tiny_scene():
     sc = inputs.make_scene("tiny")
     cam = inputs.make_cameras("tiny")[0]
-    check_all(sc, cam, label="tiny")
+    check_all(sc, cam, label="tiny", max_flagged=0)
 
 
 @pytest.mark.parametrize("degree", [0, 1, 2])
 def test_tiny_scene_lower_sh_degrees(degree):
     sc = inputs.make_scene("tiny")
-    check_all(sc, inputs.make_cameras("tiny")[0], sh_degree=degree, label="tiny")
+    check_all(sc, inputs.make_cameras("tiny")[0], sh_degree=degree, label="tiny", max_flagged=0)
 
 
 def test_ragged_image_with_background():
@@ -106,11 +113,11 @@ def test_empty_and_culled_scenes():
         assert np.all(v == 0), k
 
 
-def test_medium_scene_two_cameras():
+@pytest.mark.parametrize("cam_index", range(8))
+def test_medium_scene(cam_index):
+    # every camera of the medium workload (200k Gaussians, 1280x720)
     sc = inputs.make_scene("medium")
-    cams = inputs.make_cameras("medium")
-    for i in (0, 5):
-        check_all(sc, cams[i], label="medium cam %d" % i)
+    check_all(sc, inputs.make_cameras("medium")[cam_index], label="medium cam %d" % cam_index, cam_seed=cam_index)
 
 
 def test_mlp_eval_matches_oracle():
@@ -138,7 +145,7 @@ def test_mlp_eval_matches_oracle():
 
 def test_tiny_scene_latent():
     sc = inputs.make_scene("tiny", appearance=("latent",))
-    check_all(sc, inputs.make_cameras("tiny")[0], kind="latent", label="tiny latent")
+    check_all(sc, inputs.make_cameras("tiny")[0], kind="latent", label="tiny latent", max_flagged=0)
 
 
 def test_ragged_latent_with_background():
@@ -146,16 +153,18 @@ def test_ragged_latent_with_background():
     check_all(sc, tiny_camera(50, 37, bg=(0.25, 0.5, 0.75)), kind="latent", label="ragged latent")
 
 
-def test_medium_scene_latent():
+@pytest.mark.parametrize("cam_index", [2, 6])
+def test_medium_scene_latent(cam_index):
     sc = inputs.make_scene("medium", appearance=("latent",))
-    check_all(sc, inputs.make_cameras("medium")[2], kind="latent", label="medium latent cam 2")
+    check_all(sc, inputs.make_cameras("medium")[cam_index], kind="latent", label="medium latent cam %d" % cam_index,
+              cam_seed=cam_index)
 
 
 @pytest.mark.parametrize("degree", [0, 1, 2, 3])
 def test_tiny_scene_neural(degree):
     # the paper's neural appearance; degree 0 has the residual off
     sc = inputs.make_scene("tiny", appearance=("neural",))
-    check_all(sc, tiny_camera(), kind="neural", sh_degree=degree, label="tiny-neural")
+    check_all(sc, tiny_camera(), kind="neural", sh_degree=degree, label="tiny-neural", max_flagged=0)
 
 
 def test_ragged_neural_with_background():
@@ -340,3 +349,54 @@ def test_degenerate_gaussians(kind):
         sc.features, sc.neural_w, sc.lobes, sc.lobes_gabor = (extra.features, extra.neural_w, extra.lobes,
                                                               extra.lobes_gabor)
     check_all(sc, cam, kind=kind, label="degenerate-" + kind)
+
+
+# ---- the pair count read on the device -------------------------------------------
+
+@pytest.mark.parametrize("size", [(64, 64), (16, 16)])
+def test_device_pair_count(size):
+    # gs_bin_sort in device mode (no read-back of P): the same lists, ranges and
+    # image as the host mode; with a capacity below P nothing is listed, every
+    # range is empty, the image is the background, the gradients are zero, and
+    # pre->num_pairs keeps the P needed for the retry
+    sc = inputs.make_scene("tiny")
+    cam = tiny_camera(*size, bg=(0.2, 0.4, 0.6))
+    say("case device pair count %dx%d" % size)
+    cs = gs.camera_struct(cam)
+    st = gs.SceneTensors(sc)
+    g = torch.from_numpy(inputs.make_upstream_grad(cam.width, cam.height, 0)).cuda()
+    host = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_SH3, 1 << 14, want_tile_ids=True)
+    P = host.forward(cs, st)
+    dev = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_SH3, 1 << 14, want_tile_ids=True)
+    assert dev.forward(cs, st, sync_pairs=False) is None
+    torch.cuda.synchronize()
+    assert int(dev.num_pairs.item()) == P and not dev.pairs_overflowed()
+    for k in ("values", "tile_ids"):
+        assert torch.equal(getattr(dev, k)[:P], getattr(host, k)[:P]), k
+    for k in ("ranges", "image", "final_T", "n_contrib"):
+        assert torch.equal(getattr(dev, k), getattr(host, k)), k
+    host.backward(cs, st, g)
+    dev.backward(cs, st, g)
+    torch.cuda.synchronize()
+    for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh"):
+        a, b = getattr(dev, k).double(), getattr(host, k).double()
+        assert torch.allclose(a, b, rtol=1e-5, atol=1e-12 + 1e-6 * float(b.abs().max())), k
+    # overflow found on the device
+    small = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_SH3, P // 3)
+    small.forward(cs, st, sync_pairs=False)
+    torch.cuda.synchronize()
+    assert small.pairs_overflowed() and int(small.num_pairs.item()) == P
+    assert int(small.ranges.abs().sum().item()) == 0
+    bg = torch.tensor([0.2, 0.4, 0.6], device="cuda").view(3, 1, 1).expand_as(small.image)
+    assert torch.equal(small.image, bg.float())
+    assert bool((small.final_T == 1).all()) and int(small.n_contrib.sum().item()) == 0
+    small.backward(cs, st, g)
+    torch.cuda.synchronize()
+    for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh"):
+        assert int(torch.count_nonzero(getattr(small, k)[..., : sc.n]).item()) == 0, k
+    # retry with room for every pair
+    retry = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_SH3, P, want_tile_ids=True)
+    retry.forward(cs, st, sync_pairs=False)
+    torch.cuda.synchronize()
+    assert not retry.pairs_overflowed()
+    assert torch.equal(retry.values[:P], host.values[:P]) and torch.equal(retry.image, host.image)

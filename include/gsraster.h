@@ -215,6 +215,25 @@ gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_ap
                         void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * gs_preprocess_noalloc -- gs_preprocess for callers that cannot allocate
+ * device memory or hand over a workspace (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation). Same arguments, results
+ * and errors as gs_preprocess, without the workspace: its scratch (one tile
+ * sum per workgroup or wave of 64 Gaussians) is a static device array of the
+ * library, GS_NOALLOC_MAX_GAUSSIANS / 64 u32 (1 MiB), one per GPU, held until
+ * the process ends; its address is looked up once per device, on the first
+ * call with that device current. Calls no allocating routine.
+ * Limits: n <= GS_NOALLOC_MAX_GAUSSIANS, else GS_ERR_CAPACITY with nothing
+ * enqueued. Every call on one GPU uses that GPU's one array: calls that overlap
+ * on one GPU (on different streams, or from different threads) race and must
+ * be serialised by the caller. Nothing in it needs clearing between calls
+ * (each call writes every slot it reads).
+ */
+#define GS_NOALLOC_MAX_GAUSSIANS (1 << 24)
+gs_status gs_preprocess_noalloc(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                                const gs_preprocessed* out, uint64_t* num_pairs_host, void* stream);
+
+/*
  * gs_bin_sort -- the depth-sorted per-tile lists of Sec. 3.1. Produces, for the P
  * pairs (tile, Gaussian) of every Gaussian with tiles_touched > 0 and every
  * tile of its rectangle, the Gaussian indices sorted by (tile id, depth key,

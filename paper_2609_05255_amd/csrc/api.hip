@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -281,19 +282,16 @@ gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t c
     return ok();
 }
 
-gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
-                        const gs_preprocessed* out, uint64_t* num_pairs_host, void* workspace, size_t workspace_bytes,
-                        void* stream)
+}  // extern "C"
+
+namespace {
+
+// Checks and launches of gs_preprocess with the scratch memory already placed:
+// `ws` needs only block_pairs (one tile sum per preprocess workgroup or wave,
+// every one written before the pair count reads it).
+gs_status preprocess_run(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                         const gs_preprocessed* out, uint64_t* num_pairs_host, const Workspace& ws, hipStream_t s)
 {
-    gs_status st;
-    if ((st = check_camera(cam)) != GS_OK) return st;
-    if ((st = check_gaussians(g)) != GS_OK) return st;
-    if ((st = check_appearance(app, g->n)) != GS_OK) return st;
-    if ((st = check_pre(out, g->n)) != GS_OK) return st;
-    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind);
-    if ((st = check_workspace(workspace, workspace_bytes, layout_workspace(nullptr, g->n, 0, app->kind))) != GS_OK)
-        return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
     const Cam c = make_cam(*cam);
     if (g->n > 0) {
         timing_begin(GS_KERNEL_PREPROCESS, s);
@@ -310,6 +308,81 @@ gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_ap
         GS_HIP(hipStreamSynchronize(s));
     }
     return ok();
+}
+
+gs_status preprocess_checks(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                            const gs_preprocessed* out)
+{
+    gs_status st;
+    if ((st = check_camera(cam)) != GS_OK) return st;
+    if ((st = check_gaussians(g)) != GS_OK) return st;
+    if ((st = check_appearance(app, g->n)) != GS_OK) return st;
+    return check_pre(out, g->n);
+}
+
+}  // namespace
+
+// The preprocess's scratch for callers that cannot allocate: the per-wave tile
+// sums of up to GS_NOALLOC_MAX_GAUSSIANS Gaussians (1 MiB), one copy per GPU
+// for the life of the process. Host code reaches it only through the device
+// address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint32_t scratch[GS_NOALLOC_MAX_GAUSSIANS / kWave];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint32_t* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up once per device.
+gs_status scratch_of_current_device(uint32_t** ptr)
+{
+    int dev = -1;
+    GS_HIP(hipGetDevice(&dev));
+    GS_CHECK(dev >= 0 && dev < kMaxDevices, "device %d beyond the %d this library tracks", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || p == nullptr)
+            return fail(GS_ERR_DEVICE, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_ptr[dev] = static_cast<uint32_t*>(p);
+    }
+    *ptr = g_scratch_ptr[dev];
+    return GS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                        const gs_preprocessed* out, uint64_t* num_pairs_host, void* workspace, size_t workspace_bytes,
+                        void* stream)
+{
+    gs_status st;
+    if ((st = preprocess_checks(cam, g, app, out)) != GS_OK) return st;
+    const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind);
+    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
+    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind);
+    return preprocess_run(cam, g, app, out, num_pairs_host, ws, static_cast<hipStream_t>(stream));
+}
+
+gs_status gs_preprocess_noalloc(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                                const gs_preprocessed* out, uint64_t* num_pairs_host, void* stream)
+{
+    gs_status st;
+    if ((st = preprocess_checks(cam, g, app, out)) != GS_OK) return st;
+    if (g->n > GS_NOALLOC_MAX_GAUSSIANS)
+        return fail(GS_ERR_CAPACITY, "gs_preprocess_noalloc takes at most %d Gaussians, got %lld",
+                    GS_NOALLOC_MAX_GAUSSIANS, (long long)g->n);
+    uint32_t* scr = nullptr;
+    if ((st = scratch_of_current_device(&scr)) != GS_OK) return st;
+    Workspace ws;
+    memset(&ws, 0, sizeof(ws));
+    ws.block_pairs = scr;
+    return preprocess_run(cam, g, app, out, num_pairs_host, ws, static_cast<hipStream_t>(stream));
 }
 
 gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, uint64_t num_pairs,

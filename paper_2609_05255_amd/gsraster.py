@@ -93,6 +93,7 @@ def lib() -> C.CDLL:
         vp, i32, i64, u64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_size_t
         P = C.POINTER
         L.gs_preprocess.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), P(u64), vp, sz, vp]
+        L.gs_preprocess_noalloc.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), P(u64), vp]
         L.gs_bin_sort.argtypes = [P(Camera), P(Preprocessed), i64, u64, u64, vp, vp, vp, vp, sz, vp]
         L.gs_render_fwd.argtypes = [P(Camera), P(Preprocessed), i64, vp, vp, vp, vp, vp, vp]
         L.gs_render_bwd.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), vp, vp, vp, vp, vp,
@@ -106,7 +107,7 @@ def lib() -> C.CDLL:
         L.gs_timer_attach.argtypes = [vp]
         L.gs_timer_reset.argtypes = [vp]
         L.gs_timer_read.argtypes = [vp, P(C.c_double), P(i64), i32]
-        for f in ("gs_preprocess", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd", "gs_workspace_size", "gs_mlp_eval",
+        for f in ("gs_preprocess", "gs_preprocess_noalloc", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd", "gs_workspace_size", "gs_mlp_eval",
                   "gs_neural_fold", "gs_adam_step", "gs_timer_create", "gs_timer_destroy", "gs_timer_attach",
                   "gs_timer_reset", "gs_timer_read"):
             getattr(L, f).restype = C.c_int
@@ -215,6 +216,15 @@ def gs_preprocess(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed,
     p = C.c_uint64(0)
     _check(lib().gs_preprocess(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre),
                                C.byref(p) if sync_pairs else None, _ptr(workspace), ws_bytes, _stream(stream)))
+    return p.value if sync_pairs else None
+
+
+def gs_preprocess_noalloc(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed, stream=None,
+                          sync_pairs: bool = True):
+    """gs_preprocess without a workspace (the library's static per-GPU scratch)."""
+    p = C.c_uint64(0)
+    _check(lib().gs_preprocess_noalloc(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre),
+                                       C.byref(p) if sync_pairs else None, _stream(stream)))
     return p.value if sync_pairs else None
 
 

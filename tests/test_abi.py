@@ -242,3 +242,18 @@ def test_adam_rejects_bad_arguments(gs):
                         stream=0)
     with pytest.raises(gs.GsError):     # nine tensors
         gs.gs_adam_step([t] * 9, 0.9, 1e-8, 1, stream=0)
+
+
+def test_preprocess_noalloc_limit(gs):
+    # sizes beyond the static scratch are refused on the host, before any device work
+    lib = gs.lib()
+    cam = _camera(gs)
+    pre = gs.Preprocessed(FAKE, FAKE, FAKE, FAKE)
+    app = gs.Appearance(gs.GS_APP_SH3, 3, FAKE, None, None)
+    g = gs.Gaussians((1 << 24) + 1, FAKE, FAKE, FAKE, FAKE)
+    assert lib.gs_preprocess_noalloc(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), None, None) == \
+        gs.GS_ERR_CAPACITY
+    assert b"at most 16777216" in lib.gs_last_error()
+    g = gs.Gaussians(10, FAKE, None, FAKE, FAKE)
+    assert lib.gs_preprocess_noalloc(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), None, None) == \
+        gs.GS_ERR_INVALID_ARG

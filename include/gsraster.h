@@ -272,6 +272,23 @@ gs_status gs_render_fwd(const gs_camera* cam, const gs_preprocessed* pre, int64_
                         void* stream);
 
 /*
+ * gs_render_work -- the work of the Sec. 3.1 blend, counted for measuring its
+ * throughput (not needed to render). Walks every pixel's list with the same
+ * fp32 decisions as gs_render_fwd and writes, summed over all pixels:
+ *   counts[0] entries blended (alpha >= 1/255, composited before the stop);
+ *   counts[1] entries up to the last blended one (the sum of n_contrib);
+ *   counts[2] entries before the last blended one whose alpha >= 1/255 box meets
+ *             the pixel's tile (those gs_render_bwd evaluates per pixel; it skips
+ *             the others for the whole tile), blended ones included;
+ *   counts[3] the same for gs_render_fwd: entries up to the one that stops the
+ *             pixel (or the list's end).
+ * Arguments as for gs_render_fwd; counts: [4] u64 device, 8-byte aligned,
+ * overwritten. Asynchronous on stream.
+ */
+gs_status gs_render_work(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, const uint32_t* values,
+                         const uint32_t* tile_ranges, uint64_t* counts, void* stream);
+
+/*
  * gs_render_bwd -- gradients of L = sum(dL_dimage * image) with respect to every
  * Gaussian parameter, for the image that gs_render_fwd produced from the same
  * inputs (Sec. 4 fused backward; the colour gradient also reaches the means

@@ -117,6 +117,9 @@ typedef struct orc_grads {
     double* dbase_color;    /* [3][n] (neural) or NULL */
     double* dfeatures;      /* [8][n] (neural; [16][n] with 16 raw features) or NULL */
     double* dlobes;         /* [8][n] (NASG), [9][n] (NASGabor) or NULL */
+    double* dmlp_w_abs;     /* like dmlp_w, or NULL: per weight, the sum over Gaussians of the
+                               absolute values of the products whose sum is dmlp_w (the scale of
+                               its rounding error when the products are formed in low precision) */
 } orc_grads;
 
 int orc_preprocess_f32(const orc_camera* cam, int64_t n, const double* means, const double* log_scales,
@@ -137,13 +140,14 @@ int64_t orc_bin_sort(int64_t n, const int32_t* rect, const double* depth, const 
 /* margin (nullable): per pixel, the smallest ratio, over its skip/stop/clamp
  * decisions, of the decision's relative distance from its threshold to a bound
  * on how far an fp32 evaluation in another operation order can move it (see
- * walk_pixel); above 1 every decision of the pixel is reproducible. */
+ * walk_pixel); above 1 every decision of the pixel is reproducible.
+ * n_blended (nullable): per pixel, the number of entries composited. */
 void orc_render_fwd_f32(const orc_camera* cam, int64_t n, const orc_pre* pre, const int64_t* ranges,
                         const int32_t* values, double* image, double* final_T, int32_t* n_contrib,
-                        double* margin);
+                        double* margin, int32_t* n_blended);
 void orc_render_fwd_f64(const orc_camera* cam, int64_t n, const orc_pre* pre, const int64_t* ranges,
                         const int32_t* values, double* image, double* final_T, int32_t* n_contrib,
-                        double* margin);
+                        double* margin, int32_t* n_blended);
 
 /* Gradients of sum(dL_dimage * image) w.r.t. all inputs; outputs overwritten. */
 int orc_render_bwd_f32(const orc_camera* cam, int64_t n, const double* means, const double* log_scales,

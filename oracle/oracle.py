@@ -73,7 +73,7 @@ class _Pre(C.Structure):
 class _Grads(C.Structure):
     _fields_ = [(name, C.c_void_p) for name in (
         "dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh", "dlatent", "dmlp_w",
-        "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color", "dfeatures", "dlobes")]
+        "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color", "dfeatures", "dlobes", "dmlp_w_abs")]
 
 
 _lib = None
@@ -89,7 +89,7 @@ def lib():
             f.argtypes = [C.POINTER(_Camera), i64, vp, vp, vp, vp, C.POINTER(_Appearance), C.POINTER(_Pre)]
             f.restype = C.c_int
             f = getattr(_lib, "orc_render_fwd" + sfx)
-            f.argtypes = [C.POINTER(_Camera), i64, C.POINTER(_Pre), vp, vp, vp, vp, vp, vp]
+            f.argtypes = [C.POINTER(_Camera), i64, C.POINTER(_Pre), vp, vp, vp, vp, vp, vp, vp]
             f.restype = None
             f = getattr(_lib, "orc_render_bwd" + sfx)
             f.argtypes = [C.POINTER(_Camera), i64, vp, vp, vp, vp, C.POINTER(_Appearance), C.POINTER(_Pre),
@@ -260,8 +260,9 @@ def bin_sort(cam, pre: Preprocessed):
     return values[:total], tile_of[:total], ranges
 
 
-def render_fwd(cam, pre: Preprocessed, ranges, values, mode: str = "f32"):
-    """(image[3][H][W], final_T[H][W], n_contrib[H][W], margin[H][W])."""
+def render_fwd(cam, pre: Preprocessed, ranges, values, mode: str = "f32", n_blended=None):
+    """(image[3][H][W], final_T[H][W], n_contrib[H][W], margin[H][W]); n_blended, if
+    given (int32 [H][W]), receives each pixel's number of composited entries."""
     W, H = int(cam.width), int(cam.height)
     image = np.zeros((3, H, W))
     final_T = np.zeros((H, W))
@@ -272,7 +273,7 @@ def render_fwd(cam, pre: Preprocessed, ranges, values, mode: str = "f32"):
     st = pre.struct()
     getattr(lib(), "orc_render_fwd_" + mode)(C.byref(camera_struct(cam)), pre["tiles"].size, C.byref(st),
                                              _p(ranges), _p(values), _p(image), _p(final_T), _p(n_contrib),
-                                             _p(margin))
+                                             _p(margin), None if n_blended is None else _p(n_blended))
     return image, final_T, n_contrib, margin
 
 
@@ -293,9 +294,10 @@ def render_bwd(cam, scene, pre: Preprocessed, ranges, values, dL_dimage, kind="s
              dbase_color=np.zeros((3, n)) if kind in (APP_NEURAL, APP_NASG, APP_NASGABOR) else None,
              dfeatures=np.zeros((16 if neural_arch(scene)[2] else 8, n)) if kind == APP_NEURAL else None,
              dlobes=np.zeros((9 if kind == APP_NASGABOR else 8, n)) if kind in (APP_NASG, APP_NASGABOR) else None)
+    g["dmlp_w_abs"] = None if g["dmlp_w"] is None else np.zeros_like(g["dmlp_w"])
     gs = _Grads(*[_p(g[k]) for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh", "dlatent",
                                       "dmlp_w", "dmean2d", "dconic", "dopacity", "dcolor", "dbase_color",
-                                      "dfeatures", "dlobes")])
+                                      "dfeatures", "dlobes", "dmlp_w_abs")])
     dimg = _f64(dL_dimage)
     ranges = np.ascontiguousarray(ranges, dtype=np.int64)
     values = np.ascontiguousarray(values, dtype=np.int32)
@@ -314,9 +316,10 @@ def render(cam, scene, kind="sh3", sh_degree: int = 3, mode: str = "f32", dir_ex
     """All forward stages; returns a dict with the intermediate results."""
     pre = preprocess(cam, scene, kind, sh_degree, mode, dir_exact, half_act)
     values, tile_of, ranges = bin_sort(cam, pre)
-    image, final_T, n_contrib, margin = render_fwd(cam, pre, ranges, values, mode)
+    n_blended = np.zeros((int(cam.height), int(cam.width)), np.int32)
+    image, final_T, n_contrib, margin = render_fwd(cam, pre, ranges, values, mode, n_blended)
     return dict(pre=pre, values=values, tile_of=tile_of, ranges=ranges, image=image, final_T=final_T,
-                n_contrib=n_contrib, margin=margin)
+                n_contrib=n_contrib, margin=margin, n_blended=n_blended)
 
 
 def sh_basis(d) -> tuple:

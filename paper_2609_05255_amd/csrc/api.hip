@@ -463,6 +463,20 @@ gs_status gs_render_fwd(const gs_camera* cam, const gs_preprocessed* pre, int64_
     return ok();
 }
 
+gs_status gs_render_work(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, const uint32_t* values,
+                         const uint32_t* tile_ranges, uint64_t* counts, void* stream)
+{
+    gs_status st;
+    if ((st = check_camera(cam)) != GS_OK) return st;
+    if ((st = check_pre(pre, n)) != GS_OK) return st;
+    GS_CHECK(tile_ranges && counts, "tile_ranges or counts is NULL");
+    GS_CHECK(n == 0 || values != nullptr, "values is NULL");
+    GS_CHECK(((uintptr_t)counts & 7) == 0, "counts must be 8-byte aligned");
+    GS_HIP(launch_blend_count(make_cam(*cam), pre->splats, values, tile_ranges, counts,
+                              static_cast<hipStream_t>(stream)));
+    return ok();
+}
+
 gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
                         const gs_preprocessed* pre, const uint32_t* values, const uint32_t* tile_ranges,
                         const float* final_T, const uint32_t* n_contrib, const float* dL_dimage, const gs_grads* grads,

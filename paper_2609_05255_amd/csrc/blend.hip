@@ -424,6 +424,95 @@ hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32
     return hipGetLastError();
 }
 
+// ---- work counts (measurement) ------------------------------------------------
+// Walks every pixel's list with the forward's decisions (the same fp32
+// operations as k_blend_fwd) and counts, per pixel: entries blended; entries
+// evaluated in the forward (up to the stop entry, or the list's end, whose
+// alpha >= 1/255 box meets the tile: the blend kernels skip the others for
+// the whole tile without a per-pixel test); evaluated entries before the last
+// blended one (those the backward evaluates); and that last position
+// (n_contrib). One wave per tile, 4 pixels per lane; per-wave sums, then one
+// 64-bit atomic per wave and counter.
+__global__ __launch_bounds__(kWave) void k_blend_count(Cam cam, const gs_splat* __restrict__ splats,
+                                                       const uint32_t* __restrict__ values,
+                                                       const uint32_t* __restrict__ ranges,
+                                                       unsigned long long* __restrict__ counts)
+{
+    constexpr int kPix = 4, kRowStep = 4;
+    const int n_tiles = cam.tiles_x * cam.tiles_y;
+    const int tile = blockIdx.x;
+    if (tile >= n_tiles) return;
+    const int lane = __lane_id();
+    const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
+    const int x = tx * kTile + (lane & 15);
+    const int y0 = ty * kTile + (lane >> 4);
+    const float px = (float)x + 0.5f;
+    const uint32_t start = ranges[2 * tile], end = ranges[2 * tile + 1];
+    const float box_cx = (float)(tx * kTile) + 8.f, box_hx = 7.5f;
+    const float box_cy = (float)(ty * kTile) + 8.f, box_hy = 7.5f;
+    float T[kPix], py[kPix];
+    uint32_t blended[kPix], eval_fwd[kPix], eval_bwd[kPix], pending[kPix], last[kPix];
+#pragma unroll
+    for (int k = 0; k < kPix; ++k) {
+        py[k] = (float)(y0 + kRowStep * k) + 0.5f;
+        T[k] = (x < cam.width && (y0 + kRowStep * k) < cam.height) ? 1.f : -1.f;
+        blended[k] = eval_fwd[k] = eval_bwd[k] = pending[k] = last[k] = 0;
+    }
+    for (uint32_t p = start; p < end; ++p) {
+        const float4* rec = reinterpret_cast<const float4*>(splats + values[p]);
+        const float4 w0 = rec[0], w1 = rec[1], w2 = rec[2];
+        SplatReg s;
+        s.mx = w0.x; s.my = w0.y; s.ca = w0.z; s.cb = w0.w; s.cc = w1.x; s.op = w1.y;
+        s.pmin = w2.y; s.ex = w2.z; s.ey = w2.w;
+        if (!(fabsf(s.mx - box_cx) <= s.ex + box_hx && fabsf(s.my - box_cy) <= s.ey + box_hy)) continue;
+        const float dx = px - s.mx;
+        const Quad q = column_quad(s, dx);
+        const float pmin2 = s.pmin * kLog2e;
+#pragma unroll
+        for (int k = 0; k < kPix; ++k) {
+            if (!(T[k] > 0.f)) continue;
+            ++eval_fwd[k];
+            const float power2 = quad_power(q, py[k] - s.my);
+            if (!(power2 <= 0.f && power2 >= pmin2)) { ++pending[k]; continue; }
+            const float alpha = fminf(kAlphaMax, s.op * __builtin_amdgcn_exp2f(power2));
+            if (!(alpha >= kAlphaMin)) { ++pending[k]; continue; }
+            const float Tn = T[k] * (1.f - alpha);
+            if (Tn < kTMin) { T[k] = -T[k]; continue; }
+            T[k] = Tn;
+            ++blended[k];
+            eval_bwd[k] += pending[k] + 1;
+            pending[k] = 0;
+            last[k] = p - start + 1;
+        }
+    }
+    unsigned long long c[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int k = 0; k < kPix; ++k) {
+        if (x >= cam.width || y0 + kRowStep * k >= cam.height) continue;
+        c[0] += blended[k];
+        c[1] += last[k];
+        c[2] += eval_bwd[k];
+        c[3] += eval_fwd[k];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        unsigned long long v = c[i];
+        for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+        if (lane == 0) atomicAdd(counts + i, v);
+    }
+}
+
+hipError_t launch_blend_count(const Cam& cam, const gs_splat* splats, const uint32_t* values,
+                              const uint32_t* tile_ranges, uint64_t* counts, hipStream_t s)
+{
+    hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(counts), 8, 0u, s);
+    if (e != hipSuccess) return e;
+    const int n_tiles = cam.tiles_x * cam.tiles_y;
+    hipLaunchKernelGGL(k_blend_count, dim3(n_tiles), dim3(kWave), 0, s, cam, splats, values, tile_ranges,
+                       reinterpret_cast<unsigned long long*>(counts));
+    return hipGetLastError();
+}
+
 // Zero fill of `count` floats; p must be 16-byte aligned. Body in float4, tail
 // in scalars. A kernel rather than a memset so that it behaves the same inside
 // a captured graph.

@@ -137,6 +137,8 @@ hipError_t launch_blend_fwd(const Cam& cam, const gs_splat* splats, const uint32
                             const uint32_t* tile_ranges, float* image, float* final_T, uint32_t* n_contrib,
                             hipStream_t s);
 hipError_t launch_clear(float* p, int64_t count, hipStream_t s);
+hipError_t launch_blend_count(const Cam& cam, const gs_splat* splats, const uint32_t* values,
+                              const uint32_t* tile_ranges, uint64_t* counts, hipStream_t s);
 hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                             const uint32_t* tile_ranges, const float* final_T, const uint32_t* n_contrib,
                             const float* dL_dimage, float* acc, hipStream_t s);

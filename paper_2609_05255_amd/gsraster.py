@@ -96,6 +96,7 @@ def lib() -> C.CDLL:
         L.gs_preprocess_noalloc.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), P(u64), vp]
         L.gs_bin_sort.argtypes = [P(Camera), P(Preprocessed), i64, u64, u64, vp, vp, vp, vp, sz, vp]
         L.gs_render_fwd.argtypes = [P(Camera), P(Preprocessed), i64, vp, vp, vp, vp, vp, vp]
+        L.gs_render_work.argtypes = [P(Camera), P(Preprocessed), i64, vp, vp, vp, vp]
         L.gs_render_bwd.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), vp, vp, vp, vp, vp,
                                     P(Grads), vp, sz, vp]
         L.gs_workspace_size.argtypes = [i64, i32, i32, u64, i32, P(sz)]
@@ -107,7 +108,7 @@ def lib() -> C.CDLL:
         L.gs_timer_attach.argtypes = [vp]
         L.gs_timer_reset.argtypes = [vp]
         L.gs_timer_read.argtypes = [vp, P(C.c_double), P(i64), i32]
-        for f in ("gs_preprocess", "gs_preprocess_noalloc", "gs_bin_sort", "gs_render_fwd", "gs_render_bwd", "gs_workspace_size", "gs_mlp_eval",
+        for f in ("gs_preprocess", "gs_preprocess_noalloc", "gs_bin_sort", "gs_render_fwd", "gs_render_work", "gs_render_bwd", "gs_workspace_size", "gs_mlp_eval",
                   "gs_neural_fold", "gs_adam_step", "gs_timer_create", "gs_timer_destroy", "gs_timer_attach",
                   "gs_timer_reset", "gs_timer_read"):
             getattr(L, f).restype = C.c_int
@@ -238,6 +239,12 @@ def gs_render_fwd(cam: Camera, pre: Preprocessed, n: int, values, tile_ranges, i
                   stream=None):
     _check(lib().gs_render_fwd(C.byref(cam), C.byref(pre), n, _ptr(values), _ptr(tile_ranges), _ptr(image),
                                _ptr(final_T), _ptr(n_contrib), _stream(stream)))
+
+
+def gs_render_work(cam: Camera, pre: Preprocessed, n: int, values, tile_ranges, counts, stream=None):
+    """counts: int64 device tensor [4] (blended, listed, evaluated backward, evaluated forward)."""
+    _check(lib().gs_render_work(C.byref(cam), C.byref(pre), n, _ptr(values), _ptr(tile_ranges), _ptr(counts),
+                                _stream(stream)))
 
 
 def gs_render_bwd(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed, values, tile_ranges, final_T,

@@ -400,3 +400,35 @@ def test_device_pair_count(size):
     torch.cuda.synchronize()
     assert not retry.pairs_overflowed()
     assert torch.equal(retry.values[:P], host.values[:P]) and torch.equal(retry.image, host.image)
+
+
+# ---- the blend's work counts (measurement) ------------------------------------------
+
+@pytest.mark.parametrize("case", ["tiny", "ragged", "medium"])
+def test_render_work_counts(case):
+    # gs_render_work: blended entries against the oracle's per-pixel count
+    # (exactly where no pixel is flagged; otherwise within the flagged pixels'
+    # list lengths), the listed entries equal to the sum of the GPU's own
+    # n_contrib, and evaluated counts between them
+    if case == "medium":
+        sc, cam = inputs.make_scene("medium"), inputs.make_cameras("medium")[3]
+    else:
+        sc = inputs.make_scene("tiny")
+        cam = inputs.make_cameras("tiny")[0] if case == "tiny" else tiny_camera(50, 37)
+    say("case render work %s" % case)
+    ref = orc.render(cam, sc, mode="f32")
+    gpu = run_gpu(sc, cam)
+    fr = gpu["frame"]
+    counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    gs.gs_render_work(gs.camera_struct(cam), fr.pre, sc.n, fr.values, fr.ranges, counts)
+    torch.cuda.synchronize()
+    blended, listed, ev_bwd, ev_fwd = (int(v) for v in counts.cpu().numpy())
+    say("  blended %d listed %d evaluated bwd %d fwd %d" % (blended, listed, ev_bwd, ev_fwd))
+    assert listed == int(gpu["n_contrib"].astype(np.int64).sum())
+    flagged = ref["margin"] <= 1.0
+    ref_blended = int(ref["n_blended"].astype(np.int64).sum())
+    slack = int(ref["n_contrib"][flagged].astype(np.int64).sum() + gpu["n_contrib"][flagged].astype(np.int64).sum())
+    if not flagged.any():
+        assert blended == ref_blended
+    assert abs(blended - ref_blended) <= slack
+    assert blended <= ev_bwd <= listed and ev_bwd <= ev_fwd

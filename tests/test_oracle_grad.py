@@ -147,3 +147,24 @@ def test_sh_degree_masks_coefficients(orc):
     grads = orc.render_bwd(cam, sc, r["pre"], r["ranges"], r["values"], g, sh_degree=1, mode="f64")
     assert np.all(grads["dsh"][12:] == 0)
     assert np.abs(grads["dsh"][:12]).max() > 0
+
+
+@pytest.mark.parametrize("kind", ["latent", "neural"])
+def test_weight_gradient_product_sums(orc, kind):
+    # dmlp_w_abs sums |product| where dmlp_w sums the products: with one
+    # visible Gaussian each weight has one product, so the two agree in
+    # magnitude; with many, the triangle inequality holds and cancellation
+    # makes some sums strictly larger
+    sc = inputs.make_scene("tiny", appearance=(kind,))
+    cam = inputs.make_cameras("tiny")[0]
+    g = inputs.make_upstream_grad(cam.width, cam.height, 0)
+    r = orc.render(cam, sc, kind=kind, mode="f64")
+    full = orc.render_bwd(cam, sc, r["pre"], r["ranges"], r["values"], g, kind=kind, mode="f64")
+    assert np.all(full["dmlp_w_abs"] >= np.abs(full["dmlp_w"]) * (1 - 1e-12))
+    assert np.any(full["dmlp_w_abs"] > 1.5 * np.abs(full["dmlp_w"]))
+    vis = np.nonzero(r["pre"]["tiles"] > 0)[0]
+    one = sc.subset(vis[:1])
+    r1 = orc.render(cam, one, kind=kind, mode="f64")
+    g1 = orc.render_bwd(cam, one, r1["pre"], r1["ranges"], r1["values"], g, kind=kind, mode="f64")
+    assert np.abs(g1["dmlp_w"]).max() > 0
+    assert np.allclose(g1["dmlp_w_abs"], np.abs(g1["dmlp_w"]), rtol=1e-14, atol=0)

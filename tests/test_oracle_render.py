@@ -461,3 +461,23 @@ def test_mlp_half_activations_stay_close(orc):
     half = orc.mlp_eval(x, w, half_act=True)
     d = np.abs(exact - half)
     assert 0 < d.max() < 2e-3
+
+
+def test_blended_counts(orc):
+    # the number of composited entries per pixel: never above the last
+    # contributor's position; for a lone splat 1 exactly where its alpha
+    # reaches 1/255, else 0
+    sc = inputs.make_scene("tiny")
+    cam = inputs.make_cameras("tiny")[0]
+    r = orc.render(cam, sc)
+    assert np.all(r["n_blended"] <= r["n_contrib"]) and np.all((r["n_blended"] > 0) == (r["n_contrib"] > 0))
+    assert r["n_blended"].sum() > 10 * 4096
+    one = scene_of([[0, 0, 0]], [[-2.0] * 3], [[1, 0, 0, 0]], [0.0])
+    r1 = orc.render(cam, one)
+    pre = r1["pre"]
+    ys, xs = np.mgrid[0:64, 0:64].astype(np.float64) + 0.5
+    dx, dy = xs - pre["mean2d"][0, 0], ys - pre["mean2d"][1, 0]
+    a, b, c = pre["conic"][:, 0]
+    alpha = pre["opacity"][0] * np.exp(-0.5 * (a * dx * dx + c * dy * dy) - b * dx * dy)
+    clear = np.abs(alpha * 255.0 - 1.0) > 1e-4          # away from the threshold
+    assert np.array_equal(r1["n_blended"][clear], (alpha >= 1 / 255.0).astype(np.int32)[clear])

@@ -315,7 +315,9 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
 {
     __shared__ MlpFrags W;
     __shared__ MlpWaveStage ST[kBlock / kWave];
+    __shared__ float chain_slot;
     mlp_load_frags(a.mlp_w, W, true);
+    const float chain = decoder_chain_bound(a.mlp_w, GS_MLP_IN, GS_MLP_HIDDEN, 1, &chain_slot);
     const int wave = threadIdx.x >> 6, lane = __lane_id();
     MlpWaveStage& st = ST[wave];
     MlpGradAcc acc;
@@ -347,7 +349,7 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
         mlp_stage_row(st, valid, a.latent, n, i, d, dc);
         // the chunk's gradient scale (a power of two, see mlp_chunk_exponent)
         const float m = wave_max(fmaxf(fmaxf(fabsf(dc[0]), fabsf(dc[1])), fabsf(dc[2])));
-        mlp_grad_rescale(acc, mlp_chunk_exponent(m, acc.se));
+        mlp_grad_rescale(acc, mlp_chunk_exponent(m * chain, acc.se));
         const float scale = ldexpf(1.f, acc.se), inv = ldexpf(1.f, -acc.se);
         wave_lds_sync();
         const uint64_t vis = __ballot(valid);
@@ -427,8 +429,10 @@ __global__ __launch_bounds__(kBlock, kW == 32 ? 2 : 3) void k_preprocess_bwd_neu
     using Acc = std::conditional_t<kW == 32, MlpGradAcc, NeuralGradAcc<L>>;
     __shared__ Frags W;
     __shared__ NeuralBwdStage ST[kBlock / kWave];
+    __shared__ float chain_slot;
     const bool resid = a.sh_degree >= 1;
     if (resid) neural_load_frags(a.mlp_w, W, true);
+    const float chain = resid ? decoder_chain_bound(a.mlp_w, 32, kW, L - 1, &chain_slot) : 1.f;
     const int wave = threadIdx.x >> 6, lane = __lane_id();
     NeuralBwdStage& st = ST[wave];
     Acc acc;
@@ -490,7 +494,7 @@ __global__ __launch_bounds__(kBlock, kW == 32 ? 2 : 3) void k_preprocess_bwd_neu
             }
             st.d3[lane][3] = 0.f;
             // the chunk's gradient scale (a power of two, see neural_chunk_exponent)
-            neural_grad_rescale(acc, neural_chunk_exponent(wave_max(m), acc.se));
+            neural_grad_rescale(acc, neural_chunk_exponent(wave_max(m) * chain, acc.se));
             const float scale = ldexpf(1.f, acc.se), inv = ldexpf(1.f, -acc.se);
             wave_lds_sync();
             for (int t = 0; t < kWave / 16; ++t) {

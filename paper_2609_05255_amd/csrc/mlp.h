@@ -276,10 +276,43 @@ __device__ __forceinline__ float wave_max(float v)
     return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
 }
 
-// Scale exponent of a chunk whose largest colour-gradient magnitude is m: the
-// output gradients delta3 = dL/dc s (1 - s) <= m / 4 then stay below 2^9 after
-// scaling by 2^se, and the largest one lies within a factor 4 s (1 - s) of it,
-// far from the binary16 subnormals. m = 0 keeps the previous exponent.
+// Largest factor by which the backward can grow the output gradient on its
+// way to the first hidden layer: dH_L = Wout^T delta and dH_(l-1) = W_l^T dH_l,
+// so |dH_l| <= C_out C_L ... C_(l+1) max|delta| with C the largest column sum of
+// |W| (the infinity norm of W^T). Returns the largest of 1 and these products,
+// for weights stored [out][in] as binary16: W1 [width][n_in], `hidden`
+// matrices [width][width], Wout [3][width]. The workgroup's first wave reads
+// the weights; every thread returns the value (one barrier).
+__device__ __forceinline__ float decoder_chain_bound(const uint16_t* __restrict__ w, int n_in, int width, int hidden,
+                                                     float* slot)
+{
+    if (threadIdx.x < kWave) {
+        const int u = __lane_id();
+        const uint16_t* wo = w + width * n_in + hidden * width * width;
+        float cs = 0.f;
+        if (u < width)
+            for (int o = 0; o < 3; ++o) cs += fabsf((float)half_of_bits(wo[o * width + u]));
+        float prod = wave_max(cs), best = fmaxf(1.f, prod);
+        for (int h = hidden - 1; h >= 0; --h) {
+            const uint16_t* wh = w + width * n_in + h * width * width;
+            cs = 0.f;
+            if (u < width)
+                for (int r = 0; r < width; ++r) cs += fabsf((float)half_of_bits(wh[r * width + u]));
+            prod *= wave_max(cs);
+            best = fmaxf(best, prod);
+        }
+        if (u == 0) *slot = best;
+    }
+    __syncthreads();
+    return *slot;
+}
+
+// Scale exponent of a chunk whose largest colour-gradient magnitude, times the
+// decoder's chain bound, is m: the output gradients delta3 = dL/dc s (1 - s)
+// and the hidden-layer gradients they produce then stay below 2^9 after
+// scaling by 2^se (binary16 overflows above 65504), and the largest output
+// gradient lies within a factor 4 s (1 - s) and the chain bound of it, far
+// from the binary16 subnormals. m = 0 keeps the previous exponent.
 __device__ __forceinline__ int mlp_chunk_exponent(float m, int prev)
 {
     if (!(m > 0.f)) return prev;

@@ -275,10 +275,12 @@ __device__ __forceinline__ void neural_grad_rescale(NeuralGradAcc<L>& a, int se)
     a.se = se;
 }
 
-// Scale exponent of a chunk whose largest colour-gradient magnitude is m: the
-// output gradients dL/dc [c > 0] (1 - tanh^2) <= m stay below 2^10 after
-// scaling by 2^se, far from the binary16 subnormals and from overflow along
-// the chain. m = 0 keeps the previous exponent.
+// Scale exponent of a chunk whose largest output gradient dL/dc [c > 0]
+// (1 - tanh^2), times the decoder's chain bound (decoder_chain_bound), is m:
+// the output gradients and the hidden-layer gradients they produce then stay
+// below 2^10 after scaling by 2^se, far below the binary16 overflow at 65504;
+// the largest output gradient lies within the chain bound of 2^10, far from
+// the subnormals. m = 0 keeps the previous exponent.
 __device__ __forceinline__ int neural_chunk_exponent(float m, int prev)
 {
     if (!(m > 0.f)) return prev;

@@ -432,3 +432,41 @@ def test_render_work_counts(case):
         assert blended == ref_blended
     assert abs(blended - ref_blended) <= slack
     assert blended <= ev_bwd <= listed and ev_bwd <= ev_fwd
+
+
+# ---- decoder weights far from their initialisation -----------------------------------
+
+@pytest.mark.parametrize("kind,arch,factor", [("latent", None, 4.0), ("neural", (2, 16, 0), 4.0),
+                                              ("neural", (3, 16, 0), 4.0), ("neural", (2, 32, 0), 4.0),
+                                              ("neural", (3, 16, 0), 16.0)])
+def test_decoder_large_weights(kind, arch, factor):
+    # every decoder weight times 4 or 16 (exact in binary16): the backward's hidden-
+    # layer gradients grow by the layers' norms on the way back and must stay
+    # within binary16 range (the chunk's gradient scale accounts for them).
+    # The binary16 rounding flips of the forward grow with the weights too, so
+    # the colour and gradient bars are those of the decoder path scaled by the
+    # weights' growth along the network (the factor per layer).
+    sc = inputs.make_scene("tiny", appearance=(kind,), neural_arch=arch)
+    attr = "mlp_w" if kind == "latent" else "neural_w"
+    w = getattr(sc, attr).view(np.float16).astype(np.float32) * factor
+    setattr(sc, attr, w.astype(np.float16).view(np.uint16))
+    layers = 3 if kind == "latent" else arch[0] + 1
+    growth = factor ** layers
+    cam = tiny_camera()
+    say("case large weights %s %s x%g" % (kind, arch, factor))
+    ref = orc.render(cam, sc, kind=kind, sh_degree=3, mode="f32", half_act=True)
+    flagged = flagged_pixels(ref["margin"])
+    g = (inputs.make_upstream_grad(cam.width, cam.height, 0) * ~flagged[None]).astype(np.float32)
+    grads = orc.render_bwd(cam, sc, ref["pre"], ref["ranges"], ref["values"], g, kind=kind, sh_degree=3, mode="f32",
+                           half_act=True)
+    gpu = run_gpu(sc, cam, kind, 3, g)
+    vis = ref["pre"]["tiles"] > 0
+    err = np.abs(gpu["splat"]["color"][:, vis] - ref["pre"]["color"][:, vis])
+    say("  colours: max abs %.2e" % err.max())
+    assert err.max() <= MLP_HALF_ATOL * growth
+    for k, v in gpu["grads"].items():
+        assert np.all(np.isfinite(v)), k
+    st = grad_stats(gpu["grads"], grads)
+    report_grads(st)
+    for k, (rel, _, _, _) in st.items():
+        assert rel <= 5e-3, (k, rel)

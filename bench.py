@@ -101,7 +101,6 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="measure only --config (not the latent and stress comparisons)")
-    ap.add_argument("--cpu-tiles", type=int, default=96, help="tiles in the CPU-baseline sample")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before the steps, one device-to-device copy of this many MB (a plain copy kernel of "
                          "known size, to calibrate memory-traffic counters)")
@@ -408,7 +407,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(scene, cams, kind, args.cpu_tiles)
+        cpu = cpu_baseline(scene, cams, kind)
 
     out = {
         "metric": METRIC,
@@ -437,52 +436,56 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(scene, cams, kind, n_tiles_sample):
-    """The oracle on the host: full preprocess of every Gaussian, then binning,
-    forward and backward blending restricted to a random sample of tiles, the
-    per-tile part scaled to the whole image. One camera, single thread."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(scene, cams, kind):
+    """The oracle on the host cores, camera 0 of the workload: one full
+    iteration (preprocess of every Gaussian, binning, forward and backward
+    blending of every tile), measured on all the cores the process may use
+    and on one thread."""
     from oracle import oracle as orc
+    from paper_2609_05255_amd import inputs
 
     cam = cams[0]
-    tx, ty = orc.tile_grid(cam)
-    T = tx * ty
-    rng = np.random.default_rng(0)
-    sample = np.sort(rng.choice(T, size=min(n_tiles_sample, T), replace=False))
-    print("# cpu baseline: oracle preprocess of %d Gaussians" % scene.n, file=sys.stderr, flush=True)
-    t0 = time.perf_counter()
-    pre = orc.preprocess(cam, scene, kind=kind)
-    t_pre = time.perf_counter() - t0
-    print("# cpu baseline: preprocess %.1fs; sampled tiles next" % t_pre, file=sys.stderr, flush=True)
-    # keep only Gaussians whose rectangle meets a sampled tile
-    sx, sy = sample % tx, sample // tx
-    r = pre["rect"]
-    keep = np.zeros(scene.n, bool)
-    vis = np.nonzero(pre["tiles"] > 0)[0]
-    for lo in range(0, vis.size, 1 << 20):
-        idx = vis[lo:lo + (1 << 20)]
-        hit = ((r[0, idx, None] <= sx[None]) & (sx[None] < r[2, idx, None]) &
-               (r[1, idx, None] <= sy[None]) & (sy[None] < r[3, idx, None])).any(axis=1)
-        keep[idx[hit]] = True
-    sub = orc.Preprocessed({k: v.copy() for k, v in pre.items()})
-    sub["tiles"][~keep] = 0
-    sub["flags"][~keep] = 0
-    t1 = time.perf_counter()
-    values, _, ranges = orc.bin_sort(cam, sub)
-    mask = np.zeros(T, bool)
-    mask[sample] = True
-    ranges[~mask] = 0
-    img, fT, nc, _ = orc.render_fwd(cam, sub, ranges, values)
-    from paper_2609_05255_amd import inputs
     g = inputs.make_upstream_grad(cam.width, cam.height, 0)
-    orc.render_bwd(cam, scene, sub, ranges, values, g, kind=kind)
-    t_tiles = time.perf_counter() - t1
-    scale = T / sample.size
-    t_iter = t_pre + t_tiles * scale
-    return {"value": round(1.0 / t_iter, 6), "unit": "it/s", "cores": 1, "kind": "oracle",
-            "sample": "camera 0: preprocess of all %d Gaussians (%.1fs) + binning, forward and backward "
-                      "blending of %d random tiles of %d (%.1fs), tile part scaled x%.1f" % (
-                          scene.n, t_pre, sample.size, T, t_tiles, scale),
-            "s_per_iter": round(t_iter, 2)}
+    tx, ty = orc.tile_grid(cam)
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    threads = min(cores, int(os.environ.get("OMP_NUM_THREADS", cores)))
+    runs = {}
+    for label, k in (("all", threads), ("one", 1)):
+        orc.set_threads(k)
+        print("# cpu baseline: full oracle iteration on %d thread(s)" % k, file=sys.stderr, flush=True)
+        t0 = time.perf_counter()
+        pre = orc.preprocess(cam, scene, kind=kind)
+        t1 = time.perf_counter()
+        values, _, ranges = orc.bin_sort(cam, pre)
+        t2 = time.perf_counter()
+        orc.render_fwd(cam, pre, ranges, values)
+        t3 = time.perf_counter()
+        orc.render_bwd(cam, scene, pre, ranges, values, g, kind=kind)
+        t4 = time.perf_counter()
+        del pre, values, ranges
+        runs[label] = (t4 - t0, "preprocess %.1f, binning %.1f, forward %.1f, backward %.1f" % (
+            t1 - t0, t2 - t1, t3 - t2, t4 - t3))
+        print("# cpu baseline: %.1fs" % (t4 - t0), file=sys.stderr, flush=True)
+    orc.set_threads(threads)
+    what = ("camera 0, one full iteration: preprocess of all %d Gaussians, binning, forward and backward "
+            "blending of all %d tiles" % (scene.n, tx * ty))
+    return {"value": round(1.0 / runs["all"][0], 6), "unit": "it/s", "cores": threads, "kind": "oracle",
+            "sample": "%s, on %d threads: %.1fs (%s)" % (what, threads, runs["all"][0], runs["all"][1]),
+            "s_per_iter": round(runs["all"][0], 2), "nproc": os.cpu_count(), "cpu_model": cpu_model(),
+            "single_thread": {"value": round(1.0 / runs["one"][0], 6), "unit": "it/s", "cores": 1,
+                              "s_per_iter": round(runs["one"][0], 2),
+                              "sample": "%s, on one thread: %.1fs (%s)" % (what, runs["one"][0], runs["one"][1])}}
 
 
 if __name__ == "__main__":

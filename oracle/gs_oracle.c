@@ -4,13 +4,21 @@
  * Precision-independent helpers live here; the preprocess, blend and their
  * derivatives are in gs_oracle_body.inc, compiled once with the decision
  * precision REAL = float (suffix _f32) and once with REAL = double (_f64).
- * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -shared -fPIC.
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -fopenmp -shared -fPIC.
+ * Loops over Gaussians, pixels and tiles run on OpenMP threads; every sum is
+ * taken in an order fixed by the data (pairs, blocks of Gaussians), so the
+ * results do not depend on the number of threads.
  */
 #include "gs_oracle.h"
 
 #include <math.h>
+#include <omp.h>
 #include <stdlib.h>
 #include <string.h>
+
+void orc_set_threads(int32_t k) { omp_set_num_threads(k > 0 ? k : 1); }
+
+int32_t orc_get_threads(void) { return (int32_t)omp_get_max_threads(); }
 
 #ifndef M_PI
 #define M_PI 3.14159265358979323846
@@ -92,16 +100,17 @@ void orc_sh_basis(const double d[3], double Y[16], double dY[48])
 /* ---- pair list -------------------------------------------------------------- */
 typedef struct { int32_t tile; int32_t idx; double depth; } orc_pair;
 
-static int pair_cmp(const void* pa, const void* pb)
+static int pair_depth_cmp(const void* pa, const void* pb)
 {
     const orc_pair* a = (const orc_pair*)pa;
     const orc_pair* b = (const orc_pair*)pb;
-    if (a->tile != b->tile) return a->tile < b->tile ? -1 : 1;
     if (a->depth != b->depth) return a->depth < b->depth ? -1 : 1;
     if (a->idx != b->idx) return a->idx < b->idx ? -1 : 1;
     return 0;
 }
 
+/* Sorted by (tile, depth, index): the pairs are bucketed by tile (a counting
+ * sort), then each tile's bucket is sorted by (depth, index) on its own. */
 int64_t orc_bin_sort(int64_t n, const int32_t* rect, const double* depth, const int32_t* tiles,
                      int32_t tiles_x, int32_t tiles_y, int64_t capacity, int32_t* values,
                      int32_t* tile_of, int64_t* ranges)
@@ -109,35 +118,42 @@ int64_t orc_bin_sort(int64_t n, const int32_t* rect, const double* depth, const 
     int64_t total = 0;
     for (int64_t i = 0; i < n; ++i) total += tiles[i] > 0 ? tiles[i] : 0;
     if (total > capacity) return -1;
+    const int64_t n_tiles = (int64_t)tiles_x * tiles_y;
+    int64_t* cnt = (int64_t*)calloc((size_t)(n_tiles + 1), sizeof(int64_t));
+    for (int64_t i = 0; i < n; ++i) {
+        if (tiles[i] <= 0) continue;
+        int x0 = rect[0 * n + i], y0 = rect[1 * n + i], x1 = rect[2 * n + i], y1 = rect[3 * n + i];
+        for (int ty = y0; ty < y1; ++ty)
+            for (int tx = x0; tx < x1; ++tx) cnt[ty * tiles_x + tx] += 1;
+    }
+    int64_t start = 0;
+    for (int64_t t = 0; t < n_tiles; ++t) {
+        ranges[2 * t] = start;
+        ranges[2 * t + 1] = start;       /* fill position */
+        start += cnt[t];
+    }
     orc_pair* pairs = (orc_pair*)malloc(sizeof(orc_pair) * (size_t)(total > 0 ? total : 1));
-    int64_t k = 0;
     for (int64_t i = 0; i < n; ++i) {
         if (tiles[i] <= 0) continue;
         int x0 = rect[0 * n + i], y0 = rect[1 * n + i], x1 = rect[2 * n + i], y1 = rect[3 * n + i];
         for (int ty = y0; ty < y1; ++ty)
             for (int tx = x0; tx < x1; ++tx) {
-                pairs[k].tile = ty * tiles_x + tx;
-                pairs[k].idx = (int32_t)i;
-                pairs[k].depth = depth[i];
-                ++k;
+                const int64_t t = (int64_t)ty * tiles_x + tx;
+                orc_pair* q = &pairs[ranges[2 * t + 1]++];
+                q->tile = (int32_t)t;
+                q->idx = (int32_t)i;
+                q->depth = depth[i];
             }
     }
-    qsort(pairs, (size_t)total, sizeof(orc_pair), pair_cmp);
-    int64_t n_tiles = (int64_t)tiles_x * tiles_y;
-    for (int64_t t = 0; t < n_tiles; ++t) { ranges[2 * t] = 0; ranges[2 * t + 1] = 0; }
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t t = 0; t < n_tiles; ++t)
+        qsort(pairs + ranges[2 * t], (size_t)(ranges[2 * t + 1] - ranges[2 * t]), sizeof(orc_pair), pair_depth_cmp);
     for (int64_t p = 0; p < total; ++p) {
         values[p] = pairs[p].idx;
         if (tile_of) tile_of[p] = pairs[p].tile;
-        ranges[2 * pairs[p].tile + 1] += 1;          /* count first */
-    }
-    int64_t start = 0;
-    for (int64_t t = 0; t < n_tiles; ++t) {
-        int64_t cnt = ranges[2 * t + 1];
-        ranges[2 * t] = start;
-        ranges[2 * t + 1] = start + cnt;
-        start += cnt;
     }
     free(pairs);
+    free(cnt);
     return total;
 }
 

@@ -159,6 +159,10 @@ int orc_render_bwd_f64(const orc_camera* cam, int64_t n, const double* means, co
                        const orc_pre* pre, const int64_t* ranges, const int32_t* values,
                        const double* dL_dimage, const orc_grads* grads);
 
+/* Threads of the OpenMP loops (results do not depend on them). */
+void orc_set_threads(int32_t k);
+int32_t orc_get_threads(void);
+
 /* Real spherical harmonics of degree <= 3 (16 values) and their gradient
  * w.r.t. the direction components (16x3), built from the Legendre definition. */
 void orc_sh_basis(const double d[3], double Y[16], double dY[48]);

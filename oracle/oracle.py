@@ -42,7 +42,7 @@ def build(force: bool = False) -> str:
         if all(os.path.getmtime(os.path.join(_HERE, s)) <= lib_t for s in _SOURCES):
             return _LIB_PATH
     tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-ffp-contract=off", "-fno-fast-math",
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
            "-shared", "-fPIC", "-o", tmp, os.path.join(_HERE, "gs_oracle.c"), "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, _LIB_PATH)
@@ -320,6 +320,15 @@ def render(cam, scene, kind="sh3", sh_degree: int = 3, mode: str = "f32", dir_ex
     image, final_T, n_contrib, margin = render_fwd(cam, pre, ranges, values, mode, n_blended)
     return dict(pre=pre, values=values, tile_of=tile_of, ranges=ranges, image=image, final_T=final_T,
                 n_contrib=n_contrib, margin=margin, n_blended=n_blended)
+
+
+def set_threads(k: int):
+    """Threads of the oracle's parallel loops (its results do not depend on them)."""
+    lib().orc_set_threads(int(k))
+
+
+def get_threads() -> int:
+    return int(lib().orc_get_threads())
 
 
 def sh_basis(d) -> tuple:

@@ -8,6 +8,7 @@ compositing (transmittance bounds, skip/stop thresholds, permutation and
 translation invariance).
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -481,3 +482,25 @@ def test_blended_counts(orc):
     alpha = pre["opacity"][0] * np.exp(-0.5 * (a * dx * dx + c * dy * dy) - b * dx * dy)
     clear = np.abs(alpha * 255.0 - 1.0) > 1e-4          # away from the threshold
     assert np.array_equal(r1["n_blended"][clear], (alpha >= 1 / 255.0).astype(np.int32)[clear])
+
+
+@pytest.mark.parametrize("kind", ["sh3", "latent", "neural"])
+def test_results_do_not_depend_on_threads(orc, kind):
+    # every sum of the oracle runs in an order fixed by the data (pairs in
+    # list order, Gaussians in fixed blocks): one thread and several give the
+    # same bits, forward and backward
+    sc = inputs.make_scene("tiny", n=3000, appearance=(kind,))
+    cam = inputs.look_at_camera([0.3, -0.2, -3.0], 96, 80)
+    g = inputs.make_upstream_grad(cam.width, cam.height, 0)
+    outs = []
+    for k in (1, 5):
+        orc.set_threads(k)
+        r = orc.render(cam, sc, kind=kind)
+        gr = orc.render_bwd(cam, sc, r["pre"], r["ranges"], r["values"], g, kind=kind)
+        outs.append((r, gr))
+    orc.set_threads(os.cpu_count() or 1)
+    (r1, g1), (r5, g5) = outs
+    for k in ("values", "ranges", "image", "final_T", "n_contrib", "margin", "n_blended"):
+        assert np.array_equal(r1[k], r5[k]), k
+    for k in g1:
+        assert np.array_equal(g1[k], g5[k]), k

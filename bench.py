@@ -46,7 +46,7 @@ FP32_UNPACKED_PEAK_TFLOPS = 78.6 # 256 CU x 4 SIMD x 16 lanes x 2 flops x 2.4 GH
 #   skipped for the whole tile by the conservative alpha >= 1/255 box: 0
 BLEND_FLOPS = {"blend_fwd": (24.0, 15.0), "blend_bwd": (62.0, 15.0)}
 STAGES = {"preprocess": ("preprocess", "pair_count"),
-          "sort": ("depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges"),
+          "sort": ("depth_sort", "entry_offsets", "block_entries", "block_sort", "tile_lists"),
           "blend": ("blend_fwd",),
           "backward": ("clear", "blend_bwd", "preprocess_bwd", "mlp_reduce")}
 

@@ -250,8 +250,16 @@ gs_status gs_preprocess_noalloc(const gs_camera* cam, const gs_gaussians* g, con
  *   empty ({0, 0}: the image renders as background and the gradients as zero),
  *   and pre->num_pairs keeps the P needed, for the caller to compare with
  *   capacity when it next synchronises and to retry with a larger buffer.
+ *   A host-mode num_pairs that disagrees with the preprocess's count is also
+ *   found on the device when the lists need more than capacity; every range
+ *   then comes out empty in the same way.
  * values: [capacity] u32 device; tile_ids: optional [capacity] u32 tile of each pair.
  * tile_ranges: [n_tiles][2] u32 device.
+ * workspace: at least gs_workspace_size(n, width, height, capacity, ...) bytes
+ *   for this camera's image size (the per-block buffers depend on it).
+ * Method: the Gaussians are sorted by depth; each gets one entry per 4x4-tile
+ *   block its rectangle meets, in that order; a stable sort by block id groups
+ *   them; each block's 16 tile lists are then written by ordered compaction.
  */
 #define GS_PAIRS_ON_DEVICE UINT64_MAX
 gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, uint64_t num_pairs,
@@ -380,8 +388,8 @@ gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t c
  * attached to the calling thread detaches it. The library keeps no other
  * state between calls than the calling thread's attached timer and error text. */
 enum {
-    GS_KERNEL_PREPROCESS = 0, GS_KERNEL_PAIR_COUNT, GS_KERNEL_DEPTH_SORT, GS_KERNEL_PAIR_OFFSETS,
-    GS_KERNEL_DUPLICATE, GS_KERNEL_TILE_SORT, GS_KERNEL_RANGES, GS_KERNEL_BLEND_FWD,
+    GS_KERNEL_PREPROCESS = 0, GS_KERNEL_PAIR_COUNT, GS_KERNEL_DEPTH_SORT, GS_KERNEL_ENTRY_OFFSETS,
+    GS_KERNEL_BLOCK_ENTRIES, GS_KERNEL_BLOCK_SORT, GS_KERNEL_TILE_LISTS, GS_KERNEL_BLEND_FWD,
     GS_KERNEL_CLEAR, GS_KERNEL_BLEND_BWD, GS_KERNEL_PREPROCESS_BWD, GS_KERNEL_MLP_REDUCE,
     GS_KERNEL_ADAM, GS_KERNEL_NEURAL_FOLD, GS_KERNEL_COUNT
 };

@@ -165,7 +165,7 @@ void resolve_pending(gs_timer* t)
 }
 
 const char* const kKernelNames[GS_KERNEL_COUNT] = {
-    "preprocess", "pair_count", "depth_sort", "pair_offsets", "duplicate", "tile_sort", "ranges",
+    "preprocess", "pair_count", "depth_sort", "entry_offsets", "block_entries", "block_sort", "tile_lists",
     "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam", "neural_fold"};
 
 }  // namespace
@@ -202,7 +202,7 @@ void timing_end(int id, hipStream_t s)
     }
 }
 
-Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kind)
+Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kind, const Cam* cam)
 {
     Workspace w;
     memset(&w, 0, sizeof(w));
@@ -215,6 +215,8 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     const int64_t nn = n > 0 ? n : 1;
     const int64_t cap = capacity > 0 ? (int64_t)capacity : 1;
     const int64_t sort_blocks = std::max(div_up(nn, kSortTile), div_up(cap, kSortTile));
+    const int64_t n_blocks = cam ? (int64_t)blocks_x_of(*cam) * blocks_y_of(*cam) : 1;
+    const int64_t segs = cam ? segment_bound(*cam, (uint64_t)cap) : 1;
     w.block_pairs = (uint32_t*)take(sizeof(uint32_t) * pair_count_slots(nn));
     w.keys_a = (uint32_t*)take(sizeof(uint32_t) * nn);
     w.keys_b = (uint32_t*)take(sizeof(uint32_t) * nn);
@@ -224,10 +226,16 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.digit_tot = (uint32_t*)take(sizeof(uint32_t) * kRadix * 4);
     w.scan_part = (uint32_t*)take(sizeof(uint32_t) * (div_up(nn, kDupChunk) + 1));
     w.sorted_rect = (uint2*)take(sizeof(uint2) * nn);
+    w.entry_count = (uint64_t*)take(sizeof(uint64_t));
     w.pair_keys_a = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.pair_vals_a = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.pair_keys_b = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.pair_vals_b = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.block_ranges = (uint32_t*)take(sizeof(uint32_t) * 2 * n_blocks);
+    w.seg_base = (uint32_t*)take(sizeof(uint32_t) * (n_blocks + 1));
+    w.seg_block = (uint32_t*)take(sizeof(uint32_t) * segs);
+    w.seg_cnt = (uint32_t*)take(sizeof(uint32_t) * 16 * 4 * segs);
+    w.list_counters = (uint32_t*)take(sizeof(uint32_t) * 2);
     w.acc = (float*)take(sizeof(float) * kAccStride * nn);
     w.mlp_part = (float*)take(kind == GS_APP_LATENT_MLP ? sizeof(float) * GS_MLP_WEIGHTS * kMlpPartials
                               : kind == GS_APP_NEURAL ? sizeof(float) * GS_NEURAL_MAX_WEIGHTS * kMlpPartials : 0);
@@ -278,7 +286,10 @@ gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t c
     GS_CHECK(width > 0 && height > 0, "image size must be positive");
     GS_CHECK(capacity < ((uint64_t)1 << 32), "capacity must be below 2^32");
     GS_CHECK(kind >= GS_APP_SH3 && kind <= GS_APP_NASGABOR, "unknown appearance kind %d", kind);
-    *bytes = layout_workspace(nullptr, n, capacity, kind).bytes;
+    Cam grid;
+    grid.tiles_x = (width + kTile - 1) / kTile;
+    grid.tiles_y = (height + kTile - 1) / kTile;
+    *bytes = layout_workspace(nullptr, n, capacity, kind, &grid).bytes;
     return ok();
 }
 
@@ -363,9 +374,9 @@ gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_ap
 {
     gs_status st;
     if ((st = preprocess_checks(cam, g, app, out)) != GS_OK) return st;
-    const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind);
+    const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind, nullptr);
     if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
-    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind);
+    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind, nullptr);
     return preprocess_run(cam, g, app, out, num_pairs_host, ws, static_cast<hipStream_t>(stream));
 }
 
@@ -400,11 +411,13 @@ gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t 
                     (unsigned long long)capacity);
     GS_CHECK(tile_ranges != nullptr, "tile_ranges is NULL");
     GS_CHECK((on_device ? capacity : num_pairs) == 0 || values != nullptr, "values is NULL");
-    const Workspace need = layout_workspace(nullptr, n, capacity, GS_APP_SH3);
-    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
-    const Workspace ws = layout_workspace(workspace, n, capacity, GS_APP_SH3);
-    hipStream_t s = static_cast<hipStream_t>(stream);
     const Cam c = make_cam(*cam);
+    if (!blocks_supported(c))
+        return fail(GS_ERR_UNSUPPORTED, "%dx%d tiles exceed 65536 blocks of 4x4 tiles", c.tiles_x, c.tiles_y);
+    const Workspace need = layout_workspace(nullptr, n, capacity, GS_APP_SH3, &c);
+    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
+    const Workspace ws = layout_workspace(workspace, n, capacity, GS_APP_SH3, &c);
+    hipStream_t s = static_cast<hipStream_t>(stream);
     const int n_tiles = c.tiles_x * c.tiles_y;
     if (n == 0 || (on_device ? capacity : num_pairs) == 0) {
         // no pair can be listed (in device mode a positive count then exceeds
@@ -415,35 +428,26 @@ gs_status gs_bin_sort(const gs_camera* cam, const gs_preprocessed* pre, int64_t 
     // device mode: the kernels read P from pre->num_pairs and size nothing by it
     const PairCount pairs = on_device ? PairCount{pre->num_pairs, capacity, capacity}
                                       : PairCount{nullptr, num_pairs, capacity};
+    // block entries: at most one per pair, counted on the device (the grids
+    // are sized for the capacity in both modes)
+    const PairCount entries{ws.entry_count, capacity, capacity};
     const uint32_t* order = nullptr;
+    BlockEntries ent{nullptr, nullptr};
     timing_begin(GS_KERNEL_DEPTH_SORT, s);
     GS_HIP(launch_depth_sort(n, pre->depth_key, pre->splats, ws, &order, s));
     timing_end(GS_KERNEL_DEPTH_SORT, s);
-    timing_begin(GS_KERNEL_PAIR_OFFSETS, s);
-    GS_HIP(launch_pair_offsets(n, ws, s));
-    timing_end(GS_KERNEL_PAIR_OFFSETS, s);
-    const int passes = tile_sort_passes(c);
-    // tile ids travel as 16-bit keys through the sort when they fit; with a
-    // single tile there is no sort and the pair emission writes the 32-bit ids
-    TileKeys sorted_tiles{nullptr, false};
-    TileKeys dup_keys{ws.pair_keys_a, passes > 0 && tile_keys_narrow(c)};
-    uint32_t* dup_vals = ws.pair_vals_a;
-    if (passes == 0) {
-        dup_keys.p = tile_ids ? tile_ids : ws.pair_keys_a;
-        dup_vals = values;
-        sorted_tiles = dup_keys;
-    }
-    timing_begin(GS_KERNEL_DUPLICATE, s);
-    GS_HIP(launch_duplicate(c, n, order, ws, pairs, dup_keys, dup_vals, s));
-    timing_end(GS_KERNEL_DUPLICATE, s);
-    if (passes > 0) {
-        timing_begin(GS_KERNEL_TILE_SORT, s);
-        GS_HIP(launch_tile_sort(c, pairs, ws, values, tile_ids, &sorted_tiles, s));
-        timing_end(GS_KERNEL_TILE_SORT, s);
-    }
-    timing_begin(GS_KERNEL_RANGES, s);
-    GS_HIP(launch_ranges(c, pairs, sorted_tiles, tile_ranges, s));
-    timing_end(GS_KERNEL_RANGES, s);
+    timing_begin(GS_KERNEL_ENTRY_OFFSETS, s);
+    GS_HIP(launch_entry_offsets(n, pairs, ws, s));
+    timing_end(GS_KERNEL_ENTRY_OFFSETS, s);
+    timing_begin(GS_KERNEL_BLOCK_ENTRIES, s);
+    GS_HIP(launch_block_entries(c, n, order, entries, ws, s));
+    timing_end(GS_KERNEL_BLOCK_ENTRIES, s);
+    timing_begin(GS_KERNEL_BLOCK_SORT, s);
+    GS_HIP(launch_block_sort(c, entries, ws, &ent, s));
+    timing_end(GS_KERNEL_BLOCK_SORT, s);
+    timing_begin(GS_KERNEL_TILE_LISTS, s);
+    GS_HIP(launch_tile_lists(c, pairs, capacity, ws, ent, values, tile_ids, tile_ranges, s));
+    timing_end(GS_KERNEL_TILE_LISTS, s);
     return ok();
 }
 
@@ -502,9 +506,9 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
             GS_CHECK(grads->dbase_color && grads->dlobes, "dbase_color or dlobes is NULL");
         else GS_CHECK(grads->dlatent && grads->dmlp_w, "dlatent or dmlp_w is NULL");
     }
-    const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind);
+    const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind, nullptr);
     if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
-    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind);
+    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind, nullptr);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const Cam c = make_cam(*cam);
     if (g->n == 0) {

@@ -284,7 +284,7 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_lobe(BwdArgs a)
                 dl[5 + c] = gc[c] * G * (1.f - T[c] * T[c]);
             }
             for (int k = 0; k < 5; ++k) dl[k] = sgt * draw[k];
-            if (kGabor) dl[8] = sgt * draw[5];
+            if constexpr (kGabor) dl[8] = sgt * draw[5];
             // d = v / |v|: dv = (dd - d (d . dd)) / |v|
             const float dot = d[0] * dd[0] + d[1] * dd[1] + d[2] * dd[2];
             for (int j = 0; j < 3; ++j) gg.dmu[j] += sgt * (dd[j] - d[j] * dot) * il;
@@ -306,6 +306,35 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_lobe(BwdArgs a)
     }
 }
 
+// The geometry backward's per-Gaussian inputs that the decoder kernels read
+// before their matrix-core phase (the mean, for the view direction, and the
+// screen-space accumulator entries 0..5, read with the colour entries), kept
+// per wave in LDS across that phase so that each is read from memory once.
+// Each lane reads back only what it wrote: no barrier is needed.
+struct GeoStage {
+    float v[3 + 6][kWave];
+};
+
+__device__ __forceinline__ void geo_stage_put(GeoStage& gs, const float mu[3], const float* ap)
+{
+    const int l = __lane_id();
+#pragma unroll
+    for (int j = 0; j < 3; ++j) gs.v[j][l] = mu[j];
+#pragma unroll
+    for (int k = 0; k < 6; ++k) gs.v[3 + k][l] = ap[k];
+}
+
+__device__ __forceinline__ void geo_stage_get(const GeoStage& gs, float mu[3], float g9[kAccStride])
+{
+    const int l = __lane_id();
+#pragma unroll
+    for (int j = 0; j < 3; ++j) mu[j] = gs.v[j][l];
+#pragma unroll
+    for (int k = 0; k < 6; ++k) g9[k] = gs.v[3 + k][l];
+#pragma unroll
+    for (int k = 6; k < kAccStride; ++k) g9[k] = 0.f;   // the colour entries are the decoder's
+}
+
 // Latent + MLP backward: geometry as for SH3, then per tile of 16 Gaussians
 // the decoder is recomputed and differentiated on the matrix cores (mlp.h):
 // the latent gradient, the gradient into the view direction (chained into the
@@ -315,6 +344,7 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
 {
     __shared__ MlpFrags W;
     __shared__ MlpWaveStage ST[kBlock / kWave];
+    __shared__ GeoStage GS[kBlock / kWave];
     __shared__ float chain_slot;
     mlp_load_frags(a.mlp_w, W, true);
     const float chain = decoder_chain_bound(a.mlp_w, GS_MLP_IN, GS_MLP_HIDDEN, 1, &chain_slot);
@@ -344,7 +374,10 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
             d[1] = vy / len;
             d[2] = vz / len;
             const float* ap = a.acc + (size_t)i * kAccStride;
-            for (int ch = 0; ch < 3; ++ch) dc[ch] = ap[6 + ch];
+            float g9[kAccStride];
+            for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+            for (int ch = 0; ch < 3; ++ch) dc[ch] = g9[6 + ch];
+            geo_stage_put(GS[wave], mu, g9);
         }
         mlp_stage_row(st, valid, a.latent, n, i, d, dc);
         // the chunk's gradient scale (a power of two, see mlp_chunk_exponent)
@@ -361,11 +394,9 @@ __global__ __launch_bounds__(kBlock, 3) void k_preprocess_bwd_latent(BwdArgs a)
         wave_lds_sync();
         if (valid) {
             float mu[3], ls[3], q[4], g9[kAccStride];
-            for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
             for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
             for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
-            const float* ap = a.acc + (size_t)i * kAccStride;
-            for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+            geo_stage_get(GS[wave], mu, g9);
             GeoGrad gg;
             geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
             // the binary16 rounding of d passes the gradient; d = v / |v|
@@ -429,6 +460,7 @@ __global__ __launch_bounds__(kBlock, kW == 32 ? 2 : 3) void k_preprocess_bwd_neu
     using Acc = std::conditional_t<kW == 32, MlpGradAcc, NeuralGradAcc<L>>;
     __shared__ Frags W;
     __shared__ NeuralBwdStage ST[kBlock / kWave];
+    __shared__ GeoStage GS[kBlock / kWave];
     __shared__ float chain_slot;
     const bool resid = a.sh_degree >= 1;
     if (resid) neural_load_frags(a.mlp_w, W, true);
@@ -459,8 +491,11 @@ __global__ __launch_bounds__(kBlock, kW == 32 ? 2 : 3) void k_preprocess_bwd_neu
             d[1] = vy / len;
             d[2] = vz / len;
             const float* ap = a.acc + (size_t)i * kAccStride;
-            for (int ch = 0; ch < 3; ++ch) dc[ch] = ap[6 + ch];
+            float g9[kAccStride];
+            for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+            for (int ch = 0; ch < 3; ++ch) dc[ch] = g9[6 + ch];
             for (int ch = 0; ch < 3; ++ch) c0[ch] = a.base_color[ch * n + i];
+            geo_stage_put(GS[wave], mu, g9);
         }
         float dd[3] = {0.f, 0.f, 0.f};
         if (resid) {
@@ -525,11 +560,9 @@ __global__ __launch_bounds__(kBlock, kW == 32 ? 2 : 3) void k_preprocess_bwd_neu
         }
         if (valid) {
             float mu[3], ls[3], q[4], g9[kAccStride];
-            for (int j = 0; j < 3; ++j) mu[j] = a.means[j * n + i];
             for (int j = 0; j < 3; ++j) ls[j] = a.log_scales[j * n + i];
             for (int j = 0; j < 4; ++j) q[j] = a.quats[j * n + i];
-            const float* ap = a.acc + (size_t)i * kAccStride;
-            for (int k = 0; k < kAccStride; ++k) g9[k] = ap[k];
+            geo_stage_get(GS[wave], mu, g9);
             GeoGrad gg;
             geometry_bwd(a.cam, mu, ls, q, a.logits[i], g9, gg);
             if (resid) {

@@ -60,7 +60,8 @@ constexpr int kSortItems = 16;
 constexpr int kPairItems = 24;
 constexpr int kSortTile = kBlock * kSortItems;   // 4096
 constexpr int kRadix = 256;
-constexpr int kDupChunk = 1024;   // depth-ordered Gaussians per workgroup in pair emission
+constexpr int kDupChunk = 1024;   // depth-ordered Gaussians per workgroup in entry emission
+constexpr int kBlockDim = 4;      // a block is kBlockDim x kBlockDim tiles
 
 // Workgroups of the decoder preprocess backward (grid-stride), one partial
 // weight gradient each: as many as are resident at once, 3 per compute unit
@@ -81,18 +82,25 @@ struct Workspace {
     uint32_t* vals_b;        // [n]
     uint32_t* hist;          // [256][max sort blocks]
     uint32_t* digit_tot;     // [4 passes][256]   digit totals of each pass
-    uint32_t* scan_part;     // [n / kDupChunk + 1] chunk sums of the pair-offset scan
+    uint32_t* scan_part;     // [n / kDupChunk + 1] chunk sums of the entry-offset scan
     uint2* sorted_rect;      // [n]               tile rectangles in depth order (empty for culled)
-    uint32_t* pair_keys_a;   // [capacity]        tile ids (16-bit in the first half when narrow)
-    uint32_t* pair_vals_a;   // [capacity]
+    uint64_t* entry_count;   // [1]               block entries (0 when the pairs exceed the capacity)
+    uint32_t* pair_keys_a;   // [capacity]        entry keys: block id << 16 | tile mask
+    uint32_t* pair_vals_a;   // [capacity]        entry values: Gaussian index
     uint32_t* pair_keys_b;   // [capacity]
     uint32_t* pair_vals_b;   // [capacity]
+    uint32_t* block_ranges;  // [blocks][2]       each block's entries
+    uint32_t* seg_base;      // [blocks + 1]      first segment of each block
+    uint32_t* seg_block;     // [segments]        block of each segment
+    uint32_t* seg_cnt;       // [segments][4][16] per-tile counts, then offsets, of each wave's sub-segment
+    uint32_t* list_counters; // [2]               segments; tile lists over capacity
     float* acc;              // [n][9]            blend-backward accumulators
     float* mlp_part;         // [kMlpPartials][1664] per-workgroup decoder weight gradients
     size_t bytes;
 };
 
-Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kind);
+// `cam` (NULL for calls that bin nothing) sizes the per-block buffers.
+Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kind, const struct Cam* cam);
 
 // Number of (tile, Gaussian) pairs as the bin-sort kernels see it. Host mode:
 // `host` is P itself. Device mode: P is read on the device from the
@@ -118,21 +126,22 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
 hipError_t launch_pair_count(int64_t n, int32_t kind, const Workspace& ws, uint64_t* num_pairs, hipStream_t s);
 hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_splat* splats, const Workspace& ws,
                              const uint32_t** order_out, hipStream_t s);
-hipError_t launch_pair_offsets(int64_t n, const Workspace& ws, hipStream_t s);
-// Tile ids of the pairs: 16-bit while the image has at most 65536 tiles.
-struct TileKeys {
-    void* p;
-    bool narrow;
+hipError_t launch_entry_offsets(int64_t n, PairCount pairs, const Workspace& ws, hipStream_t s);
+int blocks_x_of(const Cam& cam);
+int blocks_y_of(const Cam& cam);
+int64_t segment_bound(const Cam& cam, uint64_t capacity);   // segments the tile-list kernels can meet
+bool blocks_supported(const Cam& cam);   // at most 65536 blocks: the block id shares a u32 key with a tile mask
+hipError_t launch_block_entries(const Cam& cam, int64_t n, const uint32_t* order, PairCount entries,
+                                const Workspace& ws, hipStream_t s);
+struct BlockEntries {
+    const uint32_t* key;   // block id << 16 | mask of the block's tiles the Gaussian meets
+    const uint32_t* gid;   // Gaussian index
 };
-bool tile_keys_narrow(const Cam& cam);
-hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const Workspace& ws,
-                            PairCount pairs, TileKeys keys_out, uint32_t* vals_out, hipStream_t s);
-int tile_sort_passes(const Cam& cam);
+hipError_t launch_block_sort(const Cam& cam, PairCount entries, const Workspace& ws, BlockEntries* out, hipStream_t s);
+hipError_t launch_tile_lists(const Cam& cam, PairCount pairs, uint64_t capacity, const Workspace& ws,
+                             const BlockEntries& ent, uint32_t* values, uint32_t* tile_ids, uint32_t* tile_ranges,
+                             hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, int64_t count, uint32_t value, hipStream_t s);
-hipError_t launch_tile_sort(const Cam& cam, PairCount pairs, const Workspace& ws, uint32_t* values,
-                            uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s);
-hipError_t launch_ranges(const Cam& cam, PairCount pairs, TileKeys sorted_tiles, uint32_t* tile_ranges,
-                         hipStream_t s);
 hipError_t launch_blend_fwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                             const uint32_t* tile_ranges, float* image, float* final_T, uint32_t* n_contrib,
                             hipStream_t s);

@@ -3,16 +3,18 @@
 //
 // Instead of radix-sorting P 45-bit (tile, depth) keys, the Gaussians are
 // sorted once by depth (4 stable 8-bit LSD passes over n 32-bit keys with the
-// index as value, so equal depths stay in index order), the pairs are emitted
-// in that order, and a stable LSD sort on the tile id alone finishes the job:
-// stability keeps (depth, index) order within a tile. The tile id needs
-// ceil(log2 T) bits, split evenly over as few passes of <= 8 bits as possible.
+// index as value, so equal depths stay in index order). Then, in that order,
+// each Gaussian gets one entry per 4x4-tile block its rectangle meets (about a
+// quarter as many entries as pairs), a stable LSD sort on the block id groups
+// the entries by block with depth order kept inside each block, and every
+// block's 16 tile lists are cut out of its entries by ordered (ballot)
+// compaction, each list written once, at its final place.
 //
 // One radix pass = k_radix_hist (per-workgroup digit counts) + k_radix_scan
 // (exclusive offsets per digit over workgroups) + k_radix_scatter: each wave
 // ranks a contiguous slice of the workgroup's keys with ballot-matched digits
 // (no workgroup barrier per round), the workgroup reorders its keys (4096 in
-// the depth sort, 6144 in the tile sort) by digit in LDS, and writes each
+// the depth sort, 6144 in the block sort) by digit in LDS, and writes each
 // digit's run to consecutive global addresses.
 #include "gs_internal.h"
 
@@ -258,42 +260,64 @@ hipError_t radix_pass(const KeyT* keys_in, const uint32_t* vals_in, PairCount cn
     return hipGetLastError();
 }
 
-// ---- pair offsets in depth order and pair emission ---------------------------
 
-// Pairs emitted by each chunk of kDupChunk depth-ordered Gaussians.
+// ---- block entries in depth order -------------------------------------------
+//
+// A block is kBlockDim x kBlockDim tiles. Each visible Gaussian gets one entry
+// per block its tile rectangle meets, in depth order; the entries are then
+// sorted by block id (stable, so depth order holds inside a block), and each
+// block's tile lists are cut out of its entries by ordered compaction.
+
+// Block rectangle (half-open, block units, packed like a tile rectangle) of a
+// tile rectangle; an empty rectangle stays empty.
 __device__ __forceinline__ uint32_t rect_area(uint2 r)
 {
     return ((r.y & 0xFFFFu) - (r.x & 0xFFFFu)) * ((r.y >> 16) - (r.x >> 16));
 }
 
-__global__ __launch_bounds__(kBlock) void k_pair_partial(const uint2* __restrict__ sorted_rect, int64_t n,
-                                                         uint32_t* __restrict__ part)
+__device__ __forceinline__ uint2 block_rect(uint2 r)
+{
+    if (rect_area(r) == 0) return make_uint2(0u, 0u);
+    const uint32_t x0 = r.x & 0xFFFFu, y0 = r.x >> 16, x1 = r.y & 0xFFFFu, y1 = r.y >> 16;
+    constexpr uint32_t kS = 2, kR = kBlockDim - 1;   // log2 and mask of the block size
+    static_assert(kBlockDim == 1 << kS, "block size");
+    return make_uint2((x0 >> kS) | ((y0 >> kS) << 16), ((x1 + kR) >> kS) | (((y1 + kR) >> kS) << 16));
+}
+
+// Entries of each chunk of kDupChunk depth-ordered Gaussians.
+__global__ __launch_bounds__(kBlock) void k_entry_partial(const uint2* __restrict__ sorted_rect, int64_t n,
+                                                          uint32_t* __restrict__ part)
 {
     __shared__ uint32_t lds4[4];
     uint32_t sum = 0;
     for (int k = 0; k < kDupItems; ++k) {
         const int64_t i = (int64_t)blockIdx.x * kDupChunk + (int64_t)k * kBlock + threadIdx.x;
-        if (i < n) sum += rect_area(sorted_rect[i]);
+        if (i < n) sum += rect_area(block_rect(sorted_rect[i]));
     }
     uint32_t total;
     block_excl_scan(sum, lds4, &total);
     if (threadIdx.x == 0) part[blockIdx.x] = total;
 }
 
-// Exclusive scan of the per-chunk totals (one workgroup).
-__global__ __launch_bounds__(kBlock) void k_scan_partials(uint32_t* __restrict__ part, int count)
+// Exclusive scan of the per-chunk totals (one workgroup); the grand total, the
+// number of entries, goes to *entries (0 when the pair count is over capacity:
+// nothing downstream then reads an entry).
+__global__ __launch_bounds__(kBlock) void k_scan_partials(uint32_t* __restrict__ part, int count, PairCount pairs,
+                                                          uint64_t* __restrict__ entries)
 {
     __shared__ uint32_t lds4[4];
     const int per = (count + kBlock - 1) / kBlock;
     const int start = threadIdx.x * per, end = min(start + per, count);
     uint32_t sum = 0;
     for (int k = start; k < end; ++k) sum += part[k];
-    uint32_t run = block_excl_scan(sum, lds4, nullptr);
+    uint32_t total;
+    uint32_t run = block_excl_scan(sum, lds4, &total);
     for (int k = start; k < end; ++k) {
         const uint32_t v = part[k];
         part[k] = run;
         run += v;
     }
+    if (threadIdx.x == 0) *entries = pairs.overflow() ? 0ull : (uint64_t)total;
 }
 
 // Inclusive maximum scan over the wave's lanes (DPP row shifts, then the row
@@ -316,33 +340,48 @@ __device__ __forceinline__ void wave_lds_fence()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Emits the (tile, Gaussian) pairs of a chunk of depth-ordered Gaussians, each
-// Gaussian's tiles in row-major order of its rectangle. The chunk's offsets
-// and rectangles are staged in LDS. Each wave then emits a contiguous quarter
-// of the chunk's pairs, kDupWin consecutive pairs per round in groups of 64
-// (consecutive lanes write consecutive addresses): the lanes mark in LDS where
-// the Gaussians of the next kDupWin - 1 slots start inside the round's window
-// (after its first pair, which belongs to the round's first Gaussian), and an
-// inclusive maximum scan over the window gives each pair its Gaussian. Depth
-// order puts every culled Gaussian (no tiles) after the visible ones, so starts
-// inside a window are distinct.
-constexpr int kDupGroups = 8;                   // 64-pair groups per round
-constexpr int kDupWin = kWave * kDupGroups;     // pairs per round
-
-template <typename KeyT>
-__global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict__ order,
-                                                      const uint2* __restrict__ sorted_rect, int64_t n,
-                                                      const uint32_t* __restrict__ part, int tiles_x,
-                                                      PairCount pairs, KeyT* __restrict__ keys,
-                                                      uint32_t* __restrict__ vals)
+// Bit 4k + i set where the tile rectangle r meets tile (4 bx + i, 4 by + k).
+__device__ __forceinline__ uint32_t tile_mask(uint2 r, int bx, int by)
 {
-    // a device count beyond the capacity: no pair is emitted
-    if (pairs.overflow()) return;
-    const uint32_t capacity = (uint32_t)pairs.cap;
+    const int ox = kBlockDim * bx, oy = kBlockDim * by;
+    const int cx0 = max((int)(r.x & 0xFFFFu) - ox, 0), cx1 = min((int)(r.y & 0xFFFFu) - ox, kBlockDim);
+    const int cy0 = max((int)(r.x >> 16) - oy, 0), cy1 = min((int)(r.y >> 16) - oy, kBlockDim);
+    if (cx1 <= cx0 || cy1 <= cy0) return 0u;
+    const uint32_t cols = ((1u << cx1) - 1u) & ~((1u << cx0) - 1u);
+    const uint32_t rows = ((1u << cy1) - 1u) & ~((1u << cy0) - 1u);
+    // rows bit k -> bit 4k, then one copy of the column bits per row
+    const uint32_t spread = (rows & 1u) | ((rows & 2u) << 3) | ((rows & 4u) << 6) | ((rows & 8u) << 9);
+    return cols * spread;
+}
+
+// Emits the entries of a chunk of depth-ordered Gaussians, each Gaussian's
+// blocks in row-major order of its block rectangle: key = block id << 16 |
+// the mask of the block's tiles that the Gaussian's rectangle meets, value =
+// the Gaussian's index. The chunk's offsets, rectangles and indices are staged
+// in LDS. Each wave then emits a contiguous quarter of the chunk's entries,
+// kDupWin consecutive entries per round in groups of 64 (consecutive lanes
+// write consecutive addresses): the lanes mark in LDS where the Gaussians of
+// the next kDupWin - 1 slots start inside the round's window (after its first
+// entry, which belongs to the round's first Gaussian), and an inclusive
+// maximum scan over the window gives each entry its Gaussian. Depth order puts
+// every culled Gaussian (no tiles) after the visible ones, so starts inside a
+// window are distinct.
+constexpr int kDupGroups = 8;                   // 64-entry groups per round
+constexpr int kDupWin = kWave * kDupGroups;     // entries per round
+constexpr int kMaskBits = 16;                   // low key bits: the tile mask
+
+__global__ __launch_bounds__(kBlock) void k_block_entries(const uint32_t* __restrict__ order,
+                                                          const uint2* __restrict__ sorted_rect, int64_t n,
+                                                          const uint32_t* __restrict__ part, int blocks_x,
+                                                          PairCount entries, uint32_t* __restrict__ keys,
+                                                          uint32_t* __restrict__ vals)
+{
+    const uint32_t count = (uint32_t)entries.get();   // 0 when the pairs are over capacity
     __shared__ uint32_t soff[kDupChunk + 1];
-    __shared__ uint32_t sgid[kDupChunk];
-    __shared__ uint32_t sorg[kDupChunk];   // rectangle origin x0 | y0 << 16
-    __shared__ uint32_t swid[kDupChunk];   // rectangle width in tiles
+    __shared__ uint32_t sorg[kDupChunk];   // block rectangle origin x0 | y0 << 16
+    __shared__ uint32_t swid[kDupChunk];   // block rectangle width
+    __shared__ uint2 srect[kDupChunk];     // tile rectangle
+    __shared__ uint32_t sgid[kDupChunk];   // Gaussian index
     __shared__ int smark[kBlock / kWave][kDupWin];
     __shared__ uint32_t lds4[4];
     const int t = threadIdx.x;
@@ -352,10 +391,12 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
     for (int k = 0; k < kDupItems; ++k) {
         const int slot = t * kDupItems + k;
         const int64_t i = base + slot;
-        uint32_t c = 0, g = 0, org = 0, w = 1;
+        uint32_t c = 0, org = 0, w = 1, g = 0;
+        uint2 tr = make_uint2(0u, 0u);
         if (i < n) {
+            tr = sorted_rect[i];
             g = order[i];
-            const uint2 r = sorted_rect[i];
+            const uint2 r = block_rect(tr);
             c = rect_area(r);
             if (c != 0) {
                 org = r.x;
@@ -364,9 +405,10 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
         }
         cnt[k] = c;
         sum += c;
-        sgid[slot] = g;
         sorg[slot] = org;
         swid[slot] = w;
+        srect[slot] = tr;
+        sgid[slot] = g;
     }
     uint32_t total;
     uint32_t off = block_excl_scan(sum, lds4, &total);
@@ -415,12 +457,14 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
             run = __builtin_amdgcn_readlane(m[k], kWave - 1);
         }
         uint32_t o[kDupGroups], w[kDupGroups], org[kDupGroups], gid[kDupGroups];
+        uint2 tr[kDupGroups];
 #pragma unroll
         for (int k = 0; k < kDupGroups; ++k) {
             const int slot = first + m[k];
             o[k] = soff[slot];
             w[k] = swid[slot];
             org[k] = sorg[slot];
+            tr[k] = srect[slot];
             gid[k] = sgid[slot];
         }
 #pragma unroll
@@ -428,16 +472,16 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
             const uint32_t p = p0 + kWave * k + lane;
             const uint32_t i = p - o[k];
             const uint32_t q = i / w[k];
-            const uint32_t tx = (org[k] & 0xFFFFu) + (i - q * w[k]);
-            const uint32_t ty = (org[k] >> 16) + q;
+            const uint32_t bx = (org[k] & 0xFFFFu) + (i - q * w[k]);
+            const uint32_t by = (org[k] >> 16) + q;
             const uint32_t out = gbase + p;
-            // only a num_pairs that disagrees with the preprocess gets past the capacity
-            if (p < q1 && out < capacity) {
-                keys[out] = (KeyT)(ty * (uint32_t)tiles_x + tx);
+            // a count of 0 (pairs over capacity) writes nothing
+            if (p < q1 && out < count) {
+                keys[out] = ((by * (uint32_t)blocks_x + bx) << kMaskBits) | tile_mask(tr[k], (int)bx, (int)by);
                 vals[out] = gid[k];
             }
         }
-        // the next round starts with the Gaussian holding pair p0 + kDupWin: the
+        // the next round starts with the Gaussian holding entry p0 + kDupWin: the
         // window's last owner, or the one after it if that ends exactly there
         const int last = first + run;
         first = last + (soff[last + 1] == p0 + kDupWin ? 1 : 0);
@@ -445,33 +489,277 @@ __global__ __launch_bounds__(kBlock) void k_duplicate(const uint32_t* __restrict
     }
 }
 
-// One wave per tile boundary v = 0..n_tiles: the first position whose tile id
-// is >= v, by a 64-way search. Each round the lanes probe 64 evenly spaced
+// One wave per boundary v = 0..n_keys of sorted keys: the first position whose
+// key >> shift is >= v, by a 64-way search. Each round the lanes probe 64 evenly spaced
 // positions of [lo, hi); the probes below v form a prefix (the keys are
 // sorted), so their count c narrows the answer to (probe c-1, probe c]. About
-// log64(P) dependent loads instead of log2(P). Boundary v ends tile v - 1 and
-// starts tile v.
-template <typename KeyT>
-__global__ __launch_bounds__(kBlock) void k_ranges(const KeyT* __restrict__ sorted_tiles, PairCount pairs,
-                                                   int n_tiles, uint32_t* __restrict__ ranges)
+// log64(count) dependent loads instead of log2(count). Boundary v ends range
+// v - 1 and starts range v.
+__global__ __launch_bounds__(kBlock) void k_ranges(const uint32_t* __restrict__ sorted_keys, int shift,
+                                                   PairCount cnt, int n_keys, uint32_t* __restrict__ ranges)
 {
-    const uint32_t count = (uint32_t)pairs.get();
+    const uint32_t count = (uint32_t)cnt.get();
     const int v = (int)blockIdx.x * (kBlock / kWave) + (int)(threadIdx.x >> 6);
-    if (v > n_tiles) return;
+    if (v > n_keys) return;
     const uint32_t lane = __lane_id();
     uint32_t lo = 0, hi = count;   // the answer lies in [lo, hi]
     while (hi > lo) {
         const uint32_t step = (hi - lo + kWave - 1) / kWave;
         const uint32_t p = lo + lane * step;
-        const bool below = p < hi && (uint32_t)sorted_tiles[p] < (uint32_t)v;
+        const bool below = p < hi && (sorted_keys[p] >> shift) < (uint32_t)v;
         const uint32_t c = (uint32_t)__popcll(__ballot(below));
         const uint32_t nlo = c ? lo + (c - 1) * step + 1 : lo;
         hi = min(hi, lo + c * step);
         lo = nlo;
     }
     if (lane == 0) {
-        if (v < n_tiles) ranges[2 * v] = lo;
+        if (v < n_keys) ranges[2 * v] = lo;
         if (v > 0) ranges[2 * v - 1] = lo;
+    }
+}
+
+// ---- tile lists out of the block entries ------------------------------------
+//
+// Each block's entries are cut into segments of kSegEntries, one workgroup
+// per segment and one sub-segment of 512 entries per wave. k_tile_count
+// counts, per sub-segment, the entries that meet each of the block's 16 tiles;
+// k_tile_scan turns the counts into each sub-segment's offset inside each
+// tile's list and each tile's length; k_tile_starts places the lists in tile
+// order (the ranges); k_tile_emit writes every tile's Gaussians, in entry
+// order, by ballot compaction.
+
+constexpr int kBlockTiles = kBlockDim * kBlockDim;             // 16
+constexpr int kSegRounds = 8;                                  // 64-entry rounds per wave
+constexpr int kSegEntries = kSegRounds * kBlock;               // 2048 entries per segment
+constexpr int kSubSegs = kBlock / kWave;                       // one sub-segment per wave
+constexpr int kListThreads = 1024;                             // single-workgroup scans
+static_assert(kBlockTiles == 16, "tile masks are 16 bits");
+
+// Exclusive scan of one u32 per thread over a 1024-thread workgroup.
+__device__ __forceinline__ uint32_t wg_excl_scan_1024(uint32_t v, uint32_t* lds16, uint32_t* total)
+{
+    const int lane = __lane_id(), wave = threadIdx.x >> 6;
+    uint32_t x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) lds16[wave] = x;
+    __syncthreads();
+    uint32_t before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kListThreads / kWave; ++w) {
+        const uint32_t s = lds16[w];
+        if (w < wave) before += s;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return before + x - v;
+}
+
+// Segment table: one workgroup. seg_base[b] = first segment of block b (and
+// seg_base[n_blocks] = their number), seg_block[s] = the block of segment s,
+// counters[0] = the number of segments.
+__global__ __launch_bounds__(kListThreads) void k_segments(const uint32_t* __restrict__ block_ranges, int n_blocks,
+                                                           uint32_t* __restrict__ seg_base,
+                                                           uint32_t* __restrict__ seg_block,
+                                                           uint32_t* __restrict__ counters)
+{
+    __shared__ uint32_t lds16[kListThreads / kWave];
+    uint32_t carry = 0;
+    for (int b0 = 0; b0 < n_blocks; b0 += kListThreads) {
+        const int b = b0 + (int)threadIdx.x;
+        const uint32_t len = b < n_blocks ? block_ranges[2 * b + 1] - block_ranges[2 * b] : 0u;
+        const uint32_t ns = (len + kSegEntries - 1) / kSegEntries;
+        uint32_t total;
+        const uint32_t first = carry + wg_excl_scan_1024(ns, lds16, &total);
+        if (b < n_blocks) {
+            seg_base[b] = first;
+            for (uint32_t k = 0; k < ns; ++k) seg_block[first + k] = (uint32_t)b;
+        }
+        carry += total;
+    }
+    if (threadIdx.x == 0) {
+        seg_base[n_blocks] = carry;
+        counters[0] = carry;
+    }
+}
+
+// The entry range of segment s: block b, entries [e0, e1).
+struct Segment {
+    uint32_t b, e0, e1;
+};
+
+__device__ __forceinline__ Segment segment_of(uint32_t s, const uint32_t* __restrict__ seg_block,
+                                              const uint32_t* __restrict__ seg_base,
+                                              const uint32_t* __restrict__ block_ranges)
+{
+    Segment g;
+    g.b = seg_block[s];
+    const uint32_t j = s - seg_base[g.b];
+    const uint32_t end = block_ranges[2 * g.b + 1];
+    g.e0 = block_ranges[2 * g.b] + j * (uint32_t)kSegEntries;
+    g.e1 = min(g.e0 + (uint32_t)kSegEntries, end);
+    return g;
+}
+
+// The tile masks (and, for the emission, the Gaussian indices) of this wave's
+// kSegRounds x 64 entries of the segment; lanes past the segment get mask 0.
+// All loads are issued together, at indices clamped into the segment.
+template <bool kIds>
+__device__ __forceinline__ void load_segment(const Segment& g, const uint32_t* __restrict__ ent_key,
+                                             const uint32_t* __restrict__ ent_gid, uint32_t mask[kSegRounds],
+                                             uint32_t gid[kSegRounds])
+{
+    const uint32_t w0 = g.e0 + (threadIdx.x >> 6) * (kSegRounds * kWave) + __lane_id();
+    const uint32_t last = g.e1 - 1u;   // segments are never empty
+#pragma unroll
+    for (int r = 0; r < kSegRounds; ++r) {
+        const uint32_t e = min(w0 + r * kWave, last);
+        mask[r] = ent_key[e];
+        if (kIds) gid[r] = ent_gid[e];
+    }
+#pragma unroll
+    for (int r = 0; r < kSegRounds; ++r)
+        mask[r] = w0 + r * kWave <= last ? mask[r] & ((1u << kMaskBits) - 1u) : 0u;
+}
+
+// k_tile_count: per wave (a sub-segment of kSegRounds x 64 entries), the
+// entries meeting each tile of the block; lane l (< 16) writes the count of
+// tile l to wave_cnt[(4 s + wave) * 16 + l]. Tile-major, so that a single count
+// is live at a time.
+__global__ __launch_bounds__(kBlock) void k_tile_count(const uint32_t* __restrict__ ent_key,
+                                                       const uint32_t* __restrict__ block_ranges,
+                                                       const uint32_t* __restrict__ seg_base,
+                                                       const uint32_t* __restrict__ seg_block,
+                                                       const uint32_t* __restrict__ counters,
+                                                       uint32_t* __restrict__ wave_cnt)
+{
+    const uint32_t s = blockIdx.x;
+    if (s >= counters[0]) return;
+    const Segment g = segment_of(s, seg_block, seg_base, block_ranges);
+    uint32_t mask[kSegRounds], gid[kSegRounds];
+    load_segment<false>(g, ent_key, nullptr, mask, gid);
+    const int lane = __lane_id();
+    uint32_t mine = 0;
+#pragma unroll
+    for (int l = 0; l < kBlockTiles; ++l) {
+        uint32_t c = 0;
+#pragma unroll
+        for (int r = 0; r < kSegRounds; ++r) c += (uint32_t)__popcll(__ballot((mask[r] >> l) & 1u));
+        // c is uniform: take it as such before the per-lane select
+        mine = lane == l ? (uint32_t)__builtin_amdgcn_readfirstlane(c) : mine;
+    }
+    if (lane < kBlockTiles) wave_cnt[((size_t)s * kSubSegs + (threadIdx.x >> 6)) * kBlockTiles + lane] = mine;
+}
+
+// One wave per block: lanes 16 q + l hold tile l of sub-segment 4 r + q in
+// round r (the block's sub-segments are 4 per segment, in entry order).
+// wave_cnt becomes each sub-segment's exclusive offset inside the tile's list;
+// the tile's length goes to tile_ranges[2 t + 1].
+__global__ __launch_bounds__(kWave) void k_tile_scan(const uint32_t* __restrict__ seg_base, int n_blocks,
+                                                     int blocks_x, int tiles_x, int tiles_y,
+                                                     uint32_t* __restrict__ wave_cnt, uint32_t* __restrict__ tile_ranges)
+{
+    const int b = blockIdx.x;
+    if (b >= n_blocks) return;
+    const int lane = __lane_id(), q = lane >> 4, l = lane & 15;
+    const uint32_t s0 = seg_base[b] * kSubSegs, s1 = seg_base[b + 1] * kSubSegs;
+    uint32_t carry = 0;
+    for (uint32_t sb = s0; sb < s1; sb += 4) {
+        const uint32_t s = sb + (uint32_t)q;
+        const uint32_t v = s < s1 ? wave_cnt[(size_t)s * kBlockTiles + l] : 0u;
+        uint32_t x = v;
+        uint32_t y = __shfl_up(x, 16);
+        if (q >= 1) x += y;
+        y = __shfl_up(x, 32);
+        if (q >= 2) x += y;
+        if (s < s1) wave_cnt[(size_t)s * kBlockTiles + l] = carry + x - v;
+        carry += __shfl(x, 48 + l);
+    }
+    const int tx = kBlockDim * (b % blocks_x) + (l & 3), ty = kBlockDim * (b / blocks_x) + (l >> 2);
+    if (q == 0 && tx < tiles_x && ty < tiles_y) tile_ranges[2 * ((int64_t)ty * tiles_x + tx) + 1] = carry;
+}
+
+// One workgroup: exclusive scan of the tile lengths in tile order, written as
+// [start, end) ranges. Pairs over capacity (the preprocess's count, or the
+// lengths' sum) leave every range empty and raise counters[1], which stops the
+// emission.
+__global__ __launch_bounds__(kListThreads) void k_tile_starts(int n_tiles, PairCount pairs, uint64_t capacity,
+                                                              uint32_t* __restrict__ tile_ranges,
+                                                              uint32_t* __restrict__ counters)
+{
+    __shared__ uint32_t lds16[kListThreads / kWave];
+    __shared__ int over;
+    if (threadIdx.x == 0) over = pairs.overflow() ? 1 : 0;
+    uint64_t carry = 0;
+    for (int t0 = 0; t0 < n_tiles; t0 += kListThreads) {
+        const int t = t0 + (int)threadIdx.x;
+        const uint32_t len = t < n_tiles ? tile_ranges[2 * t + 1] : 0u;
+        uint32_t total;
+        const uint32_t before = wg_excl_scan_1024(len, lds16, &total);   // also orders `over`
+        const uint64_t start = carry + before;
+        if (t < n_tiles) {
+            if (start + len > capacity) over = 1;
+            tile_ranges[2 * t] = (uint32_t)start;
+            tile_ranges[2 * t + 1] = (uint32_t)(start + len);
+        }
+        carry += total;
+    }
+    __syncthreads();
+    if (over) {
+        for (int t = threadIdx.x; t < n_tiles; t += kListThreads) tile_ranges[2 * t] = tile_ranges[2 * t + 1] = 0u;
+    }
+    if (threadIdx.x == 0) counters[1] = over ? 1u : 0u;
+}
+
+template <bool kTileIds>
+__global__ __launch_bounds__(kBlock) void k_tile_emit(const uint32_t* __restrict__ ent_key,
+                                                      const uint32_t* __restrict__ ent_gid,
+                                                      const uint32_t* __restrict__ block_ranges,
+                                                      const uint32_t* __restrict__ seg_base,
+                                                      const uint32_t* __restrict__ seg_block,
+                                                      const uint32_t* __restrict__ counters, int blocks_x, int tiles_x,
+                                                      const uint32_t* __restrict__ wave_off,
+                                                      const uint32_t* __restrict__ tile_ranges,
+                                                      uint32_t* __restrict__ values, uint32_t* __restrict__ tile_ids)
+{
+    const uint32_t s = blockIdx.x;
+    if (s >= counters[0] || counters[1] != 0u) return;
+    const Segment g = segment_of(s, seg_block, seg_base, block_ranges);
+    const int bx = (int)(g.b % (uint32_t)blocks_x), by = (int)(g.b / (uint32_t)blocks_x);
+    const int lane = __lane_id();
+    // lane l: this wave's offset inside the list of tile l
+    const uint32_t base_l =
+        lane < kBlockTiles ? wave_off[((size_t)s * kSubSegs + (threadIdx.x >> 6)) * kBlockTiles + lane] : 0u;
+    uint32_t mask[kSegRounds], gid[kSegRounds];
+    load_segment<true>(g, ent_key, ent_gid, mask, gid);
+    const uint64_t below = (1ull << lane) - 1ull;
+    // tile-major: one running offset live at a time
+#pragma unroll
+    for (int l = 0; l < kBlockTiles; ++l) {
+        const uint32_t tile = (uint32_t)((kBlockDim * by + (l >> 2)) * tiles_x + kBlockDim * bx + (l & 3));
+        uint32_t m_any = 0;
+#pragma unroll
+        for (int r = 0; r < kSegRounds; ++r) m_any |= (mask[r] >> l) & 1u;
+        if (__ballot(m_any) == 0) continue;
+        // the tile is inside the grid: some entry meets it
+        uint32_t off = tile_ranges[2 * tile] + __builtin_amdgcn_readlane(base_l, l);
+#pragma unroll
+        for (int r = 0; r < kSegRounds; ++r) {
+            const bool on = (mask[r] >> l) & 1u;
+            const uint64_t m = __ballot(on);
+            // inside the tile's range: the counts are those k_tile_count took,
+            // and k_tile_starts let no range past the capacity
+            if (on) {
+                const uint32_t pos = off + (uint32_t)__popcll(m & below);
+                values[pos] = gid[r];
+                if (kTileIds) tile_ids[pos] = tile;
+            }
+            off += (uint32_t)__popcll(m);
+        }
     }
 }
 
@@ -503,88 +791,90 @@ hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_spla
     return hipSuccess;
 }
 
-hipError_t launch_pair_offsets(int64_t n, const Workspace& ws, hipStream_t s)
+int blocks_x_of(const Cam& cam) { return (cam.tiles_x + kBlockDim - 1) / kBlockDim; }
+int blocks_y_of(const Cam& cam) { return (cam.tiles_y + kBlockDim - 1) / kBlockDim; }
+int64_t segment_bound(const Cam& cam, uint64_t capacity)
+{
+    return div_up((int64_t)capacity, kSegEntries) + (int64_t)blocks_x_of(cam) * blocks_y_of(cam);
+}
+
+hipError_t launch_entry_offsets(int64_t n, PairCount pairs, const Workspace& ws, hipStream_t s)
 {
     const int nb = (int)div_up(n, kDupChunk);
-    hipLaunchKernelGGL(k_pair_partial, dim3(nb), dim3(kBlock), 0, s, ws.sorted_rect, n, ws.scan_part);
-    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kBlock), 0, s, ws.scan_part, nb);
+    hipLaunchKernelGGL(k_entry_partial, dim3(nb), dim3(kBlock), 0, s, ws.sorted_rect, n, ws.scan_part);
+    hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kBlock), 0, s, ws.scan_part, nb, pairs, ws.entry_count);
     return hipGetLastError();
 }
 
-hipError_t launch_duplicate(const Cam& cam, int64_t n, const uint32_t* order, const Workspace& ws,
-                            PairCount pairs, TileKeys keys_out, uint32_t* vals_out, hipStream_t s)
+// Bits of the block id.
+static int block_bits(const Cam& cam)
 {
-    const int nb = (int)div_up(n, kDupChunk);
-    if (keys_out.narrow)
-        hipLaunchKernelGGL(k_duplicate<uint16_t>, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
-                           cam.tiles_x, pairs, static_cast<uint16_t*>(keys_out.p), vals_out);
-    else
-        hipLaunchKernelGGL(k_duplicate<uint32_t>, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
-                           cam.tiles_x, pairs, static_cast<uint32_t*>(keys_out.p), vals_out);
-    return hipGetLastError();
-}
-
-// Bits of the tile id, and how they are split over passes of at most 8 bits.
-static int tile_bits(const Cam& cam)
-{
-    const uint32_t n_tiles = (uint32_t)cam.tiles_x * (uint32_t)cam.tiles_y;
+    const uint32_t nb = (uint32_t)blocks_x_of(cam) * (uint32_t)blocks_y_of(cam);
     int bits = 0;
-    while (bits < 32 && ((n_tiles - 1) >> bits) != 0) ++bits;
+    while (bits < 32 && ((nb - 1) >> bits) != 0) ++bits;
     return bits;
 }
 
-int tile_sort_passes(const Cam& cam) { return (tile_bits(cam) + 7) / 8; }
+bool blocks_supported(const Cam& cam) { return block_bits(cam) <= 32 - kMaskBits; }
 
-bool tile_keys_narrow(const Cam& cam) { return (int64_t)cam.tiles_x * cam.tiles_y <= 65536; }
-
-template <typename KeyT>
-static hipError_t tile_sort_t(const Cam& cam, PairCount num_pairs, const Workspace& ws, uint32_t* values,
-                              uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s)
+hipError_t launch_block_entries(const Cam& cam, int64_t n, const uint32_t* order, PairCount entries,
+                                const Workspace& ws, hipStream_t s)
 {
-    const int bits = tile_bits(cam);
+    const int nb = (int)div_up(n, kDupChunk);
+    hipLaunchKernelGGL(k_block_entries, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
+                       blocks_x_of(cam), entries, ws.pair_keys_a, ws.pair_vals_a);
+    return hipGetLastError();
+}
+
+// Stable LSD sort of the entries by block id, the key bits above the tile
+// mask (passes of <= 8 bits; none with a single block), then each block's
+// entry range and the segment table.
+hipError_t launch_block_sort(const Cam& cam, PairCount entries, const Workspace& ws, BlockEntries* out, hipStream_t s)
+{
+    const int n_blocks = blocks_x_of(cam) * blocks_y_of(cam);
+    const int bits = block_bits(cam);
     const int passes = (bits + 7) / 8;
-    KeyT* kbuf[2] = {reinterpret_cast<KeyT*>(ws.pair_keys_a), reinterpret_cast<KeyT*>(ws.pair_keys_b)};
+    uint32_t* kbuf[2] = {ws.pair_keys_a, ws.pair_keys_b};
     uint32_t* vbuf[2] = {ws.pair_vals_a, ws.pair_vals_b};
-    int src = 0, shift = 0;
+    int src = 0, shift = kMaskBits;
     for (int p = 0; p < passes; ++p) {
-        const bool last = p == passes - 1;
-        const int pb = (bits - shift + (passes - p) - 1) / (passes - p);   // remaining bits spread evenly
-        uint32_t* vout = last ? values : vbuf[src ^ 1];
-        hipError_t e;
-        if (last && tile_ids_out) {
-            // the caller's 32-bit tile ids double as the sorted keys for the ranges
-            e = radix_pass(kbuf[src], vbuf[src], num_pairs, shift, pb, tile_ids_out, vout, ws.hist, ws.digit_tot, s);
-            *sorted_tiles = TileKeys{tile_ids_out, false};
-        }
-        else {
-            e = radix_pass(kbuf[src], vbuf[src], num_pairs, shift, pb, kbuf[src ^ 1], vout, ws.hist, ws.digit_tot, s);
-            if (last) *sorted_tiles = TileKeys{kbuf[src ^ 1], sizeof(KeyT) == 2};
-        }
+        const int pb = (kMaskBits + bits - shift + (passes - p) - 1) / (passes - p);   // remaining bits spread evenly
+        const hipError_t e = radix_pass(kbuf[src], vbuf[src], entries, shift, pb, kbuf[src ^ 1], vbuf[src ^ 1],
+                                        ws.hist, ws.digit_tot, s);
         if (e != hipSuccess) return e;
         shift += pb;
         src ^= 1;
     }
-    return hipSuccess;
+    const dim3 grid((unsigned)div_up(n_blocks + 1, kBlock / kWave));
+    hipLaunchKernelGGL(k_ranges, grid, dim3(kBlock), 0, s, kbuf[src], kMaskBits, entries, n_blocks, ws.block_ranges);
+    hipLaunchKernelGGL(k_segments, dim3(1), dim3(kListThreads), 0, s, ws.block_ranges, n_blocks, ws.seg_base,
+                       ws.seg_block, ws.list_counters);
+    out->key = kbuf[src];
+    out->gid = vbuf[src];
+    return hipGetLastError();
 }
 
-hipError_t launch_tile_sort(const Cam& cam, PairCount num_pairs, const Workspace& ws, uint32_t* values,
-                            uint32_t* tile_ids_out, TileKeys* sorted_tiles, hipStream_t s)
+hipError_t launch_tile_lists(const Cam& cam, PairCount pairs, uint64_t capacity, const Workspace& ws,
+                             const BlockEntries& ent, uint32_t* values, uint32_t* tile_ids, uint32_t* tile_ranges,
+                             hipStream_t s)
 {
-    return tile_keys_narrow(cam) ? tile_sort_t<uint16_t>(cam, num_pairs, ws, values, tile_ids_out, sorted_tiles, s)
-                                 : tile_sort_t<uint32_t>(cam, num_pairs, ws, values, tile_ids_out, sorted_tiles, s);
-}
-
-hipError_t launch_ranges(const Cam& cam, PairCount num_pairs, TileKeys sorted_tiles, uint32_t* tile_ranges,
-                         hipStream_t s)
-{
+    const int bx = blocks_x_of(cam), n_blocks = bx * blocks_y_of(cam);
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    const dim3 grid((unsigned)div_up(n_tiles + 1, kBlock / kWave));
-    if (sorted_tiles.narrow)
-        hipLaunchKernelGGL(k_ranges<uint16_t>, grid, dim3(kBlock), 0, s, static_cast<const uint16_t*>(sorted_tiles.p),
-                           num_pairs, n_tiles, tile_ranges);
+    const dim3 segs((unsigned)segment_bound(cam, capacity));
+    hipLaunchKernelGGL(k_tile_count, segs, dim3(kBlock), 0, s, ent.key, ws.block_ranges, ws.seg_base, ws.seg_block,
+                       ws.list_counters, ws.seg_cnt);
+    hipLaunchKernelGGL(k_tile_scan, dim3(n_blocks), dim3(kWave), 0, s, ws.seg_base, n_blocks, bx, cam.tiles_x,
+                       cam.tiles_y, ws.seg_cnt, tile_ranges);
+    hipLaunchKernelGGL(k_tile_starts, dim3(1), dim3(kListThreads), 0, s, n_tiles, pairs, capacity, tile_ranges,
+                       ws.list_counters);
+    if (tile_ids)
+        hipLaunchKernelGGL(k_tile_emit<true>, segs, dim3(kBlock), 0, s, ent.key, ent.gid, ws.block_ranges,
+                           ws.seg_base, ws.seg_block, ws.list_counters, bx, cam.tiles_x, ws.seg_cnt, tile_ranges,
+                           values, tile_ids);
     else
-        hipLaunchKernelGGL(k_ranges<uint32_t>, grid, dim3(kBlock), 0, s, static_cast<const uint32_t*>(sorted_tiles.p),
-                           num_pairs, n_tiles, tile_ranges);
+        hipLaunchKernelGGL(k_tile_emit<false>, segs, dim3(kBlock), 0, s, ent.key, ent.gid, ws.block_ranges,
+                           ws.seg_base, ws.seg_block, ws.list_counters, bx, cam.tiles_x, ws.seg_cnt, tile_ranges,
+                           values, tile_ids);
     return hipGetLastError();
 }
 

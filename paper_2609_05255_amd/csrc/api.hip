@@ -214,7 +214,6 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     };
     const int64_t nn = n > 0 ? n : 1;
     const int64_t cap = capacity > 0 ? (int64_t)capacity : 1;
-    const int64_t sort_blocks = std::max(div_up(nn, kSortTile), div_up(cap, kSortTile));
     const int64_t n_blocks = cam ? (int64_t)blocks_x_of(*cam) * blocks_y_of(*cam) : 1;
     const int64_t segs = cam ? segment_bound(*cam, (uint64_t)cap) : 1;
     w.block_pairs = (uint32_t*)take(sizeof(uint32_t) * pair_count_slots(nn));
@@ -222,7 +221,9 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.keys_b = (uint32_t*)take(sizeof(uint32_t) * nn);
     w.vals_a = (uint32_t*)take(sizeof(uint32_t) * nn);
     w.vals_b = (uint32_t*)take(sizeof(uint32_t) * nn);
-    w.hist = (uint32_t*)take(sizeof(uint32_t) * kRadix * sort_blocks);
+    // the depth sort's 8-bit digits over n keys; the block sort's up to 9-bit
+    // digits over up to `capacity` entries
+    w.hist = (uint32_t*)take(sizeof(uint32_t) * std::max(kRadix * div_up(nn, kSortTile), 2 * kRadix * div_up(cap, kSortTile)));
     w.digit_tot = (uint32_t*)take(sizeof(uint32_t) * kRadix * 4);
     w.scan_part = (uint32_t*)take(sizeof(uint32_t) * (div_up(nn, kDupChunk) + 1));
     w.sorted_rect = (uint2*)take(sizeof(uint2) * nn);

@@ -53,11 +53,9 @@ static_assert(offsetof(gs_splat, power_min) == 36 && offsetof(gs_splat, depth) =
 // Stride 9 floats: dmean_x, dmean_y, dconic_a, dconic_b, dconic_c, dopacity, dcolor rgb.
 constexpr int kAccStride = 9;
 
-// Radix-sort geometry: 256 threads x 16 keys per workgroup for the depth sort
-// (n keys), x 24 for the tile sort (P pairs, many more keys: larger workgroup
-// tiles give longer runs per digit), digits of at most 8 bits.
+// Radix-sort geometry: 256 threads x 16 keys per workgroup, digits of at most
+// 8 bits for the depth sort (n keys) and 9 for the block sort (the entries).
 constexpr int kSortItems = 16;
-constexpr int kPairItems = 24;
 constexpr int kSortTile = kBlock * kSortItems;   // 4096
 constexpr int kRadix = 256;
 constexpr int kDupChunk = 1024;   // depth-ordered Gaussians per workgroup in entry emission

@@ -13,9 +13,11 @@
 // One radix pass = k_radix_hist (per-workgroup digit counts) + k_radix_scan
 // (exclusive offsets per digit over workgroups) + k_radix_scatter: each wave
 // ranks a contiguous slice of the workgroup's keys with ballot-matched digits
-// (no workgroup barrier per round), the workgroup reorders its keys (4096 in
-// the depth sort, 6144 in the block sort) by digit in LDS, and writes each
-// digit's run to consecutive global addresses.
+// (no workgroup barrier per round), the workgroup reorders its 4096 keys by
+// digit in LDS, and writes each digit's run to consecutive global addresses.
+// The grids are sized for the most keys a call can meet (the capacity, for
+// the block entries); workgroups past the device-side count do nothing, and
+// the scan reads only the workgroups below it.
 #include "gs_internal.h"
 
 namespace gsr {
@@ -75,11 +77,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const KeyT* __restrict__ 
     constexpr int R = 1 << kBits;
     constexpr int kTile = kBlock * kItems;
     const uint64_t count = cnt.get();
-    if ((uint64_t)blockIdx.x * kTile >= count) {
-        // a workgroup past the keys (the grid is sized for the capacity)
-        if (threadIdx.x < R) hist[(size_t)threadIdx.x * nblocks + blockIdx.x] = 0;
-        return;
-    }
+    if ((uint64_t)blockIdx.x * kTile >= count) return;   // past the keys: the scan does not read it
     // 16 copies of the counts (per wave and lane % 4): a skewed digit, such as
     // the exponent byte of the depth keys, then meets at most 16 lanes of an
     // instruction on one counter
@@ -101,8 +99,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const KeyT* __restrict__ 
         if (idx < count) atomicAdd(&h[copy][(k[r] >> shift) & (R - 1)], 1u);
     }
     __syncthreads();
-    const int d = threadIdx.x;
-    if (d < R) {
+    for (int d = threadIdx.x; d < R; d += kBlock) {
         uint32_t c = 0;
 #pragma unroll
         for (int w = 0; w < 16; ++w) c += h[w][d];
@@ -110,15 +107,17 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const KeyT* __restrict__ 
     }
 }
 
-// One workgroup per digit: exclusive scan of that digit's counts over workgroups.
-__global__ __launch_bounds__(kBlock) void k_radix_scan(uint32_t* __restrict__ hist, int nblocks,
-                                                       uint32_t* __restrict__ digit_tot)
+// One workgroup per digit: exclusive scan of that digit's counts over the
+// workgroups that hold keys (the first ceil(count / tile) of the nblocks).
+__global__ __launch_bounds__(kBlock) void k_radix_scan(uint32_t* __restrict__ hist, int nblocks, PairCount cnt,
+                                                       int tile, uint32_t* __restrict__ digit_tot)
 {
     __shared__ uint32_t lds4[4];
     uint32_t* row = hist + (size_t)blockIdx.x * nblocks;
-    const int per = (nblocks + kBlock - 1) / kBlock;
+    const int active = (int)min((uint64_t)nblocks, (cnt.get() + (uint64_t)tile - 1) / (uint64_t)tile);
+    const int per = (active + kBlock - 1) / kBlock;
     const int start = threadIdx.x * per;
-    const int end = min(start + per, nblocks);
+    const int end = min(start + per, active);
     uint32_t sum = 0;
     for (int k = start; k < end; ++k) sum += row[k];
     uint32_t total;
@@ -153,11 +152,24 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict
     const uint64_t count = cnt.get();
     if ((uint64_t)blockIdx.x * kTile >= count) return;   // past the keys: nothing to move
     const int t = threadIdx.x, wave = t >> 6, lane = __lane_id();
-    const uint32_t dt = t < R ? digit_tot[t] : 0u;
-    const uint32_t dbase = block_excl_scan(dt, lds4, nullptr);
-    if (t < R) {
-        gbase[t] = dbase + hist[(size_t)t * nblocks + blockIdx.x];
-        for (int w = 0; w < 4; ++w) wcnt[w][t] = 0;
+    // digits t * kDPT + j (consecutive per thread)
+    constexpr int kDPT = R > kBlock ? R / kBlock : 1;
+    uint32_t dtv[kDPT], dsum = 0;
+#pragma unroll
+    for (int j = 0; j < kDPT; ++j) {
+        const int d = t * kDPT + j;
+        dtv[j] = d < R ? digit_tot[d] : 0u;
+        dsum += dtv[j];
+    }
+    uint32_t dbase = block_excl_scan(dsum, lds4, nullptr);
+#pragma unroll
+    for (int j = 0; j < kDPT; ++j) {
+        const int d = t * kDPT + j;
+        if (d < R) {
+            gbase[d] = dbase + hist[(size_t)d * nblocks + blockIdx.x];
+            for (int w = 0; w < 4; ++w) wcnt[w][d] = 0;
+        }
+        dbase += dtv[j];
     }
     __syncthreads();
     // rank within the wave's slice, in key order
@@ -186,16 +198,28 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict
         __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
-    uint32_t tot = 0;
-    if (t < R) {
-        for (int w = 0; w < 4; ++w) {
-            const uint32_t c = wcnt[w][t];
-            wcnt[w][t] = tot;
-            tot += c;
+    uint32_t tots[kDPT], tsum = 0;
+#pragma unroll
+    for (int j = 0; j < kDPT; ++j) {
+        const int d = t * kDPT + j;
+        uint32_t tot = 0;
+        if (d < R) {
+            for (int w = 0; w < 4; ++w) {
+                const uint32_t c = wcnt[w][d];
+                wcnt[w][d] = tot;
+                tot += c;
+            }
         }
+        tots[j] = tot;
+        tsum += tot;
     }
-    const uint32_t ls = block_excl_scan(t < R ? tot : 0u, lds4, nullptr);
-    if (t < R) lstart[t] = ls;
+    uint32_t ls = block_excl_scan(tsum, lds4, nullptr);
+#pragma unroll
+    for (int j = 0; j < kDPT; ++j) {
+        const int d = t * kDPT + j;
+        if (d < R) lstart[d] = ls;
+        ls += tots[j];
+    }
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
@@ -237,29 +261,30 @@ void radix_pass_t(const KeyT* keys_in, const uint32_t* vals_in, PairCount cnt, i
     const int nblocks = (int)std::max<int64_t>(div_up((int64_t)cnt.host, (int64_t)kBlock * kItems), 1);
     hipLaunchKernelGGL((k_radix_hist<kBits, kItems, KeyT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, cnt, shift,
                        hist, nblocks);
-    hipLaunchKernelGGL(k_radix_scan, dim3(1 << kBits), dim3(kBlock), 0, s, hist, nblocks, digit_tot);
+    hipLaunchKernelGGL(k_radix_scan, dim3(1 << kBits), dim3(kBlock), 0, s, hist, nblocks, cnt, kBlock * kItems,
+                       digit_tot);
     hipLaunchKernelGGL((k_radix_scatter<kBits, kItems, KeyT, KeyOutT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in,
                        vals_in, cnt, shift,
                        hist, nblocks, digit_tot, keys_out, vals_out, rect_src, rect_out);
 }
 
-// A tile-sort pass over `bits` (1..8) bits, chosen at run time.
-template <typename KeyT, typename KeyOutT>
-hipError_t radix_pass(const KeyT* keys_in, const uint32_t* vals_in, PairCount cnt, int shift, int bits,
-                      KeyOutT* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
+// A block-sort pass over `bits` (1..9) bits: 4096 keys per workgroup, so that
+// the 9-bit digit's LDS tables leave room for three workgroups per CU.
+constexpr int kBlockSortBits = 9;
+hipError_t block_radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, PairCount cnt, int shift, int bits,
+                            uint32_t* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
 {
     switch (bits) {
 #define GS_PASS(b)                                                                                                   \
     case b:                                                                                                          \
-        radix_pass_t<b, kPairItems>(keys_in, vals_in, cnt, shift, keys_out, vals_out, hist, digit_tot, s);        \
+        radix_pass_t<b, kSortItems>(keys_in, vals_in, cnt, shift, keys_out, vals_out, hist, digit_tot, s);        \
         break;
-        GS_PASS(1) GS_PASS(2) GS_PASS(3) GS_PASS(4) GS_PASS(5) GS_PASS(6) GS_PASS(7) GS_PASS(8)
+        GS_PASS(1) GS_PASS(2) GS_PASS(3) GS_PASS(4) GS_PASS(5) GS_PASS(6) GS_PASS(7) GS_PASS(8) GS_PASS(9)
 #undef GS_PASS
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
-
 
 // ---- block entries in depth order -------------------------------------------
 //
@@ -562,16 +587,30 @@ __device__ __forceinline__ uint32_t wg_excl_scan_1024(uint32_t v, uint32_t* lds1
 // Segment table: one workgroup. seg_base[b] = first segment of block b (and
 // seg_base[n_blocks] = their number), seg_block[s] = the block of segment s,
 // counters[0] = the number of segments.
-__global__ __launch_bounds__(kListThreads) void k_segments(const uint32_t* __restrict__ block_ranges, int n_blocks,
+__global__ __launch_bounds__(kListThreads) void k_segments(const uint32_t* __restrict__ block_count,
+                                                           uint32_t* __restrict__ block_ranges, int n_blocks,
                                                            uint32_t* __restrict__ seg_base,
                                                            uint32_t* __restrict__ seg_block,
                                                            uint32_t* __restrict__ counters)
 {
     __shared__ uint32_t lds16[kListThreads / kWave];
-    uint32_t carry = 0;
+    uint32_t carry = 0, ecarry = 0;
     for (int b0 = 0; b0 < n_blocks; b0 += kListThreads) {
         const int b = b0 + (int)threadIdx.x;
-        const uint32_t len = b < n_blocks ? block_ranges[2 * b + 1] - block_ranges[2 * b] : 0u;
+        uint32_t len = 0;
+        if (block_count) {
+            // the ranges follow from the counts (a single-pass block sort's digit totals)
+            len = b < n_blocks ? block_count[b] : 0u;
+            uint32_t etotal;
+            const uint32_t start = ecarry + wg_excl_scan_1024(len, lds16, &etotal);
+            if (b < n_blocks) {
+                block_ranges[2 * b] = start;
+                block_ranges[2 * b + 1] = start + len;
+            }
+            ecarry += etotal;
+        } else if (b < n_blocks) {
+            len = block_ranges[2 * b + 1] - block_ranges[2 * b];
+        }
         const uint32_t ns = (len + kSegEntries - 1) / kSegEntries;
         uint32_t total;
         const uint32_t first = carry + wg_excl_scan_1024(ns, lds16, &total);
@@ -655,10 +694,11 @@ __global__ __launch_bounds__(kBlock) void k_tile_count(const uint32_t* __restric
     if (lane < kBlockTiles) wave_cnt[((size_t)s * kSubSegs + (threadIdx.x >> 6)) * kBlockTiles + lane] = mine;
 }
 
-// One wave per block: lanes 16 q + l hold tile l of sub-segment 4 r + q in
-// round r (the block's sub-segments are 4 per segment, in entry order).
-// wave_cnt becomes each sub-segment's exclusive offset inside the tile's list;
-// the tile's length goes to tile_ranges[2 t + 1].
+// One wave per block: lane 16 q + l holds tile l of the q-th quarter of the
+// block's sub-segments (4 per segment, in entry order): it sums its quarter's
+// counts (loads issued together), the quarters are scanned across q, and a
+// second sweep turns wave_cnt into each sub-segment's exclusive offset inside
+// the tile's list. The tile's length goes to tile_ranges[2 t + 1].
 __global__ __launch_bounds__(kWave) void k_tile_scan(const uint32_t* __restrict__ seg_base, int n_blocks,
                                                      int blocks_x, int tiles_x, int tiles_y,
                                                      uint32_t* __restrict__ wave_cnt, uint32_t* __restrict__ tile_ranges)
@@ -667,20 +707,36 @@ __global__ __launch_bounds__(kWave) void k_tile_scan(const uint32_t* __restrict_
     if (b >= n_blocks) return;
     const int lane = __lane_id(), q = lane >> 4, l = lane & 15;
     const uint32_t s0 = seg_base[b] * kSubSegs, s1 = seg_base[b + 1] * kSubSegs;
-    uint32_t carry = 0;
-    for (uint32_t sb = s0; sb < s1; sb += 4) {
-        const uint32_t s = sb + (uint32_t)q;
-        const uint32_t v = s < s1 ? wave_cnt[(size_t)s * kBlockTiles + l] : 0u;
-        uint32_t x = v;
-        uint32_t y = __shfl_up(x, 16);
-        if (q >= 1) x += y;
-        y = __shfl_up(x, 32);
-        if (q >= 2) x += y;
-        if (s < s1) wave_cnt[(size_t)s * kBlockTiles + l] = carry + x - v;
-        carry += __shfl(x, 48 + l);
+    const uint32_t per = (s1 - s0 + 3) / 4;
+    const uint32_t a0 = min(s0 + per * q, s1), a1 = min(a0 + per, s1);
+    uint32_t sum = 0;
+    for (uint32_t sb = a0; sb < a1; sb += 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = sb + k < a1 ? wave_cnt[(size_t)(sb + k) * kBlockTiles + l] : 0u;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) sum += v[k];
+    }
+    // exclusive scan of the quarter sums across q (lanes l, l + 16, l + 32, l + 48)
+    uint32_t x = sum;
+    uint32_t y = __shfl_up(x, 16);
+    if (q >= 1) x += y;
+    y = __shfl_up(x, 32);
+    if (q >= 2) x += y;
+    const uint32_t total = __shfl(x, 48 + l);
+    uint32_t run = x - sum;
+    for (uint32_t sb = a0; sb < a1; sb += 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = sb + k < a1 ? wave_cnt[(size_t)(sb + k) * kBlockTiles + l] : 0u;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            if (sb + k < a1) wave_cnt[(size_t)(sb + k) * kBlockTiles + l] = run;
+            run += v[k];
+        }
     }
     const int tx = kBlockDim * (b % blocks_x) + (l & 3), ty = kBlockDim * (b / blocks_x) + (l >> 2);
-    if (q == 0 && tx < tiles_x && ty < tiles_y) tile_ranges[2 * ((int64_t)ty * tiles_x + tx) + 1] = carry;
+    if (q == 0 && tx < tiles_x && ty < tiles_y) tile_ranges[2 * ((int64_t)ty * tiles_x + tx) + 1] = total;
 }
 
 // One workgroup: exclusive scan of the tile lengths in tile order, written as
@@ -827,28 +883,35 @@ hipError_t launch_block_entries(const Cam& cam, int64_t n, const uint32_t* order
 }
 
 // Stable LSD sort of the entries by block id, the key bits above the tile
-// mask (passes of <= 8 bits; none with a single block), then each block's
-// entry range and the segment table.
+// mask (passes of <= 9 bits; none with a single block), then each block's
+// entry range (the digit totals of a single pass, else a search of the sorted
+// keys) and the segment table.
 hipError_t launch_block_sort(const Cam& cam, PairCount entries, const Workspace& ws, BlockEntries* out, hipStream_t s)
 {
     const int n_blocks = blocks_x_of(cam) * blocks_y_of(cam);
     const int bits = block_bits(cam);
-    const int passes = (bits + 7) / 8;
+    const int passes = (bits + kBlockSortBits - 1) / kBlockSortBits;
     uint32_t* kbuf[2] = {ws.pair_keys_a, ws.pair_keys_b};
     uint32_t* vbuf[2] = {ws.pair_vals_a, ws.pair_vals_b};
     int src = 0, shift = kMaskBits;
     for (int p = 0; p < passes; ++p) {
         const int pb = (kMaskBits + bits - shift + (passes - p) - 1) / (passes - p);   // remaining bits spread evenly
-        const hipError_t e = radix_pass(kbuf[src], vbuf[src], entries, shift, pb, kbuf[src ^ 1], vbuf[src ^ 1],
-                                        ws.hist, ws.digit_tot, s);
+        const hipError_t e = block_radix_pass(kbuf[src], vbuf[src], entries, shift, pb, kbuf[src ^ 1],
+                                              vbuf[src ^ 1], ws.hist, ws.digit_tot, s);
         if (e != hipSuccess) return e;
         shift += pb;
         src ^= 1;
     }
-    const dim3 grid((unsigned)div_up(n_blocks + 1, kBlock / kWave));
-    hipLaunchKernelGGL(k_ranges, grid, dim3(kBlock), 0, s, kbuf[src], kMaskBits, entries, n_blocks, ws.block_ranges);
-    hipLaunchKernelGGL(k_segments, dim3(1), dim3(kListThreads), 0, s, ws.block_ranges, n_blocks, ws.seg_base,
-                       ws.seg_block, ws.list_counters);
+    if (passes == 1) {
+        hipLaunchKernelGGL(k_segments, dim3(1), dim3(kListThreads), 0, s, ws.digit_tot, ws.block_ranges, n_blocks,
+                           ws.seg_base, ws.seg_block, ws.list_counters);
+    } else {
+        const dim3 grid((unsigned)div_up(n_blocks + 1, kBlock / kWave));
+        hipLaunchKernelGGL(k_ranges, grid, dim3(kBlock), 0, s, kbuf[src], kMaskBits, entries, n_blocks,
+                           ws.block_ranges);
+        hipLaunchKernelGGL(k_segments, dim3(1), dim3(kListThreads), 0, s, (const uint32_t*)nullptr,
+                           ws.block_ranges, n_blocks, ws.seg_base, ws.seg_block, ws.list_counters);
+    }
     out->key = kbuf[src];
     out->gid = vbuf[src];
     return hipGetLastError();

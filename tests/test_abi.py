@@ -58,6 +58,35 @@ def test_workspace_size(gs):
         gs.gs_workspace_size(10, 64, 64, 10, 7)
     with pytest.raises(gs.GsError):
         gs.gs_workspace_size(10, 64, 64, 1 << 32, gs.GS_APP_SH3)
+    # the bin-sort's per-block buffers (4x4-tile blocks, and the segment table
+    # bounded by capacity / 2048 + blocks) grow with the image
+    big = gs.gs_workspace_size(1000, 4096, 4096, 10_000, gs.GS_APP_SH3)
+    assert big - a >= 4 * 2 * (256 * 256 - 1)
+
+
+def test_bin_sort_workspace_follows_the_image(gs):
+    # a workspace sized for a small image is too small for a large one
+    lib = gs.lib()
+    pre = gs.Preprocessed(FAKE, FAKE, FAKE, FAKE)
+    small = gs.gs_workspace_size(10, 64, 48, 100, gs.GS_APP_SH3)
+    large = gs.gs_workspace_size(10, 4096, 4096, 100, gs.GS_APP_SH3)
+    assert large > small
+    cam = _camera(gs, width=4096, height=4096)
+    st = lib.gs_bin_sort(C.byref(cam), C.byref(pre), 10, 10, 100, C.c_void_p(FAKE), None, C.c_void_p(FAKE),
+                         C.c_void_p(FAKE * 256), small, None)
+    assert st == gs.GS_ERR_CAPACITY and b"workspace" in lib.gs_last_error()
+
+
+def test_bin_sort_rejects_more_than_65536_blocks(gs):
+    # a block id shares a 32-bit key with the 16-bit mask of its tiles: at most
+    # 65536 blocks of 4x4 tiles (1025 x 1025 tiles need 257 x 257 blocks)
+    lib = gs.lib()
+    pre = gs.Preprocessed(FAKE, FAKE, FAKE, FAKE)
+    for side, want in ((16384, gs.GS_ERR_CAPACITY), (16400, gs.GS_ERR_UNSUPPORTED)):
+        cam = _camera(gs, width=side, height=side)
+        st = lib.gs_bin_sort(C.byref(cam), C.byref(pre), 10, 10, 100, C.c_void_p(FAKE), None, C.c_void_p(FAKE),
+                             C.c_void_p(FAKE * 256), 1 << 20, None)
+        assert st == want, (side, st, lib.gs_last_error())
 
 
 def _camera(gs, **kw):

@@ -228,10 +228,10 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.scan_part = (uint32_t*)take(sizeof(uint32_t) * (div_up(nn, kDupChunk) + 1));
     w.sorted_rect = (uint2*)take(sizeof(uint2) * nn);
     w.entry_count = (uint64_t*)take(sizeof(uint64_t));
-    w.pair_keys_a = (uint32_t*)take(sizeof(uint32_t) * cap);
-    w.pair_vals_a = (uint32_t*)take(sizeof(uint32_t) * cap);
-    w.pair_keys_b = (uint32_t*)take(sizeof(uint32_t) * cap);
-    w.pair_vals_b = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.entry_keys_a = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.entry_vals_a = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.entry_keys_b = (uint32_t*)take(sizeof(uint32_t) * cap);
+    w.entry_vals_b = (uint32_t*)take(sizeof(uint32_t) * cap);
     w.block_ranges = (uint32_t*)take(sizeof(uint32_t) * 2 * n_blocks);
     w.seg_base = (uint32_t*)take(sizeof(uint32_t) * (n_blocks + 1));
     w.seg_block = (uint32_t*)take(sizeof(uint32_t) * segs);

@@ -78,15 +78,15 @@ struct Workspace {
     uint32_t* keys_b;        // [n]
     uint32_t* vals_a;        // [n]               depth-sort values
     uint32_t* vals_b;        // [n]
-    uint32_t* hist;          // [256][max sort blocks]
+    uint32_t* hist;          // [digits][workgroups] of a radix pass (256 x n / 4096, 512 x capacity / 4096)
     uint32_t* digit_tot;     // [4 passes][256]   digit totals of each pass
     uint32_t* scan_part;     // [n / kDupChunk + 1] chunk sums of the entry-offset scan
     uint2* sorted_rect;      // [n]               tile rectangles in depth order (empty for culled)
     uint64_t* entry_count;   // [1]               block entries (0 when the pairs exceed the capacity)
-    uint32_t* pair_keys_a;   // [capacity]        entry keys: block id << 16 | tile mask
-    uint32_t* pair_vals_a;   // [capacity]        entry values: Gaussian index
-    uint32_t* pair_keys_b;   // [capacity]
-    uint32_t* pair_vals_b;   // [capacity]
+    uint32_t* entry_keys_a;  // [capacity]        entry keys: block id << 16 | tile mask
+    uint32_t* entry_vals_a;  // [capacity]        entry values: Gaussian index
+    uint32_t* entry_keys_b;  // [capacity]
+    uint32_t* entry_vals_b;  // [capacity]
     uint32_t* block_ranges;  // [blocks][2]       each block's entries
     uint32_t* seg_base;      // [blocks + 1]      first segment of each block
     uint32_t* seg_block;     // [segments]        block of each segment

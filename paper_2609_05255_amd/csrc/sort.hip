@@ -293,13 +293,14 @@ hipError_t block_radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, Pa
 // sorted by block id (stable, so depth order holds inside a block), and each
 // block's tile lists are cut out of its entries by ordered compaction.
 
-// Block rectangle (half-open, block units, packed like a tile rectangle) of a
-// tile rectangle; an empty rectangle stays empty.
+// Area of a packed rectangle (x0 | y0 << 16, x1 | y1 << 16, half-open).
 __device__ __forceinline__ uint32_t rect_area(uint2 r)
 {
     return ((r.y & 0xFFFFu) - (r.x & 0xFFFFu)) * ((r.y >> 16) - (r.x >> 16));
 }
 
+// Block rectangle (half-open, block units, packed like a tile rectangle) of a
+// tile rectangle; an empty rectangle stays empty.
 __device__ __forceinline__ uint2 block_rect(uint2 r)
 {
     if (rect_area(r) == 0) return make_uint2(0u, 0u);
@@ -878,7 +879,7 @@ hipError_t launch_block_entries(const Cam& cam, int64_t n, const uint32_t* order
 {
     const int nb = (int)div_up(n, kDupChunk);
     hipLaunchKernelGGL(k_block_entries, dim3(nb), dim3(kBlock), 0, s, order, ws.sorted_rect, n, ws.scan_part,
-                       blocks_x_of(cam), entries, ws.pair_keys_a, ws.pair_vals_a);
+                       blocks_x_of(cam), entries, ws.entry_keys_a, ws.entry_vals_a);
     return hipGetLastError();
 }
 
@@ -891,8 +892,8 @@ hipError_t launch_block_sort(const Cam& cam, PairCount entries, const Workspace&
     const int n_blocks = blocks_x_of(cam) * blocks_y_of(cam);
     const int bits = block_bits(cam);
     const int passes = (bits + kBlockSortBits - 1) / kBlockSortBits;
-    uint32_t* kbuf[2] = {ws.pair_keys_a, ws.pair_keys_b};
-    uint32_t* vbuf[2] = {ws.pair_vals_a, ws.pair_vals_b};
+    uint32_t* kbuf[2] = {ws.entry_keys_a, ws.entry_keys_b};
+    uint32_t* vbuf[2] = {ws.entry_vals_a, ws.entry_vals_b};
     int src = 0, shift = kMaskBits;
     for (int p = 0; p < passes; ++p) {
         const int pb = (kMaskBits + bits - shift + (passes - p) - 1) / (passes - p);   // remaining bits spread evenly

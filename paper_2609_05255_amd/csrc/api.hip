@@ -223,7 +223,8 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.vals_b = (uint32_t*)take(sizeof(uint32_t) * nn);
     // the depth sort's 8-bit digits over n keys; the block sort's up to 9-bit
     // digits over up to `capacity` entries
-    w.hist = (uint32_t*)take(sizeof(uint32_t) * std::max(kRadix * div_up(nn, kSortTile), 2 * kRadix * div_up(cap, kSortTile)));
+    w.hist = (uint32_t*)take(sizeof(uint32_t) * std::max(kRadix * div_up(nn, kSortTile),
+                                                         2 * kRadix * div_up(cap, kBlock * kBlockSortItems)));
     w.digit_tot = (uint32_t*)take(sizeof(uint32_t) * kRadix * 4);
     w.scan_part = (uint32_t*)take(sizeof(uint32_t) * (div_up(nn, kDupChunk) + 1));
     w.sorted_rect = (uint2*)take(sizeof(uint2) * nn);

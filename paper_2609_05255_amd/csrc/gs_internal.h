@@ -53,9 +53,11 @@ static_assert(offsetof(gs_splat, power_min) == 36 && offsetof(gs_splat, depth) =
 // Stride 9 floats: dmean_x, dmean_y, dconic_a, dconic_b, dconic_c, dopacity, dcolor rgb.
 constexpr int kAccStride = 9;
 
-// Radix-sort geometry: 256 threads x 16 keys per workgroup, digits of at most
-// 8 bits for the depth sort (n keys) and 9 for the block sort (the entries).
+// Radix-sort geometry: 256 threads x 16 keys per workgroup and digits of at
+// most 8 bits for the depth sort (n keys); x 32 keys and 9 bits for the block
+// sort (the entries).
 constexpr int kSortItems = 16;
+constexpr int kBlockSortItems = 32;
 constexpr int kSortTile = kBlock * kSortItems;   // 4096
 constexpr int kRadix = 256;
 constexpr int kDupChunk = 1024;   // depth-ordered Gaussians per workgroup in entry emission
@@ -78,7 +80,7 @@ struct Workspace {
     uint32_t* keys_b;        // [n]
     uint32_t* vals_a;        // [n]               depth-sort values
     uint32_t* vals_b;        // [n]
-    uint32_t* hist;          // [digits][workgroups] of a radix pass (256 x n / 4096, 512 x capacity / 4096)
+    uint32_t* hist;          // [digits][workgroups] of a radix pass (256 x n / 4096, 512 x capacity / 8192)
     uint32_t* digit_tot;     // [4 passes][256]   digit totals of each pass
     uint32_t* scan_part;     // [n / kDupChunk + 1] chunk sums of the entry-offset scan
     uint2* sorted_rect;      // [n]               tile rectangles in depth order (empty for culled)

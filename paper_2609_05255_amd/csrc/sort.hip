@@ -268,8 +268,8 @@ void radix_pass_t(const KeyT* keys_in, const uint32_t* vals_in, PairCount cnt, i
                        hist, nblocks, digit_tot, keys_out, vals_out, rect_src, rect_out);
 }
 
-// A block-sort pass over `bits` (1..9) bits: 4096 keys per workgroup, so that
-// the 9-bit digit's LDS tables leave room for three workgroups per CU.
+// A block-sort pass over `bits` (1..9) bits, 8192 keys per workgroup: twice
+// the depth sort's, for longer runs per digit among the 9-bit digits.
 constexpr int kBlockSortBits = 9;
 hipError_t block_radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, PairCount cnt, int shift, int bits,
                             uint32_t* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
@@ -277,7 +277,7 @@ hipError_t block_radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, Pa
     switch (bits) {
 #define GS_PASS(b)                                                                                                   \
     case b:                                                                                                          \
-        radix_pass_t<b, kSortItems>(keys_in, vals_in, cnt, shift, keys_out, vals_out, hist, digit_tot, s);        \
+        radix_pass_t<b, kBlockSortItems>(keys_in, vals_in, cnt, shift, keys_out, vals_out, hist, digit_tot, s);   \
         break;
         GS_PASS(1) GS_PASS(2) GS_PASS(3) GS_PASS(4) GS_PASS(5) GS_PASS(6) GS_PASS(7) GS_PASS(8) GS_PASS(9)
 #undef GS_PASS
@@ -497,7 +497,12 @@ __global__ __launch_bounds__(kBlock) void k_block_entries(const uint32_t* __rest
         for (int k = 0; k < kDupGroups; ++k) {
             const uint32_t p = p0 + kWave * k + lane;
             const uint32_t i = p - o[k];
-            const uint32_t q = i / w[k];
+            // i / w by a float reciprocal, corrected to the exact quotient (an
+            // entry index and a block-rectangle width are both below 2^16, so
+            // the estimate is off by at most one)
+            uint32_t q = (uint32_t)((float)i * __builtin_amdgcn_rcpf((float)w[k]));
+            q = q * w[k] > i ? q - 1u : q;
+            q = (q + 1u) * w[k] <= i ? q + 1u : q;
             const uint32_t bx = (org[k] & 0xFFFFu) + (i - q * w[k]);
             const uint32_t by = (org[k] >> 16) + q;
             const uint32_t out = gbase + p;
@@ -561,22 +566,23 @@ constexpr int kSubSegs = kBlock / kWave;                       // one sub-segmen
 constexpr int kListThreads = 1024;                             // single-workgroup scans
 static_assert(kBlockTiles == 16, "tile masks are 16 bits");
 
-// Exclusive scan of one u32 per thread over a 1024-thread workgroup.
-__device__ __forceinline__ uint32_t wg_excl_scan_1024(uint32_t v, uint32_t* lds16, uint32_t* total)
+// Exclusive scan of one value per thread over a 1024-thread workgroup.
+template <typename T>
+__device__ __forceinline__ T wg_excl_scan_1024(T v, T* lds16, T* total)
 {
     const int lane = __lane_id(), wave = threadIdx.x >> 6;
-    uint32_t x = v;
+    T x = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(x, o);
+        const T y = __shfl_up(x, o);
         if (lane >= o) x += y;
     }
     if (lane == 63) lds16[wave] = x;
     __syncthreads();
-    uint32_t before = 0, tot = 0;
+    T before = 0, tot = 0;
 #pragma unroll
     for (int w = 0; w < kListThreads / kWave; ++w) {
-        const uint32_t s = lds16[w];
+        const T s = lds16[w];
         if (w < wave) before += s;
         tot += s;
     }
@@ -741,27 +747,41 @@ __global__ __launch_bounds__(kWave) void k_tile_scan(const uint32_t* __restrict_
 }
 
 // One workgroup: exclusive scan of the tile lengths in tile order, written as
-// [start, end) ranges. Pairs over capacity (the preprocess's count, or the
+// [start, end) ranges. Each thread takes kStartsPer consecutive tiles per
+// sweep (one sweep covers 8,192 tiles: every image up to 1448 x 1448 tiles of
+// 16 pixels in one). Pairs over capacity (the preprocess's count, or the
 // lengths' sum) leave every range empty and raise counters[1], which stops the
 // emission.
+constexpr int kStartsPer = 8;
+
 __global__ __launch_bounds__(kListThreads) void k_tile_starts(int n_tiles, PairCount pairs, uint64_t capacity,
                                                               uint32_t* __restrict__ tile_ranges,
                                                               uint32_t* __restrict__ counters)
 {
-    __shared__ uint32_t lds16[kListThreads / kWave];
+    __shared__ uint64_t lds16[kListThreads / kWave];
     __shared__ int over;
     if (threadIdx.x == 0) over = pairs.overflow() ? 1 : 0;
-    uint64_t carry = 0;
-    for (int t0 = 0; t0 < n_tiles; t0 += kListThreads) {
-        const int t = t0 + (int)threadIdx.x;
-        const uint32_t len = t < n_tiles ? tile_ranges[2 * t + 1] : 0u;
-        uint32_t total;
-        const uint32_t before = wg_excl_scan_1024(len, lds16, &total);   // also orders `over`
-        const uint64_t start = carry + before;
-        if (t < n_tiles) {
-            if (start + len > capacity) over = 1;
-            tile_ranges[2 * t] = (uint32_t)start;
-            tile_ranges[2 * t + 1] = (uint32_t)(start + len);
+    uint64_t carry = 0;   // 64-bit sums: a sum past the capacity is detected, never wrapped
+    for (int t0 = 0; t0 < n_tiles; t0 += kListThreads * kStartsPer) {
+        const int tb = t0 + (int)threadIdx.x * kStartsPer;
+        uint32_t len[kStartsPer];
+        uint64_t sum = 0;
+#pragma unroll
+        for (int k = 0; k < kStartsPer; ++k) {
+            len[k] = tb + k < n_tiles ? tile_ranges[2 * (tb + k) + 1] : 0u;
+            sum += len[k];
+        }
+        uint64_t total;
+        const uint64_t before = wg_excl_scan_1024(sum, lds16, &total);   // also orders `over`
+        uint64_t start = carry + before;
+#pragma unroll
+        for (int k = 0; k < kStartsPer; ++k) {
+            if (tb + k < n_tiles) {
+                if (start + len[k] > capacity) over = 1;
+                tile_ranges[2 * (tb + k)] = (uint32_t)start;
+                tile_ranges[2 * (tb + k) + 1] = (uint32_t)(start + len[k]);
+            }
+            start += len[k];
         }
         carry += total;
     }

@@ -36,14 +36,17 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 FP32_VECTOR_PEAK_TFLOPS = 157.3  # published; counts packed-fp32 FMA
 FP32_UNPACKED_PEAK_TFLOPS = 78.6 # 256 CU x 4 SIMD x 16 lanes x 2 flops x 2.4 GHz (this build emits no packed fp32)
 # fp32 work of the blend per (pixel, list entry), counting an FMA as 2, by what
-# the method does with the entry (gs_render_work counts the entries):
+# the method does with the entry. The method visits, per pixel, every entry up
+# to the one that stops the pixel (forward) or up to its last contributor
+# (backward); gs_render_work counts them ("walked_fwd", "listed"):
 #   blended:   forward 24 (quadratic form 11, exp 2, alpha 2, transmittance 2,
 #              weight 1, colour 6); backward 62 (quadratic form 11, exp 2, alpha 2,
 #              transmittance 2, dcolour 4, dalpha 15, suffix sum 6, dopacity and
 #              the dL/dpower moments 20)
-#   evaluated but not blended (alpha below 1/255, or the stopping entry):
-#              15 (quadratic form 11, exp 2, alpha 2) in either direction
-#   skipped for the whole tile by the conservative alpha >= 1/255 box: 0
+#   visited but not blended (power > 0, alpha below 1/255, or the stopping
+#   entry): 15 (quadratic form 11, exp 2, alpha 2) in either direction. The
+#   kernels skip part of these for a whole tile with a conservative box test;
+#   the work counted is the method's, not what remains after that skip.
 BLEND_FLOPS = {"blend_fwd": (24.0, 15.0), "blend_bwd": (62.0, 15.0)}
 STAGES = {"preprocess": ("preprocess", "pair_count"),
           "sort": ("depth_sort", "entry_offsets", "block_entries", "block_sort", "tile_lists"),
@@ -206,14 +209,15 @@ def measure(gs, inputs, torch, cfg_name: str, kind: str, args, arch=None, train=
 
     # the blend's work per image (gs_render_work), over the cameras the steps visit
     steps_cams = [i % ncam for i in range(args.steps)]
-    counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    counts = torch.zeros(5, dtype=torch.int64, device=dev)
     work = {}
     for i in sorted(set(steps_cams)):
         fr.forward(cstructs[i], st, stream=stream, sync_pairs=False)
         gs.gs_render_work(cstructs[i], fr.pre, scene.n, fr.values, fr.ranges, counts, stream)
         work[i] = counts.cpu().numpy().astype(np.float64)
     w = np.mean([work[i] for i in steps_cams], axis=0)
-    work_avg = {"blended": int(w[0]), "listed": int(w[1]), "evaluated_bwd": int(w[2]), "evaluated_fwd": int(w[3])}
+    work_avg = {"blended": int(w[0]), "listed": int(w[1]), "evaluated_bwd": int(w[2]), "evaluated_fwd": int(w[3]),
+                "walked_fwd": int(w[4])}
 
     # per-kernel durations: the same K steps again with HIP events around every kernel
     timer = gs.Timer()
@@ -243,8 +247,8 @@ def measure(gs, inputs, torch, cfg_name: str, kind: str, args, arch=None, train=
     alu = {}
     for k, (f_blend, f_eval) in BLEND_FLOPS.items():
         if stage_ms.get(k, 0) > 0:
-            ev_k = w[2] if k == "blend_bwd" else w[3]
-            flops = f_blend * w[0] + f_eval * (ev_k - w[0])
+            visited = w[1] if k == "blend_bwd" else w[4]
+            flops = f_blend * w[0] + f_eval * (visited - w[0])
             ach = flops / (stage_ms[k] * 1e-3) / 1e12
             alu[k] = {"GFLOP": round(flops / 1e9, 3), "ms": round(stage_ms[k], 4), "TFLOP_s": round(ach, 3),
                       "frac": round(ach / FP32_VECTOR_PEAK_TFLOPS, 4),
@@ -351,8 +355,8 @@ def main():
         roofline = {"kernel": dominant, "bound": "alu", "achieved": a["TFLOP_s"], "peak": FP32_VECTOR_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": a["frac"], "traffic": None,
                     "peak_unpacked": FP32_UNPACKED_PEAK_TFLOPS, "frac_unpacked": a["frac_unpacked"],
-                    "work": "%s flops per launch from gs_render_work's counts: blended entries x %d, evaluated "
-                            "non-blended x %d" % (a["GFLOP"], *BLEND_FLOPS[dominant])}
+                    "work": "%s GFLOP per launch from gs_render_work's counts: blended entries x %d, other entries "
+                            "the method visits x %d" % (a["GFLOP"], *BLEND_FLOPS[dominant])}
     if roofline is not None and dominant in KERNEL_SOURCES:
         tb = recorded_traffic(dominant, ctx["cfg"].name, kind)
         roofline["traffic"] = None if tb is None else round(tb)

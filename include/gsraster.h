@@ -289,8 +289,11 @@ gs_status gs_render_fwd(const gs_camera* cam, const gs_preprocessed* pre, int64_
  *             the pixel's tile (those gs_render_bwd evaluates per pixel; it skips
  *             the others for the whole tile), blended ones included;
  *   counts[3] the same for gs_render_fwd: entries up to the one that stops the
- *             pixel (or the list's end).
- * Arguments as for gs_render_fwd; counts: [4] u64 device, 8-byte aligned,
+ *             pixel (or the list's end);
+ *   counts[4] entries the method visits in the forward, whatever the box:
+ *             up to and including the one that stops the pixel, else the
+ *             whole list (the per-pixel work of the Sec. 3.1 blend).
+ * Arguments as for gs_render_fwd; counts: [5] u64 device, 8-byte aligned,
  * overwritten. Asynchronous on stream.
  */
 gs_status gs_render_work(const gs_camera* cam, const gs_preprocessed* pre, int64_t n, const uint32_t* values,

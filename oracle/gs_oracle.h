@@ -141,13 +141,15 @@ int64_t orc_bin_sort(int64_t n, const int32_t* rect, const double* depth, const 
  * decisions, of the decision's relative distance from its threshold to a bound
  * on how far an fp32 evaluation in another operation order can move it (see
  * walk_pixel); above 1 every decision of the pixel is reproducible.
- * n_blended (nullable): per pixel, the number of entries composited. */
+ * n_blended (nullable): per pixel, the number of entries composited.
+ * n_walked (nullable): per pixel, the number of entries the blend visits: up
+ * to and including the one that stops it, else the whole list. */
 void orc_render_fwd_f32(const orc_camera* cam, int64_t n, const orc_pre* pre, const int64_t* ranges,
                         const int32_t* values, double* image, double* final_T, int32_t* n_contrib,
-                        double* margin, int32_t* n_blended);
+                        double* margin, int32_t* n_blended, int32_t* n_walked);
 void orc_render_fwd_f64(const orc_camera* cam, int64_t n, const orc_pre* pre, const int64_t* ranges,
                         const int32_t* values, double* image, double* final_T, int32_t* n_contrib,
-                        double* margin, int32_t* n_blended);
+                        double* margin, int32_t* n_blended, int32_t* n_walked);
 
 /* Gradients of sum(dL_dimage * image) w.r.t. all inputs; outputs overwritten. */
 int orc_render_bwd_f32(const orc_camera* cam, int64_t n, const double* means, const double* log_scales,

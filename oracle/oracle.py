@@ -89,7 +89,7 @@ def lib():
             f.argtypes = [C.POINTER(_Camera), i64, vp, vp, vp, vp, C.POINTER(_Appearance), C.POINTER(_Pre)]
             f.restype = C.c_int
             f = getattr(_lib, "orc_render_fwd" + sfx)
-            f.argtypes = [C.POINTER(_Camera), i64, C.POINTER(_Pre), vp, vp, vp, vp, vp, vp, vp]
+            f.argtypes = [C.POINTER(_Camera), i64, C.POINTER(_Pre), vp, vp, vp, vp, vp, vp, vp, vp]
             f.restype = None
             f = getattr(_lib, "orc_render_bwd" + sfx)
             f.argtypes = [C.POINTER(_Camera), i64, vp, vp, vp, vp, C.POINTER(_Appearance), C.POINTER(_Pre),
@@ -260,9 +260,10 @@ def bin_sort(cam, pre: Preprocessed):
     return values[:total], tile_of[:total], ranges
 
 
-def render_fwd(cam, pre: Preprocessed, ranges, values, mode: str = "f32", n_blended=None):
+def render_fwd(cam, pre: Preprocessed, ranges, values, mode: str = "f32", n_blended=None, n_walked=None):
     """(image[3][H][W], final_T[H][W], n_contrib[H][W], margin[H][W]); n_blended, if
-    given (int32 [H][W]), receives each pixel's number of composited entries."""
+    given (int32 [H][W]), receives each pixel's number of composited entries, and
+    n_walked its number of visited entries (the stopping one included)."""
     W, H = int(cam.width), int(cam.height)
     image = np.zeros((3, H, W))
     final_T = np.zeros((H, W))
@@ -273,7 +274,8 @@ def render_fwd(cam, pre: Preprocessed, ranges, values, mode: str = "f32", n_blen
     st = pre.struct()
     getattr(lib(), "orc_render_fwd_" + mode)(C.byref(camera_struct(cam)), pre["tiles"].size, C.byref(st),
                                              _p(ranges), _p(values), _p(image), _p(final_T), _p(n_contrib),
-                                             _p(margin), None if n_blended is None else _p(n_blended))
+                                             _p(margin), None if n_blended is None else _p(n_blended),
+                                             None if n_walked is None else _p(n_walked))
     return image, final_T, n_contrib, margin
 
 
@@ -317,9 +319,10 @@ def render(cam, scene, kind="sh3", sh_degree: int = 3, mode: str = "f32", dir_ex
     pre = preprocess(cam, scene, kind, sh_degree, mode, dir_exact, half_act)
     values, tile_of, ranges = bin_sort(cam, pre)
     n_blended = np.zeros((int(cam.height), int(cam.width)), np.int32)
-    image, final_T, n_contrib, margin = render_fwd(cam, pre, ranges, values, mode, n_blended)
+    n_walked = np.zeros((int(cam.height), int(cam.width)), np.int32)
+    image, final_T, n_contrib, margin = render_fwd(cam, pre, ranges, values, mode, n_blended, n_walked)
     return dict(pre=pre, values=values, tile_of=tile_of, ranges=ranges, image=image, final_T=final_T,
-                n_contrib=n_contrib, margin=margin, n_blended=n_blended)
+                n_contrib=n_contrib, margin=margin, n_blended=n_blended, n_walked=n_walked)
 
 
 def set_threads(k: int):

@@ -430,9 +430,10 @@ hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32
 // evaluated in the forward (up to the stop entry, or the list's end, whose
 // alpha >= 1/255 box meets the tile: the blend kernels skip the others for
 // the whole tile without a per-pixel test); evaluated entries before the last
-// blended one (those the backward evaluates); and that last position
-// (n_contrib). One wave per tile, 4 pixels per lane; per-wave sums, then one
-// 64-bit atomic per wave and counter.
+// blended one (those the backward evaluates); that last position
+// (n_contrib); and the entries the method visits in the forward (up to and
+// including the stop entry, or the whole list). One wave per tile, 4 pixels
+// per lane; per-wave sums, then one 64-bit atomic per wave and counter.
 __global__ __launch_bounds__(kWave) void k_blend_count(Cam cam, const gs_splat* __restrict__ splats,
                                                        const uint32_t* __restrict__ values,
                                                        const uint32_t* __restrict__ ranges,
@@ -451,14 +452,16 @@ __global__ __launch_bounds__(kWave) void k_blend_count(Cam cam, const gs_splat* 
     const float box_cx = (float)(tx * kTile) + 8.f, box_hx = 7.5f;
     const float box_cy = (float)(ty * kTile) + 8.f, box_hy = 7.5f;
     float T[kPix], py[kPix];
-    uint32_t blended[kPix], eval_fwd[kPix], eval_bwd[kPix], pending[kPix], last[kPix];
+    uint32_t blended[kPix], eval_fwd[kPix], eval_bwd[kPix], pending[kPix], last[kPix], walked[kPix];
 #pragma unroll
     for (int k = 0; k < kPix; ++k) {
         py[k] = (float)(y0 + kRowStep * k) + 0.5f;
         T[k] = (x < cam.width && (y0 + kRowStep * k) < cam.height) ? 1.f : -1.f;
-        blended[k] = eval_fwd[k] = eval_bwd[k] = pending[k] = last[k] = 0;
+        blended[k] = eval_fwd[k] = eval_bwd[k] = pending[k] = last[k] = walked[k] = 0;
     }
     for (uint32_t p = start; p < end; ++p) {
+#pragma unroll
+        for (int k = 0; k < kPix; ++k) walked[k] += T[k] > 0.f ? 1u : 0u;   // visited while blending
         const float4* rec = reinterpret_cast<const float4*>(splats + values[p]);
         const float4 w0 = rec[0], w1 = rec[1], w2 = rec[2];
         SplatReg s;
@@ -485,7 +488,7 @@ __global__ __launch_bounds__(kWave) void k_blend_count(Cam cam, const gs_splat* 
             last[k] = p - start + 1;
         }
     }
-    unsigned long long c[4] = {0, 0, 0, 0};
+    unsigned long long c[5] = {0, 0, 0, 0, 0};
 #pragma unroll
     for (int k = 0; k < kPix; ++k) {
         if (x >= cam.width || y0 + kRowStep * k >= cam.height) continue;
@@ -493,9 +496,10 @@ __global__ __launch_bounds__(kWave) void k_blend_count(Cam cam, const gs_splat* 
         c[1] += last[k];
         c[2] += eval_bwd[k];
         c[3] += eval_fwd[k];
+        c[4] += walked[k];
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 5; ++i) {
         unsigned long long v = c[i];
         for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
         if (lane == 0) atomicAdd(counts + i, v);
@@ -505,7 +509,7 @@ __global__ __launch_bounds__(kWave) void k_blend_count(Cam cam, const gs_splat* 
 hipError_t launch_blend_count(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                               const uint32_t* tile_ranges, uint64_t* counts, hipStream_t s)
 {
-    hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(counts), 8, 0u, s);
+    hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t*>(counts), 10, 0u, s);
     if (e != hipSuccess) return e;
     const int n_tiles = cam.tiles_x * cam.tiles_y;
     hipLaunchKernelGGL(k_blend_count, dim3(n_tiles), dim3(kWave), 0, s, cam, splats, values, tile_ranges,

@@ -242,7 +242,8 @@ def gs_render_fwd(cam: Camera, pre: Preprocessed, n: int, values, tile_ranges, i
 
 
 def gs_render_work(cam: Camera, pre: Preprocessed, n: int, values, tile_ranges, counts, stream=None):
-    """counts: int64 device tensor [4] (blended, listed, evaluated backward, evaluated forward)."""
+    """counts: int64 device tensor [5] (blended, listed, evaluated backward, evaluated forward,
+    visited forward)."""
     _check(lib().gs_render_work(C.byref(cam), C.byref(pre), n, _ptr(values), _ptr(tile_ranges), _ptr(counts),
                                 _stream(stream)))
 

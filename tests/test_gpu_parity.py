@@ -406,10 +406,10 @@ def test_device_pair_count(size):
 
 @pytest.mark.parametrize("case", ["tiny", "ragged", "medium"])
 def test_render_work_counts(case):
-    # gs_render_work: blended entries against the oracle's per-pixel count
-    # (exactly where no pixel is flagged; otherwise within the flagged pixels'
-    # list lengths), the listed entries equal to the sum of the GPU's own
-    # n_contrib, and evaluated counts between them
+    # gs_render_work: blended and visited entries against the oracle's
+    # per-pixel counts (exactly where no pixel is flagged; otherwise within the
+    # flagged pixels' list lengths), the listed entries equal to the sum of the
+    # GPU's own n_contrib, and evaluated counts between them
     if case == "medium":
         sc, cam = inputs.make_scene("medium"), inputs.make_cameras("medium")[3]
     else:
@@ -419,19 +419,24 @@ def test_render_work_counts(case):
     ref = orc.render(cam, sc, mode="f32")
     gpu = run_gpu(sc, cam)
     fr = gpu["frame"]
-    counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+    counts = torch.zeros(5, dtype=torch.int64, device="cuda")
     gs.gs_render_work(gs.camera_struct(cam), fr.pre, sc.n, fr.values, fr.ranges, counts)
     torch.cuda.synchronize()
-    blended, listed, ev_bwd, ev_fwd = (int(v) for v in counts.cpu().numpy())
-    say("  blended %d listed %d evaluated bwd %d fwd %d" % (blended, listed, ev_bwd, ev_fwd))
+    blended, listed, ev_bwd, ev_fwd, walked = (int(v) for v in counts.cpu().numpy())
+    say("  blended %d listed %d evaluated bwd %d fwd %d visited fwd %d" % (blended, listed, ev_bwd, ev_fwd, walked))
     assert listed == int(gpu["n_contrib"].astype(np.int64).sum())
     flagged = ref["margin"] <= 1.0
     ref_blended = int(ref["n_blended"].astype(np.int64).sum())
+    ref_walked = int(ref["n_walked"].astype(np.int64).sum())
+    tiles_x = (cam.width + 15) // 16
+    ys, xs = np.mgrid[0:cam.height, 0:cam.width]
+    lens = (ref["ranges"][:, 1] - ref["ranges"][:, 0])[(ys // 16) * tiles_x + xs // 16]
     slack = int(ref["n_contrib"][flagged].astype(np.int64).sum() + gpu["n_contrib"][flagged].astype(np.int64).sum())
     if not flagged.any():
-        assert blended == ref_blended
+        assert blended == ref_blended and walked == ref_walked
     assert abs(blended - ref_blended) <= slack
-    assert blended <= ev_bwd <= listed and ev_bwd <= ev_fwd
+    assert abs(walked - ref_walked) <= int(lens[flagged].astype(np.int64).sum())
+    assert blended <= ev_bwd <= listed and ev_bwd <= ev_fwd <= walked and listed <= walked
 
 
 # ---- decoder weights far from their initialisation -----------------------------------

@@ -484,6 +484,30 @@ def test_blended_counts(orc):
     assert np.array_equal(r1["n_blended"][clear], (alpha >= 1 / 255.0).astype(np.int32)[clear])
 
 
+def test_walked_counts(orc):
+    # the entries the blend visits per pixel: at least up to the last
+    # contributor, at most the whole list, the whole list where no entry stops
+    # the pixel (every pixel of the tiny scene). Four coincident near-opaque splats (alpha capped at 0.99 where
+    # they are centred): T goes 1 -> 1 - 0.99 -> below 1e-4 on the second, which
+    # stops the pixel, so it visits 2 entries and keeps 1
+    sc = inputs.make_scene("tiny")
+    cam = inputs.make_cameras("tiny")[0]
+    r = orc.render(cam, sc)
+    tx, _ = orc.tile_grid(cam)
+    ys, xs = np.mgrid[0:64, 0:64]
+    tile = (ys // 16) * tx + xs // 16
+    lens = (r["ranges"][:, 1] - r["ranges"][:, 0])[tile]
+    assert np.all(r["n_walked"] >= r["n_contrib"]) and np.all(r["n_walked"] <= lens)
+    # no pixel of this thin scene stops: each visits its whole list
+    assert np.array_equal(r["n_walked"], lens)
+    stack = scene_of([[0, 0, 0]] * 4, [[-1.0] * 3] * 4, [[1, 0, 0, 0]] * 4, [12.0] * 4)
+    r4 = orc.render(cam, stack)
+    cx, cy = (int(v) for v in r4["pre"]["mean2d"][:, 0])
+    assert r4["n_walked"][cy, cx] == 2 and r4["n_contrib"][cy, cx] == 1
+    far = (r4["n_contrib"] == 0)
+    assert np.array_equal(r4["n_walked"][far], (r4["ranges"][:, 1] - r4["ranges"][:, 0])[tile][far])
+
+
 @pytest.mark.parametrize("kind", ["sh3", "latent", "neural"])
 def test_results_do_not_depend_on_threads(orc, kind):
     # every sum of the oracle runs in an order fixed by the data (pairs in

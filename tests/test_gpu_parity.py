@@ -394,6 +394,18 @@ def test_device_pair_count(size):
     torch.cuda.synchronize()
     for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh"):
         assert int(torch.count_nonzero(getattr(small, k)[..., : sc.n]).item()) == 0, k
+    # a host-mode count that understates P, with a capacity to match it: the
+    # lists need more than the capacity, which is found on the device, and every
+    # range comes out empty (nothing is written past the capacity)
+    low = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_SH3, P // 2)
+    gs.gs_preprocess(cs, st.gaussians(), st.appearance(gs.GS_APP_SH3, 3), low.pre, low.workspace, low.ws_bytes,
+                     sync_pairs=False)
+    guard = torch.full((64,), -7, dtype=torch.int32, device="cuda")
+    values = torch.cat([low.values, guard])
+    gs.gs_bin_sort(cs, low.pre, sc.n, P // 2, P // 2, values, None, low.ranges, low.workspace, low.ws_bytes)
+    torch.cuda.synchronize()
+    assert int(low.ranges.abs().sum().item()) == 0
+    assert torch.equal(values[P // 2:], guard)
     # retry with room for every pair
     retry = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_SH3, P, want_tile_ids=True)
     retry.forward(cs, st, sync_pairs=False)

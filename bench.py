@@ -51,7 +51,7 @@ BLEND_FLOPS = {"blend_fwd": (24.0, 15.0), "blend_bwd": (62.0, 15.0)}
 STAGES = {"preprocess": ("preprocess", "pair_count"),
           "sort": ("depth_sort", "entry_offsets", "block_entries", "block_sort", "tile_lists"),
           "blend": ("blend_fwd",),
-          "backward": ("clear", "blend_bwd", "preprocess_bwd", "mlp_reduce")}
+          "backward": ("bwd_prep", "blend_bwd", "preprocess_bwd", "mlp_reduce")}
 
 
 # HBM traffic of a kernel, from memory-counter runs summarised under profiles/

@@ -307,6 +307,11 @@ gs_status gs_render_work(const gs_camera* cam, const gs_preprocessed* pre, int64
  * the preprocess per Gaussian; for LATENT_MLP also the decoder weights.
  * dL_dimage: [3][H][W] fp32 device. The pair-level accumulation uses float
  * atomics, so results vary in the last bits between runs.
+ * workspace: at least gs_workspace_size(n, width, height, ...) bytes for this
+ *   camera's image size (it holds the per-Gaussian accumulators and an order
+ *   of the tiles: images of up to 32768 tiles are walked longest list walk
+ *   first, which evens out the work per SIMD; the order does not change what
+ *   is computed).
  */
 gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
                         const gs_preprocessed* pre, const uint32_t* values, const uint32_t* tile_ranges,
@@ -393,9 +398,9 @@ gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t c
 enum {
     GS_KERNEL_PREPROCESS = 0, GS_KERNEL_PAIR_COUNT, GS_KERNEL_DEPTH_SORT, GS_KERNEL_ENTRY_OFFSETS,
     GS_KERNEL_BLOCK_ENTRIES, GS_KERNEL_BLOCK_SORT, GS_KERNEL_TILE_LISTS, GS_KERNEL_BLEND_FWD,
-    GS_KERNEL_CLEAR, GS_KERNEL_BLEND_BWD, GS_KERNEL_PREPROCESS_BWD, GS_KERNEL_MLP_REDUCE,
+    GS_KERNEL_BWD_PREP, GS_KERNEL_BLEND_BWD, GS_KERNEL_PREPROCESS_BWD, GS_KERNEL_MLP_REDUCE,
     GS_KERNEL_ADAM, GS_KERNEL_NEURAL_FOLD, GS_KERNEL_COUNT
-};
+};   /* GS_KERNEL_BWD_PREP: the backward's accumulator clear and its tile order */
 typedef struct gs_timer gs_timer;
 gs_status gs_timer_create(gs_timer** out);
 gs_status gs_timer_destroy(gs_timer* timer);

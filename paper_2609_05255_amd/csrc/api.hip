@@ -166,7 +166,7 @@ void resolve_pending(gs_timer* t)
 
 const char* const kKernelNames[GS_KERNEL_COUNT] = {
     "preprocess", "pair_count", "depth_sort", "entry_offsets", "block_entries", "block_sort", "tile_lists",
-    "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam", "neural_fold"};
+    "blend_fwd", "bwd_prep", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam", "neural_fold"};
 
 }  // namespace
 
@@ -239,6 +239,9 @@ Workspace layout_workspace(void* base, int64_t n, uint64_t capacity, int32_t kin
     w.seg_cnt = (uint32_t*)take(sizeof(uint32_t) * 16 * 4 * segs);
     w.list_counters = (uint32_t*)take(sizeof(uint32_t) * 2);
     w.acc = (float*)take(sizeof(float) * kAccStride * nn);
+    const int64_t n_tiles = cam ? (int64_t)cam->tiles_x * cam->tiles_y : 1;
+    w.walk_cls = (uint32_t*)take(sizeof(uint32_t) * n_tiles);
+    w.tile_order = (uint32_t*)take(sizeof(uint32_t) * n_tiles);
     w.mlp_part = (float*)take(kind == GS_APP_LATENT_MLP ? sizeof(float) * GS_MLP_WEIGHTS * kMlpPartials
                               : kind == GS_APP_NEURAL ? sizeof(float) * GS_NEURAL_MAX_WEIGHTS * kMlpPartials : 0);
     w.bytes = off;
@@ -508,21 +511,24 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
             GS_CHECK(grads->dbase_color && grads->dlobes, "dbase_color or dlobes is NULL");
         else GS_CHECK(grads->dlatent && grads->dmlp_w, "dlatent or dmlp_w is NULL");
     }
-    const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind, nullptr);
-    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
-    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind, nullptr);
-    hipStream_t s = static_cast<hipStream_t>(stream);
     const Cam c = make_cam(*cam);
+    const Workspace need = layout_workspace(nullptr, g->n, 0, app->kind, &c);
+    if ((st = check_workspace(workspace, workspace_bytes, need)) != GS_OK) return st;
+    const Workspace ws = layout_workspace(workspace, g->n, 0, app->kind, &c);
+    hipStream_t s = static_cast<hipStream_t>(stream);
     if (g->n == 0) {
         if (app->kind == GS_APP_LATENT_MLP) GS_HIP(launch_clear(grads->dmlp_w, GS_MLP_WEIGHTS, s));
         if (app->kind == GS_APP_NEURAL && grads->dmlp_w) GS_HIP(launch_clear(grads->dmlp_w, neural_weights(*app), s));
         return ok();
     }
-    timing_begin(GS_KERNEL_CLEAR, s);
+    const bool ordered = tile_order_supported(c);
+    timing_begin(GS_KERNEL_BWD_PREP, s);
     GS_HIP(launch_clear(ws.acc, (int64_t)kAccStride * g->n, s));
-    timing_end(GS_KERNEL_CLEAR, s);
+    if (ordered) GS_HIP(launch_tile_order(c, tile_ranges, n_contrib, ws.walk_cls, ws.tile_order, s));
+    timing_end(GS_KERNEL_BWD_PREP, s);
     timing_begin(GS_KERNEL_BLEND_BWD, s);
-    GS_HIP(launch_blend_bwd(c, pre->splats, values, tile_ranges, final_T, n_contrib, dL_dimage, ws.acc, s));
+    GS_HIP(launch_blend_bwd(c, pre->splats, values, tile_ranges, final_T, n_contrib, dL_dimage,
+                            ordered ? ws.tile_order : nullptr, ws.acc, s));
     timing_end(GS_KERNEL_BLEND_BWD, s);
     timing_begin(GS_KERNEL_PREPROCESS_BWD, s);
     GS_HIP(launch_preprocess_bwd(c, *g, *app, *pre, ws, *grads, s));

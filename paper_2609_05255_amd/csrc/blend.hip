@@ -228,11 +228,13 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                                                                     const float* __restrict__ final_T,
                                                                     const uint32_t* __restrict__ n_contrib,
                                                                     const float* __restrict__ dL_dimage,
+                                                                    const uint32_t* __restrict__ order,
                                                                     float* __restrict__ acc)
 {
     constexpr int kRowStep = 4;   // pixel k of a lane lies 4k rows below its first
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    const int tile = tile_of_block(blockIdx.x, n_tiles);
+    const int tile = order ? (blockIdx.x < (unsigned)n_tiles ? (int)order[blockIdx.x] : n_tiles)
+                           : tile_of_block(blockIdx.x, n_tiles);
     if (tile >= n_tiles) return;
     const int lane = __lane_id();
     const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
@@ -416,11 +418,95 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
 
 hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                             const uint32_t* tile_ranges, const float* final_T, const uint32_t* n_contrib,
-                            const float* dL_dimage, float* acc, hipStream_t s)
+                            const float* dL_dimage, const uint32_t* tile_order, float* acc, hipStream_t s)
 {
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    hipLaunchKernelGGL(k_blend_bwd<GS_BWD_PIX>, dim3(blend_grid(n_tiles)), dim3(kTile * kTile / GS_BWD_PIX), 0, s,
-                       cam, splats, values, tile_ranges, final_T, n_contrib, dL_dimage, acc);
+    hipLaunchKernelGGL(k_blend_bwd<GS_BWD_PIX>, dim3(tile_order ? n_tiles : blend_grid(n_tiles)),
+                       dim3(kTile * kTile / GS_BWD_PIX), 0, s, cam, splats, values, tile_ranges, final_T, n_contrib,
+                       dL_dimage, tile_order, acc);
+    return hipGetLastError();
+}
+
+// ---- tile order of the backward -----------------------------------------------
+// The backward's work in a tile follows the longest walk among its pixels (the
+// list up to the last entry any of them blended), and that walk differs by a
+// factor of 3 or more between tiles. Workgroups are dispatched in launch order
+// and every tile's workgroup is resident at once, so each SIMD gets every
+// 1024th tile of the launch order: in list order its share of long walks
+// varies, and the SIMD with the most sets the kernel's duration. Launching
+// the tiles longest walk first deals each SIMD one tile of every length class.
+// The order is taken by a counting sort over 16 classes per octave of the walk
+// length; tiles of one class come out in no fixed order (the results do not
+// depend on it, beyond the float atomics' summation order).
+
+__device__ __forceinline__ uint32_t walk_class(uint32_t walk)
+{
+    // exponent and the 4 leading mantissa bits of the walk length as a float:
+    // 16 classes per octave, 0 .. kWalkClasses - 1 (walks of 0 and 1 share class 0)
+    const uint32_t b = __float_as_uint((float)max(walk, 1u)) >> 19;
+    return min(b - (127u << 4), (uint32_t)kWalkClasses - 1);   // 2^32 - 1 rounds up to 2^32
+}
+
+__global__ __launch_bounds__(kBlock) void k_tile_walk(Cam cam, const uint32_t* __restrict__ ranges,
+                                                      const uint32_t* __restrict__ n_contrib,
+                                                      uint32_t* __restrict__ walk_cls)
+{
+    const int n_tiles = cam.tiles_x * cam.tiles_y;
+    const int tile = (int)blockIdx.x * (kBlock / kWave) + (int)(threadIdx.x / kWave);
+    if (tile >= n_tiles) return;   // whole waves
+    const int lane = __lane_id();
+    const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
+    const int x = tx * kTile + (lane & 15);
+    uint32_t walk = 0;
+#pragma unroll
+    for (int k = 0; k < kTile / 4; ++k) {
+        const int y = ty * kTile + (lane >> 4) + 4 * k;
+        if (x < cam.width && y < cam.height) walk = max(walk, n_contrib[(int64_t)y * cam.width + x]);
+    }
+    for (int o = 32; o > 0; o >>= 1) walk = max(walk, (uint32_t)__shfl_xor((int)walk, o));
+    if (lane == 0) walk_cls[tile] = walk_class(min(walk, ranges[2 * tile + 1] - ranges[2 * tile]));
+}
+
+constexpr int kOrderThreads = 1024;
+
+__global__ __launch_bounds__(kOrderThreads) void k_tile_order(int n_tiles, const uint32_t* __restrict__ walk_cls,
+                                                              uint32_t* __restrict__ order)
+{
+    __shared__ uint32_t cnt[kWalkClasses];
+    __shared__ uint32_t scan[2][kWalkClasses];
+    const int t = threadIdx.x;
+    for (int c = t; c < kWalkClasses; c += kOrderThreads) cnt[c] = 0;
+    __syncthreads();
+    for (int i = t; i < n_tiles; i += kOrderThreads) atomicAdd(&cnt[walk_cls[i]], 1u);
+    __syncthreads();
+    // first position of each class, the longest class first: the sum of the
+    // counts of all longer classes (inclusive scan over the reversed classes)
+    int src = 0;
+    for (int c = t; c < kWalkClasses; c += kOrderThreads) scan[0][c] = cnt[kWalkClasses - 1 - c];
+    __syncthreads();
+    for (int d = 1; d < kWalkClasses; d <<= 1) {
+        for (int c = t; c < kWalkClasses; c += kOrderThreads)
+            scan[src ^ 1][c] = scan[src][c] + (c >= d ? scan[src][c - d] : 0u);
+        __syncthreads();
+        src ^= 1;
+    }
+    for (int c = t; c < kWalkClasses; c += kOrderThreads) {
+        const int r = kWalkClasses - 1 - c;   // reversed index of class c
+        cnt[c] = scan[src][r] - cnt[c];       // counts of the classes above c
+    }
+    __syncthreads();
+    for (int i = t; i < n_tiles; i += kOrderThreads) order[atomicAdd(&cnt[walk_cls[i]], 1u)] = (uint32_t)i;
+}
+
+bool tile_order_supported(const Cam& cam) { return (int64_t)cam.tiles_x * cam.tiles_y <= kMaxOrderedTiles; }
+
+hipError_t launch_tile_order(const Cam& cam, const uint32_t* tile_ranges, const uint32_t* n_contrib,
+                             uint32_t* walk_cls, uint32_t* order, hipStream_t s)
+{
+    const int n_tiles = cam.tiles_x * cam.tiles_y;
+    hipLaunchKernelGGL(k_tile_walk, dim3((unsigned)div_up(n_tiles, kBlock / kWave)), dim3(kBlock), 0, s, cam,
+                       tile_ranges, n_contrib, walk_cls);
+    hipLaunchKernelGGL(k_tile_order, dim3(1), dim3(kOrderThreads), 0, s, n_tiles, walk_cls, order);
     return hipGetLastError();
 }
 

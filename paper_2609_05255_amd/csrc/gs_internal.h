@@ -62,6 +62,10 @@ constexpr int kSortTile = kBlock * kSortItems;   // 4096
 constexpr int kRadix = 256;
 constexpr int kDupChunk = 1024;   // depth-ordered Gaussians per workgroup in entry emission
 constexpr int kBlockDim = 4;      // a block is kBlockDim x kBlockDim tiles
+// Tile order of the blend backward: classes of walk length (16 per octave of a
+// u32) and the largest image it is taken for (larger images keep the plain order).
+constexpr int kWalkClasses = 512;
+constexpr int kMaxOrderedTiles = 32768;
 
 // Workgroups of the decoder preprocess backward (grid-stride), one partial
 // weight gradient each: as many as are resident at once, 3 per compute unit
@@ -95,6 +99,8 @@ struct Workspace {
     uint32_t* seg_cnt;       // [segments][4][16] per-tile counts, then offsets, of each wave's sub-segment
     uint32_t* list_counters; // [2]               segments; tile lists over capacity
     float* acc;              // [n][9]            blend-backward accumulators
+    uint32_t* walk_cls;      // [tiles]           walk-length class of each tile (blend backward)
+    uint32_t* tile_order;    // [tiles]           tiles, longest walk first (blend backward)
     float* mlp_part;         // [kMlpPartials][1664] per-workgroup decoder weight gradients
     size_t bytes;
 };
@@ -148,9 +154,13 @@ hipError_t launch_blend_fwd(const Cam& cam, const gs_splat* splats, const uint32
 hipError_t launch_clear(float* p, int64_t count, hipStream_t s);
 hipError_t launch_blend_count(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                               const uint32_t* tile_ranges, uint64_t* counts, hipStream_t s);
+bool tile_order_supported(const Cam& cam);   // at most kMaxOrderedTiles tiles
+hipError_t launch_tile_order(const Cam& cam, const uint32_t* tile_ranges, const uint32_t* n_contrib,
+                             uint32_t* walk_cls, uint32_t* order, hipStream_t s);
+// tile_order: NULL for the plain tile order
 hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                             const uint32_t* tile_ranges, const float* final_T, const uint32_t* n_contrib,
-                            const float* dL_dimage, float* acc, hipStream_t s);
+                            const float* dL_dimage, const uint32_t* tile_order, float* acc, hipStream_t s);
 hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                                  const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr,
                                  hipStream_t s);

@@ -32,7 +32,7 @@ def neural_weight_count(arch=None) -> int:
     layers, width = (2, 16) if arch is None else (int(arch[0]), int(arch[1]))
     return 32 * width + (layers - 1) * width * width + 3 * width
 KERNEL_NAMES = ["preprocess", "pair_count", "depth_sort", "entry_offsets", "block_entries", "block_sort", "tile_lists",
-                "blend_fwd", "clear", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam", "neural_fold"]
+                "blend_fwd", "bwd_prep", "blend_bwd", "preprocess_bwd", "mlp_reduce", "adam", "neural_fold"]
 ADAM_MAX_TENSORS = 8
 ADAM_MAX_ROWS = 128
 SPLAT_BYTES = 64

@@ -95,6 +95,13 @@ def test_more_than_65536_tiles():
     check_all(sc, tiny_camera(16 * 4097, 256), label="wide", grads=False)
 
 
+def test_backward_in_plain_tile_order():
+    # 2049 x 16 tiles: above 32768 tiles the backward keeps the plain tile order
+    # (below it, every other case here, it walks the tiles longest walk first)
+    sc = inputs.make_scene("tiny").subset(np.arange(300))
+    check_all(sc, tiny_camera(16 * 2049, 256), label="wide-bwd")
+
+
 def test_capacity_retry():
     sc = inputs.make_scene("tiny")
     check_all(sc, inputs.make_cameras("tiny")[0], capacity=100, label="capacity")

@@ -95,11 +95,13 @@ def test_more_than_65536_tiles():
     check_all(sc, tiny_camera(16 * 4097, 256), label="wide", grads=False)
 
 
-def test_backward_in_plain_tile_order():
-    # 2049 x 16 tiles: above 32768 tiles the backward keeps the plain tile order
-    # (below it, every other case here, it walks the tiles longest walk first)
+@pytest.mark.parametrize("tiles_x", [2048, 2049])
+def test_backward_tile_order_limit(tiles_x):
+    # 2048 x 16 = 32768 tiles, the largest image whose backward launches its
+    # tiles longest walk first (as every other case here), and 2049 x 16, the
+    # smallest that keeps the plain tile order
     sc = inputs.make_scene("tiny").subset(np.arange(300))
-    check_all(sc, tiny_camera(16 * 2049, 256), label="wide-bwd")
+    check_all(sc, tiny_camera(16 * tiles_x, 256), label="wide-bwd-%d" % tiles_x)
 
 
 def test_capacity_retry():

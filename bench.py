@@ -306,6 +306,34 @@ def measure(gs, inputs, torch, cfg_name: str, kind: str, args, arch=None, train=
         out["train_step"] = {"it_s": round(1.0 / t_train, 3), "ms_per_step": round(1e3 * t_train, 4),
                              "adam_ms": round(adam_ms, 4),
                              "optimizer": "fused Adam over every parameter tensor, one launch per step"}
+        if kid == gs.GS_APP_SH3:
+            # the same training step with the Adam update applied inside the
+            # backward (gs_render_bwd_adam): no gradient is written or read back
+            def train_in_bwd(i):
+                c = cstructs[i % ncam]
+                fr.forward(c, st, stream=stream, sync_pairs=False)
+                opt.backward_step(fr, c, st, grads_up[i % ncam], stream=stream)
+            for i in range(args.warmup):
+                train_in_bwd(i)
+            torch.cuda.synchronize()
+            t_start = time.perf_counter()
+            for i in range(args.steps):
+                train_in_bwd(i)
+            torch.cuda.synchronize()
+            t_in = (time.perf_counter() - t_start) / args.steps
+            timer.attach()
+            timer.reset()
+            for i in range(args.steps):
+                opt.backward_step(fr, cstructs[i % ncam], st, grads_up[i % ncam], stream=stream)
+            torch.cuda.synchronize()
+            kt_in = timer.read()
+            gs.Timer.detach()
+            pb_ms, pb_n = kt_in["preprocess_bwd"]
+            pb_ms /= max(pb_n, 1)
+            out["train_step_adam_in_bwd"] = {
+                "it_s": round(1.0 / t_in, 3), "ms_per_step": round(1e3 * t_in, 4),
+                "preprocess_bwd_adam_ms": round(pb_ms, 4),
+                "optimizer": "the Adam update of the Gaussians' parameters applied inside the preprocess backward"}
         del opt
     timer.close()
     out["_kernel_counts"] = {k: cnt for k, (ms, cnt) in kt.items() if cnt}
@@ -399,6 +427,7 @@ def main():
             "sh3_it_s": main_m["it_s"], "latent_it_s": lat["it_s"], "ratio": round(lat["it_s"] / main_m["it_s"], 4),
             "sh3_train_it_s": main_m["train_step"]["it_s"], "latent_train_it_s": lat["train_step"]["it_s"],
             "train_ratio": round(lat["train_step"]["it_s"] / main_m["train_step"]["it_s"], 4),
+            "sh3_train_adam_in_bwd_it_s": main_m.get("train_step_adam_in_bwd", {}).get("it_s"),
             "sh3_render_mpix_s": main_m["render_only"]["mpix_per_s"],
             "latent_render_mpix_s": lat["render_only"]["mpix_per_s"]}
         extra["paper_latent"] = lat

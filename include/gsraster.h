@@ -381,6 +381,35 @@ typedef struct gs_adam_tensor {
 gs_status gs_adam_step(const gs_adam_tensor* tensors, int32_t count, float beta1, float eps, int64_t step,
                        void* stream);
 
+/*
+ * gs_render_bwd_adam -- gs_render_bwd followed by one gs_adam_step on the
+ * Gaussians' own parameters, in one pass: the Adam step of the paper's training
+ * pipeline (supplementary implementation details; Kingma and Ba, Algorithm 1)
+ * is applied to each parameter element where its gradient is computed, with
+ * the same fp32 operations as gs_adam_step, instead of the gradient being
+ * written and read back (for SH3 that halves the bytes the backward and the
+ * optimiser move together). SH3 appearance only: other kinds return
+ * GS_ERR_UNSUPPORTED.
+ * adam: GS_RENDER_ADAM_TENSORS tensors as gs_adam_step takes them, in the order
+ *   means [3][n], log_scales [3][n], quats [4][n], opacity_logits [1][n], sh
+ *   [48][n]. Each param must be the very array that g or app holds: the
+ *   parameters are updated in place (each Gaussian's after its own backward has
+ *   read them; no Gaussian reads another's). grad is ignored. Every element is
+ *   stepped, those of culled Gaussians and of SH bands above sh_degree with a
+ *   zero gradient, as gs_adam_step would step them. beta1, eps, step as for
+ *   gs_adam_step (the step whose bias corrections apply, >= 1).
+ * grads: every array may be NULL here; one that is not receives the gradient
+ *   the update used (dmean2d as for gs_render_bwd).
+ * Errors: as gs_render_bwd; GS_ERR_INVALID_ARG when a tensor's param, rows or n
+ *   does not match, a moment or lr array is NULL, or a constant is out of range.
+ */
+#define GS_RENDER_ADAM_TENSORS 5
+gs_status gs_render_bwd_adam(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                             const gs_preprocessed* pre, const uint32_t* values, const uint32_t* tile_ranges,
+                             const float* final_T, const uint32_t* n_contrib, const float* dL_dimage,
+                             const gs_grads* grads, const gs_adam_tensor* adam, float beta1, float eps, int64_t step,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
 /* Workspace bytes needed by any call for these sizes (host only). */
 gs_status gs_workspace_size(int64_t n, int32_t width, int32_t height, uint64_t capacity, int32_t kind,
                             size_t* bytes);

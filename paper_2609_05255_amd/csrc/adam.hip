@@ -11,6 +11,7 @@
 #include <cmath>
 #include <cstring>
 
+#include "adam_update.h"
 #include "gs_internal.h"
 
 #pragma clang fp contract(off)
@@ -31,15 +32,12 @@ struct AdamTensorArgs {
     int64_t n;
     int64_t chunk0;        // first workgroup of this tensor
     int32_t chunks_per_row;
-    int32_t row0;          // index of this tensor's first row in step_size
-    float b2, omb2, inv_sqrt_bc2;
 };
 
 struct AdamArgs {
     int32_t count;
-    float b1, omb1, eps;
     AdamTensorArgs t[GS_ADAM_MAX_TENSORS];
-    float step_size[GS_ADAM_MAX_ROWS];   // lr / (1 - b1^t) per row
+    AdamStep c;
 };
 
 __global__ __launch_bounds__(kBlock) void k_adam(AdamArgs a)
@@ -51,7 +49,8 @@ __global__ __launch_bounds__(kBlock) void k_adam(AdamArgs a)
     const int64_t local = b - T.chunk0;
     const int row = (int)(local / T.chunks_per_row);
     const int64_t c = local - (int64_t)row * T.chunks_per_row;
-    const float step = a.step_size[T.row0 + row];
+    const float step = a.c.step_size[a.c.row0[k] + row];
+    const float b2 = a.c.b2[k], omb2 = a.c.omb2[k], isbc2 = a.c.inv_sqrt_bc2[k];
     const int64_t e0 = c * kChunk + threadIdx.x;
     const int64_t rbase = (int64_t)row * T.n;
     float g[kItems], m[kItems], v[kItems], p[kItems];
@@ -72,30 +71,43 @@ __global__ __launch_bounds__(kBlock) void k_adam(AdamArgs a)
         const int64_t e = e0 + (int64_t)j * kBlock;
         if (e >= T.n) continue;
         const int64_t i = rbase + e;
-        const float mj = a.b1 * m[j] + a.omb1 * g[j];
-        const float vj = T.b2 * v[j] + T.omb2 * (g[j] * g[j]);
-        const float denom = sqrtf(vj) * T.inv_sqrt_bc2 + a.eps;
-        const float pj = p[j] - step * (mj / denom);
-        __builtin_nontemporal_store(mj, T.m + i);
-        __builtin_nontemporal_store(vj, T.v + i);
-        __builtin_nontemporal_store(pj, T.p + i);
-        if (T.h) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (_Float16)pj), T.h + i);
+        adam_update(p[j], m[j], v[j], g[j], a.c.b1, a.c.omb1, b2, omb2, isbc2, a.c.eps, step);
+        __builtin_nontemporal_store(m[j], T.m + i);
+        __builtin_nontemporal_store(v[j], T.v + i);
+        __builtin_nontemporal_store(p[j], T.p + i);
+        if (T.h) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (_Float16)p[j]), T.h + i);
     }
 }
 
 }  // namespace
+
+void adam_step_constants(const gs_adam_tensor* ts, int count, float beta1, float eps, int64_t step, AdamStep& c)
+{
+    memset(&c, 0, sizeof(c));
+    c.b1 = beta1;
+    c.omb1 = 1.f - beta1;
+    c.eps = eps;
+    const double bc1 = 1.0 - std::pow((double)beta1, (double)step);
+    int rows = 0;
+    for (int k = 0; k < count; ++k) {
+        const gs_adam_tensor& t = ts[k];
+        c.row0[k] = rows;
+        c.b2[k] = t.beta2;
+        c.omb2[k] = 1.f - t.beta2;
+        const double bc2 = 1.0 - std::pow((double)t.beta2, (double)step);
+        c.inv_sqrt_bc2[k] = (float)(1.0 / std::sqrt(bc2));
+        for (int r = 0; r < t.rows; ++r) c.step_size[rows + r] = (float)((double)t.lr[r] / bc1);
+        rows += t.rows;
+    }
+}
 
 hipError_t launch_adam(const gs_adam_tensor* ts, int count, float beta1, float eps, int64_t step, hipStream_t s)
 {
     AdamArgs a;
     memset(&a, 0, sizeof(a));
     a.count = count;
-    a.b1 = beta1;
-    a.omb1 = 1.f - beta1;
-    a.eps = eps;
-    const double bc1 = 1.0 - std::pow((double)beta1, (double)step);
+    adam_step_constants(ts, count, beta1, eps, step, a.c);
     int64_t chunks = 0;
-    int rows = 0;
     for (int k = 0; k < count; ++k) {
         const gs_adam_tensor& t = ts[k];
         AdamTensorArgs& T = a.t[k];
@@ -107,14 +119,7 @@ hipError_t launch_adam(const gs_adam_tensor* ts, int count, float beta1, float e
         T.n = t.n;
         T.chunk0 = chunks;
         T.chunks_per_row = (int32_t)div_up(t.n, kChunk);
-        T.row0 = rows;
-        T.b2 = t.beta2;
-        T.omb2 = 1.f - t.beta2;
-        const double bc2 = 1.0 - std::pow((double)t.beta2, (double)step);
-        T.inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
-        for (int r = 0; r < t.rows; ++r) a.step_size[rows + r] = (float)((double)t.lr[r] / bc1);
         chunks += (int64_t)t.rows * T.chunks_per_row;
-        rows += t.rows;
     }
     if (chunks == 0) return hipSuccess;
     hipLaunchKernelGGL(k_adam, dim3((unsigned)chunks), dim3(kBlock), 0, s, a);

@@ -486,10 +486,16 @@ gs_status gs_render_work(const gs_camera* cam, const gs_preprocessed* pre, int64
     return ok();
 }
 
-gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
-                        const gs_preprocessed* pre, const uint32_t* values, const uint32_t* tile_ranges,
-                        const float* final_T, const uint32_t* n_contrib, const float* dL_dimage, const gs_grads* grads,
-                        void* workspace, size_t workspace_bytes, void* stream)
+}  // extern "C"
+
+namespace {
+
+// gs_render_bwd, and gs_render_bwd_adam when `adam` is not NULL (checked by the caller).
+gs_status render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app, const gs_preprocessed* pre,
+                     const uint32_t* values, const uint32_t* tile_ranges, const float* final_T,
+                     const uint32_t* n_contrib, const float* dL_dimage, const gs_grads* grads, void* workspace,
+                     size_t workspace_bytes, void* stream, const gs_adam_tensor* adam, float beta1, float eps,
+                     int64_t step)
 {
     gs_status st;
     if ((st = check_camera(cam)) != GS_OK) return st;
@@ -500,7 +506,7 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
     if ((st = check_pre(pre, g->n)) != GS_OK) return st;
     GS_CHECK(tile_ranges && final_T && n_contrib && dL_dimage, "a render input array is NULL");
     GS_CHECK(grads != nullptr, "grads is NULL");
-    if (g->n > 0) {
+    if (g->n > 0 && !adam) {
         GS_CHECK(grads->dmeans && grads->dlog_scales && grads->dquats && grads->dopacity_logits,
                  "a geometry gradient array is NULL");
         if (app->kind == GS_APP_SH3) GS_CHECK(grads->dsh != nullptr, "dsh is NULL");
@@ -531,7 +537,7 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
                             ordered ? ws.tile_order : nullptr, ws.acc, s));
     timing_end(GS_KERNEL_BLEND_BWD, s);
     timing_begin(GS_KERNEL_PREPROCESS_BWD, s);
-    GS_HIP(launch_preprocess_bwd(c, *g, *app, *pre, ws, *grads, s));
+    GS_HIP(launch_preprocess_bwd(c, *g, *app, *pre, ws, *grads, s, adam, beta1, eps, step));
     timing_end(GS_KERNEL_PREPROCESS_BWD, s);
     if (app->kind == GS_APP_LATENT_MLP || app->kind == GS_APP_NEURAL) {
         timing_begin(GS_KERNEL_MLP_REDUCE, s);
@@ -539,6 +545,49 @@ gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_ap
         timing_end(GS_KERNEL_MLP_REDUCE, s);
     }
     return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+gs_status gs_render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                        const gs_preprocessed* pre, const uint32_t* values, const uint32_t* tile_ranges,
+                        const float* final_T, const uint32_t* n_contrib, const float* dL_dimage, const gs_grads* grads,
+                        void* workspace, size_t workspace_bytes, void* stream)
+{
+    return render_bwd(cam, g, app, pre, values, tile_ranges, final_T, n_contrib, dL_dimage, grads, workspace,
+                      workspace_bytes, stream, nullptr, 0.f, 0.f, 0);
+}
+
+gs_status gs_render_bwd_adam(const gs_camera* cam, const gs_gaussians* g, const gs_appearance* app,
+                             const gs_preprocessed* pre, const uint32_t* values, const uint32_t* tile_ranges,
+                             const float* final_T, const uint32_t* n_contrib, const float* dL_dimage,
+                             const gs_grads* grads, const gs_adam_tensor* adam, float beta1, float eps, int64_t step,
+                             void* workspace, size_t workspace_bytes, void* stream)
+{
+    gs_status st;
+    if ((st = check_gaussians(g)) != GS_OK) return st;
+    GS_CHECK(app != nullptr, "appearance is NULL");
+    if (app->kind != GS_APP_SH3)
+        return fail(GS_ERR_UNSUPPORTED, "gs_render_bwd_adam: appearance kind %d (SH3 only)", app->kind);
+    GS_CHECK(adam != nullptr, "adam is NULL");
+    GS_CHECK(step >= 1, "step %lld must be at least 1", (long long)step);
+    GS_CHECK(beta1 >= 0.f && beta1 < 1.f, "beta1 must lie in [0, 1)");
+    GS_CHECK(eps > 0.f, "eps must be positive");
+    const float* params[GS_RENDER_ADAM_TENSORS] = {g->means, g->log_scales, g->quats, g->opacity_logits, app->sh};
+    const int rows[GS_RENDER_ADAM_TENSORS] = {3, 3, 4, 1, GS_SH_COEFFS};
+    for (int k = 0; k < GS_RENDER_ADAM_TENSORS; ++k) {
+        const gs_adam_tensor& t = adam[k];
+        GS_CHECK(t.param == params[k], "adam[%d].param is not the parameter array it updates", k);
+        GS_CHECK(t.rows == rows[k] && t.n == g->n, "adam[%d]: rows %d, n %lld (%d rows of %lld expected)", k, t.rows,
+                 (long long)t.n, rows[k], (long long)g->n);
+        GS_CHECK(g->n == 0 || (t.exp_avg && t.exp_avg_sq), "adam[%d]: a moment array is NULL", k);
+        GS_CHECK(t.lr != nullptr, "adam[%d].lr is NULL", k);
+        GS_CHECK(t.beta2 >= 0.f && t.beta2 < 1.f, "adam[%d]: beta2 must lie in [0, 1)", k);
+    }
+    return render_bwd(cam, g, app, pre, values, tile_ranges, final_T, n_contrib, dL_dimage, grads, workspace,
+                      workspace_bytes, stream, adam, beta1, eps, step);
 }
 
 gs_status gs_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* mlp_w, float* colors, void* stream)

@@ -5,8 +5,10 @@
 // opacity logistic, and the appearance model -- including the colour gradient
 // through the view direction into the mean (Sec. 4 fused backward). Gradients
 // of culled Gaussians are written as zeros, so every output is dense.
+#include <cstring>
 #include <type_traits>
 
+#include "adam_update.h"
 #include "gs_internal.h"
 #include "mlp.h"
 #include "lobe.h"
@@ -46,6 +48,47 @@ struct BwdArgs {
     float* dlobes;
     int sh_y0_folded;
 };
+
+// The Adam step of gs_render_bwd_adam, applied where each gradient is computed.
+// Tensors in the order means, log_scales, quats, opacity_logits, then the
+// appearance's per-Gaussian parameters (SH3: sh).
+constexpr int kFusedTensors = 5;
+struct AdamFused {
+    float* p[kFusedTensors];
+    float* m[kFusedTensors];
+    float* v[kFusedTensors];
+    uint16_t* h[kFusedTensors];
+    AdamStep c;
+};
+
+// A batch of K elements (t[k], row[k], Gaussian i): p[k] is the parameter as
+// read before the update (the caller reads those the backward did not). All
+// the batch's moments are read before any element is written, so that their
+// reads are in flight together (the compiler cannot move a read past a write
+// it cannot tell apart).
+template <int K>
+__device__ __forceinline__ void adam_apply(const AdamFused& f, const int (&t)[K], const int (&row)[K], int64_t n,
+                                           int64_t i, float (&p)[K], const float (&g)[K])
+{
+    float m[K], v[K];
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int64_t e = (int64_t)row[k] * n + i;
+        m[k] = __builtin_nontemporal_load(f.m[t[k]] + e);
+        v[k] = __builtin_nontemporal_load(f.v[t[k]] + e);
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int tk = t[k];
+        const int64_t e = (int64_t)row[k] * n + i;
+        adam_update(p[k], m[k], v[k], g[k], f.c.b1, f.c.omb1, f.c.b2[tk], f.c.omb2[tk], f.c.inv_sqrt_bc2[tk],
+                    f.c.eps, f.c.step_size[f.c.row0[tk] + row[k]]);
+        __builtin_nontemporal_store(m[k], f.m[tk] + e);
+        __builtin_nontemporal_store(v[k], f.v[tk] + e);
+        __builtin_nontemporal_store(p[k], f.p[tk] + e);
+        if (f.h[tk]) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (_Float16)p[k]), f.h[tk] + e);
+    }
+}
 
 struct GeoGrad {
     float dmu[3];
@@ -228,6 +271,103 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
     }
     for (int j = 0; j < 4; ++j) __builtin_nontemporal_store(gg.dq[j], &a.dquats[j * n + i]);
     __builtin_nontemporal_store(gg.dlogit, &a.dlogits[i]);
+    if (a.dmean2d) {
+        __builtin_nontemporal_store(g9[0], &a.dmean2d[i]);
+        __builtin_nontemporal_store(g9[1], &a.dmean2d[n + i]);
+    }
+}
+
+// gs_render_bwd_adam for SH3: the backward above, with the Adam step applied
+// to every parameter element where its gradient is computed (culled Gaussians'
+// and inactive bands' elements with a zero gradient, as the standalone step
+// steps them); a gradient array of `a` that is not NULL still receives the
+// gradient. The SH rows are stepped as soon as the colour gradient is known,
+// so that the coefficients are not kept past them.
+__global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3_adam(BwdArgs a, AdamFused f)
+{
+    const int i = blockIdx.x * kBlock + threadIdx.x;
+    if (i >= a.n) return;
+    const int64_t n = a.n;
+    const bool vis = a.tiles_touched[i] != 0;
+    GeoGrad gg;
+    for (int j = 0; j < 3; ++j) { gg.dmu[j] = 0.f; gg.dls[j] = 0.f; }
+    for (int j = 0; j < 4; ++j) gg.dq[j] = 0.f;
+    gg.dlogit = 0.f;
+    float g9[kAccStride];
+    for (int k = 0; k < kAccStride; ++k) g9[k] = 0.f;
+    float Y[16], gc[3] = {0.f, 0.f, 0.f}, dY[16];
+    for (int k = 0; k < 16; ++k) Y[k] = dY[k] = 0.f;
+    const int nb = (a.sh_degree + 1) * (a.sh_degree + 1);
+    float mu[3], ls[3], q[4];
+    for (int j = 0; j < 3; ++j) mu[j] = __builtin_nontemporal_load(&a.means[j * n + i]);
+    for (int j = 0; j < 3; ++j) ls[j] = __builtin_nontemporal_load(&a.log_scales[j * n + i]);
+    for (int j = 0; j < 4; ++j) q[j] = __builtin_nontemporal_load(&a.quats[j * n + i]);
+    const float logit = __builtin_nontemporal_load(&a.logits[i]);
+    float coef[GS_SH_COEFFS];
+    for (int k = 0; k < GS_SH_COEFFS; ++k) coef[k] = 0.f;
+    float d0 = 0.f, d1 = 0.f, d2 = 0.f, il = 0.f;
+    if (vis) {
+        const float* ap = a.acc + (size_t)i * kAccStride;
+        for (int k = 0; k < kAccStride; ++k) g9[k] = __builtin_nontemporal_load(ap + k);
+        geometry_bwd(a.cam, mu, ls, q, logit, g9, gg);
+        const float vx = mu[0] - a.cam.campos[0], vy = mu[1] - a.cam.campos[1], vz = mu[2] - a.cam.campos[2];
+        const float len = sqrtf(vx * vx + vy * vy + vz * vz);
+        il = 1.f / len;
+        d0 = vx * il;
+        d1 = vy * il;
+        d2 = vz * il;
+        sh_basis16(d0, d1, d2, Y);
+        if (a.sh_y0_folded) Y[0] = 1.f;
+        float pre[3] = {0.5f, 0.5f, 0.5f};
+        for (int k = 0; k < 16; ++k)
+            for (int c = 0; c < 3; ++c) {
+                coef[3 * k + c] = k < nb ? __builtin_nontemporal_load(a.sh + (3 * k + c) * n + i) : 0.f;
+                pre[c] += Y[k] * coef[3 * k + c];
+            }
+        for (int c = 0; c < 3; ++c) gc[c] = pre[c] > 0.f ? g9[6 + c] : 0.f;
+        for (int k = 0; k < 16; ++k) dY[k] = coef[3 * k] * gc[0] + coef[3 * k + 1] * gc[1] + coef[3 * k + 2] * gc[2];
+    }
+    // the SH rows, two bands (6 rows) per batch
+    constexpr int kShBatch = 6;
+#pragma unroll
+    for (int r0 = 0; r0 < GS_SH_COEFFS; r0 += kShBatch) {
+        int tb[kShBatch], rb[kShBatch];
+        float pb[kShBatch], gb[kShBatch];
+#pragma unroll
+        for (int j = 0; j < kShBatch; ++j) {
+            const int r = r0 + j, k = r / 3, c = r % 3;
+            tb[j] = 4;
+            rb[j] = r;
+            gb[j] = k < nb ? Y[k] * gc[c] : 0.f;
+            // coefficients the backward did not read are read here
+            pb[j] = vis && k < nb ? coef[r] : __builtin_nontemporal_load(a.sh + r * n + i);
+            if (a.dsh) __builtin_nontemporal_store(gb[j], a.dsh + r * n + i);
+        }
+        adam_apply(f, tb, rb, n, i, pb, gb);
+    }
+    if (vis) {
+        float dd[3] = {0.f, 0.f, 0.f};
+        sh_basis16_vjp(d0, d1, d2, dY, dd);
+        // d = v / |v|: dv = (dd - d (d . dd)) / |v|
+        const float dot = d0 * dd[0] + d1 * dd[1] + d2 * dd[2];
+        gg.dmu[0] += (dd[0] - d0 * dot) * il;
+        gg.dmu[1] += (dd[1] - d1 * dot) * il;
+        gg.dmu[2] += (dd[2] - d2 * dot) * il;
+    }
+    for (int j = 0; j < 3; ++j) {
+        if (a.dmeans) __builtin_nontemporal_store(gg.dmu[j], &a.dmeans[j * n + i]);
+        if (a.dlog_scales) __builtin_nontemporal_store(gg.dls[j], &a.dlog_scales[j * n + i]);
+    }
+    for (int j = 0; j < 4; ++j)
+        if (a.dquats) __builtin_nontemporal_store(gg.dq[j], &a.dquats[j * n + i]);
+    if (a.dlogits) __builtin_nontemporal_store(gg.dlogit, &a.dlogits[i]);
+    // the geometry rows in one batch: means, log-scales, quaternion, opacity logit
+    const int tg[11] = {0, 0, 0, 1, 1, 1, 2, 2, 2, 2, 3};
+    const int rg[11] = {0, 1, 2, 0, 1, 2, 0, 1, 2, 3, 0};
+    float pg[11] = {mu[0], mu[1], mu[2], ls[0], ls[1], ls[2], q[0], q[1], q[2], q[3], logit};
+    const float gg11[11] = {gg.dmu[0], gg.dmu[1], gg.dmu[2], gg.dls[0], gg.dls[1], gg.dls[2],
+                            gg.dq[0], gg.dq[1], gg.dq[2], gg.dq[3], gg.dlogit};
+    adam_apply(f, tg, rg, n, i, pg, gg11);
     if (a.dmean2d) {
         __builtin_nontemporal_store(g9[0], &a.dmean2d[i]);
         __builtin_nontemporal_store(g9[1], &a.dmean2d[n + i]);
@@ -634,7 +774,8 @@ inline int decoder_bwd_grid(int64_t n, const gs_appearance& app)
 }
 
 hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
-                                 const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr, hipStream_t s)
+                                 const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr, hipStream_t s,
+                                 const gs_adam_tensor* adam, float beta1, float eps, int64_t step)
 {
     BwdArgs a;
     a.cam = cam;
@@ -664,8 +805,24 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
     a.lobes = app.lobes;
     a.dlobes = gr.dlobes;
     a.sh_y0_folded = app.sh_y0_folded;
-    if (app.kind == GS_APP_SH3)
-        hipLaunchKernelGGL(k_preprocess_bwd_sh3, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
+    AdamFused f;
+    memset(&f, 0, sizeof(f));
+    if (adam) {
+        if (app.kind != GS_APP_SH3) return hipErrorInvalidValue;   // the entry point rejects it first
+        adam_step_constants(adam, kFusedTensors, beta1, eps, step, f.c);
+        for (int t = 0; t < kFusedTensors; ++t) {
+            f.p[t] = adam[t].param;
+            f.m[t] = adam[t].exp_avg;
+            f.v[t] = adam[t].exp_avg_sq;
+            f.h[t] = adam[t].param_half;
+        }
+    }
+    if (app.kind == GS_APP_SH3) {
+        if (adam)
+            hipLaunchKernelGGL(k_preprocess_bwd_sh3_adam, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a, f);
+        else
+            hipLaunchKernelGGL(k_preprocess_bwd_sh3, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
+    }
     else if (app.kind == GS_APP_NASG)
         hipLaunchKernelGGL(k_preprocess_bwd_lobe<false>, dim3(preprocess_blocks(g.n)), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NASGABOR)

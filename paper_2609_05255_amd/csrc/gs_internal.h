@@ -161,9 +161,12 @@ hipError_t launch_tile_order(const Cam& cam, const uint32_t* tile_ranges, const 
 hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                             const uint32_t* tile_ranges, const float* final_T, const uint32_t* n_contrib,
                             const float* dL_dimage, const uint32_t* tile_order, float* acc, hipStream_t s);
+// adam: NULL, or the gs_adam_tensor of each per-Gaussian parameter in the order of
+// gs_render_bwd_adam, whose step is then applied in place (SH3 only)
 hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
                                  const gs_preprocessed& pre, const Workspace& ws, const gs_grads& gr,
-                                 hipStream_t s);
+                                 hipStream_t s, const gs_adam_tensor* adam = nullptr, float beta1 = 0.f,
+                                 float eps = 0.f, int64_t step = 0);
 hipError_t launch_mlp_reduce(int64_t n, const gs_appearance& app, const Workspace& ws, float* dmlp_w, hipStream_t s);
 hipError_t launch_adam(const gs_adam_tensor* tensors, int count, float beta1, float eps, int64_t step, hipStream_t s);
 hipError_t launch_mlp_eval(const uint16_t* x, int64_t rows, const uint16_t* w, float* out, hipStream_t s);

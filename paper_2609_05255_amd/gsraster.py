@@ -103,14 +103,17 @@ def lib() -> C.CDLL:
         L.gs_mlp_eval.argtypes = [vp, i64, vp, vp, vp]
         L.gs_neural_fold.argtypes = [vp, vp, i64, vp, vp]
         L.gs_adam_step.argtypes = [P(AdamTensor), i32, C.c_float, C.c_float, i64, vp]
+        L.gs_render_bwd_adam.argtypes = [P(Camera), P(Gaussians), P(Appearance), P(Preprocessed), vp, vp, vp, vp,
+                                         vp, P(Grads), P(AdamTensor), C.c_float, C.c_float, i64, vp, sz, vp]
         L.gs_timer_create.argtypes = [P(vp)]
         L.gs_timer_destroy.argtypes = [vp]
         L.gs_timer_attach.argtypes = [vp]
         L.gs_timer_reset.argtypes = [vp]
         L.gs_timer_read.argtypes = [vp, P(C.c_double), P(i64), i32]
-        for f in ("gs_preprocess", "gs_preprocess_noalloc", "gs_bin_sort", "gs_render_fwd", "gs_render_work", "gs_render_bwd", "gs_workspace_size", "gs_mlp_eval",
-                  "gs_neural_fold", "gs_adam_step", "gs_timer_create", "gs_timer_destroy", "gs_timer_attach",
-                  "gs_timer_reset", "gs_timer_read"):
+        for f in ("gs_preprocess", "gs_preprocess_noalloc", "gs_bin_sort", "gs_render_fwd", "gs_render_work",
+                  "gs_render_bwd", "gs_render_bwd_adam", "gs_workspace_size", "gs_mlp_eval", "gs_neural_fold",
+                  "gs_adam_step", "gs_timer_create", "gs_timer_destroy", "gs_timer_attach", "gs_timer_reset",
+                  "gs_timer_read"):
             getattr(L, f).restype = C.c_int
         L.gs_last_error.restype = C.c_char_p
         L.gs_version.restype = C.c_char_p
@@ -263,9 +266,7 @@ def gs_neural_fold(features, neural_w, n: int, preact, stream=None):
     _check(lib().gs_neural_fold(_ptr(features), _ptr(neural_w), n, _ptr(preact), _stream(stream)))
 
 
-def gs_adam_step(tensors, beta1: float, eps: float, step: int, stream=None):
-    """tensors: list of dicts with param, grad, exp_avg, exp_avg_sq (device fp32 [rows][n]), optional
-    param_half (device int16/uint16 [rows][n]), rows, n, beta2 and lr (a sequence of `rows` floats)."""
+def _adam_tensors(tensors):
     arr = (AdamTensor * max(1, len(tensors)))()
     keep = []
     for k, t in enumerate(tensors):
@@ -275,10 +276,34 @@ def gs_adam_step(tensors, beta1: float, eps: float, step: int, stream=None):
                 raise ValueError("lr needs one entry per row")
             lr = (C.c_float * len(t["lr"]))(*[float(x) for x in t["lr"]])
             keep.append(lr)
-        arr[k] = AdamTensor(_ptr(t["param"]), _ptr(t["grad"]), _ptr(t["exp_avg"]), _ptr(t["exp_avg_sq"]),
+        arr[k] = AdamTensor(_ptr(t["param"]), _ptr(t.get("grad")), _ptr(t["exp_avg"]), _ptr(t["exp_avg_sq"]),
                             _ptr(t.get("param_half")), int(t["n"]), int(t["rows"]), float(t["beta2"]),
                             C.cast(lr, C.POINTER(C.c_float)) if lr is not None else None)
+    return arr, keep
+
+
+def gs_adam_step(tensors, beta1: float, eps: float, step: int, stream=None):
+    """tensors: list of dicts with param, grad, exp_avg, exp_avg_sq (device fp32 [rows][n]), optional
+    param_half (device int16/uint16 [rows][n]), rows, n, beta2 and lr (a sequence of `rows` floats)."""
+    arr, keep = _adam_tensors(tensors)
     _check(lib().gs_adam_step(arr, len(tensors), float(beta1), float(eps), int(step), _stream(stream)))
+
+
+GS_RENDER_ADAM_TENSORS = 5
+
+
+def gs_render_bwd_adam(cam: Camera, g: Gaussians, app: Appearance, pre: Preprocessed, values, tile_ranges, final_T,
+                       n_contrib, dL_dimage, grads: Grads, tensors, beta1: float, eps: float, step: int, workspace,
+                       ws_bytes: int, stream=None):
+    """tensors: the GS_RENDER_ADAM_TENSORS per-Gaussian tensors (dicts as for gs_adam_step, grad unused) in
+    the order means, log_scales, quats, opacity_logits, sh."""
+    if len(tensors) != GS_RENDER_ADAM_TENSORS:
+        raise ValueError("gs_render_bwd_adam takes %d tensors" % GS_RENDER_ADAM_TENSORS)
+    arr, keep = _adam_tensors(tensors)
+    _check(lib().gs_render_bwd_adam(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), _ptr(values),
+                                    _ptr(tile_ranges), _ptr(final_T), _ptr(n_contrib), _ptr(dL_dimage),
+                                    C.byref(grads), arr, float(beta1), float(eps), int(step), _ptr(workspace),
+                                    ws_bytes, _stream(stream)))
 
 
 class Timer:

@@ -50,6 +50,7 @@ class FusedAdam:
     def __init__(self, scene: gs.SceneTensors, frame: gs.Frame, kind: int, betas=(0.9, 0.999), eps: float = 1e-15,
                  camera_dbar: float = LOBE_SPACING_REF):
         self.beta1, self.beta2, self.eps, self.t = betas[0], betas[1], eps, 0
+        self.kind = kind
         self.groups = []
 
         def add(param, grad, lr_rows, beta2=None, half=None):
@@ -88,6 +89,29 @@ class FusedAdam:
     def step(self, stream=None):
         self.t += 1
         gs.gs_adam_step(self.groups, self.beta1, self.eps, self.t, stream)
+
+    def backward_step(self, frame: gs.Frame, cam: gs.Camera, scene: gs.SceneTensors, dL_dimage, sh_degree: int = 3,
+                      grads: gs.Grads | None = None, stream=None):
+        """The backward with this optimiser's step of the Gaussians' own parameters applied
+        inside it (gs_render_bwd_adam, SH3): the same result as frame.backward then step(),
+        without writing the gradients (pass `grads` to have them written as well)."""
+        if self.kind != gs.GS_APP_SH3:
+            raise ValueError("the step inside the backward is built for the SH3 appearance")
+        self.t += 1
+        g = grads if grads is not None else gs.Grads()
+        gs.gs_render_bwd_adam(cam, scene.gaussians(), scene.appearance(self.kind, sh_degree), frame.pre,
+                              frame.values, frame.ranges, frame.final_T, frame.n_contrib, dL_dimage, g,
+                              self.groups[:gs.GS_RENDER_ADAM_TENSORS], self.beta1, self.eps, self.t, frame.workspace,
+                              frame.ws_bytes, stream)
+
+    def bytes_per_backward_step(self) -> int:
+        """HBM bytes of the parameter update inside the backward (backward_step), beyond those
+        the backward reads anyway: m and v read, param, m and v written, per element, and the
+        parameters the backward itself does not read (culled Gaussians', inactive bands')."""
+        total = 0
+        for g in self.groups[:gs.GS_RENDER_ADAM_TENSORS]:
+            total += g["rows"] * g["n"] * 5 * 4
+        return total
 
     def bytes_per_step(self) -> int:
         """HBM bytes one step must move: per element param, grad, m and v read, param, m and v

@@ -237,6 +237,43 @@ def test_render_calls_reject_bad_arguments(gs):
     assert st == gs.GS_ERR_INVALID_ARG and b"dlobes" in lib.gs_last_error()
 
 
+def test_render_bwd_adam_rejects_bad_arguments(gs):
+    lib = gs.lib()
+    cam = _camera(gs)
+    pre = gs.Preprocessed(FAKE, FAKE, FAKE, FAKE)
+    g = gs.Gaussians(10, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE)
+    sh = 5 * FAKE
+    app = gs.Appearance(gs.GS_APP_SH3, 3, sh, None, None)
+    grads = gs.Grads()
+    lr = (C.c_float * 48)(*([1e-3] * 48))
+
+    def tensors(params=(FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, sh), rows=(3, 3, 4, 1, 48), n=10, m=6 * FAKE):
+        arr = (gs.AdamTensor * gs.GS_RENDER_ADAM_TENSORS)()
+        for k in range(gs.GS_RENDER_ADAM_TENSORS):
+            arr[k] = gs.AdamTensor(params[k], None, m, 7 * FAKE, None, n, rows[k], 0.999,
+                                   C.cast(lr, C.POINTER(C.c_float)))
+        return arr
+
+    def call(app=app, adam=tensors(), beta1=0.9, eps=1e-15, step=1):
+        return lib.gs_render_bwd_adam(C.byref(cam), C.byref(g), C.byref(app), C.byref(pre), C.c_void_p(FAKE),
+                                      C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE),
+                                      C.byref(grads), adam, beta1, eps, step, C.c_void_p(FAKE * 256), 1 << 40, None)
+
+    # the step inside the backward is built for SH3 only
+    latent = gs.Appearance(gs.GS_APP_LATENT_MLP, 3, None, FAKE, FAKE)
+    assert call(app=latent) == gs.GS_ERR_UNSUPPORTED
+    assert call(adam=None) == gs.GS_ERR_INVALID_ARG
+    assert call(step=0) == gs.GS_ERR_INVALID_ARG
+    assert call(beta1=1.0) == gs.GS_ERR_INVALID_ARG
+    assert call(eps=0.0) == gs.GS_ERR_INVALID_ARG
+    # each tensor must be the parameter array it updates, with its rows and n
+    assert call(adam=tensors(params=(FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 9 * FAKE))) == gs.GS_ERR_INVALID_ARG
+    assert b"param" in lib.gs_last_error()
+    assert call(adam=tensors(rows=(3, 3, 4, 1, 47))) == gs.GS_ERR_INVALID_ARG
+    assert call(adam=tensors(n=11)) == gs.GS_ERR_INVALID_ARG
+    assert call(adam=tensors(m=None)) == gs.GS_ERR_INVALID_ARG and b"moment" in lib.gs_last_error()
+
+
 def test_neural_fold_rejects_bad_arguments(gs):
     lib = gs.lib()
     f = lambda *a: lib.gs_neural_fold(*[C.c_void_p(x) if x is not None else None for x in a[:2]], a[2],

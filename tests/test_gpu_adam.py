@@ -126,3 +126,76 @@ def test_fused_adam_on_a_scene(kind):
             h = g["param_half"].view(g["rows"], -1).cpu().numpy().view(np.uint16)
             assert np.array_equal(h, adam.half_copy(g["param"].cpu().numpy()))
     say("  fused Adam on the %s scene: %d tensors, %d bytes per step" % (kind, len(opt.groups), opt.bytes_per_step()))
+
+
+GRAD_NAMES = ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh")
+
+
+@pytest.mark.parametrize("scene,sh_degree", [("tiny", 3), ("tiny", 1), ("medium", 3)])
+def test_adam_inside_the_backward(scene, sh_degree):
+    # gs_render_bwd_adam: the SH3 backward with the Adam step of the Gaussians'
+    # own parameters applied where each gradient is computed, against
+    # gs_render_bwd and then gs_adam_step. The gradients it also writes are the
+    # backward's (up to the float atomics' summation order); the parameters and
+    # moments it leaves are bit-exact against gs_adam_step applied to those very
+    # gradients, culled Gaussians' and inactive bands' elements included.
+    from paper_2609_05255_amd import inputs
+    from paper_2609_05255_amd.optim import FusedAdam
+    from parity import tiny_camera
+    sc = inputs.make_scene(scene)
+    cam = tiny_camera() if scene == "tiny" else inputs.make_cameras("medium")[4]
+    say("case adam inside the backward: %s, degree %d, n=%d" % (scene, sh_degree, sc.n))
+    st = gs.SceneTensors(sc)
+    fr = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_SH3, 1 << 22)
+    cs = gs.camera_struct(cam)
+    fr.forward(cs, st, sh_degree)
+    up = torch.from_numpy(inputs.make_upstream_grad(cam.width, cam.height, 2)).cuda()
+    fr.backward(cs, st, up, sh_degree)
+    plain = {k: getattr(fr, k).clone() for k in GRAD_NAMES}
+    opt = FusedAdam(st, fr, gs.GS_APP_SH3)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    for g in opt.groups:   # a moment history, as after a few steps
+        g["exp_avg"].copy_(torch.randn(g["exp_avg"].shape, device="cuda", generator=gen) * 1e-3)
+        g["exp_avg_sq"].copy_(torch.randn(g["exp_avg_sq"].shape, device="cuda", generator=gen).square() * 1e-6)
+    opt.t = 4
+    before = [(g["param"].clone(), g["exp_avg"].clone(), g["exp_avg_sq"].clone()) for g in opt.groups]
+    for k in GRAD_NAMES:
+        getattr(fr, k).fill_(float("nan"))
+    opt.backward_step(fr, cs, st, up, sh_degree, grads=fr.grads)
+    torch.cuda.synchronize()
+    assert opt.t == 5
+    for k in GRAD_NAMES:
+        a, b = getattr(fr, k), plain[k]
+        assert not torch.isnan(a).any(), k
+        scale = float(b.abs().max())
+        assert bool(((a - b).abs() <= 1e-4 * b.abs() + 1e-6 * scale).all()), (k, float((a - b).abs().max()))
+    ref = []
+    for g, (p0, m0, v0), k in zip(opt.groups, before, GRAD_NAMES):
+        ref.append(dict(param=p0.clone(), grad=getattr(fr, k).view(g["rows"], -1), exp_avg=m0.clone(),
+                        exp_avg_sq=v0.clone(), rows=g["rows"], n=g["n"], beta2=g["beta2"], lr=g["lr"]))
+    gs.gs_adam_step(ref, opt.beta1, opt.eps, opt.t)
+    torch.cuda.synchronize()
+    for g, r in zip(opt.groups, ref):
+        for key in ("param", "exp_avg", "exp_avg_sq"):
+            assert torch.equal(g[key], r[key]), (g["rows"], key)
+    # without gradient outputs the update is the same. Compared bit-exact for an
+    # upstream gradient on one pixel: then no accumulator takes two float atomics,
+    # and both calls see the same gradients.
+    one = torch.zeros_like(up)
+    one[:, cam.height // 2, cam.width // 2] = up[:, cam.height // 2, cam.width // 2]
+    results = []
+    for grads in (fr.grads, None):
+        for g, (p0, m0, v0) in zip(opt.groups, before):
+            g["param"].copy_(p0)
+            g["exp_avg"].copy_(m0)
+            g["exp_avg_sq"].copy_(v0)
+        opt.t = 4
+        opt.backward_step(fr, cs, st, one, sh_degree, grads=grads)
+        torch.cuda.synchronize()
+        results.append([(g["param"].clone(), g["exp_avg"].clone(), g["exp_avg_sq"].clone()) for g in opt.groups])
+    moved = sum(int((x[0] != b[0]).sum()) for x, b in zip(results[1], before))
+    for x, y in zip(*results):
+        for u, w in zip(x, y):
+            assert torch.equal(u, w)
+    say("  bit-exact against the backward then gs_adam_step (%d elements); without gradient outputs the "
+        "same bits (%d parameters moved)" % (sum(g["rows"] * g["n"] for g in opt.groups), moved))

@@ -141,47 +141,50 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // skip the splats that reach alpha >= 1/255 nowhere in this wave's
+        // pixels: each lane tests the record it holds (before the next batch
+        // replaces it), and the walk below visits only the others, in order
+        const int cnt = (int)min((uint32_t)kWave, end - b);
+        const bool meets = lane < cnt && fabsf(c0.x - box_cx) <= c2.z + box_hx && fabsf(c0.y - box_cy) <= c2.w + box_hy;
+        uint64_t todo = __ballot(meets);
         if (b + kWave + lane < end) {
             const float4* p = reinterpret_cast<const float4*>(splats + values[b + kWave + lane]);
             c0 = p[0]; c1 = p[1]; c2 = p[2];
         }
-        const int cnt = (int)min((uint32_t)kWave, end - b);
-        for (int j = 0; j < cnt; ++j) {
+        while (todo != 0) {
+            const int j = (int)__builtin_ctzll(todo);
+            todo &= todo - 1;
             SplatReg s;
-            const float4 w0 = st[0][j], w2 = st[2][j];
-            s.mx = w0.x; s.my = w0.y; s.ex = w2.z; s.ey = w2.w;
-            // skip the splat if it reaches alpha >= 1/255 nowhere in this wave's pixels
-            if (fabsf(s.mx - box_cx) <= s.ex + box_hx && fabsf(s.my - box_cy) <= s.ey + box_hy) {
-                const float4 w1 = st[1][j];
-                s.ca = w0.z; s.cb = w0.w; s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w; s.b = w2.x; s.pmin = w2.y;
-                const float dx = px - s.mx;
-                const Quad q = column_quad(s, dx);
-                const float pmin2 = s.pmin * kLog2e;
+            const float4 w0 = st[0][j], w1 = st[1][j], w2 = st[2][j];
+            s.mx = w0.x; s.my = w0.y;
+            s.ca = w0.z; s.cb = w0.w; s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w; s.b = w2.x; s.pmin = w2.y;
+            const float dx = px - s.mx;
+            const Quad q = column_quad(s, dx);
+            const float pmin2 = s.pmin * kLog2e;
 #pragma unroll
-                for (int k = 0; k < kPix; ++k) {
-                    // one branch per pixel; the alpha floor and the stop rule are
-                    // selects inside it (the same decisions, fewer exec-mask changes)
-                    const float power2 = quad_power(q, py[k] - s.my);
-                    if (T[k] > 0.f && power2 <= 0.f && power2 >= pmin2) {
-                        const float alpha = fminf(kAlphaMax, s.op * __builtin_amdgcn_exp2f(power2));
-                        const float Tn = T[k] * (1.f - alpha);
-                        const bool on = alpha >= kAlphaMin;
-                        const bool stop = on && Tn < kTMin;
-                        const bool blend = on && !stop;
-                        const float w = blend ? alpha * T[k] : 0.f;
-                        C0[k] = __fmaf_rn(s.r, w, C0[k]);
-                        C1[k] = __fmaf_rn(s.g, w, C1[k]);
-                        C2[k] = __fmaf_rn(s.b, w, C2[k]);
-                        last[k] = blend ? b - start + (uint32_t)j + 1 : last[k];
-                        T[k] = stop ? -T[k] : (blend ? Tn : T[k]);
-                    }
+            for (int k = 0; k < kPix; ++k) {
+                // one branch per pixel; the alpha floor and the stop rule are
+                // selects inside it (the same decisions, fewer exec-mask changes)
+                const float power2 = quad_power(q, py[k] - s.my);
+                if (T[k] > 0.f && power2 <= 0.f && power2 >= pmin2) {
+                    const float alpha = fminf(kAlphaMax, s.op * __builtin_amdgcn_exp2f(power2));
+                    const float Tn = T[k] * (1.f - alpha);
+                    const bool on = alpha >= kAlphaMin;
+                    const bool stop = on && Tn < kTMin;
+                    const bool blend = on && !stop;
+                    const float w = blend ? alpha * T[k] : 0.f;
+                    C0[k] = __fmaf_rn(s.r, w, C0[k]);
+                    C1[k] = __fmaf_rn(s.g, w, C1[k]);
+                    C2[k] = __fmaf_rn(s.b, w, C2[k]);
+                    last[k] = blend ? b - start + (uint32_t)j + 1 : last[k];
+                    T[k] = stop ? -T[k] : (blend ? Tn : T[k]);
                 }
-                // a pixel can only stop on a splat that reaches it
-                any = false;
-#pragma unroll
-                for (int k = 0; k < kPix; ++k) any = any || T[k] > 0.f;
-                if (__ballot(any) == 0) break;
             }
+            // a pixel can only stop on a splat that reaches it
+            any = false;
+#pragma unroll
+            for (int k = 0; k < kPix; ++k) any = any || T[k] > 0.f;
+            if (__ballot(any) == 0) break;
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
@@ -304,21 +307,24 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        const int cnt = (int)min((uint32_t)kWave, stop - b);
+        // a splat that reaches alpha >= 1/255 nowhere in this wave's pixels
+        // passes nothing back (the extents are conservative): each lane tests
+        // the record it holds, and the walk visits only the others, back to front
+        uint64_t todo = __ballot(lane < cnt && fabsf(c0.x - box_cx) <= c2.z + box_hx &&
+                                 fabsf(c0.y - box_cy) <= c2.w + box_hy);
         if (bi > 0) {
             cid = values[start + b - kWave + lane];
             const float4* r = reinterpret_cast<const float4*>(splats + cid);
             c0 = r[0]; c1 = r[1]; c2 = r[2];
         }
-        const int cnt = (int)min((uint32_t)kWave, stop - b);
-        for (int j = cnt - 1; j >= 0; --j) {
+        while (todo != 0) {
+            const int j = 63 - (int)__builtin_clzll(todo);
+            todo ^= 1ull << j;
             const uint32_t pos = b + (uint32_t)j;
             SplatReg s;
             {
-                const float4 w0 = st[0][j], w2 = st[2][j];
-                // a splat that reaches alpha >= 1/255 nowhere in this wave's
-                // pixels passes nothing back (the extents are conservative)
-                if (!(fabsf(w0.x - box_cx) <= w2.z + box_hx && fabsf(w0.y - box_cy) <= w2.w + box_hy)) continue;
-                const float4 w1 = st[1][j];
+                const float4 w0 = st[0][j], w1 = st[1][j], w2 = st[2][j];
                 s.mx = w0.x; s.my = w0.y; s.ca = w0.z; s.cb = w0.w;
                 s.cc = w1.x; s.op = w1.y; s.r = w1.z; s.g = w1.w;
                 s.b = w2.x; s.pmin = w2.y;

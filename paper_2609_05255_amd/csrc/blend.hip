@@ -84,6 +84,31 @@ __device__ __forceinline__ float row_sum(float v)
     return v;
 }
 
+// Whether the splat's alpha >= 1/255 region (power >= power_min, i.e. the
+// conic's quadratic form q(u, v) = a u^2 + 2 b u v + c v^2 at most
+// r2 = -2 power_min) meets the box [x_lo, x_hi] x [y_lo, y_hi] of the wave's
+// pixel centres. The least q over the box is 0 when the mean lies inside it,
+// else it is on an edge, where q is a parabola in the free coordinate: its
+// vertex, clamped to the edge. The margin, 1e-3 plus 1e-5 of the largest sum
+// of the three terms' magnitudes over the box, is far above the rounding of
+// this evaluation and of the per-pixel power (a few ulp of that sum), so a
+// splat found apart from the box reaches power_min at none of its pixels.
+__device__ __forceinline__ bool ellipse_meets_box(float mx, float my, float a, float b, float c, float pmin,
+                                                  float x_lo, float x_hi, float y_lo, float y_hi)
+{
+    const float r2 = -2.f * pmin;
+    const float u0 = x_lo - mx, u1 = x_hi - mx, v0 = y_lo - my, v1 = y_hi - my;
+    const float ia = __builtin_amdgcn_rcpf(a), ic = __builtin_amdgcn_rcpf(c);
+    auto q = [&](float u, float v) { return a * u * u + 2.f * b * u * v + c * v * v; };
+    auto on_u = [&](float u) { return q(u, fminf(fmaxf(-b * u * ic, v0), v1)); };   // edge of fixed u
+    auto on_v = [&](float v) { return q(fminf(fmaxf(-b * v * ia, u0), u1), v); };   // edge of fixed v
+    const bool inside = u0 <= 0.f && u1 >= 0.f && v0 <= 0.f && v1 >= 0.f;
+    const float qmin = inside ? 0.f : fminf(fminf(on_u(u0), on_u(u1)), fminf(on_v(v0), on_v(v1)));
+    const float um = fmaxf(fabsf(u0), fabsf(u1)), vm = fmaxf(fabsf(v0), fabsf(v1));
+    const float terms = a * um * um + c * vm * vm + 2.f * fabsf(b) * um * vm;
+    return qmin <= r2 + (1e-3f + 1e-5f * terms);
+}
+
 }  // namespace
 
 template <int kPix>
@@ -143,9 +168,13 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         // skip the splats that reach alpha >= 1/255 nowhere in this wave's
         // pixels: each lane tests the record it holds (before the next batch
-        // replaces it), and the walk below visits only the others, in order
+        // replaces it; the bounding box first, then the ellipse), and the walk
+        // below visits only the others, in order
         const int cnt = (int)min((uint32_t)kWave, end - b);
-        const bool meets = lane < cnt && fabsf(c0.x - box_cx) <= c2.z + box_hx && fabsf(c0.y - box_cy) <= c2.w + box_hy;
+        const bool meets = lane < cnt && fabsf(c0.x - box_cx) <= c2.z + box_hx &&
+                           fabsf(c0.y - box_cy) <= c2.w + box_hy &&
+                           ellipse_meets_box(c0.x, c0.y, c0.z, c0.w, c1.x, c2.y, box_cx - box_hx, box_cx + box_hx,
+                                             box_lo, box_hi);
         uint64_t todo = __ballot(meets);
         if (b + kWave + lane < end) {
             const float4* p = reinterpret_cast<const float4*>(splats + values[b + kWave + lane]);
@@ -309,10 +338,13 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         const int cnt = (int)min((uint32_t)kWave, stop - b);
         // a splat that reaches alpha >= 1/255 nowhere in this wave's pixels
-        // passes nothing back (the extents are conservative): each lane tests
-        // the record it holds, and the walk visits only the others, back to front
+        // passes nothing back: each lane tests the record it holds (the
+        // conservative bounding box, then the ellipse), and the walk visits only
+        // the others, back to front
         uint64_t todo = __ballot(lane < cnt && fabsf(c0.x - box_cx) <= c2.z + box_hx &&
-                                 fabsf(c0.y - box_cy) <= c2.w + box_hy);
+                                 fabsf(c0.y - box_cy) <= c2.w + box_hy &&
+                                 ellipse_meets_box(c0.x, c0.y, c0.z, c0.w, c1.x, c2.y, box_cx - box_hx,
+                                                   box_cx + box_hx, box_lo, box_hi));
         if (bi > 0) {
             cid = values[start + b - kWave + lane];
             const float4* r = reinterpret_cast<const float4*>(splats + cid);

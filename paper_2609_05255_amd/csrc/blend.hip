@@ -1,16 +1,19 @@
 // Tile blend (Sec. 3.1) and its reverse. A 16x16 tile is covered by 4/PIX
-// independent wave64s; wave w owns the 4 PIX contiguous rows from 4 PIX w, and
-// every lane PIX pixels of one column (rows 4k apart), so a lane's pixels
-// share dx and the quadratic form costs two fused multiply-adds per pixel.
-// Each wave walks the tile's depth-sorted list in batches of 64 splats: every
-// lane gathers one record (the next batch is fetched while the current one is
-// blended), the batch is staged in the wave's own LDS slot, and each splat is
-// then read back by the whole wave from one address (a broadcast read). No
-// workgroup barriers; a wave stops when its own pixels are done.
+// independent wave64s (PIX = 2 in the forward, 4 in the backward); wave w owns
+// the 4 PIX contiguous rows from 4 PIX w, and every lane PIX pixels of one
+// column (rows 4k apart), so a lane's pixels share dx and the quadratic form
+// costs two fused multiply-adds per pixel. Each wave walks the tile's
+// depth-sorted list in batches of 64 splats: every lane gathers one record
+// (the next batch is fetched while the current one is blended) and tests it
+// against the wave's pixels, the batch is staged in the wave's own LDS slot,
+// and each splat that passes is then read back by the whole wave from one
+// address (a broadcast read). No workgroup barriers; a wave stops when its own
+// pixels are done.
 //
 // Workgroup ids are mapped to tiles so that each XCD (workgroups are dealt
 // round-robin over the 8 XCDs) renders a contiguous band of tiles, whose lists
-// share most splats in that XCD's L2.
+// share most splats in that XCD's L2; the backward of images up to 32768 tiles
+// takes them longest walk first instead (the tile order below).
 #include "gs_internal.h"
 
 namespace gsr {
@@ -19,9 +22,11 @@ namespace {
 
 constexpr int kXcds = 8;
 
-// Pixels per lane of the forward and the backward (1, 2 or 4).
+// Pixels per lane of the forward and the backward (1, 2 or 4). The forward's
+// two waves per tile halve the longest walks' time, which sets its end (its
+// tiles' walks differ by 3x and cannot be ordered before blending).
 #ifndef GS_FWD_PIX
-#define GS_FWD_PIX 4
+#define GS_FWD_PIX 2
 #endif
 #ifndef GS_BWD_PIX
 #define GS_BWD_PIX 4

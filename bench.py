@@ -122,15 +122,19 @@ def appearance_bytes(kind: str, sh_degree: int = 3) -> int:
 def algorithmic_bytes(kernel: str, n: int, vis: float, kind: str, pairs: float = 0.0, sh_degree: int = 3):
     """HBM bytes a launch (or stage) must move at minimum, averaged over cameras."""
     app = appearance_bytes(kind, sh_degree)
+    # SH3 hands the backward the colour's 40-byte direction Jacobian (9 floats and the clamp bits)
+    # in place of a second read of the coefficients
+    jac = 40 if kind == "sh3" else 0
     if kernel == "preprocess":
         # params 44 B + tiles 4 B + depth key 4 B per Gaussian; appearance + 48 B of projected splat
-        # (mean 8, conic 12, opacity 4, colour 12, rectangle 8, depth 4) per visible one; the record
-        # written is 64 B, the rest being the blend's early-skip fields
-        return n * (44 + 8) + vis * (app + 48)
+        # (mean 8, conic 12, opacity 4, colour 12, rectangle 8, depth 4) + the Jacobian per visible
+        # one; the record written is 64 B, the rest being the blend's early-skip fields
+        return n * (44 + 8) + vis * (app + 48 + jac)
     if kernel == "preprocess_bwd":
-        # tiles 4 B + dense gradient writes per Gaussian; params, accumulators and appearance per visible one
+        # tiles 4 B + dense gradient writes per Gaussian; params, accumulators and appearance (SH3:
+        # its Jacobian) per visible one
         grad = 44 + 4 * {"sh3": 48, "latent": 14, "neural": 11, "neural_raw16": 19, "nasg": 11, "nasgabor": 12}[kind]
-        return n * (4 + grad) + vis * (44 + 36 + app)
+        return n * (4 + grad) + vis * (44 + 36 + (jac or app))
     if kernel == "bin_sort":
         # scan and pair emission: 8 B per Gaussian (tiles, offset), 16 B per visible one (rectangle,
         # depth, index), 12 B per pair written; the sort's lower bound: one read and one write of
@@ -264,7 +268,10 @@ def measure(gs, inputs, torch, cfg_name: str, kind: str, args, arch=None, train=
            "hbm_stages": hbm, "alu_stages": alu}
 
     if render:
-        # forward only (preprocess, binning, blend): the paper's rendering rate
+        # forward only (preprocess, binning, blend): the paper's rendering rate;
+        # no backward follows, so the preprocess writes no colour Jacobian for it
+        jac = fr.pre.color_jac
+        fr.pre.color_jac = None
         for i in range(args.warmup):
             fr.forward(cstructs[i % ncam], st, stream=stream, sync_pairs=False)
         torch.cuda.synchronize()
@@ -273,6 +280,7 @@ def measure(gs, inputs, torch, cfg_name: str, kind: str, args, arch=None, train=
             fr.forward(cstructs[i % ncam], st, stream=stream, sync_pairs=False)
         torch.cuda.synchronize()
         t_r = (time.perf_counter() - t_start) / args.steps
+        fr.pre.color_jac = jac
         out["render_only"] = {"it_s": round(1.0 / t_r, 3), "ms_per_frame": round(1e3 * t_r, 4),
                               "mpix_per_s": round(cfg.width * cfg.height / t_r / 1e6, 2)}
 
@@ -308,7 +316,12 @@ def measure(gs, inputs, torch, cfg_name: str, kind: str, args, arch=None, train=
                              "optimizer": "fused Adam over every parameter tensor, one launch per step"}
         if kid == gs.GS_APP_SH3:
             # the same training step with the Adam update applied inside the
-            # backward (gs_render_bwd_adam): no gradient is written or read back
+            # backward (gs_render_bwd_adam): no gradient is written or read back;
+            # that backward reads the coefficients for the update anyway, so its
+            # forward writes no colour Jacobian
+            jac = fr.pre.color_jac
+            fr.pre.color_jac = None
+
             def train_in_bwd(i):
                 c = cstructs[i % ncam]
                 fr.forward(c, st, stream=stream, sync_pairs=False)
@@ -328,6 +341,7 @@ def measure(gs, inputs, torch, cfg_name: str, kind: str, args, arch=None, train=
             torch.cuda.synchronize()
             kt_in = timer.read()
             gs.Timer.detach()
+            fr.pre.color_jac = jac
             pb_ms, pb_n = kt_in["preprocess_bwd"]
             pb_ms /= max(pb_n, 1)
             out["train_step_adam_in_bwd"] = {

@@ -172,6 +172,15 @@ typedef struct gs_preprocessed {
     uint32_t* tiles_touched;  /* [n] tiles of the rectangle; 0 = culled */
     uint32_t* depth_key;      /* [n] sort key: bit pattern of depth, 0xFFFFFFFF when culled */
     uint64_t* num_pairs;      /* [1] total tiles touched (number of pairs P) */
+    float* color_jac;         /* optional, SH3 only (NULL: not written or read): [10][n] for the
+                                 backward, meaningful for visible Gaussians. Row 3c + j: the
+                                 derivative of colour channel c's sum 0.5 + sum_k Y_k(d) sh_k
+                                 (eq. sh_color_eval before the clamp) by direction
+                                 component d_j; row 9: bit c set where channel c is above zero
+                                 (not clamped), stored as the bits of a u32. Given here and to
+                                 gs_render_bwd, the backward takes the colour's view-direction
+                                 term from these 40 bytes instead of re-reading the 192 bytes of
+                                 coefficients. */
 } gs_preprocessed;
 
 /* Gradients, caller-allocated device arrays, OVERWRITTEN by gs_render_bwd
@@ -307,6 +316,10 @@ gs_status gs_render_work(const gs_camera* cam, const gs_preprocessed* pre, int64
  * the preprocess per Gaussian; for LATENT_MLP also the decoder weights.
  * dL_dimage: [3][H][W] fp32 device. The pair-level accumulation uses float
  * atomics, so results vary in the last bits between runs.
+ * pre: as gs_preprocess left it for this camera; for SH3, pre->color_jac must be
+ *   NULL (the coefficients are read again) or the array that gs_preprocess
+ *   filled (its Jacobian is used instead); either gives the same gradients up to
+ *   rounding.
  * workspace: at least gs_workspace_size(n, width, height, ...) bytes for this
  *   camera's image size (it holds the per-Gaussian accumulators and an order
  *   of the tiles: images of up to 32768 tiles are walked longest list walk
@@ -400,6 +413,8 @@ gs_status gs_adam_step(const gs_adam_tensor* tensors, int32_t count, float beta1
  *   gs_adam_step (the step whose bias corrections apply, >= 1).
  * grads: every array may be NULL here; one that is not receives the gradient
  *   the update used (dmean2d as for gs_render_bwd).
+ * pre->color_jac is not read: the update reads the coefficients anyway, so the
+ *   forward before this call may be given color_jac = NULL.
  * Errors: as gs_render_bwd; GS_ERR_INVALID_ARG when a tensor's param, rows or n
  *   does not match, a moment or lr array is NULL, or a constant is out of range.
  */

@@ -33,6 +33,7 @@ struct BwdArgs {
     const float* base_color;
     const uint16_t* features;
     const uint32_t* tiles_touched;
+    const float* color_jac;
     const float* acc;
     float* dmeans;
     float* dlog_scales;
@@ -242,18 +243,28 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_bwd_sh3(BwdArgs a)
         const float d0 = vx * il, d1 = vy * il, d2 = vz * il;
         sh_basis16(d0, d1, d2, Y);
         if (a.sh_y0_folded) Y[0] = 1.f;   // constant either way: no direction gradient
-        float coef[GS_SH_COEFFS];
-        float pre[3] = {0.5f, 0.5f, 0.5f};
-        for (int k = 0; k < 16; ++k)
-            for (int c = 0; c < 3; ++c) {
-                coef[3 * k + c] = k < nb ? __builtin_nontemporal_load(a.sh + (3 * k + c) * n + i) : 0.f;
-                pre[c] += Y[k] * coef[3 * k + c];
-            }
-        for (int c = 0; c < 3; ++c) gc[c] = pre[c] > 0.f ? g9[6 + c] : 0.f;
-        float dY[16];
-        for (int k = 0; k < 16; ++k) dY[k] = coef[3 * k] * gc[0] + coef[3 * k + 1] * gc[1] + coef[3 * k + 2] * gc[2];
         float dd[3] = {0.f, 0.f, 0.f};
-        sh_basis16_vjp(d0, d1, d2, dY, dd);
+        if (a.color_jac) {
+            // the forward's direction Jacobian of the colour sums and their clamp
+            float J[9];
+            for (int r = 0; r < 9; ++r) J[r] = __builtin_nontemporal_load(a.color_jac + r * n + i);
+            const uint32_t up = __float_as_uint(__builtin_nontemporal_load(a.color_jac + 9 * n + i));
+            for (int c = 0; c < 3; ++c) gc[c] = (up >> c) & 1u ? g9[6 + c] : 0.f;
+            for (int j = 0; j < 3; ++j) dd[j] = gc[0] * J[j] + gc[1] * J[3 + j] + gc[2] * J[6 + j];
+        } else {
+            float coef[GS_SH_COEFFS];
+            float pre[3] = {0.5f, 0.5f, 0.5f};
+            for (int k = 0; k < 16; ++k)
+                for (int c = 0; c < 3; ++c) {
+                    coef[3 * k + c] = k < nb ? __builtin_nontemporal_load(a.sh + (3 * k + c) * n + i) : 0.f;
+                    pre[c] += Y[k] * coef[3 * k + c];
+                }
+            for (int c = 0; c < 3; ++c) gc[c] = pre[c] > 0.f ? g9[6 + c] : 0.f;
+            float dY[16];
+            for (int k = 0; k < 16; ++k)
+                dY[k] = coef[3 * k] * gc[0] + coef[3 * k + 1] * gc[1] + coef[3 * k + 2] * gc[2];
+            sh_basis16_vjp(d0, d1, d2, dY, dd);
+        }
         // d = v / |v|: dv = (dd - d (d . dd)) / |v|
         const float dot = d0 * dd[0] + d1 * dd[1] + d2 * dd[2];
         gg.dmu[0] += (dd[0] - d0 * dot) * il;
@@ -791,6 +802,7 @@ hipError_t launch_preprocess_bwd(const Cam& cam, const gs_gaussians& g, const gs
     a.base_color = app.base_color;
     a.features = app.features;
     a.tiles_touched = pre.tiles_touched;
+    a.color_jac = app.kind == GS_APP_SH3 ? pre.color_jac : nullptr;
     a.acc = ws.acc;
     a.dmeans = gr.dmeans;
     a.dlog_scales = gr.dlog_scales;

@@ -143,6 +143,7 @@ struct PreArgs {
     const float* lobes;
     int sh_y0_folded;
     gs_splat* splats;
+    float* color_jac;
     uint32_t* tiles_touched;
     uint32_t* depth_key;
     uint32_t* block_pairs;
@@ -251,7 +252,8 @@ __device__ __forceinline__ void view_dir(const Cam& c, const float mu[3], float 
 
 // eq. sh_color_eval: c = max(0, 0.5 + sum over bands <= kDeg of Y_k(d) sh_k),
 // with Y_0 = 1 when the stored DC coefficients have Y0 folded in.
-// All coefficient loads are issued together, before the sums need them.
+// All coefficient loads are issued together, before the sums need them; the
+// sums are explicit fused multiply-adds so that sh_color_jac matches them.
 template <int kDeg>
 __device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n, int i, const float d[3],
                                          bool y0_folded, float col[3])
@@ -267,9 +269,35 @@ __device__ __forceinline__ void sh_color(const float* __restrict__ sh, int64_t n
     for (int ch = 0; ch < 3; ++ch) {
         float acc = 0.5f;
 #pragma unroll
-        for (int k = 0; k < nb; ++k) acc += Y[k] * c[3 * k + ch];
+        for (int k = 0; k < nb; ++k) acc = fmaf(Y[k], c[3 * k + ch], acc);
         col[ch] = acc > 0.f ? acc : 0.f;
     }
+}
+
+// sh_color, and with it what the backward needs of the colour's dependence on
+// the view direction: jac[3 c + j] = d(0.5 + sum_k Y_k sh_k[c]) / d d_j over
+// the active bands, and the channels above zero as bits of `unclamped`.
+template <int kDeg>
+__device__ __forceinline__ void sh_color_jac(const float* __restrict__ sh, int64_t n, int i, const float d[3],
+                                             bool y0_folded, float col[3], float jac[9], uint32_t& unclamped)
+{
+    constexpr int nb = (kDeg + 1) * (kDeg + 1);
+    float c[3 * nb];
+#pragma unroll
+    for (int k = 0; k < 3 * nb; ++k) c[k] = __builtin_nontemporal_load(sh + (int64_t)k * n + i);
+    float Y[16];
+    sh_basis16(d[0], d[1], d[2], Y);
+    if (y0_folded) Y[0] = 1.f;
+    unclamped = 0u;
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) {
+        float acc = 0.5f;
+#pragma unroll
+        for (int k = 0; k < nb; ++k) acc = fmaf(Y[k], c[3 * k + ch], acc);   // as sh_color, bit for bit
+        col[ch] = acc > 0.f ? acc : 0.f;
+        unclamped |= acc > 0.f ? 1u << ch : 0u;
+    }
+    sh_color_jacobian(d[0], d[1], d[2], c, nb, jac);   // Y_0 is constant: k >= 1 only
 }
 
 template <int kDeg>
@@ -289,7 +317,17 @@ __global__ __launch_bounds__(kBlock) void k_preprocess_sh3(PreArgs a)
         if (g.visible) {
             float d[3];
             view_dir(a.cam, mu, d);
-            sh_color<kDeg>(a.sh, a.n, i, d, a.sh_y0_folded != 0, col);
+            if (a.color_jac) {
+                float jac[9];
+                uint32_t unclamped;
+                sh_color_jac<kDeg>(a.sh, a.n, i, d, a.sh_y0_folded != 0, col, jac, unclamped);
+                const int64_t n = a.n;
+#pragma unroll
+                for (int r = 0; r < 9; ++r) __builtin_nontemporal_store(jac[r], a.color_jac + r * n + i);
+                __builtin_nontemporal_store(__uint_as_float(unclamped), a.color_jac + 9 * n + i);
+            } else {
+                sh_color<kDeg>(a.sh, a.n, i, d, a.sh_y0_folded != 0, col);
+            }
             tiles = g.tiles;
         }
         a.tiles_touched[i] = tiles;
@@ -535,6 +573,7 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     a.lobes = app.lobes;
     a.sh_y0_folded = app.sh_y0_folded;
     a.splats = out.splats;
+    a.color_jac = app.kind == GS_APP_SH3 ? out.color_jac : nullptr;
     a.tiles_touched = out.tiles_touched;
     a.depth_key = out.depth_key;
     a.block_pairs = ws.block_pairs;

@@ -19,8 +19,11 @@ constexpr float kSH3c = -0.45704579946446572f;  // -sqrt(21/(2 pi))/4
 constexpr float kSH3d = 0.37317633259011546f;   // sqrt(7/pi)/4
 constexpr float kSH3e = 1.4453057213202769f;    // sqrt(105/pi)/4
 
+// Taken without fused multiply-adds, so that every kernel that inlines it gets
+// the same bits whatever else it computes from x, y, z beside it.
 __device__ __forceinline__ void sh_basis16(float x, float y, float z, float Y[16])
 {
+#pragma clang fp contract(off)
     const float xx = x * x, yy = y * y, zz = z * z;
     Y[0] = kSH0;
     Y[1] = -kSH1 * y;
@@ -88,6 +91,39 @@ __device__ __forceinline__ void sh_basis16_vjp(float x, float y, float z, const 
     dd[0] += gx;
     dd[1] += gy;
     dd[2] += gz;
+}
+
+// jac[3 c + j] = sum over the bands below nb (k >= 1) of coef[3 k + c] dY_k/dx_j:
+// the direction Jacobian of the three colour sums, one pass over the basis.
+__device__ __forceinline__ void sh_color_jacobian(float x, float y, float z, const float* coef, int nb,
+                                                  float jac[9])
+{
+    const float xx = x * x, yy = y * y, zz = z * z;
+    for (int r = 0; r < 9; ++r) jac[r] = 0.f;
+    auto add = [&](int k, float gx, float gy, float gz) {
+        if (k >= nb) return;
+        for (int c = 0; c < 3; ++c) {
+            const float w = coef[3 * k + c];
+            jac[3 * c] += w * gx;
+            jac[3 * c + 1] += w * gy;
+            jac[3 * c + 2] += w * gz;
+        }
+    };
+    add(1, 0.f, -kSH1, 0.f);
+    add(2, 0.f, 0.f, kSH1);
+    add(3, -kSH1, 0.f, 0.f);
+    add(4, kSH2a * y, kSH2a * x, 0.f);
+    add(5, 0.f, -kSH2a * z, -kSH2a * y);
+    add(6, -2.f * kSH2b * x, -2.f * kSH2b * y, 4.f * kSH2b * z);
+    add(7, -kSH2a * z, 0.f, -kSH2a * x);
+    add(8, 2.f * kSH2c * x, -2.f * kSH2c * y, 0.f);
+    add(9, 6.f * kSH3a * x * y, 3.f * kSH3a * (xx - yy), 0.f);
+    add(10, kSH3b * y * z, kSH3b * x * z, kSH3b * x * y);
+    add(11, -2.f * kSH3c * x * y, kSH3c * (4.f * zz - xx - 3.f * yy), 8.f * kSH3c * y * z);
+    add(12, -6.f * kSH3d * x * z, -6.f * kSH3d * y * z, kSH3d * (6.f * zz - 3.f * xx - 3.f * yy));
+    add(13, kSH3c * (4.f * zz - 3.f * xx - yy), -2.f * kSH3c * x * y, 8.f * kSH3c * x * z);
+    add(14, 2.f * kSH3e * x * z, -2.f * kSH3e * y * z, kSH3e * (xx - yy));
+    add(15, 3.f * kSH3a * (xx - yy), -6.f * kSH3a * x * y, 0.f);
 }
 
 }  // namespace gsr

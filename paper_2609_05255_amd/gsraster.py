@@ -65,7 +65,7 @@ class Appearance(C.Structure):
 
 class Preprocessed(C.Structure):
     _fields_ = [("splats", C.c_void_p), ("tiles_touched", C.c_void_p), ("depth_key", C.c_void_p),
-                ("num_pairs", C.c_void_p)]
+                ("num_pairs", C.c_void_p), ("color_jac", C.c_void_p)]
 
 
 class Grads(C.Structure):
@@ -394,8 +394,10 @@ class Frame:
         raw16 = neural_arch is not None and bool(neural_arch[2])
         self.dfeatures = torch.empty(16 if raw16 else NEURAL_FEATURES, nn, device=d) if kind == GS_APP_NEURAL else None
         self.dlobes = torch.empty(LOBE_ROWS[kind], nn, device=d) if kind in LOBE_ROWS else None
+        # SH3: the colour's view-direction Jacobian, for the backward (gs_preprocessed.color_jac)
+        self.color_jac = torch.empty(10 * nn, dtype=torch.float32, device=d) if kind == GS_APP_SH3 else None
         self.pre = Preprocessed(_ptr(self.splats), _ptr(self.tiles_touched), _ptr(self.depth_key),
-                                _ptr(self.num_pairs))
+                                _ptr(self.num_pairs), _ptr(self.color_jac))
         self.grads = Grads(_ptr(self.dmeans), _ptr(self.dlog_scales), _ptr(self.dquats),
                            _ptr(self.dopacity_logits), _ptr(self.dsh), _ptr(self.dlatent), _ptr(self.dmlp_w),
                            _ptr(self.dmean2d), _ptr(self.dbase_color), _ptr(self.dfeatures), _ptr(self.dlobes))

@@ -104,6 +104,38 @@ def test_backward_tile_order_limit(tiles_x):
     check_all(sc, tiny_camera(16 * tiles_x, 256), label="wide-bwd-%d" % tiles_x)
 
 
+@pytest.mark.parametrize("degree", [3, 1])
+def test_sh3_backward_without_the_colour_jacobian(degree):
+    # gs_preprocessed.color_jac NULL: the preprocess writes no view-direction
+    # Jacobian and the backward re-reads the SH coefficients instead. The same
+    # gradients as with it (the oracle checks the Jacobian path in every other
+    # SH3 case), to the float atomics' summation order and a few ulp of the two
+    # evaluation orders of the direction term.
+    sc = inputs.make_scene("medium")
+    cam = inputs.make_cameras("medium")[6]
+    say("case SH3 backward from the coefficients, degree %d" % degree)
+    up = torch.from_numpy(inputs.make_upstream_grad(cam.width, cam.height, 6)).cuda()
+    st = gs.SceneTensors(sc)
+    cs = gs.camera_struct(cam)
+    out = []
+    for jac in (True, False):
+        fr = gs.Frame(sc.n, cam.width, cam.height, gs.GS_APP_SH3, 1 << 22)
+        if not jac:
+            fr.pre.color_jac = None
+        fr.forward(cs, st, degree)
+        fr.backward(cs, st, up, degree)
+        torch.cuda.synchronize()
+        out.append({k: getattr(fr, k).clone() for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh")})
+        out[-1]["image"] = fr.image.clone()
+    assert torch.equal(out[0]["image"], out[1]["image"])
+    for k in ("dmeans", "dlog_scales", "dquats", "dopacity_logits", "dsh"):
+        a, b = out[0][k], out[1][k]
+        scale = float(b.abs().max())
+        err = float((a - b).abs().max())
+        say("  %s: max |diff| %.2e of max |grad| %.2e" % (k, err, scale))
+        assert bool(((a - b).abs() <= 1e-4 * b.abs() + 1e-6 * scale).all()), k
+
+
 def test_capacity_retry():
     sc = inputs.make_scene("tiny")
     check_all(sc, inputs.make_cameras("tiny")[0], capacity=100, label="capacity")

@@ -529,8 +529,8 @@ gs_status render_bwd(const gs_camera* cam, const gs_gaussians* g, const gs_appea
     }
     const bool ordered = tile_order_supported(c);
     timing_begin(GS_KERNEL_BWD_PREP, s);
-    GS_HIP(launch_clear(ws.acc, (int64_t)kAccStride * g->n, s));
-    if (ordered) GS_HIP(launch_tile_order(c, tile_ranges, n_contrib, ws.walk_cls, ws.tile_order, s));
+    GS_HIP(launch_bwd_prep(c, tile_ranges, n_contrib, ws.acc, (int64_t)kAccStride * g->n, ws.walk_cls,
+                           ordered ? ws.tile_order : nullptr, s));
     timing_end(GS_KERNEL_BWD_PREP, s);
     timing_begin(GS_KERNEL_BLEND_BWD, s);
     GS_HIP(launch_blend_bwd(c, pre->splats, values, tile_ranges, final_T, n_contrib, dL_dimage,

@@ -214,10 +214,13 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
                     T[k] = stop ? -T[k] : (blend ? Tn : T[k]);
                 }
             }
-            // a pixel can only stop on a splat that reaches it
-            any = false;
+            // a pixel can only stop on a splat that reaches it. T > 0 is tested
+            // on its bits (T is never NaN): an integer maximum, where a float
+            // one would first be canonicalised
+            int tmax = __float_as_int(T[0]);
 #pragma unroll
-            for (int k = 0; k < kPix; ++k) any = any || T[k] > 0.f;
+            for (int k = 1; k < kPix; ++k) tmax = max(tmax, __float_as_int(T[k]));
+            any = tmax > 0;
             if (__ballot(any) == 0) break;
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -490,12 +493,13 @@ __device__ __forceinline__ uint32_t walk_class(uint32_t walk)
     return min(b - (127u << 4), (uint32_t)kWalkClasses - 1);   // 2^32 - 1 rounds up to 2^32
 }
 
-__global__ __launch_bounds__(kBlock) void k_tile_walk(Cam cam, const uint32_t* __restrict__ ranges,
-                                                      const uint32_t* __restrict__ n_contrib,
-                                                      uint32_t* __restrict__ walk_cls)
+// Walk class of each tile, one wave per tile (workgroup `blk` of the walk).
+__device__ __forceinline__ void tile_walk(const Cam& cam, const uint32_t* __restrict__ ranges,
+                                          const uint32_t* __restrict__ n_contrib, uint32_t* __restrict__ walk_cls,
+                                          int blk)
 {
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    const int tile = (int)blockIdx.x * (kBlock / kWave) + (int)(threadIdx.x / kWave);
+    const int tile = blk * (kBlock / kWave) + (int)(threadIdx.x / kWave);
     if (tile >= n_tiles) return;   // whole waves
     const int lane = __lane_id();
     const int tx = tile % cam.tiles_x, ty = tile / cam.tiles_x;
@@ -508,6 +512,31 @@ __global__ __launch_bounds__(kBlock) void k_tile_walk(Cam cam, const uint32_t* _
     }
     for (int o = 32; o > 0; o >>= 1) walk = max(walk, (uint32_t)__shfl_xor((int)walk, o));
     if (lane == 0) walk_cls[tile] = walk_class(min(walk, ranges[2 * tile + 1] - ranges[2 * tile]));
+}
+
+// Zeroes p[0, count) as workgroup `blk` of `nblk` (16-byte stores, grid-stride).
+__device__ __forceinline__ void clear_part(float* __restrict__ p, int64_t count, int blk, int nblk)
+{
+    const int64_t c4 = count >> 2;
+    const int64_t stride = (int64_t)nblk * kBlock;
+    float4* p4 = reinterpret_cast<float4*>(p);
+    for (int64_t i = (int64_t)blk * kBlock + threadIdx.x; i < c4; i += stride) p4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (blk == 0 && threadIdx.x < (count & 3)) p[(c4 << 2) + threadIdx.x] = 0.f;
+}
+
+// The backward's preparation in one launch: the first walk_blocks workgroups
+// take the tiles' walk classes (none when the tiles are not ordered), the
+// others clear the screen-space accumulators.
+__global__ __launch_bounds__(kBlock) void k_walk_clear(Cam cam, const uint32_t* __restrict__ ranges,
+                                                       const uint32_t* __restrict__ n_contrib,
+                                                       uint32_t* __restrict__ walk_cls, int walk_blocks,
+                                                       float* __restrict__ acc, int64_t count)
+{
+    const int blk = (int)blockIdx.x;
+    if (blk < walk_blocks)
+        tile_walk(cam, ranges, n_contrib, walk_cls, blk);
+    else
+        clear_part(acc, count, blk - walk_blocks, (int)gridDim.x - walk_blocks);
 }
 
 constexpr int kOrderThreads = 1024;
@@ -543,13 +572,15 @@ __global__ __launch_bounds__(kOrderThreads) void k_tile_order(int n_tiles, const
 
 bool tile_order_supported(const Cam& cam) { return (int64_t)cam.tiles_x * cam.tiles_y <= kMaxOrderedTiles; }
 
-hipError_t launch_tile_order(const Cam& cam, const uint32_t* tile_ranges, const uint32_t* n_contrib,
-                             uint32_t* walk_cls, uint32_t* order, hipStream_t s)
+hipError_t launch_bwd_prep(const Cam& cam, const uint32_t* tile_ranges, const uint32_t* n_contrib, float* acc,
+                           int64_t acc_count, uint32_t* walk_cls, uint32_t* order, hipStream_t s)
 {
     const int n_tiles = cam.tiles_x * cam.tiles_y;
-    hipLaunchKernelGGL(k_tile_walk, dim3((unsigned)div_up(n_tiles, kBlock / kWave)), dim3(kBlock), 0, s, cam,
-                       tile_ranges, n_contrib, walk_cls);
-    hipLaunchKernelGGL(k_tile_order, dim3(1), dim3(kOrderThreads), 0, s, n_tiles, walk_cls, order);
+    const int walk_blocks = order ? (int)div_up(n_tiles, kBlock / kWave) : 0;
+    const int clear_blocks = (int)std::min<int64_t>(std::max<int64_t>(div_up(acc_count >> 2, kBlock), 1), 4096);
+    hipLaunchKernelGGL(k_walk_clear, dim3((unsigned)(walk_blocks + clear_blocks)), dim3(kBlock), 0, s, cam,
+                       tile_ranges, n_contrib, walk_cls, walk_blocks, acc, acc_count);
+    if (order) hipLaunchKernelGGL(k_tile_order, dim3(1), dim3(kOrderThreads), 0, s, n_tiles, walk_cls, order);
     return hipGetLastError();
 }
 
@@ -651,12 +682,7 @@ hipError_t launch_blend_count(const Cam& cam, const gs_splat* splats, const uint
 // a captured graph.
 __global__ __launch_bounds__(kBlock) void k_clear(float* __restrict__ p, int64_t count)
 {
-    const int64_t c4 = count >> 2;
-    const int64_t stride = (int64_t)gridDim.x * kBlock;
-    float4* p4 = reinterpret_cast<float4*>(p);
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < c4; i += stride)
-        p4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (blockIdx.x == 0 && threadIdx.x < (count & 3)) p[(c4 << 2) + threadIdx.x] = 0.f;
+    clear_part(p, count, (int)blockIdx.x, (int)gridDim.x);
 }
 
 hipError_t launch_clear(float* p, int64_t count, hipStream_t s)

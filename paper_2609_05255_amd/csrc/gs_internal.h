@@ -155,8 +155,10 @@ hipError_t launch_clear(float* p, int64_t count, hipStream_t s);
 hipError_t launch_blend_count(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                               const uint32_t* tile_ranges, uint64_t* counts, hipStream_t s);
 bool tile_order_supported(const Cam& cam);   // at most kMaxOrderedTiles tiles
-hipError_t launch_tile_order(const Cam& cam, const uint32_t* tile_ranges, const uint32_t* n_contrib,
-                             uint32_t* walk_cls, uint32_t* order, hipStream_t s);
+// The backward's preparation: acc[0, acc_count) cleared and, when `order` is
+// given, the tiles' launch order, longest walk first (walk_cls: n_tiles scratch).
+hipError_t launch_bwd_prep(const Cam& cam, const uint32_t* tile_ranges, const uint32_t* n_contrib, float* acc,
+                           int64_t acc_count, uint32_t* walk_cls, uint32_t* order, hipStream_t s);
 // tile_order: NULL for the plain tile order
 hipError_t launch_blend_bwd(const Cam& cam, const gs_splat* splats, const uint32_t* values,
                             const uint32_t* tile_ranges, const float* final_T, const uint32_t* n_contrib,

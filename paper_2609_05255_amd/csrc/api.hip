@@ -311,10 +311,11 @@ gs_status preprocess_run(const gs_camera* cam, const gs_gaussians* g, const gs_a
     const Cam c = make_cam(*cam);
     if (g->n > 0) {
         timing_begin(GS_KERNEL_PREPROCESS, s);
-        GS_HIP(launch_preprocess(c, *g, *app, *out, ws, s));
+        int slots = 0;
+        GS_HIP(launch_preprocess(c, *g, *app, *out, ws, &slots, s));
         timing_end(GS_KERNEL_PREPROCESS, s);
         timing_begin(GS_KERNEL_PAIR_COUNT, s);
-        GS_HIP(launch_pair_count(g->n, app->kind, ws, out->num_pairs, s));
+        GS_HIP(launch_pair_count(slots, ws, out->num_pairs, s));
         timing_end(GS_KERNEL_PAIR_COUNT, s);
     } else {
         GS_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(out->num_pairs), 2, 0u, s));
@@ -338,11 +339,14 @@ gs_status preprocess_checks(const gs_camera* cam, const gs_gaussians* g, const g
 
 }  // namespace
 
-// The preprocess's scratch for callers that cannot allocate: the per-wave tile
-// sums of up to GS_NOALLOC_MAX_GAUSSIANS Gaussians (1 MiB), one copy per GPU
-// for the life of the process. Host code reaches it only through the device
-// address hipGetSymbolAddress returns for the current device.
+// The preprocess's scratch for callers that cannot allocate: the tile sums
+// (one per workgroup, or per wave of a decoder grid) of up to
+// GS_NOALLOC_MAX_GAUSSIANS Gaussians (1 MiB), one copy per GPU for the life of
+// the process. Host code reaches it only through the device address
+// hipGetSymbolAddress returns for the current device.
 static __device__ __align__(256) uint32_t scratch[GS_NOALLOC_MAX_GAUSSIANS / kWave];
+static_assert(GS_NOALLOC_MAX_GAUSSIANS / kWave >= (GS_NOALLOC_MAX_GAUSSIANS / kBlock) * (kBlock / kWave),
+              "the scratch holds pair_count_slots(GS_NOALLOC_MAX_GAUSSIANS) sums");
 
 namespace {
 

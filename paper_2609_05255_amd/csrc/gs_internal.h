@@ -127,9 +127,10 @@ struct PairCount {
 };
 
 // ---- launch helpers (defined in the kernel files) ---------------------------
+// *slots: the number of tile sums it leaves in ws.block_pairs for the pair count
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
-                             const gs_preprocessed& out, const Workspace& ws, hipStream_t s);
-hipError_t launch_pair_count(int64_t n, int32_t kind, const Workspace& ws, uint64_t* num_pairs, hipStream_t s);
+                             const gs_preprocessed& out, const Workspace& ws, int* slots, hipStream_t s);
+hipError_t launch_pair_count(int slots, const Workspace& ws, uint64_t* num_pairs, hipStream_t s);
 hipError_t launch_depth_sort(int64_t n, const uint32_t* depth_key, const gs_splat* splats, const Workspace& ws,
                              const uint32_t** order_out, hipStream_t s);
 hipError_t launch_entry_offsets(int64_t n, PairCount pairs, const Workspace& ws, hipStream_t s);
@@ -180,8 +181,9 @@ void timing_begin(int kernel_id, hipStream_t s);
 void timing_end(int kernel_id, hipStream_t s);
 
 inline int preprocess_blocks(int64_t n) { return (int)div_up(n > 0 ? n : 1, kBlock); }
-// Slots for the preprocess tile sums (enough for one per 64 Gaussians).
-inline int pair_count_slots(int64_t n) { return (int)div_up(n > 0 ? n : 1, kWave); }
+// Slots for the preprocess tile sums: one per workgroup, or one per wave of a
+// decoder grid (at most one workgroup per 256 Gaussians).
+inline int pair_count_slots(int64_t n) { return preprocess_blocks(n) * (kBlock / kWave); }
 
 // Hidden layers of the neural decoder (0 in the struct: the paper's default, 2)
 // and its weight count.

@@ -404,6 +404,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_latent(PreArgs a)
     const int lane = __lane_id(), wave = threadIdx.x >> 6;
     const int64_t nchunks = div_up((int64_t)a.n, kWave);
     const int64_t stride = (int64_t)gridDim.x * (kBlock / kWave);
+    uint64_t wave_tiles = 0;   // the pairs of this wave's chunks
     for (int64_t chunk = (int64_t)blockIdx.x * (kBlock / kWave) + wave; chunk < nchunks; chunk += stride) {
         const int64_t base = chunk * kWave;
         const int i = (int)(base + lane);
@@ -435,9 +436,11 @@ __global__ __launch_bounds__(kBlock, 4) void k_preprocess_latent(PreArgs a)
             mlp_tile_colors(o, t, col);
         }
         store_splats_wave(a.splats, a.n, base, stage[wave], g, col);
-        const uint32_t total = wave_sum_u32(tiles);
-        if (lane == 0) a.block_pairs[chunk] = total;
+        wave_tiles += __builtin_amdgcn_readfirstlane(wave_sum_u32(tiles));   // uniform: kept in scalar registers
     }
+    // one tile sum per wave of the grid (zero for a wave without a chunk),
+    // saturated: 2^32 - 1 stands for that many pairs or more
+    if (lane == 0) a.block_pairs[blockIdx.x * (kBlock / kWave) + wave] = (uint32_t)min(wave_tiles, (uint64_t)0xFFFFFFFFu);
 }
 
 // The paper's neural appearance (neural.h): geometry per thread; each lane
@@ -464,6 +467,7 @@ __global__ __launch_bounds__(kBlock, kW == 32 ? 3 : 4) void k_preprocess_neural(
     const int lane = __lane_id(), wave = threadIdx.x >> 6;
     const int64_t nchunks = div_up((int64_t)a.n, kWave);
     const int64_t stride = (int64_t)gridDim.x * (kBlock / kWave);
+    uint64_t wave_tiles = 0;   // the pairs of this wave's chunks
     for (int64_t chunk = (int64_t)blockIdx.x * (kBlock / kWave) + wave; chunk < nchunks; chunk += stride) {
         const int64_t base = chunk * kWave;
         const int i = (int)(base + lane);
@@ -541,9 +545,11 @@ __global__ __launch_bounds__(kBlock, kW == 32 ? 3 : 4) void k_preprocess_neural(
             col[ch] = v > 0.f ? v : 0.f;
         }
         store_splats_wave(a.splats, a.n, base, stage[wave], g, col);
-        const uint32_t total = wave_sum_u32(tiles);
-        if (lane == 0) a.block_pairs[chunk] = total;
+        wave_tiles += __builtin_amdgcn_readfirstlane(wave_sum_u32(tiles));   // uniform: kept in scalar registers
     }
+    // one tile sum per wave of the grid (zero for a wave without a chunk),
+    // saturated: 2^32 - 1 stands for that many pairs or more
+    if (lane == 0) a.block_pairs[blockIdx.x * (kBlock / kWave) + wave] = (uint32_t)min(wave_tiles, (uint64_t)0xFFFFFFFFu);
 }
 
 // Workgroups of the latent preprocess: the number resident at once on 256 CUs
@@ -554,7 +560,7 @@ constexpr int kNeuralBlocks = 1024;
 constexpr int kNeuralBlocks32 = 768;
 
 hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_appearance& app,
-                             const gs_preprocessed& out, const Workspace& ws, hipStream_t s)
+                             const gs_preprocessed& out, const Workspace& ws, int* slots, hipStream_t s)
 {
     PreArgs a;
     a.cam = cam;
@@ -578,6 +584,10 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     a.depth_key = out.depth_key;
     a.block_pairs = ws.block_pairs;
     const int blocks = preprocess_blocks(g.n);
+    // the SH3 and lobe kernels leave one tile sum per workgroup, the decoders
+    // one per wave of their (capped) grid
+    constexpr int kWaves = kBlock / kWave;
+    *slots = blocks;
     if (app.kind == GS_APP_SH3) {
         switch (app.sh_degree) {
         case 0: hipLaunchKernelGGL(k_preprocess_sh3<0>, dim3(blocks), dim3(kBlock), 0, s, a); break;
@@ -588,6 +598,7 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
     }
     else if (app.kind == GS_APP_NEURAL) {
         const dim3 grid(std::min(blocks, app.neural_width == 32 ? kNeuralBlocks32 : kNeuralBlocks));
+        *slots = (int)grid.x * kWaves;
         const int layers = neural_layers(app);
         if (app.neural_width == 32) {
             hipLaunchKernelGGL((k_preprocess_neural<false, 2, false, 32>), grid, dim3(kBlock), 0, s, a);
@@ -605,20 +616,25 @@ hipError_t launch_preprocess(const Cam& cam, const gs_gaussians& g, const gs_app
         hipLaunchKernelGGL(k_preprocess_lobe<false>, dim3(blocks), dim3(kBlock), 0, s, a);
     else if (app.kind == GS_APP_NASGABOR)
         hipLaunchKernelGGL(k_preprocess_lobe<true>, dim3(blocks), dim3(kBlock), 0, s, a);
-    else if (app.kind == GS_APP_NEURAL_FOLDED)
+    else if (app.kind == GS_APP_NEURAL_FOLDED) {
+        *slots = std::min(blocks, kNeuralBlocks) * kWaves;
         hipLaunchKernelGGL((k_preprocess_neural<true, 2, false>), dim3(std::min(blocks, kNeuralBlocks)), dim3(kBlock), 0,
                            s, a);
-    else
+    } else {
+        *slots = std::min(blocks, kLatentBlocks) * kWaves;
         hipLaunchKernelGGL(k_preprocess_latent, dim3(std::min(blocks, kLatentBlocks)), dim3(kBlock), 0, s, a);
+    }
     return hipGetLastError();
 }
 
-// Total pairs = sum of the per-wave tile counts (fixed order, one workgroup).
-// The counts sit at the 256-byte-aligned start of their workspace slice, so
-// each thread reads runs of four with 16-byte loads, all issued before the sums.
+// Total pairs = sum of the per-workgroup or per-wave tile counts (fixed
+// order, one workgroup). The counts sit at the 256-byte-aligned start of their
+// workspace slice, so each thread reads runs of four with 16-byte loads, all
+// issued before the sums. A saturated count (2^32 - 1, "that many or more")
+// adds one more, so that the total then exceeds any capacity.
 __global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs, int nslots, uint64_t* out)
 {
-    constexpr int kPer = 16;   // 16-byte loads in flight per thread and round
+    constexpr int kPer = 8;   // 16-byte loads in flight per thread and round
     __shared__ uint64_t red[16];
     const uint4* v4 = reinterpret_cast<const uint4*>(block_pairs);
     const int nvec = nslots >> 2;
@@ -631,10 +647,12 @@ __global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs
             q[k] = b < nvec ? v4[b] : make_uint4(0u, 0u, 0u, 0u);
         }
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) v += (uint64_t)q[k].x + q[k].y + q[k].z + q[k].w;
+        for (int k = 0; k < kPer; ++k)
+            v += (uint64_t)q[k].x + q[k].y + q[k].z + q[k].w + (q[k].x == ~0u) + (q[k].y == ~0u) + (q[k].z == ~0u) +
+                 (q[k].w == ~0u);
     }
     const int rest = (nvec << 2) + (int)threadIdx.x;
-    if (rest < nslots) v += block_pairs[rest];
+    if (rest < nslots) v += (uint64_t)block_pairs[rest] + (block_pairs[rest] == ~0u);
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
@@ -646,11 +664,8 @@ __global__ __launch_bounds__(1024) void k_pair_count(const uint32_t* block_pairs
     }
 }
 
-hipError_t launch_pair_count(int64_t n, int32_t kind, const Workspace& ws, uint64_t* num_pairs, hipStream_t s)
+hipError_t launch_pair_count(int slots, const Workspace& ws, uint64_t* num_pairs, hipStream_t s)
 {
-    // the SH3 and lobe preprocesses leave one tile sum per workgroup, the decoders one per wave
-    const bool per_block = kind == GS_APP_SH3 || kind == GS_APP_NASG || kind == GS_APP_NASGABOR;
-    const int slots = per_block ? preprocess_blocks(n) : pair_count_slots(n);
     hipLaunchKernelGGL(k_pair_count, dim3(1), dim3(1024), 0, s, ws.block_pairs, slots, num_pairs);
     return hipGetLastError();
 }

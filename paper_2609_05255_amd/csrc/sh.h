@@ -95,35 +95,42 @@ __device__ __forceinline__ void sh_basis16_vjp(float x, float y, float z, const 
 
 // jac[3 c + j] = sum over the bands below nb (k >= 1) of coef[3 k + c] dY_k/dx_j:
 // the direction Jacobian of the three colour sums, one pass over the basis.
+// Only the gradient components that are not identically zero are multiplied
+// in (band 1 has one per basis function, and sets each of the nine entries
+// first); for nb = 1 the Jacobian is zero.
 __device__ __forceinline__ void sh_color_jacobian(float x, float y, float z, const float* coef, int nb,
                                                   float jac[9])
 {
+    if (nb < 4) {
+        for (int r = 0; r < 9; ++r) jac[r] = 0.f;
+        return;
+    }
     const float xx = x * x, yy = y * y, zz = z * z;
-    for (int r = 0; r < 9; ++r) jac[r] = 0.f;
-    auto add = [&](int k, float gx, float gy, float gz) {
+    // component j of basis k's gradient is g: jac[3 c + j] += coef[3 k + c] g
+    auto add = [&](int k, int j, float g) {
         if (k >= nb) return;
-        for (int c = 0; c < 3; ++c) {
-            const float w = coef[3 * k + c];
-            jac[3 * c] += w * gx;
-            jac[3 * c + 1] += w * gy;
-            jac[3 * c + 2] += w * gz;
-        }
+        for (int c = 0; c < 3; ++c) jac[3 * c + j] = fmaf(coef[3 * k + c], g, jac[3 * c + j]);
     };
-    add(1, 0.f, -kSH1, 0.f);
-    add(2, 0.f, 0.f, kSH1);
-    add(3, -kSH1, 0.f, 0.f);
-    add(4, kSH2a * y, kSH2a * x, 0.f);
-    add(5, 0.f, -kSH2a * z, -kSH2a * y);
-    add(6, -2.f * kSH2b * x, -2.f * kSH2b * y, 4.f * kSH2b * z);
-    add(7, -kSH2a * z, 0.f, -kSH2a * x);
-    add(8, 2.f * kSH2c * x, -2.f * kSH2c * y, 0.f);
-    add(9, 6.f * kSH3a * x * y, 3.f * kSH3a * (xx - yy), 0.f);
-    add(10, kSH3b * y * z, kSH3b * x * z, kSH3b * x * y);
-    add(11, -2.f * kSH3c * x * y, kSH3c * (4.f * zz - xx - 3.f * yy), 8.f * kSH3c * y * z);
-    add(12, -6.f * kSH3d * x * z, -6.f * kSH3d * y * z, kSH3d * (6.f * zz - 3.f * xx - 3.f * yy));
-    add(13, kSH3c * (4.f * zz - 3.f * xx - yy), -2.f * kSH3c * x * y, 8.f * kSH3c * x * z);
-    add(14, 2.f * kSH3e * x * z, -2.f * kSH3e * y * z, kSH3e * (xx - yy));
-    add(15, 3.f * kSH3a * (xx - yy), -6.f * kSH3a * x * y, 0.f);
+    for (int c = 0; c < 3; ++c) {
+        jac[3 * c + 0] = coef[9 + c] * -kSH1;   // Y_3 = -K1 x
+        jac[3 * c + 1] = coef[3 + c] * -kSH1;   // Y_1 = -K1 y
+        jac[3 * c + 2] = coef[6 + c] * kSH1;    // Y_2 = K1 z
+    }
+    add(4, 0, kSH2a * y);               add(4, 1, kSH2a * x);
+    add(5, 1, -kSH2a * z);              add(5, 2, -kSH2a * y);
+    add(6, 0, -2.f * kSH2b * x);        add(6, 1, -2.f * kSH2b * y);      add(6, 2, 4.f * kSH2b * z);
+    add(7, 0, -kSH2a * z);              add(7, 2, -kSH2a * x);
+    add(8, 0, 2.f * kSH2c * x);         add(8, 1, -2.f * kSH2c * y);
+    add(9, 0, 6.f * kSH3a * x * y);     add(9, 1, 3.f * kSH3a * (xx - yy));
+    add(10, 0, kSH3b * y * z);          add(10, 1, kSH3b * x * z);        add(10, 2, kSH3b * x * y);
+    add(11, 0, -2.f * kSH3c * x * y);   add(11, 1, kSH3c * (4.f * zz - xx - 3.f * yy));
+    add(11, 2, 8.f * kSH3c * y * z);
+    add(12, 0, -6.f * kSH3d * x * z);   add(12, 1, -6.f * kSH3d * y * z);
+    add(12, 2, kSH3d * (6.f * zz - 3.f * xx - 3.f * yy));
+    add(13, 0, kSH3c * (4.f * zz - 3.f * xx - yy));
+    add(13, 1, -2.f * kSH3c * x * y);   add(13, 2, 8.f * kSH3c * x * z);
+    add(14, 0, 2.f * kSH3e * x * z);    add(14, 1, -2.f * kSH3e * y * z); add(14, 2, kSH3e * (xx - yy));
+    add(15, 0, 3.f * kSH3a * (xx - yy)); add(15, 1, -6.f * kSH3a * x * y);
 }
 
 }  // namespace gsr

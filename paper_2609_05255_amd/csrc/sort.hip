@@ -130,6 +130,18 @@ __global__ __launch_bounds__(kBlock) void k_radix_scan(uint32_t* __restrict__ hi
     if (threadIdx.x == 0) digit_tot[blockIdx.x] = total;
 }
 
+// The block entries' segment table (see k_segments), written by one extra
+// workgroup of the block sort's scatter from that pass's digit totals.
+struct SegTable {
+    uint32_t* block_ranges;   // nullptr: no table
+    uint32_t* seg_base;
+    uint32_t* seg_block;
+    uint32_t* counters;
+    int n_blocks;
+};
+
+__device__ void segment_table_256(const uint32_t* __restrict__ block_count, const SegTable& t);
+
 template <int kBits, int kItems, typename KeyT, typename KeyOutT>
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict__ keys_in,
                                                           const uint32_t* __restrict__ vals_in, PairCount cnt,
@@ -138,7 +150,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict
                                                           KeyOutT* __restrict__ keys_out,
                                                           uint32_t* __restrict__ vals_out,
                                                           const gs_splat* __restrict__ rect_src,
-                                                          uint2* __restrict__ rect_out)
+                                                          uint2* __restrict__ rect_out, SegTable seg)
 {
     constexpr int R = 1 << kBits;
     constexpr int kTile = kBlock * kItems;
@@ -149,6 +161,10 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict
     __shared__ KeyT skey[kTile];
     __shared__ uint32_t sval[kTile];
     __shared__ uint32_t lds4[4];
+    if (seg.block_ranges && blockIdx.x == gridDim.x - 1) {   // the extra workgroup
+        segment_table_256(digit_tot, seg);
+        return;
+    }
     const uint64_t count = cnt.get();
     if ((uint64_t)blockIdx.x * kTile >= count) return;   // past the keys: nothing to move
     const int t = threadIdx.x, wave = t >> 6, lane = __lane_id();
@@ -256,28 +272,31 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const KeyT* __restrict
 template <int kBits, int kItems, typename KeyT, typename KeyOutT>
 void radix_pass_t(const KeyT* keys_in, const uint32_t* vals_in, PairCount cnt, int shift, KeyOutT* keys_out,
                   uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s,
-                  const gs_splat* rect_src = nullptr, uint2* rect_out = nullptr)
+                  const gs_splat* rect_src = nullptr, uint2* rect_out = nullptr,
+                  SegTable seg = SegTable{nullptr, nullptr, nullptr, nullptr, 0})
 {
     const int nblocks = (int)std::max<int64_t>(div_up((int64_t)cnt.host, (int64_t)kBlock * kItems), 1);
     hipLaunchKernelGGL((k_radix_hist<kBits, kItems, KeyT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in, cnt, shift,
                        hist, nblocks);
     hipLaunchKernelGGL(k_radix_scan, dim3(1 << kBits), dim3(kBlock), 0, s, hist, nblocks, cnt, kBlock * kItems,
                        digit_tot);
-    hipLaunchKernelGGL((k_radix_scatter<kBits, kItems, KeyT, KeyOutT>), dim3(nblocks), dim3(kBlock), 0, s, keys_in,
-                       vals_in, cnt, shift,
-                       hist, nblocks, digit_tot, keys_out, vals_out, rect_src, rect_out);
+    hipLaunchKernelGGL((k_radix_scatter<kBits, kItems, KeyT, KeyOutT>), dim3(nblocks + (seg.block_ranges ? 1 : 0)),
+                       dim3(kBlock), 0, s, keys_in, vals_in, cnt, shift, hist, nblocks, digit_tot, keys_out, vals_out,
+                       rect_src, rect_out, seg);
 }
 
 // A block-sort pass over `bits` (1..9) bits, 8192 keys per workgroup: twice
 // the depth sort's, for longer runs per digit among the 9-bit digits.
 constexpr int kBlockSortBits = 9;
 hipError_t block_radix_pass(const uint32_t* keys_in, const uint32_t* vals_in, PairCount cnt, int shift, int bits,
-                            uint32_t* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s)
+                            uint32_t* keys_out, uint32_t* vals_out, uint32_t* hist, uint32_t* digit_tot, hipStream_t s,
+                            SegTable seg)
 {
     switch (bits) {
 #define GS_PASS(b)                                                                                                   \
     case b:                                                                                                          \
-        radix_pass_t<b, kBlockSortItems>(keys_in, vals_in, cnt, shift, keys_out, vals_out, hist, digit_tot, s);   \
+        radix_pass_t<b, kBlockSortItems>(keys_in, vals_in, cnt, shift, keys_out, vals_out, hist, digit_tot, s,     \
+                                         nullptr, nullptr, seg);                                                     \
         break;
         GS_PASS(1) GS_PASS(2) GS_PASS(3) GS_PASS(4) GS_PASS(5) GS_PASS(6) GS_PASS(7) GS_PASS(8) GS_PASS(9)
 #undef GS_PASS
@@ -633,6 +652,34 @@ __global__ __launch_bounds__(kListThreads) void k_segments(const uint32_t* __res
     }
 }
 
+// k_segments' table from the digit totals of a single-pass block sort, for
+// one 256-thread workgroup (the block sort scatter's extra one).
+__device__ void segment_table_256(const uint32_t* __restrict__ block_count, const SegTable& t)
+{
+    __shared__ uint32_t lds4s[4];
+    uint32_t carry = 0, ecarry = 0;
+    for (int b0 = 0; b0 < t.n_blocks; b0 += kBlock) {
+        const int b = b0 + (int)threadIdx.x;
+        const uint32_t len = b < t.n_blocks ? block_count[b] : 0u;
+        uint32_t etotal, total;
+        const uint32_t start = ecarry + block_excl_scan(len, lds4s, &etotal);
+        const uint32_t ns = (len + kSegEntries - 1) / kSegEntries;
+        const uint32_t first = carry + block_excl_scan(ns, lds4s, &total);
+        if (b < t.n_blocks) {
+            t.block_ranges[2 * b] = start;
+            t.block_ranges[2 * b + 1] = start + len;
+            t.seg_base[b] = first;
+            for (uint32_t k = 0; k < ns; ++k) t.seg_block[first + k] = (uint32_t)b;
+        }
+        ecarry += etotal;
+        carry += total;
+    }
+    if (threadIdx.x == 0) {
+        t.seg_base[t.n_blocks] = carry;
+        t.counters[0] = carry;
+    }
+}
+
 // The entry range of segment s: block b, entries [e0, e1).
 struct Segment {
     uint32_t b, e0, e1;
@@ -915,18 +962,20 @@ hipError_t launch_block_sort(const Cam& cam, PairCount entries, const Workspace&
     uint32_t* kbuf[2] = {ws.entry_keys_a, ws.entry_keys_b};
     uint32_t* vbuf[2] = {ws.entry_vals_a, ws.entry_vals_b};
     int src = 0, shift = kMaskBits;
+    // a single pass's digit totals are the blocks' entry counts: its scatter's
+    // extra workgroup writes the segment table
+    const SegTable seg_one{ws.block_ranges, ws.seg_base, ws.seg_block, ws.list_counters, n_blocks};
+    const SegTable seg_none{nullptr, nullptr, nullptr, nullptr, 0};
     for (int p = 0; p < passes; ++p) {
         const int pb = (kMaskBits + bits - shift + (passes - p) - 1) / (passes - p);   // remaining bits spread evenly
         const hipError_t e = block_radix_pass(kbuf[src], vbuf[src], entries, shift, pb, kbuf[src ^ 1],
-                                              vbuf[src ^ 1], ws.hist, ws.digit_tot, s);
+                                              vbuf[src ^ 1], ws.hist, ws.digit_tot, s,
+                                              passes == 1 ? seg_one : seg_none);
         if (e != hipSuccess) return e;
         shift += pb;
         src ^= 1;
     }
-    if (passes == 1) {
-        hipLaunchKernelGGL(k_segments, dim3(1), dim3(kListThreads), 0, s, ws.digit_tot, ws.block_ranges, n_blocks,
-                           ws.seg_base, ws.seg_block, ws.list_counters);
-    } else {
+    if (passes != 1) {   // none (a single block) or several: ranges by search, then the table
         const dim3 grid((unsigned)div_up(n_blocks + 1, kBlock / kWave));
         hipLaunchKernelGGL(k_ranges, grid, dim3(kBlock), 0, s, kbuf[src], kMaskBits, entries, n_blocks,
                            ws.block_ranges);

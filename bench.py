@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 METRIC = "fwd+bwd iterations/sec and rendered Mpix/s at 3M Gaussians, 1600x1064"
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 FP32_VECTOR_PEAK_TFLOPS = 157.3  # published; counts packed-fp32 FMA
-FP32_UNPACKED_PEAK_TFLOPS = 78.6 # 256 CU x 4 SIMD x 16 lanes x 2 flops x 2.4 GHz (this build emits no packed fp32)
+FP32_UNPACKED_PEAK_TFLOPS = 78.6 # 256 CU x 4 SIMD x 16 lanes x 2 flops x 2.4 GHz (the kernels emit no packed fp32)
 # fp32 work of the blend per (pixel, list entry), counting an FMA as 2, by what
 # the method does with the entry. The method visits, per pixel, every entry up
 # to the one that stops the pixel (forward) or up to its last contributor

@@ -47,7 +47,7 @@ typedef enum gs_status {
     GS_ERR_INVALID_ARG = 1,   /* bad pointer, size, enum value or camera */
     GS_ERR_CAPACITY = 2,      /* a caller buffer is too small; the needed size is reported */
     GS_ERR_DEVICE = 3,        /* HIP reported an error */
-    GS_ERR_UNSUPPORTED = 4,   /* valid request this build does not implement */
+    GS_ERR_UNSUPPORTED = 4,   /* valid request the library does not implement */
 } gs_status;
 
 #define GS_TILE 16            /* tile edge in pixels (Sec. 3.1) */

@@ -298,7 +298,7 @@ def flagged_pixels(margin, max_count=None, label="", region=None):
     return flagged
 
 
-# Gradients (survey reading S-26): every element within
+# Gradients (the fp32 tolerance of the workload): every element within
 # |gpu - ref| <= GRAD_ELEM_RTOL |ref| + GRAD_ELEM_FLOOR max|ref| of its tensor,
 # and the tensor's relative L2 error <= GRAD_REL_L2. The pair sums use float
 # atomics in fp32 against the oracle's fp64, hence the relative terms.

@@ -6,7 +6,7 @@ sides), the number of pairs, the sorted per-tile lists, tile ids and ranges.
 Images: abs 1e-5 + rel 1e-4 on every pixel whose decisions lie outside the
 rounding bound of the oracle's margin; the others (flagged) are counted and
 bounded, and get a zero upstream gradient on both sides.
-Gradients (survey reading S-26): every element within 1e-3 |ref| + 1e-5 max|ref|
+Gradients (the fp32 tolerance of the workload): every element within 1e-3 |ref| + 1e-5 max|ref|
 and relative L2 <= 1e-4 per tensor; the decoder paths as stated in MLP_GRADS.
 """
 import numpy as np

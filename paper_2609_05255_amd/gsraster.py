@@ -45,6 +45,12 @@ class GsError(RuntimeError):
         self.status = status
 
 
+# gs_splat's fields as 4-byte word offsets into its 64-byte record (the four
+# int16 of the rectangle fill words 12 and 13)
+SPLAT_WORDS = dict(mean_x=0, mean_y=1, conic_a=2, conic_b=3, conic_c=4, opacity=5, color=6, power_min=9,
+                   ext_x=10, ext_y=11, rect=12, depth=14)
+
+
 class Camera(C.Structure):
     _fields_ = [("viewmat", C.c_float * 12), ("campos", C.c_float * 3), ("fx", C.c_float), ("fy", C.c_float),
                 ("cx", C.c_float), ("cy", C.c_float), ("width", C.c_int32), ("height", C.c_int32),
@@ -431,10 +437,12 @@ class Frame:
         """Host copy of the splat records, split into fields."""
         raw = self.splats.view(-1, 16).cpu()
         f = raw.numpy()
-        rect = raw.view(torch.int32).numpy()[:, 12:14]
+        w = SPLAT_WORDS
+        rect = raw.view(torch.int32).numpy()[:, w["rect"]:w["rect"] + 2]
         r01, r23 = rect[:, 0].astype("int64") & 0xFFFFFFFF, rect[:, 1].astype("int64") & 0xFFFFFFFF
         import numpy as np
         rects = np.stack([r01 & 0xFFFF, r01 >> 16, r23 & 0xFFFF, r23 >> 16]).astype(np.int32)
-        return dict(mean2d=f[:, 0:2].T.copy(), conic=f[:, 2:5].T.copy(), opacity=f[:, 5].copy(),
-                    color=f[:, 6:9].T.copy(), power_min=f[:, 9].copy(), ext=f[:, 10:12].T.copy(),
-                    depth=f[:, 14].copy(), rect=rects)
+        return dict(mean2d=f[:, w["mean_x"]:w["mean_y"] + 1].T.copy(), conic=f[:, w["conic_a"]:w["conic_c"] + 1].T.copy(),
+                    opacity=f[:, w["opacity"]].copy(), color=f[:, w["color"]:w["color"] + 3].T.copy(),
+                    power_min=f[:, w["power_min"]].copy(), ext=f[:, w["ext_x"]:w["ext_y"] + 1].T.copy(),
+                    depth=f[:, w["depth"]].copy(), rect=rects)

@@ -24,12 +24,19 @@ MIRRORS = {
 }
 
 
+# where the binding reads each field of a 64-byte splat record, in 4-byte words
+SPLAT_WORDS = sorted(gs.SPLAT_WORDS.items(), key=lambda kv: kv[1])
+
+
 def c_layout(tmp_path):
     lines = ["#include <stddef.h>", "#include <stdio.h>", '#include "gsraster.h"', "int main(void) {"]
     for cname, cls in MIRRORS.items():
         lines.append('    printf("%s size %%zu\\n", sizeof(%s));' % (cname, cname))
         for fname, _ in cls._fields_:
             lines.append('    printf("%s %s %%zu\\n", offsetof(%s, %s));' % (cname, fname, cname, fname))
+    for fname, _ in SPLAT_WORDS:
+        lines.append('    printf("gs_splat %s %%zu\\n", offsetof(gs_splat, %s));' % (fname, fname))
+    lines.append('    printf("gs_splat size %zu\\n", sizeof(gs_splat));')
     lines += ["    return 0;", "}"]
     src = tmp_path / "layout.c"
     src.write_text("\n".join(lines) + "\n")
@@ -50,3 +57,6 @@ def test_ctypes_mirrors_match_the_header(tmp_path):
         assert layout[(cname, "size")] == ctypes.sizeof(cls), cname
         for fname, _ in cls._fields_:
             assert layout[(cname, fname)] == getattr(cls, fname).offset, (cname, fname)
+    assert layout[("gs_splat", "size")] == 64
+    for fname, word in SPLAT_WORDS:
+        assert layout[("gs_splat", fname)] == 4 * word, fname

@@ -166,6 +166,8 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
         const float4* p = reinterpret_cast<const float4*>(splats + values[start + lane]);
         c0 = p[0]; c1 = p[1]; c2 = p[2];
     }
+    // the list entry of the batch after the prefetched one, loaded a batch early
+    uint32_t nid = start + kWave + lane < end ? values[start + kWave + lane] : 0u;
     for (uint32_t b = start; b < end && __ballot(any) != 0; b += kWave) {
         st[0][lane] = c0; st[1][lane] = c1; st[2][lane] = c2;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -182,9 +184,10 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_fwd(Cam cam, con
                                              box_lo, box_hi);
         uint64_t todo = __ballot(meets);
         if (b + kWave + lane < end) {
-            const float4* p = reinterpret_cast<const float4*>(splats + values[b + kWave + lane]);
+            const float4* p = reinterpret_cast<const float4*>(splats + nid);
             c0 = p[0]; c1 = p[1]; c2 = p[2];
         }
+        if (b + 2 * kWave + lane < end) nid = values[b + 2 * kWave + lane];
         while (todo != 0) {
             const int j = (int)__builtin_ctzll(todo);
             todo &= todo - 1;
@@ -328,7 +331,7 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
     float4 (*st)[kWave] = stage[wave];
     uint32_t* sid = stage_id[wave];
     float4 c0 = make_float4(0.f, 0.f, 0.f, 0.f), c1 = c0, c2 = c0;
-    uint32_t cid = 0;
+    uint32_t cid = 0, nid = 0;   // nid: the list entry of the batch after the prefetched one, loaded a batch early
     {
         const uint32_t p = (uint32_t)(nbatch - 1) * kWave + lane;
         if (p < stop) {
@@ -336,6 +339,7 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
             const float4* r = reinterpret_cast<const float4*>(splats + cid);
             c0 = r[0]; c1 = r[1]; c2 = r[2];
         }
+        if (nbatch >= 2) nid = values[start + (uint32_t)(nbatch - 2) * kWave + lane];
     }
     for (int bi = nbatch - 1; bi >= 0; --bi) {
         const uint32_t b = (uint32_t)bi * kWave;
@@ -354,9 +358,10 @@ __global__ __launch_bounds__(kTile * kTile / kPix) void k_blend_bwd(Cam cam, con
                                  ellipse_meets_box(c0.x, c0.y, c0.z, c0.w, c1.x, c2.y, box_cx - box_hx,
                                                    box_cx + box_hx, box_lo, box_hi));
         if (bi > 0) {
-            cid = values[start + b - kWave + lane];
+            cid = nid;
             const float4* r = reinterpret_cast<const float4*>(splats + cid);
             c0 = r[0]; c1 = r[1]; c2 = r[2];
+            if (bi > 1) nid = values[start + b - 2 * kWave + lane];
         }
         while (todo != 0) {
             const int j = 63 - (int)__builtin_clzll(todo);

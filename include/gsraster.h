@@ -211,7 +211,9 @@ typedef struct gs_grads {
  * Sigma2D = J R_view Sigma R_view^T J^T + 0.3 I, culled unless det > 0; conic;
  * r = ceil(3 sqrt(lambda_max)) with lambda_max = mid + sqrt(max(0.1, mid^2 - det));
  * rect = [floor((px - r)/16), ceil((px + r)/16)) per axis clamped to the grid,
- * culled if empty; colour from the appearance model.
+ * culled if empty; colour from the appearance model. For SH3 with
+ * out->color_jac non-NULL, also the colour's view-direction Jacobian and clamp
+ * bits there (see gs_preprocessed), for gs_render_bwd.
  * The geometry is one fixed sequence of correctly rounded fp32 operations
  * (no fused multiply-add), so tile rectangles and depth keys are reproducible.
  * num_pairs_host: optional HOST pointer; if non-NULL the call synchronises the
@@ -228,7 +230,8 @@ gs_status gs_preprocess(const gs_camera* cam, const gs_gaussians* g, const gs_ap
  * device memory or hand over a workspace (code under HIP graph capture, tight
  * serving loops, harnesses that forbid allocation). Same arguments, results
  * and errors as gs_preprocess, without the workspace: its scratch (one tile
- * sum per workgroup or wave of 64 Gaussians) is a static device array of the
+ * sum per preprocess workgroup, or per wave of a decoder's grid) is a static
+ * device array of the
  * library, GS_NOALLOC_MAX_GAUSSIANS / 64 u32 (1 MiB), one per GPU, held until
  * the process ends; its address is looked up once per device, on the first
  * call with that device current. Calls no allocating routine.

@@ -17,7 +17,9 @@
 // digit in LDS, and writes each digit's run to consecutive global addresses.
 // The grids are sized for the most keys a call can meet (the capacity, for
 // the block entries); workgroups past the device-side count do nothing, and
-// the scan reads only the workgroups below it.
+// the scan reads only the workgroups below it. A single-pass block sort's
+// scatter has one workgroup more, which writes the tile lists' segment table
+// from that pass's digit totals (the blocks' entry counts).
 #include "gs_internal.h"
 
 namespace gsr {

@@ -84,7 +84,8 @@ def tile_pixels(sample, tiles_x, W, H):
                                                          ("paper_nasg", "nasg", 11, None),
                                                          ("paper_nasgabor", "nasgabor", 13, None),
                                                          ("stress", "sh3", 5, None),
-                                                         ("stress", "latent", 10, None)])
+                                                         ("stress", "latent", 10, None),
+                                                         ("stress", "neural", 2, None)])
 def test_full_size_sampled(config, kind, cam_index, arch):
     latent = kind in ("latent", "neural")
     sc = inputs.make_scene(config, appearance=(kind,), neural_arch=arch)

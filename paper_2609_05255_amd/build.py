@@ -38,8 +38,15 @@ COMMON = [
 # register pairs, which then spill; without it the latent kernel needs 117
 # registers and no spills instead of 128 and 28 bytes of scratch per lane, the
 # neural one 97 instead of 123 (latent preprocess 0.138 -> 0.127 ms, neural
-# 0.161 -> 0.140 ms; the other kernels' times unchanged).
-PER_FILE = {"preprocess.hip": ["-mllvm", "-disable-machine-licm"]}
+# 0.161 -> 0.140 ms; the other kernels' times unchanged). blend.hip: the
+# scheduler's instruction-level-parallelism strategy, which keeps more loads in
+# flight in the per-splat loops at the same occupancy (blend forward 0.192 ->
+# 0.188 ms, backward 0.331 -> 0.324 ms at 3M Gaussians; for the other files it
+# is neutral or slower, the latent decoder backward by 20 us).
+PER_FILE = {
+    "preprocess.hip": ["-mllvm", "-disable-machine-licm"],
+    "blend.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+}
 
 
 def sources():

@@ -57,10 +57,12 @@ STAGES = {"preprocess": ("preprocess", "pair_count"),
 # HBM traffic of a kernel, from memory-counter runs summarised under profiles/
 # (FETCH_SIZE and WRITE_SIZE per dispatch, each scaled by what the counter reads
 # for a copy of known size). Each summary records a hash of the kernel's
-# sources; once they change, the recorded figure no longer describes the
-# kernel and the traffic is reported as null.
+# sources and of the build script (its per-file compiler options); once they
+# change, the recorded figure no longer describes the kernel and the traffic is
+# reported as null.
 TRAFFIC_SUMMARIES = {("blend_bwd", "paper_sh3", "sh3"): "profiles/blend_bwd_paper_sh3_traffic.txt"}
-KERNEL_SOURCES = {"blend_bwd": ("paper_2609_05255_amd/csrc/blend.hip", "paper_2609_05255_amd/csrc/gs_internal.h")}
+KERNEL_SOURCES = {"blend_bwd": ("paper_2609_05255_amd/csrc/blend.hip", "paper_2609_05255_amd/csrc/gs_internal.h",
+                                 "paper_2609_05255_amd/build.py")}
 
 
 def source_hash(kernel: str) -> str:
